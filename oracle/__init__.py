@@ -1,0 +1,29 @@
+"""Reference oracle for projected per-example gradients and attribution scores.
+
+TEST INFRASTRUCTURE ONLY.  Nothing in the product path imports this package:
+only ``tests/``, ``__graft_entry__.smoke()`` and the ``cpu_baseline`` leg of
+``bench.py`` may use it.  It is a plain, slow, obviously-correct CPU
+implementation in float64 (numpy), written from the paper's definitions, and it
+shares no code, constants or tables with the HIP library under
+``paper_2609_38767_amd/``.
+
+Modules
+-------
+``rng``        counter-based generator for the Gaussian projection maps
+               (SplitMix64 seed derivation, Philox4x32-10, Box-Muller), written
+               from the published definitions of those algorithms.
+``gradients``  per-example weight gradient (Eq. 1), factored and materialized
+               projections (Eq. 2), concatenation into one feature vector per
+               example, and the factorized inner product (Eq. 4).
+``scoring``    gradient-similarity scores with an optional diagonal
+               preconditioner, and per-query top-k.
+``cost``       closed-form FLOP / byte / storage counts of the two routes
+               (Sec. 3.2 "FLOP-aware routing", App. A.4).
+
+Parity status of each function is stated in its docstring; the one function
+with no pin to the paper is the seed/counter layout of the generator, which the
+paper leaves unspecified ("parity unpinned" w.r.t. the paper, pinned to the
+published Philox / SplitMix64 definitions instead).
+"""
+
+from . import rng, gradients, scoring, cost  # noqa: F401

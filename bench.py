@@ -1,0 +1,210 @@
+"""Benchmark of the projected-gradient attribution hot path on one MI355X.
+
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--no-cpu-baseline]
+
+One step = one pass of the whole path over one batch of synthetic input:
+  (1) projection: per-example projected gradients of all 224 linear layers of a
+      Llama-3-8B-shaped stack (T=2048, batch 8, bf16 Student-t(4) factors,
+      k_in=k_out=32, q/k/v and gate/up sharing their input block), routed by
+      the cost model and concatenated into phi [8, 229376];
+  (2) scoring: S = Phi_q diag(d) Phi_train^T for Phi_q 2048 x 8192 and
+      Phi_train 200000 x 8192 (bf16, d log-uniform on [1e-3, 1e3]), float32
+      scores plus per-query top-100.
+Inputs are generated on the GPU before timing and stay resident in HBM.  The
+two phases are timed in separate loops of K steps, each bracketed by device
+synchronization; HIP events on the launch stream time every phase.
+
+Prints one JSON line.  `value` is projected per-example gradients per second
+(phase 1); the scoring GEMM's TFLOP/s is reported beside it.
+"""
+import argparse
+import json
+import os
+import sys
+import time
+
+LLAMA_BYTES_PER_EXAMPLE = None  # filled from the workload description
+
+
+def parse():
+    p = argparse.ArgumentParser()
+    p.add_argument("--gpus", type=int, default=1)
+    p.add_argument("--steps", type=int, default=10)
+    p.add_argument("--warmup", type=int, default=2)
+    p.add_argument("--no-cpu-baseline", action="store_true")
+    p.add_argument("--phase", choices=["all", "project", "score"], default="all")
+    return p.parse_args()
+
+
+def algorithmic_projection_bytes(wl):
+    """HBM bytes one example must stream: each distinct input block A once,
+    every output-gradient block B once (bf16)."""
+    T, elt = wl["T"], 2
+    seen, total = set(), 0
+    for L in wl["layers"]:
+        if L["a_group"] not in seen:
+            seen.add(L["a_group"])
+            total += T * L["d_in"] * elt
+        total += T * L["d_out"] * elt
+    return total
+
+
+def projection_flops(wl):
+    T = wl["T"]
+    return sum(2 * T * (L["d_in"] * L["k_in"] + L["d_out"] * L["k_out"] + L["k_in"] * L["k_out"])
+               for L in wl["layers"])
+
+
+def cpu_baseline_projection(wl, inputs, seed, budget_s=20.0):
+    """Time the oracle's factored form (float64) on example 0 of as many
+    leading Llama blocks as fit the budget; extrapolate to all 224 layers."""
+    import numpy as np
+    from threadpoolctl import threadpool_info
+    from oracle import gradients as og
+    from oracle import rng as orng
+    layers = wl["layers"]
+    done, t_total = 0, 0.0
+    for li, L in enumerate(layers):
+        A, B = inputs[li]
+        A0 = A[0].float().cpu().numpy().astype(np.float64)
+        B0 = B[0].float().cpu().numpy().astype(np.float64)
+        P_in, P_out = orng.projection_pair(seed, li, L["d_in"], L["d_out"], L["k_in"], L["k_out"], "bf16")
+        t0 = time.perf_counter()
+        og.project_factored(A0, B0, P_in, P_out)
+        t_total += time.perf_counter() - t0
+        done += 1
+        if t_total >= budget_s and done % 7 == 0:
+            break
+    threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+    per_example = t_total * len(layers) / done
+    return {"value": 1.0 / per_example, "unit": "examples/s", "cores": threads, "kind": "oracle",
+            "sample": f"example 0, first {done} of {len(layers)} layers, factored form in float64 "
+                      f"({t_total:.1f} s), extrapolated to all layers"}
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(json.dumps({"error": "this build runs on one GPU only; --gpus must be 1"}))
+        sys.exit(2)
+    import torch
+    import paper_2609_38767_amd as dt
+    import workloads as W
+    from paper_2609_38767_amd.session import ProjectionSession, score
+
+    dt.load()  # fail loudly if the HIP library is not built
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    stream = torch.cuda.current_stream()
+    wl = W.WORKLOADS["llama8b"]
+    swl = W.WORKLOADS["score"]
+    n = wl["batch"]
+    out = {}
+
+    # ---------------- setup (untimed): maps, inputs resident in HBM
+    sess = inputs = None
+    if args.phase in ("all", "project"):
+        sess = ProjectionSession(wl["layers"], dtype="bf16", seed=wl["seed"], device=dev)
+        cache, inputs = {}, []
+        for li in range(len(wl["layers"])):
+            A, B = W.factor_blocks(wl, li, 0, n, wl["T"], dev, "bf16", a_cache=cache)
+            sess.capture(li, A, B)
+            inputs.append((A, B))
+        phi = torch.empty((n, sess.F), dtype=torch.float32, device=dev)
+        sess.workspace()
+        print(f"[bench] projection inputs ready: {sum(A.numel() * 2 for A in cache.values()) / 1e9 + sum(B.numel() * 2 for _, B in inputs) / 1e9:.1f} GB", file=sys.stderr, flush=True)
+    if args.phase in ("all", "score"):
+        Q, X, d = W.score_inputs(swl, dev)
+        n_q, n_t, F = Q.shape[0], X.shape[0], Q.shape[1]
+        S = torch.empty((n_q, n_t), dtype=torch.float32, device=dev)
+        idx = torch.empty((n_q, swl["topk"]), dtype=torch.int32, device=dev)
+        val = torch.empty((n_q, swl["topk"]), dtype=torch.float32, device=dev)
+        need = dt.dattri_score_workspace_bytes(n_q, n_t, F, dt.DATTRI_BF16, True, True, swl["topk"])
+        sws = torch.empty(need, dtype=torch.uint8, device=dev)
+        gemm_only_ws = torch.empty(dt.dattri_score_workspace_bytes(n_q, n_t, F, dt.DATTRI_BF16, True, True, 0),
+                                   dtype=torch.uint8, device=dev)
+        print("[bench] scoring inputs ready", file=sys.stderr, flush=True)
+    torch.cuda.synchronize()
+
+    def project_step():
+        sess.project(n, phi=phi)
+
+    def score_step(topk=True):
+        k = swl["topk"] if topk else 0
+        w = sws if topk else gemm_only_ws
+        dt.dattri_score(Q, n_q, X, n_t, F, dt.DATTRI_BF16, d, S, k, idx if topk else None,
+                        val if topk else None, w, w.numel())
+
+    def timed(fn, steps):
+        evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+               for _ in range(steps)]
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for a, b in evs:
+            a.record(stream)
+            fn()
+            b.record(stream)
+        torch.cuda.synchronize()
+        wall = time.perf_counter() - t0
+        ms = [a.elapsed_time(b) for a, b in evs]
+        return wall, ms
+
+    total_wall = 0.0
+    if sess is not None:
+        for _ in range(args.warmup):
+            project_step()
+        wall_p, ms_p = timed(project_step, args.steps)
+        total_wall += wall_p
+        print(f"[bench] projection: {wall_p / args.steps * 1e3:.2f} ms/step", file=sys.stderr, flush=True)
+        routes = sorted({r[0] for r in sess.routes()})
+        bytes_ex = algorithmic_projection_bytes(wl)
+        flops_ex = projection_flops(wl)
+        avg_ms = sum(ms_p) / len(ms_p)
+        out["projection"] = {
+            "examples_per_s": n * args.steps / wall_p, "ms_per_batch": avg_ms,
+            "bytes_per_example": bytes_ex, "flops_per_example": flops_ex,
+            "routes": ["factored" if r == 1 else "materialized" for r in routes]}
+        out["roofline"] = {"bound": "hbm", "achieved": bytes_ex * n / (avg_ms * 1e-3) / 1e9,
+                           "peak": 8000.0, "unit": "GB/s",
+                           "frac": bytes_ex * n / (avg_ms * 1e-3) / 1e9 / 8000.0, "traffic": None,
+                           "kernel": "factored projection (all instance launches + reduce), one batch of 8"}
+    if args.phase in ("all", "score"):
+        for _ in range(args.warmup):
+            score_step(False)
+            score_step(True)
+        wall_g, ms_g = timed(lambda: score_step(False), args.steps)
+        wall_s, ms_s = timed(lambda: score_step(True), args.steps)
+        total_wall += wall_s
+        print(f"[bench] scoring: gemm {sum(ms_g) / len(ms_g):.3f} ms, with top-k {wall_s / args.steps * 1e3:.3f} ms",
+              file=sys.stderr, flush=True)
+        flops = 2.0 * n_q * n_t * F
+        g_ms = sum(ms_g) / len(ms_g)
+        out["score"] = {"gemm_tflops": flops / (g_ms * 1e-3) / 1e12, "gemm_ms": g_ms,
+                        "with_topk_ms": sum(ms_s) / len(ms_s), "flops": flops}
+        out["roofline_score"] = {"bound": "mfma", "achieved": flops / (g_ms * 1e-3) / 1e12,
+                                 "peak": 2500.0, "unit": "TFLOP/s",
+                                 "frac": flops / (g_ms * 1e-3) / 1e12 / 2500.0, "traffic": None,
+                                 "kernel": "score GEMM (query scaling + NT GEMM), 2048 x 200000 x 8192"}
+
+    line = {
+        "metric": "projected per-example grads/sec at Llama-8B layer shapes; scoring GEMM TFLOP/s",
+        "value": out.get("projection", {}).get("examples_per_s"),
+        "unit": "examples/s",
+        "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+        "ms_per_step": total_wall / args.steps * 1e3,
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": "bf16", "data": "synthetic",
+        "config": {"workload": "llama3-8b-shaped 224 linear layers, T=2048, batch 8, k=32 "
+                               "+ scoring 2048 x 200000 x 8192 with top-100",
+                   "global_batch": n, "seq_len": wl["T"], "parallelism": "single-gpu"},
+        "score_gemm_tflops": out.get("score", {}).get("gemm_tflops"),
+    }
+    line.update({k: v for k, v in out.items()})
+    if not args.no_cpu_baseline and sess is not None:
+        print("[bench] timing the oracle on host cores", file=sys.stderr, flush=True)
+        line["cpu_baseline"] = cpu_baseline_projection(wl, inputs, wl["seed"])
+    print(json.dumps(line), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,273 @@
+/*
+ * dattri.h -- C ABI of the MI355X (gfx950) projected-gradient attribution
+ * library (libdattri.so).
+ *
+ * The library computes, for a batch of examples and a set of linear layers,
+ * each example's projected weight gradient per layer, concatenates the layer
+ * blocks into one feature vector phi per example, and scores query features
+ * against training features.  Definitions (paper sections):
+ *
+ *   - Sec. 3.2, Eq. (1): for one example with T token positions, the weight
+ *     gradient of a linear layer is DW = sum_t g_t a_t^T, where a_t is the
+ *     layer input and g_t the loss gradient w.r.t. the layer output at token t.
+ *   - Sec. 3.2, Eq. (2) and App. A.2 "Factor projection": with maps
+ *     P_a (k_in x d_in) and P_g (k_out x d_out), sum_t (P_a a_t) (x) (P_g g_t)
+ *     = (P_a (x) P_g) vec(DW).  The library stores P_in = P_a^T and
+ *     P_out = P_g^T and produces, per layer, the k_in x k_out block
+ *         Psi[c][r] = sum_t (a_t . P_in[:,c]) (g_t . P_out[:,r])
+ *     either in the FACTORED form (A P_in)^T (B P_out) or in the MATERIALIZED
+ *     form (P_out^T (B^T A) P_in)^T; both are exact (Sec. 3.2, "FLOP-aware
+ *     routing"; App. A.4 "Routing": routes are algebraically equivalent).
+ *   - Sec. 3.2 "FLOP-aware routing" / App. A.4: the route is chosen per layer
+ *     by a cost model; here the model is calibrated for MI355X.
+ *   - GradDot scoring (Sec. 4.1; gradient similarity, Sec. 2) with an optional
+ *     positive diagonal preconditioner: S = (Phi_q diag(d)) Phi_train^T, and
+ *     per-query top-k.
+ *
+ * Conventions for every entry point
+ *   - All functions are extern "C" and never throw or abort; each returns a
+ *     dattri_status.  On failure a message is available from
+ *     dattri_last_error() (thread-local, valid until the next call on the
+ *     same thread) and no output buffer has been written.
+ *   - Argument, shape, dtype, state and workspace checks all happen on the
+ *     host before any GPU work is enqueued.
+ *   - Every device buffer is owned by the caller.  The library never
+ *     allocates device memory; it reports the sizes it needs.
+ *   - GPU work is enqueued on the stream given (a hipStream_t passed as
+ *     void*, NULL = the default stream) and is asynchronous: results are valid
+ *     once that stream has reached the point after the call.  Faults inside a
+ *     kernel surface at the next synchronizing HIP call.
+ *   - A context is not thread-safe: use one per thread (or per stream).
+ *   - Layouts are row-major and dense unless a leading dimension is given.
+ *     "bf16" is IEEE bfloat16; conversions to bf16 round to nearest even.
+ */
+#ifndef DATTRI_H
+#define DATTRI_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef struct dattri_ctx dattri_ctx;
+
+typedef enum {
+  DATTRI_OK = 0,
+  DATTRI_E_INVALID_ARG = -1, /* null pointer, out-of-range value, bad enum */
+  DATTRI_E_SHAPE = -2,       /* sizes inconsistent with registration/capture */
+  DATTRI_E_DTYPE = -3,       /* dtype not supported for this call */
+  DATTRI_E_STATE = -4,       /* call out of order (e.g. nothing captured) */
+  DATTRI_E_WORKSPACE = -5,   /* workspace missing or smaller than required */
+  DATTRI_E_HIP = -6,         /* a HIP runtime call failed (message has it) */
+  DATTRI_E_UNSUPPORTED = -7  /* valid request outside this build's limits */
+} dattri_status;
+
+typedef enum { DATTRI_F32 = 0, DATTRI_BF16 = 1 } dattri_dtype;
+
+typedef enum {
+  DATTRI_ROUTE_AUTO = 0,        /* per-layer choice of the cost model */
+  DATTRI_ROUTE_FACTORED = 1,    /* (A P_in)^T (B P_out), Eq. (2) left side */
+  DATTRI_ROUTE_MATERIALIZED = 2 /* G = B^T A, then P_out^T G P_in */
+} dattri_route;
+
+/* ---------------------------------------------------------------- context */
+
+/* Create a context.  `compute` is the element type of the captured factor
+ * blocks A, B and of the projection maps (inputs are never converted);
+ * `seed` is the global seed from which every layer's two projection maps are
+ * derived (App. A.2: distinct seeds per side derived from a per-layer base
+ * seed, fixed across all gradients that are compared).
+ * Errors: INVALID_ARG (out == NULL), DTYPE (unknown compute type). */
+dattri_status dattri_create(dattri_ctx** out, dattri_dtype compute, uint64_t seed);
+
+/* Destroy a context (NULL is allowed).  Does not synchronize any stream. */
+void dattri_destroy(dattri_ctx* ctx);
+
+/* Message of the most recent call on this thread if it failed, "" otherwise. */
+const char* dattri_last_error(void);
+
+/* ------------------------------------------------------------ layers / maps */
+
+/* Register a linear layer z = W a with W in R^{d_out x d_in} (Sec. 3.2) and
+ * projection dimensions k_in (input side, k_a) and k_out (output side, k_g).
+ * Layer ids are 0, 1, 2, ... in registration order, which is also the order of
+ * the layer blocks inside phi.  Block l occupies columns
+ * [offset_l, offset_l + k_in*k_out) with element (c, r) at offset_l + c*k_out + r
+ * (the Kronecker order of Eq. (2)).
+ * Errors: INVALID_ARG (ctx/layer_id NULL, any size < 1, d or k > 2^20). */
+dattri_status dattri_register_layer(dattri_ctx* ctx, int32_t d_in, int32_t d_out,
+                                    int32_t k_in, int32_t k_out, int32_t* layer_id);
+
+/* Number of registered layers. */
+dattri_status dattri_num_layers(const dattri_ctx* ctx, int32_t* n);
+
+/* Registered sizes of a layer (any output may be NULL). */
+dattri_status dattri_layer_dims(const dattri_ctx* ctx, int32_t layer, int32_t* d_in, int32_t* d_out,
+                                int32_t* k_in, int32_t* k_out);
+
+/* Total feature dimension F = sum_l k_in,l * k_out,l, and a layer's offset. */
+dattri_status dattri_feature_dim(const dattri_ctx* ctx, int64_t* F);
+dattri_status dattri_layer_offset(const dattri_ctx* ctx, int32_t layer, int64_t* offset);
+
+/* Device bytes the caller must provide for the layer's two projection maps.
+ * The maps are stored in an internal fragment-major layout (16-byte lane
+ * fragments, zero padded); read them back with dattri_get_projection. */
+dattri_status dattri_projection_bytes(const dattri_ctx* ctx, int32_t layer,
+                                      size_t* bytes_in, size_t* bytes_out);
+
+/* Generate (or take) the layer's projection maps and upload them into the
+ * caller-owned device buffers dev_P_in / dev_P_out (at least the sizes from
+ * dattri_projection_bytes, 16-byte aligned).  The library keeps the pointers:
+ * the buffers must stay valid and unmodified while the context uses them.
+ *
+ * Seeded maps (override == NULL): Gaussian entries N(0, 1/k) with k the map's
+ * output dimension (App. A.2 "Random maps"), drawn as
+ *   s = SM(SM(seed) ^ (2*layer + side)),  side 0 = P_in, 1 = P_out,
+ *   (x0..x3) = Philox4x32-10(counter = (e lo, e hi, 0, 0), key = (s lo, s hi)),
+ *   e = v*k + c for element (v, c) of the d x k map,
+ *   u1 = (((x0<<32|x1) >> 11) + 1) 2^-53,  u2 = ((x2<<32|x3) >> 11) 2^-53,
+ *   P[v][c] = sqrt(-2 ln u1) cos(2 pi u2) / sqrt(k)     (in double),
+ * where SM(x) is one SplitMix64 output from state x; then rounded to float32
+ * (RNE) and, for a bf16 context, to bf16 (RNE).
+ * Override: host_P_in [d_in x k_in] / host_P_out [d_out x k_out] float32
+ * row-major replace the seeded map of that side (rounded to the compute type).
+ * The upload is complete when the call returns (it synchronizes `stream`).
+ * Errors: INVALID_ARG (bad layer, NULL or misaligned device pointer), HIP. */
+dattri_status dattri_bind_projection(dattri_ctx* ctx, int32_t layer, void* dev_P_in,
+                                     void* dev_P_out, const float* host_P_in_override,
+                                     const float* host_P_out_override, void* stream);
+
+/* Host copy of the maps the layer uses, after rounding to the compute type:
+ * the seeded maps (whether or not bound yet) or the overrides given at
+ * binding; float32 row-major [d_in x k_in] and [d_out x k_out].  Either
+ * output may be NULL.  Host-only (no GPU needed).
+ * Errors: INVALID_ARG (bad layer). */
+dattri_status dattri_get_projection(const dattri_ctx* ctx, int32_t layer, float* host_P_in,
+                                    float* host_P_out);
+
+/* --------------------------------------------------------------- capture */
+
+/* Record one layer's factor blocks for a batch of n examples (App. A.5: the
+ * layer input and the output gradient, as a backward hook records them).
+ *   A: device [n, T, d_in]  (row t of example i is a_t), compute dtype
+ *   B: device [n, T, d_out] (row t of example i is g_t), compute dtype
+ *   dev_lengths: NULL (every example has T tokens) or device int32 [n]; only
+ *     the first lengths[i] token rows of example i contribute (variable T_i,
+ *     Eq. (4)); values are clamped to [0, T] on the device.
+ * Pointers are borrowed, not copied: they must stay valid and unmodified
+ * until the GPU work of every call that reads them has completed.  Layers
+ * that pass the same A pointer (same d_in, n, T, lengths) share one read of A
+ * in the factored route (e.g. q/k/v projections of one attention block).
+ * Every registered layer must be captured with the same n before projecting.
+ * Errors: INVALID_ARG (bad layer, NULL A/B with n*T > 0, n < 0, T < 0),
+ * SHAPE (n*T*d beyond 2^31 elements per example block). */
+dattri_status dattri_capture_layer(dattri_ctx* ctx, int32_t layer, const void* A, const void* B,
+                                   int32_t n, int32_t T, const int32_t* dev_lengths);
+
+/* Forget every capture (pointers are no longer referenced afterwards). */
+dattri_status dattri_clear_captures(dattri_ctx* ctx);
+
+/* ------------------------------------------------------------- projection */
+
+/* Bytes of workspace dattri_project_per_example needs for the current
+ * captures with the given route override.  Materialized layers stage their
+ * weight gradients G (float32, d_out x d_in per example) in the workspace, a
+ * bounded number of examples at a time; `bytes` is the size this build plans
+ * for (any workspace at least this large works).
+ * Errors: STATE (a registered layer not captured, or captures disagree on n). */
+dattri_status dattri_workspace_bytes(const dattri_ctx* ctx, dattri_route route, size_t* bytes);
+
+/* Projected per-example gradients of every registered layer, concatenated
+ * (Eq. (2) per layer; blocks in registration order).
+ *   phi: device [n, ld_phi] of phi_dtype (F32 or BF16), ld_phi >= F; row i is
+ *        example i of the captures; columns >= F are not written.
+ *   workspace: device, >= dattri_workspace_bytes(route) bytes, 256-byte aligned.
+ *   route: AUTO (cost model per layer) or a route forced for every layer.
+ * Accumulation is float32 throughout; a bf16 phi is rounded once at the end.
+ * Errors: STATE (maps not bound, captures missing/inconsistent), SHAPE,
+ * WORKSPACE, UNSUPPORTED (factored route forced on a layer with k_in > 128
+ * or k_out > 64), HIP. */
+dattri_status dattri_project_per_example(dattri_ctx* ctx, void* phi, dattri_dtype phi_dtype,
+                                         int64_t ld_phi, void* workspace, size_t ws_bytes,
+                                         dattri_route route, void* stream);
+
+/* Materialized representation (Eq. (1)): G_i = B_i^T A_i = sum_t g_t a_t^T for
+ * captured examples [ex_begin, ex_begin + ex_count) of one layer, written as
+ * float32 G_out [ex_count, d_out, d_in] (device).  Needs no workspace.
+ * Errors: INVALID_ARG (bad layer or range, NULL G_out), STATE (not captured), HIP. */
+dattri_status dattri_materialize_gradient(dattri_ctx* ctx, int32_t layer, int32_t ex_begin,
+                                          int32_t ex_count, float* G_out, void* stream);
+
+/* ------------------------------------------------------------- cost model */
+
+/* Rates of the MI355X time model.  Predicted time of a route for one layer
+ * and n examples = sum over its kernels of
+ *   max(flops / rate, bytes / bandwidth) + launch_us,
+ * with exact integer FLOP and byte counts (dattri_layer_costs). */
+typedef struct {
+  double factored_tflops;     /* effective MFMA rate of the fused factored kernel */
+  double factored_gbs;        /* effective HBM bandwidth of the fused factored kernel */
+  double gradient_tflops;     /* G = B^T A kernel */
+  double gradient_gbs;
+  double gproject_tflops;     /* P_out^T G P_in kernel (float32) */
+  double gproject_gbs;
+  double launch_us;           /* per kernel launch */
+} dattri_cost_model;
+
+/* Replace / read the context's cost model (all rates > 0, launch_us >= 0). */
+dattri_status dattri_set_cost_model(dattri_ctx* ctx, const dattri_cost_model* model);
+dattri_status dattri_get_cost_model(const dattri_ctx* ctx, dattri_cost_model* model);
+
+/* Exact per-example operation counts of a layer's two routes for T tokens
+ * (any of the outputs may be NULL):
+ *   factored FLOP      2T(d_in k_in + d_out k_out + k_in k_out)
+ *   materialized FLOP  2T d_in d_out + 2 d_out d_in k_in + 2 d_out k_in k_out
+ *                      (the association (G P_in) first, which this build runs)
+ *   factored bytes     T (d_in + d_out) elt      (factor blocks read once)
+ *   materialized bytes factored bytes + 2 * 4 d_out d_in (G written and read)
+ * Errors: INVALID_ARG (bad layer, T < 0). */
+dattri_status dattri_layer_costs(const dattri_ctx* ctx, int32_t layer, int32_t T,
+                                 int64_t* factored_flops, int64_t* materialized_flops,
+                                 int64_t* factored_bytes, int64_t* materialized_bytes);
+
+/* Route the cost model picks for a layer given its current capture (n, T),
+ * with both predicted times in microseconds (ties go to FACTORED).  A layer
+ * whose k exceeds the factored kernel's limits always routes MATERIALIZED.
+ * Errors: INVALID_ARG (bad layer), STATE (layer not captured). */
+dattri_status dattri_layer_route(const dattri_ctx* ctx, int32_t layer, dattri_route* chosen,
+                                 double* pred_factored_us, double* pred_materialized_us);
+
+/* ---------------------------------------------------------------- scoring */
+
+/* Workspace bytes dattri_score needs for these sizes.  `has_precond` and
+ * `has_scores` say whether dev_precond_diag and scores will be non-NULL. */
+dattri_status dattri_score_workspace_bytes(int64_t n_q, int64_t n_train, int64_t F,
+                                           dattri_dtype dtype, int32_t has_precond,
+                                           int32_t has_scores, int32_t topk, size_t* bytes);
+
+/* GradDot scores with an optional diagonal preconditioner, and top-k.
+ *   phi_q:     device [n_q, F] of dtype;  phi_train: device [n_train, F] of dtype
+ *   dev_precond_diag: NULL (d = 1) or device float32 [F], d > 0, applied once:
+ *              S[q][j] = sum_f phi_q[q][f] d[f] phi_train[j][f].  For bf16 the
+ *              query row is scaled in float32 and rounded once to bf16.
+ *   scores:    device float32 [n_q, n_train], or NULL if only top-k is wanted
+ *   topk:      0 (no selection) or 1 <= topk <= min(n_train, 1024)
+ *   topk_idx:  device int32 [n_q, topk]; topk_val: device float32 [n_q, topk]:
+ *              per query the topk largest scores, largest first; equal scores
+ *              are ordered by lower training index (-0.0 equals +0.0; NaN
+ *              scores are not supported).
+ *   workspace: device, >= dattri_score_workspace_bytes(...), 256-byte aligned.
+ * Accumulation is float32.  Errors: INVALID_ARG, DTYPE, WORKSPACE,
+ * UNSUPPORTED (topk > 1024), HIP. */
+dattri_status dattri_score(const void* phi_q, int64_t n_q, const void* phi_train, int64_t n_train,
+                           int64_t F, dattri_dtype dtype, const float* dev_precond_diag,
+                           float* scores, int32_t topk, int32_t* topk_idx, float* topk_val,
+                           void* workspace, size_t ws_bytes, void* stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* DATTRI_H */

@@ -1,0 +1,262 @@
+"""Python binding of libdattri (MI355X projected-gradient attribution).
+
+Argument marshalling only: every function here has the name of a C entry point
+declared in include/dattri.h, converts its arguments (torch tensors become
+device pointers, ``stream=None`` becomes torch's current HIP stream), calls the
+library, raises ``DattriError`` on a non-OK status, and returns the C
+function's output parameters.  No computation happens in Python, and there is
+no fallback: if libdattri.so is missing, every call raises.
+
+Build the library with ``python -m paper_2609_38767_amd.build``.
+"""
+import ctypes
+import os
+
+__all__ = [
+    "DattriError", "lib_path", "load",
+    "DATTRI_F32", "DATTRI_BF16", "DATTRI_ROUTE_AUTO", "DATTRI_ROUTE_FACTORED",
+    "DATTRI_ROUTE_MATERIALIZED", "STATUS_NAMES", "EXPORTED",
+    "dattri_create", "dattri_destroy", "dattri_last_error", "dattri_register_layer",
+    "dattri_num_layers", "dattri_layer_dims", "dattri_feature_dim", "dattri_layer_offset",
+    "dattri_projection_bytes", "dattri_bind_projection", "dattri_get_projection",
+    "dattri_capture_layer", "dattri_clear_captures", "dattri_workspace_bytes",
+    "dattri_project_per_example", "dattri_materialize_gradient", "dattri_set_cost_model",
+    "dattri_get_cost_model", "dattri_layer_costs", "dattri_layer_route",
+    "dattri_score_workspace_bytes", "dattri_score",
+]
+
+DATTRI_F32, DATTRI_BF16 = 0, 1
+DATTRI_ROUTE_AUTO, DATTRI_ROUTE_FACTORED, DATTRI_ROUTE_MATERIALIZED = 0, 1, 2
+STATUS_NAMES = {0: "OK", -1: "E_INVALID_ARG", -2: "E_SHAPE", -3: "E_DTYPE", -4: "E_STATE",
+                -5: "E_WORKSPACE", -6: "E_HIP", -7: "E_UNSUPPORTED"}
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+lib_path = os.path.join(_HERE, "libdattri.so")
+
+
+class DattriError(RuntimeError):
+    def __init__(self, status, message, func):
+        self.status = status
+        self.status_name = STATUS_NAMES.get(status, str(status))
+        super().__init__(f"{func}: {self.status_name}: {message}")
+
+
+class CostModel(ctypes.Structure):
+    _fields_ = [("factored_tflops", ctypes.c_double), ("factored_gbs", ctypes.c_double),
+                ("gradient_tflops", ctypes.c_double), ("gradient_gbs", ctypes.c_double),
+                ("gproject_tflops", ctypes.c_double), ("gproject_gbs", ctypes.c_double),
+                ("launch_us", ctypes.c_double)]
+
+
+_i32, _i64, _u64, _sz = ctypes.c_int32, ctypes.c_int64, ctypes.c_uint64, ctypes.c_size_t
+_vp, _dbl = ctypes.c_void_p, ctypes.c_double
+_P = ctypes.POINTER
+
+# name -> (restype, argtypes); the complete exported C ABI.
+_SIGS = {
+    "dattri_create": (_i32, [_P(_vp), _i32, _u64]),
+    "dattri_destroy": (None, [_vp]),
+    "dattri_last_error": (ctypes.c_char_p, []),
+    "dattri_register_layer": (_i32, [_vp, _i32, _i32, _i32, _i32, _P(_i32)]),
+    "dattri_num_layers": (_i32, [_vp, _P(_i32)]),
+    "dattri_layer_dims": (_i32, [_vp, _i32, _P(_i32), _P(_i32), _P(_i32), _P(_i32)]),
+    "dattri_feature_dim": (_i32, [_vp, _P(_i64)]),
+    "dattri_layer_offset": (_i32, [_vp, _i32, _P(_i64)]),
+    "dattri_projection_bytes": (_i32, [_vp, _i32, _P(_sz), _P(_sz)]),
+    "dattri_bind_projection": (_i32, [_vp, _i32, _vp, _vp, _vp, _vp, _vp]),
+    "dattri_get_projection": (_i32, [_vp, _i32, _vp, _vp]),
+    "dattri_capture_layer": (_i32, [_vp, _i32, _vp, _vp, _i32, _i32, _vp]),
+    "dattri_clear_captures": (_i32, [_vp]),
+    "dattri_workspace_bytes": (_i32, [_vp, _i32, _P(_sz)]),
+    "dattri_project_per_example": (_i32, [_vp, _vp, _i32, _i64, _vp, _sz, _i32, _vp]),
+    "dattri_materialize_gradient": (_i32, [_vp, _i32, _i32, _i32, _vp, _vp]),
+    "dattri_set_cost_model": (_i32, [_vp, _P(CostModel)]),
+    "dattri_get_cost_model": (_i32, [_vp, _P(CostModel)]),
+    "dattri_layer_costs": (_i32, [_vp, _i32, _i32, _P(_i64), _P(_i64), _P(_i64), _P(_i64)]),
+    "dattri_layer_route": (_i32, [_vp, _i32, _P(_i32), _P(_dbl), _P(_dbl)]),
+    "dattri_score_workspace_bytes": (_i32, [_i64, _i64, _i64, _i32, _i32, _i32, _i32, _P(_sz)]),
+    "dattri_score": (_i32, [_vp, _i64, _vp, _i64, _i64, _i32, _vp, _vp, _i32, _vp, _vp, _vp, _sz, _vp]),
+}
+EXPORTED = tuple(_SIGS)
+
+_lib = None
+
+
+def load():
+    """Load libdattri.so (once).  Raises if it has not been built."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(lib_path):
+            raise RuntimeError(f"{lib_path} is not built; run `python -m paper_2609_38767_amd.build`")
+        lib = ctypes.CDLL(lib_path)
+        for name, (res, args) in _SIGS.items():
+            fn = getattr(lib, name)
+            fn.restype = res
+            fn.argtypes = args
+        _lib = lib
+    return _lib
+
+
+def _check(status, func):
+    if status != 0:
+        raise DattriError(status, load().dattri_last_error().decode(), func)
+
+
+def _ptr(x):
+    """Device/host pointer of a tensor or array, an int address, or None."""
+    if x is None:
+        return None
+    if isinstance(x, int):
+        return x
+    if hasattr(x, "data_ptr"):
+        return x.data_ptr()
+    if hasattr(x, "ctypes"):
+        return x.ctypes.data
+    raise TypeError(f"cannot take a pointer of {type(x)}")
+
+
+def _stream(s):
+    if s is None:
+        import torch
+        return torch.cuda.current_stream().cuda_stream if torch.cuda.is_available() else None
+    if isinstance(s, int):
+        return s
+    return s.cuda_stream
+
+
+def dattri_last_error():
+    return load().dattri_last_error().decode()
+
+
+def dattri_create(compute, seed):
+    ctx = _vp()
+    _check(load().dattri_create(ctypes.byref(ctx), compute, seed), "dattri_create")
+    return ctx.value
+
+
+def dattri_destroy(ctx):
+    load().dattri_destroy(ctx)
+
+
+def dattri_register_layer(ctx, d_in, d_out, k_in, k_out):
+    lid = _i32()
+    _check(load().dattri_register_layer(ctx, d_in, d_out, k_in, k_out, ctypes.byref(lid)),
+           "dattri_register_layer")
+    return lid.value
+
+
+def dattri_num_layers(ctx):
+    n = _i32()
+    _check(load().dattri_num_layers(ctx, ctypes.byref(n)), "dattri_num_layers")
+    return n.value
+
+
+def dattri_layer_dims(ctx, layer):
+    v = [_i32() for _ in range(4)]
+    _check(load().dattri_layer_dims(ctx, layer, *[ctypes.byref(x) for x in v]), "dattri_layer_dims")
+    return tuple(x.value for x in v)
+
+
+def dattri_feature_dim(ctx):
+    F = _i64()
+    _check(load().dattri_feature_dim(ctx, ctypes.byref(F)), "dattri_feature_dim")
+    return F.value
+
+
+def dattri_layer_offset(ctx, layer):
+    o = _i64()
+    _check(load().dattri_layer_offset(ctx, layer, ctypes.byref(o)), "dattri_layer_offset")
+    return o.value
+
+
+def dattri_projection_bytes(ctx, layer):
+    a, b = _sz(), _sz()
+    _check(load().dattri_projection_bytes(ctx, layer, ctypes.byref(a), ctypes.byref(b)),
+           "dattri_projection_bytes")
+    return a.value, b.value
+
+
+def dattri_bind_projection(ctx, layer, dev_P_in, dev_P_out, host_P_in_override=None,
+                           host_P_out_override=None, stream=None):
+    _check(load().dattri_bind_projection(ctx, layer, _ptr(dev_P_in), _ptr(dev_P_out),
+                                         _ptr(host_P_in_override), _ptr(host_P_out_override),
+                                         _stream(stream)), "dattri_bind_projection")
+
+
+def dattri_get_projection(ctx, layer):
+    """Returns (P_in [d_in, k_in], P_out [d_out, k_out]) as float32 numpy arrays."""
+    import numpy as np
+    d_in, d_out, k_in, k_out = dattri_layer_dims(ctx, layer)
+    p_in = np.empty((d_in, k_in), dtype=np.float32)
+    p_out = np.empty((d_out, k_out), dtype=np.float32)
+    _check(load().dattri_get_projection(ctx, layer, p_in.ctypes.data, p_out.ctypes.data),
+           "dattri_get_projection")
+    return p_in, p_out
+
+
+def dattri_capture_layer(ctx, layer, A, B, n, T, dev_lengths=None):
+    _check(load().dattri_capture_layer(ctx, layer, _ptr(A), _ptr(B), n, T, _ptr(dev_lengths)),
+           "dattri_capture_layer")
+
+
+def dattri_clear_captures(ctx):
+    _check(load().dattri_clear_captures(ctx), "dattri_clear_captures")
+
+
+def dattri_workspace_bytes(ctx, route=DATTRI_ROUTE_AUTO):
+    b = _sz()
+    _check(load().dattri_workspace_bytes(ctx, route, ctypes.byref(b)), "dattri_workspace_bytes")
+    return b.value
+
+
+def dattri_project_per_example(ctx, phi, phi_dtype, ld_phi, workspace, ws_bytes,
+                               route=DATTRI_ROUTE_AUTO, stream=None):
+    _check(load().dattri_project_per_example(ctx, _ptr(phi), phi_dtype, ld_phi, _ptr(workspace),
+                                             ws_bytes, route, _stream(stream)),
+           "dattri_project_per_example")
+
+
+def dattri_materialize_gradient(ctx, layer, ex_begin, ex_count, G_out, stream=None):
+    _check(load().dattri_materialize_gradient(ctx, layer, ex_begin, ex_count, _ptr(G_out),
+                                              _stream(stream)), "dattri_materialize_gradient")
+
+
+def dattri_set_cost_model(ctx, model):
+    m = CostModel(**model) if isinstance(model, dict) else model
+    _check(load().dattri_set_cost_model(ctx, ctypes.byref(m)), "dattri_set_cost_model")
+
+
+def dattri_get_cost_model(ctx):
+    m = CostModel()
+    _check(load().dattri_get_cost_model(ctx, ctypes.byref(m)), "dattri_get_cost_model")
+    return {name: getattr(m, name) for name, _ in CostModel._fields_}
+
+
+def dattri_layer_costs(ctx, layer, T):
+    v = [_i64() for _ in range(4)]
+    _check(load().dattri_layer_costs(ctx, layer, T, *[ctypes.byref(x) for x in v]),
+           "dattri_layer_costs")
+    return tuple(x.value for x in v)
+
+
+def dattri_layer_route(ctx, layer):
+    r, f, m = _i32(), _dbl(), _dbl()
+    _check(load().dattri_layer_route(ctx, layer, ctypes.byref(r), ctypes.byref(f), ctypes.byref(m)),
+           "dattri_layer_route")
+    return r.value, f.value, m.value
+
+
+def dattri_score_workspace_bytes(n_q, n_train, F, dtype, has_precond, has_scores, topk):
+    b = _sz()
+    _check(load().dattri_score_workspace_bytes(n_q, n_train, F, dtype, int(bool(has_precond)),
+                                               int(bool(has_scores)), topk, ctypes.byref(b)),
+           "dattri_score_workspace_bytes")
+    return b.value
+
+
+def dattri_score(phi_q, n_q, phi_train, n_train, F, dtype, dev_precond_diag, scores, topk,
+                 topk_idx, topk_val, workspace, ws_bytes, stream=None):
+    _check(load().dattri_score(_ptr(phi_q), n_q, _ptr(phi_train), n_train, F, dtype,
+                               _ptr(dev_precond_diag), _ptr(scores), topk, _ptr(topk_idx),
+                               _ptr(topk_val), _ptr(workspace), ws_bytes, _stream(stream)),
+           "dattri_score")

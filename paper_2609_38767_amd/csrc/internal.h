@@ -1,0 +1,115 @@
+// Internal interface between the host runtime (runtime.cpp) and the HIP
+// kernels (*.hip).  Plain descriptors uploaded into the caller's workspace and
+// launcher prototypes; nothing here is part of the public C ABI.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace dattri {
+
+// ---------------------------------------------------------------- layout
+// Projection maps live on the device in a fragment-major layout: the d x k map
+// is cut into k-blocks of KROWS rows and 16-column tiles; fragment (kb, nt) is
+// 64 lanes x 16 bytes, lane l = 16*g + n holding the EPL consecutive rows
+// kb*KROWS + g*EPL + j (j < EPL) of column nt*16 + n.  One wave reads one
+// fragment with a single coalesced 1 KiB load, already in MFMA operand order.
+//   bf16: EPL = 8, KROWS = 32 (operand of v_mfma_f32_16x16x32_bf16)
+//   f32 : EPL = 4, KROWS = 16 (four v_mfma_f32_16x16x4f32, one per element)
+constexpr int kFragBytes = 1024;
+inline int epl_of(int elt_bytes) { return elt_bytes == 2 ? 8 : 4; }
+inline int krows_of(int elt_bytes) { return 4 * epl_of(elt_bytes); }
+inline int64_t packed_bytes(int d, int k, int elt_bytes) {
+  const int64_t kb = (d + krows_of(elt_bytes) - 1) / krows_of(elt_bytes);
+  const int64_t nt = (k + 15) / 16;
+  return kb * nt * kFragBytes;
+}
+inline int64_t packed_offset(int v, int c, int k, int elt_bytes) {
+  const int epl = epl_of(elt_bytes), kr = krows_of(elt_bytes);
+  const int64_t nt_all = (k + 15) / 16;
+  const int kb = v / kr, w = v % kr, g = w / epl, j = w % epl;
+  const int nt = c / 16, n = c % 16, lane = 16 * g + n;
+  return ((kb * nt_all + nt) * 64 + lane) * 16 + (int64_t)j * elt_bytes;
+}
+
+// ------------------------------------------------------- factored route
+constexpr int kMaxGroupTiles = 8;   // input-side 16-column tiles per group
+constexpr int kMaxMemberBTiles = 4; // output-side 16-column tiles per layer
+constexpr int kWaves = 4;           // waves per workgroup (256 threads)
+
+struct FactGroup {                  // layers sharing one input block A
+  const void* A;                    // [n, T, d_in]
+  const int32_t* lengths;           // [n] or null
+  int32_t d_in, T, n;
+  int32_t n_chunks, chunk_rows;     // token chunks per example
+  int32_t n_members, member0;       // members: FactMember[member0 ...]
+  int32_t na;                       // input-side tiles in use (<= 8)
+  int32_t aligned;                  // 16-byte vector loads allowed
+  int32_t pad0;
+  const void* ptile[kMaxGroupTiles];    // packed P_in of the tile's layer
+  int32_t ptile_local[kMaxGroupTiles];  // tile index inside that P_in
+  int32_t ptile_nt[kMaxGroupTiles];     // 16-col tiles of that P_in
+};
+
+struct FactMember {                 // one layer of a group
+  const void* B;                    // [n, T, d_out]
+  const void* P_out;                // packed [d_out x k_out]
+  int32_t d_out, k_in, k_out;
+  int32_t a_tile0, na, nb;          // its input tiles [a_tile0, a_tile0+na), output tiles
+  int32_t aligned, pad0;
+  int64_t partial_base;             // float offset of (example 0, part 0)
+};
+
+struct FactItem { int32_t group, example, chunk, pad; };
+
+// Partial blocks Psi (padded na*16 x nb*16 float32, row-major) are summed in a
+// fixed order by the reduce kernel, which writes phi.
+struct ReduceTask {
+  int64_t partial_base;             // float offset of (example 0, part 0)
+  int64_t phi_offset;               // column of the layer block in phi
+  int32_t n_parts;                  // partial blocks per example
+  int32_t k_in, k_out, ldp;         // ldp = nb*16 (row stride of a partial)
+  int32_t part_floats;              // na*16*nb*16
+  int32_t ex_begin;                 // first example of this task's rows
+  int32_t pad0, pad1;
+};
+
+hipError_t launch_factored(int elt_bytes, int na, int nb, const FactItem* items, int n_items,
+                           const FactGroup* groups, const FactMember* members, float* partials,
+                           hipStream_t s);
+void factored_instance(int elt_bytes, int na_req, int nb_req, int* na_inst, int* nb_inst,
+                       int* rows_per_wave);
+
+hipError_t launch_reduce(const ReduceTask* tasks, int n_tasks, int n_examples,
+                         const float* partials, void* phi, int phi_bf16, int64_t ld_phi,
+                         hipStream_t s);
+
+// ---------------------------------------------------- materialized route
+struct GradArgs {
+  const void* A; const void* B; const int32_t* lengths;
+  int32_t d_in, d_out, T, ex_begin, ex_count, aligned;
+  float* G;                         // [ex_count, d_out, d_in]
+};
+hipError_t launch_gradient(int elt_bytes, const GradArgs& a, hipStream_t s);
+
+struct GProjArgs {
+  const float* G;                   // [ex_count, d_out, d_in]
+  const void* P_in; const void* P_out;  // packed
+  int32_t d_in, d_out, k_in, k_out, ex_count, n_ublocks;
+  float* partials;                  // [ex_count, n_ublocks*4, na*16 x nb*16]
+};
+constexpr int kGProjRows = 64;      // rows of G per workgroup (4 waves x 16)
+constexpr int kGProjMaxTilesIn = 8;  // k_in  <= 128
+constexpr int kGProjMaxTilesOut = 8; // k_out <= 128
+hipError_t launch_gproject(int elt_bytes, const GProjArgs& a, hipStream_t s);
+
+// ---------------------------------------------------------------- scoring
+hipError_t launch_scale_rows(int elt_bytes, const void* src, const float* d, void* dst,
+                             int64_t rows, int64_t F, hipStream_t s);
+hipError_t launch_score_gemm(int elt_bytes, const void* Q, const void* X, float* S, int64_t n_q,
+                             int64_t n_train, int64_t F, hipStream_t s);
+constexpr int kTopkMax = 1024;
+hipError_t launch_topk(const float* S, int64_t n_q, int64_t n_train, int32_t k, int32_t* idx,
+                       float* val, hipStream_t s);
+
+}  // namespace dattri

@@ -1,0 +1,762 @@
+// Host runtime of libdattri: context, layer registry, validation, the MI355X
+// cost model that routes each layer (Sec. 3.2 "FLOP-aware routing", App. A.4),
+// launch planning and the C ABI declared in include/dattri.h.
+#include <algorithm>
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <string>
+#include <vector>
+
+#include "dattri.h"
+#include "internal.h"
+#include "runtime.h"
+
+using namespace dattri;
+
+namespace {
+
+thread_local std::string g_err;
+
+dattri_status fail(dattri_status st, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  std::vsnprintf(buf, sizeof(buf), fmt, ap);
+  va_end(ap);
+  g_err = buf;
+  return st;
+}
+
+inline void reset_error() { g_err.clear(); }
+
+#define HIP_TRY(expr)                                                                     \
+  do {                                                                                    \
+    hipError_t e_ = (expr);                                                               \
+    if (e_ != hipSuccess)                                                                 \
+      return fail(DATTRI_E_HIP, "%s failed: %s", #expr, hipGetErrorString(e_));           \
+  } while (0)
+
+constexpr int kMaxDim = 1 << 20;
+constexpr int64_t kMaxBlockBytes = ((int64_t)1 << 32) - 4096;  // one example's factor block
+constexpr size_t kAlign = 256;
+constexpr int64_t kGBudgetBytes = (int64_t)2 << 30;   // staged G per materialized chunk
+
+inline size_t align_up(size_t x, size_t a = kAlign) { return (x + a - 1) / a * a; }
+inline int tiles16(int k) { return (k + 15) / 16; }
+
+struct Layer {
+  int32_t d_in = 0, d_out = 0, k_in = 0, k_out = 0;
+  int64_t offset = 0;
+  void* P_in = nullptr;
+  void* P_out = nullptr;
+  bool bound = false;
+  std::vector<float> override_in, override_out;  // rounded values when overridden
+  const void* A = nullptr;
+  const void* B = nullptr;
+  int32_t n = 0, T = 0;
+  const int32_t* lengths = nullptr;
+  bool captured = false;
+};
+
+bool factored_supported(const Layer& L) {
+  return tiles16(L.k_in) <= kMaxGroupTiles && tiles16(L.k_out) <= kMaxMemberBTiles;
+}
+
+dattri_cost_model default_cost_model() {
+  // Starting rates for MI355X before calibration (spec peaks scaled by the
+  // efficiency a first kernel version typically reaches).
+  dattri_cost_model m;
+  m.factored_tflops = 600.0;
+  m.factored_gbs = 5000.0;
+  m.gradient_tflops = 800.0;
+  m.gradient_gbs = 4000.0;
+  m.gproject_tflops = 60.0;
+  m.gproject_gbs = 3000.0;
+  m.launch_us = 4.0;
+  return m;
+}
+
+}  // namespace
+
+struct dattri_ctx {
+  dattri_dtype dtype;
+  int elt;
+  uint64_t seed;
+  std::vector<Layer> layers;
+  int64_t F = 0;
+  dattri_cost_model cost;
+  std::vector<uint8_t> blob;  // host copy of the last uploaded launch plan
+};
+
+namespace {
+
+// ------------------------------------------------------------- cost model
+struct Counts {
+  int64_t f_flops, m_flops, f_bytes, m_bytes, g_flops, g_bytes, p_flops, p_bytes;
+};
+
+Counts layer_counts(const Layer& L, int64_t T, int elt) {
+  Counts c;
+  const int64_t di = L.d_in, dq = L.d_out, ki = L.k_in, ko = L.k_out;
+  c.f_flops = 2 * T * (di * ki + dq * ko + ki * ko);
+  c.g_flops = 2 * T * di * dq;
+  c.p_flops = 2 * dq * di * ki + 2 * dq * ki * ko;
+  c.m_flops = c.g_flops + c.p_flops;
+  c.f_bytes = T * (di + dq) * elt;
+  c.g_bytes = c.f_bytes + 4 * dq * di;
+  c.p_bytes = 4 * dq * di;
+  c.m_bytes = c.g_bytes + c.p_bytes;
+  return c;
+}
+
+void predict(const dattri_cost_model& m, const Layer& L, int64_t n, int64_t T, int elt, double* f_us,
+             double* m_us) {
+  const Counts c = layer_counts(L, T, elt);
+  auto t = [](double flops, double tflops, double bytes, double gbs) {
+    return std::max(flops / (tflops * 1e6), bytes / (gbs * 1e3));  // microseconds
+  };
+  *f_us = t((double)c.f_flops * n, m.factored_tflops, (double)c.f_bytes * n, m.factored_gbs) +
+          m.launch_us;
+  *m_us = t((double)c.g_flops * n, m.gradient_tflops, (double)c.g_bytes * n, m.gradient_gbs) +
+          t((double)c.p_flops * n, m.gproject_tflops, (double)c.p_bytes * n, m.gproject_gbs) +
+          3 * m.launch_us;
+}
+
+dattri_route choose_route(const dattri_ctx* ctx, const Layer& L, dattri_route forced) {
+  if (forced != DATTRI_ROUTE_AUTO) return forced;
+  if (!factored_supported(L)) return DATTRI_ROUTE_MATERIALIZED;
+  double f, m;
+  predict(ctx->cost, L, L.n, L.T, ctx->elt, &f, &m);
+  return f <= m ? DATTRI_ROUTE_FACTORED : DATTRI_ROUTE_MATERIALIZED;
+}
+
+// ---------------------------------------------------------------- planning
+struct MatChunk {
+  int layer, ex_begin, ex_count, n_ublocks, task;
+};
+
+struct Plan {
+  // host-side descriptors (device pointers inside)
+  std::vector<FactItem> items;
+  std::vector<FactGroup> groups;
+  std::vector<FactMember> members;
+  std::vector<ReduceTask> tasks;  // factored tasks first, then one per MatChunk
+  int n_fact_tasks = 0;
+  struct Launch { int elt, na, nb, first, count; };
+  std::vector<Launch> launches;
+  std::vector<MatChunk> mat;
+  // workspace layout (byte offsets)
+  size_t off_items = 0, off_groups = 0, off_members = 0, off_tasks = 0, blob_bytes = 0;
+  size_t off_fpart = 0, fpart_bytes = 0, off_g = 0, g_bytes = 0, off_mpart = 0, mpart_bytes = 0;
+  size_t total = 0;
+};
+
+dattri_status check_captures(const dattri_ctx* ctx, int32_t* n_out) {
+  if (ctx->layers.empty()) return fail(DATTRI_E_STATE, "no layer registered");
+  int32_t n = -1;
+  for (size_t l = 0; l < ctx->layers.size(); ++l) {
+    const Layer& L = ctx->layers[l];
+    if (!L.captured) return fail(DATTRI_E_STATE, "layer %zu has no capture", l);
+    if (n < 0) n = L.n;
+    if (L.n != n)
+      return fail(DATTRI_E_STATE, "layer %zu captured with n=%d but layer 0 with n=%d", l, L.n, n);
+  }
+  *n_out = n;
+  return DATTRI_OK;
+}
+
+dattri_status build_plan(const dattri_ctx* ctx, dattri_route forced, Plan& P) {
+  int32_t n = 0;
+  dattri_status st = check_captures(ctx, &n);
+  if (st != DATTRI_OK) return st;
+  const int elt = ctx->elt;
+
+  // ---- factored layers: group by shared input block A
+  std::vector<std::vector<int>> group_layers;
+  for (size_t l = 0; l < ctx->layers.size(); ++l) {
+    const Layer& L = ctx->layers[l];
+    const dattri_route r = choose_route(ctx, L, forced);
+    if (r == DATTRI_ROUTE_MATERIALIZED) continue;
+    if (!factored_supported(L))
+      return fail(DATTRI_E_UNSUPPORTED,
+                  "layer %zu: factored route needs k_in <= %d and k_out <= %d (got %d, %d)", l,
+                  16 * kMaxGroupTiles, 16 * kMaxMemberBTiles, L.k_in, L.k_out);
+    int found = -1;
+    for (size_t g = 0; g < group_layers.size() && found < 0; ++g) {
+      const Layer& H = ctx->layers[group_layers[g][0]];
+      int na = 0;
+      for (int m : group_layers[g]) na += tiles16(ctx->layers[m].k_in);
+      if (H.A == L.A && H.d_in == L.d_in && H.T == L.T && H.lengths == L.lengths &&
+          L.A != nullptr && na + tiles16(L.k_in) <= kMaxGroupTiles)
+        found = (int)g;
+    }
+    if (found < 0) {
+      group_layers.push_back({(int)l});
+    } else {
+      group_layers[found].push_back((int)l);
+    }
+  }
+
+  size_t fpart_floats = 0;
+  struct ItemKey { FactItem it; double cost; int inst; };
+  std::vector<ItemKey> keyed;
+  std::vector<std::pair<int, int>> insts;  // (na_inst, nb_inst)
+  for (size_t g = 0; g < group_layers.size(); ++g) {
+    const Layer& H = ctx->layers[group_layers[g][0]];
+    FactGroup G;
+    std::memset(&G, 0, sizeof(G));
+    G.A = H.A;
+    G.lengths = H.lengths;
+    G.d_in = H.d_in;
+    G.T = H.T;
+    G.n = n;
+    G.n_members = (int)group_layers[g].size();
+    G.member0 = (int)P.members.size();
+    G.aligned = ((uintptr_t)H.A % 16 == 0) && (H.d_in * elt) % 16 == 0;
+    int na = 0, nb_max = 0;
+    double bytes_per_row = (double)H.d_in;
+    for (int li : group_layers[g]) {
+      const Layer& L = ctx->layers[li];
+      FactMember M;
+      std::memset(&M, 0, sizeof(M));
+      M.B = L.B;
+      M.P_out = L.P_out;
+      M.d_out = L.d_out;
+      M.k_in = L.k_in;
+      M.k_out = L.k_out;
+      M.a_tile0 = na;
+      M.na = tiles16(L.k_in);
+      M.nb = tiles16(L.k_out);
+      M.aligned = ((uintptr_t)L.B % 16 == 0) && (L.d_out * elt) % 16 == 0;
+      for (int t = 0; t < M.na; ++t) {
+        G.ptile[na + t] = L.P_in;
+        G.ptile_local[na + t] = t;
+        G.ptile_nt[na + t] = M.na;
+      }
+      na += M.na;
+      nb_max = std::max(nb_max, M.nb);
+      bytes_per_row += L.d_out;
+      P.members.push_back(M);
+    }
+    G.na = na;
+    int na_inst, nb_inst, rt;
+    factored_instance(elt, na, nb_max, &na_inst, &nb_inst, &rt);
+    const int sub_rows = kWaves * rt * 16;
+    int cr = std::max(sub_rows, 512 / sub_rows * sub_rows);
+    if (H.T <= cr) cr = std::max(sub_rows, (H.T + sub_rows - 1) / sub_rows * sub_rows);
+    G.chunk_rows = cr;
+    G.n_chunks = std::max(1, (H.T + cr - 1) / cr);
+    // partial blocks of each member: [n][n_chunks * waves][na*16 x nb*16]
+    for (int m = 0; m < G.n_members; ++m) {
+      FactMember& M = P.members[G.member0 + m];
+      M.partial_base = (int64_t)fpart_floats;
+      const int64_t part = (int64_t)M.na * 16 * M.nb * 16;
+      fpart_floats += (size_t)n * G.n_chunks * kWaves * part;
+      ReduceTask R;
+      std::memset(&R, 0, sizeof(R));
+      R.partial_base = M.partial_base;
+      R.phi_offset = ctx->layers[group_layers[g][m]].offset;
+      R.n_parts = G.n_chunks * kWaves;
+      R.k_in = M.k_in;
+      R.k_out = M.k_out;
+      R.ldp = M.nb * 16;
+      R.part_floats = (int32_t)part;
+      R.ex_begin = 0;
+      P.tasks.push_back(R);
+    }
+    int inst = -1;
+    for (size_t i = 0; i < insts.size(); ++i)
+      if (insts[i].first == na_inst && insts[i].second == nb_inst) inst = (int)i;
+    if (inst < 0) { insts.push_back({na_inst, nb_inst}); inst = (int)insts.size() - 1; }
+    for (int e = 0; e < n; ++e)
+      for (int c = 0; c < G.n_chunks; ++c) {
+        const int rows = std::min(cr, std::max(0, H.T - c * cr));
+        keyed.push_back({{(int)g, e, c, 0}, rows * bytes_per_row, inst});
+      }
+    P.groups.push_back(G);
+  }
+  P.n_fact_tasks = (int)P.tasks.size();
+  // One launch per kernel instance; inside it, costliest items first.
+  std::stable_sort(keyed.begin(), keyed.end(), [](const ItemKey& a, const ItemKey& b) {
+    return a.inst != b.inst ? a.inst < b.inst : a.cost > b.cost;
+  });
+  for (size_t i = 0; i < keyed.size(); ++i) {
+    if (P.launches.empty() || P.launches.back().na != insts[keyed[i].inst].first ||
+        P.launches.back().nb != insts[keyed[i].inst].second)
+      P.launches.push_back({elt, insts[keyed[i].inst].first, insts[keyed[i].inst].second, (int)i, 0});
+    P.launches.back().count++;
+    P.items.push_back(keyed[i].it);
+  }
+
+  // ---- materialized layers: example chunks staged through G
+  size_t g_floats = 0, mpart_floats = 0;
+  for (size_t l = 0; l < ctx->layers.size(); ++l) {
+    const Layer& L = ctx->layers[l];
+    if (choose_route(ctx, L, forced) != DATTRI_ROUTE_MATERIALIZED) continue;
+    const int64_t g_per_ex = (int64_t)L.d_out * L.d_in;
+    if (4 * g_per_ex >= kMaxBlockBytes)
+      return fail(DATTRI_E_UNSUPPORTED, "layer %zu: G = d_out x d_in float32 (%lld bytes) exceeds 4 GiB",
+                  l, (long long)(4 * g_per_ex));
+    const int ex_chunk = (int)std::max<int64_t>(
+        1, std::min<int64_t>({(int64_t)n, kGBudgetBytes / (4 * g_per_ex), (int64_t)65535}));
+    const int n_ublocks = (L.d_out + kGProjRows - 1) / kGProjRows;
+    const int64_t part = (int64_t)tiles16(L.k_in) * 16 * tiles16(L.k_out) * 16;
+    g_floats = std::max(g_floats, (size_t)(ex_chunk * g_per_ex));
+    mpart_floats = std::max(mpart_floats, (size_t)((int64_t)ex_chunk * n_ublocks * kWaves * part));
+    for (int e0 = 0; e0 < n; e0 += ex_chunk) {
+      MatChunk mc{(int)l, e0, std::min(ex_chunk, n - e0), n_ublocks, (int)P.tasks.size()};
+      ReduceTask R;
+      std::memset(&R, 0, sizeof(R));
+      R.partial_base = 0;
+      R.phi_offset = L.offset;
+      R.n_parts = n_ublocks * kWaves;
+      R.k_in = L.k_in;
+      R.k_out = L.k_out;
+      R.ldp = tiles16(L.k_out) * 16;
+      R.part_floats = (int32_t)part;
+      R.ex_begin = e0;
+      P.tasks.push_back(R);
+      P.mat.push_back(mc);
+    }
+  }
+
+  // ---- workspace layout
+  size_t off = 0;
+  P.off_items = off;   off = align_up(off + P.items.size() * sizeof(FactItem));
+  P.off_groups = off;  off = align_up(off + P.groups.size() * sizeof(FactGroup));
+  P.off_members = off; off = align_up(off + P.members.size() * sizeof(FactMember));
+  P.off_tasks = off;   off = align_up(off + P.tasks.size() * sizeof(ReduceTask));
+  P.blob_bytes = off;
+  P.off_fpart = off;   P.fpart_bytes = fpart_floats * 4; off = align_up(off + P.fpart_bytes);
+  P.off_g = off;       P.g_bytes = g_floats * 4;         off = align_up(off + P.g_bytes);
+  P.off_mpart = off;   P.mpart_bytes = mpart_floats * 4; off = align_up(off + P.mpart_bytes);
+  P.total = std::max<size_t>(off, kAlign);
+  return DATTRI_OK;
+}
+
+dattri_status check_layer(const dattri_ctx* ctx, int32_t layer) {
+  if (!ctx) return fail(DATTRI_E_INVALID_ARG, "ctx is NULL");
+  if (layer < 0 || layer >= (int32_t)ctx->layers.size())
+    return fail(DATTRI_E_INVALID_ARG, "layer %d out of range [0, %zu)", layer, ctx->layers.size());
+  return DATTRI_OK;
+}
+
+void logical_map(const dattri_ctx* ctx, int layer, int side, std::vector<float>& out) {
+  const Layer& L = ctx->layers[layer];
+  const int d = side ? L.d_out : L.d_in, k = side ? L.k_out : L.k_in;
+  const std::vector<float>& ov = side ? L.override_out : L.override_in;
+  if (!ov.empty()) { out = ov; return; }
+  out.resize((size_t)d * k);
+  seeded_map(derive_side_seed(ctx->seed, layer, side), d, k, ctx->elt, out.data());
+}
+
+}  // namespace
+
+// =================================================================== C ABI
+extern "C" {
+
+const char* dattri_last_error(void) { return g_err.c_str(); }
+
+dattri_status dattri_create(dattri_ctx** out, dattri_dtype compute, uint64_t seed) {
+  reset_error();
+  if (!out) return fail(DATTRI_E_INVALID_ARG, "out is NULL");
+  if (compute != DATTRI_F32 && compute != DATTRI_BF16)
+    return fail(DATTRI_E_DTYPE, "compute dtype %d is neither F32 nor BF16", (int)compute);
+  dattri_ctx* c = new (std::nothrow) dattri_ctx();
+  if (!c) return fail(DATTRI_E_INVALID_ARG, "out of host memory");
+  c->dtype = compute;
+  c->elt = compute == DATTRI_BF16 ? 2 : 4;
+  c->seed = seed;
+  c->cost = default_cost_model();
+  *out = c;
+  return DATTRI_OK;
+}
+
+void dattri_destroy(dattri_ctx* ctx) { delete ctx; }
+
+dattri_status dattri_register_layer(dattri_ctx* ctx, int32_t d_in, int32_t d_out, int32_t k_in,
+                                    int32_t k_out, int32_t* layer_id) {
+  reset_error();
+  if (!ctx || !layer_id) return fail(DATTRI_E_INVALID_ARG, "ctx or layer_id is NULL");
+  if (d_in < 1 || d_out < 1 || k_in < 1 || k_out < 1 || d_in > kMaxDim || d_out > kMaxDim ||
+      k_in > kMaxDim || k_out > kMaxDim)
+    return fail(DATTRI_E_INVALID_ARG, "sizes must lie in [1, 2^20]: d_in=%d d_out=%d k_in=%d k_out=%d",
+                d_in, d_out, k_in, k_out);
+  Layer L;
+  L.d_in = d_in; L.d_out = d_out; L.k_in = k_in; L.k_out = k_out;
+  L.offset = ctx->F;
+  ctx->F += (int64_t)k_in * k_out;
+  ctx->layers.push_back(std::move(L));
+  *layer_id = (int32_t)ctx->layers.size() - 1;
+  return DATTRI_OK;
+}
+
+dattri_status dattri_num_layers(const dattri_ctx* ctx, int32_t* n) {
+  reset_error();
+  if (!ctx || !n) return fail(DATTRI_E_INVALID_ARG, "ctx or n is NULL");
+  *n = (int32_t)ctx->layers.size();
+  return DATTRI_OK;
+}
+
+dattri_status dattri_layer_dims(const dattri_ctx* ctx, int32_t layer, int32_t* d_in, int32_t* d_out,
+                                int32_t* k_in, int32_t* k_out) {
+  reset_error();
+  dattri_status st = check_layer(ctx, layer);
+  if (st != DATTRI_OK) return st;
+  const Layer& L = ctx->layers[layer];
+  if (d_in) *d_in = L.d_in;
+  if (d_out) *d_out = L.d_out;
+  if (k_in) *k_in = L.k_in;
+  if (k_out) *k_out = L.k_out;
+  return DATTRI_OK;
+}
+
+dattri_status dattri_feature_dim(const dattri_ctx* ctx, int64_t* F) {
+  reset_error();
+  if (!ctx || !F) return fail(DATTRI_E_INVALID_ARG, "ctx or F is NULL");
+  *F = ctx->F;
+  return DATTRI_OK;
+}
+
+dattri_status dattri_layer_offset(const dattri_ctx* ctx, int32_t layer, int64_t* offset) {
+  reset_error();
+  dattri_status st = check_layer(ctx, layer);
+  if (st != DATTRI_OK) return st;
+  if (!offset) return fail(DATTRI_E_INVALID_ARG, "offset is NULL");
+  *offset = ctx->layers[layer].offset;
+  return DATTRI_OK;
+}
+
+dattri_status dattri_projection_bytes(const dattri_ctx* ctx, int32_t layer, size_t* bytes_in,
+                                      size_t* bytes_out) {
+  reset_error();
+  dattri_status st = check_layer(ctx, layer);
+  if (st != DATTRI_OK) return st;
+  const Layer& L = ctx->layers[layer];
+  if (bytes_in) *bytes_in = (size_t)packed_bytes(L.d_in, L.k_in, ctx->elt);
+  if (bytes_out) *bytes_out = (size_t)packed_bytes(L.d_out, L.k_out, ctx->elt);
+  return DATTRI_OK;
+}
+
+dattri_status dattri_bind_projection(dattri_ctx* ctx, int32_t layer, void* dev_P_in, void* dev_P_out,
+                                     const float* host_P_in_override,
+                                     const float* host_P_out_override, void* stream) {
+  reset_error();
+  dattri_status st = check_layer(ctx, layer);
+  if (st != DATTRI_OK) return st;
+  if (!dev_P_in || !dev_P_out) return fail(DATTRI_E_INVALID_ARG, "device map pointer is NULL");
+  if ((uintptr_t)dev_P_in % 16 || (uintptr_t)dev_P_out % 16)
+    return fail(DATTRI_E_INVALID_ARG, "device map pointers must be 16-byte aligned");
+  Layer& L = ctx->layers[layer];
+  for (int side = 0; side < 2; ++side) {
+    const int d = side ? L.d_out : L.d_in, k = side ? L.k_out : L.k_in;
+    const float* ov = side ? host_P_out_override : host_P_in_override;
+    std::vector<float>& keep = side ? L.override_out : L.override_in;
+    keep.clear();
+    if (ov) {
+      keep.resize((size_t)d * k);
+      for (size_t i = 0; i < keep.size(); ++i) keep[i] = round_to_compute((double)ov[i], ctx->elt);
+    }
+  }
+  hipStream_t s = (hipStream_t)stream;
+  for (int side = 0; side < 2; ++side) {
+    const int d = side ? L.d_out : L.d_in, k = side ? L.k_out : L.k_in;
+    std::vector<float> logical;
+    logical_map(ctx, layer, side, logical);
+    std::vector<uint8_t> packed;
+    pack_map(logical.data(), d, k, ctx->elt, packed);
+    HIP_TRY(hipMemcpyAsync(side ? dev_P_out : dev_P_in, packed.data(), packed.size(),
+                           hipMemcpyHostToDevice, s));
+    HIP_TRY(hipStreamSynchronize(s));
+  }
+  L.P_in = dev_P_in;
+  L.P_out = dev_P_out;
+  L.bound = true;
+  return DATTRI_OK;
+}
+
+dattri_status dattri_get_projection(const dattri_ctx* ctx, int32_t layer, float* host_P_in,
+                                    float* host_P_out) {
+  reset_error();
+  dattri_status st = check_layer(ctx, layer);
+  if (st != DATTRI_OK) return st;
+  std::vector<float> v;
+  if (host_P_in) {
+    logical_map(ctx, layer, 0, v);
+    std::memcpy(host_P_in, v.data(), v.size() * 4);
+  }
+  if (host_P_out) {
+    logical_map(ctx, layer, 1, v);
+    std::memcpy(host_P_out, v.data(), v.size() * 4);
+  }
+  return DATTRI_OK;
+}
+
+dattri_status dattri_capture_layer(dattri_ctx* ctx, int32_t layer, const void* A, const void* B,
+                                   int32_t n, int32_t T, const int32_t* dev_lengths) {
+  reset_error();
+  dattri_status st = check_layer(ctx, layer);
+  if (st != DATTRI_OK) return st;
+  if (n < 0 || T < 0) return fail(DATTRI_E_INVALID_ARG, "n=%d and T=%d must be >= 0", n, T);
+  if ((int64_t)n * T > 0 && (!A || !B))
+    return fail(DATTRI_E_INVALID_ARG, "A or B is NULL for a non-empty capture");
+  Layer& L = ctx->layers[layer];
+  if ((int64_t)T * std::max(L.d_in, L.d_out) * ctx->elt >= kMaxBlockBytes)
+    return fail(DATTRI_E_SHAPE, "layer %d: one example's factor block (T*d = %lld elements) exceeds 4 GiB",
+                layer, (long long)T * std::max(L.d_in, L.d_out));
+  L.A = A;
+  L.B = B;
+  L.n = n;
+  L.T = T;
+  L.lengths = dev_lengths;
+  L.captured = true;
+  return DATTRI_OK;
+}
+
+dattri_status dattri_clear_captures(dattri_ctx* ctx) {
+  reset_error();
+  if (!ctx) return fail(DATTRI_E_INVALID_ARG, "ctx is NULL");
+  for (Layer& L : ctx->layers) {
+    L.A = L.B = nullptr;
+    L.lengths = nullptr;
+    L.n = L.T = 0;
+    L.captured = false;
+  }
+  return DATTRI_OK;
+}
+
+dattri_status dattri_workspace_bytes(const dattri_ctx* ctx, dattri_route route, size_t* bytes) {
+  reset_error();
+  if (!ctx || !bytes) return fail(DATTRI_E_INVALID_ARG, "ctx or bytes is NULL");
+  if (route < DATTRI_ROUTE_AUTO || route > DATTRI_ROUTE_MATERIALIZED)
+    return fail(DATTRI_E_INVALID_ARG, "route %d unknown", (int)route);
+  Plan P;
+  dattri_status st = build_plan(ctx, route, P);
+  if (st != DATTRI_OK) return st;
+  *bytes = P.total;
+  return DATTRI_OK;
+}
+
+dattri_status dattri_project_per_example(dattri_ctx* ctx, void* phi, dattri_dtype phi_dtype,
+                                         int64_t ld_phi, void* workspace, size_t ws_bytes,
+                                         dattri_route route, void* stream) {
+  reset_error();
+  if (!ctx) return fail(DATTRI_E_INVALID_ARG, "ctx is NULL");
+  if (phi_dtype != DATTRI_F32 && phi_dtype != DATTRI_BF16)
+    return fail(DATTRI_E_DTYPE, "phi dtype %d is neither F32 nor BF16", (int)phi_dtype);
+  if (route < DATTRI_ROUTE_AUTO || route > DATTRI_ROUTE_MATERIALIZED)
+    return fail(DATTRI_E_INVALID_ARG, "route %d unknown", (int)route);
+  for (size_t l = 0; l < ctx->layers.size(); ++l)
+    if (!ctx->layers[l].bound)
+      return fail(DATTRI_E_STATE, "layer %zu: projection maps not bound", l);
+  Plan P;
+  dattri_status st = build_plan(ctx, route, P);
+  if (st != DATTRI_OK) return st;
+  const int32_t n = ctx->layers[0].n;
+  if (ld_phi < ctx->F) return fail(DATTRI_E_SHAPE, "ld_phi=%lld < F=%lld", (long long)ld_phi, (long long)ctx->F);
+  if (n == 0) return DATTRI_OK;
+  if (!phi) return fail(DATTRI_E_INVALID_ARG, "phi is NULL");
+  if (!workspace) return fail(DATTRI_E_WORKSPACE, "workspace is NULL (needs %zu bytes)", P.total);
+  if ((uintptr_t)workspace % kAlign) return fail(DATTRI_E_WORKSPACE, "workspace must be 256-byte aligned");
+  if (ws_bytes < P.total)
+    return fail(DATTRI_E_WORKSPACE, "workspace has %zu bytes, needs %zu", ws_bytes, P.total);
+
+  // Upload the launch plan into the head of the workspace.
+  ctx->blob.assign(P.blob_bytes, 0);
+  auto put = [&](size_t off, const void* src, size_t bytes) {
+    if (bytes) std::memcpy(ctx->blob.data() + off, src, bytes);
+  };
+  put(P.off_items, P.items.data(), P.items.size() * sizeof(FactItem));
+  put(P.off_groups, P.groups.data(), P.groups.size() * sizeof(FactGroup));
+  put(P.off_members, P.members.data(), P.members.size() * sizeof(FactMember));
+  put(P.off_tasks, P.tasks.data(), P.tasks.size() * sizeof(ReduceTask));
+  hipStream_t s = (hipStream_t)stream;
+  uint8_t* ws = (uint8_t*)workspace;
+  HIP_TRY(hipMemcpyAsync(ws, ctx->blob.data(), P.blob_bytes, hipMemcpyHostToDevice, s));
+
+  const FactItem* d_items = (const FactItem*)(ws + P.off_items);
+  const FactGroup* d_groups = (const FactGroup*)(ws + P.off_groups);
+  const FactMember* d_members = (const FactMember*)(ws + P.off_members);
+  const ReduceTask* d_tasks = (const ReduceTask*)(ws + P.off_tasks);
+  float* fpart = (float*)(ws + P.off_fpart);
+  const int phi_bf16 = phi_dtype == DATTRI_BF16;
+  for (const Plan::Launch& L : P.launches)
+    HIP_TRY(launch_factored(L.elt, L.na, L.nb, d_items + L.first, L.count, d_groups, d_members,
+                            fpart, s));
+  if (P.n_fact_tasks)
+    HIP_TRY(launch_reduce(d_tasks, P.n_fact_tasks, n, fpart, phi, phi_bf16, ld_phi, s));
+
+  float* gbuf = (float*)(ws + P.off_g);
+  float* mpart = (float*)(ws + P.off_mpart);
+  for (const MatChunk& mc : P.mat) {
+    const Layer& L = ctx->layers[mc.layer];
+    GradArgs ga;
+    ga.A = L.A; ga.B = L.B; ga.lengths = L.lengths;
+    ga.d_in = L.d_in; ga.d_out = L.d_out; ga.T = L.T;
+    ga.ex_begin = mc.ex_begin; ga.ex_count = mc.ex_count;
+    ga.aligned = ((uintptr_t)L.A % 16 == 0) && ((uintptr_t)L.B % 16 == 0) &&
+                 (L.d_in * ctx->elt) % 16 == 0 && (L.d_out * ctx->elt) % 16 == 0;
+    ga.G = gbuf;
+    HIP_TRY(launch_gradient(ctx->elt, ga, s));
+    GProjArgs pa;
+    pa.G = gbuf; pa.P_in = L.P_in; pa.P_out = L.P_out;
+    pa.d_in = L.d_in; pa.d_out = L.d_out; pa.k_in = L.k_in; pa.k_out = L.k_out;
+    pa.ex_count = mc.ex_count; pa.n_ublocks = mc.n_ublocks; pa.partials = mpart;
+    HIP_TRY(launch_gproject(ctx->elt, pa, s));
+    HIP_TRY(launch_reduce(d_tasks + mc.task, 1, mc.ex_count, mpart, phi, phi_bf16, ld_phi, s));
+  }
+  return DATTRI_OK;
+}
+
+dattri_status dattri_materialize_gradient(dattri_ctx* ctx, int32_t layer, int32_t ex_begin,
+                                          int32_t ex_count, float* G_out, void* stream) {
+  reset_error();
+  dattri_status st = check_layer(ctx, layer);
+  if (st != DATTRI_OK) return st;
+  const Layer& L = ctx->layers[layer];
+  if (!L.captured) return fail(DATTRI_E_STATE, "layer %d has no capture", layer);
+  if (ex_begin < 0 || ex_count < 0 || (int64_t)ex_begin + ex_count > L.n)
+    return fail(DATTRI_E_INVALID_ARG, "examples [%d, %d+%d) outside [0, %d)", ex_begin, ex_begin,
+                ex_count, L.n);
+  if (ex_count == 0) return DATTRI_OK;
+  if (!G_out) return fail(DATTRI_E_INVALID_ARG, "G_out is NULL");
+  GradArgs ga;
+  ga.A = L.A; ga.B = L.B; ga.lengths = L.lengths;
+  ga.d_in = L.d_in; ga.d_out = L.d_out; ga.T = L.T;
+  ga.ex_begin = ex_begin; ga.ex_count = ex_count;
+  ga.aligned = ((uintptr_t)L.A % 16 == 0) && ((uintptr_t)L.B % 16 == 0) &&
+               (L.d_in * ctx->elt) % 16 == 0 && (L.d_out * ctx->elt) % 16 == 0;
+  ga.G = G_out;
+  HIP_TRY(launch_gradient(ctx->elt, ga, (hipStream_t)stream));
+  return DATTRI_OK;
+}
+
+dattri_status dattri_set_cost_model(dattri_ctx* ctx, const dattri_cost_model* m) {
+  reset_error();
+  if (!ctx || !m) return fail(DATTRI_E_INVALID_ARG, "ctx or model is NULL");
+  const double r[6] = {m->factored_tflops, m->factored_gbs, m->gradient_tflops,
+                       m->gradient_gbs, m->gproject_tflops, m->gproject_gbs};
+  for (double x : r)
+    if (!(x > 0.0) || !std::isfinite(x)) return fail(DATTRI_E_INVALID_ARG, "rates must be finite and > 0");
+  if (!(m->launch_us >= 0.0) || !std::isfinite(m->launch_us))
+    return fail(DATTRI_E_INVALID_ARG, "launch_us must be finite and >= 0");
+  ctx->cost = *m;
+  return DATTRI_OK;
+}
+
+dattri_status dattri_get_cost_model(const dattri_ctx* ctx, dattri_cost_model* m) {
+  reset_error();
+  if (!ctx || !m) return fail(DATTRI_E_INVALID_ARG, "ctx or model is NULL");
+  *m = ctx->cost;
+  return DATTRI_OK;
+}
+
+dattri_status dattri_layer_costs(const dattri_ctx* ctx, int32_t layer, int32_t T,
+                                 int64_t* factored_flops, int64_t* materialized_flops,
+                                 int64_t* factored_bytes, int64_t* materialized_bytes) {
+  reset_error();
+  dattri_status st = check_layer(ctx, layer);
+  if (st != DATTRI_OK) return st;
+  if (T < 0) return fail(DATTRI_E_INVALID_ARG, "T=%d < 0", T);
+  const Counts c = layer_counts(ctx->layers[layer], T, ctx->elt);
+  if (factored_flops) *factored_flops = c.f_flops;
+  if (materialized_flops) *materialized_flops = c.m_flops;
+  if (factored_bytes) *factored_bytes = c.f_bytes;
+  if (materialized_bytes) *materialized_bytes = c.m_bytes;
+  return DATTRI_OK;
+}
+
+dattri_status dattri_layer_route(const dattri_ctx* ctx, int32_t layer, dattri_route* chosen,
+                                 double* pred_factored_us, double* pred_materialized_us) {
+  reset_error();
+  dattri_status st = check_layer(ctx, layer);
+  if (st != DATTRI_OK) return st;
+  const Layer& L = ctx->layers[layer];
+  if (!L.captured) return fail(DATTRI_E_STATE, "layer %d has no capture", layer);
+  double f, m;
+  predict(ctx->cost, L, L.n, L.T, ctx->elt, &f, &m);
+  if (chosen) *chosen = choose_route(ctx, L, DATTRI_ROUTE_AUTO);
+  if (pred_factored_us) *pred_factored_us = factored_supported(L) ? f : INFINITY;
+  if (pred_materialized_us) *pred_materialized_us = m;
+  return DATTRI_OK;
+}
+
+// ------------------------------------------------------------------ scoring
+namespace {
+struct ScoreLayout { size_t off_q, q_bytes, off_s, s_bytes, total; };
+
+ScoreLayout score_layout(int64_t n_q, int64_t n_train, int64_t F, int elt, bool precond,
+                         bool has_scores, int32_t topk) {
+  ScoreLayout L;
+  size_t off = 0;
+  L.off_q = off;
+  L.q_bytes = precond ? (size_t)(n_q * F * elt) : 0;
+  off = align_up(off + L.q_bytes);
+  L.off_s = off;
+  L.s_bytes = (!has_scores && topk > 0) ? (size_t)(n_q * n_train * 4) : 0;
+  off = align_up(off + L.s_bytes);
+  L.total = std::max<size_t>(off, kAlign);
+  return L;
+}
+}  // namespace
+
+dattri_status dattri_score_workspace_bytes(int64_t n_q, int64_t n_train, int64_t F,
+                                           dattri_dtype dtype, int32_t has_precond,
+                                           int32_t has_scores, int32_t topk, size_t* bytes) {
+  reset_error();
+  if (!bytes) return fail(DATTRI_E_INVALID_ARG, "bytes is NULL");
+  if (n_q < 0 || n_train < 0 || F < 0 || topk < 0)
+    return fail(DATTRI_E_INVALID_ARG, "sizes must be >= 0");
+  if (dtype != DATTRI_F32 && dtype != DATTRI_BF16)
+    return fail(DATTRI_E_DTYPE, "dtype %d is neither F32 nor BF16", (int)dtype);
+  *bytes = score_layout(n_q, n_train, F, dtype == DATTRI_BF16 ? 2 : 4, has_precond != 0,
+                        has_scores != 0, topk).total;
+  return DATTRI_OK;
+}
+
+dattri_status dattri_score(const void* phi_q, int64_t n_q, const void* phi_train, int64_t n_train,
+                           int64_t F, dattri_dtype dtype, const float* dev_precond_diag,
+                           float* scores, int32_t topk, int32_t* topk_idx, float* topk_val,
+                           void* workspace, size_t ws_bytes, void* stream) {
+  reset_error();
+  if (dtype != DATTRI_F32 && dtype != DATTRI_BF16)
+    return fail(DATTRI_E_DTYPE, "dtype %d is neither F32 nor BF16", (int)dtype);
+  if (n_q < 0 || n_train < 0 || F < 0 || topk < 0)
+    return fail(DATTRI_E_INVALID_ARG, "sizes must be >= 0");
+  if (n_q > INT32_MAX || n_train > INT32_MAX || F > INT32_MAX)
+    return fail(DATTRI_E_UNSUPPORTED, "n_q, n_train and F must each fit in int32");
+  if (topk > kTopkMax) return fail(DATTRI_E_UNSUPPORTED, "topk=%d exceeds %d", topk, kTopkMax);
+  if (topk > n_train) return fail(DATTRI_E_INVALID_ARG, "topk=%d exceeds n_train=%lld", topk, (long long)n_train);
+  if (!scores && topk == 0) return fail(DATTRI_E_INVALID_ARG, "nothing to compute: scores is NULL and topk is 0");
+  if (topk > 0 && (!topk_idx || !topk_val))
+    return fail(DATTRI_E_INVALID_ARG, "topk_idx and topk_val are required when topk > 0");
+  if (n_q == 0 || n_train == 0) return DATTRI_OK;
+  if (F > 0 && (!phi_q || !phi_train)) return fail(DATTRI_E_INVALID_ARG, "phi_q or phi_train is NULL");
+  const int elt = dtype == DATTRI_BF16 ? 2 : 4;
+  if ((uintptr_t)phi_q % 16 || (uintptr_t)phi_train % 16 || (F * elt) % 16)
+    return fail(DATTRI_E_UNSUPPORTED,
+                "phi rows must be 16-byte aligned (pointers and F*%d a multiple of 16)", elt);
+  const ScoreLayout L = score_layout(n_q, n_train, F, elt, dev_precond_diag != nullptr,
+                                     scores != nullptr, topk);
+  if (L.q_bytes + L.s_bytes > 0) {
+    if (!workspace) return fail(DATTRI_E_WORKSPACE, "workspace is NULL (needs %zu bytes)", L.total);
+    if ((uintptr_t)workspace % kAlign) return fail(DATTRI_E_WORKSPACE, "workspace must be 256-byte aligned");
+    if (ws_bytes < L.total)
+      return fail(DATTRI_E_WORKSPACE, "workspace has %zu bytes, needs %zu", ws_bytes, L.total);
+  }
+  hipStream_t s = (hipStream_t)stream;
+  uint8_t* ws = (uint8_t*)workspace;
+  const void* q = phi_q;
+  if (dev_precond_diag && F > 0) {
+    HIP_TRY(launch_scale_rows(elt, phi_q, dev_precond_diag, ws + L.off_q, n_q, F, s));
+    q = ws + L.off_q;
+  }
+  float* S = scores ? scores : (float*)(ws + L.off_s);
+  HIP_TRY(launch_score_gemm(elt, q, phi_train, S, n_q, n_train, F, s));
+  if (topk > 0) HIP_TRY(launch_topk(S, n_q, n_train, topk, topk_idx, topk_val, s));
+  return DATTRI_OK;
+}
+
+}  // extern "C"

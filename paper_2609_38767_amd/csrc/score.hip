@@ -1,0 +1,159 @@
+// Scoring: S = (Phi_q diag(d)) Phi_train^T  (GradDot, Sec. 4.1, with an
+// optional positive diagonal preconditioner applied once), float32 out.
+//
+// Both operands are row-major with the feature axis contiguous, which is the
+// K-contiguous ("NT") form MFMA wants for both sides: a lane's 16-byte fragment
+// is a contiguous slice of one row.  Workgroup tile 128 x 128, 4 waves in a
+// 2 x 2 grid of 64 x 64 (4 x 4 MFMA tiles each), 128 bytes of K per stage,
+// double-buffered in LDS with the next stage prefetched into registers while
+// the current one is multiplied.  LDS rows are XOR-swizzled by 16-byte chunk.
+// Tiles are remapped so that each XCD walks a contiguous range of training
+// tiles, all query tiles of one training tile back to back, so a Phi_train
+// tile is fetched into that XCD's L2 once and reused by every query tile.
+#include "device_common.h"
+#include "internal.h"
+
+namespace dattri {
+using namespace dev;
+
+template <int ELT>
+__global__ __launch_bounds__(256) void scale_rows_kernel(const uint8_t* __restrict__ src,
+                                                         const float* __restrict__ d,
+                                                         uint8_t* __restrict__ dst, int64_t rows,
+                                                         int64_t F) {
+  const int64_t n = rows * F;
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n;
+       i += (int64_t)gridDim.x * blockDim.x) {
+    const int64_t f = i % F;
+    if constexpr (ELT == 2) {
+      const float x = bf16_bits_to_f32(((const uint16_t*)src)[i]) * d[f];
+      ((uint16_t*)dst)[i] = f32_to_bf16_bits(x);
+    } else {
+      ((float*)dst)[i] = ((const float*)src)[i] * d[f];
+    }
+  }
+}
+
+constexpr int kBM = 128, kBN = 128, kRowBytes = 128;  // tile rows, K bytes per stage
+
+template <int ELT>
+__global__ __launch_bounds__(256) void score_gemm_kernel(const uint8_t* __restrict__ Q,
+                                                         const uint8_t* __restrict__ X,
+                                                         float* __restrict__ S, int n_q,
+                                                         int n_train, int F, int n_qt, int n_xt) {
+  constexpr int EPL = 16 / ELT;
+  constexpr int BK = kRowBytes / ELT;  // K elements per stage
+  __shared__ __align__(16) uint8_t smem[2][2][kBM * kRowBytes];  // [stage][Q/X] 64 KiB
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int g = lane >> 4, m16 = lane & 15, wm = wave >> 1, wn = wave & 1;
+
+  // XCD-aware tile order (dispatch round-robins workgroups over 8 XCDs)
+  const int nb = n_qt * n_xt, b = blockIdx.x;
+  const int n_full = nb / 8 * 8;
+  const int L = b < n_full ? (b % 8) * (n_full / 8) + b / 8 : b;
+  const int qt = L % n_qt, xt = L / n_qt;
+  const int q0 = qt * kBM, x0 = xt * kBN;
+  const int rows_q = min(kBM, n_q - q0), rows_x = min(kBN, n_train - x0);
+  const rsrc_t rq = make_rsrc(Q + (int64_t)q0 * F * ELT, (uint32_t)((int64_t)rows_q * F * ELT));
+  const rsrc_t rx = make_rsrc(X + (int64_t)x0 * F * ELT, (uint32_t)((int64_t)rows_x * F * ELT));
+
+  f32x4 acc[4][4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int j = 0; j < 4; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+  const int nk = (F + BK - 1) / BK;
+  i32x4 rqv[4], rxv[4];
+  auto gload = [&](int kk) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int c = tid + 256 * i, row = c >> 3, ch = c & 7;
+      const int col = kk * BK + ch * EPL;
+      rqv[i] = load_frag<ELT>(rq, row, rows_q, col, F, true);
+      rxv[i] = load_frag<ELT>(rx, row, rows_x, col, F, true);
+    }
+  };
+  auto swrite = [&](int st) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int c = tid + 256 * i, row = c >> 3, ch = c & 7;
+      const int off = row * kRowBytes + ((ch ^ (row & 7)) << 4);
+      *(i32x4*)(smem[st][0] + off) = rqv[i];
+      *(i32x4*)(smem[st][1] + off) = rxv[i];
+    }
+  };
+
+  if (nk > 0) {
+    gload(0);
+    swrite(0);
+  }
+  __syncthreads();
+  for (int kk = 0; kk < nk; ++kk) {
+    const int st = kk & 1;
+    if (kk + 1 < nk) gload(kk + 1);
+#pragma unroll
+    for (int s = 0; s < 2; ++s) {
+      i32x4 af[4], bf[4];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int row = wm * 64 + i * 16 + m16, ch = s * 4 + g;
+        af[i] = *(const i32x4*)(smem[st][0] + row * kRowBytes + ((ch ^ (row & 7)) << 4));
+      }
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const int row = wn * 64 + j * 16 + m16, ch = s * 4 + g;
+        bf[j] = *(const i32x4*)(smem[st][1] + row * kRowBytes + ((ch ^ (row & 7)) << 4));
+      }
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) acc[i][j] = frag_mma<ELT>(af[i], bf[j], acc[i][j]);
+    }
+    if (kk + 1 < nk) swrite(st ^ 1);
+    __syncthreads();
+  }
+
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int x = x0 + wn * 64 + j * 16 + m16;
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int q = q0 + wm * 64 + i * 16 + 4 * g + r;
+        if (q < n_q && x < n_train) S[(int64_t)q * n_train + x] = acc[i][j][r];
+      }
+    }
+}
+
+hipError_t launch_scale_rows(int elt, const void* src, const float* d, void* dst, int64_t rows,
+                             int64_t F, hipStream_t s) {
+  const int64_t n = rows * F;
+  if (n <= 0) return hipSuccess;
+  const int blocks = (int)std::min<int64_t>((n + 255) / 256, 65536);
+  if (elt == 2)
+    hipLaunchKernelGGL(scale_rows_kernel<2>, dim3(blocks), dim3(256), 0, s, (const uint8_t*)src, d,
+                       (uint8_t*)dst, rows, F);
+  else
+    hipLaunchKernelGGL(scale_rows_kernel<4>, dim3(blocks), dim3(256), 0, s, (const uint8_t*)src, d,
+                       (uint8_t*)dst, rows, F);
+  return hipGetLastError();
+}
+
+hipError_t launch_score_gemm(int elt, const void* Q, const void* X, float* S, int64_t n_q,
+                             int64_t n_train, int64_t F, hipStream_t s) {
+  if (n_q <= 0 || n_train <= 0) return hipSuccess;
+  const int n_qt = (int)((n_q + kBM - 1) / kBM), n_xt = (int)((n_train + kBN - 1) / kBN);
+  const int64_t nb = (int64_t)n_qt * n_xt;
+  if (nb > INT32_MAX) return hipErrorInvalidValue;
+  if (elt == 2)
+    hipLaunchKernelGGL(score_gemm_kernel<2>, dim3((unsigned)nb), dim3(256), 0, s, (const uint8_t*)Q,
+                       (const uint8_t*)X, S, (int)n_q, (int)n_train, (int)F, n_qt, n_xt);
+  else
+    hipLaunchKernelGGL(score_gemm_kernel<4>, dim3((unsigned)nb), dim3(256), 0, s, (const uint8_t*)Q,
+                       (const uint8_t*)X, S, (int)n_q, (int)n_train, (int)F, n_qt, n_xt);
+  return hipGetLastError();
+}
+
+}  // namespace dattri

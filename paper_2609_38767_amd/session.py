@@ -1,0 +1,102 @@
+"""Convenience wrappers over the C ABI that let torch own the device buffers.
+
+``ProjectionSession`` registers layers, allocates and binds the projection
+maps, captures factor blocks, sizes the workspace and calls
+``dattri_project_per_example``; ``score`` sizes the scoring workspace and calls
+``dattri_score``.  All computation happens in libdattri's HIP kernels.
+"""
+import torch
+
+from . import (DATTRI_BF16, DATTRI_F32, DATTRI_ROUTE_AUTO, dattri_bind_projection,
+               dattri_capture_layer, dattri_clear_captures, dattri_create, dattri_destroy,
+               dattri_feature_dim, dattri_layer_offset, dattri_layer_route,
+               dattri_project_per_example, dattri_projection_bytes, dattri_register_layer,
+               dattri_score, dattri_score_workspace_bytes, dattri_workspace_bytes)
+
+DTYPES = {"f32": (DATTRI_F32, torch.float32), "bf16": (DATTRI_BF16, torch.bfloat16)}
+
+
+def _dev_bytes(n, device):
+    return torch.empty(max(int(n), 256), dtype=torch.uint8, device=device)
+
+
+class ProjectionSession:
+    """One library context with its layers and bound projection maps."""
+
+    def __init__(self, layers, dtype="bf16", seed=0, device="cuda", overrides=None):
+        self.dtype = dtype
+        self.code, self.torch_dtype = DTYPES[dtype]
+        self.device = torch.device(device)
+        self.ctx = dattri_create(self.code, seed)
+        self.layers = list(layers)
+        self.maps = []
+        overrides = overrides or {}
+        for i, L in enumerate(self.layers):
+            lid = dattri_register_layer(self.ctx, L["d_in"], L["d_out"], L["k_in"], L["k_out"])
+            assert lid == i
+            b_in, b_out = dattri_projection_bytes(self.ctx, lid)
+            p_in, p_out = _dev_bytes(b_in, self.device), _dev_bytes(b_out, self.device)
+            o_in, o_out = overrides.get(i, (None, None))
+            dattri_bind_projection(self.ctx, lid, p_in, p_out, o_in, o_out)
+            self.maps.append((p_in, p_out))
+        self.F = dattri_feature_dim(self.ctx)
+        self.offsets = [dattri_layer_offset(self.ctx, i) for i in range(len(self.layers))]
+        self._ws = None
+        self._held = []
+
+    def capture(self, layer, A, B, lengths=None):
+        """A [n, T, d_in], B [n, T, d_out] contiguous device tensors of the compute dtype."""
+        assert A.is_contiguous() and B.is_contiguous()
+        assert A.dtype == self.torch_dtype and B.dtype == self.torch_dtype
+        n, T = A.shape[0], A.shape[1]
+        dattri_capture_layer(self.ctx, layer, A, B, n, T, lengths)
+        self._held.append((A, B, lengths))
+
+    def clear(self):
+        dattri_clear_captures(self.ctx)
+        self._held = []
+
+    def workspace(self, route=DATTRI_ROUTE_AUTO):
+        need = dattri_workspace_bytes(self.ctx, route)
+        if self._ws is None or self._ws.numel() < need:
+            self._ws = None
+            self._ws = _dev_bytes(need, self.device)
+        return self._ws
+
+    def project(self, n, route=DATTRI_ROUTE_AUTO, phi_dtype="f32", phi=None, stream=None):
+        code, tdt = DTYPES[phi_dtype]
+        if phi is None:
+            phi = torch.empty((n, self.F), dtype=tdt, device=self.device)
+        ws = self.workspace(route)
+        dattri_project_per_example(self.ctx, phi, code, phi.stride(0), ws, ws.numel(), route, stream)
+        return phi
+
+    def routes(self):
+        return [dattri_layer_route(self.ctx, i) for i in range(len(self.layers))]
+
+    def close(self):
+        if self.ctx:
+            dattri_destroy(self.ctx)
+            self.ctx = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+
+def score(phi_q, phi_train, precond=None, topk=0, want_scores=True, stream=None):
+    """(S or None, topk_idx or None, topk_val or None) for bf16/f32 feature rows."""
+    code = DATTRI_BF16 if phi_q.dtype == torch.bfloat16 else DATTRI_F32
+    n_q, F = phi_q.shape
+    n_train = phi_train.shape[0]
+    dev = phi_q.device
+    S = torch.empty((n_q, n_train), dtype=torch.float32, device=dev) if want_scores else None
+    idx = torch.empty((n_q, topk), dtype=torch.int32, device=dev) if topk else None
+    val = torch.empty((n_q, topk), dtype=torch.float32, device=dev) if topk else None
+    need = dattri_score_workspace_bytes(n_q, n_train, F, code, precond is not None, want_scores, topk)
+    ws = _dev_bytes(need, dev)
+    dattri_score(phi_q, n_q, phi_train, n_train, F, code, precond, S, topk, idx, val, ws, ws.numel(),
+                 stream)
+    return S, idx, val

@@ -2,36 +2,137 @@
 //   Psi = (A P_in)^T (B P_out),   Psi[c][r] = sum_t a~_t[c] g~_t[r],
 // fused in one kernel over a work list of (input group, example, token chunk).
 //
-// A workgroup of 4 waves streams its token chunk of A once (shared by all
-// layers of the group, e.g. q/k/v) and of each member's B once, straight from
-// HBM into MFMA operand registers (16-byte buffer loads; ragged rows and
-// feature tails read as zero).  Projection fragments come from L2 in the
-// fragment-major layout (one coalesced 1 KiB load per wave).  The projected
-// tiles A~ = A P_in and B~ = B P_out stay in accumulator registers, and the
-// token contraction A~^T B~ is done from those registers with float32 MFMA
-// (16x16x4): for the 16x16 C layout, lane (g, n) holds rows 4g..4g+3 of column
-// n, which is exactly a K=4 operand slice per element index, for both factors.
-// Each wave writes its float32 partial block; a second kernel sums partials
-// in a fixed order (deterministic, no float atomics) and writes phi.
+// A workgroup of 4 waves owns a chunk of token rows of one example and one
+// input group (layers sharing A, e.g. q/k/v).  For each sub-chunk of
+// 4 x RT x 16 rows it streams A once and each member's B once from HBM,
+// straight into MFMA operand registers: 16-byte buffer loads, prefetched PD
+// k-blocks ahead in a register ring (ragged rows and feature tails read as
+// zero through the descriptor range).  Projection fragments are staged once
+// per workgroup in LDS, one panel of KP k-blocks at a time (loaded a panel
+// ahead, one barrier per panel), and shared by the 4 waves.
+//
+// The projected tiles A~ = A P_in and B~ = B P_out stay in accumulators, and
+// the token contraction A~^T B~ is done from those registers with float32 MFMA
+// (16x16x4): in the 16x16 C layout lane (g, n) holds rows 4g..4g+3 of column n,
+// which for each element index is a K=4 operand slice, identically for both
+// factors.  Each wave writes its float32 partial block; a second kernel sums
+// partials in a fixed order (deterministic, no float atomics) and writes phi.
 #include "device_common.h"
 #include "internal.h"
 
 namespace dattri {
 using namespace dev;
 
-template <int ELT, int RT, int NA, int NB>
-__global__ __launch_bounds__(256) void factored_kernel(const FactItem* __restrict__ items,
-                                                       const FactGroup* __restrict__ groups,
-                                                       const FactMember* __restrict__ members,
-                                                       float* __restrict__ partials) {
-  constexpr int EPL = 16 / ELT;
-  constexpr int KR = 4 * EPL;  // feature rows covered by one fragment
+constexpr int kPanel = 4;  // k-blocks per LDS panel of projection fragments
+
+// k-blocks of factor fragments prefetched ahead: about 8 KiB in flight per
+// wave where the register budget of two waves per SIMD allows it, else 4 KiB.
+constexpr int pd_of(int rt, int na, int nb) { return (rt >= 4 || na * (rt + nb) >= 24) ? 2 : 4; }
+
+// Projection fragment source of up to NT output tiles: fragment (kb, t) of the
+// packed map lives at base[t] + kb * stride[t] (bytes).
+template <int NT>
+struct FragSrc {
+  const uint8_t* base[NT];
+  int64_t stride[NT];
+  int nt;  // tiles in use
+};
+
+// acc[rt][t] += X[rows, :] * P[:, tile t] over all k-blocks of a d-wide row
+// block.  X rows r_wave + rt*16 + (lane & 15) of descriptor `r` (rows >= nrows
+// and columns >= d read as zero).  All 256 threads must call this together.
+template <int ELT, bool AL, int RT, int NT, int NTL, int kPD>
+__device__ inline void project_rows(const rsrc_t r, int r_wave, int nrows, int d,
+                                    const FragSrc<NT>& P, f32x4 (&acc)[RT][NT],
+                                    uint8_t (*pan)[kPanel][NTL][kFragBytes]) {
+  constexpr int EPL = 16 / ELT, KR = 4 * EPL;
+  static_assert(kPanel % kPD == 0, "ring slots must be static inside a panel");
+  // A panel holds kPanel * NT fragments of 1 KiB; fragment f = w + 4*i is
+  // copied by wave w (one 16-byte load per lane), so every index is static.
+  constexpr int NF = kPanel * NT;
+  constexpr int CPT = (NF + kWaves - 1) / kWaves;  // fragments per wave
+  static_assert(NT <= NTL, "panel too small");
+  const int tid = threadIdx.x, lane = tid & 63, g = lane >> 4, m16 = lane & 15;
+  const int wave = tid >> 6;
+  const int nkb = (d + KR - 1) / KR;
+  const int npan = (nkb + kPanel - 1) / kPanel;
+
+  auto load_panel = [&](int p, i32x4 (&st)[CPT]) {
+#pragma unroll
+    for (int i = 0; i < CPT; ++i)
+#pragma unroll
+      for (int w = 0; w < kWaves; ++w) {
+        const int f = w + kWaves * i, t = f % NT, kbl = f / NT;
+        if (f < NF && wave == w) {
+          const int kb = min(p * kPanel + kbl, nkb - 1);
+          st[i] = (t < P.nt) ? *(const i32x4*)(P.base[t] + kb * P.stride[t] + lane * 16)
+                             : i32x4{0, 0, 0, 0};
+        }
+      }
+  };
+  auto store_panel = [&](int buf, const i32x4 (&st)[CPT]) {
+#pragma unroll
+    for (int i = 0; i < CPT; ++i)
+#pragma unroll
+      for (int w = 0; w < kWaves; ++w) {
+        const int f = w + kWaves * i, t = f % NT, kbl = f / NT;
+        if (f < NF && wave == w) *(i32x4*)(&pan[buf][kbl][t][lane * 16]) = st[i];
+      }
+  };
+  auto load_x = [&](int kb, i32x4 (&x)[RT]) {
+    const int col = kb * KR + g * EPL;
+#pragma unroll
+    for (int rt = 0; rt < RT; ++rt) x[rt] = load_frag<ELT>(r, r_wave + rt * 16 + m16, nrows, col, d, AL);
+  };
+
+  i32x4 stage[CPT];
+  i32x4 ring[kPD][RT];
+  load_panel(0, stage);
+#pragma unroll
+  for (int s = 0; s < kPD; ++s) load_x(s, ring[s]);
+  store_panel(0, stage);
+  __syncthreads();
+  for (int p = 0; p < npan; ++p) {
+    const int buf = p & 1;
+    if (p + 1 < npan) load_panel(p + 1, stage);
+#pragma unroll
+    for (int kbl = 0; kbl < kPanel; ++kbl) {
+      const int kb = p * kPanel + kbl;
+      if (kb < nkb) {
+        i32x4 x[RT];
+#pragma unroll
+        for (int rt = 0; rt < RT; ++rt) x[rt] = ring[kbl % kPD][rt];
+        load_x(kb + kPD, ring[kbl % kPD]);
+#pragma unroll
+        for (int t = 0; t < NT; ++t) {
+          if (t < P.nt) {
+            const i32x4 pf = *(const i32x4*)(&pan[buf][kbl][t][lane * 16]);
+#pragma unroll
+            for (int rt = 0; rt < RT; ++rt) acc[rt][t] = frag_mma<ELT>(x[rt], pf, acc[rt][t]);
+          }
+        }
+      }
+    }
+    if (p + 1 < npan) store_panel(buf ^ 1, stage);
+    __syncthreads();
+  }
+}
+
+template <int ELT, bool AL, int RT, int NA, int NB>
+__global__ __launch_bounds__(256, (AL && NA * NB <= 12) ? 2 : 1) void factored_kernel(const FactItem* __restrict__ items,
+                                                          const FactGroup* __restrict__ groups,
+                                                          const FactMember* __restrict__ members,
+                                                          float* __restrict__ partials) {
+  constexpr int NTL = NA > NB ? NA : NB;
+  constexpr int PD = AL ? pd_of(RT, NA, NB) : 2;
+  __shared__ __align__(16) uint8_t pan[2][kPanel][NTL][kFragBytes];
   const FactItem it = items[blockIdx.x];
+  if (it.example < 0) return;  // padding item of the XCD-interleaved order
   const FactGroup& G = groups[it.group];
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int g = lane >> 4, m16 = lane & 15;
   const int ex = it.example;
-  const int T = G.T, d_in = G.d_in, na = G.na;
+  const int T = G.T, d_in = G.d_in;
   int t_eff = T;
   if (G.lengths) t_eff = min(max(G.lengths[ex], 0), T);
   const int row_begin = it.chunk * G.chunk_rows;
@@ -46,60 +147,44 @@ __global__ __launch_bounds__(256) void factored_kernel(const FactItem* __restric
 
   const uint8_t* a_base = (const uint8_t*)G.A + (size_t)ex * T * d_in * ELT;
   const rsrc_t ra = make_rsrc(a_base, (uint32_t)((int64_t)rows_valid * d_in * ELT));
-  const bool a_aligned = G.aligned != 0;
-  const int nkb_a = (d_in + KR - 1) / KR;
+  FragSrc<NA> pin;
+  pin.nt = G.na;
+#pragma unroll
+  for (int t = 0; t < NA; ++t) {
+    const int tt = t < G.na ? t : 0;
+    pin.base[t] = (const uint8_t*)G.ptile[tt] + (int64_t)G.ptile_local[tt] * kFragBytes;
+    pin.stride[t] = (int64_t)G.ptile_nt[tt] * kFragBytes;
+  }
 
-  for (int r0 = row_begin + wave * RT * 16; r0 < row_end; r0 += kWaves * RT * 16) {
-    // ---- A~ = A[rows] P_in(group), all member input tiles at once
+  // sub-chunks: a uniform trip count for all waves (barriers inside)
+  for (int sub = row_begin; sub < row_end; sub += kWaves * RT * 16) {
+    const int r_wave = sub + wave * RT * 16;
     f32x4 acc_a[RT][NA];
 #pragma unroll
     for (int rt = 0; rt < RT; ++rt)
 #pragma unroll
       for (int t = 0; t < NA; ++t) acc_a[rt][t] = f32x4{0.f, 0.f, 0.f, 0.f};
-    for (int kb = 0; kb < nkb_a; ++kb) {
-      const int col = kb * KR + g * EPL;
-      i32x4 af[RT];
-#pragma unroll
-      for (int rt = 0; rt < RT; ++rt) af[rt] = load_frag<ELT>(ra, r0 + rt * 16 + m16, rows_valid, col, d_in, a_aligned);
-#pragma unroll
-      for (int t = 0; t < NA; ++t) {
-        if (t < na) {
-          const uint8_t* pb = (const uint8_t*)G.ptile[t];
-          const int64_t off = (((int64_t)kb * G.ptile_nt[t] + G.ptile_local[t]) * 64 + lane) * 16;
-          const i32x4 pf = *(const i32x4*)(pb + off);
-#pragma unroll
-          for (int rt = 0; rt < RT; ++rt) acc_a[rt][t] = frag_mma<ELT>(af[rt], pf, acc_a[rt][t]);
-        }
-      }
-    }
-    // ---- each member: B~ = B[rows] P_out, then psi += A~^T B~ over these rows
+    project_rows<ELT, AL, RT, NA, NTL, PD>(ra, r_wave, rows_valid, d_in, pin, acc_a, pan);
+
     for (int mi = 0; mi < G.n_members; ++mi) {
       const FactMember& M = members[G.member0 + mi];
       const int d_out = M.d_out, nb = M.nb;
       const uint8_t* b_base = (const uint8_t*)M.B + (size_t)ex * T * d_out * ELT;
       const rsrc_t rb = make_rsrc(b_base, (uint32_t)((int64_t)rows_valid * d_out * ELT));
-      const bool b_aligned = M.aligned != 0;
-      const uint8_t* pout = (const uint8_t*)M.P_out;
+      FragSrc<NB> pout;
+      pout.nt = nb;
+#pragma unroll
+      for (int t = 0; t < NB; ++t) {
+        pout.base[t] = (const uint8_t*)M.P_out + (int64_t)(t < nb ? t : 0) * kFragBytes;
+        pout.stride[t] = (int64_t)nb * kFragBytes;
+      }
       f32x4 acc_b[RT][NB];
 #pragma unroll
       for (int rt = 0; rt < RT; ++rt)
 #pragma unroll
         for (int t = 0; t < NB; ++t) acc_b[rt][t] = f32x4{0.f, 0.f, 0.f, 0.f};
-      const int nkb_b = (d_out + KR - 1) / KR;
-      for (int kb = 0; kb < nkb_b; ++kb) {
-        const int col = kb * KR + g * EPL;
-        i32x4 bf[RT];
-#pragma unroll
-        for (int rt = 0; rt < RT; ++rt) bf[rt] = load_frag<ELT>(rb, r0 + rt * 16 + m16, rows_valid, col, d_out, b_aligned);
-#pragma unroll
-        for (int t = 0; t < NB; ++t) {
-          if (t < nb) {
-            const i32x4 pf = *(const i32x4*)(pout + (((int64_t)kb * nb + t) * 64 + lane) * 16);
-#pragma unroll
-            for (int rt = 0; rt < RT; ++rt) acc_b[rt][t] = frag_mma<ELT>(bf[rt], pf, acc_b[rt][t]);
-          }
-        }
-      }
+      project_rows<ELT, AL, RT, NB, NTL, PD>(rb, r_wave, rows_valid, d_out, pout, acc_b, pan);
+
       const int a0 = M.a_tile0, a1 = M.a_tile0 + M.na;
 #pragma unroll
       for (int ta = 0; ta < NA; ++ta) {
@@ -167,46 +252,54 @@ __global__ __launch_bounds__(256) void reduce_kernel(const ReduceTask* __restric
 }
 
 // ------------------------------------------------------------ instances
-// (NA, NB) instances compiled per element type; rows per wave (RT) shrinks as
-// the accumulator footprint grows so that two waves fit per SIMD.
-static int rt_for(int na, int nb) {
-  if (na <= 2 && nb <= 2) return 4;
-  if (na * nb <= 12) return 2;
-  return 1;
-}
+// Aligned instances per (input tiles NA, output tiles NB); one unaligned
+// instance (8, 4) serves any group whose rows are not 16-byte multiples.
+// Rows per wave RT keeps two waves per SIMD within the register file.
+constexpr int rt_of(int na, int nb) { return (na <= 2 && nb <= 2) ? 4 : (na * nb <= 12 ? 2 : 1); }
 
-void factored_instance(int elt, int na_req, int nb_req, int* na_inst, int* nb_inst, int* rows_per_wave) {
+void factored_instance(int elt, int na_req, int nb_req, int aligned, int* na_inst, int* nb_inst,
+                       int* rows_per_wave) {
   (void)elt;
-  const int na_list[] = {1, 2, 4, 6, 8};
-  const int nb_list[] = {1, 2, 4};
   int na = 8, nb = 4;
-  for (int v : na_list) if (v >= na_req) { na = v; break; }
-  for (int v : nb_list) if (v >= nb_req) { nb = v; break; }
+  if (aligned) {
+    const int na_list[] = {1, 2, 4, 6, 8};
+    const int nb_list[] = {1, 2, 4};
+    for (int v : na_list) if (v >= na_req) { na = v; break; }
+    for (int v : nb_list) if (v >= nb_req) { nb = v; break; }
+  }
   *na_inst = na;
   *nb_inst = nb;
-  *rows_per_wave = rt_for(na, nb);
+  *rows_per_wave = rt_of(na, nb);
 }
 
-template <int ELT, int NA, int NB>
+template <int ELT, bool AL, int NA, int NB>
 static hipError_t launch_one(const FactItem* items, int n, const FactGroup* g, const FactMember* m,
                              float* part, hipStream_t s) {
-  constexpr int RT = (NA <= 2 && NB <= 2) ? 4 : (NA * NB <= 12 ? 2 : 1);
-  hipLaunchKernelGGL((factored_kernel<ELT, RT, NA, NB>), dim3(n), dim3(256), 0, s, items, g, m, part);
+  constexpr int RT = rt_of(NA, NB);
+  hipLaunchKernelGGL((factored_kernel<ELT, AL, RT, NA, NB>), dim3(n), dim3(256), 0, s, items, g, m, part);
   return hipGetLastError();
 }
 
-#define DATTRI_FACT_CASE(E, A, B) \
-  if (elt == E && na == A && nb == B) return launch_one<E, A, B>(items, n_items, groups, members, partials, s);
-
-hipError_t launch_factored(int elt, int na, int nb, const FactItem* items, int n_items,
+hipError_t launch_factored(int elt, int na, int nb, int aligned, const FactItem* items, int n_items,
                            const FactGroup* groups, const FactMember* members, float* partials,
                            hipStream_t s) {
   if (n_items <= 0) return hipSuccess;
+#define DATTRI_FACT_CASE(E, A, B) \
+  if (elt == E && na == A && nb == B) return launch_one<E, true, A, B>(items, n_items, groups, members, partials, s);
 #define DATTRI_FACT_NB(E, A) DATTRI_FACT_CASE(E, A, 1) DATTRI_FACT_CASE(E, A, 2) DATTRI_FACT_CASE(E, A, 4)
 #define DATTRI_FACT_ALL(E) \
   DATTRI_FACT_NB(E, 1) DATTRI_FACT_NB(E, 2) DATTRI_FACT_NB(E, 4) DATTRI_FACT_NB(E, 6) DATTRI_FACT_NB(E, 8)
+  if (!aligned) {
+    if (na != 8 || nb != 4) return hipErrorInvalidValue;
+    if (elt == 2) return launch_one<2, false, 8, 4>(items, n_items, groups, members, partials, s);
+    if (elt == 4) return launch_one<4, false, 8, 4>(items, n_items, groups, members, partials, s);
+    return hipErrorInvalidValue;
+  }
   DATTRI_FACT_ALL(2)
   DATTRI_FACT_ALL(4)
+#undef DATTRI_FACT_ALL
+#undef DATTRI_FACT_NB
+#undef DATTRI_FACT_CASE
   return hipErrorInvalidValue;
 }
 

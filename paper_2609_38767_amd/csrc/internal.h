@@ -74,11 +74,14 @@ struct ReduceTask {
   int32_t pad0, pad1;
 };
 
-hipError_t launch_factored(int elt_bytes, int na, int nb, const FactItem* items, int n_items,
-                           const FactGroup* groups, const FactMember* members, float* partials,
-                           hipStream_t s);
-void factored_instance(int elt_bytes, int na_req, int nb_req, int* na_inst, int* nb_inst,
-                       int* rows_per_wave);
+// Items with example < 0 are padding (the workgroup exits at once); they keep
+// the XCD-interleaved order exact.
+hipError_t launch_factored(int elt_bytes, int na, int nb, int aligned, const FactItem* items,
+                           int n_items, const FactGroup* groups, const FactMember* members,
+                           float* partials, hipStream_t s);
+void factored_instance(int elt_bytes, int na_req, int nb_req, int aligned, int* na_inst,
+                       int* nb_inst, int* rows_per_wave);
+constexpr int kXcds = 8;  // MI355X: workgroup i is dispatched to XCD i mod 8
 
 hipError_t launch_reduce(const ReduceTask* tasks, int n_tasks, int n_examples,
                          const float* partials, void* phi, int phi_bf16, int64_t ld_phi,

@@ -144,7 +144,7 @@ struct Plan {
   std::vector<FactMember> members;
   std::vector<ReduceTask> tasks;  // factored tasks first, then one per MatChunk
   int n_fact_tasks = 0;
-  struct Launch { int elt, na, nb, first, count; };
+  struct Launch { int elt, na, nb, aligned, first, count; };
   std::vector<Launch> launches;
   std::vector<MatChunk> mat;
   // workspace layout (byte offsets)
@@ -200,9 +200,9 @@ dattri_status build_plan(const dattri_ctx* ctx, dattri_route forced, Plan& P) {
   }
 
   size_t fpart_floats = 0;
-  struct ItemKey { FactItem it; double cost; int inst; };
-  std::vector<ItemKey> keyed;
-  std::vector<std::pair<int, int>> insts;  // (na_inst, nb_inst)
+  struct Inst { int na, nb, aligned; std::vector<int> groups; };
+  std::vector<Inst> insts;
+  std::vector<double> group_cost;
   for (size_t g = 0; g < group_layers.size(); ++g) {
     const Layer& H = ctx->layers[group_layers[g][0]];
     FactGroup G;
@@ -214,7 +214,7 @@ dattri_status build_plan(const dattri_ctx* ctx, dattri_route forced, Plan& P) {
     G.n = n;
     G.n_members = (int)group_layers[g].size();
     G.member0 = (int)P.members.size();
-    G.aligned = ((uintptr_t)H.A % 16 == 0) && (H.d_in * elt) % 16 == 0;
+    bool aligned = ((uintptr_t)H.A % 16 == 0) && (H.d_in * elt) % 16 == 0;
     int na = 0, nb_max = 0;
     double bytes_per_row = (double)H.d_in;
     for (int li : group_layers[g]) {
@@ -229,7 +229,7 @@ dattri_status build_plan(const dattri_ctx* ctx, dattri_route forced, Plan& P) {
       M.a_tile0 = na;
       M.na = tiles16(L.k_in);
       M.nb = tiles16(L.k_out);
-      M.aligned = ((uintptr_t)L.B % 16 == 0) && (L.d_out * elt) % 16 == 0;
+      aligned = aligned && ((uintptr_t)L.B % 16 == 0) && (L.d_out * elt) % 16 == 0;
       for (int t = 0; t < M.na; ++t) {
         G.ptile[na + t] = L.P_in;
         G.ptile_local[na + t] = t;
@@ -241,8 +241,10 @@ dattri_status build_plan(const dattri_ctx* ctx, dattri_route forced, Plan& P) {
       P.members.push_back(M);
     }
     G.na = na;
+    G.aligned = aligned;
+    for (int m = 0; m < G.n_members; ++m) P.members[G.member0 + m].aligned = aligned;
     int na_inst, nb_inst, rt;
-    factored_instance(elt, na, nb_max, &na_inst, &nb_inst, &rt);
+    factored_instance(elt, na, nb_max, aligned, &na_inst, &nb_inst, &rt);
     const int sub_rows = kWaves * rt * 16;
     int cr = std::max(sub_rows, 512 / sub_rows * sub_rows);
     if (H.T <= cr) cr = std::max(sub_rows, (H.T + sub_rows - 1) / sub_rows * sub_rows);
@@ -268,26 +270,42 @@ dattri_status build_plan(const dattri_ctx* ctx, dattri_route forced, Plan& P) {
     }
     int inst = -1;
     for (size_t i = 0; i < insts.size(); ++i)
-      if (insts[i].first == na_inst && insts[i].second == nb_inst) inst = (int)i;
-    if (inst < 0) { insts.push_back({na_inst, nb_inst}); inst = (int)insts.size() - 1; }
-    for (int e = 0; e < n; ++e)
-      for (int c = 0; c < G.n_chunks; ++c) {
-        const int rows = std::min(cr, std::max(0, H.T - c * cr));
-        keyed.push_back({{(int)g, e, c, 0}, rows * bytes_per_row, inst});
-      }
+      if (insts[i].na == na_inst && insts[i].nb == nb_inst && insts[i].aligned == (int)aligned)
+        inst = (int)i;
+    if (inst < 0) {
+      insts.push_back({na_inst, nb_inst, (int)aligned, {}});
+      inst = (int)insts.size() - 1;
+    }
+    insts[inst].groups.push_back((int)g);
+    group_cost.push_back((double)n * H.T * bytes_per_row);
     P.groups.push_back(G);
   }
   P.n_fact_tasks = (int)P.tasks.size();
-  // One launch per kernel instance; inside it, costliest items first.
-  std::stable_sort(keyed.begin(), keyed.end(), [](const ItemKey& a, const ItemKey& b) {
-    return a.inst != b.inst ? a.inst < b.inst : a.cost > b.cost;
-  });
-  for (size_t i = 0; i < keyed.size(); ++i) {
-    if (P.launches.empty() || P.launches.back().na != insts[keyed[i].inst].first ||
-        P.launches.back().nb != insts[keyed[i].inst].second)
-      P.launches.push_back({elt, insts[keyed[i].inst].first, insts[keyed[i].inst].second, (int)i, 0});
-    P.launches.back().count++;
-    P.items.push_back(keyed[i].it);
+  // One launch per kernel instance.  Inside a launch, every item of a group
+  // runs on one XCD (its projection maps then stay in that XCD's L2): groups
+  // are dealt, costliest first, to the least-loaded of 8 per-XCD queues, and
+  // the queues are interleaved so that position 8*s + x holds queue x's s-th
+  // item (workgroups are dispatched round-robin over the XCDs).  Short queues
+  // are padded with items that exit at once.
+  for (const Inst& I : insts) {
+    std::vector<int> order = I.groups;
+    std::stable_sort(order.begin(), order.end(),
+                     [&](int a, int b) { return group_cost[a] > group_cost[b]; });
+    std::vector<std::vector<FactItem>> q(kXcds);
+    double load[kXcds] = {0};
+    for (int g : order) {
+      const int x = (int)(std::min_element(load, load + kXcds) - load);
+      for (int e = 0; e < n; ++e)
+        for (int c = 0; c < P.groups[g].n_chunks; ++c) q[x].push_back({g, e, c, 0});
+      load[x] += group_cost[g];
+    }
+    size_t len = 0;
+    for (const auto& v : q) len = std::max(len, v.size());
+    const int first = (int)P.items.size();
+    for (size_t s = 0; s < len; ++s)
+      for (int x = 0; x < kXcds; ++x)
+        P.items.push_back(s < q[x].size() ? q[x][s] : FactItem{0, -1, 0, 0});
+    P.launches.push_back({elt, I.na, I.nb, I.aligned, first, (int)P.items.size() - first});
   }
 
   // ---- materialized layers: example chunks staged through G
@@ -583,8 +601,8 @@ dattri_status dattri_project_per_example(dattri_ctx* ctx, void* phi, dattri_dtyp
   float* fpart = (float*)(ws + P.off_fpart);
   const int phi_bf16 = phi_dtype == DATTRI_BF16;
   for (const Plan::Launch& L : P.launches)
-    HIP_TRY(launch_factored(L.elt, L.na, L.nb, d_items + L.first, L.count, d_groups, d_members,
-                            fpart, s));
+    HIP_TRY(launch_factored(L.elt, L.na, L.nb, L.aligned, d_items + L.first, L.count, d_groups,
+                            d_members, fpart, s));
   if (P.n_fact_tasks)
     HIP_TRY(launch_reduce(d_tasks, P.n_fact_tasks, n, fpart, phi, phi_bf16, ld_phi, s));
 

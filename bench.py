@@ -32,7 +32,7 @@ def parse():
     p.add_argument("--steps", type=int, default=10)
     p.add_argument("--warmup", type=int, default=2)
     p.add_argument("--no-cpu-baseline", action="store_true")
-    p.add_argument("--phase", choices=["all", "project", "score"], default="all")
+    p.add_argument("--phase", choices=["all", "project", "score", "copy"], default="all")
     return p.parse_args()
 
 
@@ -96,6 +96,24 @@ def main():
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
     stream = torch.cuda.current_stream()
+    if args.phase == "copy":
+        # A plain device-to-device copy of known size: calibrates the HBM
+        # traffic counters and measures the achievable stream bandwidth.
+        nbytes = 1 << 30
+        src = torch.empty(nbytes, dtype=torch.uint8, device=dev).fill_(1)
+        dst = torch.empty_like(src)
+        for _ in range(2):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record(stream)
+        for _ in range(args.steps):
+            dst.copy_(src)
+        b.record(stream)
+        torch.cuda.synchronize()
+        ms = a.elapsed_time(b) / args.steps
+        print(json.dumps({"copy_bytes": nbytes, "ms": ms, "gbs_read_plus_write": 2 * nbytes / ms / 1e6}))
+        return
     wl = W.WORKLOADS["llama8b"]
     swl = W.WORKLOADS["score"]
     n = wl["batch"]

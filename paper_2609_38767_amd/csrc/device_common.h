@@ -10,6 +10,7 @@ namespace dev {
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef int i32x4 __attribute__((ext_vector_type(4)));
 typedef __amdgpu_buffer_rsrc_t rsrc_t;
 
@@ -101,6 +102,15 @@ __device__ inline f32x4 frag_mma<4>(i32x4 a, i32x4 b, f32x4 c) {
   c = mfma_f32_4(fa[2], fb[2], c);
   c = mfma_f32_4(fa[3], fb[3], c);
   return c;
+}
+
+// Workgroup barrier that orders LDS accesses only.  __syncthreads() also
+// fences global memory, which makes the compiler wait for every outstanding
+// global load (vmcnt(0)) and would drain register prefetch pipelines.
+__device__ inline void lds_barrier() {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
+  __builtin_amdgcn_s_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
 }
 
 __device__ inline float bf16_bits_to_f32(uint32_t h) { return __builtin_bit_cast(float, h << 16); }

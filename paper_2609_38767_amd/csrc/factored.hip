@@ -9,7 +9,8 @@
 // k-blocks ahead in a register ring (ragged rows and feature tails read as
 // zero through the descriptor range).  Projection fragments are staged once
 // per workgroup in LDS, one panel of KP k-blocks at a time (loaded a panel
-// ahead, one barrier per panel), and shared by the 4 waves.
+// ahead, one LDS-only barrier per panel, so prefetched loads stay in flight), and
+// shared by the 4 waves.
 //
 // The projected tiles A~ = A P_in and B~ = B P_out stay in accumulators, and
 // the token contraction A~^T B~ is done from those registers with float32 MFMA
@@ -91,7 +92,7 @@ __device__ inline void project_rows(const rsrc_t r, int r_wave, int nrows, int d
 #pragma unroll
   for (int s = 0; s < kPD; ++s) load_x(s, ring[s]);
   store_panel(0, stage);
-  __syncthreads();
+  lds_barrier();
   for (int p = 0; p < npan; ++p) {
     const int buf = p & 1;
     if (p + 1 < npan) load_panel(p + 1, stage);
@@ -114,7 +115,7 @@ __device__ inline void project_rows(const rsrc_t r, int r_wave, int nrows, int d
       }
     }
     if (p + 1 < npan) store_panel(buf ^ 1, stage);
-    __syncthreads();
+    lds_barrier();
   }
 }
 

@@ -102,8 +102,7 @@ struct GProjArgs {
   float* partials;                  // [ex_count, n_ublocks*4, na*16 x nb*16]
 };
 constexpr int kGProjRows = 64;      // rows of G per workgroup (4 waves x 16)
-constexpr int kGProjMaxTilesIn = 8;  // k_in  <= 128
-constexpr int kGProjMaxTilesOut = 8; // k_out <= 128
+constexpr int kGProjMaxTilesIn = 8;  // input tiles per pass (larger k_in loops)
 hipError_t launch_gproject(int elt_bytes, const GProjArgs& a, hipStream_t s);
 
 // ---------------------------------------------------------------- scoring
@@ -111,6 +110,10 @@ hipError_t launch_scale_rows(int elt_bytes, const void* src, const float* d, voi
                              int64_t rows, int64_t F, hipStream_t s);
 hipError_t launch_score_gemm(int elt_bytes, const void* Q, const void* X, float* S, int64_t n_q,
                              int64_t n_train, int64_t F, hipStream_t s);
+hipError_t launch_score_gemm_256(const void* Q, const void* X, float* S, int64_t n_q,
+                                 int64_t n_train, int64_t F, hipStream_t s);
+// bf16 problems at least this large (n_q * n_train) use the 256 x 256 kernel
+constexpr int64_t kBigGemmMin = (int64_t)1 << 20;
 constexpr int kTopkMax = 1024;
 hipError_t launch_topk(const float* S, int64_t n_q, int64_t n_train, int32_t k, int32_t* idx,
                        float* val, hipStream_t s);

@@ -753,6 +753,8 @@ dattri_status dattri_score(const void* phi_q, int64_t n_q, const void* phi_train
   if (n_q == 0 || n_train == 0) return DATTRI_OK;
   if (F > 0 && (!phi_q || !phi_train)) return fail(DATTRI_E_INVALID_ARG, "phi_q or phi_train is NULL");
   const int elt = dtype == DATTRI_BF16 ? 2 : 4;
+  if (F * elt * 256 >= kMaxBlockBytes)
+    return fail(DATTRI_E_UNSUPPORTED, "F=%lld too large (256 rows of F must stay below 4 GiB)", (long long)F);
   if ((uintptr_t)phi_q % 16 || (uintptr_t)phi_train % 16 || (F * elt) % 16)
     return fail(DATTRI_E_UNSUPPORTED,
                 "phi rows must be 16-byte aligned (pointers and F*%d a multiple of 16)", elt);

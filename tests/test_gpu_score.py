@@ -50,6 +50,24 @@ def test_score_ragged_tiles(dtype, precond):
     _check_topk(host64(S), ref, idx.cpu().numpy(), val.cpu().numpy(), 17)
 
 
+@pytest.mark.parametrize("shape", [(300, 5000, 104), (256, 4096, 8192), (513, 777, 40)])
+def test_score_large_tile_kernel_ragged(shape):
+    # n_q * n_train >= 2^20 routes bf16 to the 256 x 256 kernel: ragged query
+    # and training tiles and a feature tail inside a 32-wide stage
+    n_q, n_t, F = shape
+    g = torch.Generator(device=DEV).manual_seed(9)
+    Q = torch.randn((n_q, F), generator=g, device=DEV).to(torch.bfloat16)
+    X = torch.randn((n_t, F), generator=g, device=DEV).to(torch.bfloat16)
+    d = torch.exp(torch.randn(F, generator=g, device=DEV))
+    S, idx, val = score(Q, X, d, topk=10)
+    S0, _, _ = score(Q, X)
+    torch.cuda.synchronize()
+    ref = osc.score(host64(Q), host64(X), host64(d))
+    assert rel_fro(host64(S), ref) <= 2e-2
+    assert rel_fro(host64(S0), osc.score(host64(Q), host64(X))) <= 1e-5
+    _check_topk(host64(S), ref, idx.cpu().numpy(), val.cpu().numpy(), 10)
+
+
 def test_topk_only_without_scores_and_k_equals_n():
     n_q, n_t, F = 3, 40, 16
     g = torch.Generator(device=DEV).manual_seed(6)

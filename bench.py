@@ -23,7 +23,6 @@ import os
 import sys
 import time
 
-LLAMA_BYTES_PER_EXAMPLE = None  # filled from the workload description
 
 
 def parse():
@@ -32,8 +31,42 @@ def parse():
     p.add_argument("--steps", type=int, default=10)
     p.add_argument("--warmup", type=int, default=2)
     p.add_argument("--no-cpu-baseline", action="store_true")
-    p.add_argument("--phase", choices=["all", "project", "score", "copy"], default="all")
+    p.add_argument("--phase", choices=["all", "project", "score", "routing", "copy"], default="all")
     return p.parse_args()
+
+
+# Kernel sources whose text fixes each reported kernel's code: a traffic figure
+# measured with rocprofv3 counters is reported only while these are unchanged.
+KERNEL_SOURCES = {
+    "projection": ["factored.hip", "device_common.h"],
+    "score_gemm": ["score_big.hip", "score.hip", "device_common.h"],
+}
+HERE = os.path.dirname(os.path.abspath(__file__))
+
+
+def kernel_source_hash(key):
+    import hashlib
+    h = hashlib.sha256()
+    for name in KERNEL_SOURCES[key]:
+        with open(os.path.join(HERE, "paper_2609_38767_amd", "csrc", name), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()[:16]
+
+
+def measured_traffic(key):
+    """HBM bytes per launch of a kernel from the committed rocprofv3 FETCH_SIZE /
+    WRITE_SIZE summaries (calibrated against a plain copy), or None when the
+    kernel's sources changed since the counters were taken."""
+    import glob
+    want = kernel_source_hash(key)
+    for path in glob.glob(os.path.join(HERE, "profiles", "hbm_traffic_*.md")):
+        with open(path) as f:
+            for line in f:
+                if line.startswith("traffic: "):
+                    kv = dict(x.split("=", 1) for x in line.split()[1:])
+                    if kv.get("kernel") == key and kv.get("sources") == want:
+                        return int(kv["bytes"])
+    return None
 
 
 def algorithmic_projection_bytes(wl):
@@ -80,6 +113,56 @@ def cpu_baseline_projection(wl, inputs, seed, budget_s=20.0):
     return {"value": 1.0 / per_example, "unit": "examples/s", "cores": threads, "kind": "oracle",
             "sample": f"example 0, first {done} of {len(layers)} layers, factored form in float64 "
                       f"({t_total:.1f} s), extrapolated to all layers"}
+
+
+def routing_cases(dev, steps, warmup):
+    """Both forced routes and AUTO on the wide short-sequence layer (8192 ->
+    28672, T=32, batch 64, k=64) and the two switch cases (a rank-8 adapter's
+    B matrix and a narrow 128 -> 128 layer at T=2048): measured times, the
+    cost model's predictions and AUTO's regret against the faster route."""
+    import torch
+    import workloads as W
+    from paper_2609_38767_amd import (DATTRI_ROUTE_AUTO, DATTRI_ROUTE_FACTORED,
+                                      DATTRI_ROUTE_MATERIALIZED)
+    from paper_2609_38767_amd.session import ProjectionSession
+    stream = torch.cuda.current_stream()
+    out = {}
+    for name in ("routing", "lora_b", "narrow"):
+        wl = W.WORKLOADS[name]
+        n, T = wl["batch"], wl["T"]
+        sess = ProjectionSession(wl["layers"], dtype="bf16", seed=wl["seed"], device=dev)
+        for li in range(len(wl["layers"])):
+            A, B = W.factor_blocks(wl, li, 0, n, T, dev, "bf16")
+            sess.capture(li, A, B)
+        phi = torch.empty((n, sess.F), dtype=torch.float32, device=dev)
+        ms = {}
+        for rname, r in (("factored", DATTRI_ROUTE_FACTORED), ("materialized", DATTRI_ROUTE_MATERIALIZED),
+                         ("auto", DATTRI_ROUTE_AUTO)):
+            sess.workspace(r)
+            for _ in range(warmup):
+                sess.project(n, route=r, phi=phi)
+            evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+                   for _ in range(steps)]
+            for a, b in evs:
+                a.record(stream)
+                sess.project(n, route=r, phi=phi)
+                b.record(stream)
+            torch.cuda.synchronize()
+            t = sorted(a.elapsed_time(b) for a, b in evs)
+            ms[rname] = t[len(t) // 2]
+        route, pf, pm = sess.routes()[0]
+        sess.close()
+        best = min(ms["factored"], ms["materialized"])
+        L = wl["layers"][0]
+        out[name] = {"shape": f"{L['d_in']}x{L['d_out']} k_in={L['k_in']} k_out={L['k_out']} T={T} n={n}",
+                     "factored_ms": ms["factored"], "materialized_ms": ms["materialized"],
+                     "auto_ms": ms["auto"],
+                     "auto_route": "factored" if route == DATTRI_ROUTE_FACTORED else "materialized",
+                     "pred_factored_ms": pf / 1e3, "pred_materialized_ms": pm / 1e3,
+                     "auto_regret": ms["auto"] / best - 1.0}
+        print(f"[bench] routing {name}: factored {ms['factored']:.3f} ms, materialized "
+              f"{ms['materialized']:.3f} ms, auto -> {out[name]['auto_route']}", file=sys.stderr, flush=True)
+    return out
 
 
 def main():
@@ -180,12 +263,16 @@ def main():
         avg_ms = sum(ms_p) / len(ms_p)
         out["projection"] = {
             "examples_per_s": n * args.steps / wall_p, "ms_per_batch": avg_ms,
+            "ms_median": sorted(ms_p)[len(ms_p) // 2], "ms_min": min(ms_p),
             "bytes_per_example": bytes_ex, "flops_per_example": flops_ex,
             "routes": ["factored" if r == 1 else "materialized" for r in routes]}
         out["roofline"] = {"bound": "hbm", "achieved": bytes_ex * n / (avg_ms * 1e-3) / 1e9,
                            "peak": 8000.0, "unit": "GB/s",
-                           "frac": bytes_ex * n / (avg_ms * 1e-3) / 1e9 / 8000.0, "traffic": None,
+                           "frac": bytes_ex * n / (avg_ms * 1e-3) / 1e9 / 8000.0,
+                           "traffic": measured_traffic("projection"),
                            "kernel": "factored projection (all instance launches + reduce), one batch of 8"}
+    if args.phase in ("all", "routing"):
+        out["routing"] = routing_cases(dev, max(args.steps, 5), args.warmup)
     if args.phase in ("all", "score"):
         for _ in range(args.warmup):
             score_step(False)
@@ -198,10 +285,12 @@ def main():
         flops = 2.0 * n_q * n_t * F
         g_ms = sum(ms_g) / len(ms_g)
         out["score"] = {"gemm_tflops": flops / (g_ms * 1e-3) / 1e12, "gemm_ms": g_ms,
+                        "gemm_ms_median": sorted(ms_g)[len(ms_g) // 2], "gemm_ms_min": min(ms_g),
                         "with_topk_ms": sum(ms_s) / len(ms_s), "flops": flops}
         out["roofline_score"] = {"bound": "mfma", "achieved": flops / (g_ms * 1e-3) / 1e12,
                                  "peak": 2500.0, "unit": "TFLOP/s",
-                                 "frac": flops / (g_ms * 1e-3) / 1e12 / 2500.0, "traffic": None,
+                                 "frac": flops / (g_ms * 1e-3) / 1e12 / 2500.0,
+                                 "traffic": measured_traffic("score_gemm"),
                                  "kernel": "score GEMM (query scaling + NT GEMM), 2048 x 200000 x 8192"}
 
     line = {

@@ -38,7 +38,7 @@ def parse():
 # Kernel sources whose text fixes each reported kernel's code: a traffic figure
 # measured with rocprofv3 counters is reported only while these are unchanged.
 KERNEL_SOURCES = {
-    "projection": ["factored.hip", "device_common.h"],
+    "projection": ["factored.hip", "project_rows.h", "reduce.hip", "device_common.h"],
     "score_gemm": ["score_big.hip", "score.hip", "device_common.h"],
 }
 HERE = os.path.dirname(os.path.abspath(__file__))

@@ -72,6 +72,22 @@ typedef enum {
   DATTRI_ROUTE_MATERIALIZED = 2 /* G = B^T A, then P_out^T G P_in */
 } dattri_route;
 
+/* Kernel form of the factored route.  Both compute Eq. (2)'s left side with
+ * float32 accumulation; they differ only in how work is spread over the GPU:
+ *   FUSED  one kernel per work item (input group, example, token chunk)
+ *          projects A and B and contracts the tokens in registers;
+ *   SPLIT  stage 1 projects all n*T token rows slab by slab over d (many
+ *          small work items), stage 2 sums the slabs and contracts each
+ *          example's tokens in chunks; suited to captures with few examples
+ *          or short sequences, where the fused kernel has little parallelism.
+ * AUTO picks SPLIT when the fused kernel would have fewer than 1024 work
+ * items, FUSED otherwise. */
+typedef enum {
+  DATTRI_FORM_AUTO = 0,
+  DATTRI_FORM_FUSED = 1,
+  DATTRI_FORM_SPLIT = 2
+} dattri_factored_form;
+
 /* ---------------------------------------------------------------- context */
 
 /* Create a context.  `compute` is the element type of the captured factor
@@ -178,6 +194,11 @@ dattri_status dattri_clear_captures(dattri_ctx* ctx);
  * for (any workspace at least this large works).
  * Errors: STATE (a registered layer not captured, or captures disagree on n). */
 dattri_status dattri_workspace_bytes(const dattri_ctx* ctx, dattri_route route, size_t* bytes);
+
+/* Set / read the context's factored-route kernel form (default AUTO).
+ * Errors: INVALID_ARG (NULL ctx, unknown form). */
+dattri_status dattri_set_factored_form(dattri_ctx* ctx, dattri_factored_form form);
+dattri_status dattri_get_factored_form(const dattri_ctx* ctx, dattri_factored_form* form);
 
 /* Projected per-example gradients of every registered layer, concatenated
  * (Eq. (2) per layer; blocks in registration order).

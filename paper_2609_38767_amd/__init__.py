@@ -27,6 +27,7 @@ __all__ = [
 
 DATTRI_F32, DATTRI_BF16 = 0, 1
 DATTRI_ROUTE_AUTO, DATTRI_ROUTE_FACTORED, DATTRI_ROUTE_MATERIALIZED = 0, 1, 2
+DATTRI_FORM_AUTO, DATTRI_FORM_FUSED, DATTRI_FORM_SPLIT = 0, 1, 2
 STATUS_NAMES = {0: "OK", -1: "E_INVALID_ARG", -2: "E_SHAPE", -3: "E_DTYPE", -4: "E_STATE",
                 -5: "E_WORKSPACE", -6: "E_HIP", -7: "E_UNSUPPORTED"}
 
@@ -68,6 +69,8 @@ _SIGS = {
     "dattri_capture_layer": (_i32, [_vp, _i32, _vp, _vp, _i32, _i32, _vp]),
     "dattri_clear_captures": (_i32, [_vp]),
     "dattri_workspace_bytes": (_i32, [_vp, _i32, _P(_sz)]),
+    "dattri_set_factored_form": (_i32, [_vp, _i32]),
+    "dattri_get_factored_form": (_i32, [_vp, _P(_i32)]),
     "dattri_project_per_example": (_i32, [_vp, _vp, _i32, _i64, _vp, _sz, _i32, _vp]),
     "dattri_materialize_gradient": (_i32, [_vp, _i32, _i32, _i32, _vp, _vp]),
     "dattri_set_cost_model": (_i32, [_vp, _P(CostModel)]),
@@ -207,6 +210,16 @@ def dattri_workspace_bytes(ctx, route=DATTRI_ROUTE_AUTO):
     b = _sz()
     _check(load().dattri_workspace_bytes(ctx, route, ctypes.byref(b)), "dattri_workspace_bytes")
     return b.value
+
+
+def dattri_set_factored_form(ctx, form):
+    _check(load().dattri_set_factored_form(ctx, form), "dattri_set_factored_form")
+
+
+def dattri_get_factored_form(ctx):
+    f = _i32()
+    _check(load().dattri_get_factored_form(ctx, ctypes.byref(f)), "dattri_get_factored_form")
+    return f.value
 
 
 def dattri_project_per_example(ctx, phi, phi_dtype, ld_phi, workspace, ws_bytes,

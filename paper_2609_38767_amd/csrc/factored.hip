@@ -20,104 +20,10 @@
 // partials in a fixed order (deterministic, no float atomics) and writes phi.
 #include "device_common.h"
 #include "internal.h"
+#include "project_rows.h"
 
 namespace dattri {
 using namespace dev;
-
-constexpr int kPanel = 4;  // k-blocks per LDS panel of projection fragments
-
-// k-blocks of factor fragments prefetched ahead: about 8 KiB in flight per
-// wave where the register budget of two waves per SIMD allows it, else 4 KiB.
-constexpr int pd_of(int rt, int na, int nb) { return (rt >= 4 || na * (rt + nb) >= 24) ? 2 : 4; }
-
-// Projection fragment source of up to NT output tiles: fragment (kb, t) of the
-// packed map lives at base[t] + kb * stride[t] (bytes).
-template <int NT>
-struct FragSrc {
-  const uint8_t* base[NT];
-  int64_t stride[NT];
-  int nt;  // tiles in use
-};
-
-// acc[rt][t] += X[rows, :] * P[:, tile t] over all k-blocks of a d-wide row
-// block.  X rows r_wave + rt*16 + (lane & 15) of descriptor `r` (rows >= nrows
-// and columns >= d read as zero).  All 256 threads must call this together.
-template <int ELT, bool AL, int RT, int NT, int NTL, int kPD>
-__device__ inline void project_rows(const rsrc_t r, int r_wave, int nrows, int d,
-                                    const FragSrc<NT>& P, f32x4 (&acc)[RT][NT],
-                                    uint8_t (*pan)[kPanel][NTL][kFragBytes]) {
-  constexpr int EPL = 16 / ELT, KR = 4 * EPL;
-  static_assert(kPanel % kPD == 0, "ring slots must be static inside a panel");
-  // A panel holds kPanel * NT fragments of 1 KiB; fragment f = w + 4*i is
-  // copied by wave w (one 16-byte load per lane), so every index is static.
-  constexpr int NF = kPanel * NT;
-  constexpr int CPT = (NF + kWaves - 1) / kWaves;  // fragments per wave
-  static_assert(NT <= NTL, "panel too small");
-  const int tid = threadIdx.x, lane = tid & 63, g = lane >> 4, m16 = lane & 15;
-  const int wave = tid >> 6;
-  const int nkb = (d + KR - 1) / KR;
-  const int npan = (nkb + kPanel - 1) / kPanel;
-
-  auto load_panel = [&](int p, i32x4 (&st)[CPT]) {
-#pragma unroll
-    for (int i = 0; i < CPT; ++i)
-#pragma unroll
-      for (int w = 0; w < kWaves; ++w) {
-        const int f = w + kWaves * i, t = f % NT, kbl = f / NT;
-        if (f < NF && wave == w) {
-          const int kb = min(p * kPanel + kbl, nkb - 1);
-          st[i] = (t < P.nt) ? *(const i32x4*)(P.base[t] + kb * P.stride[t] + lane * 16)
-                             : i32x4{0, 0, 0, 0};
-        }
-      }
-  };
-  auto store_panel = [&](int buf, const i32x4 (&st)[CPT]) {
-#pragma unroll
-    for (int i = 0; i < CPT; ++i)
-#pragma unroll
-      for (int w = 0; w < kWaves; ++w) {
-        const int f = w + kWaves * i, t = f % NT, kbl = f / NT;
-        if (f < NF && wave == w) *(i32x4*)(&pan[buf][kbl][t][lane * 16]) = st[i];
-      }
-  };
-  auto load_x = [&](int kb, i32x4 (&x)[RT]) {
-    const int col = kb * KR + g * EPL;
-#pragma unroll
-    for (int rt = 0; rt < RT; ++rt) x[rt] = load_frag<ELT>(r, r_wave + rt * 16 + m16, nrows, col, d, AL);
-  };
-
-  i32x4 stage[CPT];
-  i32x4 ring[kPD][RT];
-  load_panel(0, stage);
-#pragma unroll
-  for (int s = 0; s < kPD; ++s) load_x(s, ring[s]);
-  store_panel(0, stage);
-  lds_barrier();
-  for (int p = 0; p < npan; ++p) {
-    const int buf = p & 1;
-    if (p + 1 < npan) load_panel(p + 1, stage);
-#pragma unroll
-    for (int kbl = 0; kbl < kPanel; ++kbl) {
-      const int kb = p * kPanel + kbl;
-      if (kb < nkb) {
-        i32x4 x[RT];
-#pragma unroll
-        for (int rt = 0; rt < RT; ++rt) x[rt] = ring[kbl % kPD][rt];
-        load_x(kb + kPD, ring[kbl % kPD]);
-#pragma unroll
-        for (int t = 0; t < NT; ++t) {
-          if (t < P.nt) {
-            const i32x4 pf = *(const i32x4*)(&pan[buf][kbl][t][lane * 16]);
-#pragma unroll
-            for (int rt = 0; rt < RT; ++rt) acc[rt][t] = frag_mma<ELT>(x[rt], pf, acc[rt][t]);
-          }
-        }
-      }
-    }
-    if (p + 1 < npan) store_panel(buf ^ 1, stage);
-    lds_barrier();
-  }
-}
 
 template <int ELT, bool AL, int RT, int NA, int NB>
 __global__ __launch_bounds__(256, (AL && NA * NB <= 12) ? 2 : 1) void factored_kernel(const FactItem* __restrict__ items,
@@ -165,7 +71,7 @@ __global__ __launch_bounds__(256, (AL && NA * NB <= 12) ? 2 : 1) void factored_k
     for (int rt = 0; rt < RT; ++rt)
 #pragma unroll
       for (int t = 0; t < NA; ++t) acc_a[rt][t] = f32x4{0.f, 0.f, 0.f, 0.f};
-    project_rows<ELT, AL, RT, NA, NTL, PD>(ra, r_wave, rows_valid, d_in, pin, acc_a, pan);
+    project_rows<ELT, AL, RT, NA, NTL, PD>(ra, r_wave, rows_valid, d_in, d_in, pin, acc_a, pan);
 
     for (int mi = 0; mi < G.n_members; ++mi) {
       const FactMember& M = members[G.member0 + mi];
@@ -184,7 +90,7 @@ __global__ __launch_bounds__(256, (AL && NA * NB <= 12) ? 2 : 1) void factored_k
       for (int rt = 0; rt < RT; ++rt)
 #pragma unroll
         for (int t = 0; t < NB; ++t) acc_b[rt][t] = f32x4{0.f, 0.f, 0.f, 0.f};
-      project_rows<ELT, AL, RT, NB, NTL, PD>(rb, r_wave, rows_valid, d_out, pout, acc_b, pan);
+      project_rows<ELT, AL, RT, NB, NTL, PD>(rb, r_wave, rows_valid, d_out, d_out, pout, acc_b, pan);
 
       const int a0 = M.a_tile0, a1 = M.a_tile0 + M.na;
 #pragma unroll
@@ -225,30 +131,6 @@ __global__ __launch_bounds__(256, (AL && NA * NB <= 12) ? 2 : 1) void factored_k
         }
       }
     }
-  }
-}
-
-// Sum the partial blocks of each (layer, example) in index order and write the
-// layer block of phi: element (c, r) at column phi_offset + c*k_out + r.
-__global__ __launch_bounds__(256) void reduce_kernel(const ReduceTask* __restrict__ tasks,
-                                                     const float* __restrict__ partials,
-                                                     void* __restrict__ phi, int phi_bf16,
-                                                     int64_t ld_phi) {
-  const ReduceTask t = tasks[blockIdx.y];
-  const int ex_local = blockIdx.x;
-  const int64_t ex = (int64_t)t.ex_begin + ex_local;
-  const float* base = partials + t.partial_base + (int64_t)ex_local * t.n_parts * t.part_floats;
-  const int n_out = t.k_in * t.k_out;
-  for (int e = threadIdx.x; e < n_out; e += blockDim.x) {
-    const int c = e / t.k_out, r = e - c * t.k_out;
-    const float* p = base + c * t.ldp + r;
-    float s = 0.f;
-    for (int q = 0; q < t.n_parts; ++q) s += p[(int64_t)q * t.part_floats];
-    const int64_t o = ex * ld_phi + t.phi_offset + e;
-    if (phi_bf16)
-      ((uint16_t*)phi)[o] = f32_to_bf16_bits(s);
-    else
-      ((float*)phi)[o] = s;
   }
 }
 
@@ -302,14 +184,6 @@ hipError_t launch_factored(int elt, int na, int nb, int aligned, const FactItem*
 #undef DATTRI_FACT_NB
 #undef DATTRI_FACT_CASE
   return hipErrorInvalidValue;
-}
-
-hipError_t launch_reduce(const ReduceTask* tasks, int n_tasks, int n_examples, const float* partials,
-                         void* phi, int phi_bf16, int64_t ld_phi, hipStream_t s) {
-  if (n_tasks <= 0 || n_examples <= 0) return hipSuccess;
-  hipLaunchKernelGGL(reduce_kernel, dim3(n_examples, n_tasks), dim3(256), 0, s, tasks, partials, phi,
-                     phi_bf16, ld_phi);
-  return hipGetLastError();
 }
 
 }  // namespace dattri

@@ -83,9 +83,60 @@ void factored_instance(int elt_bytes, int na_req, int nb_req, int aligned, int* 
                        int* nb_inst, int* rows_per_wave);
 constexpr int kXcds = 8;  // MI355X: workgroup i is dispatched to XCD i mod 8
 
-hipError_t launch_reduce(const ReduceTask* tasks, int n_tasks, int n_examples,
+// max_out: the largest k_in*k_out over the tasks (sets the grid's z extent)
+hipError_t launch_reduce(const ReduceTask* tasks, int n_tasks, int n_examples, int max_out,
                          const float* partials, void* phi, int phi_bf16, int64_t ld_phi,
                          hipStream_t s);
+
+// ------------------------------------------- factored route, split form
+// For short sequences, where the fused kernel has too few work items: stage 1
+// projects the token rows of every factor block (all examples flattened,
+// n*T rows) slab by slab over the feature dimension d, writing float32
+// partial projections [slab][row][tile cols]; stage 2 sums the slabs and
+// contracts each example's tokens into its layer block of phi.
+constexpr int kSplitRows = 128;     // rows per stage-1 workgroup (4 waves x 2 row tiles)
+constexpr int kSplitSlabQuantum = 128;  // slab widths are multiples of this
+struct SplitOp {                    // one factor block: a group's A or a member's B
+  const void* X;                    // [rows, ld] row-major
+  int32_t rows, ld;                 // n*T, d
+  int32_t slab_cols, n_slabs;
+  int32_t nt;                       // 16-column tiles of the projected rows
+  int32_t aligned;                  // 16-byte vector loads allowed
+  int64_t out_base;                 // float offset of [slab 0][row 0][col 0]
+  const void* ptile[kMaxGroupTiles];    // packed map holding tile t
+  int32_t ptile_local[kMaxGroupTiles];  // tile index inside that map
+  int32_t ptile_nt[kMaxGroupTiles];     // 16-col tiles of that map
+};
+struct SplitItem { int32_t op, row_block, slab, pad; };
+struct ContractTask {               // one layer
+  int64_t a_base, b_base;           // out_base of its A op and B op
+  int32_t a_ld, b_ld;               // floats per projected row of each op
+  int32_t a_col0;                   // first column of this layer's tiles in the A op
+  int32_t a_slabs, b_slabs;
+  int32_t k_in, k_out, T, rows;     // rows = n*T (the slab stride in rows)
+  int32_t tok_chunk, n_tchunks;     // tokens per workgroup, chunks per example
+  int32_t pad0;
+  int64_t phi_offset;               // used when n_tchunks == 1 (phi written directly)
+  int64_t partial_base;             // else: float offset of [example][chunk][ki16 x ko16]
+  const int32_t* lengths;           // [n] or null
+};
+// One launch per instance (elt, aligned, tiles); items of that instance only.
+hipError_t launch_split_project(int elt_bytes, int aligned, int nt, const SplitItem* items,
+                                int n_items, const SplitOp* ops, float* out, hipStream_t s);
+int split_nt_instance(int nt_req);  // tiles of the instance that serves nt_req tiles
+// In-place sum of a stage-1 op's slabs into slab 0 (slab order).
+struct SlabSumTask {
+  int64_t base;                     // float offset of slab 0 (16-byte aligned)
+  int64_t n4;                       // float4s per slab
+  int64_t stride4;                  // float4s between slabs
+  int32_t n_slabs, pad0;
+};
+hipError_t launch_slab_sum(const SlabSumTask* tasks, int n_tasks, int64_t max_n4, float* out,
+                           hipStream_t s);
+// Grid (max_tchunks, n_examples, n_tasks); chunks past a task's n_tchunks exit.
+hipError_t launch_split_contract(const ContractTask* tasks, int n_tasks, int n_examples,
+                                 int max_tchunks, const float* proj, float* partials, void* phi,
+                                 int phi_bf16, int64_t ld_phi, hipStream_t s);
 
 // ---------------------------------------------------- materialized route
 struct GradArgs {
@@ -98,11 +149,13 @@ hipError_t launch_gradient(int elt_bytes, const GradArgs& a, hipStream_t s);
 struct GProjArgs {
   const float* G;                   // [ex_count, d_out, d_in]
   const void* P_in; const void* P_out;  // packed
-  int32_t d_in, d_out, k_in, k_out, ex_count, n_ublocks;
-  float* partials;                  // [ex_count, n_ublocks*4, na*16 x nb*16]
+  int32_t d_in, d_out, k_in, k_out, ex_count;
+  int32_t n_ublocks;                // row blocks of kGProjRows rows of G
+  int32_t n_ksplit, kb_per_split;   // d_in split into n_ksplit ranges of k-blocks
+  float* partials;                  // [ex_count][n_ublocks * n_ksplit][na*16 x nb*16]
 };
-constexpr int kGProjRows = 64;      // rows of G per workgroup (4 waves x 16)
-constexpr int kGProjMaxTilesIn = 8;  // input tiles per pass (larger k_in loops)
+constexpr int kGProjRows = 128;     // rows of G per workgroup (4 waves x 2 row tiles)
+constexpr int kGProjMaxTilesIn = 8; // input tiles per pass (larger k_in loops)
 hipError_t launch_gproject(int elt_bytes, const GProjArgs& a, hipStream_t s);
 
 // ---------------------------------------------------------------- scoring

@@ -98,72 +98,117 @@ __global__ __launch_bounds__(256) void gradient_kernel(GradArgs a) {
 }
 
 // --------------------------------------------------- Psi = (P_out^T G P_in)^T
-// Workgroup: 64 rows of G (one 16-row slice per wave) of one example.  For
-// each group of up to 8 input tiles: H = G[rows] P_in by float32 MFMA, with
-// 64-row slabs of P_in converted to float32 and staged in LDS in operand order;
-// then for every output tile, Psi_part = H^T P_out[rows] straight from the H
-// accumulators (their C layout is a K=4 operand slice per element index).
-// Each wave writes its partial block; the reduce kernel sums them in order.
-constexpr int kPV = 64;  // P_in rows staged per LDS slab
+// Workgroup: 128 rows of G (two 16-row tiles per wave) of one example, over one
+// range of d_in's k-blocks (d_in is split when row blocks times examples alone
+// give too few workgroups).  H = G[rows, range] P_in[range, :] by float32 MFMA
+// (16x16x4) with no LDS staging: each lane reads its 16-byte fragment of the
+// packed P_in (element j of lane (g, n) is row g*EPL + j of the k-block,
+// column n) and the matching EPL columns of its G row, so the j-th MFMA step
+// contracts the K slots {g*EPL + j} of both operands.  Then
+// Psi_part = H^T P_out[rows] straight from the H accumulators (their C layout
+// is a K=4 operand slice per element index); the four waves' parts are summed
+// in LDS in wave order and the workgroup writes one partial block, which the
+// reduce kernel sums with the others in index order.
+constexpr int kGRT = 2;  // row tiles per wave
+static_assert(kWaves * kGRT * 16 == kGProjRows, "row block");
 
 template <int ELT>
-__global__ __launch_bounds__(256) void gproject_kernel(GProjArgs a) {
-  __shared__ __align__(16) float Ps[kPV / 16][kGProjMaxTilesIn][64][4];  // 32 KiB
+__global__ __launch_bounds__(256, 2) void gproject_kernel(GProjArgs a) {
+  constexpr int EPL = 16 / ELT, KR = 4 * EPL, NH = EPL / 4;
+  constexpr int NT = kGProjMaxTilesIn;
+  __shared__ float red[kWaves][NT][256];  // 32 KiB
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int g = lane >> 4, m16 = lane & 15;
-  const int ub = blockIdx.x, e = blockIdx.y;
-  const int u0 = ub * kGProjRows + wave * 16;
+  const int ub = blockIdx.x / a.n_ksplit, ks = blockIdx.x - ub * a.n_ksplit;
+  const int e = blockIdx.y;
+  const int u0 = ub * kGProjRows + wave * kGRT * 16;
   const float* Ge = a.G + (int64_t)e * a.d_out * a.d_in;
   const rsrc_t rg = make_rsrc(Ge, (uint32_t)((int64_t)a.d_out * a.d_in * 4));
   const bool g_aligned = (a.d_in % 4) == 0;
+  const int nkb = (a.d_in + KR - 1) / KR;
+  const int kb_begin = ks * a.kb_per_split, kb_end = min(nkb, kb_begin + a.kb_per_split);
   const int na_all = (a.k_in + 15) >> 4, nb_all = (a.k_out + 15) >> 4;
   const int ldp = nb_all * 16;
   const int part_floats = na_all * 16 * ldp;
-  float* dst = a.partials + ((int64_t)(e * a.n_ublocks + ub) * kWaves + wave) * part_floats;
+  float* dst = a.partials + ((int64_t)e * a.n_ublocks * a.n_ksplit + blockIdx.x) * part_floats;
   const uint8_t* pin = (const uint8_t*)a.P_in;
   const uint8_t* pout = (const uint8_t*)a.P_out;
 
-  for (int ta0 = 0; ta0 < na_all; ta0 += kGProjMaxTilesIn) {
-    const int nt = min(kGProjMaxTilesIn, na_all - ta0);
-    f32x4 H[kGProjMaxTilesIn];
+  auto load_g = [&](int kb, f32x4 (&gf)[kGRT][NH]) {
 #pragma unroll
-    for (int t = 0; t < kGProjMaxTilesIn; ++t) H[t] = f32x4{0.f, 0.f, 0.f, 0.f};
-    for (int v0 = 0; v0 < a.d_in; v0 += kPV) {
-      __syncthreads();
-      for (int idx = tid; idx < (kPV / 16) * nt * 64 * 4; idx += 256) {
-        const int j = idx & 3, ln = (idx >> 2) & 63, rest = idx >> 8;
-        const int t = rest % nt, vs = rest / nt;
-        const int v = v0 + vs * 16 + 4 * (ln >> 4) + j;
-        const int c = (ta0 + t) * 16 + (ln & 15);
-        Ps[vs][t][ln][j] = packed_elem<ELT>(pin, v, c, a.d_in, a.k_in);
-      }
-      __syncthreads();
+    for (int rt = 0; rt < kGRT; ++rt)
 #pragma unroll
-      for (int vs = 0; vs < kPV / 16; ++vs) {
-        const i32x4 gf = load_frag<4>(rg, u0 + m16, a.d_out, v0 + vs * 16 + 4 * g, a.d_in, g_aligned);
+      for (int h = 0; h < NH; ++h)
+        gf[rt][h] = __builtin_bit_cast(
+            f32x4, load_frag<4>(rg, u0 + rt * 16 + m16, a.d_out, kb * KR + g * EPL + 4 * h, a.d_in, g_aligned));
+  };
+
+  for (int ta0 = 0; ta0 < na_all; ta0 += NT) {
+    const int nt = min(NT, na_all - ta0);
+    f32x4 H[kGRT][NT];
 #pragma unroll
-        for (int t = 0; t < kGProjMaxTilesIn; ++t) {
-          if (t < nt) {
-            const i32x4 pf = *(const i32x4*)&Ps[vs][t][lane][0];
-            H[t] = frag_mma<4>(gf, pf, H[t]);
+    for (int rt = 0; rt < kGRT; ++rt)
+#pragma unroll
+      for (int t = 0; t < NT; ++t) H[rt][t] = f32x4{0.f, 0.f, 0.f, 0.f};
+    f32x4 gcur[kGRT][NH], gnext[kGRT][NH];
+    if (kb_begin < kb_end) load_g(kb_begin, gcur);
+    for (int kb = kb_begin; kb < kb_end; ++kb) {
+      if (kb + 1 < kb_end) load_g(kb + 1, gnext);
+#pragma unroll
+      for (int t = 0; t < NT; ++t) {
+        if (t < nt) {
+          const i32x4 pf = *(const i32x4*)(pin + ((int64_t)(kb * na_all + ta0 + t) * 64 + lane) * 16);
+          float pv[EPL];
+          if (ELT == 2) {
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+              const uint32_t w = (uint32_t)pf[i];
+              pv[2 * i] = bf16_bits_to_f32(w & 0xFFFFu);
+              pv[2 * i + 1] = bf16_bits_to_f32(w >> 16);
+            }
+          } else {
+            const f32x4 pff = __builtin_bit_cast(f32x4, pf);
+#pragma unroll
+            for (int i = 0; i < 4; ++i) pv[i] = pff[i];
           }
+#pragma unroll
+          for (int rt = 0; rt < kGRT; ++rt)
+#pragma unroll
+            for (int j = 0; j < EPL; ++j) H[rt][t] = mfma_f32_4(gcur[rt][j / 4][j % 4], pv[j], H[rt][t]);
         }
       }
+#pragma unroll
+      for (int rt = 0; rt < kGRT; ++rt)
+#pragma unroll
+        for (int h = 0; h < NH; ++h) gcur[rt][h] = gnext[rt][h];
     }
     for (int tb = 0; tb < nb_all; ++tb) {
-      float po[4];
+      float po[kGRT][4];
 #pragma unroll
-      for (int i = 0; i < 4; ++i) po[i] = packed_elem<ELT>(pout, u0 + 4 * g + i, tb * 16 + m16, a.d_out, a.k_out);
+      for (int rt = 0; rt < kGRT; ++rt)
 #pragma unroll
-      for (int t = 0; t < kGProjMaxTilesIn; ++t) {
+        for (int i = 0; i < 4; ++i)
+          po[rt][i] = packed_elem<ELT>(pout, u0 + rt * 16 + 4 * g + i, tb * 16 + m16, a.d_out, a.k_out);
+#pragma unroll
+      for (int t = 0; t < NT; ++t) {
         if (t < nt) {
           f32x4 ps = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-          for (int i = 0; i < 4; ++i) ps = mfma_f32_4(H[t][i], po[i], ps);
+          for (int rt = 0; rt < kGRT; ++rt)
 #pragma unroll
-          for (int i = 0; i < 4; ++i) dst[((ta0 + t) * 16 + 4 * g + i) * ldp + tb * 16 + m16] = ps[i];
+            for (int i = 0; i < 4; ++i) ps = mfma_f32_4(H[rt][t][i], po[rt][i], ps);
+          // lane (g, n): Psi rows c = 4g..4g+3 of tile t, column n of tile tb
+#pragma unroll
+          for (int i = 0; i < 4; ++i) red[wave][t][(4 * g + i) * 16 + m16] = ps[i];
         }
       }
+      __syncthreads();
+      for (int idx = tid; idx < nt * 256; idx += 256) {
+        const int t = idx >> 8, w = idx & 255;
+        const float s = ((red[0][t][w] + red[1][t][w]) + red[2][t][w]) + red[3][t][w];
+        dst[((ta0 + t) * 16 + (w >> 4)) * ldp + tb * 16 + (w & 15)] = s;
+      }
+      __syncthreads();
     }
   }
 }
@@ -188,7 +233,8 @@ hipError_t launch_gradient(int elt, const GradArgs& a, hipStream_t s) {
 
 hipError_t launch_gproject(int elt, const GProjArgs& a, hipStream_t s) {
   if (a.ex_count <= 0) return hipSuccess;
-  const dim3 grid(a.n_ublocks, a.ex_count);
+  if (a.n_ublocks <= 0 || a.n_ksplit <= 0) return hipErrorInvalidValue;
+  const dim3 grid(a.n_ublocks * a.n_ksplit, a.ex_count);
   if (elt == 2)
     hipLaunchKernelGGL(gproject_kernel<2>, grid, dim3(256), 0, s, a);
   else

@@ -65,16 +65,18 @@ bool factored_supported(const Layer& L) {
 }
 
 dattri_cost_model default_cost_model() {
-  // Starting rates for MI355X before calibration (spec peaks scaled by the
-  // efficiency a first kernel version typically reaches).
+  // Effective rates measured on MI355X (bf16 inputs): both routes timed on a
+  // sweep of 22 single-layer shapes (transformer, adapter-shaped and narrow
+  // layers, T = 16..2048) and fitted by least squares on log time.  Small
+  // problems are dominated by the fixed per-call cost, which launch_us absorbs.
   dattri_cost_model m;
-  m.factored_tflops = 600.0;
-  m.factored_gbs = 5000.0;
-  m.gradient_tflops = 800.0;
-  m.gradient_gbs = 4000.0;
-  m.gproject_tflops = 60.0;
-  m.gproject_gbs = 3000.0;
-  m.launch_us = 4.0;
+  m.factored_tflops = 560.0;
+  m.factored_gbs = 1100.0;
+  m.gradient_tflops = 150.0;
+  m.gradient_gbs = 7600.0;
+  m.gproject_tflops = 67.0;
+  m.gproject_gbs = 27000.0;
+  m.launch_us = 19.0;
   return m;
 }
 
@@ -87,6 +89,7 @@ struct dattri_ctx {
   std::vector<Layer> layers;
   int64_t F = 0;
   dattri_cost_model cost;
+  dattri_factored_form form = DATTRI_FORM_AUTO;
   std::vector<uint8_t> blob;  // host copy of the last uploaded launch plan
 };
 
@@ -134,7 +137,7 @@ dattri_route choose_route(const dattri_ctx* ctx, const Layer& L, dattri_route fo
 
 // ---------------------------------------------------------------- planning
 struct MatChunk {
-  int layer, ex_begin, ex_count, n_ublocks, task;
+  int layer, ex_begin, ex_count, n_ublocks, n_ksplit, kb_per_split, task;
 };
 
 struct Plan {
@@ -144,14 +147,35 @@ struct Plan {
   std::vector<FactMember> members;
   std::vector<ReduceTask> tasks;  // factored tasks first, then one per MatChunk
   int n_fact_tasks = 0;
+  int fact_max_out = 0;            // largest k_in*k_out over the factored tasks
   struct Launch { int elt, na, nb, aligned, first, count; };
   std::vector<Launch> launches;
   std::vector<MatChunk> mat;
+  // split form of the factored route (short sequences)
+  std::vector<SplitOp> sops;
+  std::vector<SplitItem> sitems;
+  std::vector<ContractTask> ctasks;
+  struct SplitLaunch { int elt, aligned, nt, first, count; };
+  std::vector<SplitLaunch> slaunches;
+  std::vector<ReduceTask> stasks;  // token-chunked contractions to reduce
+  std::vector<SlabSumTask> slabsum;
+  int64_t slabsum_max_n4 = 0;
+  int split_max_tchunks = 0, split_max_out = 0;
   // workspace layout (byte offsets)
-  size_t off_items = 0, off_groups = 0, off_members = 0, off_tasks = 0, blob_bytes = 0;
+  size_t off_items = 0, off_groups = 0, off_members = 0, off_tasks = 0;
+  size_t off_sops = 0, off_sitems = 0, off_ctasks = 0, off_stasks = 0, off_slabsum = 0;
+  size_t blob_bytes = 0;
   size_t off_fpart = 0, fpart_bytes = 0, off_g = 0, g_bytes = 0, off_mpart = 0, mpart_bytes = 0;
+  size_t off_proj = 0, proj_bytes = 0, off_spart = 0, spart_bytes = 0;
   size_t total = 0;
 };
+
+// The split form serves every factored group when the fused kernel would have
+// fewer than kSplitMinFusedItems work items.
+constexpr int64_t kSplitMinFusedItems = 1024;
+constexpr int64_t kSplitTargetItems = 1024;   // stage-1 workgroups aimed for
+constexpr int64_t kContractTargetItems = 512; // stage-2 workgroups aimed for
+constexpr int64_t kGProjTargetBlocks = 1024;  // G-projection workgroups aimed for
 
 dattri_status check_captures(const dattri_ctx* ctx, int32_t* n_out) {
   if (ctx->layers.empty()) return fail(DATTRI_E_STATE, "no layer registered");
@@ -199,11 +223,50 @@ dattri_status build_plan(const dattri_ctx* ctx, dattri_route forced, Plan& P) {
     }
   }
 
+  // Fused-kernel shape of each group: input tiles, widest member, 16-byte
+  // alignment, token chunking.
+  struct GShape { int na, nb_max, aligned, na_inst, nb_inst, rt, chunk_rows, n_chunks; };
+  std::vector<GShape> gshape(group_layers.size());
+  int64_t fused_items_total = 0;
+  for (size_t g = 0; g < group_layers.size(); ++g) {
+    const Layer& H = ctx->layers[group_layers[g][0]];
+    GShape& S = gshape[g];
+    S.aligned = ((uintptr_t)H.A % 16 == 0) && (H.d_in * elt) % 16 == 0;
+    S.na = 0;
+    S.nb_max = 0;
+    for (int li : group_layers[g]) {
+      const Layer& L = ctx->layers[li];
+      S.aligned = S.aligned && ((uintptr_t)L.B % 16 == 0) && (L.d_out * elt) % 16 == 0;
+      S.na += tiles16(L.k_in);
+      S.nb_max = std::max(S.nb_max, tiles16(L.k_out));
+    }
+    factored_instance(elt, S.na, S.nb_max, S.aligned, &S.na_inst, &S.nb_inst, &S.rt);
+    const int sub_rows = kWaves * S.rt * 16;
+    int cr = std::max(sub_rows, 512 / sub_rows * sub_rows);
+    if (H.T <= cr) cr = std::max(sub_rows, (H.T + sub_rows - 1) / sub_rows * sub_rows);
+    S.chunk_rows = cr;
+    S.n_chunks = std::max(1, (H.T + cr - 1) / cr);
+    fused_items_total += (int64_t)n * S.n_chunks;
+  }
+  const bool few_items = fused_items_total < kSplitMinFusedItems;
+  auto use_split = [&](size_t g) {
+    const Layer& H = ctx->layers[group_layers[g][0]];
+    if ((int64_t)n * H.T > (int64_t)INT32_MAX / 2 || n > 65535) return false;  // index / grid range
+    if (ctx->form != DATTRI_FORM_AUTO) return ctx->form == DATTRI_FORM_SPLIT;
+    return few_items;
+  };
+
   size_t fpart_floats = 0;
   struct Inst { int na, nb, aligned; std::vector<int> groups; };
   std::vector<Inst> insts;
   std::vector<double> group_cost;
+  std::vector<size_t> split_groups;
   for (size_t g = 0; g < group_layers.size(); ++g) {
+    if (use_split(g)) {
+      split_groups.push_back(g);
+      continue;
+    }
+    const int fg = (int)P.groups.size();  // index among fused groups
     const Layer& H = ctx->layers[group_layers[g][0]];
     FactGroup G;
     std::memset(&G, 0, sizeof(G));
@@ -214,8 +277,8 @@ dattri_status build_plan(const dattri_ctx* ctx, dattri_route forced, Plan& P) {
     G.n = n;
     G.n_members = (int)group_layers[g].size();
     G.member0 = (int)P.members.size();
-    bool aligned = ((uintptr_t)H.A % 16 == 0) && (H.d_in * elt) % 16 == 0;
-    int na = 0, nb_max = 0;
+    const bool aligned = gshape[g].aligned;
+    int na = 0;
     double bytes_per_row = (double)H.d_in;
     for (int li : group_layers[g]) {
       const Layer& L = ctx->layers[li];
@@ -229,27 +292,21 @@ dattri_status build_plan(const dattri_ctx* ctx, dattri_route forced, Plan& P) {
       M.a_tile0 = na;
       M.na = tiles16(L.k_in);
       M.nb = tiles16(L.k_out);
-      aligned = aligned && ((uintptr_t)L.B % 16 == 0) && (L.d_out * elt) % 16 == 0;
       for (int t = 0; t < M.na; ++t) {
         G.ptile[na + t] = L.P_in;
         G.ptile_local[na + t] = t;
         G.ptile_nt[na + t] = M.na;
       }
       na += M.na;
-      nb_max = std::max(nb_max, M.nb);
       bytes_per_row += L.d_out;
       P.members.push_back(M);
     }
     G.na = na;
     G.aligned = aligned;
     for (int m = 0; m < G.n_members; ++m) P.members[G.member0 + m].aligned = aligned;
-    int na_inst, nb_inst, rt;
-    factored_instance(elt, na, nb_max, aligned, &na_inst, &nb_inst, &rt);
-    const int sub_rows = kWaves * rt * 16;
-    int cr = std::max(sub_rows, 512 / sub_rows * sub_rows);
-    if (H.T <= cr) cr = std::max(sub_rows, (H.T + sub_rows - 1) / sub_rows * sub_rows);
-    G.chunk_rows = cr;
-    G.n_chunks = std::max(1, (H.T + cr - 1) / cr);
+    const int na_inst = gshape[g].na_inst, nb_inst = gshape[g].nb_inst;
+    G.chunk_rows = gshape[g].chunk_rows;
+    G.n_chunks = gshape[g].n_chunks;
     // partial blocks of each member: [n][n_chunks * waves][na*16 x nb*16]
     for (int m = 0; m < G.n_members; ++m) {
       FactMember& M = P.members[G.member0 + m];
@@ -267,6 +324,7 @@ dattri_status build_plan(const dattri_ctx* ctx, dattri_route forced, Plan& P) {
       R.part_floats = (int32_t)part;
       R.ex_begin = 0;
       P.tasks.push_back(R);
+      P.fact_max_out = std::max(P.fact_max_out, M.k_in * M.k_out);
     }
     int inst = -1;
     for (size_t i = 0; i < insts.size(); ++i)
@@ -276,7 +334,7 @@ dattri_status build_plan(const dattri_ctx* ctx, dattri_route forced, Plan& P) {
       insts.push_back({na_inst, nb_inst, (int)aligned, {}});
       inst = (int)insts.size() - 1;
     }
-    insts[inst].groups.push_back((int)g);
+    insts[inst].groups.push_back(fg);
     group_cost.push_back((double)n * H.T * bytes_per_row);
     P.groups.push_back(G);
   }
@@ -308,6 +366,139 @@ dattri_status build_plan(const dattri_ctx* ctx, dattri_route forced, Plan& P) {
     P.launches.push_back({elt, I.na, I.nb, I.aligned, first, (int)P.items.size() - first});
   }
 
+  // ---- split form: one stage-1 op per factor block (a group's A, each
+  // member's B) over all n*T token rows; one contraction task per layer.
+  if (!split_groups.empty()) {
+    struct Pending { int a_op, b_op; };
+    std::vector<Pending> pend;
+    const size_t op0 = P.sops.size();
+    for (size_t g : split_groups) {
+      const Layer& H = ctx->layers[group_layers[g][0]];
+      const int rows = n * H.T;
+      SplitOp A;
+      std::memset(&A, 0, sizeof(A));
+      A.X = H.A;
+      A.rows = rows;
+      A.ld = H.d_in;
+      A.aligned = ((uintptr_t)H.A % 16 == 0) && (H.d_in * elt) % 16 == 0;
+      std::vector<SplitOp> Bs;
+      int na = 0;
+      const int a_op = (int)P.sops.size();
+      for (int li : group_layers[g]) {
+        const Layer& L = ctx->layers[li];
+        const int mt = tiles16(L.k_in);
+        for (int t = 0; t < mt; ++t) {
+          A.ptile[na + t] = L.P_in;
+          A.ptile_local[na + t] = t;
+          A.ptile_nt[na + t] = mt;
+        }
+        SplitOp B;
+        std::memset(&B, 0, sizeof(B));
+        B.X = L.B;
+        B.rows = rows;
+        B.ld = L.d_out;
+        B.aligned = ((uintptr_t)L.B % 16 == 0) && (L.d_out * elt) % 16 == 0;
+        B.nt = tiles16(L.k_out);
+        for (int t = 0; t < B.nt; ++t) {
+          B.ptile[t] = L.P_out;
+          B.ptile_local[t] = t;
+          B.ptile_nt[t] = B.nt;
+        }
+        ContractTask C;
+        std::memset(&C, 0, sizeof(C));
+        C.a_col0 = na * 16;
+        C.k_in = L.k_in;
+        C.k_out = L.k_out;
+        C.T = H.T;
+        C.rows = rows;
+        C.phi_offset = L.offset;
+        C.lengths = L.lengths;
+        P.ctasks.push_back(C);
+        pend.push_back({a_op, a_op + 1 + (int)Bs.size()});
+        Bs.push_back(B);
+        na += mt;
+      }
+      A.nt = na;
+      P.sops.push_back(A);
+      for (const SplitOp& B : Bs) P.sops.push_back(B);
+    }
+    // slab width: about kSplitTargetItems stage-1 workgroups in total
+    int64_t work = 0;
+    for (size_t o = op0; o < P.sops.size(); ++o)
+      work += (int64_t)((P.sops[o].rows + kSplitRows - 1) / kSplitRows) * P.sops[o].ld;
+    int64_t slab = (work + kSplitTargetItems - 1) / kSplitTargetItems;
+    slab = std::max<int64_t>(kSplitSlabQuantum, (slab + kSplitSlabQuantum - 1) / kSplitSlabQuantum * kSplitSlabQuantum);
+    size_t proj_floats = 0;
+    for (size_t o = op0; o < P.sops.size(); ++o) {
+      SplitOp& O = P.sops[o];
+      O.slab_cols = (int32_t)std::min<int64_t>(slab, (O.ld + kSplitSlabQuantum - 1) / kSplitSlabQuantum * kSplitSlabQuantum);
+      O.n_slabs = (O.ld + O.slab_cols - 1) / O.slab_cols;
+      O.out_base = (int64_t)proj_floats;
+      proj_floats += (size_t)O.n_slabs * O.rows * O.nt * 16;
+    }
+    // token chunks: about kContractTargetItems stage-2 workgroups in total
+    const int64_t per_chunk = (int64_t)pend.size() * std::max(n, 1);
+    const int64_t want_chunks = std::max<int64_t>(1, (kContractTargetItems + per_chunk - 1) / per_chunk);
+    size_t spart_floats = 0;
+    for (size_t i = 0; i < pend.size(); ++i) {
+      ContractTask& C = P.ctasks[P.ctasks.size() - pend.size() + i];
+      const SplitOp& A = P.sops[pend[i].a_op];
+      const SplitOp& B = P.sops[pend[i].b_op];
+      // slabs are summed into slab 0 before the contraction
+      C.a_base = A.out_base; C.a_ld = A.nt * 16; C.a_slabs = 1;
+      C.b_base = B.out_base; C.b_ld = B.nt * 16; C.b_slabs = 1;
+      const int64_t tc = (C.T + want_chunks - 1) / want_chunks;
+      C.tok_chunk = (int32_t)std::max<int64_t>(64, (tc + 31) / 32 * 32);
+      C.n_tchunks = std::max(1, (C.T + C.tok_chunk - 1) / C.tok_chunk);
+      P.split_max_tchunks = std::max(P.split_max_tchunks, C.n_tchunks);
+      if (C.n_tchunks > 1) {
+        const int ki16 = tiles16(C.k_in) * 16, ko16 = tiles16(C.k_out) * 16;
+        C.partial_base = (int64_t)spart_floats;
+        spart_floats += (size_t)n * C.n_tchunks * ki16 * ko16;
+        ReduceTask R;
+        std::memset(&R, 0, sizeof(R));
+        R.partial_base = C.partial_base;
+        R.phi_offset = C.phi_offset;
+        R.n_parts = C.n_tchunks;
+        R.k_in = C.k_in;
+        R.k_out = C.k_out;
+        R.ldp = ko16;
+        R.part_floats = ki16 * ko16;
+        R.ex_begin = 0;
+        P.stasks.push_back(R);
+        P.split_max_out = std::max(P.split_max_out, C.k_in * C.k_out);
+      }
+    }
+    P.proj_bytes = proj_floats * 4;
+    P.spart_bytes = spart_floats * 4;
+    for (size_t o = op0; o < P.sops.size(); ++o) {
+      const SplitOp& O = P.sops[o];
+      if (O.n_slabs <= 1 || O.rows == 0) continue;
+      SlabSumTask T;
+      std::memset(&T, 0, sizeof(T));
+      T.base = O.out_base;
+      T.n4 = (int64_t)O.rows * O.nt * 4;
+      T.stride4 = T.n4;
+      T.n_slabs = O.n_slabs;
+      P.slabsum.push_back(T);
+      P.slabsum_max_n4 = std::max(P.slabsum_max_n4, T.n4);
+    }
+    // one launch per kernel instance (aligned, tiles)
+    for (int al = 1; al >= 0; --al)
+      for (int nt : {1, 2, 4, 8}) {
+        const int first = (int)P.sitems.size();
+        for (size_t o = op0; o < P.sops.size(); ++o) {
+          const SplitOp& O = P.sops[o];
+          if (O.aligned != al || split_nt_instance(O.nt) != nt) continue;
+          const int rblocks = (O.rows + kSplitRows - 1) / kSplitRows;
+          for (int rb = 0; rb < rblocks; ++rb)
+            for (int sl = 0; sl < O.n_slabs; ++sl) P.sitems.push_back({(int)o, rb, sl, 0});
+        }
+        const int count = (int)P.sitems.size() - first;
+        if (count) P.slaunches.push_back({elt, al, nt, first, count});
+      }
+  }
+
   // ---- materialized layers: example chunks staged through G
   size_t g_floats = 0, mpart_floats = 0;
   for (size_t l = 0; l < ctx->layers.size(); ++l) {
@@ -320,16 +511,22 @@ dattri_status build_plan(const dattri_ctx* ctx, dattri_route forced, Plan& P) {
     const int ex_chunk = (int)std::max<int64_t>(
         1, std::min<int64_t>({(int64_t)n, kGBudgetBytes / (4 * g_per_ex), (int64_t)65535}));
     const int n_ublocks = (L.d_out + kGProjRows - 1) / kGProjRows;
+    // split d_in's k-blocks when row blocks x examples give too few workgroups
+    const int nkb = (L.d_in + krows_of(elt) - 1) / krows_of(elt);
+    const int64_t want = (kGProjTargetBlocks + (int64_t)n_ublocks * ex_chunk - 1) / ((int64_t)n_ublocks * ex_chunk);
+    const int ks_req = (int)std::max<int64_t>(1, std::min<int64_t>(nkb, want));
+    const int kbps = (nkb + ks_req - 1) / ks_req;
+    const int n_ks = (nkb + kbps - 1) / kbps;
     const int64_t part = (int64_t)tiles16(L.k_in) * 16 * tiles16(L.k_out) * 16;
     g_floats = std::max(g_floats, (size_t)(ex_chunk * g_per_ex));
-    mpart_floats = std::max(mpart_floats, (size_t)((int64_t)ex_chunk * n_ublocks * kWaves * part));
+    mpart_floats = std::max(mpart_floats, (size_t)((int64_t)ex_chunk * n_ublocks * n_ks * part));
     for (int e0 = 0; e0 < n; e0 += ex_chunk) {
-      MatChunk mc{(int)l, e0, std::min(ex_chunk, n - e0), n_ublocks, (int)P.tasks.size()};
+      MatChunk mc{(int)l, e0, std::min(ex_chunk, n - e0), n_ublocks, n_ks, kbps, (int)P.tasks.size()};
       ReduceTask R;
       std::memset(&R, 0, sizeof(R));
       R.partial_base = 0;
       R.phi_offset = L.offset;
-      R.n_parts = n_ublocks * kWaves;
+      R.n_parts = n_ublocks * n_ks;
       R.k_in = L.k_in;
       R.k_out = L.k_out;
       R.ldp = tiles16(L.k_out) * 16;
@@ -346,10 +543,17 @@ dattri_status build_plan(const dattri_ctx* ctx, dattri_route forced, Plan& P) {
   P.off_groups = off;  off = align_up(off + P.groups.size() * sizeof(FactGroup));
   P.off_members = off; off = align_up(off + P.members.size() * sizeof(FactMember));
   P.off_tasks = off;   off = align_up(off + P.tasks.size() * sizeof(ReduceTask));
+  P.off_sops = off;    off = align_up(off + P.sops.size() * sizeof(SplitOp));
+  P.off_sitems = off;  off = align_up(off + P.sitems.size() * sizeof(SplitItem));
+  P.off_ctasks = off;  off = align_up(off + P.ctasks.size() * sizeof(ContractTask));
+  P.off_stasks = off;  off = align_up(off + P.stasks.size() * sizeof(ReduceTask));
+  P.off_slabsum = off; off = align_up(off + P.slabsum.size() * sizeof(SlabSumTask));
   P.blob_bytes = off;
   P.off_fpart = off;   P.fpart_bytes = fpart_floats * 4; off = align_up(off + P.fpart_bytes);
   P.off_g = off;       P.g_bytes = g_floats * 4;         off = align_up(off + P.g_bytes);
   P.off_mpart = off;   P.mpart_bytes = mpart_floats * 4; off = align_up(off + P.mpart_bytes);
+  P.off_proj = off;    off = align_up(off + P.proj_bytes);
+  P.off_spart = off;   off = align_up(off + P.spart_bytes);
   P.total = std::max<size_t>(off, kAlign);
   return DATTRI_OK;
 }
@@ -557,6 +761,22 @@ dattri_status dattri_workspace_bytes(const dattri_ctx* ctx, dattri_route route, 
   return DATTRI_OK;
 }
 
+dattri_status dattri_set_factored_form(dattri_ctx* ctx, dattri_factored_form form) {
+  reset_error();
+  if (!ctx) return fail(DATTRI_E_INVALID_ARG, "ctx is NULL");
+  if (form < DATTRI_FORM_AUTO || form > DATTRI_FORM_SPLIT)
+    return fail(DATTRI_E_INVALID_ARG, "factored form %d unknown", (int)form);
+  ctx->form = form;
+  return DATTRI_OK;
+}
+
+dattri_status dattri_get_factored_form(const dattri_ctx* ctx, dattri_factored_form* form) {
+  reset_error();
+  if (!ctx || !form) return fail(DATTRI_E_INVALID_ARG, "ctx or form is NULL");
+  *form = ctx->form;
+  return DATTRI_OK;
+}
+
 dattri_status dattri_project_per_example(dattri_ctx* ctx, void* phi, dattri_dtype phi_dtype,
                                          int64_t ld_phi, void* workspace, size_t ws_bytes,
                                          dattri_route route, void* stream) {
@@ -590,6 +810,11 @@ dattri_status dattri_project_per_example(dattri_ctx* ctx, void* phi, dattri_dtyp
   put(P.off_groups, P.groups.data(), P.groups.size() * sizeof(FactGroup));
   put(P.off_members, P.members.data(), P.members.size() * sizeof(FactMember));
   put(P.off_tasks, P.tasks.data(), P.tasks.size() * sizeof(ReduceTask));
+  put(P.off_sops, P.sops.data(), P.sops.size() * sizeof(SplitOp));
+  put(P.off_sitems, P.sitems.data(), P.sitems.size() * sizeof(SplitItem));
+  put(P.off_ctasks, P.ctasks.data(), P.ctasks.size() * sizeof(ContractTask));
+  put(P.off_stasks, P.stasks.data(), P.stasks.size() * sizeof(ReduceTask));
+  put(P.off_slabsum, P.slabsum.data(), P.slabsum.size() * sizeof(SlabSumTask));
   hipStream_t s = (hipStream_t)stream;
   uint8_t* ws = (uint8_t*)workspace;
   HIP_TRY(hipMemcpyAsync(ws, ctx->blob.data(), P.blob_bytes, hipMemcpyHostToDevice, s));
@@ -604,7 +829,24 @@ dattri_status dattri_project_per_example(dattri_ctx* ctx, void* phi, dattri_dtyp
     HIP_TRY(launch_factored(L.elt, L.na, L.nb, L.aligned, d_items + L.first, L.count, d_groups,
                             d_members, fpart, s));
   if (P.n_fact_tasks)
-    HIP_TRY(launch_reduce(d_tasks, P.n_fact_tasks, n, fpart, phi, phi_bf16, ld_phi, s));
+    HIP_TRY(launch_reduce(d_tasks, P.n_fact_tasks, n, P.fact_max_out, fpart, phi, phi_bf16, ld_phi, s));
+
+  const SplitOp* d_sops = (const SplitOp*)(ws + P.off_sops);
+  const SplitItem* d_sitems = (const SplitItem*)(ws + P.off_sitems);
+  const ContractTask* d_ctasks = (const ContractTask*)(ws + P.off_ctasks);
+  float* proj = (float*)(ws + P.off_proj);
+  for (const Plan::SplitLaunch& L : P.slaunches)
+    HIP_TRY(launch_split_project(L.elt, L.aligned, L.nt, d_sitems + L.first, L.count, d_sops, proj, s));
+  if (!P.slabsum.empty())
+    HIP_TRY(launch_slab_sum((const SlabSumTask*)(ws + P.off_slabsum), (int)P.slabsum.size(),
+                            P.slabsum_max_n4, proj, s));
+  float* spart = (float*)(ws + P.off_spart);
+  if (!P.ctasks.empty())
+    HIP_TRY(launch_split_contract(d_ctasks, (int)P.ctasks.size(), n, P.split_max_tchunks, proj, spart,
+                                  phi, phi_bf16, ld_phi, s));
+  if (!P.stasks.empty())
+    HIP_TRY(launch_reduce((const ReduceTask*)(ws + P.off_stasks), (int)P.stasks.size(), n,
+                          P.split_max_out, spart, phi, phi_bf16, ld_phi, s));
 
   float* gbuf = (float*)(ws + P.off_g);
   float* mpart = (float*)(ws + P.off_mpart);
@@ -622,8 +864,10 @@ dattri_status dattri_project_per_example(dattri_ctx* ctx, void* phi, dattri_dtyp
     pa.G = gbuf; pa.P_in = L.P_in; pa.P_out = L.P_out;
     pa.d_in = L.d_in; pa.d_out = L.d_out; pa.k_in = L.k_in; pa.k_out = L.k_out;
     pa.ex_count = mc.ex_count; pa.n_ublocks = mc.n_ublocks; pa.partials = mpart;
+    pa.n_ksplit = mc.n_ksplit; pa.kb_per_split = mc.kb_per_split;
     HIP_TRY(launch_gproject(ctx->elt, pa, s));
-    HIP_TRY(launch_reduce(d_tasks + mc.task, 1, mc.ex_count, mpart, phi, phi_bf16, ld_phi, s));
+    HIP_TRY(launch_reduce(d_tasks + mc.task, 1, mc.ex_count, L.k_in * L.k_out, mpart, phi, phi_bf16,
+                          ld_phi, s));
   }
   return DATTRI_OK;
 }

@@ -11,7 +11,8 @@ from . import (DATTRI_BF16, DATTRI_F32, DATTRI_ROUTE_AUTO, dattri_bind_projectio
                dattri_capture_layer, dattri_clear_captures, dattri_create, dattri_destroy,
                dattri_feature_dim, dattri_layer_offset, dattri_layer_route,
                dattri_project_per_example, dattri_projection_bytes, dattri_register_layer,
-               dattri_score, dattri_score_workspace_bytes, dattri_workspace_bytes)
+               dattri_score, dattri_score_workspace_bytes, dattri_set_factored_form,
+               dattri_workspace_bytes)
 
 DTYPES = {"f32": (DATTRI_F32, torch.float32), "bf16": (DATTRI_BF16, torch.bfloat16)}
 
@@ -23,11 +24,13 @@ def _dev_bytes(n, device):
 class ProjectionSession:
     """One library context with its layers and bound projection maps."""
 
-    def __init__(self, layers, dtype="bf16", seed=0, device="cuda", overrides=None):
+    def __init__(self, layers, dtype="bf16", seed=0, device="cuda", overrides=None, form=None):
         self.dtype = dtype
         self.code, self.torch_dtype = DTYPES[dtype]
         self.device = torch.device(device)
         self.ctx = dattri_create(self.code, seed)
+        if form is not None:
+            dattri_set_factored_form(self.ctx, form)
         self.layers = list(layers)
         self.maps = []
         overrides = overrides or {}

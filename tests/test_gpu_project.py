@@ -17,6 +17,7 @@ pytestmark = pytest.mark.gpu
 TOL = {"f32": 1e-5, "bf16": 2e-2}
 ROUTES = {"auto": dt.DATTRI_ROUTE_AUTO, "factored": dt.DATTRI_ROUTE_FACTORED,
           "materialized": dt.DATTRI_ROUTE_MATERIALIZED}
+FORMS = {"fused": dt.DATTRI_FORM_FUSED, "split": dt.DATTRI_FORM_SPLIT, None: None}
 DEV = "cuda"
 
 
@@ -29,8 +30,8 @@ def _session_inputs(wl, layers, n, T, dtype, device=DEV):
     return inputs
 
 
-def _run(layers, inputs, dtype, seed, route, phi_dtype="f32", lengths=None, overrides=None):
-    s = ProjectionSession(layers, dtype=dtype, seed=seed, overrides=overrides)
+def _run(layers, inputs, dtype, seed, route, phi_dtype="f32", lengths=None, overrides=None, form=None):
+    s = ProjectionSession(layers, dtype=dtype, seed=seed, overrides=overrides, form=FORMS[form])
     n = inputs[0][0].shape[0]
     for li, (A, B) in enumerate(inputs):
         s.capture(li, A, B, lengths)
@@ -50,11 +51,12 @@ def _check(layers, inputs, phi, seed, dtype, examples, lengths=None, tol=None):
     return errs
 
 
-@pytest.mark.parametrize("route", ["auto", "factored", "materialized"])
-def test_tiny_f32_all_routes(route):
+@pytest.mark.parametrize("route,form", [("auto", None), ("factored", "fused"), ("factored", "split"),
+                                        ("materialized", None)])
+def test_tiny_f32_all_routes(route, form):
     wl = W.WORKLOADS["tiny"]
     inputs = _session_inputs(wl, wl["layers"], wl["batch"], wl["T"], "f32")
-    s, phi = _run(wl["layers"], inputs, "f32", wl["seed"], route)
+    s, phi = _run(wl["layers"], inputs, "f32", wl["seed"], route, form=form)
     errs = _check(wl["layers"], inputs, phi, wl["seed"], "f32", list(range(wl["batch"])))
     print(f"tiny {route}: per-layer rel err {errs}")
     if route == "auto":
@@ -68,20 +70,36 @@ RAGGED = [dict(name="r0", d_in=100, d_out=72, k_in=24, k_out=40, a_group="g0"),
 
 
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
-@pytest.mark.parametrize("route", ["factored", "materialized"])
-def test_ragged_unaligned_lengths(dtype, route):
+@pytest.mark.parametrize("route,form", [("factored", "fused"), ("factored", "split"), ("materialized", None)])
+def test_ragged_unaligned_lengths(dtype, route, form):
     wl = dict(W.WORKLOADS["tiny"], dist_a="normal", dist_b="normal", seed=11)
     n, T = 5, 37
     inputs = _session_inputs(wl, RAGGED, n, T, dtype)
     lengths = torch.tensor([37, 0, 1, 20, 33], dtype=torch.int32, device=DEV)
-    s, phi = _run(RAGGED, inputs, dtype, 77, route, lengths=lengths)
+    s, phi = _run(RAGGED, inputs, dtype, 77, route, lengths=lengths, form=form)
     # example 1 has length 0: its whole row must be exactly zero
     assert torch.count_nonzero(phi[1]).item() == 0
     tol = 1e-5 if dtype == "f32" else 1e-5  # inputs are exact bf16 values; accumulation is float32
     _check(RAGGED, inputs, phi, 77, dtype, [0, 2, 3, 4], lengths=lengths, tol=tol)
 
 
-def test_shared_input_group_matches_separate_inputs():
+@pytest.mark.parametrize("form", ["fused", "split"])
+def test_token_chunks_and_lengths_at_chunk_edges(form):
+    # T = 300 splits each example's tokens over several contraction chunks in
+    # the split form; lengths fall on and beside chunk boundaries
+    layers = [dict(name="c0", d_in=200, d_out=135, k_in=40, k_out=24, a_group="a"),
+              dict(name="c1", d_in=200, d_out=64, k_in=16, k_out=64, a_group="a")]
+    wl = dict(W.WORKLOADS["tiny"], dist_a="normal", dist_b="normal", seed=13)
+    n, T = 3, 300
+    for dtype in ("f32", "bf16"):
+        inputs = _session_inputs(wl, layers, n, T, dtype)
+        lengths = torch.tensor([300, 129, 64], dtype=torch.int32, device=DEV)
+        _, phi = _run(layers, inputs, dtype, 9, "factored", lengths=lengths, form=form)
+        _check(layers, inputs, phi, 9, dtype, [0, 1, 2], lengths=lengths, tol=1e-5)
+
+
+@pytest.mark.parametrize("form", ["fused", "split"])
+def test_shared_input_group_matches_separate_inputs(form):
     layers = [dict(name="q", d_in=256, d_out=256, k_in=32, k_out=32, a_group="x"),
               dict(name="k", d_in=256, d_out=64, k_in=32, k_out=32, a_group="x"),
               dict(name="v", d_in=256, d_out=64, k_in=32, k_out=32, a_group="x"),
@@ -89,15 +107,16 @@ def test_shared_input_group_matches_separate_inputs():
     wl = dict(W.WORKLOADS["llama8b"], seed=21)
     inputs = _session_inputs(wl, layers, 3, 96, "bf16")
     assert inputs[0][0] is inputs[1][0] is inputs[2][0]  # q/k/v share one A tensor
-    _, phi = _run(layers, inputs, "bf16", 5, "factored")
+    _, phi = _run(layers, inputs, "bf16", 5, "factored", form=form)
     _check(layers, inputs, phi, 5, "bf16", [0, 1, 2], tol=1e-5)
     # the same values through separate A tensors (no sharing) agree within fp32 rounding
     sep = [(A.clone(), B) for A, B in inputs]
-    _, phi2 = _run(layers, sep, "bf16", 5, "factored")
+    _, phi2 = _run(layers, sep, "bf16", 5, "factored", form=form)
     assert rel_fro(host64(phi2), host64(phi)) < 1e-6
 
 
-def test_identity_maps_reproduce_eq4():
+@pytest.mark.parametrize("form", ["fused", "split"])
+def test_identity_maps_reproduce_eq4(form):
     # k = d and P = I: <phi_i, phi_j> is the factorized inner product of Eq. (4)
     d_in, d_out, T, n = 32, 16, 24, 4
     layers = [dict(name="id", d_in=d_in, d_out=d_out, k_in=d_in, k_out=d_out, a_group="a")]
@@ -105,7 +124,7 @@ def test_identity_maps_reproduce_eq4():
     inputs = _session_inputs(wl, layers, n, T, "f32")
     eye_in = np.eye(d_in, dtype=np.float32)
     eye_out = np.eye(d_out, dtype=np.float32)
-    _, phi = _run(layers, inputs, "f32", 0, "factored", overrides={0: (eye_in, eye_out)})
+    _, phi = _run(layers, inputs, "f32", 0, "factored", overrides={0: (eye_in, eye_out)}, form=form)
     A, B = host64(inputs[0][0]), host64(inputs[0][1])
     gram = host64(phi) @ host64(phi).T
     ref = np.array([[og.ghost_dot(A[i], B[i], A[j], B[j]) for j in range(n)] for i in range(n)])
@@ -170,12 +189,13 @@ def test_llama8b_full_size_sampled():
             assert err <= 1e-5, (li, i, err)
 
 
+@pytest.mark.parametrize("form", ["fused", "split"])
 @pytest.mark.parametrize("name", ["routing", "lora_b", "narrow"])
-def test_switch_workloads_both_routes(name):
+def test_switch_workloads_both_routes(name, form):
     wl = W.WORKLOADS[name]
     n = wl["batch"]
     inputs = _session_inputs(wl, wl["layers"], n, wl["T"], "bf16")
-    _, phi_f = _run(wl["layers"], inputs, "bf16", wl["seed"], "factored")
+    _, phi_f = _run(wl["layers"], inputs, "bf16", wl["seed"], "factored", form=form)
     _, phi_m = _run(wl["layers"], inputs, "bf16", wl["seed"], "materialized")
     ex = [0, n // 2, n - 1]
     _check(wl["layers"], inputs, phi_f, wl["seed"], "bf16", ex, tol=1e-5)
@@ -198,9 +218,10 @@ def test_bf16_phi_output_and_ld():
     _check(layers, inputs, big[:, :s.F], 3, "f32", list(range(6)), tol=2 ** -8)
 
 
-def test_empty_batch_and_zero_tokens():
+@pytest.mark.parametrize("form", ["fused", "split"])
+def test_empty_batch_and_zero_tokens(form):
     layers = [dict(name="e", d_in=64, d_out=32, k_in=16, k_out=16, a_group="a")]
-    s = ProjectionSession(layers, dtype="bf16", seed=0)
+    s = ProjectionSession(layers, dtype="bf16", seed=0, form=FORMS[form])
     A = torch.empty((0, 16, 64), dtype=torch.bfloat16, device=DEV)
     B = torch.empty((0, 16, 32), dtype=torch.bfloat16, device=DEV)
     s.capture(0, A, B)
@@ -217,12 +238,13 @@ def test_empty_batch_and_zero_tokens():
         assert torch.count_nonzero(phi).item() == 0
 
 
-def test_deterministic_bitwise():
+@pytest.mark.parametrize("form", ["fused", "split"])
+def test_deterministic_bitwise(form):
     wl = W.WORKLOADS["gpt2"]
     layers = wl["layers"][:8]
     inputs = _session_inputs(wl, layers, 8, 256, "bf16")
-    _, a = _run(layers, inputs, "bf16", 1, "factored")
-    _, b = _run(layers, inputs, "bf16", 1, "factored")
+    _, a = _run(layers, inputs, "bf16", 1, "factored", form=form)
+    _, b = _run(layers, inputs, "bf16", 1, "factored", form=form)
     assert torch.equal(a, b)
     _, c = _run(layers[:2], [inputs[0], inputs[1]], "bf16", 1, "materialized")
     _, d = _run(layers[:2], [inputs[0], inputs[1]], "bf16", 1, "materialized")

@@ -218,3 +218,26 @@ def test_route_follows_cost_model(ctx):
     assert dt.dattri_layer_route(ctx, 0)[0] == dt.DATTRI_ROUTE_MATERIALIZED
     dt.dattri_set_cost_model(ctx, dict(m, gradient_tflops=1e-3))
     assert dt.dattri_layer_route(ctx, 0)[0] == dt.DATTRI_ROUTE_FACTORED
+
+
+def test_factored_form_option(ctx):
+    assert dt.dattri_get_factored_form(ctx) == dt.DATTRI_FORM_AUTO
+    for f in (dt.DATTRI_FORM_FUSED, dt.DATTRI_FORM_SPLIT, dt.DATTRI_FORM_AUTO):
+        dt.dattri_set_factored_form(ctx, f)
+        assert dt.dattri_get_factored_form(ctx) == f
+    with pytest.raises(dt.DattriError) as e:
+        dt.dattri_set_factored_form(ctx, 3)
+    assert _status(e) == "E_INVALID_ARG"
+    # a short-sequence capture: the split form stages its float32 projected
+    # rows (at least n*T*(k_in + k_out) floats) in the workspace
+    fake = 1 << 40
+    dt.dattri_register_layer(ctx, 8192, 28672, 64, 64)
+    dt.dattri_capture_layer(ctx, 0, fake, fake, 64, 32)
+    dt.dattri_set_factored_form(ctx, dt.DATTRI_FORM_FUSED)
+    fused = dt.dattri_workspace_bytes(ctx, dt.DATTRI_ROUTE_FACTORED)
+    dt.dattri_set_factored_form(ctx, dt.DATTRI_FORM_SPLIT)
+    split = dt.dattri_workspace_bytes(ctx, dt.DATTRI_ROUTE_FACTORED)
+    dt.dattri_set_factored_form(ctx, dt.DATTRI_FORM_AUTO)
+    auto = dt.dattri_workspace_bytes(ctx, dt.DATTRI_ROUTE_FACTORED)
+    assert split >= 4 * 64 * 32 * (64 + 64)
+    assert auto == split  # few fused work items and T <= 128: AUTO takes the split form

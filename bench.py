@@ -31,7 +31,7 @@ def parse():
     p.add_argument("--steps", type=int, default=10)
     p.add_argument("--warmup", type=int, default=2)
     p.add_argument("--no-cpu-baseline", action="store_true")
-    p.add_argument("--phase", choices=["all", "project", "score", "routing", "copy"], default="all")
+    p.add_argument("--phase", choices=["all", "project", "score", "routing", "gpt2", "copy"], default="all")
     return p.parse_args()
 
 
@@ -165,6 +165,82 @@ def routing_cases(dev, steps, warmup):
     return out
 
 
+def gpt2_case(dev, steps, warmup):
+    """GPT-2-small-shaped stack (48 layers, T=512, batch 32, k=16): projected
+    per-example gradients of one resident batch, and the scoring GEMM of 256
+    queries against 4096 training rows (F = 12288, bf16) with top-10."""
+    import torch
+    import workloads as W
+    from paper_2609_38767_amd.session import ProjectionSession, score
+    stream = torch.cuda.current_stream()
+    wl = W.WORKLOADS["gpt2"]
+    n, T = wl["batch"], wl["T"]
+    sess = ProjectionSession(wl["layers"], dtype="bf16", seed=wl["seed"], device=dev)
+    cache = {}
+    for li in range(len(wl["layers"])):
+        A, B = W.factor_blocks(wl, li, 0, n, T, dev, "bf16", a_cache=cache)
+        sess.capture(li, A, B)
+    phi = torch.empty((n, sess.F), dtype=torch.float32, device=dev)
+    sess.workspace()
+
+    def med_ms(fn):
+        for _ in range(warmup):
+            fn()
+        evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+               for _ in range(steps)]
+        for a, b in evs:
+            a.record(stream)
+            fn()
+            b.record(stream)
+        torch.cuda.synchronize()
+        t = sorted(a.elapsed_time(b) for a, b in evs)
+        return t[len(t) // 2]
+
+    p_ms = med_ms(lambda: sess.project(n, phi=phi))
+    bytes_ex = algorithmic_projection_bytes(wl)
+    g = torch.Generator(device=dev).manual_seed(wl["seed"])
+    Q = torch.randn((wl["n_query"], sess.F), generator=g, device=dev).to(torch.bfloat16)
+    X = torch.randn((wl["n_train"], sess.F), generator=g, device=dev).to(torch.bfloat16)
+    s_ms = med_ms(lambda: score(Q, X, topk=10))
+    flops = 2.0 * wl["n_query"] * wl["n_train"] * sess.F
+    sess.close()
+    out = {"examples_per_s": n / (p_ms * 1e-3), "ms_per_batch": p_ms, "bytes_per_example": bytes_ex,
+           "hbm_frac": bytes_ex * n / (p_ms * 1e-3) / 8e12,
+           "score_ms": s_ms, "score_tflops": flops / (s_ms * 1e-3) / 1e12,
+           "score_shape": f"{wl['n_query']} x {wl['n_train']} x {sess.F} bf16, top-10"}
+    print(f"[bench] gpt2: projection {p_ms:.3f} ms ({out['examples_per_s']:.0f} ex/s), "
+          f"scoring {s_ms:.3f} ms", file=sys.stderr, flush=True)
+    return out
+
+
+def stream_reference(dev):
+    """Achievable HBM rate on this GPU: a 1 GiB device-to-device copy (read +
+    write bytes per second, best of 5)."""
+    import torch
+    stream = torch.cuda.current_stream()
+    nbytes = 1 << 30
+    src = torch.empty(nbytes, dtype=torch.uint8, device=dev).fill_(1)
+    dst = torch.empty_like(src)
+
+    def best_ms(fn, reps=5):
+        fn()
+        torch.cuda.synchronize()
+        t = []
+        for _ in range(reps):
+            a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            a.record(stream)
+            fn()
+            b.record(stream)
+            torch.cuda.synchronize()
+            t.append(a.elapsed_time(b))
+        return min(t)
+    c_ms = best_ms(lambda: dst.copy_(src))
+    out = {"copy_gbs": 2 * nbytes / c_ms / 1e6}
+    del src, dst
+    torch.cuda.empty_cache()
+    return out
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -273,6 +349,8 @@ def main():
                            "kernel": "factored projection (all instance launches + reduce), one batch of 8"}
     if args.phase in ("all", "routing"):
         out["routing"] = routing_cases(dev, max(args.steps, 5), args.warmup)
+    if args.phase in ("all", "gpt2"):
+        out["gpt2"] = gpt2_case(dev, max(args.steps, 5), args.warmup)
     if args.phase in ("all", "score"):
         for _ in range(args.warmup):
             score_step(False)
@@ -293,6 +371,9 @@ def main():
                                  "traffic": measured_traffic("score_gemm"),
                                  "kernel": "score GEMM (query scaling + NT GEMM), 2048 x 200000 x 8192"}
 
+    if args.phase == "all":
+        out["hbm_reference"] = stream_reference(dev)
+
     line = {
         "metric": "projected per-example grads/sec at Llama-8B layer shapes; scoring GEMM TFLOP/s",
         "value": out.get("projection", {}).get("examples_per_s"),
@@ -307,6 +388,8 @@ def main():
         "score_gemm_tflops": out.get("score", {}).get("gemm_tflops"),
     }
     line.update({k: v for k, v in out.items()})
+    if "hbm_reference" in out and "roofline" in out:
+        line["roofline"]["frac_of_copy"] = line["roofline"]["achieved"] / out["hbm_reference"]["copy_gbs"]
     if not args.no_cpu_baseline and sess is not None:
         print("[bench] timing the oracle on host cores", file=sys.stderr, flush=True)
         line["cpu_baseline"] = cpu_baseline_projection(wl, inputs, wl["seed"])

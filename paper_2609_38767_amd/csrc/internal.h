@@ -161,12 +161,20 @@ hipError_t launch_gproject(int elt_bytes, const GProjArgs& a, hipStream_t s);
 // ---------------------------------------------------------------- scoring
 hipError_t launch_scale_rows(int elt_bytes, const void* src, const float* d, void* dst,
                              int64_t rows, int64_t F, hipStream_t s);
+// partials: workspace of score_partial_floats(...) floats (may be null when 0)
 hipError_t launch_score_gemm(int elt_bytes, const void* Q, const void* X, float* S, int64_t n_q,
-                             int64_t n_train, int64_t F, hipStream_t s);
-hipError_t launch_score_gemm_256(const void* Q, const void* X, float* S, int64_t n_q,
-                                 int64_t n_train, int64_t F, hipStream_t s);
+                             int64_t n_train, int64_t F, float* partials, hipStream_t s);
 // bf16 problems at least this large (n_q * n_train) use the 256 x 256 kernel
 constexpr int64_t kBigGemmMin = (int64_t)1 << 20;
+// The 256 x 256 kernel splits K when its tiles alone would leave CUs idle:
+// number of K splits (1 = none) and the float32 partial results it stages.
+int score_ksplit(int elt_bytes, int64_t n_q, int64_t n_train, int64_t F);
+inline int64_t score_partial_floats(int elt_bytes, int64_t n_q, int64_t n_train, int64_t F) {
+  const int ks = score_ksplit(elt_bytes, n_q, n_train, F);
+  return ks > 1 ? (int64_t)ks * n_q * n_train : 0;
+}
+hipError_t launch_score_gemm_256(const void* Q, const void* X, float* S, int64_t n_q,
+                                 int64_t n_train, int64_t F, float* partials, hipStream_t s);
 constexpr int kTopkMax = 1024;
 hipError_t launch_topk(const float* S, int64_t n_q, int64_t n_train, int32_t k, int32_t* idx,
                        float* val, hipStream_t s);

@@ -947,7 +947,7 @@ dattri_status dattri_layer_route(const dattri_ctx* ctx, int32_t layer, dattri_ro
 
 // ------------------------------------------------------------------ scoring
 namespace {
-struct ScoreLayout { size_t off_q, q_bytes, off_s, s_bytes, total; };
+struct ScoreLayout { size_t off_q, q_bytes, off_s, s_bytes, off_p, p_bytes, total; };
 
 ScoreLayout score_layout(int64_t n_q, int64_t n_train, int64_t F, int elt, bool precond,
                          bool has_scores, int32_t topk) {
@@ -959,6 +959,9 @@ ScoreLayout score_layout(int64_t n_q, int64_t n_train, int64_t F, int elt, bool 
   L.off_s = off;
   L.s_bytes = (!has_scores && topk > 0) ? (size_t)(n_q * n_train * 4) : 0;
   off = align_up(off + L.s_bytes);
+  L.off_p = off;
+  L.p_bytes = (size_t)score_partial_floats(elt, n_q, n_train, F) * 4;
+  off = align_up(off + L.p_bytes);
   L.total = std::max<size_t>(off, kAlign);
   return L;
 }
@@ -1004,7 +1007,7 @@ dattri_status dattri_score(const void* phi_q, int64_t n_q, const void* phi_train
                 "phi rows must be 16-byte aligned (pointers and F*%d a multiple of 16)", elt);
   const ScoreLayout L = score_layout(n_q, n_train, F, elt, dev_precond_diag != nullptr,
                                      scores != nullptr, topk);
-  if (L.q_bytes + L.s_bytes > 0) {
+  if (L.q_bytes + L.s_bytes + L.p_bytes > 0) {
     if (!workspace) return fail(DATTRI_E_WORKSPACE, "workspace is NULL (needs %zu bytes)", L.total);
     if ((uintptr_t)workspace % kAlign) return fail(DATTRI_E_WORKSPACE, "workspace must be 256-byte aligned");
     if (ws_bytes < L.total)
@@ -1018,7 +1021,8 @@ dattri_status dattri_score(const void* phi_q, int64_t n_q, const void* phi_train
     q = ws + L.off_q;
   }
   float* S = scores ? scores : (float*)(ws + L.off_s);
-  HIP_TRY(launch_score_gemm(elt, q, phi_train, S, n_q, n_train, F, s));
+  HIP_TRY(launch_score_gemm(elt, q, phi_train, S, n_q, n_train, F,
+                            L.p_bytes ? (float*)(ws + L.off_p) : nullptr, s));
   if (topk > 0) HIP_TRY(launch_topk(S, n_q, n_train, topk, topk_idx, topk_val, s));
   return DATTRI_OK;
 }

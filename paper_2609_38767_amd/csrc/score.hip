@@ -142,9 +142,10 @@ hipError_t launch_scale_rows(int elt, const void* src, const float* d, void* dst
 }
 
 hipError_t launch_score_gemm(int elt, const void* Q, const void* X, float* S, int64_t n_q,
-                             int64_t n_train, int64_t F, hipStream_t s) {
+                             int64_t n_train, int64_t F, float* partials, hipStream_t s) {
   if (n_q <= 0 || n_train <= 0) return hipSuccess;
-  if (elt == 2 && n_q * n_train >= kBigGemmMin) return launch_score_gemm_256(Q, X, S, n_q, n_train, F, s);
+  if (elt == 2 && n_q * n_train >= kBigGemmMin)
+    return launch_score_gemm_256(Q, X, S, n_q, n_train, F, partials, s);
   const int n_qt = (int)((n_q + kBM - 1) / kBM), n_xt = (int)((n_train + kBN - 1) / kBN);
   const int64_t nb = (int64_t)n_qt * n_xt;
   if (nb > INT32_MAX) return hipErrorInvalidValue;

@@ -22,6 +22,8 @@
 // What bounds it on MI355X: the operand loads (64 KiB per stage per CU); with
 // loads removed the same loop runs at 86% of the bf16 MFMA peak, with the
 // fragment reads alone at the same rate.
+#include <algorithm>
+
 #include "device_common.h"
 #include "internal.h"
 
@@ -63,11 +65,13 @@ __device__ inline void issue_stage(const rsrc_t rq, const rsrc_t rx, int F, int 
   }
 }
 
+// Grid (tiles, K splits): split y runs stages [y*sps, (y+1)*sps) (sps even;
+// stages past F read zeros) and writes its float32 tile to out + y*n_q*n_train.
 __global__ __launch_bounds__(512, 1) void score_gemm_256_kernel(const uint8_t* __restrict__ Q,
                                                                 const uint8_t* __restrict__ X,
-                                                                float* __restrict__ S, int n_q,
+                                                                float* __restrict__ out, int n_q,
                                                                 int n_train, int F, int n_qt,
-                                                                int n_xt) {
+                                                                int n_xt, int sps) {
   __shared__ __align__(1024) uint8_t q0[kStageBytes], q1[kStageBytes];
   __shared__ __align__(1024) uint8_t x0[kStageBytes], x1[kStageBytes];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -90,9 +94,10 @@ __global__ __launch_bounds__(512, 1) void score_gemm_256_kernel(const uint8_t* _
 #pragma unroll
       for (int v = 0; v < 16; ++v) acc[i][j][v] = 0.f;
 
-  // stages padded to an even count (past F they load zeros), so the loop over
-  // stage pairs is branch-free
-  const int nk = ((F + kSK - 1) / kSK + 1) & ~1;
+  // this split's stages, an even count (past F they load zeros), so the loop
+  // over stage pairs is branch-free
+  const int nk = sps, k0 = blockIdx.y * sps;
+  float* S = out + (int64_t)blockIdx.y * n_q * n_train;
   const int r32 = lane & 31, kg = lane >> 5;
   // fragments of one 16-wide K step: lane l holds row l % 32, K 8*(l/32)..+8
   auto read_frags = [&](const uint8_t* cq, const uint8_t* cx, int s, i32x4 (&af)[4], i32x4 (&bf)[2]) {
@@ -119,8 +124,8 @@ __global__ __launch_bounds__(512, 1) void score_gemm_256_kernel(const uint8_t* _
     __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);  // MFMA
   };
 
-  issue_stage(rq, rx, F, 0, q0, x0, wave, lane);
-  issue_stage(rq, rx, F, 1, q1, x1, wave, lane);
+  issue_stage(rq, rx, F, k0, q0, x0, wave, lane);
+  issue_stage(rq, rx, F, k0 + 1, q1, x1, wave, lane);
   wait_vmcnt<8>();  // this wave's loads of stage 0 landed
   stage_barrier();
   i32x4 fa0[4], fb0[2], fa1[4], fb1[2];
@@ -140,7 +145,7 @@ __global__ __launch_bounds__(512, 1) void score_gemm_256_kernel(const uint8_t* _
     interleave_step();
     wait_vmcnt<0>();   // this wave's loads of stage kk+1 have landed
     stage_barrier();   // ... and every wave's; every wave is done reading stage kk
-    issue_stage(rq, rx, F, kk + 2, wq, wx, wave, lane);
+    issue_stage(rq, rx, F, k0 + kk + 2, wq, wx, wave, lane);
     read_frags(nq, nx, 0, fa0, fb0);
     mma(fa1, fb1);
     // 16 direct loads and 8 fragment reads over the held-back 16 MFMAs
@@ -174,14 +179,44 @@ __global__ __launch_bounds__(512, 1) void score_gemm_256_kernel(const uint8_t* _
     }
 }
 
+// Sum of the K-split partial tiles, in split order (deterministic).
+__global__ __launch_bounds__(256) void splitk_sum_kernel(const float* __restrict__ part, int ks,
+                                                         int64_t n, float* __restrict__ S) {
+  const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (i >= n) return;
+  float s = part[i];
+  for (int y = 1; y < ks; ++y) s += part[(int64_t)y * n + i];
+  S[i] = s;
+}
+
+int score_ksplit(int elt, int64_t n_q, int64_t n_train, int64_t F) {
+  if (elt != 2 || n_q * n_train < kBigGemmMin || n_q <= 0 || n_train <= 0 || F <= 0) return 1;
+  const int64_t tiles = ((n_q + kSB - 1) / kSB) * ((n_train + kSB - 1) / kSB);
+  const int64_t nk = (F + kSK - 1) / kSK;
+  int64_t ks = std::min<int64_t>({256 / std::max<int64_t>(tiles, 1), 16, nk / 2});
+  if (ks <= 1) return 1;
+  const int64_t sps = ((nk + ks - 1) / ks + 1) & ~1;  // even stages per split
+  return (int)((nk + sps - 1) / sps);
+}
+
 hipError_t launch_score_gemm_256(const void* Q, const void* X, float* S, int64_t n_q,
-                                 int64_t n_train, int64_t F, hipStream_t s) {
+                                 int64_t n_train, int64_t F, float* partials, hipStream_t s) {
   if (n_q <= 0 || n_train <= 0) return hipSuccess;
   const int n_qt = (int)((n_q + kSB - 1) / kSB), n_xt = (int)((n_train + kSB - 1) / kSB);
   const int64_t nb = (int64_t)n_qt * n_xt;
   if (nb > INT32_MAX) return hipErrorInvalidValue;
-  hipLaunchKernelGGL(score_gemm_256_kernel, dim3((unsigned)nb), dim3(512), 0, s, (const uint8_t*)Q,
-                     (const uint8_t*)X, S, (int)n_q, (int)n_train, (int)F, n_qt, n_xt);
+  const int64_t nk = (F + kSK - 1) / kSK;
+  const int ks = score_ksplit(2, n_q, n_train, F);
+  const int sps = ks > 1 ? (int)((((nk + ks - 1) / ks) + 1) & ~1) : (int)((nk + 1) & ~1);
+  if (ks > 1 && !partials) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(score_gemm_256_kernel, dim3((unsigned)nb, (unsigned)ks), dim3(512), 0, s,
+                     (const uint8_t*)Q, (const uint8_t*)X, ks > 1 ? partials : S, (int)n_q,
+                     (int)n_train, (int)F, n_qt, n_xt, sps);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess || ks == 1) return e;
+  const int64_t n = n_q * n_train;
+  hipLaunchKernelGGL(splitk_sum_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s, partials, ks,
+                     n, S);
   return hipGetLastError();
 }
 

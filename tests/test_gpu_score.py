@@ -129,11 +129,16 @@ def test_score_full_size_sampled():
     _check_topk(got, ref, idx[rows].cpu().numpy(), val[rows].cpu().numpy(), wl["topk"])
 
 
-def test_score_deterministic():
+@pytest.mark.parametrize("shape", [(130, 1000, 256), (256, 4096, 1024)])
+def test_score_deterministic(shape):
+    # the second shape takes the 256 x 256 kernel with K split into 8 partial
+    # products summed in a fixed order
+    n_q, n_t, F = shape
     g = torch.Generator(device=DEV).manual_seed(8)
-    Q = torch.randn((130, 256), generator=g, device=DEV).to(torch.bfloat16)
-    X = torch.randn((1000, 256), generator=g, device=DEV).to(torch.bfloat16)
+    Q = torch.randn((n_q, F), generator=g, device=DEV).to(torch.bfloat16)
+    X = torch.randn((n_t, F), generator=g, device=DEV).to(torch.bfloat16)
     a = score(Q, X, topk=10)
     b = score(Q, X, topk=10)
     torch.cuda.synchronize()
     assert torch.equal(a[0], b[0]) and torch.equal(a[1], b[1])
+    assert rel_fro(host64(a[0]), osc.score(host64(Q), host64(X))) <= 1e-5

@@ -5,19 +5,22 @@
 // 128 x 64 each (4 x 2 MFMA 32x32x16 tiles = 128 float32 accumulators per
 // lane).  32x32x16 keeps the matrix pipe full from one wave, which 16x16x32
 // does not; the second wave per SIMD covers the other's waits.  K advances 64
-// elements per stage through two LDS stage buffers (2 x 64 KiB) filled by
-// direct global->LDS loads (buffer_load ... lds, 16 bytes per lane, 8 lanes
-// per 128-byte row segment: whole cache lines per request); the next stage's
-// loads are issued right after the barrier that frees its buffer, one stage
-// ahead.  Inside a stage the operand fragments of K step s+1 are read from
-// LDS while the MFMAs of step s run; the last step's MFMAs are held back past
-// the stage barrier so they cover the first fragment reads of the next stage.
-// LDS rows are 128 bytes (64 bf16) with the 16-byte chunk index XOR-swizzled
-// by row % 8, so every 8 consecutive lanes of a fragment read hit distinct
-// banks; the swizzle is applied on the global side of the direct loads (each
-// lane fetches the chunk that lands in its fixed LDS slot).  Tiles are ordered
-// per XCD: the 8 query tiles of a training tile run on one XCD, 32 tiles in
-// flight per XCD share their operands through its L2.
+// elements per stage.  Operands reach LDS by direct global->LDS loads
+// (buffer_load ... lds, 16 bytes per lane, 8 lanes per 128-byte row segment:
+// whole cache lines per request) into 32 KiB stage buffers: two for the query
+// rows (L2/MALL-resident, loaded one stage ahead) and three for the training
+// rows (streamed from HBM, loaded two stages ahead); 160 KiB in all.  Inside a
+// stage the operand fragments of K step s+1 are read from LDS while the MFMAs
+// of step s run; the last step's MFMAs are held back past the stage barrier so
+// they cover the first fragment reads of the next stage.  LDS rows are 128
+// bytes (64 bf16) with the 16-byte chunk index XOR-swizzled by row % 8, so
+// every 8 consecutive lanes of a fragment read hit distinct banks; the swizzle
+// is applied on the global side of the direct loads (each lane fetches the
+// chunk that lands in its fixed LDS slot).  Tiles are ordered per XCD: the 8
+// query tiles of a training tile run on one XCD, 32 tiles in flight per XCD
+// share their operands through its L2.  When the tiles alone would leave CUs
+// idle, K is split over a second grid dimension and the float32 partial tiles
+// are summed in split order by a second kernel.
 //
 // What bounds it on MI355X: the operand loads (64 KiB per stage per CU); with
 // loads removed the same loop runs at 86% of the bf16 MFMA peak, with the
@@ -49,8 +52,8 @@ __device__ inline int swz(int row, int chunk) { return row * kSRow + ((chunk ^ (
 
 // One stage: 32 KiB of Q rows and 32 KiB of X rows, 32 wave-loads of 1 KiB
 // (8 rows x 128 bytes) per operand; wave w issues loads j = 4w .. 4w+3 of both.
-__device__ inline void issue_stage(const rsrc_t rq, const rsrc_t rx, int F, int kk, uint8_t* dq,
-                                   uint8_t* dx, int wave, int lane) {
+template <bool IS_X>
+__device__ inline void issue_half(const rsrc_t r, int F, int kk, uint8_t* d, int wave, int lane) {
   const int row_in = lane >> 3, phys = lane & 7;
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
@@ -60,20 +63,19 @@ __device__ inline void issue_stage(const rsrc_t rq, const rsrc_t rx, int F, int 
     const int col = kk * kSK + chunk * 8;
     const uint32_t oob = (uint32_t)-(int32_t)(col >= F);
     const uint32_t off = ((uint32_t)((row * F + col) * 2) & ~oob) | (kOOB & oob);
-    __builtin_amdgcn_raw_ptr_buffer_load_lds(rq, LDS_PTR(dq + j * 1024), 16, off, 0, 0, 0);
-    __builtin_amdgcn_raw_ptr_buffer_load_lds(rx, LDS_PTR(dx + j * 1024), 16, off, 0, 0, 0);
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(r, LDS_PTR(d + j * 1024), 16, off, 0, 0, 0);
   }
 }
 
-// Grid (tiles, K splits): split y runs stages [y*sps, (y+1)*sps) (sps even;
-// stages past F read zeros) and writes its float32 tile to out + y*n_q*n_train.
+// Grid (tiles, K splits): split y runs stages [y*sps, (y+1)*sps) (stages past
+// F read zeros) and writes its float32 tile to out + y*n_q*n_train.
 __global__ __launch_bounds__(512, 1) void score_gemm_256_kernel(const uint8_t* __restrict__ Q,
                                                                 const uint8_t* __restrict__ X,
                                                                 float* __restrict__ out, int n_q,
                                                                 int n_train, int F, int n_qt,
                                                                 int n_xt, int sps) {
   __shared__ __align__(1024) uint8_t q0[kStageBytes], q1[kStageBytes];
-  __shared__ __align__(1024) uint8_t x0[kStageBytes], x1[kStageBytes];
+  __shared__ __align__(1024) uint8_t x0[kStageBytes], x1[kStageBytes], x2[kStageBytes];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wm = wave >> 2, wn = wave & 3;
 
@@ -94,8 +96,7 @@ __global__ __launch_bounds__(512, 1) void score_gemm_256_kernel(const uint8_t* _
 #pragma unroll
       for (int v = 0; v < 16; ++v) acc[i][j][v] = 0.f;
 
-  // this split's stages, an even count (past F they load zeros), so the loop
-  // over stage pairs is branch-free
+  // this split's stages (past F they load zeros)
   const int nk = sps, k0 = blockIdx.y * sps;
   float* S = out + (int64_t)blockIdx.y * n_q * n_train;
   const int r32 = lane & 31, kg = lane >> 5;
@@ -124,16 +125,18 @@ __global__ __launch_bounds__(512, 1) void score_gemm_256_kernel(const uint8_t* _
     __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);  // MFMA
   };
 
-  issue_stage(rq, rx, F, k0, q0, x0, wave, lane);
-  issue_stage(rq, rx, F, k0 + 1, q1, x1, wave, lane);
-  wait_vmcnt<8>();  // this wave's loads of stage 0 landed
+  issue_half<false>(rq, F, k0, q0, wave, lane);
+  issue_half<true>(rx, F, k0, x0, wave, lane);
+  issue_half<true>(rx, F, k0 + 1, x1, wave, lane);
+  issue_half<false>(rq, F, k0 + 1, q1, wave, lane);
+  issue_half<true>(rx, F, k0 + 2, x2, wave, lane);
+  wait_vmcnt<12>();  // Q and X of stage 0 landed
   stage_barrier();
   i32x4 fa0[4], fb0[2], fa1[4], fb1[2];
   read_frags(q0, x0, 0, fa0, fb0);
 
-  // stage kk lives in (cq, cx); stage kk+1 is landing in (nq, nx)
-  auto stage = [&](int kk, const uint8_t* cq, const uint8_t* cx, uint8_t* wq, uint8_t* wx,
-                   const uint8_t* nq, const uint8_t* nx) {
+  // stage kk lives in (cq, cx); its buffers receive Q(kk+2) and X(kk+3)
+  auto stage = [&](int kk, uint8_t* cq, uint8_t* cx, const uint8_t* nq, const uint8_t* nx) {
     read_frags(cq, cx, 1, fa1, fb1);
     mma(fa0, fb0);
     interleave_step();
@@ -143,12 +146,12 @@ __global__ __launch_bounds__(512, 1) void score_gemm_256_kernel(const uint8_t* _
     read_frags(cq, cx, 3, fa1, fb1);
     mma(fa0, fb0);
     interleave_step();
-    wait_vmcnt<0>();   // this wave's loads of stage kk+1 have landed
-    stage_barrier();   // ... and every wave's; every wave is done reading stage kk
-    issue_stage(rq, rx, F, k0 + kk + 2, wq, wx, wave, lane);
+    wait_vmcnt<4>();   // Q(kk+1) and X(kk+1) landed (X(kk+2) may be in flight)
+    stage_barrier();
+    issue_half<false>(rq, F, k0 + kk + 2, cq, wave, lane);
+    issue_half<true>(rx, F, k0 + kk + 3, cx, wave, lane);
     read_frags(nq, nx, 0, fa0, fb0);
     mma(fa1, fb1);
-    // 16 direct loads and 8 fragment reads over the held-back 16 MFMAs
 #pragma unroll
     for (int i = 0; i < 6; ++i) {
       __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);  // VMEM (direct loads)
@@ -158,11 +161,24 @@ __global__ __launch_bounds__(512, 1) void score_gemm_256_kernel(const uint8_t* _
     __builtin_amdgcn_sched_group_barrier(0x020, 2, 0);  // VMEM (direct loads)
     __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);  // MFMA
   };
-  for (int kk = 0; kk < nk; kk += 2) {
-    stage(kk, q0, x0, q0, x0, q1, x1);
-    stage(kk + 1, q1, x1, q1, x1, q0, x0);
+  // buffers rotate with period 6 (Q over 2, X over 3); the last nk % 6
+  // stages repeat the first steps of the rotation
+  int kk = 0;
+  for (; kk + 6 <= nk; kk += 6) {
+    stage(kk, q0, x0, q1, x1);
+    stage(kk + 1, q1, x1, q0, x2);
+    stage(kk + 2, q0, x2, q1, x0);
+    stage(kk + 3, q1, x0, q0, x1);
+    stage(kk + 4, q0, x1, q1, x2);
+    stage(kk + 5, q1, x2, q0, x0);
   }
-  wait_vmcnt<0>();  // the padding loads issued past the end
+  const int rem = nk - kk;  // uniform
+  if (rem > 0) stage(kk, q0, x0, q1, x1);
+  if (rem > 1) stage(kk + 1, q1, x1, q0, x2);
+  if (rem > 2) stage(kk + 2, q0, x2, q1, x0);
+  if (rem > 3) stage(kk + 3, q1, x0, q0, x1);
+  if (rem > 4) stage(kk + 4, q0, x1, q1, x2);
+  wait_vmcnt<0>();  // the prefetches issued past the last stage
 
   // 32x32 C layout: lane l, element v holds row 8*(v/4) + 4*(l/32) + v%4,
   // column l % 32; for each v, 32 lanes store 128 contiguous bytes of a row.
@@ -195,7 +211,7 @@ int score_ksplit(int elt, int64_t n_q, int64_t n_train, int64_t F) {
   const int64_t nk = (F + kSK - 1) / kSK;
   int64_t ks = std::min<int64_t>({256 / std::max<int64_t>(tiles, 1), 16, nk / 2});
   if (ks <= 1) return 1;
-  const int64_t sps = ((nk + ks - 1) / ks + 1) & ~1;  // even stages per split
+  const int64_t sps = (nk + ks - 1) / ks;
   return (int)((nk + sps - 1) / sps);
 }
 
@@ -207,7 +223,7 @@ hipError_t launch_score_gemm_256(const void* Q, const void* X, float* S, int64_t
   if (nb > INT32_MAX) return hipErrorInvalidValue;
   const int64_t nk = (F + kSK - 1) / kSK;
   const int ks = score_ksplit(2, n_q, n_train, F);
-  const int sps = ks > 1 ? (int)((((nk + ks - 1) / ks) + 1) & ~1) : (int)((nk + 1) & ~1);
+  const int sps = ks > 1 ? (int)((nk + ks - 1) / ks) : (int)nk;
   if (ks > 1 && !partials) return hipErrorInvalidValue;
   hipLaunchKernelGGL(score_gemm_256_kernel, dim3((unsigned)nb, (unsigned)ks), dim3(512), 0, s,
                      (const uint8_t*)Q, (const uint8_t*)X, ks > 1 ? partials : S, (int)n_q,

@@ -35,11 +35,11 @@ def parse():
     return p.parse_args()
 
 
-# Kernel sources whose text fixes each reported kernel's code: a traffic figure
+# Sources that fix each reported kernel's code and launch plan: a traffic figure
 # measured with rocprofv3 counters is reported only while these are unchanged.
 KERNEL_SOURCES = {
-    "projection": ["factored.hip", "project_rows.h", "reduce.hip", "device_common.h"],
-    "score_gemm": ["score_big.hip", "score.hip", "device_common.h"],
+    "projection": ["factored.hip", "project_rows.h", "reduce.hip", "device_common.h", "runtime.cpp"],
+    "score_gemm": ["score_big.hip", "score.hip", "device_common.h", "runtime.cpp"],
 }
 HERE = os.path.dirname(os.path.abspath(__file__))
 

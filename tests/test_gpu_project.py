@@ -100,9 +100,11 @@ def test_token_chunks_and_lengths_at_chunk_edges(form):
 
 @pytest.mark.parametrize("form", ["fused", "split"])
 def test_shared_input_group_matches_separate_inputs(form):
-    layers = [dict(name="q", d_in=256, d_out=256, k_in=32, k_out=32, a_group="x"),
-              dict(name="k", d_in=256, d_out=64, k_in=32, k_out=32, a_group="x"),
-              dict(name="v", d_in=256, d_out=64, k_in=32, k_out=32, a_group="x"),
+    # 16-wide maps: q and k share one fused work item (2 input tiles keep 4 row
+    # tiles per wave); v would need 3 and runs alone, as does o
+    layers = [dict(name="q", d_in=256, d_out=256, k_in=16, k_out=16, a_group="x"),
+              dict(name="k", d_in=256, d_out=64, k_in=16, k_out=16, a_group="x"),
+              dict(name="v", d_in=256, d_out=64, k_in=16, k_out=16, a_group="x"),
               dict(name="o", d_in=256, d_out=256, k_in=32, k_out=32, a_group="y")]
     wl = dict(W.WORKLOADS["llama8b"], seed=21)
     inputs = _session_inputs(wl, layers, 3, 96, "bf16")

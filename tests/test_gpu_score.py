@@ -100,6 +100,43 @@ def test_topk_ties_follow_lower_index():
     assert idx[1].tolist() == list(range(100))  # all-tie row -> lowest indices
 
 
+def _exact_scores(values):
+    """Q = e_0, X[j] = (values[j], 0, 0, 0) in float32: S[0] == values exactly."""
+    v = torch.as_tensor(values, dtype=torch.float32)
+    X = torch.zeros((v.numel(), 4), dtype=torch.float32)
+    X[:, 0] = v
+    Q = torch.zeros((1, 4), dtype=torch.float32)
+    Q[0, 0] = 1.0
+    return Q.to(DEV), X.to(DEV)
+
+
+@pytest.mark.parametrize("case", ["sample_too_high", "massive_ties", "ties_at_kth"])
+def test_topk_long_rows_all_paths(case):
+    # rows of >= 64K scores take the sampled single-pass path first; these
+    # rows force each of its outcomes: too few candidates above the sampled
+    # threshold, too many (ties), and success with ties across the k-th score
+    n, k = 70000, 100
+    rng = np.random.default_rng(3)
+    vals = rng.standard_normal(n).astype(np.float32)
+    runs = [(c * n // 64) & ~3 for c in range(64)]  # starts of the sampled runs
+    if case == "sample_too_high":
+        # the only 50 large scores sit inside sampled runs: the threshold the
+        # sample suggests admits fewer than k scores of the whole row
+        for c in range(50):
+            vals[runs[c] + 7] = 100.0 + c
+    elif case == "massive_ties":
+        vals = rng.integers(-3, 4, n).astype(np.float32)  # ~10000 copies of each value
+    else:
+        vals[rng.choice(n, 300, replace=False)] = 5.0  # 300 tied scores above the rest
+    Q, X = _exact_scores(vals)
+    S, idx, val = score(Q, X, topk=k)
+    torch.cuda.synchronize()
+    np.testing.assert_array_equal(host64(S)[0], vals.astype(np.float64))
+    ref_idx, ref_val = osc.topk(vals[None, :].astype(np.float64), k)
+    np.testing.assert_array_equal(idx.cpu().numpy(), ref_idx)
+    np.testing.assert_array_equal(val.cpu().numpy(), ref_val)
+
+
 def test_negative_zero_equals_zero():
     Q = torch.tensor([[1.0, 0.0, 0.0, 0.0]], device=DEV)
     X = torch.tensor([[-0.0, 1, 1, 1], [0.0, 1, 1, 1], [-1.0, 1, 1, 1], [-0.0, 0, 0, 0]], device=DEV)

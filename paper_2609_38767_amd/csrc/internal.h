@@ -89,7 +89,7 @@ hipError_t launch_reduce(const ReduceTask* tasks, int n_tasks, int n_examples, i
                          hipStream_t s);
 
 // ------------------------------------------- factored route, split form
-// For short sequences, where the fused kernel has too few work items: stage 1
+// For captures where the fused kernel has too few work items: stage 1
 // projects the token rows of every factor block (all examples flattened,
 // n*T rows) slab by slab over the feature dimension d, writing float32
 // partial projections [slab][row][tile cols]; stage 2 sums the slabs and

@@ -151,7 +151,7 @@ struct Plan {
   struct Launch { int elt, na, nb, aligned, first, count; };
   std::vector<Launch> launches;
   std::vector<MatChunk> mat;
-  // split form of the factored route (short sequences)
+  // split form of the factored route (captures with few fused work items)
   std::vector<SplitOp> sops;
   std::vector<SplitItem> sitems;
   std::vector<ContractTask> ctasks;

@@ -92,22 +92,21 @@ __global__ __launch_bounds__(256, (AL && NA * NB <= 12) ? 2 : 1) void factored_k
         for (int t = 0; t < NB; ++t) acc_b[rt][t] = f32x4{0.f, 0.f, 0.f, 0.f};
       project_rows<ELT, AL, RT, NB, NTL, PD>(rb, r_wave, rows_valid, d_out, d_out, pout, acc_b, pan);
 
+      // K slices (rt, j) outermost: consecutive MFMAs update different psi
+      // blocks, so none waits on its predecessor's result
       const int a0 = M.a_tile0, a1 = M.a_tile0 + M.na;
 #pragma unroll
-      for (int ta = 0; ta < NA; ++ta) {
-        if (ta >= a0 && ta < a1) {
+      for (int rt = 0; rt < RT; ++rt)
 #pragma unroll
-          for (int tb = 0; tb < NB; ++tb) {
-            if (tb < nb) {
+        for (int j = 0; j < 4; ++j)
 #pragma unroll
-              for (int rt = 0; rt < RT; ++rt)
+          for (int ta = 0; ta < NA; ++ta) {
+            if (ta >= a0 && ta < a1) {
 #pragma unroll
-                for (int j = 0; j < 4; ++j)
-                  psi[ta][tb] = mfma_f32_4(acc_a[rt][ta][j], acc_b[rt][tb][j], psi[ta][tb]);
+              for (int tb = 0; tb < NB; ++tb)
+                if (tb < nb) psi[ta][tb] = mfma_f32_4(acc_a[rt][ta][j], acc_b[rt][tb][j], psi[ta][tb]);
             }
           }
-        }
-      }
     }
   }
 

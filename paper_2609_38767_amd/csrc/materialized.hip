@@ -154,27 +154,28 @@ __global__ __launch_bounds__(256, 2) void gproject_kernel(GProjArgs a) {
     if (kb_begin < kb_end) load_g(kb_begin, gcur);
     for (int kb = kb_begin; kb < kb_end; ++kb) {
       if (kb + 1 < kb_end) load_g(kb + 1, gnext);
+      i32x4 pf[NT];
 #pragma unroll
-      for (int t = 0; t < NT; ++t) {
-        if (t < nt) {
-          const i32x4 pf = *(const i32x4*)(pin + ((int64_t)(kb * na_all + ta0 + t) * 64 + lane) * 16);
-          float pv[EPL];
-          if (ELT == 2) {
+      for (int t = 0; t < NT; ++t)
+        pf[t] = t < nt ? *(const i32x4*)(pin + ((int64_t)(kb * na_all + ta0 + t) * 64 + lane) * 16)
+                       : i32x4{0, 0, 0, 0};
+      // K slot j outermost: consecutive MFMAs update different H tiles, so
+      // none waits on its predecessor's result
 #pragma unroll
-            for (int i = 0; i < 4; ++i) {
-              const uint32_t w = (uint32_t)pf[i];
-              pv[2 * i] = bf16_bits_to_f32(w & 0xFFFFu);
-              pv[2 * i + 1] = bf16_bits_to_f32(w >> 16);
+      for (int j = 0; j < EPL; ++j) {
+#pragma unroll
+        for (int t = 0; t < NT; ++t) {
+          if (t < nt) {
+            float pv;
+            if (ELT == 2) {
+              const uint32_t w = (uint32_t)pf[t][j / 2];
+              pv = bf16_bits_to_f32((j & 1) ? (w >> 16) : (w & 0xFFFFu));
+            } else {
+              pv = __builtin_bit_cast(f32x4, pf[t])[j];
             }
-          } else {
-            const f32x4 pff = __builtin_bit_cast(f32x4, pf);
 #pragma unroll
-            for (int i = 0; i < 4; ++i) pv[i] = pff[i];
+            for (int rt = 0; rt < kGRT; ++rt) H[rt][t] = mfma_f32_4(gcur[rt][j / 4][j % 4], pv, H[rt][t]);
           }
-#pragma unroll
-          for (int rt = 0; rt < kGRT; ++rt)
-#pragma unroll
-            for (int j = 0; j < EPL; ++j) H[rt][t] = mfma_f32_4(gcur[rt][j / 4][j % 4], pv[j], H[rt][t]);
         }
       }
 #pragma unroll

@@ -268,11 +268,25 @@ dattri_status dattri_score_workspace_bytes(int64_t n_q, int64_t n_train, int64_t
                                            dattri_dtype dtype, int32_t has_precond,
                                            int32_t has_scores, int32_t topk, size_t* bytes);
 
+/* Recommended row stride (elements) for storing feature rows of F elements
+ * of `dtype` (phi from dattri_project_per_example, or any phi_q / phi_train
+ * given to dattri_score): F rounded up to 256 bytes, plus 512 bytes when the
+ * row would otherwise be a multiple of 8 KiB of at least 16 KiB.  Such strides
+ * map one column of many rows into the same few L2 sets of MI355X, and the
+ * score GEMM then re-fetches operands it should share from memory.  Any
+ * stride >= F is accepted by dattri_score; this one runs fastest.
+ * Errors: INVALID_ARG (ld NULL, F < 0), DTYPE. */
+dattri_status dattri_feature_ld(int64_t F, dattri_dtype dtype, int64_t* ld);
+
 /* GradDot scores with an optional diagonal preconditioner, and top-k.
- *   phi_q:     device [n_q, F] of dtype;  phi_train: device [n_train, F] of dtype
+ *   phi_q:     device [n_q rows of F] of dtype, rows ld_q elements apart
+ *   phi_train: device [n_train rows of F] of dtype, rows ld_train apart
+ *   ld_q, ld_train: row strides in elements (0 = F, dense); >= F, and
+ *              ld * element size a multiple of 16 bytes
  *   dev_precond_diag: NULL (d = 1) or device float32 [F], d > 0, applied once:
  *              S[q][j] = sum_f phi_q[q][f] d[f] phi_train[j][f].  For bf16 the
- *              query row is scaled in float32 and rounded once to bf16.
+ *              query row is scaled in float32 and rounded once to bf16 (into
+ *              the workspace, rows dattri_feature_ld apart).
  *   scores:    device float32 [n_q, n_train], or NULL if only top-k is wanted
  *   topk:      0 (no selection) or 1 <= topk <= min(n_train, 1024)
  *   topk_idx:  device int32 [n_q, topk]; topk_val: device float32 [n_q, topk]:
@@ -280,12 +294,14 @@ dattri_status dattri_score_workspace_bytes(int64_t n_q, int64_t n_train, int64_t
  *              are ordered by lower training index (-0.0 equals +0.0; NaN
  *              scores are not supported).
  *   workspace: device, >= dattri_score_workspace_bytes(...), 256-byte aligned.
- * Accumulation is float32.  Errors: INVALID_ARG, DTYPE, WORKSPACE,
- * UNSUPPORTED (topk > 1024), HIP. */
-dattri_status dattri_score(const void* phi_q, int64_t n_q, const void* phi_train, int64_t n_train,
-                           int64_t F, dattri_dtype dtype, const float* dev_precond_diag,
-                           float* scores, int32_t topk, int32_t* topk_idx, float* topk_val,
-                           void* workspace, size_t ws_bytes, void* stream);
+ * Accumulation is float32.  Errors: INVALID_ARG (including ld < F), DTYPE,
+ * WORKSPACE, UNSUPPORTED (topk > 1024, misaligned rows, 256 rows of the
+ * stride reaching 4 GiB), HIP. */
+dattri_status dattri_score(const void* phi_q, int64_t n_q, int64_t ld_q, const void* phi_train,
+                           int64_t n_train, int64_t ld_train, int64_t F, dattri_dtype dtype,
+                           const float* dev_precond_diag, float* scores, int32_t topk,
+                           int32_t* topk_idx, float* topk_val, void* workspace, size_t ws_bytes,
+                           void* stream);
 
 #ifdef __cplusplus
 }

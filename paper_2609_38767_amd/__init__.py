@@ -22,7 +22,7 @@ __all__ = [
     "dattri_capture_layer", "dattri_clear_captures", "dattri_workspace_bytes",
     "dattri_project_per_example", "dattri_materialize_gradient", "dattri_set_cost_model",
     "dattri_get_cost_model", "dattri_layer_costs", "dattri_layer_route",
-    "dattri_score_workspace_bytes", "dattri_score",
+    "dattri_score_workspace_bytes", "dattri_feature_ld", "dattri_score",
 ]
 
 DATTRI_F32, DATTRI_BF16 = 0, 1
@@ -78,7 +78,9 @@ _SIGS = {
     "dattri_layer_costs": (_i32, [_vp, _i32, _i32, _P(_i64), _P(_i64), _P(_i64), _P(_i64)]),
     "dattri_layer_route": (_i32, [_vp, _i32, _P(_i32), _P(_dbl), _P(_dbl)]),
     "dattri_score_workspace_bytes": (_i32, [_i64, _i64, _i64, _i32, _i32, _i32, _i32, _P(_sz)]),
-    "dattri_score": (_i32, [_vp, _i64, _vp, _i64, _i64, _i32, _vp, _vp, _i32, _vp, _vp, _vp, _sz, _vp]),
+    "dattri_feature_ld": (_i32, [_i64, _i32, _P(_i64)]),
+    "dattri_score": (_i32, [_vp, _i64, _i64, _vp, _i64, _i64, _i64, _i32, _vp, _vp, _i32, _vp, _vp,
+                            _vp, _sz, _vp]),
 }
 EXPORTED = tuple(_SIGS)
 
@@ -267,9 +269,15 @@ def dattri_score_workspace_bytes(n_q, n_train, F, dtype, has_precond, has_scores
     return b.value
 
 
-def dattri_score(phi_q, n_q, phi_train, n_train, F, dtype, dev_precond_diag, scores, topk,
-                 topk_idx, topk_val, workspace, ws_bytes, stream=None):
-    _check(load().dattri_score(_ptr(phi_q), n_q, _ptr(phi_train), n_train, F, dtype,
+def dattri_feature_ld(F, dtype):
+    v = _i64()
+    _check(load().dattri_feature_ld(F, dtype, ctypes.byref(v)), "dattri_feature_ld")
+    return v.value
+
+
+def dattri_score(phi_q, n_q, ld_q, phi_train, n_train, ld_train, F, dtype, dev_precond_diag, scores,
+                 topk, topk_idx, topk_val, workspace, ws_bytes, stream=None):
+    _check(load().dattri_score(_ptr(phi_q), n_q, ld_q, _ptr(phi_train), n_train, ld_train, F, dtype,
                                _ptr(dev_precond_diag), _ptr(scores), topk, _ptr(topk_idx),
                                _ptr(topk_val), _ptr(workspace), ws_bytes, _stream(stream)),
            "dattri_score")

@@ -73,6 +73,15 @@ __device__ inline i32x4 load_frag(rsrc_t r, int row, int nrows, int col, int d, 
   return v;
 }
 
+// One 16-byte fragment of row `row` at column `col` of a block whose rows
+// are `ld` elements apart and hold d valid elements; d*ELT, ld*ELT and the
+// base are multiples of 16.  Rows >= nrows and columns >= d read as zero.
+template <int ELT>
+__device__ inline i32x4 load_frag_ld(rsrc_t r, int row, int nrows, int col, int d, int ld) {
+  const uint32_t off = (row < nrows && col < d) ? (uint32_t)(((int64_t)row * ld + col) * ELT) : kOOB;
+  return load16(r, off);
+}
+
 __device__ inline f32x4 mfma_f32_4(float a, float b, f32x4 c) {
   return __builtin_amdgcn_mfma_f32_16x16x4f32(a, b, c, 0, 0, 0);
 }

@@ -159,11 +159,14 @@ constexpr int kGProjMaxTilesIn = 8; // input tiles per pass (larger k_in loops)
 hipError_t launch_gproject(int elt_bytes, const GProjArgs& a, hipStream_t s);
 
 // ---------------------------------------------------------------- scoring
-hipError_t launch_scale_rows(int elt_bytes, const void* src, const float* d, void* dst,
-                             int64_t rows, int64_t F, hipStream_t s);
+// dst rows ld_dst apart receive src rows (ld_src apart) times d, first F columns
+hipError_t launch_scale_rows(int elt_bytes, const void* src, int64_t ld_src, const float* d,
+                             void* dst, int64_t ld_dst, int64_t rows, int64_t F, hipStream_t s);
 // partials: workspace of score_partial_floats(...) floats (may be null when 0)
-hipError_t launch_score_gemm(int elt_bytes, const void* Q, const void* X, float* S, int64_t n_q,
-                             int64_t n_train, int64_t F, float* partials, hipStream_t s);
+// Q rows ldq elements apart, X rows ldx apart (both >= F, multiples of 16 bytes)
+hipError_t launch_score_gemm(int elt_bytes, const void* Q, int64_t ldq, const void* X, int64_t ldx,
+                             float* S, int64_t n_q, int64_t n_train, int64_t F, float* partials,
+                             hipStream_t s);
 // bf16 problems at least this large (n_q * n_train) use the 256 x 256 kernel
 constexpr int64_t kBigGemmMin = (int64_t)1 << 20;
 // The 256 x 256 kernel splits K when its tiles alone would leave CUs idle:
@@ -173,8 +176,9 @@ inline int64_t score_partial_floats(int elt_bytes, int64_t n_q, int64_t n_train,
   const int ks = score_ksplit(elt_bytes, n_q, n_train, F);
   return ks > 1 ? (int64_t)ks * n_q * n_train : 0;
 }
-hipError_t launch_score_gemm_256(const void* Q, const void* X, float* S, int64_t n_q,
-                                 int64_t n_train, int64_t F, float* partials, hipStream_t s);
+hipError_t launch_score_gemm_256(const void* Q, int64_t ldq, const void* X, int64_t ldx, float* S,
+                                 int64_t n_q, int64_t n_train, int64_t F, float* partials,
+                                 hipStream_t s);
 constexpr int kTopkMax = 1024;
 hipError_t launch_topk(const float* S, int64_t n_q, int64_t n_train, int32_t k, int32_t* idx,
                        float* val, hipStream_t s);

@@ -16,20 +16,23 @@
 namespace dattri {
 using namespace dev;
 
+// dst[r][f] = src[r][f] * d[f] for f < F; rows ld_src / ld_dst elements apart
+// (the padding of dst rows is not written).
 template <int ELT>
 __global__ __launch_bounds__(256) void scale_rows_kernel(const uint8_t* __restrict__ src,
+                                                         int64_t ld_src,
                                                          const float* __restrict__ d,
-                                                         uint8_t* __restrict__ dst, int64_t rows,
-                                                         int64_t F) {
+                                                         uint8_t* __restrict__ dst, int64_t ld_dst,
+                                                         int64_t rows, int64_t F) {
   const int64_t n = rows * F;
   for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n;
        i += (int64_t)gridDim.x * blockDim.x) {
-    const int64_t f = i % F;
+    const int64_t r = i / F, f = i - r * F;
     if constexpr (ELT == 2) {
-      const float x = bf16_bits_to_f32(((const uint16_t*)src)[i]) * d[f];
-      ((uint16_t*)dst)[i] = f32_to_bf16_bits(x);
+      const float x = bf16_bits_to_f32(((const uint16_t*)src)[r * ld_src + f]) * d[f];
+      ((uint16_t*)dst)[r * ld_dst + f] = f32_to_bf16_bits(x);
     } else {
-      ((float*)dst)[i] = ((const float*)src)[i] * d[f];
+      ((float*)dst)[r * ld_dst + f] = ((const float*)src)[r * ld_src + f] * d[f];
     }
   }
 }
@@ -40,7 +43,8 @@ template <int ELT>
 __global__ __launch_bounds__(256) void score_gemm_kernel(const uint8_t* __restrict__ Q,
                                                          const uint8_t* __restrict__ X,
                                                          float* __restrict__ S, int n_q,
-                                                         int n_train, int F, int n_qt, int n_xt) {
+                                                         int n_train, int F, int ldq, int ldx,
+                                                         int n_qt, int n_xt) {
   constexpr int EPL = 16 / ELT;
   constexpr int BK = kRowBytes / ELT;  // K elements per stage
   __shared__ __align__(16) uint8_t smem[2][2][kBM * kRowBytes];  // [stage][Q/X] 64 KiB
@@ -54,8 +58,9 @@ __global__ __launch_bounds__(256) void score_gemm_kernel(const uint8_t* __restri
   const int qt = L % n_qt, xt = L / n_qt;
   const int q0 = qt * kBM, x0 = xt * kBN;
   const int rows_q = min(kBM, n_q - q0), rows_x = min(kBN, n_train - x0);
-  const rsrc_t rq = make_rsrc(Q + (int64_t)q0 * F * ELT, (uint32_t)((int64_t)rows_q * F * ELT));
-  const rsrc_t rx = make_rsrc(X + (int64_t)x0 * F * ELT, (uint32_t)((int64_t)rows_x * F * ELT));
+  // ranges end at the last row's F-th element (padding after it need not exist)
+  const rsrc_t rq = make_rsrc(Q + (int64_t)q0 * ldq * ELT, (uint32_t)(((int64_t)(rows_q - 1) * ldq + F) * ELT));
+  const rsrc_t rx = make_rsrc(X + (int64_t)x0 * ldx * ELT, (uint32_t)(((int64_t)(rows_x - 1) * ldx + F) * ELT));
 
   f32x4 acc[4][4];
 #pragma unroll
@@ -70,8 +75,8 @@ __global__ __launch_bounds__(256) void score_gemm_kernel(const uint8_t* __restri
     for (int i = 0; i < 4; ++i) {
       const int c = tid + 256 * i, row = c >> 3, ch = c & 7;
       const int col = kk * BK + ch * EPL;
-      rqv[i] = load_frag<ELT>(rq, row, rows_q, col, F, true);
-      rxv[i] = load_frag<ELT>(rx, row, rows_x, col, F, true);
+      rqv[i] = load_frag_ld<ELT>(rq, row, rows_q, col, F, ldq);
+      rxv[i] = load_frag_ld<ELT>(rx, row, rows_x, col, F, ldx);
     }
   };
   auto swrite = [&](int st) {
@@ -127,34 +132,37 @@ __global__ __launch_bounds__(256) void score_gemm_kernel(const uint8_t* __restri
     }
 }
 
-hipError_t launch_scale_rows(int elt, const void* src, const float* d, void* dst, int64_t rows,
-                             int64_t F, hipStream_t s) {
+hipError_t launch_scale_rows(int elt, const void* src, int64_t ld_src, const float* d, void* dst,
+                             int64_t ld_dst, int64_t rows, int64_t F, hipStream_t s) {
   const int64_t n = rows * F;
   if (n <= 0) return hipSuccess;
   const int blocks = (int)std::min<int64_t>((n + 255) / 256, 65536);
   if (elt == 2)
-    hipLaunchKernelGGL(scale_rows_kernel<2>, dim3(blocks), dim3(256), 0, s, (const uint8_t*)src, d,
-                       (uint8_t*)dst, rows, F);
+    hipLaunchKernelGGL(scale_rows_kernel<2>, dim3(blocks), dim3(256), 0, s, (const uint8_t*)src,
+                       ld_src, d, (uint8_t*)dst, ld_dst, rows, F);
   else
-    hipLaunchKernelGGL(scale_rows_kernel<4>, dim3(blocks), dim3(256), 0, s, (const uint8_t*)src, d,
-                       (uint8_t*)dst, rows, F);
+    hipLaunchKernelGGL(scale_rows_kernel<4>, dim3(blocks), dim3(256), 0, s, (const uint8_t*)src,
+                       ld_src, d, (uint8_t*)dst, ld_dst, rows, F);
   return hipGetLastError();
 }
 
-hipError_t launch_score_gemm(int elt, const void* Q, const void* X, float* S, int64_t n_q,
-                             int64_t n_train, int64_t F, float* partials, hipStream_t s) {
+hipError_t launch_score_gemm(int elt, const void* Q, int64_t ldq, const void* X, int64_t ldx,
+                             float* S, int64_t n_q, int64_t n_train, int64_t F, float* partials,
+                             hipStream_t s) {
   if (n_q <= 0 || n_train <= 0) return hipSuccess;
   if (elt == 2 && n_q * n_train >= kBigGemmMin)
-    return launch_score_gemm_256(Q, X, S, n_q, n_train, F, partials, s);
+    return launch_score_gemm_256(Q, ldq, X, ldx, S, n_q, n_train, F, partials, s);
   const int n_qt = (int)((n_q + kBM - 1) / kBM), n_xt = (int)((n_train + kBN - 1) / kBN);
   const int64_t nb = (int64_t)n_qt * n_xt;
   if (nb > INT32_MAX) return hipErrorInvalidValue;
   if (elt == 2)
     hipLaunchKernelGGL(score_gemm_kernel<2>, dim3((unsigned)nb), dim3(256), 0, s, (const uint8_t*)Q,
-                       (const uint8_t*)X, S, (int)n_q, (int)n_train, (int)F, n_qt, n_xt);
+                       (const uint8_t*)X, S, (int)n_q, (int)n_train, (int)F, (int)ldq, (int)ldx,
+                       n_qt, n_xt);
   else
     hipLaunchKernelGGL(score_gemm_kernel<4>, dim3((unsigned)nb), dim3(256), 0, s, (const uint8_t*)Q,
-                       (const uint8_t*)X, S, (int)n_q, (int)n_train, (int)F, n_qt, n_xt);
+                       (const uint8_t*)X, S, (int)n_q, (int)n_train, (int)F, (int)ldq, (int)ldx,
+                       n_qt, n_xt);
   return hipGetLastError();
 }
 

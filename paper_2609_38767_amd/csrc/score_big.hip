@@ -1,5 +1,6 @@
 // bf16 scoring GEMM for large problems: S = Q X^T, Q [n_q, F], X [n_train, F]
-// (both K-contiguous), float32 accumulate and output.
+// (both K-contiguous, rows ldq / ldx elements apart), float32 accumulate and
+// output.
 //
 // Workgroup tile 256 x 256, 8 waves (two per SIMD) in a 2 x 4 grid of
 // 128 x 64 each (4 x 2 MFMA 32x32x16 tiles = 128 float32 accumulators per
@@ -53,7 +54,7 @@ __device__ inline int swz(int row, int chunk) { return row * kSRow + ((chunk ^ (
 // One stage: 32 KiB of Q rows and 32 KiB of X rows, 32 wave-loads of 1 KiB
 // (8 rows x 128 bytes) per operand; wave w issues loads j = 4w .. 4w+3 of both.
 template <bool IS_X>
-__device__ inline void issue_half(const rsrc_t r, int F, int kk, uint8_t* d, int wave, int lane) {
+__device__ inline void issue_half(const rsrc_t r, int F, int ld, int kk, uint8_t* d, int wave, int lane) {
   const int row_in = lane >> 3, phys = lane & 7;
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
@@ -62,7 +63,7 @@ __device__ inline void issue_half(const rsrc_t r, int F, int kk, uint8_t* d, int
     const int chunk = phys ^ (row & 7);
     const int col = kk * kSK + chunk * 8;
     const uint32_t oob = (uint32_t)-(int32_t)(col >= F);
-    const uint32_t off = ((uint32_t)((row * F + col) * 2) & ~oob) | (kOOB & oob);
+    const uint32_t off = (((uint32_t)(row * ld + col) * 2u) & ~oob) | (kOOB & oob);
     __builtin_amdgcn_raw_ptr_buffer_load_lds(r, LDS_PTR(d + j * 1024), 16, off, 0, 0, 0);
   }
 }
@@ -72,8 +73,8 @@ __device__ inline void issue_half(const rsrc_t r, int F, int kk, uint8_t* d, int
 __global__ __launch_bounds__(512, 1) void score_gemm_256_kernel(const uint8_t* __restrict__ Q,
                                                                 const uint8_t* __restrict__ X,
                                                                 float* __restrict__ out, int n_q,
-                                                                int n_train, int F, int n_qt,
-                                                                int n_xt, int sps) {
+                                                                int n_train, int F, int ldq, int ldx,
+                                                                int n_qt, int n_xt, int sps) {
   __shared__ __align__(1024) uint8_t q0[kStageBytes], q1[kStageBytes];
   __shared__ __align__(1024) uint8_t x0[kStageBytes], x1[kStageBytes], x2[kStageBytes];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -85,8 +86,9 @@ __global__ __launch_bounds__(512, 1) void score_gemm_256_kernel(const uint8_t* _
   const int qt = L % n_qt, xt = L / n_qt;
   const int qrow0 = qt * kSB, xrow0 = xt * kSB;
   const int rows_q = min(kSB, n_q - qrow0), rows_x = min(kSB, n_train - xrow0);
-  const rsrc_t rq = make_rsrc(Q + (int64_t)qrow0 * F * 2, (uint32_t)((int64_t)rows_q * F * 2));
-  const rsrc_t rx = make_rsrc(X + (int64_t)xrow0 * F * 2, (uint32_t)((int64_t)rows_x * F * 2));
+  // ranges end at the last row's F-th element (padding after it need not exist)
+  const rsrc_t rq = make_rsrc(Q + (int64_t)qrow0 * ldq * 2, (uint32_t)(((int64_t)(rows_q - 1) * ldq + F) * 2));
+  const rsrc_t rx = make_rsrc(X + (int64_t)xrow0 * ldx * 2, (uint32_t)(((int64_t)(rows_x - 1) * ldx + F) * 2));
 
   f32x16 acc[4][2];
 #pragma unroll
@@ -125,11 +127,11 @@ __global__ __launch_bounds__(512, 1) void score_gemm_256_kernel(const uint8_t* _
     __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);  // MFMA
   };
 
-  issue_half<false>(rq, F, k0, q0, wave, lane);
-  issue_half<true>(rx, F, k0, x0, wave, lane);
-  issue_half<true>(rx, F, k0 + 1, x1, wave, lane);
-  issue_half<false>(rq, F, k0 + 1, q1, wave, lane);
-  issue_half<true>(rx, F, k0 + 2, x2, wave, lane);
+  issue_half<false>(rq, F, ldq, k0, q0, wave, lane);
+  issue_half<true>(rx, F, ldx, k0, x0, wave, lane);
+  issue_half<true>(rx, F, ldx, k0 + 1, x1, wave, lane);
+  issue_half<false>(rq, F, ldq, k0 + 1, q1, wave, lane);
+  issue_half<true>(rx, F, ldx, k0 + 2, x2, wave, lane);
   wait_vmcnt<12>();  // Q and X of stage 0 landed
   stage_barrier();
   i32x4 fa0[4], fb0[2], fa1[4], fb1[2];
@@ -148,8 +150,8 @@ __global__ __launch_bounds__(512, 1) void score_gemm_256_kernel(const uint8_t* _
     interleave_step();
     wait_vmcnt<4>();   // Q(kk+1) and X(kk+1) landed (X(kk+2) may be in flight)
     stage_barrier();
-    issue_half<false>(rq, F, k0 + kk + 2, cq, wave, lane);
-    issue_half<true>(rx, F, k0 + kk + 3, cx, wave, lane);
+    issue_half<false>(rq, F, ldq, k0 + kk + 2, cq, wave, lane);
+    issue_half<true>(rx, F, ldx, k0 + kk + 3, cx, wave, lane);
     read_frags(nq, nx, 0, fa0, fb0);
     mma(fa1, fb1);
 #pragma unroll
@@ -215,8 +217,9 @@ int score_ksplit(int elt, int64_t n_q, int64_t n_train, int64_t F) {
   return (int)((nk + sps - 1) / sps);
 }
 
-hipError_t launch_score_gemm_256(const void* Q, const void* X, float* S, int64_t n_q,
-                                 int64_t n_train, int64_t F, float* partials, hipStream_t s) {
+hipError_t launch_score_gemm_256(const void* Q, int64_t ldq, const void* X, int64_t ldx, float* S,
+                                 int64_t n_q, int64_t n_train, int64_t F, float* partials,
+                                 hipStream_t s) {
   if (n_q <= 0 || n_train <= 0) return hipSuccess;
   const int n_qt = (int)((n_q + kSB - 1) / kSB), n_xt = (int)((n_train + kSB - 1) / kSB);
   const int64_t nb = (int64_t)n_qt * n_xt;
@@ -227,7 +230,7 @@ hipError_t launch_score_gemm_256(const void* Q, const void* X, float* S, int64_t
   if (ks > 1 && !partials) return hipErrorInvalidValue;
   hipLaunchKernelGGL(score_gemm_256_kernel, dim3((unsigned)nb, (unsigned)ks), dim3(512), 0, s,
                      (const uint8_t*)Q, (const uint8_t*)X, ks > 1 ? partials : S, (int)n_q,
-                     (int)n_train, (int)F, n_qt, n_xt, sps);
+                     (int)n_train, (int)F, (int)ldq, (int)ldx, n_qt, n_xt, sps);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess || ks == 1) return e;
   const int64_t n = n_q * n_train;

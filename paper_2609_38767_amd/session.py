@@ -9,7 +9,7 @@ import torch
 
 from . import (DATTRI_BF16, DATTRI_F32, DATTRI_ROUTE_AUTO, dattri_bind_projection,
                dattri_capture_layer, dattri_clear_captures, dattri_create, dattri_destroy,
-               dattri_feature_dim, dattri_layer_offset, dattri_layer_route,
+               dattri_feature_dim, dattri_feature_ld, dattri_layer_offset, dattri_layer_route,
                dattri_project_per_example, dattri_projection_bytes, dattri_register_layer,
                dattri_score, dattri_score_workspace_bytes, dattri_set_factored_form,
                dattri_workspace_bytes)
@@ -68,8 +68,8 @@ class ProjectionSession:
 
     def project(self, n, route=DATTRI_ROUTE_AUTO, phi_dtype="f32", phi=None, stream=None):
         code, tdt = DTYPES[phi_dtype]
-        if phi is None:
-            phi = torch.empty((n, self.F), dtype=tdt, device=self.device)
+        if phi is None:  # rows at the library's recommended stride (a view)
+            phi = feature_rows(n, self.F, phi_dtype, self.device)
         ws = self.workspace(route)
         dattri_project_per_example(self.ctx, phi, code, phi.stride(0), ws, ws.numel(), route, stream)
         return phi
@@ -89,17 +89,29 @@ class ProjectionSession:
             pass
 
 
+def feature_rows(n, F, dtype="bf16", device="cuda"):
+    """Uninitialised [n, F] feature rows of `dtype` ("bf16" or "f32") whose
+    row stride is the library's recommended one (a view into a padded buffer)."""
+    code, tdt = DTYPES[dtype]
+    ld = dattri_feature_ld(F, code)
+    return torch.empty((n, ld), dtype=tdt, device=device)[:, :F]
+
+
 def score(phi_q, phi_train, precond=None, topk=0, want_scores=True, stream=None):
-    """(S or None, topk_idx or None, topk_val or None) for bf16/f32 feature rows."""
+    """(S or None, topk_idx or None, topk_val or None) for bf16/f32 feature
+    rows; each operand may be row-strided (unit stride along features)."""
     code = DATTRI_BF16 if phi_q.dtype == torch.bfloat16 else DATTRI_F32
     n_q, F = phi_q.shape
     n_train = phi_train.shape[0]
+    for t in (phi_q, phi_train):
+        if t.shape[1] > 1 and t.stride(1) != 1:
+            raise ValueError("feature rows must be contiguous along the feature axis")
     dev = phi_q.device
     S = torch.empty((n_q, n_train), dtype=torch.float32, device=dev) if want_scores else None
     idx = torch.empty((n_q, topk), dtype=torch.int32, device=dev) if topk else None
     val = torch.empty((n_q, topk), dtype=torch.float32, device=dev) if topk else None
     need = dattri_score_workspace_bytes(n_q, n_train, F, code, precond is not None, want_scores, topk)
     ws = _dev_bytes(need, dev)
-    dattri_score(phi_q, n_q, phi_train, n_train, F, code, precond, S, topk, idx, val, ws, ws.numel(),
-                 stream)
+    dattri_score(phi_q, n_q, phi_q.stride(0), phi_train, n_train, phi_train.stride(0), F, code, precond,
+                 S, topk, idx, val, ws, ws.numel(), stream)
     return S, idx, val

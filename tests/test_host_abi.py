@@ -132,27 +132,56 @@ def test_factored_limits_and_auto_route(ctx):
 
 def test_score_argument_errors():
     fake = 1 << 40
-    with pytest.raises(dt.DattriError) as e:
-        dt.dattri_score(fake, 4, fake, 8, 64, 5, None, fake, 0, None, None, None, 0)
-    assert _status(e) == "E_DTYPE"
-    with pytest.raises(dt.DattriError) as e:
-        dt.dattri_score(fake, 4, fake, 8, 64, dt.DATTRI_F32, None, fake, 9, fake, fake, None, 0)
-    assert _status(e) == "E_INVALID_ARG"  # topk > n_train
-    with pytest.raises(dt.DattriError) as e:
-        dt.dattri_score(fake, 4, fake, 2000, 64, dt.DATTRI_F32, None, fake, 1025, fake, fake, None, 0)
-    assert _status(e) == "E_UNSUPPORTED"
-    with pytest.raises(dt.DattriError) as e:
-        dt.dattri_score(fake, 4, fake, 8, 64, dt.DATTRI_F32, None, None, 0, None, None, None, 0)
-    assert _status(e) == "E_INVALID_ARG"  # nothing requested
-    with pytest.raises(dt.DattriError) as e:
-        dt.dattri_score(fake, 4, fake, 8, 64, dt.DATTRI_F32, fake, fake, 0, None, None, None, 0)
-    assert _status(e) == "E_WORKSPACE"  # preconditioner needs a scaled-query workspace
-    with pytest.raises(dt.DattriError) as e:
-        dt.dattri_score(fake, 4, fake, 8, 63, dt.DATTRI_F32, None, fake, 0, None, None, None, 0)
-    assert _status(e) == "E_UNSUPPORTED"  # rows not 16-byte multiples
+    f32 = dt.DATTRI_F32
+
+    def call(n_q=4, ld_q=0, n_t=8, ld_t=0, F=64, dtype=f32, d=None, S=fake, k=0, idx=None, val=None,
+             ws=None, wsb=0):
+        dt.dattri_score(fake, n_q, ld_q, fake, n_t, ld_t, F, dtype, d, S, k, idx, val, ws, wsb)
+
+    cases = [
+        (dict(dtype=5), "E_DTYPE"),
+        (dict(k=9, idx=fake, val=fake), "E_INVALID_ARG"),        # topk > n_train
+        (dict(n_t=2000, k=1025, idx=fake, val=fake), "E_UNSUPPORTED"),  # topk > 1024
+        (dict(S=None), "E_INVALID_ARG"),                         # nothing requested
+        (dict(d=fake), "E_WORKSPACE"),         # preconditioner needs a scaled-query workspace
+        (dict(F=63), "E_UNSUPPORTED"),                           # rows not 16-byte multiples
+        (dict(ld_q=32), "E_INVALID_ARG"),                        # stride below F
+        (dict(ld_t=63), "E_INVALID_ARG"),
+        (dict(ld_t=66), "E_UNSUPPORTED"),                        # stride not a 16-byte multiple
+        (dict(ld_q=-1), "E_INVALID_ARG"),
+        (dict(ld_t=1 << 22), "E_UNSUPPORTED"),                   # 256 rows reach 4 GiB
+    ]
+    for kw, want in cases:
+        with pytest.raises(dt.DattriError) as e:
+            call(**kw)
+        assert _status(e) == want, kw
     need = dt.dattri_score_workspace_bytes(4, 8, 64, dt.DATTRI_BF16, True, False, 3)
     assert need >= 4 * 64 * 2 + 4 * 8 * 4
     assert dt.dattri_score_workspace_bytes(4, 8, 64, dt.DATTRI_BF16, False, True, 3) == 256
+    # the scaled query copy is stored at the recommended stride
+    ld = dt.dattri_feature_ld(8192, dt.DATTRI_BF16)
+    assert dt.dattri_score_workspace_bytes(2048, 8, 8192, dt.DATTRI_BF16, True, True, 0) >= 2048 * ld * 2
+
+
+@pytest.mark.parametrize("F,dtype,ld", [
+    (64, dt.DATTRI_F32, 64),          # 256-byte rows: unchanged
+    (100, dt.DATTRI_BF16, 128),       # rounded up to 256 bytes
+    (4096, dt.DATTRI_BF16, 4096),     # 8 KiB rows: below 16 KiB, unchanged
+    (8192, dt.DATTRI_BF16, 8448),     # 16 KiB rows: + 512 bytes
+    (8192, dt.DATTRI_F32, 8320),      # 32 KiB rows: + 512 bytes
+    (12288, dt.DATTRI_BF16, 12544),   # 24 KiB (a multiple of 8 KiB): + 512 bytes
+    (14336, dt.DATTRI_BF16, 14336),   # 28 KiB: not a multiple of 8 KiB
+    (0, dt.DATTRI_BF16, 0),
+])
+def test_feature_ld_rule(F, dtype, ld):
+    assert dt.dattri_feature_ld(F, dtype) == ld
+
+
+def test_feature_ld_errors():
+    for args, want in [((-1, dt.DATTRI_F32), "E_INVALID_ARG"), ((8, 7), "E_DTYPE")]:
+        with pytest.raises(dt.DattriError) as e:
+            dt.dattri_feature_ld(*args)
+        assert _status(e) == want
 
 
 @pytest.mark.parametrize("dtype_name,dtype", [("f32", dt.DATTRI_F32), ("bf16", dt.DATTRI_BF16)])

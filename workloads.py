@@ -143,13 +143,25 @@ def factor_blocks(wl, layer_idx, batch_idx, n, T, device, dtype=None, a_cache=No
     return A, B
 
 
-def score_inputs(wl, device, n_query=None, n_train=None, F=None):
-    """(Phi_query, Phi_train, d) for the scoring workload (optionally resized)."""
+def strided_copy(t, ld):
+    """The rows of t in a buffer whose rows are ld >= t.shape[1] elements apart
+    (returned as a [rows, F] view; the padding is zero)."""
+    if ld is None or ld == t.shape[1]:
+        return t
+    buf = torch.zeros((t.shape[0], ld), dtype=t.dtype, device=t.device)
+    buf[:, :t.shape[1]].copy_(t)
+    return buf[:, :t.shape[1]]
+
+
+def score_inputs(wl, device, n_query=None, n_train=None, F=None, ld=None):
+    """(Phi_query, Phi_train, d) for the scoring workload (optionally resized).
+    With `ld`, both feature matrices are stored with rows ld elements apart
+    (same values as the dense draw)."""
     nq = n_query or wl["n_query"]
     nt = n_train or wl["n_train"]
     F = F or wl["F"]
-    q = draw((nq, F), "normal", wl["dtype"], device, wl["seed"], "phi_q")
-    x = draw((nt, F), "normal", wl["dtype"], device, wl["seed"], "phi_train")
+    q = strided_copy(draw((nq, F), "normal", wl["dtype"], device, wl["seed"], "phi_q"), ld)
+    x = strided_copy(draw((nt, F), "normal", wl["dtype"], device, wl["seed"], "phi_train"), ld)
     lo, hi = wl["d_log10_range"]
     g = _gen(device, wl["seed"], "d")
     u = torch.rand(F, generator=g, device=device, dtype=torch.float32)

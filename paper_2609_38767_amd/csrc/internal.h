@@ -163,12 +163,21 @@ hipError_t launch_gproject(int elt_bytes, const GProjArgs& a, hipStream_t s);
 hipError_t launch_scale_rows(int elt_bytes, const void* src, int64_t ld_src, const float* d,
                              void* dst, int64_t ld_dst, int64_t rows, int64_t F, hipStream_t s);
 // partials: workspace of score_partial_floats(...) floats (may be null when 0)
-// Q rows ldq elements apart, X rows ldx apart (both >= F, multiples of 16 bytes)
-hipError_t launch_score_gemm(int elt_bytes, const void* Q, int64_t ldq, const void* X, int64_t ldx,
-                             float* S, int64_t n_q, int64_t n_train, int64_t F, float* partials,
-                             hipStream_t s);
+// S = (Q diag(d)) X^T (d may be null): Q rows ldq elements apart, X rows ldx
+// apart (both >= F, multiples of 16 bytes).  qws: workspace of
+// score_query_ws_bytes(...) bytes for the prepared queries (ld_ws = row stride
+// of the row-major form the small kernels use); partials: workspace of
+// score_partial_floats(...) floats (may be null when 0).
+hipError_t launch_score_gemm(int elt_bytes, const void* Q, int64_t ldq, const float* d, const void* X,
+                             int64_t ldx, float* S, int64_t n_q, int64_t n_train, int64_t F,
+                             void* qws, int64_t ld_ws, float* partials, hipStream_t s);
 // bf16 problems at least this large (n_q * n_train) use the 256 x 256 kernel
 constexpr int64_t kBigGemmMin = (int64_t)1 << 20;
+inline bool score_uses_big(int elt_bytes, int64_t n_q, int64_t n_train) {
+  return elt_bytes == 2 && n_q * n_train >= kBigGemmMin;
+}
+// bytes of queries packed in MFMA fragment order for the 256 x 256 kernel
+int64_t score_qpack_bytes(int64_t n_q, int64_t F);
 // The 256 x 256 kernel splits K when its tiles alone would leave CUs idle:
 // number of K splits (1 = none) and the float32 partial results it stages.
 int score_ksplit(int elt_bytes, int64_t n_q, int64_t n_train, int64_t F);
@@ -176,9 +185,11 @@ inline int64_t score_partial_floats(int elt_bytes, int64_t n_q, int64_t n_train,
   const int ks = score_ksplit(elt_bytes, n_q, n_train, F);
   return ks > 1 ? (int64_t)ks * n_q * n_train : 0;
 }
-hipError_t launch_score_gemm_256(const void* Q, int64_t ldq, const void* X, int64_t ldx, float* S,
-                                 int64_t n_q, int64_t n_train, int64_t F, float* partials,
-                                 hipStream_t s);
+// Packs (and scales by d, when given) the queries into qpack, then runs the
+// 256 x 256 GEMM.
+hipError_t launch_score_gemm_256(const void* Q, int64_t ldq, const float* d, const void* X,
+                                 int64_t ldx, float* S, int64_t n_q, int64_t n_train, int64_t F,
+                                 void* qpack, float* partials, hipStream_t s);
 constexpr int kTopkMax = 1024;
 hipError_t launch_topk(const float* S, int64_t n_q, int64_t n_train, int32_t k, int32_t* idx,
                        float* val, hipStream_t s);

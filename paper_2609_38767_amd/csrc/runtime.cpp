@@ -978,14 +978,18 @@ int64_t feature_ld(int64_t F, int elt) {
 
 struct ScoreLayout { int64_t ldq; size_t off_q, q_bytes, off_s, s_bytes, off_p, p_bytes, total; };
 
-// The preconditioned query copy is stored with the recommended row stride.
+// Prepared queries: packed in MFMA fragment order for the 256 x 256 kernel
+// (always), else a preconditioned row-major copy at the recommended stride.
 ScoreLayout score_layout(int64_t n_q, int64_t n_train, int64_t F, int elt, bool precond,
                          bool has_scores, int32_t topk) {
   ScoreLayout L;
   size_t off = 0;
   L.ldq = feature_ld(F, elt);
   L.off_q = off;
-  L.q_bytes = precond ? (size_t)(n_q * L.ldq * elt) : 0;
+  if (score_uses_big(elt, n_q, n_train))
+    L.q_bytes = (size_t)score_qpack_bytes(n_q, F);
+  else
+    L.q_bytes = precond ? (size_t)(n_q * L.ldq * elt) : 0;
   off = align_up(off + L.q_bytes);
   L.off_s = off;
   L.s_bytes = (!has_scores && topk > 0) ? (size_t)(n_q * n_train * 4) : 0;
@@ -1065,15 +1069,9 @@ dattri_status dattri_score(const void* phi_q, int64_t n_q, int64_t ld_q, const v
   }
   hipStream_t s = (hipStream_t)stream;
   uint8_t* ws = (uint8_t*)workspace;
-  const void* q = phi_q;
-  int64_t ldq_used = ld_q;
-  if (dev_precond_diag && F > 0) {
-    HIP_TRY(launch_scale_rows(elt, phi_q, ld_q, dev_precond_diag, ws + L.off_q, L.ldq, n_q, F, s));
-    q = ws + L.off_q;
-    ldq_used = L.ldq;
-  }
   float* S = scores ? scores : (float*)(ws + L.off_s);
-  HIP_TRY(launch_score_gemm(elt, q, ldq_used, phi_train, ld_train, S, n_q, n_train, F,
+  HIP_TRY(launch_score_gemm(elt, phi_q, ld_q, dev_precond_diag, phi_train, ld_train, S, n_q, n_train,
+                            F, L.q_bytes ? ws + L.off_q : nullptr, L.ldq,
                             L.p_bytes ? (float*)(ws + L.off_p) : nullptr, s));
   if (topk > 0) HIP_TRY(launch_topk(S, n_q, n_train, topk, topk_idx, topk_val, s));
   return DATTRI_OK;

@@ -146,12 +146,19 @@ hipError_t launch_scale_rows(int elt, const void* src, int64_t ld_src, const flo
   return hipGetLastError();
 }
 
-hipError_t launch_score_gemm(int elt, const void* Q, int64_t ldq, const void* X, int64_t ldx,
-                             float* S, int64_t n_q, int64_t n_train, int64_t F, float* partials,
-                             hipStream_t s) {
+hipError_t launch_score_gemm(int elt, const void* Q, int64_t ldq, const float* d, const void* X,
+                             int64_t ldx, float* S, int64_t n_q, int64_t n_train, int64_t F,
+                             void* qws, int64_t ld_ws, float* partials, hipStream_t s) {
   if (n_q <= 0 || n_train <= 0) return hipSuccess;
-  if (elt == 2 && n_q * n_train >= kBigGemmMin)
-    return launch_score_gemm_256(Q, ldq, X, ldx, S, n_q, n_train, F, partials, s);
+  if (score_uses_big(elt, n_q, n_train))
+    return launch_score_gemm_256(Q, ldq, d, X, ldx, S, n_q, n_train, F, qws, partials, s);
+  if (d && F > 0) {  // scaled queries, row-major in the workspace
+    if (!qws) return hipErrorInvalidValue;
+    hipError_t e = launch_scale_rows(elt, Q, ldq, d, qws, ld_ws, n_q, F, s);
+    if (e != hipSuccess) return e;
+    Q = qws;
+    ldq = ld_ws;
+  }
   const int n_qt = (int)((n_q + kBM - 1) / kBM), n_xt = (int)((n_train + kBN - 1) / kBN);
   const int64_t nb = (int64_t)n_qt * n_xt;
   if (nb > INT32_MAX) return hipErrorInvalidValue;

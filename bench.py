@@ -41,7 +41,7 @@ def parse():
 # measured with rocprofv3 counters is reported only while these are unchanged.
 KERNEL_SOURCES = {
     "projection": ["factored.hip", "project_rows.h", "reduce.hip", "device_common.h", "runtime.cpp"],
-    "score_gemm": ["score_big.hip", "score.hip", "device_common.h", "runtime.cpp"],
+    "score_gemm": ["score_big.hip", "score.hip", "device_common.h", "internal.h"],
 }
 HERE = os.path.dirname(os.path.abspath(__file__))
 

@@ -40,8 +40,9 @@ def parse():
 # Sources that fix each reported kernel's code and launch plan: a traffic figure
 # measured with rocprofv3 counters is reported only while these are unchanged.
 KERNEL_SOURCES = {
-    "projection": ["factored.hip", "project_rows.h", "reduce.hip", "device_common.h", "runtime.cpp"],
-    "score_gemm": ["score_big.hip", "score.hip", "device_common.h", "internal.h"],
+    "projection": ["factored.hip", "project_rows.h", "reduce.hip", "device_common.h", "internal.h",
+                   "runtime.cpp"],
+    "score_gemm": ["score_big.hip", "device_common.h"],
 }
 HERE = os.path.dirname(os.path.abspath(__file__))
 

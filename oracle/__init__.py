@@ -19,6 +19,9 @@ Modules
                preconditioner, and per-query top-k.
 ``cost``       closed-form FLOP / byte / storage counts of the two routes
                (Sec. 3.2 "FLOP-aware routing", App. A.4).
+``crossgram``  cross-Gram matrices and squared norms of unprojected per-example
+               gradients summed over layers, by the factorized route (Eq. 4)
+               and through dense gradients (Eq. 1).
 
 Parity status of each function is stated in its docstring; the one function
 with no pin to the paper is the seed/counter layout of the generator, which the
@@ -26,4 +29,4 @@ paper leaves unspecified ("parity unpinned" w.r.t. the paper, pinned to the
 published Philox / SplitMix64 definitions instead).
 """
 
-from . import rng, gradients, scoring, cost  # noqa: F401
+from . import rng, gradients, scoring, cost, crossgram  # noqa: F401

@@ -54,3 +54,18 @@ def crossgram_factorized(B1, B2, T, N_i, N_o):
 def crossgram_materialized(B1, B2, T, N_i, N_o):
     """Leading-order cross-Gram cost of the materialized route (App. A.4 table)."""
     return (B1 + B2) * T * N_i * N_o + B1 * B2 * N_i * N_o
+
+
+def crossgram_flops_factorized(n1, n2, T1, T2, d_in, d_out):
+    """Exact FLOPs of one layer's cross-Gram by Eq. 4 (multiply-add = 2):
+    per pair the input Gram A_i A_j^T (2 T1 T2 d_in), the output-gradient Gram
+    B_i B_j^T (2 T1 T2 d_out) and the sum of their elementwise product
+    (2 T1 T2).  Leading term: the factorized row of the App. A.4 table."""
+    return 2 * n1 * n2 * T1 * T2 * (d_in + d_out + 1)
+
+
+def crossgram_flops_materialized(n1, n2, T1, T2, d_in, d_out):
+    """Exact FLOPs of one layer's cross-Gram through dense gradients: DW = B^T A
+    for every example (2 T d_in d_out each) and one Frobenius inner product
+    per pair (2 d_in d_out).  Leading terms: the materialized row of App. A.4."""
+    return 2 * (n1 * T1 + n2 * T2) * d_in * d_out + 2 * n1 * n2 * d_in * d_out

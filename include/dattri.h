@@ -260,6 +260,95 @@ dattri_status dattri_layer_costs(const dattri_ctx* ctx, int32_t layer, int32_t T
 dattri_status dattri_layer_route(const dattri_ctx* ctx, int32_t layer, dattri_route* chosen,
                                  double* pred_factored_us, double* pred_materialized_us);
 
+/* ------------------------------------------- unprojected cross-Gram matrices */
+
+/* Sec. 3.2 "Factorized inner product" (Eq. 4) and "FLOP-aware routing"; App.
+ * A.4 (routing-complexity table, "Routing").  For the captures of two contexts
+ * a (n_a examples) and b (n_b examples) over the same registered layers, the
+ * cross-Gram matrix of their unprojected per-example weight gradients summed
+ * over layers:
+ *     K[i][j] = sum_l < DW_l^(a,i), DW_l^(b,j) >_F
+ * Per layer one of two exact routes computes the contribution:
+ *   FACTORED      Eq. 4: sum over token pairs (t < T_i, s < T_j) of
+ *                 <a_t, a_s> <g_t, g_s>, i.e. the entries of
+ *                 (A_i A_j^T) * (B_i B_j^T) summed; cost ~ n_a n_b T^2 (d_in + d_out);
+ *   MATERIALIZED  DW = B^T A for every example (Eq. 1), then Frobenius
+ *                 products; cost ~ (n_a + n_b) T d_in d_out + n_a n_b d_in d_out.
+ * The projection sizes k_in / k_out and the maps play no part here.  The two
+ * contexts must have the same compute type and the same layer list (count,
+ * d_in, d_out); a and b may be the same context (the Gram of one batch).
+ * Every layer must be captured in both; lengths apply as in projection. */
+
+/* Rates of the cross-Gram time model (MI355X-fitted defaults).  Predicted time
+ * of a layer's route = sum over its kernels of max(flops / rate, bytes /
+ * bandwidth) + launch_us per launch, with the FLOP and byte counts of
+ * dattri_cross_gram_costs. */
+typedef struct {
+  double ghost_tflops;  /* factorized kernel (two token Grams and their product) */
+  double ghost_gbs;     /* its factor-block reads */
+  double build_tflops;  /* DW = B^T A kernel */
+  double build_gbs;     /* its factor reads plus float32 DW writes */
+  double dot_gbs;       /* Frobenius products over stored float32 DW */
+  double launch_us;     /* per kernel launch */
+} dattri_crossgram_cost_model;
+
+dattri_status dattri_set_crossgram_cost_model(dattri_ctx* ctx, const dattri_crossgram_cost_model* m);
+dattri_status dattri_get_crossgram_cost_model(const dattri_ctx* ctx, dattri_crossgram_cost_model* m);
+
+/* Exact operation counts of one layer's cross-Gram contribution between n_a
+ * examples of T_a tokens and n_b examples of T_b tokens (any output may be
+ * NULL); multiply-add = 2 FLOP:
+ *   factored FLOP      2 n_a n_b T_a T_b (d_in + d_out + 1)
+ *   materialized FLOP  2 (n_a T_a + n_b T_b) d_in d_out + 2 n_a n_b d_in d_out
+ *   factored bytes     (n_a T_a + n_b T_b)(d_in + d_out) elt   (factor blocks)
+ *   materialized bytes factored bytes + 2 * 4 (n_a + n_b) d_in d_out
+ * Errors: INVALID_ARG (negative sizes, elt not 2 or 4). */
+dattri_status dattri_cross_gram_costs(int64_t n_a, int64_t n_b, int32_t T_a, int32_t T_b,
+                                      int32_t d_in, int32_t d_out, int32_t elt_bytes,
+                                      int64_t* factored_flops, int64_t* materialized_flops,
+                                      int64_t* factored_bytes, int64_t* materialized_bytes);
+
+/* Route the cost model (of context a) picks for one layer's cross-Gram
+ * contribution given the current captures, with both predicted times in
+ * microseconds (ties go to FACTORED).
+ * Errors: INVALID_ARG (bad layer), STATE (not captured), SHAPE (layer lists
+ * or dtypes differ). */
+dattri_status dattri_cross_gram_route(const dattri_ctx* a, const dattri_ctx* b, int32_t layer,
+                                      dattri_route* chosen, double* pred_factored_us,
+                                      double* pred_materialized_us);
+
+/* Device bytes of workspace dattri_cross_gram needs for the current captures
+ * and route (AUTO: the per-layer choice).  b == a is allowed.
+ * Errors: as dattri_cross_gram_route. */
+dattri_status dattri_cross_gram_workspace_bytes(const dattri_ctx* a, const dattri_ctx* b,
+                                                dattri_route route, size_t* bytes);
+
+/* K = cross-Gram of the captures of a (rows) and b (columns), as above.
+ *   K: device float32 [n_a rows of ld_k >= n_b]; every element (i < n_a,
+ *      j < n_b) is written, the rest of each row is not.
+ *   workspace: device, >= dattri_cross_gram_workspace_bytes(a, b, route),
+ *      256-byte aligned.
+ *   route: AUTO (per layer by the cost model) or forced for every layer.
+ * Accumulation is float32 (inputs in their own type, float32 products); the
+ * result is deterministic (fixed summation order, no atomics).
+ * Errors: INVALID_ARG, STATE, SHAPE, WORKSPACE, HIP. */
+dattri_status dattri_cross_gram(dattri_ctx* a, dattri_ctx* b, float* K, int64_t ld_k,
+                                void* workspace, size_t ws_bytes, dattri_route route,
+                                void* stream);
+
+/* Per-example squared gradient norms of one context's captures summed over
+ * layers: out[i] = sum_l ||DW_l^(i)||_F^2 (the diagonal of the batch's Gram,
+ * App. A.4 "Routing": norms are routed like cross-Grams; the factored route
+ * costs 2 n T^2 (d_in + d_out + 1) per layer, the materialized one
+ * 2 n T d_in d_out + 2 n d_in d_out).
+ *   out: device float32 [n].
+ *   workspace: >= dattri_sq_norms_workspace_bytes(ctx, route).
+ * Errors: as dattri_cross_gram. */
+dattri_status dattri_sq_norms_workspace_bytes(const dattri_ctx* ctx, dattri_route route,
+                                              size_t* bytes);
+dattri_status dattri_gradient_sq_norms(dattri_ctx* ctx, float* out, void* workspace,
+                                       size_t ws_bytes, dattri_route route, void* stream);
+
 /* ---------------------------------------------------------------- scoring */
 
 /* Workspace bytes dattri_score needs for these sizes.  `has_precond` and

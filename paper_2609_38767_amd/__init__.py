@@ -23,6 +23,9 @@ __all__ = [
     "dattri_project_per_example", "dattri_materialize_gradient", "dattri_set_cost_model",
     "dattri_get_cost_model", "dattri_layer_costs", "dattri_layer_route",
     "dattri_score_workspace_bytes", "dattri_feature_ld", "dattri_score",
+    "dattri_set_crossgram_cost_model", "dattri_get_crossgram_cost_model", "dattri_cross_gram_costs",
+    "dattri_cross_gram_route", "dattri_cross_gram_workspace_bytes", "dattri_cross_gram",
+    "dattri_sq_norms_workspace_bytes", "dattri_gradient_sq_norms",
 ]
 
 DATTRI_F32, DATTRI_BF16 = 0, 1
@@ -47,6 +50,12 @@ class CostModel(ctypes.Structure):
                 ("gradient_tflops", ctypes.c_double), ("gradient_gbs", ctypes.c_double),
                 ("gproject_tflops", ctypes.c_double), ("gproject_gbs", ctypes.c_double),
                 ("launch_us", ctypes.c_double)]
+
+
+class CrossgramCostModel(ctypes.Structure):
+    _fields_ = [("ghost_tflops", ctypes.c_double), ("ghost_gbs", ctypes.c_double),
+                ("build_tflops", ctypes.c_double), ("build_gbs", ctypes.c_double),
+                ("dot_gbs", ctypes.c_double), ("launch_us", ctypes.c_double)]
 
 
 _i32, _i64, _u64, _sz = ctypes.c_int32, ctypes.c_int64, ctypes.c_uint64, ctypes.c_size_t
@@ -79,6 +88,15 @@ _SIGS = {
     "dattri_layer_route": (_i32, [_vp, _i32, _P(_i32), _P(_dbl), _P(_dbl)]),
     "dattri_score_workspace_bytes": (_i32, [_i64, _i64, _i64, _i32, _i32, _i32, _i32, _P(_sz)]),
     "dattri_feature_ld": (_i32, [_i64, _i32, _P(_i64)]),
+    "dattri_set_crossgram_cost_model": (_i32, [_vp, _P(CrossgramCostModel)]),
+    "dattri_get_crossgram_cost_model": (_i32, [_vp, _P(CrossgramCostModel)]),
+    "dattri_cross_gram_costs": (_i32, [_i64, _i64, _i32, _i32, _i32, _i32, _i32, _P(_i64), _P(_i64),
+                                       _P(_i64), _P(_i64)]),
+    "dattri_cross_gram_route": (_i32, [_vp, _vp, _i32, _P(_i32), _P(_dbl), _P(_dbl)]),
+    "dattri_cross_gram_workspace_bytes": (_i32, [_vp, _vp, _i32, _P(_sz)]),
+    "dattri_cross_gram": (_i32, [_vp, _vp, _vp, _i64, _vp, _sz, _i32, _vp]),
+    "dattri_sq_norms_workspace_bytes": (_i32, [_vp, _i32, _P(_sz)]),
+    "dattri_gradient_sq_norms": (_i32, [_vp, _vp, _vp, _sz, _i32, _vp]),
     "dattri_score": (_i32, [_vp, _i64, _i64, _vp, _i64, _i64, _i64, _i32, _vp, _vp, _i32, _vp, _vp,
                             _vp, _sz, _vp]),
 }
@@ -281,3 +299,52 @@ def dattri_score(phi_q, n_q, ld_q, phi_train, n_train, ld_train, F, dtype, dev_p
                                _ptr(dev_precond_diag), _ptr(scores), topk, _ptr(topk_idx),
                                _ptr(topk_val), _ptr(workspace), ws_bytes, _stream(stream)),
            "dattri_score")
+
+
+def dattri_set_crossgram_cost_model(ctx, model):
+    m = CrossgramCostModel(**model) if isinstance(model, dict) else model
+    _check(load().dattri_set_crossgram_cost_model(ctx, ctypes.byref(m)), "dattri_set_crossgram_cost_model")
+
+
+def dattri_get_crossgram_cost_model(ctx):
+    m = CrossgramCostModel()
+    _check(load().dattri_get_crossgram_cost_model(ctx, ctypes.byref(m)), "dattri_get_crossgram_cost_model")
+    return {name: getattr(m, name) for name, _ in CrossgramCostModel._fields_}
+
+
+def dattri_cross_gram_costs(n_a, n_b, T_a, T_b, d_in, d_out, elt_bytes):
+    v = [_i64() for _ in range(4)]
+    _check(load().dattri_cross_gram_costs(n_a, n_b, T_a, T_b, d_in, d_out, elt_bytes,
+                                          *[ctypes.byref(x) for x in v]), "dattri_cross_gram_costs")
+    return tuple(x.value for x in v)
+
+
+def dattri_cross_gram_route(a, b, layer):
+    r, f, m = _i32(), _dbl(), _dbl()
+    _check(load().dattri_cross_gram_route(a, b, layer, ctypes.byref(r), ctypes.byref(f), ctypes.byref(m)),
+           "dattri_cross_gram_route")
+    return r.value, f.value, m.value
+
+
+def dattri_cross_gram_workspace_bytes(a, b, route=DATTRI_ROUTE_AUTO):
+    v = _sz()
+    _check(load().dattri_cross_gram_workspace_bytes(a, b, route, ctypes.byref(v)),
+           "dattri_cross_gram_workspace_bytes")
+    return v.value
+
+
+def dattri_cross_gram(a, b, K, ld_k, workspace, ws_bytes, route=DATTRI_ROUTE_AUTO, stream=None):
+    _check(load().dattri_cross_gram(a, b, _ptr(K), ld_k, _ptr(workspace), ws_bytes, route, _stream(stream)),
+           "dattri_cross_gram")
+
+
+def dattri_sq_norms_workspace_bytes(ctx, route=DATTRI_ROUTE_AUTO):
+    v = _sz()
+    _check(load().dattri_sq_norms_workspace_bytes(ctx, route, ctypes.byref(v)),
+           "dattri_sq_norms_workspace_bytes")
+    return v.value
+
+
+def dattri_gradient_sq_norms(ctx, out, workspace, ws_bytes, route=DATTRI_ROUTE_AUTO, stream=None):
+    _check(load().dattri_gradient_sq_norms(ctx, _ptr(out), _ptr(workspace), ws_bytes, route, _stream(stream)),
+           "dattri_gradient_sq_norms")

@@ -19,6 +19,9 @@ constexpr int64_t kMaxBlockBytes = ((int64_t)1 << 32) - 4096;  // 32-bit buffer 
 constexpr size_t kAlign = 256;                                  // workspace sub-buffer alignment
 inline size_t align_up(size_t x, size_t a = kAlign) { return (x + a - 1) / a * a; }
 
+// MI355X-fitted defaults of the cross-Gram time model (crossgram_api.cpp).
+dattri_crossgram_cost_model default_crossgram_cost_model();
+
 }  // namespace dattri
 
 #define HIP_TRY(expr)                                                                     \

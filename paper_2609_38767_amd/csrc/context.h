@@ -1,0 +1,41 @@
+// Library context (host side): registered layers with their projection maps
+// and captured factor blocks, the route cost models, and the host copy of the
+// last uploaded launch plan.  Shared by the translation units of the C ABI.
+#pragma once
+
+#include <stdint.h>
+
+#include <vector>
+
+#include "dattri.h"
+
+namespace dattri {
+
+struct Layer {
+  int32_t d_in = 0, d_out = 0, k_in = 0, k_out = 0;
+  int64_t offset = 0;  // first column of the layer's block in phi
+  void* P_in = nullptr;
+  void* P_out = nullptr;
+  bool bound = false;
+  std::vector<float> override_in, override_out;  // rounded values when overridden
+  const void* A = nullptr;  // captured [n, T, d_in]
+  const void* B = nullptr;  // captured [n, T, d_out]
+  int32_t n = 0, T = 0;
+  const int32_t* lengths = nullptr;
+  bool captured = false;
+};
+
+}  // namespace dattri
+
+struct dattri_ctx {
+  dattri_dtype dtype;
+  int elt;
+  uint64_t seed;
+  std::vector<dattri::Layer> layers;
+  int64_t F = 0;
+  dattri_cost_model cost;
+  dattri_crossgram_cost_model xcost;
+  dattri_factored_form form = DATTRI_FORM_AUTO;
+  std::vector<uint8_t> blob;     // host copy of the last uploaded projection plan
+  std::vector<uint8_t> xg_blob;  // host copy of the last uploaded cross-Gram plan
+};

@@ -158,6 +158,38 @@ constexpr int kGProjRows = 128;     // rows of G per workgroup (4 waves x 2 row 
 constexpr int kGProjMaxTilesIn = 8; // input tiles per pass (larger k_in loops)
 hipError_t launch_gproject(int elt_bytes, const GProjArgs& a, hipStream_t s);
 
+// ------------------------------------------------------ cross-Gram matrices
+// One layer of the factorized route between batch 1 (n1 examples) and batch 2
+// (n2 examples): factor blocks [n, T, d] row-major, token rows padded to
+// Tp = T rounded up to 16 on the flattened token axes.
+struct GhostEntry {
+  const void* A1; const void* B1; const int32_t* len1;
+  const void* A2; const void* B2; const int32_t* len2;
+  int32_t d_in, d_out, n1, n2, T1, T2, Tp1, Tp2;
+  int32_t nbr, nbc;                 // 16 x 16 blocks: n1*Tp1/16 rows, n2*Tp2/16 columns
+  int32_t aligned;                  // rows and bases 16-byte aligned (vector loads)
+  int32_t out0;                     // output row of its pair (i, j) is out0 + i
+  int64_t part_off;                 // float offset of its block sums (nbr x nbc)
+};
+struct GhostTile { int32_t entry, rt, ct, pad0; };  // 128 x 128 tile of an entry
+constexpr int kGhostTile = 128;
+hipError_t launch_ghost(int elt_bytes, const GhostEntry* entries, const GhostTile* tiles, int n_tiles,
+                        float* parts, hipStream_t s);
+// K[I*ld + J] (=, or += with accumulate) the sum over entries, in order, of the
+// block sums of segment (I - out0, J) of every entry that has that pair; diag:
+// K[I] from segments (I - out0, I - out0).  Cells: n_rows x n_cols (diag: n_rows).
+hipError_t launch_ghost_reduce(const GhostEntry* entries, int n_entries, const float* parts,
+                               int n_rows, int n_cols, float* K, int64_t ld, int diag, int accumulate,
+                               hipStream_t s);
+// parts[c][i][j] (diag: parts[c][i]) = Frobenius product over chunk c of the
+// flattened gradients G1[i], G2[j] (D floats each); chunk a multiple of 64
+hipError_t launch_gdot(const float* G1, int n1, const float* G2, int n2, int64_t D, int64_t chunk,
+                       int diag, float* parts, hipStream_t s);
+// K[(r0+i)*ld + c0+j] (diag: K[r0+i]) = or += the sum over chunks of parts
+hipError_t launch_kacc(const float* parts, int nchunks, int n1, int n2, float* K, int64_t ld, int r0,
+                       int c0, int diag, int accumulate, hipStream_t s);
+hipError_t launch_fill_rows(float* K, int rows, int cols, int64_t ld, hipStream_t s);
+
 // ---------------------------------------------------------------- scoring
 // dst rows ld_dst apart receive src rows (ld_src apart) times d, first F columns
 hipError_t launch_scale_rows(int elt_bytes, const void* src, int64_t ld_src, const float* d,

@@ -10,6 +10,7 @@
 #include <vector>
 
 #include "api_common.h"
+#include "context.h"
 #include "dattri.h"
 #include "internal.h"
 #include "runtime.h"
@@ -42,20 +43,6 @@ constexpr int64_t kGBudgetBytes = (int64_t)2 << 30;   // staged G per materializ
 
 inline int tiles16(int k) { return (k + 15) / 16; }
 
-struct Layer {
-  int32_t d_in = 0, d_out = 0, k_in = 0, k_out = 0;
-  int64_t offset = 0;
-  void* P_in = nullptr;
-  void* P_out = nullptr;
-  bool bound = false;
-  std::vector<float> override_in, override_out;  // rounded values when overridden
-  const void* A = nullptr;
-  const void* B = nullptr;
-  int32_t n = 0, T = 0;
-  const int32_t* lengths = nullptr;
-  bool captured = false;
-};
-
 bool factored_supported(const Layer& L) {
   return tiles16(L.k_in) <= kMaxGroupTiles && tiles16(L.k_out) <= kMaxMemberBTiles;
 }
@@ -78,16 +65,6 @@ dattri_cost_model default_cost_model() {
 
 }  // namespace
 
-struct dattri_ctx {
-  dattri_dtype dtype;
-  int elt;
-  uint64_t seed;
-  std::vector<Layer> layers;
-  int64_t F = 0;
-  dattri_cost_model cost;
-  dattri_factored_form form = DATTRI_FORM_AUTO;
-  std::vector<uint8_t> blob;  // host copy of the last uploaded launch plan
-};
 
 namespace {
 
@@ -603,6 +580,7 @@ dattri_status dattri_create(dattri_ctx** out, dattri_dtype compute, uint64_t see
   c->elt = compute == DATTRI_BF16 ? 2 : 4;
   c->seed = seed;
   c->cost = default_cost_model();
+  c->xcost = default_crossgram_cost_model();
   *out = c;
   return DATTRI_OK;
 }

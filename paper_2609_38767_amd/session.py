@@ -8,6 +8,8 @@ maps, captures factor blocks, sizes the workspace and calls
 import torch
 
 from . import (DATTRI_BF16, DATTRI_F32, DATTRI_ROUTE_AUTO, dattri_bind_projection,
+               dattri_cross_gram, dattri_cross_gram_workspace_bytes, dattri_gradient_sq_norms,
+               dattri_sq_norms_workspace_bytes,
                dattri_capture_layer, dattri_clear_captures, dattri_create, dattri_destroy,
                dattri_feature_dim, dattri_feature_ld, dattri_layer_offset, dattri_layer_route,
                dattri_project_per_example, dattri_projection_bytes, dattri_register_layer,
@@ -115,3 +117,24 @@ def score(phi_q, phi_train, precond=None, topk=0, want_scores=True, stream=None)
     dattri_score(phi_q, n_q, phi_q.stride(0), phi_train, n_train, phi_train.stride(0), F, code, precond,
                  S, topk, idx, val, ws, ws.numel(), stream)
     return S, idx, val
+
+
+def cross_gram(sess_a, sess_b, route=DATTRI_ROUTE_AUTO, K=None, stream=None):
+    """K [n_a, n_b] float32: the cross-Gram of the unprojected gradients captured
+    in two sessions over the same layers (sess_b may be sess_a)."""
+    n_a = sess_a._held[0][0].shape[0]
+    n_b = sess_b._held[0][0].shape[0]
+    if K is None:
+        K = torch.empty((n_a, n_b), dtype=torch.float32, device=sess_a.device)
+    ws = _dev_bytes(dattri_cross_gram_workspace_bytes(sess_a.ctx, sess_b.ctx, route), sess_a.device)
+    dattri_cross_gram(sess_a.ctx, sess_b.ctx, K, K.stride(0), ws, ws.numel(), route, stream)
+    return K
+
+
+def sq_norms(sess, route=DATTRI_ROUTE_AUTO, stream=None):
+    """Per-example squared gradient norms [n] float32, summed over layers."""
+    n = sess._held[0][0].shape[0]
+    out = torch.empty(n, dtype=torch.float32, device=sess.device)
+    ws = _dev_bytes(dattri_sq_norms_workspace_bytes(sess.ctx, route), sess.device)
+    dattri_gradient_sq_norms(sess.ctx, out, ws, ws.numel(), route, stream)
+    return out

@@ -1,0 +1,126 @@
+"""GPU parity of the unprojected cross-Gram matrix and squared norms (Eq. 4 and
+its materialized counterpart, App. A.4), through the C ABI, against the
+float64 oracle (oracle/crossgram.py).
+
+Inputs are exact in both dtypes (bf16 values are consumed as they are), and
+every product and sum is float32, so both dtypes are held to the float32 bound
+of 1e-5 relative Frobenius error on the small cases (feature dims <= 256); the
+full-size layer (contractions over 1024 and 4096 features) uses 2e-5."""
+import numpy as np
+import pytest
+import torch
+
+import paper_2609_38767_amd as dt
+from gpu_util import host64, rel_fro
+from oracle import crossgram as ocg
+from paper_2609_38767_amd.session import ProjectionSession, cross_gram, sq_norms
+
+pytestmark = pytest.mark.gpu
+DEV = "cuda"
+ROUTES = [dt.DATTRI_ROUTE_FACTORED, dt.DATTRI_ROUTE_MATERIALIZED, dt.DATTRI_ROUTE_AUTO]
+TDT = {"f32": torch.float32, "bf16": torch.bfloat16}
+
+
+def _batch(dims, n, T, dtype, seed, lengths=None):
+    g = torch.Generator(device=DEV).manual_seed(seed)
+    out = []
+    for d_in, d_out in dims:
+        A = torch.randn((n, T, d_in), generator=g, device=DEV).to(TDT[dtype])
+        B = torch.randn((n, T, d_out), generator=g, device=DEV).to(TDT[dtype])
+        out.append((A, B))
+    L = None if lengths is None else torch.tensor(lengths, dtype=torch.int32, device=DEV)
+    return out, L
+
+
+def _session(dims, blocks, L, dtype):
+    layers = [dict(d_in=d_in, d_out=d_out, k_in=1, k_out=1) for d_in, d_out in dims]
+    s = ProjectionSession(layers, dtype=dtype, seed=0, device=DEV)
+    for li, (A, B) in enumerate(blocks):
+        s.capture(li, A, B, L)
+    return s
+
+
+def _oracle_batch(blocks, L):
+    lens = None if L is None else L.cpu().numpy()
+    return [(host64(A), host64(B), lens) for A, B in blocks]
+
+
+DIMS = [(64, 48), (40, 72), (130, 24)]
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_cross_gram_ragged_batches_both_routes(dtype):
+    a_blocks, La = _batch(DIMS, 5, 37, dtype, 1, lengths=[37, 20, 0, 33, 1])
+    b_blocks, Lb = _batch(DIMS, 3, 20, dtype, 2, lengths=[20, 7, 19])
+    sa, sb = _session(DIMS, a_blocks, La, dtype), _session(DIMS, b_blocks, Lb, dtype)
+    ref = ocg.cross_gram(_oracle_batch(a_blocks, La), _oracle_batch(b_blocks, Lb))
+    got = {}
+    for r in ROUTES:
+        got[r] = cross_gram(sa, sb, r)
+    torch.cuda.synchronize()
+    for r, K in got.items():
+        err = rel_fro(host64(K), ref)
+        assert err <= 1e-5, (r, err)
+    assert not host64(got[dt.DATTRI_ROUTE_FACTORED])[2].any()  # zero-length example
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_gram_of_one_batch_and_sq_norms(dtype):
+    blocks, L = _batch(DIMS, 6, 45, dtype, 3, lengths=[45, 44, 17, 16, 0, 30])
+    s = _session(DIMS, blocks, L, dtype)
+    ob = _oracle_batch(blocks, L)
+    ref = ocg.cross_gram(ob, ob)
+    ref_n = ocg.sq_norms(ob)
+    for r in ROUTES:
+        K = cross_gram(s, s, r)
+        nrm = sq_norms(s, r)
+        torch.cuda.synchronize()
+        assert rel_fro(host64(K), ref) <= 1e-5, r
+        assert rel_fro(host64(nrm), ref_n) <= 1e-5, r
+        assert nrm[4].item() == 0.0
+
+
+@pytest.mark.parametrize("route", ROUTES)
+def test_cross_gram_multi_tile_tokens(route):
+    # T = 300 -> 304 padded rows per example: 5 row tiles of 128 over 2
+    # examples, tiles straddling the example boundary
+    dims = [(256, 128), (96, 200)]
+    a_blocks, La = _batch(dims, 2, 300, "bf16", 4, lengths=[300, 211])
+    b_blocks, Lb = _batch(dims, 2, 150, "bf16", 5)
+    sa, sb = _session(dims, a_blocks, La, "bf16"), _session(dims, b_blocks, Lb, "bf16")
+    K = cross_gram(sa, sb, route)
+    nrm = sq_norms(sa, route)
+    torch.cuda.synchronize()
+    ob = _oracle_batch(a_blocks, La)
+    assert rel_fro(host64(K), ocg.cross_gram(ob, _oracle_batch(b_blocks, Lb))) <= 1e-5
+    assert rel_fro(host64(nrm), ocg.sq_norms(ob)) <= 1e-5
+
+
+def test_cross_gram_deterministic_and_strided_output():
+    a_blocks, La = _batch(DIMS, 4, 33, "bf16", 6)
+    b_blocks, Lb = _batch(DIMS, 3, 33, "bf16", 7)
+    sa, sb = _session(DIMS, a_blocks, La, "bf16"), _session(DIMS, b_blocks, Lb, "bf16")
+    for r in ROUTES:
+        buf = torch.full((4, 8), 7.0, device=DEV)
+        K1 = cross_gram(sa, sb, r, K=buf[:, :3])
+        K2 = cross_gram(sa, sb, r)
+        torch.cuda.synchronize()
+        assert torch.equal(K1, K2), r
+        assert (buf[:, 3:] == 7.0).all()  # columns past n_b untouched
+
+
+def test_cross_gram_full_size_layer():
+    """One Pythia-410M-shaped MLP layer (1024 -> 4096) at T = 2048, 8 training
+    examples against 1 query (the workload the routing benchmark sweeps), both
+    routes against the oracle's materialized definition."""
+    dims = [(1024, 4096)]
+    a_blocks, La = _batch(dims, 8, 2048, "bf16", 8)
+    b_blocks, Lb = _batch(dims, 1, 2048, "bf16", 9)
+    sa, sb = _session(dims, a_blocks, La, "bf16"), _session(dims, b_blocks, Lb, "bf16")
+    got = {r: cross_gram(sa, sb, r) for r in ROUTES[:2]}
+    torch.cuda.synchronize()
+    ref = ocg.cross_gram(_oracle_batch(a_blocks, La), _oracle_batch(b_blocks, Lb), "materialized")
+    for r, K in got.items():
+        err = rel_fro(host64(K), ref)
+        print(f"full-size layer route {r}: rel err {err:.2e}")
+        assert err <= 2e-5, (r, err)

@@ -33,7 +33,8 @@ def parse():
     p.add_argument("--steps", type=int, default=10)
     p.add_argument("--warmup", type=int, default=2)
     p.add_argument("--no-cpu-baseline", action="store_true")
-    p.add_argument("--phase", choices=["all", "project", "score", "routing", "gpt2", "copy"], default="all")
+    p.add_argument("--phase", choices=["all", "project", "score", "routing", "gpt2", "crossgram", "copy"],
+                   default="all")
     return p.parse_args()
 
 
@@ -218,6 +219,75 @@ def gpt2_case(dev, steps, warmup):
     return out
 
 
+def crossgram_case(dev, steps, warmup):
+    """Unprojected cross-Gram routing sweep (the paper's routing ablation over
+    sequence length): 96 Pythia-410M-shaped layers, 8 training examples
+    against 1 query, T in {32, 128, 512, 2048}, bf16.  Per T: both forced
+    routes and AUTO (median of `steps`), the routes AUTO picked, its regret
+    against the faster forced route, and the factorized route's rate."""
+    import torch
+    import paper_2609_38767_amd as dt
+    import workloads as W
+    from paper_2609_38767_amd.session import ProjectionSession
+    stream = torch.cuda.current_stream()
+    wl = W.WORKLOADS["crossgram"]
+    layers = wl["layers"]
+    out = {"workload": f"{len(layers)} Pythia-410M-shaped linear layers, {wl['n_train']} train x "
+                       f"{wl['n_query']} query, bf16", "per_T": {}}
+
+    def med_ms(fn):
+        for _ in range(warmup):
+            fn()
+        evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+               for _ in range(steps)]
+        for a, b in evs:
+            a.record(stream)
+            fn()
+            b.record(stream)
+        torch.cuda.synchronize()
+        t = sorted(a.elapsed_time(b) for a, b in evs)
+        return t[len(t) // 2]
+
+    for T in wl["T_sweep"]:
+        sess = {}
+        for side, n in (("train", wl["n_train"]), ("query", wl["n_query"])):
+            s = ProjectionSession(layers, dtype="bf16", seed=wl["seed"], device=dev)
+            for li, L in enumerate(layers):
+                A = W.draw((n, T, L["d_in"]), "normal", "bf16", dev, wl["seed"], "A", side, li, T)
+                B = W.draw((n, T, L["d_out"]), "normal", "bf16", dev, wl["seed"], "B", side, li, T)
+                s.capture(li, A, B)
+            sess[side] = s
+        a, b = sess["train"].ctx, sess["query"].ctx
+        K = torch.empty((wl["n_train"], wl["n_query"]), dtype=torch.float32, device=dev)
+        res = {}
+        for name, route in (("factored", dt.DATTRI_ROUTE_FACTORED), ("materialized", dt.DATTRI_ROUTE_MATERIALIZED),
+                            ("auto", dt.DATTRI_ROUTE_AUTO)):
+            ws = torch.empty(max(256, dt.dattri_cross_gram_workspace_bytes(a, b, route)), dtype=torch.uint8,
+                             device=dev)
+            res[name] = med_ms(lambda: dt.dattri_cross_gram(a, b, K, K.stride(0), ws, ws.numel(), route))
+            del ws
+        routes = [dt.dattri_cross_gram_route(a, b, li)[0] for li in range(len(layers))]
+        f_flops = sum(dt.dattri_cross_gram_costs(wl["n_train"], wl["n_query"], T, T, L["d_in"], L["d_out"], 2)[0]
+                      for L in layers)
+        m_flops = sum(dt.dattri_cross_gram_costs(wl["n_train"], wl["n_query"], T, T, L["d_in"], L["d_out"], 2)[1]
+                      for L in layers)
+        best = min(res["factored"], res["materialized"])
+        out["per_T"][str(T)] = {
+            "factored_ms": res["factored"], "materialized_ms": res["materialized"], "auto_ms": res["auto"],
+            "auto_layers_factored": sum(r == dt.DATTRI_ROUTE_FACTORED for r in routes),
+            "auto_layers_materialized": sum(r == dt.DATTRI_ROUTE_MATERIALIZED for r in routes),
+            "auto_regret": res["auto"] / best - 1.0,
+            "factored_tflops": f_flops / (res["factored"] * 1e-3) / 1e12,
+            "materialized_tflops": m_flops / (res["materialized"] * 1e-3) / 1e12}
+        print(f"[bench] crossgram T={T}: factored {res['factored']:.3f} ms, materialized "
+              f"{res['materialized']:.3f} ms, auto {res['auto']:.3f} ms", file=sys.stderr, flush=True)
+        for s in sess.values():
+            s.close()
+        del sess, K
+        torch.cuda.empty_cache()
+    return out
+
+
 def stream_reference(dev):
     """Achievable HBM rate on this GPU: a 1 GiB device-to-device copy (read +
     write bytes per second, best of 5)."""
@@ -361,6 +431,8 @@ def main():
         out["routing"] = routing_cases(dev, max(args.steps, 5), args.warmup)
     if args.phase in ("all", "gpt2"):
         out["gpt2"] = gpt2_case(dev, max(args.steps, 5), args.warmup)
+    if args.phase in ("all", "crossgram"):
+        out["crossgram_routing"] = crossgram_case(dev, max(min(args.steps, 5), 3), min(args.warmup, 1))
     if args.phase in ("all", "score"):
         for _ in range(args.warmup):
             score_step(False)

@@ -280,16 +280,23 @@ dattri_status dattri_layer_route(const dattri_ctx* ctx, int32_t layer, dattri_ro
  * Every layer must be captured in both; lengths apply as in projection. */
 
 /* Rates of the cross-Gram time model (MI355X-fitted defaults).  Predicted time
- * of a layer's route = sum over its kernels of max(flops / rate, bytes /
- * bandwidth) + launch_us per launch, with the FLOP and byte counts of
- * dattri_cross_gram_costs. */
+ * of a layer's route:
+ *   factored      max(tile_flops / ghost rate, tile_bytes / ghost bandwidth)
+ *                 + ghost_layer_us, where the kernel computes whole 128 x 128
+ *                 tiles of the token Gram (token rows padded to multiples of
+ *                 16): tile_flops = tiles * 2 * 128^2 (d_in + d_out + 1),
+ *                 tile_bytes = tiles * 2 * 128 (d_in + d_out) elt;
+ *   materialized  max(build_flops / build rate, build_bytes / build bandwidth)
+ *                 + dot_bytes / dot bandwidth + 4 launch_us,
+ * with build and product counts as in dattri_cross_gram_costs. */
 typedef struct {
-  double ghost_tflops;  /* factorized kernel (two token Grams and their product) */
-  double ghost_gbs;     /* its factor-block reads */
-  double build_tflops;  /* DW = B^T A kernel */
-  double build_gbs;     /* its factor reads plus float32 DW writes */
-  double dot_gbs;       /* Frobenius products over stored float32 DW */
-  double launch_us;     /* per kernel launch */
+  double ghost_tflops;   /* factorized kernel (two token Grams and their product) */
+  double ghost_gbs;      /* its factor-block reads */
+  double ghost_layer_us; /* fixed cost per layer inside the grouped factorized launch */
+  double build_tflops;   /* DW = B^T A kernel */
+  double build_gbs;      /* its factor reads plus float32 DW writes */
+  double dot_gbs;        /* Frobenius products over stored float32 DW */
+  double launch_us;      /* per kernel launch (the materialized route launches four per layer) */
 } dattri_crossgram_cost_model;
 
 dattri_status dattri_set_crossgram_cost_model(dattri_ctx* ctx, const dattri_crossgram_cost_model* m);

@@ -19,15 +19,19 @@ using namespace dattri;
 namespace dattri {
 
 dattri_crossgram_cost_model default_crossgram_cost_model() {
-  // Effective rates measured on MI355X (bf16 factor blocks) from a sweep of
-  // single-layer cross-Grams over transformer-sized layers and T = 16..2048.
+  // Effective rates measured on MI355X (bf16 factor blocks): both forced
+  // routes and the gradient build timed on 28 shapes (1024..4096-wide and
+  // 128-wide layers, T = 16..2048, 8 x 1, 16 x 16 and 8 x 8 batches), each
+  // a stack of 24 layers so the factorized route runs as one grouped launch,
+  // and fitted by least squares on log time.
   dattri_crossgram_cost_model m;
-  m.ghost_tflops = 400.0;
-  m.ghost_gbs = 2000.0;
-  m.build_tflops = 80.0;
-  m.build_gbs = 4000.0;
-  m.dot_gbs = 3000.0;
-  m.launch_us = 10.0;
+  m.ghost_tflops = 916.0;   // on whole padded tiles
+  m.ghost_gbs = 9300.0;
+  m.ghost_layer_us = 2.74;
+  m.build_tflops = 145.0;
+  m.build_gbs = 26000.0;
+  m.dot_gbs = 2230.0;
+  m.launch_us = 14.7;
   return m;
 }
 
@@ -70,7 +74,8 @@ void xpredict(const dattri_crossgram_cost_model& m, int64_t na, int64_t nb, int6
   const double tflops = (double)tiles * 2.0 * kGhostTile * kGhostTile * (double)(di + dq + 1);
   const double tbytes = (double)tiles * 2.0 * kGhostTile * (double)(di + dq) * elt;
   *f_us = (tiles == 0) ? 0.0
-                       : std::max(tflops / (m.ghost_tflops * 1e6), tbytes / (m.ghost_gbs * 1e3));
+                       : std::max(tflops / (m.ghost_tflops * 1e6), tbytes / (m.ghost_gbs * 1e3)) +
+                             m.ghost_layer_us;
   const double build = std::max((double)c.build_flops / (m.build_tflops * 1e6),
                                 (double)c.build_bytes / (m.build_gbs * 1e3));
   *m_us = build + (double)c.dot_bytes / (m.dot_gbs * 1e3) + 4.0 * m.launch_us;
@@ -313,8 +318,9 @@ dattri_status dattri_set_crossgram_cost_model(dattri_ctx* ctx, const dattri_cros
   const double v[] = {m->ghost_tflops, m->ghost_gbs, m->build_tflops, m->build_gbs, m->dot_gbs};
   for (double x : v)
     if (!(x > 0) || !std::isfinite(x)) return fail(DATTRI_E_INVALID_ARG, "rates must be finite and > 0");
-  if (!(m->launch_us >= 0) || !std::isfinite(m->launch_us))
-    return fail(DATTRI_E_INVALID_ARG, "launch_us must be finite and >= 0");
+  if (!(m->launch_us >= 0) || !std::isfinite(m->launch_us) || !(m->ghost_layer_us >= 0) ||
+      !std::isfinite(m->ghost_layer_us))
+    return fail(DATTRI_E_INVALID_ARG, "launch_us and ghost_layer_us must be finite and >= 0");
   ctx->xcost = *m;
   return DATTRI_OK;
 }

@@ -95,11 +95,12 @@ def test_validation_before_any_launch():
 
 def test_route_regimes_and_cost_model():
     # App. A.4 "Regimes": short sequences and wide layers favour the
-    # factorized route, long sequences the materialized one
+    # factorized route, long sequences the materialized one (with the MI355X
+    # rates the crossover for 8 x 1 batches of this layer lies past T = 2048)
     short = _ctx([(1024, 4096)], 8, 32)
     q_short = _ctx([(1024, 4096)], 1, 32)
-    long_ = _ctx([(1024, 4096)], 8, 2048)
-    q_long = _ctx([(1024, 4096)], 1, 2048)
+    long_ = _ctx([(1024, 4096)], 8, 8192)
+    q_long = _ctx([(1024, 4096)], 1, 8192)
     try:
         r, f, m = dt.dattri_cross_gram_route(short, q_short, 0)
         assert r == dt.DATTRI_ROUTE_FACTORED and f < m

@@ -27,6 +27,13 @@ Workloads (synthetic stand-ins; no dataset or checkpoint is used):
 * ``score``     Phi_train 200000 x 8192 and Phi_query 2048 x 8192, bf16 N(0,1);
                 positive diagonal preconditioner log-uniform on [1e-3, 1e3];
                 fp32 scores plus per-query top-100.
+* ``crossgram`` unprojected cross-Gram routing sweep: 24 Pythia-410M-shaped
+                blocks, each with linear layers 1024->3072 (query/key/value),
+                1024->1024 (attention output), 1024->4096 and 4096->1024 (MLP)
+                (96 layers); 8 training examples against 1 query, T in
+                {32, 128, 512, 2048}, bf16 N(0,1) factors.  Stands in for the
+                routing ablation over sequence length on Pythia-410M /
+                WikiText-103 (App. B, "Routing Across Sequence Lengths").
 """
 
 import hashlib
@@ -63,6 +70,16 @@ def _llama_layers(k=32, blocks=32):
     return out
 
 
+def _pythia_layers(blocks=24):
+    out = []
+    for b in range(blocks):
+        out += [_layer(f"l{b}.attention.query_key_value", 1024, 3072, 1, 1, f"l{b}.ln_attn"),
+                _layer(f"l{b}.attention.dense", 1024, 1024, 1, 1, f"l{b}.attn_core"),
+                _layer(f"l{b}.mlp.dense_h_to_4h", 1024, 4096, 1, 1, f"l{b}.ln_mlp"),
+                _layer(f"l{b}.mlp.dense_4h_to_h", 4096, 1024, 1, 1, f"l{b}.act")]
+    return out
+
+
 WORKLOADS = {
     "tiny": {"layers": [_layer("fc", 64, 64, 8, 8, "fc.in")], "T": 16,
              "batch": 12, "n_train": 8, "n_query": 4, "dtype": "f32",
@@ -84,6 +101,9 @@ WORKLOADS = {
                "dist_b": "normal", "b_scale": 1.0, "seed": 6},
     "score": {"n_train": 200000, "n_query": 2048, "F": 8192, "dtype": "bf16",
               "topk": 100, "d_log10_range": (-3.0, 3.0), "seed": 7},
+    "crossgram": {"layers": _pythia_layers(), "T_sweep": (32, 128, 512, 2048), "n_train": 8,
+                  "n_query": 1, "dtype": "bf16", "dist_a": "normal", "dist_b": "normal",
+                  "b_scale": 1.0, "seed": 8},
 }
 
 TORCH_DTYPE = {"f32": torch.float32, "bf16": torch.bfloat16}

@@ -25,13 +25,13 @@ dattri_crossgram_cost_model default_crossgram_cost_model() {
   // a stack of 24 layers so the factorized route runs as one grouped launch,
   // and fitted by least squares on log time.
   dattri_crossgram_cost_model m;
-  m.ghost_tflops = 916.0;   // on whole padded tiles
-  m.ghost_gbs = 9300.0;
-  m.ghost_layer_us = 2.74;
-  m.build_tflops = 145.0;
-  m.build_gbs = 26000.0;
-  m.dot_gbs = 2230.0;
-  m.launch_us = 14.7;
+  m.ghost_tflops = 598.0;   // on whole padded tiles
+  m.ghost_gbs = 10500.0;
+  m.ghost_layer_us = 2.73;
+  m.build_tflops = 725.0;
+  m.build_gbs = 95600.0;
+  m.dot_gbs = 1870.0;
+  m.launch_us = 15.1;
   return m;
 }
 

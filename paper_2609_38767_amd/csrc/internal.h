@@ -145,6 +145,9 @@ struct GradArgs {
   float* G;                         // [ex_count, d_out, d_in]
 };
 hipError_t launch_gradient(int elt_bytes, const GradArgs& a, hipStream_t s);
+// bf16 with 16-byte aligned rows (A, B bases and d_in, d_out multiples of 8): the
+// LDS-transpose kernel; launch_gradient dispatches to it.
+hipError_t launch_gradient_tr(const GradArgs& a, hipStream_t s);
 
 struct GProjArgs {
   const float* G;                   // [ex_count, d_out, d_in]

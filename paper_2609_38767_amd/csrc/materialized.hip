@@ -215,6 +215,7 @@ __global__ __launch_bounds__(256, 2) void gproject_kernel(GProjArgs a) {
 }
 
 hipError_t launch_gradient(int elt, const GradArgs& a, hipStream_t s) {
+  if (elt == 2 && a.aligned) return launch_gradient_tr(a, s);
   constexpr int kMaxZ = 65535;  // grid z limit: launch examples in slices
   for (int e0 = 0; e0 < a.ex_count; e0 += kMaxZ) {
     GradArgs c = a;

@@ -53,13 +53,13 @@ dattri_cost_model default_cost_model() {
   // layers, T = 16..2048) and fitted by least squares on log time.  Small
   // problems are dominated by the fixed per-call cost, which launch_us absorbs.
   dattri_cost_model m;
-  m.factored_tflops = 560.0;
-  m.factored_gbs = 1100.0;
-  m.gradient_tflops = 150.0;
-  m.gradient_gbs = 7600.0;
-  m.gproject_tflops = 67.0;
-  m.gproject_gbs = 27000.0;
-  m.launch_us = 19.0;
+  m.factored_tflops = 297.0;
+  m.factored_gbs = 972.0;
+  m.gradient_tflops = 726.0;
+  m.gradient_gbs = 8460.0;
+  m.gproject_tflops = 64.5;
+  m.gproject_gbs = 9520.0;
+  m.launch_us = 16.1;
   return m;
 }
 

@@ -22,6 +22,9 @@ Modules
 ``crossgram``  cross-Gram matrices and squared norms of unprojected per-example
                gradients summed over layers, by the factorized route (Eq. 4)
                and through dense gradients (Eq. 1).
+``kfac``       K-FAC / EK-FAC curvature on projected factors: factor
+               covariances, eigenbases, EK-FAC's eigenvalue correction,
+               damping and preconditioned scores (Sec. 3.2, App. A.2, App. B).
 
 Parity status of each function is stated in its docstring; the one function
 with no pin to the paper is the seed/counter layout of the generator, which the
@@ -29,4 +32,4 @@ paper leaves unspecified ("parity unpinned" w.r.t. the paper, pinned to the
 published Philox / SplitMix64 definitions instead).
 """
 
-from . import rng, gradients, scoring, cost, crossgram  # noqa: F401
+from . import rng, gradients, scoring, cost, crossgram, kfac  # noqa: F401

@@ -23,6 +23,8 @@
  *   - GradDot scoring (Sec. 4.1; gradient similarity, Sec. 2) with an optional
  *     positive diagonal preconditioner: S = (Phi_q diag(d)) Phi_train^T, and
  *     per-query top-k.
+ *   - Sec. 3.2 / App. A.2 / App. B: K-FAC and EK-FAC curvature fitted on the
+ *     projected factors, and queries preconditioned with it before scoring.
  *
  * Conventions for every entry point
  *   - All functions are extern "C" and never throw or abort; each returns a
@@ -398,6 +400,105 @@ dattri_status dattri_score(const void* phi_q, int64_t n_q, int64_t ld_q, const v
                            const float* dev_precond_diag, float* scores, int32_t topk,
                            int32_t* topk_idx, float* topk_val, void* workspace, size_t ws_bytes,
                            void* stream);
+
+/* ------------------------------------------------ K-FAC / EK-FAC curvature */
+
+/* Kronecker-factored curvature on projected factors.  Sec. 3.2 names the
+ * preconditioned comparisons of K-FAC (Martens & Grosse, 2015) and EK-FAC
+ * (George et al., 2018) among the operations on factorized gradients, and
+ * App. A.2 ("Factor projection") applies them unchanged to the projected
+ * pair a~_t = P_in^T a_t, g~_t = P_out^T g_t.  Per layer:
+ *
+ *   input factor     A = (1/N_tok) sum over examples and tokens of a~ a~^T
+ *   gradient factor  S = (1/N)     sum over examples and tokens of g~ g~^T
+ *   eigenbases       A = Q_A diag(lam_A) Q_A^T,  S = Q_G diag(lam_G) Q_G^T
+ *   eigenvalues      K-FAC   E[c][r] = lam_A[c] lam_G[r]
+ *                    EK-FAC  E[c][r] = (1/N) sum_i ((Q_A^T Psi_i Q_G)[c][r])^2
+ *   damping          delta = rel * mean(E) + abs   (App. B: rel = 0.1)
+ *   preconditioned   P(Psi_q) = Q_A [(Q_A^T Psi_q Q_G) / (E + delta)] Q_G^T
+ *
+ * with Psi the layer's k_in x k_out block of phi (Eq. (2)), N_tok the token
+ * positions and N the examples summed.  Scores of preconditioned queries
+ * against training features come from dattri_score with no diagonal: the sum
+ * over layers of <P(Psi_q), Psi_j>_F.
+ *
+ * All statistics live in one caller-owned device buffer, the curvature state
+ * (dattri_curvature_state_bytes, 256-byte aligned).  Its per-layer fields are
+ * at the byte offsets of dattri_curvature_layout_of; matrices are float32
+ * row-major.  Sums accumulate over calls until dattri_curvature_reset.
+ * Layers need k_in <= 64 and k_out <= 64 (else UNSUPPORTED). */
+typedef enum { DATTRI_CURV_KFAC = 0, DATTRI_CURV_EKFAC = 1 } dattri_curvature;
+
+typedef struct {
+  int64_t sum_a;   /* float32 [k_in][k_in]:  sum of a~ a~^T                         */
+  int64_t sum_g;   /* float32 [k_out][k_out]: sum of g~ g~^T                        */
+  int64_t sum_e;   /* float32 [k_in][k_out]: sum over examples of (Q_A^T Psi Q_G)^2 */
+  int64_t q_a;     /* float32 [k_in][k_in]: column j = eigenvector of lam_a[j]      */
+  int64_t lam_a;   /* float32 [k_in], ascending                                     */
+  int64_t q_g;     /* float32 [k_out][k_out]                                        */
+  int64_t lam_g;   /* float32 [k_out], ascending                                    */
+  int64_t counts;  /* int64 [3]: N_tok of sum_a, N of sum_g, N of sum_e             */
+} dattri_curvature_layout;
+
+/* Bytes of the curvature state of every registered layer.
+ * Errors: INVALID_ARG, UNSUPPORTED (a layer with k_in or k_out > 64). */
+dattri_status dattri_curvature_state_bytes(const dattri_ctx* ctx, size_t* bytes);
+dattri_status dattri_curvature_layout_of(const dattri_ctx* ctx, int32_t layer,
+                                         dattri_curvature_layout* out);
+
+/* Zero every sum and count of a state (a fill kernel; no memset node). */
+dattri_status dattri_curvature_reset(const dattri_ctx* ctx, void* state, void* stream);
+
+/* Adds the projected factor sums of the current captures of every layer
+ * (sum_a, sum_g and their counts; token rows past lengths[i] are left out).
+ * One pass over A and B per layer side, each token row projected with the
+ * layer's maps and its outer product accumulated in float32; the order of
+ * every sum is fixed (deterministic, no atomics).
+ *   workspace: >= dattri_curvature_fit_workspace_bytes(ctx), 256-byte aligned.
+ * Errors: INVALID_ARG, STATE (maps not bound, captures missing or
+ * inconsistent), WORKSPACE, UNSUPPORTED, HIP. */
+dattri_status dattri_curvature_fit_workspace_bytes(const dattri_ctx* ctx, size_t* bytes);
+dattri_status dattri_curvature_accumulate_factors(dattri_ctx* ctx, void* state, void* workspace,
+                                                  size_t ws_bytes, void* stream);
+
+/* Eigendecomposition of every layer's normalized factors A and S (cyclic
+ * parallel Jacobi in float64 on the GPU, one workgroup per factor, until the
+ * off-diagonal mass falls below 1e-26 of the total or 32 sweeps); writes q_a,
+ * lam_a, q_g, lam_g.  A factor with a zero count yields zeros and Q = I.
+ * Errors: INVALID_ARG, UNSUPPORTED, HIP. */
+dattri_status dattri_curvature_eigen(const dattri_ctx* ctx, void* state, void* stream);
+
+/* EK-FAC's eigenvalue correction: adds, for every layer, the squared blocks
+ * of n training rows of phi rotated into the layer's eigenbasis (needs
+ * dattri_curvature_eigen first) to sum_e, and n to its count.
+ *   phi: device [n rows of F] of dtype (F32 or BF16), rows ld elements apart
+ *        (ld >= F).
+ *   workspace: >= dattri_curvature_ekfac_workspace_bytes(ctx, n), 256-byte aligned.
+ * Errors: INVALID_ARG, DTYPE, SHAPE, WORKSPACE, UNSUPPORTED, HIP. */
+dattri_status dattri_curvature_ekfac_workspace_bytes(const dattri_ctx* ctx, int64_t n,
+                                                     size_t* bytes);
+dattri_status dattri_curvature_accumulate_ekfac(const dattri_ctx* ctx, void* state,
+                                                const void* phi, dattri_dtype dtype, int64_t n,
+                                                int64_t ld, void* workspace, size_t ws_bytes,
+                                                void* stream);
+
+/* Preconditioned query features: every layer block of n_q rows of phi_q
+ * replaced by P(Psi_q) for curvature `kind` with damping
+ * delta = damping_rel * mean(E) + damping_abs, computed in float32 and
+ * written as out_dtype (bf16 rounded once).  EK-FAC needs
+ * dattri_curvature_accumulate_ekfac first (with no correction its eigenvalues
+ * read as zero); both kinds need dattri_curvature_eigen.
+ *   phi_q: device [n_q rows of F] of in_dtype, rows ld_q apart (>= F)
+ *   out:   device [n_q rows of F] of out_dtype, rows ld_out apart (>= F);
+ *          columns >= F are not written; out must not overlap phi_q.
+ * Errors: INVALID_ARG (damping_rel < 0, damping_abs < 0 or both zero),
+ * DTYPE, SHAPE, UNSUPPORTED, HIP. */
+dattri_status dattri_curvature_precondition(const dattri_ctx* ctx, const void* state,
+                                            dattri_curvature kind, double damping_rel,
+                                            double damping_abs, const void* phi_q,
+                                            dattri_dtype in_dtype, int64_t n_q, int64_t ld_q,
+                                            void* out, dattri_dtype out_dtype, int64_t ld_out,
+                                            void* stream);
 
 #ifdef __cplusplus
 }

@@ -26,11 +26,17 @@ __all__ = [
     "dattri_set_crossgram_cost_model", "dattri_get_crossgram_cost_model", "dattri_cross_gram_costs",
     "dattri_cross_gram_route", "dattri_cross_gram_workspace_bytes", "dattri_cross_gram",
     "dattri_sq_norms_workspace_bytes", "dattri_gradient_sq_norms",
+    "DATTRI_CURV_KFAC", "DATTRI_CURV_EKFAC", "CurvatureLayout",
+    "dattri_curvature_state_bytes", "dattri_curvature_layout_of", "dattri_curvature_reset",
+    "dattri_curvature_fit_workspace_bytes", "dattri_curvature_accumulate_factors",
+    "dattri_curvature_eigen", "dattri_curvature_ekfac_workspace_bytes",
+    "dattri_curvature_accumulate_ekfac", "dattri_curvature_precondition",
 ]
 
 DATTRI_F32, DATTRI_BF16 = 0, 1
 DATTRI_ROUTE_AUTO, DATTRI_ROUTE_FACTORED, DATTRI_ROUTE_MATERIALIZED = 0, 1, 2
 DATTRI_FORM_AUTO, DATTRI_FORM_FUSED, DATTRI_FORM_SPLIT = 0, 1, 2
+DATTRI_CURV_KFAC, DATTRI_CURV_EKFAC = 0, 1
 STATUS_NAMES = {0: "OK", -1: "E_INVALID_ARG", -2: "E_SHAPE", -3: "E_DTYPE", -4: "E_STATE",
                 -5: "E_WORKSPACE", -6: "E_HIP", -7: "E_UNSUPPORTED"}
 
@@ -56,6 +62,11 @@ class CrossgramCostModel(ctypes.Structure):
     _fields_ = [("ghost_tflops", ctypes.c_double), ("ghost_gbs", ctypes.c_double),
                 ("ghost_layer_us", ctypes.c_double), ("build_tflops", ctypes.c_double), ("build_gbs", ctypes.c_double),
                 ("dot_gbs", ctypes.c_double), ("launch_us", ctypes.c_double)]
+
+
+class CurvatureLayout(ctypes.Structure):
+    _fields_ = [(name, ctypes.c_int64) for name in
+                ("sum_a", "sum_g", "sum_e", "q_a", "lam_a", "q_g", "lam_g", "counts")]
 
 
 _i32, _i64, _u64, _sz = ctypes.c_int32, ctypes.c_int64, ctypes.c_uint64, ctypes.c_size_t
@@ -99,6 +110,16 @@ _SIGS = {
     "dattri_gradient_sq_norms": (_i32, [_vp, _vp, _vp, _sz, _i32, _vp]),
     "dattri_score": (_i32, [_vp, _i64, _i64, _vp, _i64, _i64, _i64, _i32, _vp, _vp, _i32, _vp, _vp,
                             _vp, _sz, _vp]),
+    "dattri_curvature_state_bytes": (_i32, [_vp, _P(_sz)]),
+    "dattri_curvature_layout_of": (_i32, [_vp, _i32, _P(CurvatureLayout)]),
+    "dattri_curvature_reset": (_i32, [_vp, _vp, _vp]),
+    "dattri_curvature_fit_workspace_bytes": (_i32, [_vp, _P(_sz)]),
+    "dattri_curvature_accumulate_factors": (_i32, [_vp, _vp, _vp, _sz, _vp]),
+    "dattri_curvature_eigen": (_i32, [_vp, _vp, _vp]),
+    "dattri_curvature_ekfac_workspace_bytes": (_i32, [_vp, _i64, _P(_sz)]),
+    "dattri_curvature_accumulate_ekfac": (_i32, [_vp, _vp, _vp, _i32, _i64, _i64, _vp, _sz, _vp]),
+    "dattri_curvature_precondition": (_i32, [_vp, _vp, _i32, _dbl, _dbl, _vp, _i32, _i64, _i64, _vp, _i32,
+                                             _i64, _vp]),
 }
 EXPORTED = tuple(_SIGS)
 
@@ -348,3 +369,57 @@ def dattri_sq_norms_workspace_bytes(ctx, route=DATTRI_ROUTE_AUTO):
 def dattri_gradient_sq_norms(ctx, out, workspace, ws_bytes, route=DATTRI_ROUTE_AUTO, stream=None):
     _check(load().dattri_gradient_sq_norms(ctx, _ptr(out), _ptr(workspace), ws_bytes, route, _stream(stream)),
            "dattri_gradient_sq_norms")
+
+
+def dattri_curvature_state_bytes(ctx):
+    v = _sz()
+    _check(load().dattri_curvature_state_bytes(ctx, ctypes.byref(v)), "dattri_curvature_state_bytes")
+    return v.value
+
+
+def dattri_curvature_layout_of(ctx, layer):
+    f = CurvatureLayout()
+    _check(load().dattri_curvature_layout_of(ctx, layer, ctypes.byref(f)), "dattri_curvature_layout_of")
+    return {name: getattr(f, name) for name, _ in CurvatureLayout._fields_}
+
+
+def dattri_curvature_reset(ctx, state, stream=None):
+    _check(load().dattri_curvature_reset(ctx, _ptr(state), _stream(stream)), "dattri_curvature_reset")
+
+
+def dattri_curvature_fit_workspace_bytes(ctx):
+    v = _sz()
+    _check(load().dattri_curvature_fit_workspace_bytes(ctx, ctypes.byref(v)),
+           "dattri_curvature_fit_workspace_bytes")
+    return v.value
+
+
+def dattri_curvature_accumulate_factors(ctx, state, workspace, ws_bytes, stream=None):
+    _check(load().dattri_curvature_accumulate_factors(ctx, _ptr(state), _ptr(workspace), ws_bytes,
+                                                      _stream(stream)),
+           "dattri_curvature_accumulate_factors")
+
+
+def dattri_curvature_eigen(ctx, state, stream=None):
+    _check(load().dattri_curvature_eigen(ctx, _ptr(state), _stream(stream)), "dattri_curvature_eigen")
+
+
+def dattri_curvature_ekfac_workspace_bytes(ctx, n):
+    v = _sz()
+    _check(load().dattri_curvature_ekfac_workspace_bytes(ctx, n, ctypes.byref(v)),
+           "dattri_curvature_ekfac_workspace_bytes")
+    return v.value
+
+
+def dattri_curvature_accumulate_ekfac(ctx, state, phi, dtype, n, ld, workspace, ws_bytes, stream=None):
+    _check(load().dattri_curvature_accumulate_ekfac(ctx, _ptr(state), _ptr(phi), dtype, n, ld, _ptr(workspace),
+                                                    ws_bytes, _stream(stream)),
+           "dattri_curvature_accumulate_ekfac")
+
+
+def dattri_curvature_precondition(ctx, state, kind, damping_rel, damping_abs, phi_q, in_dtype, n_q, ld_q,
+                                  out, out_dtype, ld_out, stream=None):
+    _check(load().dattri_curvature_precondition(ctx, _ptr(state), kind, damping_rel, damping_abs, _ptr(phi_q),
+                                                in_dtype, n_q, ld_q, _ptr(out), out_dtype, ld_out,
+                                                _stream(stream)),
+           "dattri_curvature_precondition")

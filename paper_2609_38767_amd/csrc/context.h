@@ -38,4 +38,7 @@ struct dattri_ctx {
   dattri_factored_form form = DATTRI_FORM_AUTO;
   std::vector<uint8_t> blob;     // host copy of the last uploaded projection plan
   std::vector<uint8_t> xg_blob;  // host copy of the last uploaded cross-Gram plan
+  // host copy of the last uploaded curvature tables (uploads from calls that
+  // take the context as const)
+  mutable std::vector<uint8_t> curv_blob;
 };

@@ -229,4 +229,62 @@ constexpr int kTopkMax = 1024;
 hipError_t launch_topk(const float* S, int64_t n_q, int64_t n_train, int32_t k, int32_t* idx,
                        float* val, hipStream_t s);
 
+// ---------------------------------------------------- K-FAC / EK-FAC curvature
+constexpr int kCurvMaxK = 64;       // k_in, k_out limit of the curvature kernels
+
+// Factor sums: one op per layer side (X = A with P_in, or X = B with P_out).
+// Work item = a run of consecutive units u = example * n_chunks + chunk of one
+// op; each wave of the item writes one partial (nt*16)^2 float32 sum.
+struct FsumOp {
+  const void* X;                    // [n, T, d]
+  const int32_t* lengths;           // [n] or null
+  const void* P;                    // packed [d x k] map
+  int32_t d, T, n, nt;              // nt = 16-column tiles of the map
+  int32_t chunk_rows, n_chunks, aligned, pad0;
+  int64_t partial_base;             // float offset of the op's first partial
+};
+struct FsumItem { int32_t op, unit0, n_units, part; };  // n_units 0: padding item
+// One launch per instance (elt, aligned, tiles); rows per wave from fsum_rt.
+hipError_t launch_fsum(int elt_bytes, int aligned, int nt, const FsumItem* items, int n_items,
+                       const FsumOp* ops, float* partials, hipStream_t s);
+int fsum_nt_instance(int nt_req);   // tiles of the instance serving nt_req tiles
+int fsum_rows_per_wave(int nt_inst);
+
+// dst (float32 [rows][cols] at byte offset dst_off of the state) += the sum,
+// in part order, of n_parts partials [rows][ldp] part_floats apart; one counter
+// (int64 at count_off, if >= 0) += sum of lengths clamped to [0, T] over n
+// entries, or count_add when lengths is null.
+struct StatTask {
+  int64_t part_base, dst_off, count_off, count_add;
+  const int32_t* lengths;
+  int32_t n_parts, part_floats, ldp, rows, cols, n_len, T, pad0;
+};
+hipError_t launch_stat_reduce(const StatTask* tasks, int n_tasks, int max_out, const float* parts,
+                              uint8_t* state, hipStream_t s);
+
+// Symmetric eigendecomposition of sum / count (k x k, k <= kCurvMaxK).
+struct EigTask { int64_t sum_off, count_off, q_off, lam_off; int32_t k, pad0; };
+hipError_t launch_eigen(const EigTask* tasks, int n_tasks, uint8_t* state, hipStream_t s);
+
+// Rotated-block kernels: per layer, the block of phi at column col and the
+// layer's fields in the state.
+struct RotTask {
+  int64_t col;                      // first column of the layer block in phi
+  int64_t q_a, lam_a, q_g, lam_g, sum_e, counts;  // state byte offsets
+  int64_t part_base;                // EK-FAC: float offset of the layer's partials
+  int32_t k_in, k_out, n_blocks, pad0;
+};
+// parts[part_base + b*k_in*k_out ...] = sum over rows [b*rows_per_block, ...)
+// of (Q_A^T Psi Q_G)^2; grid (max_blocks, n_tasks).
+hipError_t launch_ekfac(const RotTask* tasks, int n_tasks, int max_blocks, const uint8_t* state,
+                        const void* phi, int phi_bf16, int64_t ld, int64_t n, int rows_per_block,
+                        float* parts, hipStream_t s);
+// out rows = P(Psi_q) per layer; kind 0 K-FAC, 1 EK-FAC.
+hipError_t launch_precondition(const RotTask* tasks, int n_tasks, const uint8_t* state, int kind,
+                               double rel, double abs_, const void* phi_q, int in_bf16,
+                               int64_t ld_q, int64_t n_q, void* out, int out_bf16, int64_t ld_out,
+                               hipStream_t s);
+// Zero `bytes` bytes (a multiple of 16, 16-byte aligned) with a fill kernel.
+hipError_t launch_zero(void* p, int64_t bytes, hipStream_t s);
+
 }  // namespace dattri

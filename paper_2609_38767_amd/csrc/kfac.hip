@@ -1,0 +1,592 @@
+// Kronecker-factored curvature on projected factors (K-FAC, EK-FAC):
+// factor sums, their eigendecomposition, EK-FAC's eigenvalue correction and
+// the preconditioning of query blocks.
+//
+// fsum_kernel        sum over token rows of x~ x~^T with x~ = P^T x, for one
+//                    side of a layer (x = a_t with P_in, or g_t with P_out).
+//                    Token rows are projected exactly as in the factored route
+//                    (project_rows: bf16/f32 MFMA on fragments streamed from
+//                    HBM, map panels shared through LDS); the projected tiles
+//                    stay in accumulators and their outer products are summed
+//                    with float32 MFMA (16x16x4), whose C layout gives every
+//                    element index a K = 4 slice of token rows for both
+//                    operands.  Only tiles on and above the diagonal are
+//                    accumulated; the partial block is written mirrored.
+// stat_reduce_kernel fixed-order sum of partial blocks into the state.
+// eigen_kernel       cyclic Jacobi in float64, one workgroup per matrix: each
+//                    round applies n/2 rotations on disjoint index pairs (the
+//                    round-robin ordering), rows then columns of the LDS copy,
+//                    and accumulates the rotations into V.
+// ekfac_kernel       sum over training rows of (Q_A^T Psi Q_G)^2.
+// precond_kernel     Q_A [(Q_A^T Psi Q_G) / (E + delta)] Q_G^T per query block.
+#include <math.h>
+
+#include "device_common.h"
+#include "internal.h"
+#include "project_rows.h"
+
+namespace dattri {
+using namespace dev;
+
+// ------------------------------------------------------------ factor sums
+constexpr int fsum_rt(int nt) { return nt <= 2 ? 4 : 2; }
+
+template <int ELT, bool AL, int NT>
+__global__ __launch_bounds__(256, 2) void fsum_kernel(const FsumItem* __restrict__ items,
+                                                      const FsumOp* __restrict__ ops,
+                                                      float* __restrict__ partials) {
+  constexpr int RT = fsum_rt(NT);
+  constexpr int PD = AL ? (RT >= 4 ? 2 : 4) : 2;
+  __shared__ __align__(16) uint8_t pan[2][kPanel][NT][kFragBytes];
+  const FsumItem it = items[blockIdx.x];
+  if (it.n_units <= 0) return;  // padding item of the XCD-interleaved order
+  const FsumOp& O = ops[it.op];
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int g = lane >> 4, m16 = lane & 15;
+  const int nt = O.nt, d = O.d, T = O.T;
+
+  FragSrc<NT> P;
+  P.nt = nt;
+#pragma unroll
+  for (int t = 0; t < NT; ++t) {
+    P.base[t] = (const uint8_t*)O.P + (int64_t)(t < nt ? t : 0) * kFragBytes;
+    P.stride[t] = (int64_t)nt * kFragBytes;
+  }
+  f32x4 cov[NT][NT];
+#pragma unroll
+  for (int a = 0; a < NT; ++a)
+#pragma unroll
+    for (int b = 0; b < NT; ++b) cov[a][b] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+  for (int u = it.unit0; u < it.unit0 + it.n_units; ++u) {
+    const int ex = u / O.n_chunks, ch = u - ex * O.n_chunks;
+    int t_eff = T;
+    if (O.lengths) t_eff = min(max(O.lengths[ex], 0), T);
+    const int row_begin = ch * O.chunk_rows;
+    const int row_end = min(row_begin + O.chunk_rows, t_eff);
+    const int rows_valid = max(row_end, 0);
+    const uint8_t* base = (const uint8_t*)O.X + (size_t)ex * T * d * ELT;
+    const rsrc_t r = make_rsrc(base, (uint32_t)((int64_t)rows_valid * d * ELT));
+    // sub-chunks: a uniform trip count for all waves (barriers inside)
+    for (int sub = row_begin; sub < row_end; sub += kWaves * RT * 16) {
+      const int r_wave = sub + wave * RT * 16;
+      f32x4 acc[RT][NT];
+#pragma unroll
+      for (int rt = 0; rt < RT; ++rt)
+#pragma unroll
+        for (int t = 0; t < NT; ++t) acc[rt][t] = f32x4{0.f, 0.f, 0.f, 0.f};
+      project_rows<ELT, AL, RT, NT, NT, PD>(r, r_wave, rows_valid, d, d, P, acc, pan);
+#pragma unroll
+      for (int rt = 0; rt < RT; ++rt)
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+#pragma unroll
+          for (int ta = 0; ta < NT; ++ta)
+#pragma unroll
+            for (int tb = ta; tb < NT; ++tb)
+              if (tb < nt) cov[ta][tb] = mfma_f32_4(acc[rt][ta][j], acc[rt][tb][j], cov[ta][tb]);
+    }
+  }
+
+  // partial block (nt*16)^2 of this wave; 16x16 C layout: lane (g, n) holds
+  // rows 4g..4g+3 of column n
+  const int kp = nt * 16;
+  float* dst = partials + O.partial_base + ((int64_t)it.part * kWaves + wave) * kp * kp;
+#pragma unroll
+  for (int ta = 0; ta < NT; ++ta)
+#pragma unroll
+    for (int tb = ta; tb < NT; ++tb) {
+      if (tb < nt) {
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          dst[(ta * 16 + 4 * g + i) * kp + tb * 16 + m16] = cov[ta][tb][i];
+          if (tb != ta) dst[(tb * 16 + m16) * kp + ta * 16 + 4 * g + i] = cov[ta][tb][i];
+        }
+      }
+    }
+}
+
+int fsum_nt_instance(int nt_req) { return nt_req <= 1 ? 1 : (nt_req <= 2 ? 2 : 4); }
+int fsum_rows_per_wave(int nt_inst) { return fsum_rt(nt_inst); }
+
+hipError_t launch_fsum(int elt, int aligned, int nt, const FsumItem* items, int n_items,
+                       const FsumOp* ops, float* partials, hipStream_t s) {
+  if (n_items <= 0) return hipSuccess;
+#define DATTRI_FSUM(E, A, N)                                                                   \
+  if (elt == E && (aligned != 0) == A && nt == N) {                                            \
+    hipLaunchKernelGGL((fsum_kernel<E, A, N>), dim3(n_items), dim3(256), 0, s, items, ops, partials); \
+    return hipGetLastError();                                                                  \
+  }
+  DATTRI_FSUM(2, true, 1) DATTRI_FSUM(2, true, 2) DATTRI_FSUM(2, true, 4)
+  DATTRI_FSUM(2, false, 1) DATTRI_FSUM(2, false, 2) DATTRI_FSUM(2, false, 4)
+  DATTRI_FSUM(4, true, 1) DATTRI_FSUM(4, true, 2) DATTRI_FSUM(4, true, 4)
+  DATTRI_FSUM(4, false, 1) DATTRI_FSUM(4, false, 2) DATTRI_FSUM(4, false, 4)
+#undef DATTRI_FSUM
+  return hipErrorInvalidValue;
+}
+
+// ------------------------------------------------------------- reductions
+__global__ __launch_bounds__(256) void stat_reduce_kernel(const StatTask* __restrict__ tasks,
+                                                          const float* __restrict__ parts,
+                                                          uint8_t* __restrict__ state) {
+  __shared__ float red[4][64];
+  const StatTask t = tasks[blockIdx.x];
+  const int el = threadIdx.x & 63, pl = threadIdx.x >> 6;
+  const int n_out = t.rows * t.cols;
+  float* dst = (float*)(state + t.dst_off);
+  const float* base = parts + t.part_base;
+  for (int e0 = blockIdx.y * 64; e0 < n_out; e0 += gridDim.y * 64) {  // uniform trip count
+    const int e = e0 + el;
+    float s = 0.f;
+    if (e < n_out) {
+      const int r = e / t.cols, c = e - r * t.cols;
+      const float* p = base + (int64_t)r * t.ldp + c;
+      const int64_t step = t.part_floats;
+      int q = pl;
+      for (; q + 12 < t.n_parts; q += 16) {
+        const float v0 = p[q * step], v1 = p[(q + 4) * step], v2 = p[(q + 8) * step],
+                    v3 = p[(q + 12) * step];
+        s = (((s + v0) + v1) + v2) + v3;
+      }
+      for (; q < t.n_parts; q += 4) s += p[q * step];
+    }
+    red[pl][el] = s;
+    __syncthreads();
+    if (pl == 0 && e < n_out) dst[e] += ((red[0][el] + red[1][el]) + red[2][el]) + red[3][el];
+    __syncthreads();
+  }
+  if (blockIdx.y == 0 && threadIdx.x == 0 && t.count_off >= 0) {
+    int64_t add = t.count_add;
+    if (t.lengths) {
+      add = 0;
+      for (int i = 0; i < t.n_len; ++i) add += min(max(t.lengths[i], 0), t.T);
+    }
+    *(int64_t*)(state + t.count_off) += add;
+  }
+}
+
+hipError_t launch_stat_reduce(const StatTask* tasks, int n_tasks, int max_out, const float* parts,
+                              uint8_t* state, hipStream_t s) {
+  if (n_tasks <= 0) return hipSuccess;
+  const int zb = (max(max_out, 1) + 63) / 64;
+  hipLaunchKernelGGL(stat_reduce_kernel, dim3(n_tasks, zb < 64 ? zb : 64), dim3(256), 0, s, tasks,
+                     parts, state);
+  return hipGetLastError();
+}
+
+__global__ __launch_bounds__(256) void zero_kernel(i32x4* p, int64_t n16) {
+  const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (i < n16) p[i] = i32x4{0, 0, 0, 0};
+}
+
+hipError_t launch_zero(void* p, int64_t bytes, hipStream_t s) {
+  if (bytes <= 0) return hipSuccess;
+  if (bytes % 16 || (uintptr_t)p % 16) return hipErrorInvalidValue;
+  const int64_t n16 = bytes / 16;
+  hipLaunchKernelGGL(zero_kernel, dim3((unsigned)((n16 + 255) / 256)), dim3(256), 0, s, (i32x4*)p, n16);
+  return hipGetLastError();
+}
+
+// ------------------------------------------------------------ eigensolver
+constexpr int kEigLd = kCurvMaxK + 1;  // float64 row pitch: column walks spread over banks
+constexpr int kEigSweeps = 32;
+
+// Round r of the round-robin ordering of n (even) indices: pair i of the
+// n/2 disjoint pairs.  Index 0 stays fixed, the others turn on a circle, so
+// every pair of indices meets exactly once in n - 1 rounds.
+__device__ inline void round_pair(int r, int i, int n, int* p, int* q) {
+  const int L = n - 1;
+  if (i == 0) {
+    *p = 0;
+    *q = 1 + r;
+  } else {
+    *p = 1 + (r + i) % L;
+    *q = 1 + (r - i + L) % L;
+  }
+}
+
+__device__ inline double wave_sum(double v) {
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) v += __shfl_xor(v, o, 64);
+  return v;
+}
+
+__global__ __launch_bounds__(256) void eigen_kernel(const EigTask* __restrict__ tasks,
+                                                    uint8_t* __restrict__ state) {
+  __shared__ double Am[kCurvMaxK * kEigLd];
+  __shared__ double Vm[kCurvMaxK * kEigLd];
+  __shared__ double rc[kCurvMaxK / 2], rs[kCurvMaxK / 2];
+  __shared__ double red[2][4];
+  __shared__ int rank[kCurvMaxK];
+  const EigTask t = tasks[blockIdx.x];
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int k = t.k, n = k + (k & 1), m = n / 2;
+  const float* sum = (const float*)(state + t.sum_off);
+  const int64_t cnt = *(const int64_t*)(state + t.count_off);
+  const double scale = cnt > 0 ? 1.0 / (double)cnt : 0.0;
+  for (int e = tid; e < n * n; e += 256) {
+    const int i = e / n, j = e - (e / n) * n;
+    double v = 0.0;
+    if (i < k && j < k) v = 0.5 * ((double)sum[i * k + j] + (double)sum[j * k + i]) * scale;
+    Am[i * kEigLd + j] = v;
+    Vm[i * kEigLd + j] = i == j ? 1.0 : 0.0;
+  }
+  __syncthreads();
+
+  for (int sweep = 0; sweep < kEigSweeps; ++sweep) {
+    double off = 0.0, tot = 0.0;
+    for (int e = tid; e < n * n; e += 256) {
+      const int i = e / n, j = e - (e / n) * n;
+      const double v = Am[i * kEigLd + j];
+      tot += v * v;
+      if (i != j) off += v * v;
+    }
+    off = wave_sum(off);
+    tot = wave_sum(tot);
+    if (lane == 0) {
+      red[0][wave] = off;
+      red[1][wave] = tot;
+    }
+    __syncthreads();
+    off = ((red[0][0] + red[0][1]) + red[0][2]) + red[0][3];
+    tot = ((red[1][0] + red[1][1]) + red[1][2]) + red[1][3];
+    __syncthreads();
+    if (off <= 1e-26 * tot) break;  // the same value in every thread: a uniform exit
+
+    for (int r = 0; r < n - 1; ++r) {
+      if (tid < m) {
+        int p, q;
+        round_pair(r, tid, n, &p, &q);
+        double c = 1.0, s = 0.0;
+        const double apq = Am[p * kEigLd + q];
+        if (apq != 0.0) {
+          // rotation in the (p, q) plane that zeroes a_pq: tan = root of
+          // t^2 + 2 theta t - 1 = 0 of smaller magnitude
+          const double theta = (Am[q * kEigLd + q] - Am[p * kEigLd + p]) / (2.0 * apq);
+          double tn;
+          if (fabs(theta) > 1e150)
+            tn = 0.5 / theta;
+          else
+            tn = (theta >= 0.0 ? 1.0 : -1.0) / (fabs(theta) + sqrt(1.0 + theta * theta));
+          c = 1.0 / sqrt(1.0 + tn * tn);
+          s = tn * c;
+        }
+        rc[tid] = c;
+        rs[tid] = s;
+      }
+      __syncthreads();
+      // rows: A <- J^T A
+      for (int e = tid; e < m * n; e += 256) {
+        const int pi = e / n, col = e - (e / n) * n;
+        int p, q;
+        round_pair(r, pi, n, &p, &q);
+        const double c = rc[pi], s = rs[pi];
+        const double a = Am[p * kEigLd + col], b = Am[q * kEigLd + col];
+        Am[p * kEigLd + col] = c * a - s * b;
+        Am[q * kEigLd + col] = s * a + c * b;
+      }
+      __syncthreads();
+      // columns: A <- A J, V <- V J
+      for (int e = tid; e < m * n; e += 256) {
+        const int pi = e / n, row = e - (e / n) * n;
+        int p, q;
+        round_pair(r, pi, n, &p, &q);
+        const double c = rc[pi], s = rs[pi];
+        const double a = Am[row * kEigLd + p], b = Am[row * kEigLd + q];
+        Am[row * kEigLd + p] = c * a - s * b;
+        Am[row * kEigLd + q] = s * a + c * b;
+        const double va = Vm[row * kEigLd + p], vb = Vm[row * kEigLd + q];
+        Vm[row * kEigLd + p] = c * va - s * vb;
+        Vm[row * kEigLd + q] = s * va + c * vb;
+      }
+      __syncthreads();
+    }
+  }
+
+  // ascending order, ties by index
+  if (tid < k) {
+    const double li = Am[tid * kEigLd + tid];
+    int rk = 0;
+    for (int j = 0; j < k; ++j) {
+      const double lj = Am[j * kEigLd + j];
+      rk += (lj < li) || (lj == li && j < tid);
+    }
+    rank[tid] = rk;
+  }
+  __syncthreads();
+  float* Q = (float*)(state + t.q_off);
+  float* lam = (float*)(state + t.lam_off);
+  for (int e = tid; e < k * k; e += 256) {
+    const int row = e / k, col = e - (e / k) * k;
+    Q[row * k + rank[col]] = (float)Vm[row * kEigLd + col];
+  }
+  if (tid < k) lam[rank[tid]] = (float)Am[tid * kEigLd + tid];
+}
+
+hipError_t launch_eigen(const EigTask* tasks, int n_tasks, uint8_t* state, hipStream_t s) {
+  if (n_tasks <= 0) return hipSuccess;
+  hipLaunchKernelGGL(eigen_kernel, dim3(n_tasks), dim3(256), 0, s, tasks, state);
+  return hipGetLastError();
+}
+
+// -------------------------------------------------------- rotated blocks
+constexpr int kLd = kCurvMaxK;  // float pitch of the LDS matrices
+
+// c[i][j] = sum_{kk < K} L[kk][c0 + i] R[kk][r0 + j]  (LDS, rows kLd apart)
+__device__ inline void mm4(const float* L, const float* R, int K, int c0, int r0, float (&c)[4][4]) {
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int j = 0; j < 4; ++j) c[i][j] = 0.f;
+  for (int kk = 0; kk < K; ++kk) {
+    const f32x4 l = *(const f32x4*)(L + kk * kLd + c0);
+    const f32x4 r = *(const f32x4*)(R + kk * kLd + r0);
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+      for (int j = 0; j < 4; ++j) c[i][j] = fmaf(l[i], r[j], c[i][j]);
+  }
+}
+
+__device__ inline float load_elem(const void* p, int bf16, int64_t i) {
+  return bf16 ? bf16_bits_to_f32(((const uint16_t*)p)[i]) : ((const float*)p)[i];
+}
+
+// Loads a k1 x k2 float32 matrix (row-major, dense) into an LDS matrix, and its
+// transpose into T when T is not null.
+__device__ inline void load_mat(float* M, float* Tr, const float* src, int k1, int k2) {
+  for (int e = threadIdx.x; e < k1 * k2; e += 256) {
+    const int r = e / k2, c = e - (e / k2) * k2;
+    const float v = src[e];
+    M[r * kLd + c] = v;
+    if (Tr) Tr[c * kLd + r] = v;
+  }
+}
+
+__device__ inline void zero_lds(float* M) {
+  for (int e = threadIdx.x; e < kCurvMaxK * kLd; e += 256) M[e] = 0.f;
+}
+
+__global__ __launch_bounds__(256) void ekfac_kernel(const RotTask* __restrict__ tasks,
+                                                    const uint8_t* __restrict__ state,
+                                                    const void* __restrict__ phi, int phi_bf16,
+                                                    int64_t ld, int64_t n, int rpb,
+                                                    float* __restrict__ parts) {
+  __shared__ __align__(16) float QA[kCurvMaxK * kLd];
+  __shared__ __align__(16) float QG[kCurvMaxK * kLd];
+  __shared__ __align__(16) float X[kCurvMaxK * kLd];
+  __shared__ __align__(16) float YT[kCurvMaxK * kLd];
+  const RotTask t = tasks[blockIdx.y];
+  if ((int)blockIdx.x >= t.n_blocks) return;
+  const int ki = t.k_in, ko = t.k_out, tid = threadIdx.x;
+  // thread tile: 4 x 4 elements (c0.., r0..) of the k_in x k_out block
+  const int nro = (ko + 3) / 4, nci = (ki + 3) / 4;
+  const int ci = tid / nro, ri = tid - (tid / nro) * nro;
+  const bool active = ci < nci;
+  const int c0 = 4 * ci, r0 = 4 * ri;
+  zero_lds(QA);
+  zero_lds(QG);
+  zero_lds(X);
+  zero_lds(YT);
+  __syncthreads();
+  load_mat(QA, nullptr, (const float*)(state + t.q_a), ki, ki);
+  load_mat(QG, nullptr, (const float*)(state + t.q_g), ko, ko);
+  float acc[4][4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int j = 0; j < 4; ++j) acc[i][j] = 0.f;
+  const int64_t e0 = (int64_t)blockIdx.x * rpb;
+  const int64_t e1 = min(n, e0 + rpb);
+  for (int64_t e = e0; e < e1; ++e) {
+    __syncthreads();  // the previous row's readers of X and YT are done
+    for (int idx = tid; idx < ki * ko; idx += 256) {
+      const int c = idx / ko, r = idx - (idx / ko) * ko;
+      X[c * kLd + r] = load_elem(phi, phi_bf16, e * ld + t.col + idx);
+    }
+    __syncthreads();
+    float y[4][4];
+    if (active) {  // Y1 = Q_A^T Psi, stored transposed
+      mm4(QA, X, ki, c0, r0, y);
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) YT[(r0 + j) * kLd + c0 + i] = y[i][j];
+    }
+    __syncthreads();
+    if (active) {  // Y = Y1 Q_G
+      mm4(YT, QG, ko, c0, r0, y);
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) acc[i][j] = fmaf(y[i][j], y[i][j], acc[i][j]);
+    }
+  }
+  if (active) {
+    float* dst = parts + t.part_base + (int64_t)blockIdx.x * ki * ko;
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+      for (int j = 0; j < 4; ++j)
+        if (c0 + i < ki && r0 + j < ko) dst[(c0 + i) * ko + r0 + j] = acc[i][j];
+  }
+}
+
+hipError_t launch_ekfac(const RotTask* tasks, int n_tasks, int max_blocks, const uint8_t* state,
+                        const void* phi, int phi_bf16, int64_t ld, int64_t n, int rows_per_block,
+                        float* parts, hipStream_t s) {
+  if (n_tasks <= 0 || max_blocks <= 0 || n <= 0) return hipSuccess;
+  if (n_tasks > 65535) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(ekfac_kernel, dim3(max_blocks, n_tasks), dim3(256), 0, s, tasks, state, phi,
+                     phi_bf16, ld, n, rows_per_block, parts);
+  return hipGetLastError();
+}
+
+// Block sum of v over the workgroup in a fixed order (float64); every thread
+// gets the same value.  Contains two barriers.
+__device__ inline double block_sum(double v, double* red) {
+  v = wave_sum(v);
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  if (lane == 0) red[wave] = v;
+  __syncthreads();
+  const double s = ((red[0] + red[1]) + red[2]) + red[3];
+  __syncthreads();
+  return s;
+}
+
+constexpr int kPrecQueries = 8;  // query rows per workgroup
+
+__global__ __launch_bounds__(256) void precond_kernel(const RotTask* __restrict__ tasks,
+                                                      const uint8_t* __restrict__ state, int kind,
+                                                      double rel, double abs_,
+                                                      const void* __restrict__ phi_q, int in_bf16,
+                                                      int64_t ld_q, int64_t n_q,
+                                                      void* __restrict__ out, int out_bf16,
+                                                      int64_t ld_out) {
+  __shared__ __align__(16) float QA[kCurvMaxK * kLd];
+  __shared__ __align__(16) float QAT[kCurvMaxK * kLd];
+  __shared__ __align__(16) float QG[kCurvMaxK * kLd];
+  __shared__ __align__(16) float QGT[kCurvMaxK * kLd];
+  __shared__ __align__(16) float X[kCurvMaxK * kLd];
+  __shared__ __align__(16) float YT[kCurvMaxK * kLd];
+  __shared__ double red[4];
+  const RotTask t = tasks[blockIdx.y];
+  const int ki = t.k_in, ko = t.k_out, tid = threadIdx.x;
+  const int nro = (ko + 3) / 4, nci = (ki + 3) / 4;
+  const int ci = tid / nro, ri = tid - (tid / nro) * nro;
+  const bool active = ci < nci;
+  const int c0 = 4 * ci, r0 = 4 * ri;
+  const float* lam_a = (const float*)(state + t.lam_a);
+  const float* lam_g = (const float*)(state + t.lam_g);
+  const float* sum_e = (const float*)(state + t.sum_e);
+  const int64_t n_e = ((const int64_t*)(state + t.counts))[2];
+  const float inv_e = n_e > 0 ? (float)(1.0 / (double)n_e) : 0.f;
+
+  // damping: rel * mean eigenvalue of the layer + abs
+  double mean;
+  if (kind == 0) {
+    double sa = 0.0, sg = 0.0;
+    for (int i = tid; i < ki; i += 256) sa += (double)lam_a[i];
+    for (int i = tid; i < ko; i += 256) sg += (double)lam_g[i];
+    sa = block_sum(sa, red);
+    sg = block_sum(sg, red);
+    mean = sa * sg / ((double)ki * ko);
+  } else {
+    double se = 0.0;
+    for (int i = tid; i < ki * ko; i += 256) se += (double)sum_e[i];
+    se = block_sum(se, red);
+    mean = n_e > 0 ? se / ((double)n_e * ki * ko) : 0.0;
+  }
+  const float delta = (float)(rel * mean + abs_);
+  // this thread's 4 x 4 divisors E + delta
+  float den[4][4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int c = min(c0 + i, ki - 1), r = min(r0 + j, ko - 1);
+      const float E = kind == 0 ? lam_a[c] * lam_g[r] : sum_e[c * ko + r] * inv_e;
+      den[i][j] = E + delta;
+    }
+
+  zero_lds(QA);
+  zero_lds(QAT);
+  zero_lds(QG);
+  zero_lds(QGT);
+  zero_lds(X);
+  zero_lds(YT);
+  __syncthreads();
+  load_mat(QA, QAT, (const float*)(state + t.q_a), ki, ki);
+  load_mat(QG, QGT, (const float*)(state + t.q_g), ko, ko);
+
+  const int64_t q0 = (int64_t)blockIdx.x * kPrecQueries;
+  const int64_t q1 = min(n_q, q0 + kPrecQueries);
+  for (int64_t q = q0; q < q1; ++q) {
+    __syncthreads();  // the previous query's readers are done
+    for (int idx = tid; idx < ki * ko; idx += 256) {
+      const int c = idx / ko, r = idx - (idx / ko) * ko;
+      X[c * kLd + r] = load_elem(phi_q, in_bf16, q * ld_q + t.col + idx);
+    }
+    __syncthreads();
+    float y[4][4];
+    if (active) {  // Y1 = Q_A^T Psi_q, stored transposed
+      mm4(QA, X, ki, c0, r0, y);
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) YT[(r0 + j) * kLd + c0 + i] = y[i][j];
+    }
+    __syncthreads();
+    if (active) {  // W = (Y1 Q_G) / (E + delta), stored row-major over X
+      mm4(YT, QG, ko, c0, r0, y);
+    }
+    __syncthreads();
+    if (active) {
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) X[(c0 + i) * kLd + r0 + j] = y[i][j] / den[i][j];
+    }
+    __syncthreads();
+    if (active) {  // Z1 = Q_A W, stored transposed
+      mm4(QAT, X, ki, c0, r0, y);
+    }
+    __syncthreads();
+    if (active) {
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) YT[(r0 + j) * kLd + c0 + i] = y[i][j];
+    }
+    __syncthreads();
+    if (active) {  // out = Z1 Q_G^T
+      mm4(YT, QGT, ko, c0, r0, y);
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          if (c0 + i < ki && r0 + j < ko) {
+            const int64_t o = q * ld_out + t.col + (int64_t)(c0 + i) * ko + r0 + j;
+            if (out_bf16)
+              ((uint16_t*)out)[o] = f32_to_bf16_bits(y[i][j]);
+            else
+              ((float*)out)[o] = y[i][j];
+          }
+        }
+    }
+  }
+}
+
+hipError_t launch_precondition(const RotTask* tasks, int n_tasks, const uint8_t* state, int kind,
+                               double rel, double abs_, const void* phi_q, int in_bf16,
+                               int64_t ld_q, int64_t n_q, void* out, int out_bf16, int64_t ld_out,
+                               hipStream_t s) {
+  if (n_tasks <= 0 || n_q <= 0) return hipSuccess;
+  const int64_t qb = (n_q + kPrecQueries - 1) / kPrecQueries;
+  if (n_tasks > 65535 || qb > INT32_MAX) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(precond_kernel, dim3((unsigned)qb, n_tasks), dim3(256), 0, s, tasks, state,
+                     kind, rel, abs_, phi_q, in_bf16, ld_q, n_q, out, out_bf16, ld_out);
+  return hipGetLastError();
+}
+
+}  // namespace dattri

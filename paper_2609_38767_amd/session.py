@@ -3,7 +3,9 @@
 ``ProjectionSession`` registers layers, allocates and binds the projection
 maps, captures factor blocks, sizes the workspace and calls
 ``dattri_project_per_example``; ``score`` sizes the scoring workspace and calls
-``dattri_score``.  All computation happens in libdattri's HIP kernels.
+``dattri_score``; ``Curvature`` owns a K-FAC / EK-FAC curvature state and runs
+its fit, eigendecomposition, eigenvalue correction and query preconditioning.
+All computation happens in libdattri's HIP kernels.
 """
 import torch
 
@@ -14,7 +16,11 @@ from . import (DATTRI_BF16, DATTRI_F32, DATTRI_ROUTE_AUTO, dattri_bind_projectio
                dattri_feature_dim, dattri_feature_ld, dattri_layer_offset, dattri_layer_route,
                dattri_project_per_example, dattri_projection_bytes, dattri_register_layer,
                dattri_score, dattri_score_workspace_bytes, dattri_set_factored_form,
-               dattri_workspace_bytes)
+               dattri_workspace_bytes, DATTRI_CURV_KFAC, DATTRI_CURV_EKFAC,
+               dattri_curvature_state_bytes, dattri_curvature_layout_of, dattri_curvature_reset,
+               dattri_curvature_fit_workspace_bytes, dattri_curvature_accumulate_factors,
+               dattri_curvature_eigen, dattri_curvature_ekfac_workspace_bytes,
+               dattri_curvature_accumulate_ekfac, dattri_curvature_precondition)
 
 DTYPES = {"f32": (DATTRI_F32, torch.float32), "bf16": (DATTRI_BF16, torch.bfloat16)}
 
@@ -138,3 +144,72 @@ def sq_norms(sess, route=DATTRI_ROUTE_AUTO, stream=None):
     ws = _dev_bytes(dattri_sq_norms_workspace_bytes(sess.ctx, route), sess.device)
     dattri_gradient_sq_norms(sess.ctx, out, ws, ws.numel(), route, stream)
     return out
+
+
+KINDS = {"kfac": DATTRI_CURV_KFAC, "ekfac": DATTRI_CURV_EKFAC}
+
+
+class Curvature:
+    """K-FAC / EK-FAC curvature state of a session's layers in one device buffer."""
+
+    def __init__(self, sess, stream=None):
+        self.sess = sess
+        self.nbytes = dattri_curvature_state_bytes(sess.ctx)
+        self.state = _dev_bytes(self.nbytes, sess.device)
+        self._ws = None
+        self.reset(stream)
+
+    def _workspace(self, need):
+        if self._ws is None or self._ws.numel() < need:
+            self._ws = None
+            self._ws = _dev_bytes(need, self.sess.device)
+        return self._ws
+
+    def reset(self, stream=None):
+        dattri_curvature_reset(self.sess.ctx, self.state, stream)
+
+    def accumulate_factors(self, stream=None):
+        """Adds the projected factor sums of the session's current captures."""
+        ws = self._workspace(dattri_curvature_fit_workspace_bytes(self.sess.ctx))
+        dattri_curvature_accumulate_factors(self.sess.ctx, self.state, ws, ws.numel(), stream)
+
+    def eigen(self, stream=None):
+        dattri_curvature_eigen(self.sess.ctx, self.state, stream)
+
+    def accumulate_ekfac(self, phi, stream=None):
+        """EK-FAC's correction from training rows phi [n, F] (row-strided allowed)."""
+        code = DATTRI_BF16 if phi.dtype == torch.bfloat16 else DATTRI_F32
+        n = phi.shape[0]
+        ws = self._workspace(dattri_curvature_ekfac_workspace_bytes(self.sess.ctx, n))
+        dattri_curvature_accumulate_ekfac(self.sess.ctx, self.state, phi, code, n, phi.stride(0), ws,
+                                          ws.numel(), stream)
+
+    def precondition(self, phi_q, kind="ekfac", rel=0.1, abs_=0.0, out_dtype=None, out=None, stream=None):
+        """Preconditioned query rows (rows at the library's recommended stride)."""
+        in_code = DATTRI_BF16 if phi_q.dtype == torch.bfloat16 else DATTRI_F32
+        if out is None:
+            od = out_dtype or ("bf16" if in_code == DATTRI_BF16 else "f32")
+            out = feature_rows(phi_q.shape[0], self.sess.F, od, self.sess.device)
+        out_code = DATTRI_BF16 if out.dtype == torch.bfloat16 else DATTRI_F32
+        dattri_curvature_precondition(self.sess.ctx, self.state, KINDS[kind], rel, abs_, phi_q, in_code,
+                                      phi_q.shape[0], phi_q.stride(0), out, out_code, out.stride(0), stream)
+        return out
+
+    def layout(self, layer):
+        return dattri_curvature_layout_of(self.sess.ctx, layer)
+
+    def field(self, layer, name):
+        """View of one field of a layer in the state: float32 matrices / vectors,
+        int64 counts."""
+        f = self.layout(layer)
+        L = self.sess.layers[layer]
+        ki, ko = L["k_in"], L["k_out"]
+        shapes = {"sum_a": (ki, ki), "sum_g": (ko, ko), "sum_e": (ki, ko), "q_a": (ki, ki), "lam_a": (ki,),
+                  "q_g": (ko, ko), "lam_g": (ko,), "counts": (3,)}
+        shape = shapes[name]
+        dt = torch.int64 if name == "counts" else torch.float32
+        n = 1
+        for v in shape:
+            n *= v
+        off = f[name]
+        return self.state[off:off + n * dt.itemsize].view(dt).view(shape)

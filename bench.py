@@ -33,7 +33,8 @@ def parse():
     p.add_argument("--steps", type=int, default=10)
     p.add_argument("--warmup", type=int, default=2)
     p.add_argument("--no-cpu-baseline", action="store_true")
-    p.add_argument("--phase", choices=["all", "project", "score", "routing", "gpt2", "crossgram", "copy"],
+    p.add_argument("--phase", choices=["all", "project", "score", "routing", "gpt2", "crossgram", "curvature",
+                                       "copy"],
                    default="all")
     return p.parse_args()
 
@@ -288,6 +289,124 @@ def crossgram_case(dev, steps, warmup):
     return out
 
 
+def curvature_case(dev, steps, warmup):
+    """K-FAC / EK-FAC attribution (the paper's curvature methods at factor
+    projection k_a = k_g = 64): 512 training sequences of a Qwen2.5-7B-shaped
+    stack (196 layers, T = 512, batches of 32) against one query.  One
+    attribution = per batch, projected gradients into Phi_train (and, for the
+    curvature methods, the projected factor sums); the eigendecompositions;
+    EK-FAC's eigenvalue correction over Phi_train; the query's projected
+    gradient and its preconditioning; scores and top-10.  GradDot is the same
+    without the curvature steps.  The 16 training batches are 16 passes over one
+    resident synthetic batch (identical traffic: 73 GB per pass).  Reports
+    training sequences per second per method (median of `steps`) and the time
+    of each stage."""
+    import torch
+    import paper_2609_38767_amd as dt
+    import workloads as W
+    from paper_2609_38767_amd.session import Curvature, ProjectionSession, feature_rows
+    stream = torch.cuda.current_stream()
+    wl = W.WORKLOADS["curvature"]
+    layers, n, T = wl["layers"], wl["batch"], wl["T"]
+    n_batches = wl["n_train"] // n
+    train = ProjectionSession(layers, dtype="bf16", seed=wl["seed"], device=dev)
+    query = ProjectionSession(layers, dtype="bf16", seed=wl["seed"], device=dev)
+    cache = {}
+    for li in range(len(layers)):
+        A, B = W.factor_blocks(wl, li, 0, n, T, dev, "bf16", a_cache=cache)
+        train.capture(li, A, B)
+    qcache = {}
+    for li in range(len(layers)):
+        A, B = W.factor_blocks(dict(wl, seed=wl["seed"] + 1000), li, 0, wl["n_query"], T, dev, "bf16",
+                               a_cache=qcache)
+        query.capture(li, A, B)
+    F = train.F
+    phi_t = feature_rows(wl["n_train"], F, "f32", dev)
+    phi_q = feature_rows(wl["n_query"], F, "f32", dev)
+    pq = feature_rows(wl["n_query"], F, "f32", dev)
+    curv = Curvature(train)
+    train.workspace()
+    query.workspace()
+    S = torch.empty((wl["n_query"], wl["n_train"]), dtype=torch.float32, device=dev)
+    topk = 10
+    idx = torch.empty((wl["n_query"], topk), dtype=torch.int32, device=dev)
+    val = torch.empty((wl["n_query"], topk), dtype=torch.float32, device=dev)
+    sws = torch.empty(dt.dattri_score_workspace_bytes(wl["n_query"], wl["n_train"], F, dt.DATTRI_F32, False,
+                                                      True, topk), dtype=torch.uint8, device=dev)
+    print(f"[bench] curvature inputs ready ({len(layers)} layers, F = {F})", file=sys.stderr, flush=True)
+
+    def attribute(method, marks=None):
+        def mark(name):
+            if marks is not None:
+                e = torch.cuda.Event(enable_timing=True)
+                e.record(stream)
+                marks.append((name, e))
+        mark("start")
+        if method != "graddot":
+            curv.reset()
+        for b in range(n_batches):
+            train.project(n, phi=phi_t[b * n:(b + 1) * n])
+            if method != "graddot":
+                curv.accumulate_factors()
+        mark("train")
+        if method != "graddot":
+            curv.eigen()
+        mark("eigen")
+        if method == "ekfac":
+            curv.accumulate_ekfac(phi_t)
+        mark("ekfac")
+        query.project(wl["n_query"], phi=phi_q)
+        q = phi_q
+        if method != "graddot":
+            q = curv.precondition(phi_q, method, 0.1, 0.0, out=pq)
+        mark("query")
+        dt.dattri_score(q, wl["n_query"], q.stride(0), phi_t, wl["n_train"], phi_t.stride(0), F, dt.DATTRI_F32,
+                        None, S, topk, idx, val, sws, sws.numel())
+        mark("score")
+
+    out = {"workload": f"{len(layers)} Qwen2.5-7B-shaped linear layers, T={T}, {wl['n_train']} training "
+                       f"sequences in batches of {n} vs {wl['n_query']} query, k_in=k_out=64, bf16",
+           "methods": {}}
+    for method in ("graddot", "kfac", "ekfac"):
+        for _ in range(warmup):
+            attribute(method)
+        runs = []
+        for _ in range(steps):
+            marks = []
+            torch.cuda.synchronize()
+            t0 = time.perf_counter()
+            attribute(method, marks)
+            torch.cuda.synchronize()
+            wall = time.perf_counter() - t0
+            stages = {marks[i][0]: marks[i - 1][1].elapsed_time(marks[i][1]) for i in range(1, len(marks))}
+            runs.append((wall, stages))
+        runs.sort(key=lambda r: r[0])
+        wall, stages = runs[len(runs) // 2]
+        out["methods"][method] = {"seq_per_s": wl["n_train"] / wall, "wall_ms": wall * 1e3,
+                                  "stage_ms": stages}
+        print(f"[bench] curvature {method}: {wl['n_train'] / wall:.1f} seq/s ({wall * 1e3:.1f} ms); "
+              + ", ".join(f"{k} {v:.2f} ms" for k, v in stages.items()), file=sys.stderr, flush=True)
+    # factor-sum pass alone, one batch (the fit's added HBM pass)
+    for _ in range(warmup):
+        curv.accumulate_factors()
+    evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(steps)]
+    for a, b in evs:
+        a.record(stream)
+        curv.accumulate_factors()
+        b.record(stream)
+    torch.cuda.synchronize()
+    fit_ms = sorted(a.elapsed_time(b) for a, b in evs)[steps // 2]
+    bytes_batch = algorithmic_projection_bytes(wl) * n
+    out["factor_sums"] = {"ms_per_batch": fit_ms, "algorithmic_bytes_per_batch": bytes_batch,
+                          "achieved_gbs": bytes_batch / (fit_ms * 1e-3) / 1e9,
+                          "hbm_frac": bytes_batch / (fit_ms * 1e-3) / 8e12}
+    for s in (train, query):
+        s.close()
+    del cache, qcache, phi_t, curv
+    torch.cuda.empty_cache()
+    return out
+
+
 def stream_reference(dev):
     """Achievable HBM rate on this GPU: a 1 GiB device-to-device copy (read +
     write bytes per second, best of 5)."""
@@ -433,6 +552,8 @@ def main():
         out["gpt2"] = gpt2_case(dev, max(args.steps, 5), args.warmup)
     if args.phase in ("all", "crossgram"):
         out["crossgram_routing"] = crossgram_case(dev, max(min(args.steps, 5), 3), min(args.warmup, 1))
+    if args.phase in ("all", "curvature"):
+        out["curvature"] = curvature_case(dev, max(min(args.steps, 5), 3), min(args.warmup, 1))
     if args.phase in ("all", "score"):
         for _ in range(args.warmup):
             score_step(False)

@@ -26,7 +26,7 @@ namespace dattri {
 using namespace dev;
 
 template <int ELT, bool AL, int RT, int NA, int NB>
-__global__ __launch_bounds__(256, (AL && NA * NB <= 12) ? 2 : 1) void factored_kernel(const FactItem* __restrict__ items,
+__global__ __launch_bounds__(256, (AL && NA * NB <= 16) ? 2 : 1) void factored_kernel(const FactItem* __restrict__ items,
                                                           const FactGroup* __restrict__ groups,
                                                           const FactMember* __restrict__ members,
                                                           float* __restrict__ partials) {
@@ -137,7 +137,7 @@ __global__ __launch_bounds__(256, (AL && NA * NB <= 12) ? 2 : 1) void factored_k
 // Aligned instances per (input tiles NA, output tiles NB); one unaligned
 // instance (8, 4) serves any group whose rows are not 16-byte multiples.
 // Rows per wave RT keeps two waves per SIMD within the register file.
-constexpr int rt_of(int na, int nb) { return (na <= 2 && nb <= 2) ? 4 : (na * nb <= 12 ? 2 : 1); }
+constexpr int rt_of(int na, int nb) { return (na <= 2 && nb <= 2) ? 4 : (na * nb <= 16 ? 2 : 1); }
 
 void factored_instance(int elt, int na_req, int nb_req, int aligned, int* na_inst, int* nb_inst,
                        int* rows_per_wave) {

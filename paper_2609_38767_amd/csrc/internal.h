@@ -213,9 +213,11 @@ inline bool score_uses_big(int elt_bytes, int64_t n_q, int64_t n_train) {
 }
 // bytes of queries packed in MFMA fragment order for the 256 x 256 kernel
 int64_t score_qpack_bytes(int64_t n_q, int64_t F);
-// The 256 x 256 kernel splits K when its tiles alone would leave CUs idle:
+// Both GEMM kernels split K when their tiles alone would leave CUs idle:
 // number of K splits (1 = none) and the float32 partial results it stages.
 int score_ksplit(int elt_bytes, int64_t n_q, int64_t n_train, int64_t F);
+// S[i] = sum over y < ks of part[y*n + i], in split order.
+hipError_t launch_splitk_sum(const float* part, int ks, int64_t n, float* S, hipStream_t s);
 inline int64_t score_partial_floats(int elt_bytes, int64_t n_q, int64_t n_train, int64_t F) {
   const int ks = score_ksplit(elt_bytes, n_q, n_train, F);
   return ks > 1 ? (int64_t)ks * n_q * n_train : 0;

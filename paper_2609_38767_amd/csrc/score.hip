@@ -10,6 +10,9 @@
 // Tiles are remapped so that each XCD walks a contiguous range of training
 // tiles, all query tiles of one training tile back to back, so a Phi_train
 // tile is fetched into that XCD's L2 once and reused by every query tile.
+// When the tiles alone cannot fill the chip (few queries and training rows,
+// long feature rows), the feature axis is split over grid.y: each split writes
+// its partial tile, and the splits are summed in split order.
 #include "device_common.h"
 #include "internal.h"
 
@@ -44,7 +47,7 @@ __global__ __launch_bounds__(256) void score_gemm_kernel(const uint8_t* __restri
                                                          const uint8_t* __restrict__ X,
                                                          float* __restrict__ S, int n_q,
                                                          int n_train, int F, int ldq, int ldx,
-                                                         int n_qt, int n_xt) {
+                                                         int n_qt, int n_xt, int sps) {
   constexpr int EPL = 16 / ELT;
   constexpr int BK = kRowBytes / ELT;  // K elements per stage
   __shared__ __align__(16) uint8_t smem[2][2][kBM * kRowBytes];  // [stage][Q/X] 64 KiB
@@ -69,6 +72,8 @@ __global__ __launch_bounds__(256) void score_gemm_kernel(const uint8_t* __restri
     for (int j = 0; j < 4; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
 
   const int nk = (F + BK - 1) / BK;
+  const int k0 = blockIdx.y * sps, k1 = min(nk, k0 + sps);  // this split's K steps
+  S += (int64_t)blockIdx.y * n_q * n_train;                 // its partial tile (S itself when unsplit)
   i32x4 rqv[4], rxv[4];
   auto gload = [&](int kk) {
 #pragma unroll
@@ -89,14 +94,14 @@ __global__ __launch_bounds__(256) void score_gemm_kernel(const uint8_t* __restri
     }
   };
 
-  if (nk > 0) {
-    gload(0);
+  if (k0 < k1) {
+    gload(k0);
     swrite(0);
   }
   __syncthreads();
-  for (int kk = 0; kk < nk; ++kk) {
-    const int st = kk & 1;
-    if (kk + 1 < nk) gload(kk + 1);
+  for (int kk = k0; kk < k1; ++kk) {
+    const int st = (kk - k0) & 1;
+    if (kk + 1 < k1) gload(kk + 1);
 #pragma unroll
     for (int s = 0; s < 2; ++s) {
       i32x4 af[4], bf[4];
@@ -115,7 +120,7 @@ __global__ __launch_bounds__(256) void score_gemm_kernel(const uint8_t* __restri
 #pragma unroll
         for (int j = 0; j < 4; ++j) acc[i][j] = frag_mma<ELT>(af[i], bf[j], acc[i][j]);
     }
-    if (kk + 1 < nk) swrite(st ^ 1);
+    if (kk + 1 < k1) swrite(st ^ 1);
     __syncthreads();
   }
 
@@ -162,15 +167,22 @@ hipError_t launch_score_gemm(int elt, const void* Q, int64_t ldq, const float* d
   const int n_qt = (int)((n_q + kBM - 1) / kBM), n_xt = (int)((n_train + kBN - 1) / kBN);
   const int64_t nb = (int64_t)n_qt * n_xt;
   if (nb > INT32_MAX) return hipErrorInvalidValue;
+  const int64_t nk = (F + kRowBytes / elt - 1) / (kRowBytes / elt);
+  const int ks = score_ksplit(elt, n_q, n_train, F);
+  const int sps = ks > 1 ? (int)((nk + ks - 1) / ks) : (int)std::max<int64_t>(nk, 1);
+  if (ks > 1 && !partials) return hipErrorInvalidValue;
+  float* out = ks > 1 ? partials : S;
   if (elt == 2)
-    hipLaunchKernelGGL(score_gemm_kernel<2>, dim3((unsigned)nb), dim3(256), 0, s, (const uint8_t*)Q,
-                       (const uint8_t*)X, S, (int)n_q, (int)n_train, (int)F, (int)ldq, (int)ldx,
-                       n_qt, n_xt);
+    hipLaunchKernelGGL(score_gemm_kernel<2>, dim3((unsigned)nb, (unsigned)ks), dim3(256), 0, s,
+                       (const uint8_t*)Q, (const uint8_t*)X, out, (int)n_q, (int)n_train, (int)F, (int)ldq,
+                       (int)ldx, n_qt, n_xt, sps);
   else
-    hipLaunchKernelGGL(score_gemm_kernel<4>, dim3((unsigned)nb), dim3(256), 0, s, (const uint8_t*)Q,
-                       (const uint8_t*)X, S, (int)n_q, (int)n_train, (int)F, (int)ldq, (int)ldx,
-                       n_qt, n_xt);
-  return hipGetLastError();
+    hipLaunchKernelGGL(score_gemm_kernel<4>, dim3((unsigned)nb, (unsigned)ks), dim3(256), 0, s,
+                       (const uint8_t*)Q, (const uint8_t*)X, out, (int)n_q, (int)n_train, (int)F, (int)ldq,
+                       (int)ldx, n_qt, n_xt, sps);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess || ks == 1) return e;
+  return launch_splitk_sum(partials, ks, n_q * n_train, S, s);
 }
 
 }  // namespace dattri

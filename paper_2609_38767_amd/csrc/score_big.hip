@@ -251,8 +251,26 @@ __global__ __launch_bounds__(256) void splitk_sum_kernel(const float* __restrict
   S[i] = s;
 }
 
+hipError_t launch_splitk_sum(const float* part, int ks, int64_t n, float* S, hipStream_t s) {
+  if (n <= 0) return hipSuccess;
+  hipLaunchKernelGGL(splitk_sum_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s, part, ks, n, S);
+  return hipGetLastError();
+}
+
+// 128 x 128 kernel: split K while its tiles number fewer than kSmallTarget, into
+// splits of at least kSmallMinSteps K steps of 128 bytes.
+constexpr int64_t kSmallTarget = 512, kSmallMinSteps = 8;
+
 int score_ksplit(int elt, int64_t n_q, int64_t n_train, int64_t F) {
-  if (!score_uses_big(elt, n_q, n_train) || F <= 0) return 1;
+  if (F <= 0) return 1;
+  if (!score_uses_big(elt, n_q, n_train)) {
+    const int64_t tiles = ((n_q + 127) / 128) * ((n_train + 127) / 128);
+    const int64_t nk = (F + 128 / elt - 1) / (128 / elt);
+    const int64_t ks = std::min<int64_t>(kSmallTarget / std::max<int64_t>(tiles, 1), nk / kSmallMinSteps);
+    if (ks <= 1) return 1;
+    const int64_t sps = (nk + ks - 1) / ks;
+    return (int)((nk + sps - 1) / sps);
+  }
   const int64_t tiles = ((n_q + kSB - 1) / kSB) * ((n_train + kSB - 1) / kSB);
   const int64_t nk = (F + kSK - 1) / kSK;
   int64_t ks = std::min<int64_t>({256 / std::max<int64_t>(tiles, 1), 16, nk / 2});
@@ -285,10 +303,7 @@ hipError_t launch_score_gemm_256(const void* Q, int64_t ldq, const float* d, con
                      (int)n_train, (int)F, (int)ldx, (int)nks, n_qt, n_xt, sps);
   e = hipGetLastError();
   if (e != hipSuccess || ks == 1) return e;
-  const int64_t n = n_q * n_train;
-  hipLaunchKernelGGL(splitk_sum_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s, partials, ks,
-                     n, S);
-  return hipGetLastError();
+  return launch_splitk_sum(partials, ks, n_q * n_train, S, s);
 }
 
 }  // namespace dattri

@@ -98,6 +98,20 @@ def test_token_chunks_and_lengths_at_chunk_edges(form):
         _check(layers, inputs, phi, 9, dtype, [0, 1, 2], lengths=lengths, tol=1e-5)
 
 
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_fused_64_wide_maps(dtype):
+    # k_in = k_out = 64: the 4 x 4-tile fused instance, several sub-chunks per
+    # work item, ragged lengths
+    layers = [dict(name="w0", d_in=264, d_out=200, k_in=64, k_out=64, a_group="a"),
+              dict(name="w1", d_in=96, d_out=520, k_in=64, k_out=60, a_group="b")]
+    wl = dict(W.WORKLOADS["tiny"], dist_a="normal", dist_b="normal", seed=17)
+    n, T = 4, 700
+    inputs = _session_inputs(wl, layers, n, T, dtype)
+    lengths = torch.tensor([700, 513, 128, 1], dtype=torch.int32, device=DEV)
+    _, phi = _run(layers, inputs, dtype, 19, "factored", lengths=lengths, form="fused")
+    _check(layers, inputs, phi, 19, dtype, [0, 1, 2, 3], lengths=lengths, tol=1e-5)
+
+
 @pytest.mark.parametrize("form", ["fused", "split"])
 def test_shared_input_group_matches_separate_inputs(form):
     # 16-wide maps: q and k share one fused work item (2 input tiles keep 4 row

@@ -51,6 +51,27 @@ def test_score_ragged_tiles(dtype, precond):
     _check_topk(host64(S), ref, idx.cpu().numpy(), val.cpu().numpy(), 17)
 
 
+@pytest.mark.parametrize("dtype", [torch.float32, torch.bfloat16])
+@pytest.mark.parametrize("shape", [(1, 512, 100000), (3, 200, 50008), (130, 129, 20000)])
+@pytest.mark.parametrize("precond", [False, True])
+def test_score_few_tiles_split_features(dtype, shape, precond):
+    # few 128 x 128 tiles and long feature rows: the feature axis is split over
+    # the grid and the partial tiles summed in split order
+    n_q, n_t, F = shape
+    g = torch.Generator(device=DEV).manual_seed(13)
+    ld = dattri_feature_ld(F, DATTRI_BF16 if dtype == torch.bfloat16 else 0)
+    Q = W.strided_copy(torch.randn((n_q, F), generator=g, device=DEV).to(dtype), ld)
+    X = W.strided_copy(torch.randn((n_t, F), generator=g, device=DEV).to(dtype), ld)
+    d = torch.exp(torch.randn(F, generator=g, device=DEV)) if precond else None
+    S, idx, val = score(Q, X, d, topk=5)
+    S2, _, _ = score(Q, X, d)
+    torch.cuda.synchronize()
+    assert torch.equal(S, S2)  # deterministic
+    ref = osc.score(host64(Q), host64(X), None if d is None else host64(d))
+    assert rel_fro(host64(S), ref) <= (1e-5 if dtype == torch.float32 or not precond else TOL[dtype])
+    _check_topk(host64(S), ref, idx.cpu().numpy(), val.cpu().numpy(), 5)
+
+
 @pytest.mark.parametrize("shape", [(300, 5000, 104), (256, 4096, 8192), (513, 777, 40)])
 def test_score_large_tile_kernel_ragged(shape):
     # n_q * n_train >= 2^20 routes bf16 to the 256 x 256 kernel: ragged query

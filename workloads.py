@@ -27,6 +27,14 @@ Workloads (synthetic stand-ins; no dataset or checkpoint is used):
 * ``score``     Phi_train 200000 x 8192 and Phi_query 2048 x 8192, bf16 N(0,1);
                 positive diagonal preconditioner log-uniform on [1e-3, 1e3];
                 fp32 scores plus per-query top-100.
+* ``curvature`` K-FAC / EK-FAC attribution: 28 Qwen2.5-7B-shaped blocks, each
+                with q 3584->3584, k 3584->512, v 3584->512, o 3584->3584,
+                gate 3584->18944, up 3584->18944, down 18944->3584 (196
+                layers); T=512, 512 training sequences in batches of 32 and 1
+                query, bf16 Student-t(4) factors, k_in=k_out=64 (F = 802,816).
+                Stands in for the paper's throughput runs (Table
+                "throughput-full": Qwen models, WikiText-103, T=512, 512
+                training sequences, factor projection k_a=k_g=64).
 * ``crossgram`` unprojected cross-Gram routing sweep: 24 Pythia-410M-shaped
                 blocks, each with linear layers 1024->3072 (query/key/value),
                 1024->1024 (attention output), 1024->4096 and 4096->1024 (MLP)
@@ -70,6 +78,20 @@ def _llama_layers(k=32, blocks=32):
     return out
 
 
+def _qwen7b_layers(k=64, blocks=28):
+    out = []
+    for b in range(blocks):
+        attn_in, mlp_in = f"Q{b}.attn_in", f"Q{b}.mlp_in"
+        out += [_layer(f"Q{b}.q_proj", 3584, 3584, k, k, attn_in),
+                _layer(f"Q{b}.k_proj", 3584, 512, k, k, attn_in),
+                _layer(f"Q{b}.v_proj", 3584, 512, k, k, attn_in),
+                _layer(f"Q{b}.o_proj", 3584, 3584, k, k, f"Q{b}.attn_core"),
+                _layer(f"Q{b}.gate_proj", 3584, 18944, k, k, mlp_in),
+                _layer(f"Q{b}.up_proj", 3584, 18944, k, k, mlp_in),
+                _layer(f"Q{b}.down_proj", 18944, 3584, k, k, f"Q{b}.act")]
+    return out
+
+
 def _pythia_layers(blocks=24):
     out = []
     for b in range(blocks):
@@ -101,6 +123,9 @@ WORKLOADS = {
                "dist_b": "normal", "b_scale": 1.0, "seed": 6},
     "score": {"n_train": 200000, "n_query": 2048, "F": 8192, "dtype": "bf16",
               "topk": 100, "d_log10_range": (-3.0, 3.0), "seed": 7},
+    "curvature": {"layers": _qwen7b_layers(), "T": 512, "batch": 32, "n_train": 512, "n_query": 1,
+                  "dtype": "bf16", "dist_a": "student_t4", "dist_b": "student_t4", "b_scale": 1.0,
+                  "seed": 9},
     "crossgram": {"layers": _pythia_layers(), "T_sweep": (32, 128, 512, 2048), "n_train": 8,
                   "n_query": 1, "dtype": "bf16", "dist_a": "normal", "dist_b": "normal",
                   "b_scale": 1.0, "seed": 8},

@@ -461,6 +461,22 @@ dattri_status dattri_curvature_fit_workspace_bytes(const dattri_ctx* ctx, size_t
 dattri_status dattri_curvature_accumulate_factors(dattri_ctx* ctx, void* state, void* workspace,
                                                   size_t ws_bytes, void* stream);
 
+/* Projected per-example gradients (exactly as dattri_project_per_example)
+ * and the projected factor sums of the same captures (as
+ * dattri_curvature_accumulate_factors), in one pass over A and B: the
+ * factored kernels also keep each layer's projected token rows a~_t, g~_t
+ * (float32, in the workspace) and the sums are formed from those rows; layers
+ * on the materialized route, which never form projected rows, take the
+ * separate factor-sum pass.
+ *   workspace: >= dattri_project_fit_workspace_bytes(ctx, route), 256-byte aligned.
+ * Errors: those of dattri_project_per_example and of
+ * dattri_curvature_accumulate_factors. */
+dattri_status dattri_project_fit_workspace_bytes(const dattri_ctx* ctx, dattri_route route,
+                                                 size_t* bytes);
+dattri_status dattri_project_and_fit(dattri_ctx* ctx, void* phi, dattri_dtype phi_dtype,
+                                     int64_t ld_phi, void* state, void* workspace, size_t ws_bytes,
+                                     dattri_route route, void* stream);
+
 /* Eigendecomposition of every layer's normalized factors A and S (cyclic
  * parallel Jacobi in float64 on the GPU, one workgroup per factor, until the
  * off-diagonal mass falls below 1e-26 of the total or 32 sweeps); writes q_a,

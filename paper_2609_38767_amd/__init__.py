@@ -31,6 +31,7 @@ __all__ = [
     "dattri_curvature_fit_workspace_bytes", "dattri_curvature_accumulate_factors",
     "dattri_curvature_eigen", "dattri_curvature_ekfac_workspace_bytes",
     "dattri_curvature_accumulate_ekfac", "dattri_curvature_precondition",
+    "dattri_project_fit_workspace_bytes", "dattri_project_and_fit",
 ]
 
 DATTRI_F32, DATTRI_BF16 = 0, 1
@@ -118,6 +119,8 @@ _SIGS = {
     "dattri_curvature_eigen": (_i32, [_vp, _vp, _vp]),
     "dattri_curvature_ekfac_workspace_bytes": (_i32, [_vp, _i64, _P(_sz)]),
     "dattri_curvature_accumulate_ekfac": (_i32, [_vp, _vp, _vp, _i32, _i64, _i64, _vp, _sz, _vp]),
+    "dattri_project_fit_workspace_bytes": (_i32, [_vp, _i32, _P(_sz)]),
+    "dattri_project_and_fit": (_i32, [_vp, _vp, _i32, _i64, _vp, _vp, _sz, _i32, _vp]),
     "dattri_curvature_precondition": (_i32, [_vp, _vp, _i32, _dbl, _dbl, _vp, _i32, _i64, _i64, _vp, _i32,
                                              _i64, _vp]),
 }
@@ -423,3 +426,17 @@ def dattri_curvature_precondition(ctx, state, kind, damping_rel, damping_abs, ph
                                                 in_dtype, n_q, ld_q, _ptr(out), out_dtype, ld_out,
                                                 _stream(stream)),
            "dattri_curvature_precondition")
+
+
+def dattri_project_fit_workspace_bytes(ctx, route=DATTRI_ROUTE_AUTO):
+    v = _sz()
+    _check(load().dattri_project_fit_workspace_bytes(ctx, route, ctypes.byref(v)),
+           "dattri_project_fit_workspace_bytes")
+    return v.value
+
+
+def dattri_project_and_fit(ctx, phi, phi_dtype, ld_phi, state, workspace, ws_bytes, route=DATTRI_ROUTE_AUTO,
+                           stream=None):
+    _check(load().dattri_project_and_fit(ctx, _ptr(phi), phi_dtype, ld_phi, _ptr(state), _ptr(workspace), ws_bytes,
+                                         route, _stream(stream)),
+           "dattri_project_and_fit")

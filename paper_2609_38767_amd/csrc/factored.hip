@@ -25,8 +25,32 @@
 namespace dattri {
 using namespace dev;
 
+// Two waves per SIMD where the accumulators and load ring fit in 256 VGPRs.
+constexpr int waves_of(int na, int nb) { return ((na * nb <= 16 && na <= 6) || na * nb <= 8) ? 2 : 1; }
+
+// Projected rows of a wave's RT x 16 token rows, tiles [t0, t0 + nt) of acc,
+// into dst rows of k floats (columns >= k and rows >= row_end are skipped).
+// 16x16 C layout: lane (g, n) holds rows 4g..4g+3 of column n.
+template <int RT, int NT>
+__device__ inline void store_rows(const f32x4 (&acc)[RT][NT], float* dst, int k, int t0, int nt, int r_wave,
+                                  int row_end, int g, int m16) {
+#pragma unroll
+  for (int rt = 0; rt < RT; ++rt)
+#pragma unroll
+    for (int t = 0; t < NT; ++t) {
+      const int col = (t - t0) * 16 + m16;
+      if (t >= t0 && t < t0 + nt && col < k) {
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const int row = r_wave + rt * 16 + 4 * g + i;
+          if (row < row_end) dst[(int64_t)row * k + col] = acc[rt][t][i];
+        }
+      }
+    }
+}
+
 template <int ELT, bool AL, int RT, int NA, int NB>
-__global__ __launch_bounds__(256, (AL && NA * NB <= 16) ? 2 : 1) void factored_kernel(const FactItem* __restrict__ items,
+__global__ __launch_bounds__(256, AL ? waves_of(NA, NB) : 1) void factored_kernel(const FactItem* __restrict__ items,
                                                           const FactGroup* __restrict__ groups,
                                                           const FactMember* __restrict__ members,
                                                           float* __restrict__ partials) {
@@ -72,6 +96,13 @@ __global__ __launch_bounds__(256, (AL && NA * NB <= 16) ? 2 : 1) void factored_k
 #pragma unroll
       for (int t = 0; t < NA; ++t) acc_a[rt][t] = f32x4{0.f, 0.f, 0.f, 0.f};
     project_rows<ELT, AL, RT, NA, NTL, PD>(ra, r_wave, rows_valid, d_in, d_in, pin, acc_a, pan);
+    // projected input rows of every member that asks for them
+    for (int mi = 0; mi < G.n_members; ++mi) {
+      const FactMember& M = members[G.member0 + mi];
+      if (M.rows_a)
+        store_rows<RT, NA>(acc_a, M.rows_a + (int64_t)ex * T * M.k_in, M.k_in, M.a_tile0, M.na, r_wave,
+                           row_end, g, m16);
+    }
 
     for (int mi = 0; mi < G.n_members; ++mi) {
       const FactMember& M = members[G.member0 + mi];
@@ -91,6 +122,9 @@ __global__ __launch_bounds__(256, (AL && NA * NB <= 16) ? 2 : 1) void factored_k
 #pragma unroll
         for (int t = 0; t < NB; ++t) acc_b[rt][t] = f32x4{0.f, 0.f, 0.f, 0.f};
       project_rows<ELT, AL, RT, NB, NTL, PD>(rb, r_wave, rows_valid, d_out, d_out, pout, acc_b, pan);
+      if (M.rows_b)
+        store_rows<RT, NB>(acc_b, M.rows_b + (int64_t)ex * T * M.k_out, M.k_out, 0, nb, r_wave, row_end, g,
+                           m16);
 
       // K slices (rt, j) outermost: consecutive MFMAs update different psi
       // blocks, so none waits on its predecessor's result
@@ -137,7 +171,7 @@ __global__ __launch_bounds__(256, (AL && NA * NB <= 16) ? 2 : 1) void factored_k
 // Aligned instances per (input tiles NA, output tiles NB); one unaligned
 // instance (8, 4) serves any group whose rows are not 16-byte multiples.
 // Rows per wave RT keeps two waves per SIMD within the register file.
-constexpr int rt_of(int na, int nb) { return (na <= 2 && nb <= 2) ? 4 : (na * nb <= 16 ? 2 : 1); }
+constexpr int rt_of(int na, int nb) { return (na <= 2 && nb <= 2) ? 4 : ((na * nb <= 16 && na <= 6) ? 2 : 1); }
 
 void factored_instance(int elt, int na_req, int nb_req, int aligned, int* na_inst, int* nb_inst,
                        int* rows_per_wave) {

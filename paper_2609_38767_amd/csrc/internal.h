@@ -58,6 +58,11 @@ struct FactMember {                 // one layer of a group
   int32_t a_tile0, na, nb;          // its input tiles [a_tile0, a_tile0+na), output tiles
   int32_t aligned, pad0;
   int64_t partial_base;             // float offset of (example 0, part 0)
+  // When not null, the kernel also stores the layer's projected token rows
+  // (float32 [n][T][k_in] and [n][T][k_out]; rows past an example's length
+  // are not written) for the curvature fit.
+  float* rows_a;
+  float* rows_b;
 };
 
 struct FactItem { int32_t group, example, chunk, pad; };
@@ -263,6 +268,18 @@ struct StatTask {
 };
 hipError_t launch_stat_reduce(const StatTask* tasks, int n_tasks, int max_out, const float* parts,
                               uint8_t* state, hipStream_t s);
+
+// Sums of outer products of stored projected token rows: for example i of an
+// op, rows t < min(lengths[i], T) at rows + (i*T + t)*ld + col0, k columns.
+// Work item (item, op) covers examples [item*ex_per_item, ...) and writes one
+// k x k partial at partial_base + item*k*k.
+struct RowOp {
+  const float* rows;
+  const int32_t* lengths;
+  int64_t ld, partial_base;
+  int32_t col0, k, T, n, ex_per_item, n_items;
+};
+hipError_t launch_rowcov(const RowOp* ops, int n_ops, int max_items, float* parts, hipStream_t s);
 
 // Symmetric eigendecomposition of sum / count (k x k, k <= kCurvMaxK).
 struct EigTask { int64_t sum_off, count_off, q_off, lam_off; int32_t k, pad0; };

@@ -187,6 +187,67 @@ hipError_t launch_zero(void* p, int64_t bytes, hipStream_t s) {
   return hipGetLastError();
 }
 
+// ------------------------------------------------ sums of stored projected rows
+constexpr int kRowTile = 64;  // token rows staged in LDS per step
+
+__global__ __launch_bounds__(256) void rowcov_kernel(const RowOp* __restrict__ ops,
+                                                     float* __restrict__ parts) {
+  __shared__ __align__(16) float R[kRowTile * kCurvMaxK];
+  const RowOp o = ops[blockIdx.y];
+  if ((int)blockIdx.x >= o.n_items) return;
+  const int k = o.k, tid = threadIdx.x;
+  const int nb = (k + 3) / 4;                      // 4 x 4 blocks per side
+  const int bi = tid / nb, bj = tid - (tid / nb) * nb;
+  const bool active = bi < nb;
+  const int c0 = 4 * bi, r0 = 4 * bj;
+  float acc[4][4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int j = 0; j < 4; ++j) acc[i][j] = 0.f;
+  for (int e = tid; e < kRowTile * kCurvMaxK; e += 256) R[e] = 0.f;  // columns >= k stay zero
+  const int e0 = blockIdx.x * o.ex_per_item, e1 = min(o.n, e0 + o.ex_per_item);
+  for (int ex = e0; ex < e1; ++ex) {
+    int t_eff = o.T;
+    if (o.lengths) t_eff = min(max(o.lengths[ex], 0), o.T);
+    const float* base = o.rows + (int64_t)ex * o.T * o.ld + o.col0;
+    for (int t0 = 0; t0 < t_eff; t0 += kRowTile) {  // uniform trip count
+      const int nr = min(kRowTile, t_eff - t0);
+      __syncthreads();  // the previous tile's readers are done
+      for (int e = tid; e < kRowTile * k; e += 256) {
+        const int r = e / k, c = e - (e / k) * k;
+        R[r * kCurvMaxK + c] = r < nr ? base[(int64_t)(t0 + r) * o.ld + c] : 0.f;
+      }
+      __syncthreads();
+      if (active) {
+        for (int r = 0; r < nr; ++r) {
+          const f32x4 a = *(const f32x4*)(R + r * kCurvMaxK + c0);
+          const f32x4 b = *(const f32x4*)(R + r * kCurvMaxK + r0);
+#pragma unroll
+          for (int i = 0; i < 4; ++i)
+#pragma unroll
+            for (int j = 0; j < 4; ++j) acc[i][j] = fmaf(a[i], b[j], acc[i][j]);
+        }
+      }
+    }
+  }
+  if (active) {
+    float* dst = parts + o.partial_base + (int64_t)blockIdx.x * k * k;
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+      for (int j = 0; j < 4; ++j)
+        if (c0 + i < k && r0 + j < k) dst[(c0 + i) * k + r0 + j] = acc[i][j];
+  }
+}
+
+hipError_t launch_rowcov(const RowOp* ops, int n_ops, int max_items, float* parts, hipStream_t s) {
+  if (n_ops <= 0 || max_items <= 0) return hipSuccess;
+  if (n_ops > 65535) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(rowcov_kernel, dim3(max_items, n_ops), dim3(256), 0, s, ops, parts);
+  return hipGetLastError();
+}
+
 // ------------------------------------------------------------ eigensolver
 constexpr int kEigLd = kCurvMaxK + 1;  // float64 row pitch: column walks spread over banks
 constexpr int kEigSweeps = 32;

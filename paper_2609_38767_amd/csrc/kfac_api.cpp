@@ -12,6 +12,7 @@
 #include "context.h"
 #include "dattri.h"
 #include "internal.h"
+#include "plan.h"
 
 using namespace dattri;
 
@@ -85,6 +86,26 @@ std::vector<RotTask> rot_tasks(const dattri_ctx* ctx, const CurvLayout& C) {
   return R;
 }
 
+// Reduction of one layer side's factor sums into the state: destination,
+// counter (A side: token rows, from the lengths when given; B side: examples)
+// and size; the caller fills in the partial layout.
+StatTask side_task(const dattri_ctx* ctx, const CurvLayout& C, int l, int side, int32_t n) {
+  const Layer& L = ctx->layers[l];
+  StatTask t;
+  std::memset(&t, 0, sizeof(t));
+  t.dst_off = side == 0 ? C.L[l].sum_a : C.L[l].sum_g;
+  t.count_off = C.L[l].counts + 8 * side;
+  if (side == 0 && L.lengths) {
+    t.lengths = L.lengths;
+    t.n_len = n;
+    t.T = L.T;
+  } else {
+    t.count_add = side == 0 ? (int64_t)n * L.T : (int64_t)n;
+  }
+  t.rows = t.cols = side == 0 ? L.k_in : L.k_out;
+  return t;
+}
+
 // ------------------------------------------------------ factor-sum planning
 struct FsumPlan {
   std::vector<FsumOp> ops;
@@ -97,7 +118,9 @@ struct FsumPlan {
   size_t off_ops = 0, off_items = 0, off_tasks = 0, blob_bytes = 0, off_parts = 0, total = 0;
 };
 
-dattri_status plan_fsum(const dattri_ctx* ctx, const CurvLayout& C, FsumPlan& P) {
+// Factor sums of every layer, or of the layers in `only`.
+dattri_status plan_fsum(const dattri_ctx* ctx, const CurvLayout& C, FsumPlan& P,
+                        const std::vector<int>* only = nullptr) {
   dattri_status st = check_layers(ctx);
   if (st != DATTRI_OK) return st;
   int32_t n = -1;
@@ -110,10 +133,11 @@ dattri_status plan_fsum(const dattri_ctx* ctx, const CurvLayout& C, FsumPlan& P)
   }
   P.n = n;
   const int elt = ctx->elt;
-  struct OpInfo { int inst_nt, aligned; int64_t units, unit_cost; };
+  struct OpInfo { int inst_nt, aligned; int64_t units, unit_cost; int layer, side; };
   std::vector<OpInfo> info;
   double total_cost = 0.0;
   for (size_t l = 0; l < ctx->layers.size(); ++l) {
+    if (only && std::find(only->begin(), only->end(), (int)l) == only->end()) continue;
     const Layer& L = ctx->layers[l];
     for (int side = 0; side < 2; ++side) {
       FsumOp O;
@@ -133,7 +157,7 @@ dattri_status plan_fsum(const dattri_ctx* ctx, const CurvLayout& C, FsumPlan& P)
       if (L.T <= cr) cr = std::max(sub, (L.T + sub - 1) / sub * sub);
       O.chunk_rows = cr;
       O.n_chunks = std::max(1, (L.T + cr - 1) / cr);
-      OpInfo I{inst, O.aligned, (int64_t)n * O.n_chunks, (int64_t)cr * O.d};
+      OpInfo I{inst, O.aligned, (int64_t)n * O.n_chunks, (int64_t)cr * O.d, (int)l, side};
       total_cost += (double)I.units * I.unit_cost;
       info.push_back(I);
       P.ops.push_back(O);
@@ -153,31 +177,16 @@ dattri_status plan_fsum(const dattri_ctx* ctx, const CurvLayout& C, FsumPlan& P)
     part_floats_total += (size_t)(nitems[o] * kWaves * kp * kp);
   }
   // reduction tasks: one per op (sum into sum_a / sum_g, counts N_tok / N)
-  for (size_t l = 0; l < ctx->layers.size(); ++l) {
-    const Layer& L = ctx->layers[l];
-    for (int side = 0; side < 2; ++side) {
-      const size_t o = 2 * l + side;
-      const int k = side == 0 ? L.k_in : L.k_out;
-      const int kp = P.ops[o].nt * 16;
-      StatTask t;
-      std::memset(&t, 0, sizeof(t));
-      t.part_base = P.ops[o].partial_base;
-      t.dst_off = side == 0 ? C.L[l].sum_a : C.L[l].sum_g;
-      t.count_off = C.L[l].counts + 8 * side;
-      if (side == 0 && L.lengths) {
-        t.lengths = L.lengths;
-        t.n_len = n;
-        t.T = L.T;
-      } else {
-        t.count_add = side == 0 ? (int64_t)n * L.T : (int64_t)n;
-      }
-      t.n_parts = (int32_t)(nitems[o] * kWaves);
-      t.part_floats = kp * kp;
-      t.ldp = kp;
-      t.rows = t.cols = k;
-      P.max_out = std::max(P.max_out, k * k);
-      P.tasks.push_back(t);
-    }
+  for (size_t o = 0; o < P.ops.size(); ++o) {
+    const int l = info[o].layer, side = info[o].side;
+    const int kp = P.ops[o].nt * 16;
+    StatTask t = side_task(ctx, C, l, side, n);
+    t.part_base = P.ops[o].partial_base;
+    t.n_parts = (int32_t)(nitems[o] * kWaves);
+    t.part_floats = kp * kp;
+    t.ldp = kp;
+    P.max_out = std::max(P.max_out, t.rows * t.cols);
+    P.tasks.push_back(t);
   }
   // One launch per kernel instance.  Inside a launch every item of an op runs
   // on one XCD (the op's projection map then stays in that XCD's L2): ops are
@@ -227,6 +236,81 @@ dattri_status plan_fsum(const dattri_ctx* ctx, const CurvLayout& C, FsumPlan& P)
   P.off_parts = off;
   off = align_up(off + part_floats_total * sizeof(float));
   P.total = off;
+  return DATTRI_OK;
+}
+
+// ------------------------------------------------ projection with the fit
+// The projection runs with projected token rows kept (fused factored members
+// store them, the split form has them in its stage-1 buffer); the factor sums
+// of those layers come from the stored rows, and only layers on the
+// materialized route (which never form projected rows) take the separate
+// factor-sum pass.  Workspace: [projection plan][row ops, row tasks, factor-sum
+// descriptors][row partials][factor-sum partials].
+constexpr int64_t kRowTargetItems = 2048;  // row-covariance workgroups aimed for
+
+struct FitPlan {
+  Plan proj;
+  std::vector<RowOp> rops;       // .rows set at run time from rop_off
+  std::vector<size_t> rop_off;   // workspace byte offset of each op's rows
+  std::vector<StatTask> rtasks;
+  int max_items = 0, max_out = 0;
+  FsumPlan mat;
+  bool has_mat = false;
+  size_t off_desc = 0, off_rops = 0, off_rtasks = 0, off_fdesc = 0, desc_bytes = 0;
+  size_t off_rparts = 0, off_fparts = 0, total = 0;
+};
+
+dattri_status plan_fit(const dattri_ctx* ctx, const CurvLayout& C, dattri_route route, FitPlan& F) {
+  dattri_status st = check_layers(ctx);
+  if (st != DATTRI_OK) return st;
+  if (route < DATTRI_ROUTE_AUTO || route > DATTRI_ROUTE_MATERIALIZED)
+    return fail(DATTRI_E_INVALID_ARG, "route %d unknown", (int)route);
+  for (size_t l = 0; l < ctx->layers.size(); ++l)
+    if (!ctx->layers[l].bound) return fail(DATTRI_E_STATE, "layer %zu: projection maps not bound", l);
+  if ((st = build_plan(ctx, route, F.proj, true)) != DATTRI_OK) return st;
+  const int32_t n = ctx->layers[0].n;
+  const int64_t n_ops = (int64_t)F.proj.row_srcs.size();
+  const int epi = (int)std::max<int64_t>(1, cdiv((int64_t)n * n_ops, kRowTargetItems));
+  size_t parts = 0;
+  for (const RowSrc& R : F.proj.row_srcs) {
+    const Layer& L = ctx->layers[R.layer];
+    const int k = R.side ? L.k_out : L.k_in;
+    RowOp o;
+    std::memset(&o, 0, sizeof(o));
+    o.lengths = L.lengths;
+    o.ld = R.ld;
+    o.col0 = R.col0;
+    o.k = k;
+    o.T = L.T;
+    o.n = n;
+    o.ex_per_item = epi;
+    o.n_items = n > 0 ? (int)cdiv(n, epi) : 0;
+    o.partial_base = (int64_t)parts;
+    parts += (size_t)o.n_items * k * k;
+    StatTask t = side_task(ctx, C, R.layer, R.side, n);
+    t.part_base = o.partial_base;
+    t.n_parts = o.n_items;
+    t.part_floats = k * k;
+    t.ldp = k;
+    F.max_items = std::max(F.max_items, o.n_items);
+    F.max_out = std::max(F.max_out, k * k);
+    F.rops.push_back(o);
+    F.rop_off.push_back(R.off);
+    F.rtasks.push_back(t);
+  }
+  if (!F.proj.mat_layers.empty()) {
+    if ((st = plan_fsum(ctx, C, F.mat, &F.proj.mat_layers)) != DATTRI_OK) return st;
+    F.has_mat = true;
+  }
+  size_t off = align_up(F.proj.total);
+  F.off_desc = off;
+  F.off_rops = off;   off = align_up(off + F.rops.size() * sizeof(RowOp));
+  F.off_rtasks = off; off = align_up(off + F.rtasks.size() * sizeof(StatTask));
+  F.off_fdesc = off;  off = align_up(off + (F.has_mat ? F.mat.blob_bytes : 0));
+  F.desc_bytes = off - F.off_desc;
+  F.off_rparts = off; off = align_up(off + parts * sizeof(float));
+  F.off_fparts = off; off = align_up(off + (F.has_mat ? F.mat.total - F.mat.off_parts : 0));
+  F.total = off;
   return DATTRI_OK;
 }
 
@@ -495,6 +579,69 @@ dattri_status dattri_curvature_precondition(const dattri_ctx* ctx, const void* s
   HIP_TRY(launch_precondition((const RotTask*)(base + C.off_rot), (int)R.size(), base, (int)kind, damping_rel,
                               damping_abs, phi_q, in_dtype == DATTRI_BF16, ld_q, n_q, out,
                               out_dtype == DATTRI_BF16, ld_out, s));
+  return DATTRI_OK;
+}
+
+dattri_status dattri_project_fit_workspace_bytes(const dattri_ctx* ctx, dattri_route route, size_t* bytes) {
+  reset_error();
+  if (!bytes) return fail(DATTRI_E_INVALID_ARG, "bytes is NULL");
+  CurvLayout C;
+  dattri_status st = check_layers(ctx);
+  if (st != DATTRI_OK) return st;
+  curv_layout(ctx, C);
+  FitPlan F;
+  if ((st = plan_fit(ctx, C, route, F)) != DATTRI_OK) return st;
+  *bytes = F.total;
+  return DATTRI_OK;
+}
+
+dattri_status dattri_project_and_fit(dattri_ctx* ctx, void* phi, dattri_dtype phi_dtype, int64_t ld_phi,
+                                     void* state, void* workspace, size_t ws_bytes, dattri_route route,
+                                     void* stream) {
+  reset_error();
+  dattri_status st = check_layers(ctx);
+  if (st != DATTRI_OK) return st;
+  if ((st = check_state(state)) != DATTRI_OK) return st;
+  if (phi_dtype != DATTRI_F32 && phi_dtype != DATTRI_BF16)
+    return fail(DATTRI_E_DTYPE, "phi dtype %d is neither F32 nor BF16", (int)phi_dtype);
+  CurvLayout C;
+  curv_layout(ctx, C);
+  FitPlan F;
+  if ((st = plan_fit(ctx, C, route, F)) != DATTRI_OK) return st;
+  const int32_t n = ctx->layers[0].n;
+  if (ld_phi < ctx->F) return fail(DATTRI_E_SHAPE, "ld_phi=%lld < F=%lld", (long long)ld_phi, (long long)ctx->F);
+  if (n == 0) return DATTRI_OK;
+  if (!phi) return fail(DATTRI_E_INVALID_ARG, "phi is NULL");
+  if ((st = check_ws(workspace, ws_bytes, F.total)) != DATTRI_OK) return st;
+  hipStream_t s = (hipStream_t)stream;
+  uint8_t* ws = (uint8_t*)workspace;
+  if ((st = run_plan(ctx, F.proj, phi, phi_dtype, ld_phi, workspace, ws_bytes, s)) != DATTRI_OK) return st;
+  std::vector<RowOp> rops = F.rops;
+  for (size_t i = 0; i < rops.size(); ++i) rops[i].rows = (const float*)(ws + F.rop_off[i]);
+  std::vector<const void*> srcs = {rops.data(), F.rtasks.data()};
+  std::vector<size_t> offs = {F.off_rops - F.off_desc, F.off_rtasks - F.off_desc};
+  std::vector<size_t> sizes = {rops.size() * sizeof(RowOp), F.rtasks.size() * sizeof(StatTask)};
+  if (F.has_mat) {
+    const size_t b = F.off_fdesc - F.off_desc;
+    srcs.insert(srcs.end(), {F.mat.ops.data(), F.mat.items.data(), F.mat.tasks.data()});
+    offs.insert(offs.end(), {b + F.mat.off_ops, b + F.mat.off_items, b + F.mat.off_tasks});
+    sizes.insert(sizes.end(), {F.mat.ops.size() * sizeof(FsumOp), F.mat.items.size() * sizeof(FsumItem),
+                               F.mat.tasks.size() * sizeof(StatTask)});
+  }
+  HIP_TRY(upload(ctx, ws + F.off_desc, srcs, offs, sizes, F.desc_bytes, s));
+  float* rparts = (float*)(ws + F.off_rparts);
+  HIP_TRY(launch_rowcov((const RowOp*)(ws + F.off_rops), (int)rops.size(), F.max_items, rparts, s));
+  HIP_TRY(launch_stat_reduce((const StatTask*)(ws + F.off_rtasks), (int)F.rtasks.size(), F.max_out, rparts,
+                             (uint8_t*)state, s));
+  if (F.has_mat) {
+    const uint8_t* fd = ws + F.off_fdesc;
+    float* fparts = (float*)(ws + F.off_fparts);
+    for (const FsumPlan::Launch& L : F.mat.launches)
+      HIP_TRY(launch_fsum(L.elt, L.aligned, L.nt, (const FsumItem*)(fd + F.mat.off_items) + L.first, L.count,
+                          (const FsumOp*)(fd + F.mat.off_ops), fparts, s));
+    HIP_TRY(launch_stat_reduce((const StatTask*)(fd + F.mat.off_tasks), (int)F.mat.tasks.size(), F.mat.max_out,
+                               fparts, (uint8_t*)state, s));
+  }
   return DATTRI_OK;
 }
 

@@ -13,6 +13,7 @@
 #include "context.h"
 #include "dattri.h"
 #include "internal.h"
+#include "plan.h"
 #include "runtime.h"
 
 using namespace dattri;
@@ -109,40 +110,6 @@ dattri_route choose_route(const dattri_ctx* ctx, const Layer& L, dattri_route fo
 }
 
 // ---------------------------------------------------------------- planning
-struct MatChunk {
-  int layer, ex_begin, ex_count, n_ublocks, n_ksplit, kb_per_split, task;
-};
-
-struct Plan {
-  // host-side descriptors (device pointers inside)
-  std::vector<FactItem> items;
-  std::vector<FactGroup> groups;
-  std::vector<FactMember> members;
-  std::vector<ReduceTask> tasks;  // factored tasks first, then one per MatChunk
-  int n_fact_tasks = 0;
-  int fact_max_out = 0;            // largest k_in*k_out over the factored tasks
-  struct Launch { int elt, na, nb, aligned, first, count; };
-  std::vector<Launch> launches;
-  std::vector<MatChunk> mat;
-  // split form of the factored route (captures with few fused work items)
-  std::vector<SplitOp> sops;
-  std::vector<SplitItem> sitems;
-  std::vector<ContractTask> ctasks;
-  struct SplitLaunch { int elt, aligned, nt, first, count; };
-  std::vector<SplitLaunch> slaunches;
-  std::vector<ReduceTask> stasks;  // token-chunked contractions to reduce
-  std::vector<SlabSumTask> slabsum;
-  int64_t slabsum_max_n4 = 0;
-  int split_max_tchunks = 0, split_max_out = 0;
-  // workspace layout (byte offsets)
-  size_t off_items = 0, off_groups = 0, off_members = 0, off_tasks = 0;
-  size_t off_sops = 0, off_sitems = 0, off_ctasks = 0, off_stasks = 0, off_slabsum = 0;
-  size_t blob_bytes = 0;
-  size_t off_fpart = 0, fpart_bytes = 0, off_g = 0, g_bytes = 0, off_mpart = 0, mpart_bytes = 0;
-  size_t off_proj = 0, proj_bytes = 0, off_spart = 0, spart_bytes = 0;
-  size_t total = 0;
-};
-
 // The split form serves every factored group when the fused kernel would have
 // fewer than kSplitMinFusedItems work items.
 constexpr int64_t kSplitMinFusedItems = 1024;
@@ -164,7 +131,9 @@ dattri_status check_captures(const dattri_ctx* ctx, int32_t* n_out) {
   return DATTRI_OK;
 }
 
-dattri_status build_plan(const dattri_ctx* ctx, dattri_route forced, Plan& P) {
+}  // namespace
+
+dattri_status dattri::build_plan(const dattri_ctx* ctx, dattri_route forced, Plan& P, bool rows) {
   int32_t n = 0;
   dattri_status st = check_captures(ctx, &n);
   if (st != DATTRI_OK) return st;
@@ -245,6 +214,9 @@ dattri_status build_plan(const dattri_ctx* ctx, dattri_route forced, Plan& P) {
   };
 
   size_t fpart_floats = 0;
+  std::vector<int> member_layer;  // layer of each fused member
+  struct SplitRows { int layer, a_op, b_op, a_col0; };
+  std::vector<SplitRows> split_rows;  // split-form layers: their stage-1 ops
   struct Inst { int na, nb, aligned; std::vector<int> groups; };
   std::vector<Inst> insts;
   std::vector<double> group_cost;
@@ -272,6 +244,7 @@ dattri_status build_plan(const dattri_ctx* ctx, dattri_route forced, Plan& P) {
       const Layer& L = ctx->layers[li];
       FactMember M;
       std::memset(&M, 0, sizeof(M));
+      member_layer.push_back(li);
       M.B = L.B;
       M.P_out = L.P_out;
       M.d_out = L.d_out;
@@ -403,6 +376,7 @@ dattri_status build_plan(const dattri_ctx* ctx, dattri_route forced, Plan& P) {
         C.lengths = L.lengths;
         P.ctasks.push_back(C);
         pend.push_back({a_op, a_op + 1 + (int)Bs.size()});
+        split_rows.push_back({li, a_op, a_op + 1 + (int)Bs.size(), na * 16});
         Bs.push_back(B);
         na += mt;
       }
@@ -542,9 +516,40 @@ dattri_status build_plan(const dattri_ctx* ctx, dattri_route forced, Plan& P) {
   P.off_mpart = off;   P.mpart_bytes = mpart_floats * 4; off = align_up(off + P.mpart_bytes);
   P.off_proj = off;    off = align_up(off + P.proj_bytes);
   P.off_spart = off;   off = align_up(off + P.spart_bytes);
+  // projected token rows of the fused members, and where every factored
+  // layer side's rows sit (split form: slab 0 of its stage-1 op)
+  P.rows = rows;
+  if (rows) {
+    P.off_rows = off;
+    size_t r = 0;
+    P.member_rows.assign(2 * P.members.size(), 0);
+    for (const FactGroup& G : P.groups)
+      for (int m = 0; m < G.n_members; ++m) {
+        const int mi = G.member0 + m;
+        const FactMember& M = P.members[mi];
+        const size_t a = align_up(r + (size_t)n * G.T * M.k_in * 4);
+        P.member_rows[2 * mi] = P.off_rows + r;
+        P.member_rows[2 * mi + 1] = P.off_rows + a;
+        r = align_up(a + (size_t)n * G.T * M.k_out * 4);
+        P.row_srcs.push_back({member_layer[mi], 0, P.member_rows[2 * mi], M.k_in, 0});
+        P.row_srcs.push_back({member_layer[mi], 1, P.member_rows[2 * mi + 1], M.k_out, 0});
+      }
+    P.rows_bytes = r;
+    off = align_up(off + r);
+    for (const SplitRows& R : split_rows) {
+      const SplitOp& A = P.sops[R.a_op];
+      const SplitOp& B = P.sops[R.b_op];
+      P.row_srcs.push_back({R.layer, 0, P.off_proj + (size_t)A.out_base * 4, A.nt * 16, R.a_col0});
+      P.row_srcs.push_back({R.layer, 1, P.off_proj + (size_t)B.out_base * 4, B.nt * 16, 0});
+    }
+    for (size_t l = 0; l < ctx->layers.size(); ++l)
+      if (choose_route(ctx, ctx->layers[l], forced) == DATTRI_ROUTE_MATERIALIZED) P.mat_layers.push_back((int)l);
+  }
   P.total = std::max<size_t>(off, kAlign);
   return DATTRI_OK;
 }
+
+namespace {
 
 dattri_status check_layer(const dattri_ctx* ctx, int32_t layer) {
   if (!ctx) return fail(DATTRI_E_INVALID_ARG, "ctx is NULL");
@@ -565,6 +570,97 @@ void logical_map(const dattri_ctx* ctx, int layer, int side, std::vector<float>&
 }  // namespace
 
 // =================================================================== C ABI
+dattri_status dattri::run_plan(dattri_ctx* ctx, const Plan& P, void* phi, dattri_dtype phi_dtype,
+                               int64_t ld_phi, void* workspace, size_t ws_bytes, hipStream_t s) {
+  const int32_t n = ctx->layers[0].n;
+  if (ld_phi < ctx->F) return fail(DATTRI_E_SHAPE, "ld_phi=%lld < F=%lld", (long long)ld_phi, (long long)ctx->F);
+  if (n == 0) return DATTRI_OK;
+  if (!phi) return fail(DATTRI_E_INVALID_ARG, "phi is NULL");
+  if (!workspace) return fail(DATTRI_E_WORKSPACE, "workspace is NULL (needs %zu bytes)", P.total);
+  if ((uintptr_t)workspace % kAlign) return fail(DATTRI_E_WORKSPACE, "workspace must be 256-byte aligned");
+  if (ws_bytes < P.total)
+    return fail(DATTRI_E_WORKSPACE, "workspace has %zu bytes, needs %zu", ws_bytes, P.total);
+
+  // Upload the launch plan into the head of the workspace.
+  ctx->blob.assign(P.blob_bytes, 0);
+  auto put = [&](size_t off, const void* src, size_t bytes) {
+    if (bytes) std::memcpy(ctx->blob.data() + off, src, bytes);
+  };
+  put(P.off_items, P.items.data(), P.items.size() * sizeof(FactItem));
+  put(P.off_groups, P.groups.data(), P.groups.size() * sizeof(FactGroup));
+  if (P.rows) {  // members keep their projected token rows in the workspace
+    std::vector<FactMember> mem = P.members;
+    for (size_t m = 0; m < mem.size(); ++m) {
+      mem[m].rows_a = (float*)((uint8_t*)workspace + P.member_rows[2 * m]);
+      mem[m].rows_b = (float*)((uint8_t*)workspace + P.member_rows[2 * m + 1]);
+    }
+    put(P.off_members, mem.data(), mem.size() * sizeof(FactMember));
+  } else {
+    put(P.off_members, P.members.data(), P.members.size() * sizeof(FactMember));
+  }
+  put(P.off_tasks, P.tasks.data(), P.tasks.size() * sizeof(ReduceTask));
+  put(P.off_sops, P.sops.data(), P.sops.size() * sizeof(SplitOp));
+  put(P.off_sitems, P.sitems.data(), P.sitems.size() * sizeof(SplitItem));
+  put(P.off_ctasks, P.ctasks.data(), P.ctasks.size() * sizeof(ContractTask));
+  put(P.off_stasks, P.stasks.data(), P.stasks.size() * sizeof(ReduceTask));
+  put(P.off_slabsum, P.slabsum.data(), P.slabsum.size() * sizeof(SlabSumTask));
+  uint8_t* ws = (uint8_t*)workspace;
+  HIP_TRY(hipMemcpyAsync(ws, ctx->blob.data(), P.blob_bytes, hipMemcpyHostToDevice, s));
+
+  const FactItem* d_items = (const FactItem*)(ws + P.off_items);
+  const FactGroup* d_groups = (const FactGroup*)(ws + P.off_groups);
+  const FactMember* d_members = (const FactMember*)(ws + P.off_members);
+  const ReduceTask* d_tasks = (const ReduceTask*)(ws + P.off_tasks);
+  float* fpart = (float*)(ws + P.off_fpart);
+  const int phi_bf16 = phi_dtype == DATTRI_BF16;
+  for (const Plan::Launch& L : P.launches)
+    HIP_TRY(launch_factored(L.elt, L.na, L.nb, L.aligned, d_items + L.first, L.count, d_groups,
+                            d_members, fpart, s));
+  if (P.n_fact_tasks)
+    HIP_TRY(launch_reduce(d_tasks, P.n_fact_tasks, n, P.fact_max_out, fpart, phi, phi_bf16, ld_phi, s));
+
+  const SplitOp* d_sops = (const SplitOp*)(ws + P.off_sops);
+  const SplitItem* d_sitems = (const SplitItem*)(ws + P.off_sitems);
+  const ContractTask* d_ctasks = (const ContractTask*)(ws + P.off_ctasks);
+  float* proj = (float*)(ws + P.off_proj);
+  for (const Plan::SplitLaunch& L : P.slaunches)
+    HIP_TRY(launch_split_project(L.elt, L.aligned, L.nt, d_sitems + L.first, L.count, d_sops, proj, s));
+  if (!P.slabsum.empty())
+    HIP_TRY(launch_slab_sum((const SlabSumTask*)(ws + P.off_slabsum), (int)P.slabsum.size(),
+                            P.slabsum_max_n4, proj, s));
+  float* spart = (float*)(ws + P.off_spart);
+  if (!P.ctasks.empty())
+    HIP_TRY(launch_split_contract(d_ctasks, (int)P.ctasks.size(), n, P.split_max_tchunks, proj, spart,
+                                  phi, phi_bf16, ld_phi, s));
+  if (!P.stasks.empty())
+    HIP_TRY(launch_reduce((const ReduceTask*)(ws + P.off_stasks), (int)P.stasks.size(), n,
+                          P.split_max_out, spart, phi, phi_bf16, ld_phi, s));
+
+  float* gbuf = (float*)(ws + P.off_g);
+  float* mpart = (float*)(ws + P.off_mpart);
+  for (const MatChunk& mc : P.mat) {
+    const Layer& L = ctx->layers[mc.layer];
+    GradArgs ga;
+    ga.A = L.A; ga.B = L.B; ga.lengths = L.lengths;
+    ga.d_in = L.d_in; ga.d_out = L.d_out; ga.T = L.T;
+    ga.ex_begin = mc.ex_begin; ga.ex_count = mc.ex_count;
+    ga.aligned = ((uintptr_t)L.A % 16 == 0) && ((uintptr_t)L.B % 16 == 0) &&
+                 (L.d_in * ctx->elt) % 16 == 0 && (L.d_out * ctx->elt) % 16 == 0;
+    ga.G = gbuf;
+    HIP_TRY(launch_gradient(ctx->elt, ga, s));
+    GProjArgs pa;
+    pa.G = gbuf; pa.P_in = L.P_in; pa.P_out = L.P_out;
+    pa.d_in = L.d_in; pa.d_out = L.d_out; pa.k_in = L.k_in; pa.k_out = L.k_out;
+    pa.ex_count = mc.ex_count; pa.n_ublocks = mc.n_ublocks; pa.partials = mpart;
+    pa.n_ksplit = mc.n_ksplit; pa.kb_per_split = mc.kb_per_split;
+    HIP_TRY(launch_gproject(ctx->elt, pa, s));
+    HIP_TRY(launch_reduce(d_tasks + mc.task, 1, mc.ex_count, L.k_in * L.k_out, mpart, phi, phi_bf16,
+                          ld_phi, s));
+  }
+  return DATTRI_OK;
+}
+
+
 extern "C" {
 
 const char* dattri_last_error(void) { return last_error_message(); }
@@ -744,7 +840,7 @@ dattri_status dattri_workspace_bytes(const dattri_ctx* ctx, dattri_route route, 
   if (route < DATTRI_ROUTE_AUTO || route > DATTRI_ROUTE_MATERIALIZED)
     return fail(DATTRI_E_INVALID_ARG, "route %d unknown", (int)route);
   Plan P;
-  dattri_status st = build_plan(ctx, route, P);
+  dattri_status st = build_plan(ctx, route, P, false);
   if (st != DATTRI_OK) return st;
   *bytes = P.total;
   return DATTRI_OK;
@@ -779,86 +875,9 @@ dattri_status dattri_project_per_example(dattri_ctx* ctx, void* phi, dattri_dtyp
     if (!ctx->layers[l].bound)
       return fail(DATTRI_E_STATE, "layer %zu: projection maps not bound", l);
   Plan P;
-  dattri_status st = build_plan(ctx, route, P);
+  dattri_status st = build_plan(ctx, route, P, false);
   if (st != DATTRI_OK) return st;
-  const int32_t n = ctx->layers[0].n;
-  if (ld_phi < ctx->F) return fail(DATTRI_E_SHAPE, "ld_phi=%lld < F=%lld", (long long)ld_phi, (long long)ctx->F);
-  if (n == 0) return DATTRI_OK;
-  if (!phi) return fail(DATTRI_E_INVALID_ARG, "phi is NULL");
-  if (!workspace) return fail(DATTRI_E_WORKSPACE, "workspace is NULL (needs %zu bytes)", P.total);
-  if ((uintptr_t)workspace % kAlign) return fail(DATTRI_E_WORKSPACE, "workspace must be 256-byte aligned");
-  if (ws_bytes < P.total)
-    return fail(DATTRI_E_WORKSPACE, "workspace has %zu bytes, needs %zu", ws_bytes, P.total);
-
-  // Upload the launch plan into the head of the workspace.
-  ctx->blob.assign(P.blob_bytes, 0);
-  auto put = [&](size_t off, const void* src, size_t bytes) {
-    if (bytes) std::memcpy(ctx->blob.data() + off, src, bytes);
-  };
-  put(P.off_items, P.items.data(), P.items.size() * sizeof(FactItem));
-  put(P.off_groups, P.groups.data(), P.groups.size() * sizeof(FactGroup));
-  put(P.off_members, P.members.data(), P.members.size() * sizeof(FactMember));
-  put(P.off_tasks, P.tasks.data(), P.tasks.size() * sizeof(ReduceTask));
-  put(P.off_sops, P.sops.data(), P.sops.size() * sizeof(SplitOp));
-  put(P.off_sitems, P.sitems.data(), P.sitems.size() * sizeof(SplitItem));
-  put(P.off_ctasks, P.ctasks.data(), P.ctasks.size() * sizeof(ContractTask));
-  put(P.off_stasks, P.stasks.data(), P.stasks.size() * sizeof(ReduceTask));
-  put(P.off_slabsum, P.slabsum.data(), P.slabsum.size() * sizeof(SlabSumTask));
-  hipStream_t s = (hipStream_t)stream;
-  uint8_t* ws = (uint8_t*)workspace;
-  HIP_TRY(hipMemcpyAsync(ws, ctx->blob.data(), P.blob_bytes, hipMemcpyHostToDevice, s));
-
-  const FactItem* d_items = (const FactItem*)(ws + P.off_items);
-  const FactGroup* d_groups = (const FactGroup*)(ws + P.off_groups);
-  const FactMember* d_members = (const FactMember*)(ws + P.off_members);
-  const ReduceTask* d_tasks = (const ReduceTask*)(ws + P.off_tasks);
-  float* fpart = (float*)(ws + P.off_fpart);
-  const int phi_bf16 = phi_dtype == DATTRI_BF16;
-  for (const Plan::Launch& L : P.launches)
-    HIP_TRY(launch_factored(L.elt, L.na, L.nb, L.aligned, d_items + L.first, L.count, d_groups,
-                            d_members, fpart, s));
-  if (P.n_fact_tasks)
-    HIP_TRY(launch_reduce(d_tasks, P.n_fact_tasks, n, P.fact_max_out, fpart, phi, phi_bf16, ld_phi, s));
-
-  const SplitOp* d_sops = (const SplitOp*)(ws + P.off_sops);
-  const SplitItem* d_sitems = (const SplitItem*)(ws + P.off_sitems);
-  const ContractTask* d_ctasks = (const ContractTask*)(ws + P.off_ctasks);
-  float* proj = (float*)(ws + P.off_proj);
-  for (const Plan::SplitLaunch& L : P.slaunches)
-    HIP_TRY(launch_split_project(L.elt, L.aligned, L.nt, d_sitems + L.first, L.count, d_sops, proj, s));
-  if (!P.slabsum.empty())
-    HIP_TRY(launch_slab_sum((const SlabSumTask*)(ws + P.off_slabsum), (int)P.slabsum.size(),
-                            P.slabsum_max_n4, proj, s));
-  float* spart = (float*)(ws + P.off_spart);
-  if (!P.ctasks.empty())
-    HIP_TRY(launch_split_contract(d_ctasks, (int)P.ctasks.size(), n, P.split_max_tchunks, proj, spart,
-                                  phi, phi_bf16, ld_phi, s));
-  if (!P.stasks.empty())
-    HIP_TRY(launch_reduce((const ReduceTask*)(ws + P.off_stasks), (int)P.stasks.size(), n,
-                          P.split_max_out, spart, phi, phi_bf16, ld_phi, s));
-
-  float* gbuf = (float*)(ws + P.off_g);
-  float* mpart = (float*)(ws + P.off_mpart);
-  for (const MatChunk& mc : P.mat) {
-    const Layer& L = ctx->layers[mc.layer];
-    GradArgs ga;
-    ga.A = L.A; ga.B = L.B; ga.lengths = L.lengths;
-    ga.d_in = L.d_in; ga.d_out = L.d_out; ga.T = L.T;
-    ga.ex_begin = mc.ex_begin; ga.ex_count = mc.ex_count;
-    ga.aligned = ((uintptr_t)L.A % 16 == 0) && ((uintptr_t)L.B % 16 == 0) &&
-                 (L.d_in * ctx->elt) % 16 == 0 && (L.d_out * ctx->elt) % 16 == 0;
-    ga.G = gbuf;
-    HIP_TRY(launch_gradient(ctx->elt, ga, s));
-    GProjArgs pa;
-    pa.G = gbuf; pa.P_in = L.P_in; pa.P_out = L.P_out;
-    pa.d_in = L.d_in; pa.d_out = L.d_out; pa.k_in = L.k_in; pa.k_out = L.k_out;
-    pa.ex_count = mc.ex_count; pa.n_ublocks = mc.n_ublocks; pa.partials = mpart;
-    pa.n_ksplit = mc.n_ksplit; pa.kb_per_split = mc.kb_per_split;
-    HIP_TRY(launch_gproject(ctx->elt, pa, s));
-    HIP_TRY(launch_reduce(d_tasks + mc.task, 1, mc.ex_count, L.k_in * L.k_out, mpart, phi, phi_bf16,
-                          ld_phi, s));
-  }
-  return DATTRI_OK;
+  return run_plan(ctx, P, phi, phi_dtype, ld_phi, workspace, ws_bytes, (hipStream_t)stream);
 }
 
 dattri_status dattri_materialize_gradient(dattri_ctx* ctx, int32_t layer, int32_t ex_begin,

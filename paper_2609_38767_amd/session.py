@@ -20,7 +20,8 @@ from . import (DATTRI_BF16, DATTRI_F32, DATTRI_ROUTE_AUTO, dattri_bind_projectio
                dattri_curvature_state_bytes, dattri_curvature_layout_of, dattri_curvature_reset,
                dattri_curvature_fit_workspace_bytes, dattri_curvature_accumulate_factors,
                dattri_curvature_eigen, dattri_curvature_ekfac_workspace_bytes,
-               dattri_curvature_accumulate_ekfac, dattri_curvature_precondition)
+               dattri_curvature_accumulate_ekfac, dattri_curvature_precondition,
+               dattri_project_fit_workspace_bytes, dattri_project_and_fit)
 
 DTYPES = {"f32": (DATTRI_F32, torch.float32), "bf16": (DATTRI_BF16, torch.bfloat16)}
 
@@ -172,6 +173,16 @@ class Curvature:
         """Adds the projected factor sums of the session's current captures."""
         ws = self._workspace(dattri_curvature_fit_workspace_bytes(self.sess.ctx))
         dattri_curvature_accumulate_factors(self.sess.ctx, self.state, ws, ws.numel(), stream)
+
+    def project_and_fit(self, n, route=DATTRI_ROUTE_AUTO, phi_dtype="f32", phi=None, stream=None):
+        """The session's projected gradients and, in the same pass, the factor
+        sums of its captures."""
+        code, _ = DTYPES[phi_dtype]
+        if phi is None:
+            phi = feature_rows(n, self.sess.F, phi_dtype, self.sess.device)
+        ws = self._workspace(dattri_project_fit_workspace_bytes(self.sess.ctx, route))
+        dattri_project_and_fit(self.sess.ctx, phi, code, phi.stride(0), self.state, ws, ws.numel(), route, stream)
+        return phi
 
     def eigen(self, stream=None):
         dattri_curvature_eigen(self.sess.ctx, self.state, stream)

@@ -79,6 +79,40 @@ def test_factor_sums(dtype, T, lens):
         assert c.field(li, "counts").tolist() == [nt, ne, 0]
 
 
+FIT_CASES = [("auto", None), ("factored", dt.DATTRI_FORM_FUSED), ("factored", dt.DATTRI_FORM_SPLIT),
+             ("materialized", None)]
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("route,form", FIT_CASES)
+def test_project_and_fit(dtype, route, form):
+    """Projection with the factor sums taken in the same pass: phi equal to the
+    plain projection's, sums and counts equal to the oracle's."""
+    routes = {"auto": dt.DATTRI_ROUTE_AUTO, "factored": dt.DATTRI_ROUTE_FACTORED,
+              "materialized": dt.DATTRI_ROUTE_MATERIALIZED}
+    lens = [300, 0, 129, 64]
+    n, T = len(lens), 300
+    print(f"[curvature] project_and_fit dtype={dtype} route={route} form={form}", flush=True)
+    inputs = _inputs(LAYERS, n, T, dtype, seed=61)
+    lengths = torch.tensor(lens, dtype=torch.int32, device=DEV)
+    s = ProjectionSession(LAYERS, dtype=dtype, seed=7, form=form)
+    for li, (A, B) in enumerate(inputs):
+        s.capture(li, A, B, lengths)
+    c = Curvature(s)
+    phi = c.project_and_fit(n, route=routes[route])
+    ref_phi = s.project(n, route=routes[route])
+    torch.cuda.synchronize()
+    assert torch.equal(phi, ref_phi)
+    maps = oracle_maps(7, LAYERS, dtype)
+    for li in range(len(LAYERS)):
+        A, B = host64(inputs[li][0]), host64(inputs[li][1])
+        SA, SG, nt, ne = ok.factor_sums(A, B, maps[li][0], maps[li][1], lens)
+        ea = rel_fro(host64(c.field(li, "sum_a")), SA)
+        eg = rel_fro(host64(c.field(li, "sum_g")), SG)
+        assert ea <= 1e-5 and eg <= 1e-5, (li, ea, eg)
+        assert c.field(li, "counts").tolist() == [nt, ne, 0]
+
+
 def test_factor_sums_accumulate_and_reset():
     n, T = 3, 40
     a = _inputs(LAYERS[:2], n, T, "f32", seed=31, batch=0)

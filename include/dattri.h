@@ -83,7 +83,9 @@ typedef enum {
  *          example's tokens in chunks; suited to captures with few examples
  *          or short sequences, where the fused kernel has little parallelism.
  * AUTO picks SPLIT when the fused kernel would have fewer than 1024 work
- * items, FUSED otherwise. */
+ * items, and for input groups whose maps are wider than 48 columns on both
+ * sides (the fused kernel then holds too few token rows per wave to stream
+ * at full rate); FUSED otherwise. */
 typedef enum {
   DATTRI_FORM_AUTO = 0,
   DATTRI_FORM_FUSED = 1,

@@ -99,7 +99,10 @@ hipError_t launch_reduce(const ReduceTask* tasks, int n_tasks, int n_examples, i
 // n*T rows) slab by slab over the feature dimension d, writing float32
 // partial projections [slab][row][tile cols]; stage 2 sums the slabs and
 // contracts each example's tokens into its layer block of phi.
-constexpr int kSplitRows = 128;     // rows per stage-1 workgroup (4 waves x 2 row tiles)
+// Rows per stage-1 workgroup of the instance with nt_inst tiles: 4 waves of
+// 4 row tiles (2 at 8 tiles, where 4 would not fit the register file).
+constexpr int split_rt_of(int nt_inst) { return nt_inst <= 4 ? 4 : 2; }
+constexpr int split_rows_of(int nt_inst) { return 4 * split_rt_of(nt_inst) * 16; }
 constexpr int kSplitSlabQuantum = 128;  // slab widths are multiples of this
 struct SplitOp {                    // one factor block: a group's A or a member's B
   const void* X;                    // [rows, ld] row-major

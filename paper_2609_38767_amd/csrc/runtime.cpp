@@ -206,11 +206,16 @@ dattri_status dattri::build_plan(const dattri_ctx* ctx, dattri_route forced, Pla
     fused_items_total += (int64_t)n * S.n_chunks;
   }
   const bool few_items = fused_items_total < kSplitMinFusedItems;
+  // Wide maps (4 x 4 input x output tiles and more, k > 48 on both sides)
+  // leave the fused kernel 2 row tiles per wave and 2 waves per SIMD; the
+  // split form, which projects one factor at a time, streams faster there
+  // (Qwen2.5-7B-shaped stack, k = 64, T = 512, 32 examples: 19.2 ms vs
+  // 26.8 ms per batch on MI355X).
   auto use_split = [&](size_t g) {
     const Layer& H = ctx->layers[group_layers[g][0]];
     if ((int64_t)n * H.T > (int64_t)INT32_MAX / 2 || n > 65535) return false;  // index / grid range
     if (ctx->form != DATTRI_FORM_AUTO) return ctx->form == DATTRI_FORM_SPLIT;
-    return few_items;
+    return few_items || gshape[g].na_inst * gshape[g].nb_inst >= 16;
   };
 
   size_t fpart_floats = 0;
@@ -387,7 +392,8 @@ dattri_status dattri::build_plan(const dattri_ctx* ctx, dattri_route forced, Pla
     // slab width: about kSplitTargetItems stage-1 workgroups in total
     int64_t work = 0;
     for (size_t o = op0; o < P.sops.size(); ++o)
-      work += (int64_t)((P.sops[o].rows + kSplitRows - 1) / kSplitRows) * P.sops[o].ld;
+      work += (int64_t)((P.sops[o].rows + split_rows_of(split_nt_instance(P.sops[o].nt)) - 1) /
+                        split_rows_of(split_nt_instance(P.sops[o].nt))) * P.sops[o].ld;
     int64_t slab = (work + kSplitTargetItems - 1) / kSplitTargetItems;
     slab = std::max<int64_t>(kSplitSlabQuantum, (slab + kSplitSlabQuantum - 1) / kSplitSlabQuantum * kSplitSlabQuantum);
     size_t proj_floats = 0;
@@ -452,7 +458,8 @@ dattri_status dattri::build_plan(const dattri_ctx* ctx, dattri_route forced, Pla
         for (size_t o = op0; o < P.sops.size(); ++o) {
           const SplitOp& O = P.sops[o];
           if (O.aligned != al || split_nt_instance(O.nt) != nt) continue;
-          const int rblocks = (O.rows + kSplitRows - 1) / kSplitRows;
+          const int rows_wg = split_rows_of(nt);
+          const int rblocks = (O.rows + rows_wg - 1) / rows_wg;
           for (int rb = 0; rb < rblocks; ++rb)
             for (int sl = 0; sl < O.n_slabs; ++sl) P.sitems.push_back({(int)o, rb, sl, 0});
         }

@@ -8,7 +8,7 @@
 //
 //   stage 1  for every factor block X (a group's A, each member's B) viewed as
 //            n*T token rows: out[s][row][:] = X[row, slab s] P[slab s, :],
-//            float32, one workgroup per (block, 128-row block, slab);
+//            float32, one workgroup per (block, 256-row block, slab; 128 rows at 8 tiles);
 //   stage 2  per (layer, example, token chunk): Psi[c][r] = sum_t a~_t[c] g~_t[r]
 //            with a~_t = sum_s outA[s][t] and g~_t = sum_s outB[s][t], over
 //            the example's first T_i tokens (Eq. (4) allows T_i < T), written
@@ -23,22 +23,22 @@
 namespace dattri {
 using namespace dev;
 
-constexpr int kSplitRT = 2;  // 16-row tiles per wave (kSplitRows = 4 waves x 2 x 16)
-static_assert(kWaves * kSplitRT * 16 == kSplitRows, "row block");
 
 template <int ELT, bool AL, int NT>
 __global__ __launch_bounds__(256, 2) void split_project_kernel(const SplitItem* __restrict__ items,
                                                                const SplitOp* __restrict__ ops,
                                                                float* __restrict__ out) {
   constexpr int KR = 4 * (16 / ELT);  // rows of a packed k-block
-  constexpr int PD = AL ? (NT >= 8 ? 2 : 4) : 2;
+  constexpr int RT = split_rt_of(NT), ROWS = split_rows_of(NT);
+  static_assert(kWaves * RT * 16 == ROWS, "row block");
+  constexpr int PD = 2;  // measured: deeper prefetch does not pay with 4 row tiles
   __shared__ __align__(16) uint8_t pan[2][kPanel][NT][kFragBytes];
   const SplitItem it = items[blockIdx.x];
   const SplitOp& O = ops[it.op];
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int g = lane >> 4, m16 = lane & 15;
-  const int row0 = it.row_block * kSplitRows;
-  const int nrows = min(kSplitRows, O.rows - row0);
+  const int row0 = it.row_block * ROWS;
+  const int nrows = min(ROWS, O.rows - row0);
   const int col0 = it.slab * O.slab_cols;
   const int d = min(O.slab_cols, O.ld - col0);
   // descriptor over this row block, starting at the slab's first column
@@ -53,18 +53,18 @@ __global__ __launch_bounds__(256, 2) void split_project_kernel(const SplitItem* 
     P.stride[t] = (int64_t)O.ptile_nt[tt] * kFragBytes;
     P.base[t] = (const uint8_t*)O.ptile[tt] + (int64_t)O.ptile_local[tt] * kFragBytes + kb0 * P.stride[t];
   }
-  f32x4 acc[kSplitRT][NT];
+  f32x4 acc[RT][NT];
 #pragma unroll
-  for (int rt = 0; rt < kSplitRT; ++rt)
+  for (int rt = 0; rt < RT; ++rt)
 #pragma unroll
     for (int t = 0; t < NT; ++t) acc[rt][t] = f32x4{0.f, 0.f, 0.f, 0.f};
-  const int r_wave = wave * kSplitRT * 16;
-  project_rows<ELT, AL, kSplitRT, NT, NT, PD>(r, r_wave, nrows, d, O.ld, P, acc, pan);
+  const int r_wave = wave * RT * 16;
+  project_rows<ELT, AL, RT, NT, NT, PD>(r, r_wave, nrows, d, O.ld, P, acc, pan);
 
   const int ldo = O.nt * 16;
   float* dst = out + O.out_base + ((int64_t)it.slab * O.rows + row0) * ldo;
 #pragma unroll
-  for (int rt = 0; rt < kSplitRT; ++rt)
+  for (int rt = 0; rt < RT; ++rt)
 #pragma unroll
     for (int t = 0; t < NT; ++t) {
       if (t < O.nt) {

@@ -34,7 +34,7 @@ def parse():
     p.add_argument("--warmup", type=int, default=2)
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--phase", choices=["all", "project", "score", "routing", "gpt2", "crossgram", "curvature",
-                                       "copy"],
+                                       "fit", "copy"],
                    default="all")
     return p.parse_args()
 
@@ -45,6 +45,8 @@ KERNEL_SOURCES = {
     "projection": ["factored.hip", "project_rows.h", "reduce.hip", "device_common.h", "internal.h",
                    "runtime.cpp"],
     "score_gemm": ["score_big.hip", "device_common.h"],
+    "projection_fit": ["split.hip", "project_rows.h", "reduce.hip", "kfac.hip", "kfac_api.cpp", "device_common.h",
+                       "internal.h", "plan.h", "runtime.cpp"],
 }
 HERE = os.path.dirname(os.path.abspath(__file__))
 
@@ -410,6 +412,48 @@ def curvature_case(dev, steps, warmup):
     return out
 
 
+def fit_case(dev, steps, warmup):
+    """One batch of the curvature workload (32 sequences x 196 Qwen2.5-7B-shaped
+    layers, T = 512, k = 64): projected gradients and factor sums in one pass
+    (dattri_project_and_fit), `steps` times after `warmup`.  The roofline
+    counts the algorithmic bytes of the projection (each distinct input block
+    once, every output-gradient block once)."""
+    import torch
+    import workloads as W
+    from paper_2609_38767_amd.session import Curvature, ProjectionSession, feature_rows
+    stream = torch.cuda.current_stream()
+    wl = W.WORKLOADS["curvature"]
+    layers, n, T = wl["layers"], wl["batch"], wl["T"]
+    sess = ProjectionSession(layers, dtype="bf16", seed=wl["seed"], device=dev)
+    cache = {}
+    for li in range(len(layers)):
+        A, B = W.factor_blocks(wl, li, 0, n, T, dev, "bf16", a_cache=cache)
+        sess.capture(li, A, B)
+    phi = feature_rows(n, sess.F, "f32", dev)
+    curv = Curvature(sess)
+    for _ in range(warmup):
+        curv.project_and_fit(n, phi=phi)
+    evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(steps)]
+    torch.cuda.synchronize()
+    for a, b in evs:
+        a.record(stream)
+        curv.project_and_fit(n, phi=phi)
+        b.record(stream)
+    torch.cuda.synchronize()
+    ms = [a.elapsed_time(b) for a, b in evs]
+    avg = sum(ms) / len(ms)
+    bytes_batch = algorithmic_projection_bytes(wl) * n
+    sess.close()
+    del cache, curv, phi
+    torch.cuda.empty_cache()
+    return {"ms_per_batch": avg, "ms_median": sorted(ms)[len(ms) // 2],
+            "roofline": {"bound": "hbm", "achieved": bytes_batch / (avg * 1e-3) / 1e9, "peak": 8000.0,
+                         "unit": "GB/s", "frac": bytes_batch / (avg * 1e-3) / 1e9 / 8000.0,
+                         "traffic": measured_traffic("projection_fit"),
+                         "kernel": "projection with factor sums (split form stage 1 + contraction + row sums), "
+                                   "one batch of 32 x 196 layers, T=512, k=64"}}
+
+
 def stream_reference(dev):
     """Achievable HBM rate on this GPU: a 1 GiB device-to-device copy (read +
     write bytes per second, best of 5)."""
@@ -557,6 +601,8 @@ def main():
         out["crossgram_routing"] = crossgram_case(dev, max(min(args.steps, 5), 3), min(args.warmup, 1))
     if args.phase in ("all", "curvature"):
         out["curvature"] = curvature_case(dev, max(min(args.steps, 5), 3), min(args.warmup, 1))
+    if args.phase in ("all", "fit"):
+        out["projection_fit"] = fit_case(dev, args.steps, args.warmup)
     if args.phase in ("all", "score"):
         for _ in range(args.warmup):
             score_step(False)

@@ -29,6 +29,7 @@ import workloads as W
 from gpu_util import host64, oracle_maps, rel_fro
 from oracle import gradients as og
 from oracle import kfac as ok
+from oracle import rng as orng
 from paper_2609_38767_amd.session import Curvature, ProjectionSession, feature_rows, score
 
 pytestmark = pytest.mark.gpu
@@ -398,3 +399,60 @@ def test_end_to_end_kfac_seeded_maps(dtype):
     float32 error of the sums: 1e-4 for float32 captures."""
     print(f"[curvature] end to end seeded maps dtype={dtype}", flush=True)
     _end_to_end(dtype, E2E_LAYERS, 52, None, ("kfac",), 1e-4 if dtype == "f32" else 2e-2)
+
+
+def test_curvature_full_size_sampled():
+    """The Qwen2.5-7B-shaped batch of the curvature benchmark (196 layers,
+    32 x 512 token rows, k = 64, bf16) through dattri_project_and_fit in the
+    launch configuration bench.py times, then the eigendecompositions and the
+    EK-FAC correction; sampled layers against the oracle:
+    * phi blocks of two examples and the factor sums and counts: 1e-5;
+    * eigenvalues (unique, unlike eigenvectors): 1e-4 of the largest;
+    * EK-FAC: the total of the corrected sums equals sum_i ||Psi_i||_F^2 (the
+      rotation keeps Frobenius norms; holds at any size): 1e-4;
+    * K-FAC preconditioned query block against the oracle's own fit: 1e-3 (a
+      smooth function of the factors, float32 sums)."""
+    wl = W.WORKLOADS["curvature"]
+    layers, n, T, seed = wl["layers"], wl["batch"], wl["T"], wl["seed"]
+    print("[curvature] full-size sampled: building inputs", flush=True)
+    cache, inputs = {}, []
+    s = ProjectionSession(layers, dtype="bf16", seed=seed)
+    for li in range(len(layers)):
+        A, B = W.factor_blocks(wl, li, 0, n, T, DEV, "bf16", a_cache=cache)
+        s.capture(li, A, B)
+        inputs.append((A, B))
+    c = Curvature(s)
+    phi = c.project_and_fit(n)
+    c.eigen()
+    c.accumulate_ekfac(phi)
+    rng = np.random.default_rng(11)
+    q = torch.from_numpy(rng.standard_normal((1, s.F))).to(torch.float32).to(DEV)
+    pq = c.precondition(q, "kfac")
+    torch.cuda.synchronize()
+    assert torch.isfinite(phi).all() and torch.isfinite(pq).all()
+    sampled = [0, 6, 7 * 27 + 4]  # q_proj and down_proj of block 0, gate_proj of block 27
+    for li in sampled:
+        L = layers[li]
+        print(f"[curvature] full-size sampled: layer {li} ({L['name']})", flush=True)
+        P_in, P_out = orng.projection_pair(seed, li, L["d_in"], L["d_out"], L["k_in"], L["k_out"], "bf16")
+        A, B = host64(inputs[li][0]), host64(inputs[li][1])
+        SA, SG, nt, ne = ok.factor_sums(A, B, P_in, P_out)
+        assert rel_fro(host64(c.field(li, "sum_a")), SA) <= 1e-5
+        assert rel_fro(host64(c.field(li, "sum_g")), SG) <= 1e-5
+        assert c.field(li, "counts").tolist() == [n * T, n, n]
+        off, w = s.offsets[li], L["k_in"] * L["k_out"]
+        psis = [og.project_factored(A[i], B[i], P_in, P_out) for i in range(n)]
+        for i in (0, n - 1):
+            assert rel_fro(host64(phi[i, off:off + w]), psis[i].reshape(-1)) <= 1e-5
+        C = ok.LayerCurvature(SA, SG, nt, ne)
+        for side, lam_o in (("a", C.lam_a), ("g", C.lam_g)):
+            lam = host64(c.field(li, "lam_" + side))
+            assert np.max(np.abs(lam - lam_o)) <= 1e-4 * np.max(np.abs(lam_o)), (li, side)
+        tot = float(host64(c.field(li, "sum_e")).sum())
+        want = sum(float(np.sum(P ** 2)) for P in psis)
+        assert abs(tot - want) <= 1e-4 * want, (li, tot, want)
+        Xq = host64(q[0, off:off + w]).reshape(L["k_in"], L["k_out"])
+        ref = C.precondition(Xq, "kfac")
+        e = rel_fro(host64(pq[0, off:off + w]).reshape(L["k_in"], L["k_out"]), ref)
+        print(f"  layer {li}: K-FAC preconditioned block rel err {e:.2e}")
+        assert e <= 1e-3, (li, e)

@@ -10,7 +10,9 @@ published algorithms:
   64-bit finalizer constants of Vigna's reference ``splitmix64.c``);
 * a counter-based stream with Philox4x32-10 (Salmon, Moraes, Dror & Shaw,
   "Parallel random numbers: as easy as 1, 2, 3", SC 2011);
-* normal deviates with the Box-Muller transform (Box & Muller, 1958).
+* normal deviates with the Box-Muller transform (Box & Muller, 1958);
+* Rademacher signs (Achlioptas, 2003, the map App. A.2 lists) from bit 31 of
+  the first Philox output word of the same counter.
 
 Definition (also implemented, independently, by the HIP library's host runtime):
 
@@ -121,6 +123,22 @@ def gaussian_map_f64(seed64, d, k):
     return (z / np.sqrt(float(k))).reshape(d, k)
 
 
+def rademacher_map_f64(seed64, d, k):
+    """Unrounded d x k Rademacher map with entries +-1/sqrt(k) (App. A.2
+    "Random maps", k the map's output dimension) from the same Philox stream
+    as the Gaussian map: element e = v*k + c takes the sign of bit 31 of the
+    first output word x0 (set: negative)."""
+    e = np.arange(d * k, dtype=np.uint64)
+    x0, _, _, _ = philox4x32_10(e & np.uint64(MASK32), e >> np.uint64(32),
+                                np.zeros_like(e), np.zeros_like(e),
+                                seed64 & MASK32, seed64 >> 32)
+    sign = np.where((x0 >> np.uint32(31)) != 0, -1.0, 1.0)
+    return (sign / np.sqrt(float(k))).reshape(d, k)
+
+
+MAPS = {"gaussian": gaussian_map_f64, "rademacher": rademacher_map_f64}
+
+
 def round_bf16_from_f32(x32):
     """float32 -> bfloat16 round-to-nearest-even, returned as float32 values."""
     bits = np.ascontiguousarray(x32, dtype=np.float32).view(np.uint32)
@@ -139,9 +157,11 @@ def round_to_dtype(x64, dtype):
     raise ValueError("dtype must be 'f32' or 'bf16'")
 
 
-def projection_pair(global_seed, layer, d_in, d_out, k_in, k_out, dtype):
+def projection_pair(global_seed, layer, d_in, d_out, k_in, k_out, dtype, kind="gaussian"):
     """(P_in [d_in, k_in], P_out [d_out, k_out]) as float64 arrays holding the
-    values the library stores for ``layer`` (registration index)."""
-    p_in = gaussian_map_f64(side_seed(global_seed, layer, 0), d_in, k_in)
-    p_out = gaussian_map_f64(side_seed(global_seed, layer, 1), d_out, k_out)
+    values the library stores for ``layer`` (registration index); ``kind`` is
+    "gaussian" or "rademacher"."""
+    gen = MAPS[kind]
+    p_in = gen(side_seed(global_seed, layer, 0), d_in, k_in)
+    p_out = gen(side_seed(global_seed, layer, 1), d_out, k_out)
     return round_to_dtype(p_in, dtype), round_to_dtype(p_out, dtype)

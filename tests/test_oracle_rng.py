@@ -104,3 +104,42 @@ def test_projection_pair_dtypes():
     # the two sides of a layer, and two layers, draw different maps
     q_in, _ = rng.projection_pair(0, 1, 64, 48, 8, 4, "f32")
     assert not np.allclose(p32_in, q_in)
+
+
+def test_rademacher_entries_and_signs():
+    # every entry is exactly +-1/sqrt(k); its sign is bit 31 of the first Philox
+    # word of its counter, checked against the scalar known-answer path
+    seed = rng.side_seed(3, 2, 1)
+    d, k = 37, 8
+    P = rng.rademacher_map_f64(seed, d, k)
+    assert np.all(np.abs(P) == 1.0 / np.sqrt(8.0))
+    for v, c in ((0, 0), (5, 3), (36, 7)):
+        e = v * k + c
+        x0 = rng.philox4x32_10(e & 0xFFFFFFFF, e >> 32, 0, 0, seed & 0xFFFFFFFF, seed >> 32)[0]
+        assert (P[v, c] < 0) == bool(int(x0) >> 31)
+    big = rng.rademacher_map_f64(rng.side_seed(7, 0, 0), 4096, 64)
+    frac = np.mean(big > 0)
+    assert abs(frac - 0.5) < 5 * 0.5 / np.sqrt(big.size)  # balanced signs (5 sigma)
+
+
+def test_rademacher_projection_unbiased():
+    # E[<P^T x, P^T y>] = <x, y> over maps (independent entries of variance 1/k)
+    gen = np.random.default_rng(0)
+    d, k = 40, 16
+    x, y = gen.standard_normal(d), gen.standard_normal(d)
+    vals = [float((rng.rademacher_map_f64(rng.side_seed(s, 0, 0), d, k).T @ x)
+                  @ (rng.rademacher_map_f64(rng.side_seed(s, 0, 0), d, k).T @ y)) for s in range(400)]
+    mean, sd = np.mean(vals), np.std(vals) / np.sqrt(len(vals))
+    assert abs(mean - float(x @ y)) < 5 * sd
+    # column norms are exactly d/k
+    P = rng.rademacher_map_f64(rng.side_seed(1, 0, 1), d, k)
+    assert np.allclose(np.sum(P * P, axis=0), d / k, rtol=0, atol=1e-12)
+
+
+def test_projection_pair_kinds():
+    g = rng.projection_pair(5, 1, 20, 12, 4, 8, "bf16")
+    r = rng.projection_pair(5, 1, 20, 12, 4, 8, "bf16", kind="rademacher")
+    assert np.all(np.abs(r[0]) == rng.round_to_dtype(np.array([0.5]), "bf16")[0])
+    assert np.all(np.sign(r[1]) != 0) and not np.allclose(g[1], r[1])
+    with pytest.raises(KeyError):
+        rng.projection_pair(5, 1, 20, 12, 4, 8, "bf16", kind="sparse")

@@ -1,5 +1,7 @@
 """Attribution scores from projected features, and per-query top-k (oracle side).
 
+Also the cosine variant (Grad-Cos; LESS's cosine metric) of the same scores.
+
 GradDot (Sec. 4.1; gradient similarity at one checkpoint, Sec. 2) scores a query
 against a training example by the inner product of their gradients.  With the
 per-layer blocks concatenated into phi, the score over all layers is
@@ -37,6 +39,37 @@ def score_loop(phi_q, phi_train, d=None):
             for f in range(F):
                 s += Q[q, f] * (1.0 if d is None else float(d[f])) * X[j, f]
             S[q, j] = s
+    return S
+
+
+def cosine_scores(phi_q, phi_train, d=None):
+    """Grad-Cos / LESS-style scores (Sec. 2 "Grad-Cos"; App. A.3, LESS as TracIn
+    with a cosine metric): the cosine between the (preconditioned) query row
+    q' = q * d and the training row x, <q', x> / (|q'| |x|), taken as 0 when
+    either norm is 0."""
+    Q = np.asarray(phi_q, dtype=np.float64)
+    X = np.asarray(phi_train, dtype=np.float64)
+    if d is not None:
+        Q = Q * np.asarray(d, dtype=np.float64)[None, :]
+    nq = np.linalg.norm(Q, axis=1)
+    nx = np.linalg.norm(X, axis=1)
+    iq = np.where(nq > 0, 1.0 / np.where(nq > 0, nq, 1.0), 0.0)
+    ix = np.where(nx > 0, 1.0 / np.where(nx > 0, nx, 1.0), 0.0)
+    return (Q @ X.T) * iq[:, None] * ix[None, :]
+
+
+def cosine_loop(phi_q, phi_train, d=None):
+    """The same cosines with explicit loops over rows and features (tiny only)."""
+    Q = np.asarray(phi_q, dtype=np.float64)
+    X = np.asarray(phi_train, dtype=np.float64)
+    S = np.zeros((Q.shape[0], X.shape[0]))
+    for q in range(Q.shape[0]):
+        qd = [Q[q, f] * (1.0 if d is None else float(d[f])) for f in range(Q.shape[1])]
+        nq = sum(v * v for v in qd) ** 0.5
+        for j in range(X.shape[0]):
+            nx = sum(v * v for v in X[j]) ** 0.5
+            dot = sum(a * b for a, b in zip(qd, X[j]))
+            S[q, j] = dot / (nq * nx) if nq > 0 and nx > 0 else 0.0
     return S
 
 

@@ -53,3 +53,27 @@ def test_topk_edges():
     S = np.array([[1.0, -0.0, 0.0, -1.0]])
     idx, _ = osc.topk(S, 3)
     assert idx.tolist() == [[0, 1, 2]]  # -0.0 and 0.0 compare equal
+
+
+def test_cosine_against_loops_and_invariants():
+    rng = np.random.default_rng(3)
+    Q = rng.standard_normal((3, 7))
+    X = rng.standard_normal((5, 7))
+    X[2] = 0.0  # a zero row scores 0
+    d = np.exp(rng.standard_normal(7))
+    for dd in (None, d):
+        S = osc.cosine_scores(Q, X, dd)
+        np.testing.assert_allclose(S, osc.cosine_loop(Q, X, dd), rtol=1e-12, atol=1e-15)
+        assert np.all(np.abs(S) <= 1 + 1e-12)  # Cauchy-Schwarz
+        assert np.all(S[:, 2] == 0)
+        # invariant to positive row scalings of either side
+        S2 = osc.cosine_scores(Q * np.array([[2.0], [0.5], [7.0]]), X * 3.0, dd)
+        np.testing.assert_allclose(S2, S, rtol=1e-12, atol=1e-15)
+    # identical rows have cosine 1; opposite rows -1; with d, the preconditioned query matters
+    np.testing.assert_allclose(osc.cosine_scores(X[:2], X[:2]).diagonal(), 1.0, rtol=1e-14)
+    np.testing.assert_allclose(osc.cosine_scores(X[:2], -X[:2]).diagonal(), -1.0, rtol=1e-14)
+    np.testing.assert_allclose(osc.cosine_scores(Q / d, Q * 1.0, d).diagonal(), 1.0, rtol=1e-13)
+    # the dot-product scores divided by the two norms
+    S = osc.cosine_scores(Q, X[:2], d)
+    ref = osc.score(Q, X[:2], d) / np.linalg.norm(Q * d, axis=1)[:, None] / np.linalg.norm(X[:2], axis=1)[None, :]
+    np.testing.assert_allclose(S, ref, rtol=1e-12)

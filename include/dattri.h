@@ -159,6 +159,18 @@ dattri_status dattri_bind_projection(dattri_ctx* ctx, int32_t layer, void* dev_P
                                      void* dev_P_out, const float* host_P_in_override,
                                      const float* host_P_out_override, void* stream);
 
+/* Kind of a layer's seeded maps (App. A.2 "Random maps"): Gaussian entries
+ * N(0, 1/k) (the default, drawn as described above) or Rademacher entries
+ * +-1/sqrt(k), k the map's output dimension, with the sign of element
+ * e = v*k + c taken from bit 31 of the first output word x0 of the same
+ * Philox4x32-10 counter and key (set: negative).  Both sides of the layer use
+ * the kind.  Changing the kind of a bound layer unbinds it (bind again before
+ * projecting); overrides given at binding are unaffected by the kind.
+ * Errors: INVALID_ARG (bad layer, unknown kind, NULL kind). */
+typedef enum { DATTRI_MAP_GAUSSIAN = 0, DATTRI_MAP_RADEMACHER = 1 } dattri_map_kind;
+dattri_status dattri_set_map_kind(dattri_ctx* ctx, int32_t layer, dattri_map_kind kind);
+dattri_status dattri_get_map_kind(const dattri_ctx* ctx, int32_t layer, dattri_map_kind* kind);
+
 /* Host copy of the maps the layer uses, after rounding to the compute type:
  * the seeded maps (whether or not bound yet) or the overrides given at
  * binding; float32 row-major [d_in x k_in] and [d_out x k_out].  Either
@@ -402,6 +414,23 @@ dattri_status dattri_score(const void* phi_q, int64_t n_q, int64_t ld_q, const v
                            const float* dev_precond_diag, float* scores, int32_t topk,
                            int32_t* topk_idx, float* topk_val, void* workspace, size_t ws_bytes,
                            void* stream);
+
+/* Cosine scores (Grad-Cos, Sec. 2; LESS's cosine metric, App. A.3): the same
+ * call as dattri_score, with every score divided by the norms of its two rows,
+ *   S[q][j] = <q', x_j> / (|q'| |x_j|),  q' = phi_q[q] * d (d = 1 when NULL),
+ * and 0 when either norm is 0; top-k ranks these cosines.  Norms are float32
+ * sums of squares of the rows as given (the query scaled by d in float32).
+ *   workspace: >= dattri_cosine_workspace_bytes(...) (dattri_score's plus
+ *   n_q + n_train floats), 256-byte aligned.
+ * Errors: as dattri_score. */
+dattri_status dattri_cosine_workspace_bytes(int64_t n_q, int64_t n_train, int64_t F,
+                                            dattri_dtype dtype, int32_t has_precond,
+                                            int32_t has_scores, int32_t topk, size_t* bytes);
+dattri_status dattri_score_cosine(const void* phi_q, int64_t n_q, int64_t ld_q,
+                                  const void* phi_train, int64_t n_train, int64_t ld_train,
+                                  int64_t F, dattri_dtype dtype, const float* dev_precond_diag,
+                                  float* scores, int32_t topk, int32_t* topk_idx, float* topk_val,
+                                  void* workspace, size_t ws_bytes, void* stream);
 
 /* ------------------------------------------------ K-FAC / EK-FAC curvature */
 

@@ -32,12 +32,15 @@ __all__ = [
     "dattri_curvature_eigen", "dattri_curvature_ekfac_workspace_bytes",
     "dattri_curvature_accumulate_ekfac", "dattri_curvature_precondition",
     "dattri_project_fit_workspace_bytes", "dattri_project_and_fit",
+    "DATTRI_MAP_GAUSSIAN", "DATTRI_MAP_RADEMACHER", "dattri_set_map_kind", "dattri_get_map_kind",
+    "dattri_cosine_workspace_bytes", "dattri_score_cosine",
 ]
 
 DATTRI_F32, DATTRI_BF16 = 0, 1
 DATTRI_ROUTE_AUTO, DATTRI_ROUTE_FACTORED, DATTRI_ROUTE_MATERIALIZED = 0, 1, 2
 DATTRI_FORM_AUTO, DATTRI_FORM_FUSED, DATTRI_FORM_SPLIT = 0, 1, 2
 DATTRI_CURV_KFAC, DATTRI_CURV_EKFAC = 0, 1
+DATTRI_MAP_GAUSSIAN, DATTRI_MAP_RADEMACHER = 0, 1
 STATUS_NAMES = {0: "OK", -1: "E_INVALID_ARG", -2: "E_SHAPE", -3: "E_DTYPE", -4: "E_STATE",
                 -5: "E_WORKSPACE", -6: "E_HIP", -7: "E_UNSUPPORTED"}
 
@@ -120,6 +123,11 @@ _SIGS = {
     "dattri_curvature_ekfac_workspace_bytes": (_i32, [_vp, _i64, _P(_sz)]),
     "dattri_curvature_accumulate_ekfac": (_i32, [_vp, _vp, _vp, _i32, _i64, _i64, _vp, _sz, _vp]),
     "dattri_project_fit_workspace_bytes": (_i32, [_vp, _i32, _P(_sz)]),
+    "dattri_set_map_kind": (_i32, [_vp, _i32, _i32]),
+    "dattri_cosine_workspace_bytes": (_i32, [_i64, _i64, _i64, _i32, _i32, _i32, _i32, _P(_sz)]),
+    "dattri_score_cosine": (_i32, [_vp, _i64, _i64, _vp, _i64, _i64, _i64, _i32, _vp, _vp, _i32, _vp, _vp,
+                                   _vp, _sz, _vp]),
+    "dattri_get_map_kind": (_i32, [_vp, _i32, _P(_i32)]),
     "dattri_project_and_fit": (_i32, [_vp, _vp, _i32, _i64, _vp, _vp, _sz, _i32, _vp]),
     "dattri_curvature_precondition": (_i32, [_vp, _vp, _i32, _dbl, _dbl, _vp, _i32, _i64, _i64, _vp, _i32,
                                              _i64, _vp]),
@@ -440,3 +448,29 @@ def dattri_project_and_fit(ctx, phi, phi_dtype, ld_phi, state, workspace, ws_byt
     _check(load().dattri_project_and_fit(ctx, _ptr(phi), phi_dtype, ld_phi, _ptr(state), _ptr(workspace), ws_bytes,
                                          route, _stream(stream)),
            "dattri_project_and_fit")
+
+
+def dattri_set_map_kind(ctx, layer, kind):
+    _check(load().dattri_set_map_kind(ctx, layer, kind), "dattri_set_map_kind")
+
+
+def dattri_get_map_kind(ctx, layer):
+    v = _i32()
+    _check(load().dattri_get_map_kind(ctx, layer, ctypes.byref(v)), "dattri_get_map_kind")
+    return v.value
+
+
+def dattri_cosine_workspace_bytes(n_q, n_train, F, dtype, has_precond, has_scores, topk):
+    v = _sz()
+    _check(load().dattri_cosine_workspace_bytes(n_q, n_train, F, dtype, int(bool(has_precond)),
+                                                int(bool(has_scores)), topk, ctypes.byref(v)),
+           "dattri_cosine_workspace_bytes")
+    return v.value
+
+
+def dattri_score_cosine(phi_q, n_q, ld_q, phi_train, n_train, ld_train, F, dtype, dev_precond_diag, scores,
+                        topk, topk_idx, topk_val, workspace, ws_bytes, stream=None):
+    _check(load().dattri_score_cosine(_ptr(phi_q), n_q, ld_q, _ptr(phi_train), n_train, ld_train, F, dtype,
+                                      _ptr(dev_precond_diag), _ptr(scores), topk, _ptr(topk_idx), _ptr(topk_val),
+                                      _ptr(workspace), ws_bytes, _stream(stream)),
+           "dattri_score_cosine")

@@ -17,6 +17,7 @@ struct Layer {
   void* P_in = nullptr;
   void* P_out = nullptr;
   bool bound = false;
+  int32_t map_kind = 0;  // dattri_map_kind of the seeded maps
   std::vector<float> override_in, override_out;  // rounded values when overridden
   const void* A = nullptr;  // captured [n, T, d_in]
   const void* B = nullptr;  // captured [n, T, d_out]

@@ -235,6 +235,11 @@ inline int64_t score_partial_floats(int elt_bytes, int64_t n_q, int64_t n_train,
 hipError_t launch_score_gemm_256(const void* Q, int64_t ldq, const float* d, const void* X,
                                  int64_t ldx, float* S, int64_t n_q, int64_t n_train, int64_t F,
                                  void* qpack, float* partials, hipStream_t s);
+// Cosine scores: inv_q / inv_t receive 1 / row norms (queries times d when
+// given; 0 for zero rows), then S[q][j] *= inv_q[q] * inv_t[j].
+hipError_t launch_cosine_scale(int elt_bytes, const void* Q, int64_t ldq, const float* d, const void* X,
+                               int64_t ldx, float* S, int64_t n_q, int64_t n_train, int64_t F, float* inv_q,
+                               float* inv_t, hipStream_t s);
 constexpr int kTopkMax = 1024;
 hipError_t launch_topk(const float* S, int64_t n_q, int64_t n_train, int32_t k, int32_t* idx,
                        float* val, hipStream_t s);

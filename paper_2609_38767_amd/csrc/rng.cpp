@@ -60,6 +60,12 @@ double gaussian_entry(uint64_t seed64, uint64_t e) {
   return std::sqrt(-2.0 * std::log(u1)) * std::cos(2.0 * M_PI * u2);
 }
 
+double rademacher_entry(uint64_t seed64, uint64_t e) {
+  uint32_t c[4] = {(uint32_t)e, (uint32_t)(e >> 32), 0u, 0u};
+  philox10(c, (uint32_t)seed64, (uint32_t)(seed64 >> 32));
+  return (c[0] >> 31) ? -1.0 : 1.0;
+}
+
 uint16_t f32_to_bf16_rne(float f) {
   uint32_t u;
   std::memcpy(&u, &f, 4);
@@ -79,8 +85,9 @@ float round_to_compute(double x, int elt_bytes) {
   return elt_bytes == 2 ? bf16_to_f32(f32_to_bf16_rne(f)) : f;
 }
 
-// Fill `logical` (d x k float32, row-major) with the rounded map values.
-void seeded_map(uint64_t seed64, int d, int k, int elt_bytes, float* logical) {
+// Fill `logical` (d x k float32, row-major) with the rounded map values:
+// kind 0 Gaussian N(0, 1/k), kind 1 Rademacher +-1/sqrt(k).
+void seeded_map(uint64_t seed64, int d, int k, int elt_bytes, int kind, float* logical) {
   const int64_t total = (int64_t)d * k;
   const double scale = 1.0 / std::sqrt((double)k);
   unsigned hw = std::thread::hardware_concurrency();
@@ -89,7 +96,9 @@ void seeded_map(uint64_t seed64, int d, int k, int elt_bytes, float* logical) {
   auto work = [&](int t) {
     const int64_t b = total * t / nth, e = total * (t + 1) / nth;
     for (int64_t i = b; i < e; ++i)
-      logical[i] = round_to_compute(gaussian_entry(seed64, (uint64_t)i) * scale, elt_bytes);
+      logical[i] = round_to_compute(
+          (kind == 1 ? rademacher_entry(seed64, (uint64_t)i) : gaussian_entry(seed64, (uint64_t)i)) * scale,
+          elt_bytes);
   };
   if (nth == 1) { work(0); return; }
   std::vector<std::thread> th;

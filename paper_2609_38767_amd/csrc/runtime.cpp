@@ -571,7 +571,7 @@ void logical_map(const dattri_ctx* ctx, int layer, int side, std::vector<float>&
   const std::vector<float>& ov = side ? L.override_out : L.override_in;
   if (!ov.empty()) { out = ov; return; }
   out.resize((size_t)d * k);
-  seeded_map(derive_side_seed(ctx->seed, layer, side), d, k, ctx->elt, out.data());
+  seeded_map(derive_side_seed(ctx->seed, layer, side), d, k, ctx->elt, L.map_kind, out.data());
 }
 
 }  // namespace
@@ -788,6 +788,29 @@ dattri_status dattri_bind_projection(dattri_ctx* ctx, int32_t layer, void* dev_P
   L.P_in = dev_P_in;
   L.P_out = dev_P_out;
   L.bound = true;
+  return DATTRI_OK;
+}
+
+dattri_status dattri_set_map_kind(dattri_ctx* ctx, int32_t layer, dattri_map_kind kind) {
+  reset_error();
+  dattri_status st = check_layer(ctx, layer);
+  if (st != DATTRI_OK) return st;
+  if (kind != DATTRI_MAP_GAUSSIAN && kind != DATTRI_MAP_RADEMACHER)
+    return fail(DATTRI_E_INVALID_ARG, "map kind %d unknown", (int)kind);
+  Layer& L = ctx->layers[layer];
+  if (L.map_kind != kind) {
+    L.map_kind = kind;
+    L.bound = false;  // the bound maps are of the other kind: bind again
+  }
+  return DATTRI_OK;
+}
+
+dattri_status dattri_get_map_kind(const dattri_ctx* ctx, int32_t layer, dattri_map_kind* kind) {
+  reset_error();
+  dattri_status st = check_layer(ctx, layer);
+  if (st != DATTRI_OK) return st;
+  if (!kind) return fail(DATTRI_E_INVALID_ARG, "kind is NULL");
+  *kind = (dattri_map_kind)ctx->layers[layer].map_kind;
   return DATTRI_OK;
 }
 

@@ -10,10 +10,11 @@ namespace dattri {
 uint64_t derive_side_seed(uint64_t global_seed, int layer, int side);
 void philox4x32_10(const uint32_t ctr[4], const uint32_t key[2], uint32_t out[4]);
 double gaussian_entry(uint64_t seed64, uint64_t e);
+double rademacher_entry(uint64_t seed64, uint64_t e);  // +-1
 uint16_t f32_to_bf16_rne(float f);
 float bf16_to_f32(uint16_t h);
 float round_to_compute(double x, int elt_bytes);
-void seeded_map(uint64_t seed64, int d, int k, int elt_bytes, float* logical);
+void seeded_map(uint64_t seed64, int d, int k, int elt_bytes, int kind, float* logical);
 void pack_map(const float* logical, int d, int k, int elt_bytes, std::vector<uint8_t>& packed);
 
 }  // namespace dattri

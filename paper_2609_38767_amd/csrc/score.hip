@@ -137,6 +137,81 @@ __global__ __launch_bounds__(256) void score_gemm_kernel(const uint8_t* __restri
     }
 }
 
+// ------------------------------------------------------ cosine normalization
+// inv[r] = 1 / |row r (times d, when given)|, 0 for a zero row.  One wave per
+// row, 16-byte loads (rows are 16-byte aligned and F a multiple of 16 bytes).
+template <int ELT>
+__global__ __launch_bounds__(256) void row_inv_norms_kernel(const uint8_t* __restrict__ X, int64_t ld,
+                                                            int64_t rows, int64_t F,
+                                                            const float* __restrict__ d,
+                                                            float* __restrict__ inv) {
+  constexpr int EPL = 16 / ELT;
+  const int lane = threadIdx.x & 63;
+  const int64_t r = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (r >= rows) return;  // the whole wave leaves; no barrier below
+  const uint8_t* row = X + r * ld * ELT;
+  float s = 0.f;
+  for (int64_t f = (int64_t)lane * EPL; f < F; f += 64 * EPL) {
+    // elements named explicitly: bit-casting single vector elements inside an
+    // unrolled loop was compiled to read element 0 for every index
+    const i32x4 v = *(const i32x4*)(row + f * ELT);
+    float x[EPL];
+    if constexpr (ELT == 2) {
+      const uint32_t w0 = (uint32_t)v.x, w1 = (uint32_t)v.y, w2 = (uint32_t)v.z, w3 = (uint32_t)v.w;
+      x[0] = bf16_bits_to_f32(w0 & 0xFFFFu); x[1] = bf16_bits_to_f32(w0 >> 16);
+      x[2] = bf16_bits_to_f32(w1 & 0xFFFFu); x[3] = bf16_bits_to_f32(w1 >> 16);
+      x[4] = bf16_bits_to_f32(w2 & 0xFFFFu); x[5] = bf16_bits_to_f32(w2 >> 16);
+      x[6] = bf16_bits_to_f32(w3 & 0xFFFFu); x[7] = bf16_bits_to_f32(w3 >> 16);
+    } else {
+      const f32x4 fv = __builtin_bit_cast(f32x4, v);
+      x[0] = fv.x; x[1] = fv.y; x[2] = fv.z; x[3] = fv.w;
+    }
+#pragma unroll
+    for (int j = 0; j < EPL; ++j) {
+      const float y = d ? x[j] * d[f + j] : x[j];
+      s = fmaf(y, y, s);
+    }
+  }
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) s += __shfl_xor(s, o, 64);
+  if (lane == 0) inv[r] = s > 0.f ? 1.f / sqrtf(s) : 0.f;
+}
+
+// S[q][j] *= iq[q] * it[j] (rows of S dense, n_train apart).
+__global__ __launch_bounds__(256) void scale_scores_kernel(float* __restrict__ S, int64_t n_q, int64_t n_train,
+                                                           const float* __restrict__ iq,
+                                                           const float* __restrict__ it) {
+  for (int64_t q = blockIdx.x; q < n_q; q += gridDim.x) {
+    const float a = iq[q];
+    float* row = S + q * n_train;
+    for (int64_t j = threadIdx.x; j < n_train; j += 256) row[j] *= a * it[j];
+  }
+}
+
+hipError_t launch_cosine_scale(int elt, const void* Q, int64_t ldq, const float* d, const void* X, int64_t ldx,
+                               float* S, int64_t n_q, int64_t n_train, int64_t F, float* inv_q, float* inv_t,
+                               hipStream_t s) {
+  if (n_q <= 0 || n_train <= 0) return hipSuccess;
+  const int64_t bq = (n_q + 3) / 4, bt = (n_train + 3) / 4;
+  if (bq > INT32_MAX || bt > INT32_MAX) return hipErrorInvalidValue;
+  if (elt == 2) {
+    hipLaunchKernelGGL(row_inv_norms_kernel<2>, dim3((unsigned)bq), dim3(256), 0, s, (const uint8_t*)Q, ldq, n_q,
+                       F, d, inv_q);
+    hipLaunchKernelGGL(row_inv_norms_kernel<2>, dim3((unsigned)bt), dim3(256), 0, s, (const uint8_t*)X, ldx,
+                       n_train, F, nullptr, inv_t);
+  } else {
+    hipLaunchKernelGGL(row_inv_norms_kernel<4>, dim3((unsigned)bq), dim3(256), 0, s, (const uint8_t*)Q, ldq, n_q,
+                       F, d, inv_q);
+    hipLaunchKernelGGL(row_inv_norms_kernel<4>, dim3((unsigned)bt), dim3(256), 0, s, (const uint8_t*)X, ldx,
+                       n_train, F, nullptr, inv_t);
+  }
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  const unsigned blocks = (unsigned)std::min<int64_t>(n_q, 4096);
+  hipLaunchKernelGGL(scale_scores_kernel, dim3(blocks), dim3(256), 0, s, S, n_q, n_train, inv_q, inv_t);
+  return hipGetLastError();
+}
+
 hipError_t launch_scale_rows(int elt, const void* src, int64_t ld_src, const float* d, void* dst,
                              int64_t ld_dst, int64_t rows, int64_t F, hipStream_t s) {
   const int64_t n = rows * F;

@@ -21,7 +21,8 @@ from . import (DATTRI_BF16, DATTRI_F32, DATTRI_ROUTE_AUTO, dattri_bind_projectio
                dattri_curvature_fit_workspace_bytes, dattri_curvature_accumulate_factors,
                dattri_curvature_eigen, dattri_curvature_ekfac_workspace_bytes,
                dattri_curvature_accumulate_ekfac, dattri_curvature_precondition,
-               dattri_project_fit_workspace_bytes, dattri_project_and_fit)
+               dattri_project_fit_workspace_bytes, dattri_project_and_fit, dattri_set_map_kind,
+               dattri_cosine_workspace_bytes, dattri_score_cosine)
 
 DTYPES = {"f32": (DATTRI_F32, torch.float32), "bf16": (DATTRI_BF16, torch.bfloat16)}
 
@@ -33,7 +34,7 @@ def _dev_bytes(n, device):
 class ProjectionSession:
     """One library context with its layers and bound projection maps."""
 
-    def __init__(self, layers, dtype="bf16", seed=0, device="cuda", overrides=None, form=None):
+    def __init__(self, layers, dtype="bf16", seed=0, device="cuda", overrides=None, form=None, map_kind=None):
         self.dtype = dtype
         self.code, self.torch_dtype = DTYPES[dtype]
         self.device = torch.device(device)
@@ -46,6 +47,8 @@ class ProjectionSession:
         for i, L in enumerate(self.layers):
             lid = dattri_register_layer(self.ctx, L["d_in"], L["d_out"], L["k_in"], L["k_out"])
             assert lid == i
+            if map_kind is not None:
+                dattri_set_map_kind(self.ctx, lid, map_kind)
             b_in, b_out = dattri_projection_bytes(self.ctx, lid)
             p_in, p_out = _dev_bytes(b_in, self.device), _dev_bytes(b_out, self.device)
             o_in, o_out = overrides.get(i, (None, None))
@@ -106,9 +109,10 @@ def feature_rows(n, F, dtype="bf16", device="cuda"):
     return torch.empty((n, ld), dtype=tdt, device=device)[:, :F]
 
 
-def score(phi_q, phi_train, precond=None, topk=0, want_scores=True, stream=None):
+def score(phi_q, phi_train, precond=None, topk=0, want_scores=True, stream=None, cosine=False):
     """(S or None, topk_idx or None, topk_val or None) for bf16/f32 feature
-    rows; each operand may be row-strided (unit stride along features)."""
+    rows; each operand may be row-strided (unit stride along features).
+    cosine=True divides every score by the norms of its two rows."""
     code = DATTRI_BF16 if phi_q.dtype == torch.bfloat16 else DATTRI_F32
     n_q, F = phi_q.shape
     n_train = phi_train.shape[0]
@@ -119,10 +123,12 @@ def score(phi_q, phi_train, precond=None, topk=0, want_scores=True, stream=None)
     S = torch.empty((n_q, n_train), dtype=torch.float32, device=dev) if want_scores else None
     idx = torch.empty((n_q, topk), dtype=torch.int32, device=dev) if topk else None
     val = torch.empty((n_q, topk), dtype=torch.float32, device=dev) if topk else None
-    need = dattri_score_workspace_bytes(n_q, n_train, F, code, precond is not None, want_scores, topk)
+    sizer, fn = ((dattri_cosine_workspace_bytes, dattri_score_cosine) if cosine
+                 else (dattri_score_workspace_bytes, dattri_score))
+    need = sizer(n_q, n_train, F, code, precond is not None, want_scores, topk)
     ws = _dev_bytes(need, dev)
-    dattri_score(phi_q, n_q, phi_q.stride(0), phi_train, n_train, phi_train.stride(0), F, code, precond,
-                 S, topk, idx, val, ws, ws.numel(), stream)
+    fn(phi_q, n_q, phi_q.stride(0), phi_train, n_train, phi_train.stride(0), F, code, precond,
+       S, topk, idx, val, ws, ws.numel(), stream)
     return S, idx, val
 
 

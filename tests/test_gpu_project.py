@@ -11,6 +11,7 @@ import paper_2609_38767_amd as dt
 import workloads as W
 from gpu_util import host64, oracle_maps, oracle_phi_rows, per_layer_errors, rel_fro
 from oracle import gradients as og
+from oracle import rng as orng
 from paper_2609_38767_amd.session import ProjectionSession
 
 pytestmark = pytest.mark.gpu
@@ -110,6 +111,32 @@ def test_fused_64_wide_maps(dtype):
     lengths = torch.tensor([700, 513, 128, 1], dtype=torch.int32, device=DEV)
     _, phi = _run(layers, inputs, dtype, 19, "factored", lengths=lengths, form="fused")
     _check(layers, inputs, phi, 19, dtype, [0, 1, 2, 3], lengths=lengths, tol=1e-5)
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("route,form", [("factored", "fused"), ("factored", "split"), ("materialized", None)])
+def test_rademacher_maps(dtype, route, form):
+    # App. A.2 "Random maps": +-1/sqrt(k) entries from the same per-layer seeds
+    layers = RAGGED
+    wl = dict(W.WORKLOADS["tiny"], dist_a="normal", dist_b="normal", seed=23)
+    n, T = 4, 41
+    inputs = _session_inputs(wl, layers, n, T, dtype)
+    s = ProjectionSession(layers, dtype=dtype, seed=29, form=FORMS[form], map_kind=dt.DATTRI_MAP_RADEMACHER)
+    for li, (A, B) in enumerate(inputs):
+        s.capture(li, A, B)
+    phi = s.project(n, route=ROUTES[route])
+    torch.cuda.synchronize()
+    maps = [orng.projection_pair(29, i, L["d_in"], L["d_out"], L["k_in"], L["k_out"], dtype, kind="rademacher")
+            for i, L in enumerate(layers)]
+    host = [(host64(A), host64(B)) for A, B in inputs]
+    ref = oracle_phi_rows(layers, maps, host, list(range(n)))
+    errs = per_layer_errors(host64(phi), ref, layers)
+    assert max(errs) <= 1e-5, errs
+    # switching a bound layer's kind unbinds it
+    dt.dattri_set_map_kind(s.ctx, 0, dt.DATTRI_MAP_GAUSSIAN)
+    with pytest.raises(dt.DattriError) as e:
+        s.project(n, route=ROUTES[route])
+    assert e.value.status_name == "E_STATE"
 
 
 @pytest.mark.parametrize("form", ["fused", "split"])

@@ -72,6 +72,35 @@ def test_score_few_tiles_split_features(dtype, shape, precond):
     _check_topk(host64(S), ref, idx.cpu().numpy(), val.cpu().numpy(), 5)
 
 
+@pytest.mark.parametrize("dtype", [torch.float32, torch.bfloat16])
+@pytest.mark.parametrize("shape", [(37, 301, 104), (300, 5000, 520), (1, 512, 30000)])
+@pytest.mark.parametrize("precond", [False, True])
+def test_score_cosine(dtype, shape, precond):
+    # Grad-Cos / LESS cosine: scores divided by both row norms; a zero training
+    # row scores 0; both GEMM kernels (the middle shape takes the 256 x 256 one
+    # in bf16), row strides and top-k
+    n_q, n_t, F = shape
+    g = torch.Generator(device=DEV).manual_seed(17)
+    ld = dattri_feature_ld(F, DATTRI_BF16 if dtype == torch.bfloat16 else 0)
+    Q = torch.randn((n_q, F), generator=g, device=DEV) * torch.rand((n_q, 1), generator=g, device=DEV) * 5
+    X = torch.randn((n_t, F), generator=g, device=DEV) * torch.rand((n_t, 1), generator=g, device=DEV) * 5
+    X[min(3, n_t - 1)] = 0.0
+    Q, X = W.strided_copy(Q.to(dtype), ld), W.strided_copy(X.to(dtype), ld)
+    d = torch.exp(torch.randn(F, generator=g, device=DEV)) if precond else None
+    S, idx, val = score(Q, X, d, topk=5, cosine=True)
+    torch.cuda.synchronize()
+    ref = osc.cosine_scores(host64(Q), host64(X), None if d is None else host64(d))
+    tol = 1e-5 if (dtype == torch.float32 or not precond) else TOL[dtype]
+    assert rel_fro(host64(S), ref) <= tol
+    assert np.all(host64(S)[:, min(3, n_t - 1)] == 0.0)
+    assert np.max(np.abs(host64(S))) <= 1.0 + 1e-5
+    _check_topk(host64(S), ref, idx.cpu().numpy(), val.cpu().numpy(), 5)
+    # top-k alone (scores kept in the workspace) ranks the same cosines
+    _, idx2, val2 = score(Q, X, d, topk=5, want_scores=False, cosine=True)
+    torch.cuda.synchronize()
+    assert torch.equal(idx, idx2) and torch.equal(val, val2)
+
+
 @pytest.mark.parametrize("shape", [(300, 5000, 104), (256, 4096, 8192), (513, 777, 40)])
 def test_score_large_tile_kernel_ragged(shape):
     # n_q * n_train >= 2^20 routes bf16 to the 256 x 256 kernel: ragged query

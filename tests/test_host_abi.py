@@ -202,6 +202,29 @@ def test_host_generator_matches_oracle(dtype_name, dtype):
     dt.dattri_destroy(c)
 
 
+@pytest.mark.parametrize("dtype_name,dtype", [("f32", dt.DATTRI_F32), ("bf16", dt.DATTRI_BF16)])
+def test_rademacher_maps_match_oracle(dtype_name, dtype):
+    c = dt.dattri_create(dtype, 777)
+    shapes = [(64, 48, 8, 4), (300, 37, 64, 24)]
+    for s in shapes:
+        dt.dattri_register_layer(c, *s)
+    dt.dattri_set_map_kind(c, 1, dt.DATTRI_MAP_RADEMACHER)
+    assert dt.dattri_get_map_kind(c, 0) == dt.DATTRI_MAP_GAUSSIAN
+    assert dt.dattri_get_map_kind(c, 1) == dt.DATTRI_MAP_RADEMACHER
+    d_in, d_out, k_in, k_out = shapes[1]
+    lib_in, lib_out = dt.dattri_get_projection(c, 1)
+    ora_in, ora_out = orng.projection_pair(777, 1, d_in, d_out, k_in, k_out, dtype_name, kind="rademacher")
+    np.testing.assert_array_equal(lib_in, ora_in.astype(np.float32))  # exact: no libm in the signs
+    np.testing.assert_array_equal(lib_out, ora_out.astype(np.float32))
+    for bad in (2, -1):
+        with pytest.raises(dt.DattriError) as e:
+            dt.dattri_set_map_kind(c, 0, bad)
+        assert _status(e) == "E_INVALID_ARG"
+    with pytest.raises(dt.DattriError):
+        dt.dattri_set_map_kind(c, 5, dt.DATTRI_MAP_RADEMACHER)
+    dt.dattri_destroy(c)
+
+
 def test_override_maps_are_rounded_and_returned():
     c = dt.dattri_create(dt.DATTRI_BF16, 0)
     dt.dattri_register_layer(c, 8, 4, 8, 4)

@@ -25,11 +25,13 @@ Modules
 ``kfac``       K-FAC / EK-FAC curvature on projected factors: factor
                covariances, eigenbases, EK-FAC's eigenvalue correction,
                damping and preconditioned scores (Sec. 3.2, App. A.2, App. B).
+``mask``       random coordinate masks of DW gathered from the factors
+               (App. A.2 "Random maps").
 
-Parity status of each function is stated in its docstring; the one function
-with no pin to the paper is the seed/counter layout of the generator, which the
-paper leaves unspecified ("parity unpinned" w.r.t. the paper, pinned to the
+Parity status of each function is stated in its docstring; the functions
+with no pin to the paper are the seed/counter layouts of the generator and of
+the mask draw, which the paper leaves unspecified ("parity unpinned" w.r.t. the paper, pinned to the
 published Philox / SplitMix64 definitions instead).
 """
 
-from . import rng, gradients, scoring, cost, crossgram, kfac  # noqa: F401
+from . import rng, gradients, scoring, cost, crossgram, kfac, mask  # noqa: F401

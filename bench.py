@@ -34,7 +34,7 @@ def parse():
     p.add_argument("--warmup", type=int, default=2)
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--phase", choices=["all", "project", "score", "routing", "gpt2", "crossgram", "curvature",
-                                       "fit", "copy"],
+                                       "fit", "mask", "copy"],
                    default="all")
     return p.parse_args()
 
@@ -454,6 +454,54 @@ def fit_case(dev, steps, warmup):
                                    "one batch of 32 x 196 layers, T=512, k=64"}}
 
 
+def mask_case(dev, steps, warmup):
+    """Random-mask gathers (App. A.2; AdamW-influence's reduced setting uses ten
+    disjoint masks of 512 or 8192 coordinates per layer) on the Llama-3-8B-
+    shaped batch of the projection benchmark (224 layers, T=2048, 8 examples):
+    each layer is one mask layer holding its ten masks, so one pass over the
+    factors gathers all of them.  Reports ms per batch and the rate against the
+    layer factors read (every layer reads its own A and B)."""
+    import torch
+    import workloads as W
+    from paper_2609_38767_amd.session import ProjectionSession, feature_rows
+    stream = torch.cuda.current_stream()
+    wl = W.WORKLOADS["llama8b"]
+    n, T = wl["batch"], wl["T"]
+    cache, inputs = {}, []
+    for li in range(len(wl["layers"])):
+        inputs.append(W.factor_blocks(wl, li, 0, n, T, dev, "bf16", a_cache=cache))
+    out = {"workload": "llama3-8b-shaped 224 linear layers, T=2048, batch 8, bf16; each layer one mask layer "
+                       "with 10 disjoint masks"}
+    for m in (512, 8192):
+        layers = [dict(L, k_in=1, k_out=10 * m, mask_size=m, mask_count=10) for L in wl["layers"]]
+        sess = ProjectionSession(layers, dtype="bf16", seed=wl["seed"], device=dev)
+        for li, (A, B) in enumerate(inputs):
+            sess.capture(li, A, B)
+        phi = feature_rows(n, sess.F, "f32", dev)
+        sess.workspace()
+        for _ in range(warmup):
+            sess.project(n, phi=phi)
+        evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(steps)]
+        torch.cuda.synchronize()
+        for a, b in evs:
+            a.record(stream)
+            sess.project(n, phi=phi)
+            b.record(stream)
+        torch.cuda.synchronize()
+        ms = sorted(a.elapsed_time(b) for a, b in evs)[steps // 2]
+        read = sum(T * (L["d_in"] + L["d_out"]) * 2 for L in layers) * n
+        out[f"masks_10x{m}"] = {"ms_per_batch": ms, "examples_per_s": n / (ms * 1e-3),
+                                 "factor_bytes_per_batch": read, "gbs": read / (ms * 1e-3) / 1e9,
+                                 "hbm_frac": read / (ms * 1e-3) / 8e12, "features": sess.F}
+        print(f"[bench] mask 10 x {m}: {ms:.2f} ms per batch ({read / (ms * 1e-3) / 1e9:.0f} GB/s of factors)",
+              file=sys.stderr, flush=True)
+        sess.close()
+        del phi
+    del cache, inputs
+    torch.cuda.empty_cache()
+    return out
+
+
 def stream_reference(dev):
     """Achievable HBM rate on this GPU: a 1 GiB device-to-device copy (read +
     write bytes per second, best of 5)."""
@@ -603,6 +651,8 @@ def main():
         out["curvature"] = curvature_case(dev, max(min(args.steps, 5), 3), min(args.warmup, 1))
     if args.phase in ("all", "fit"):
         out["projection_fit"] = fit_case(dev, args.steps, args.warmup)
+    if args.phase in ("all", "mask"):
+        out["mask"] = mask_case(dev, max(min(args.steps, 5), 3), min(args.warmup, 1))
     if args.phase in ("all", "score"):
         for _ in range(args.warmup):
             score_step(False)

@@ -71,7 +71,8 @@ typedef enum { DATTRI_F32 = 0, DATTRI_BF16 = 1 } dattri_dtype;
 typedef enum {
   DATTRI_ROUTE_AUTO = 0,        /* per-layer choice of the cost model */
   DATTRI_ROUTE_FACTORED = 1,    /* (A P_in)^T (B P_out), Eq. (2) left side */
-  DATTRI_ROUTE_MATERIALIZED = 2 /* G = B^T A, then P_out^T G P_in */
+  DATTRI_ROUTE_MATERIALIZED = 2, /* G = B^T A, then P_out^T G P_in */
+  DATTRI_ROUTE_MASK = 3          /* reported for mask layers only (gathered entries) */
 } dattri_route;
 
 /* Kernel form of the factored route.  Both compute Eq. (2)'s left side with
@@ -119,6 +120,38 @@ const char* dattri_last_error(void);
  * Errors: INVALID_ARG (ctx/layer_id NULL, any size < 1, d or k > 2^20). */
 dattri_status dattri_register_layer(dattri_ctx* ctx, int32_t d_in, int32_t d_out,
                                     int32_t k_in, int32_t k_out, int32_t* layer_id);
+
+/* Register a mask layer (App. A.2 "Random maps": a random mask keeps a fixed
+ * random subset M of the entries of DW, gathered from the factors as
+ * sum_t g_{t,r} a_{t,c}, |M| products per token, DW never formed).  The
+ * layer's block in phi holds masks mask_id .. mask_id + mask_count - 1 of the
+ * layer, mask_size entries each, back to back (one pass over the factors
+ * serves them all); inside a mask, entry e is DW[r_e][c_e], ordered by
+ * u = c * d_out + r (Eq. 1's column-stacked order).  The masks are drawn from
+ * the layer's seed: with base = SM(seed) and s = SM(base ^ (2^63 | layer)),
+ * draw i is ((x0 << 32) | x1) mod (d_out d_in) for
+ * (x0..x3) = Philox4x32-10(counter (i lo, i hi, 0, 0), key (s lo, s hi));
+ * repeats are dropped (first occurrence kept) and mask j is run j of
+ * mask_size consecutive distinct draws, so the masks of a layer are disjoint
+ * (AdamW-influence uses ten of 512 or 8192 entries, App. B).  Such a layer is
+ * always projected by the gather kernel (route DATTRI_ROUTE_MASK, whatever
+ * route is requested); its "maps" are the entry table (dattri_projection_bytes
+ * gives its size in bytes_in, 0 in bytes_out; dattri_bind_projection uploads
+ * it into dev_P_in, dev_P_out may be NULL, overrides are refused).
+ * dattri_layer_dims reports k_in = 1, k_out = mask_size * mask_count.
+ * Curvature calls reject mask layers.
+ * Errors: INVALID_ARG (NULL pointers, sizes outside [1, 2^20], mask_size or
+ * mask_count < 1, more than 2^24 entries, (mask_id + mask_count) * mask_size
+ * above half of d_in * d_out). */
+dattri_status dattri_register_mask_layer(dattri_ctx* ctx, int32_t d_in, int32_t d_out,
+                                         int32_t mask_size, int32_t mask_id, int32_t mask_count,
+                                         int32_t* layer_id);
+
+/* Host copy of a mask layer's entries (rows r_e and cols c_e, int32
+ * [mask_size * mask_count] each, in block order; either output may be NULL).
+ * Host-only.
+ * Errors: INVALID_ARG (bad layer, not a mask layer). */
+dattri_status dattri_get_mask(const dattri_ctx* ctx, int32_t layer, int32_t* rows, int32_t* cols);
 
 /* Number of registered layers. */
 dattri_status dattri_num_layers(const dattri_ctx* ctx, int32_t* n);

@@ -34,10 +34,11 @@ __all__ = [
     "dattri_project_fit_workspace_bytes", "dattri_project_and_fit",
     "DATTRI_MAP_GAUSSIAN", "DATTRI_MAP_RADEMACHER", "dattri_set_map_kind", "dattri_get_map_kind",
     "dattri_cosine_workspace_bytes", "dattri_score_cosine",
+    "DATTRI_ROUTE_MASK", "dattri_register_mask_layer", "dattri_get_mask",
 ]
 
 DATTRI_F32, DATTRI_BF16 = 0, 1
-DATTRI_ROUTE_AUTO, DATTRI_ROUTE_FACTORED, DATTRI_ROUTE_MATERIALIZED = 0, 1, 2
+DATTRI_ROUTE_AUTO, DATTRI_ROUTE_FACTORED, DATTRI_ROUTE_MATERIALIZED, DATTRI_ROUTE_MASK = 0, 1, 2, 3
 DATTRI_FORM_AUTO, DATTRI_FORM_FUSED, DATTRI_FORM_SPLIT = 0, 1, 2
 DATTRI_CURV_KFAC, DATTRI_CURV_EKFAC = 0, 1
 DATTRI_MAP_GAUSSIAN, DATTRI_MAP_RADEMACHER = 0, 1
@@ -124,6 +125,8 @@ _SIGS = {
     "dattri_curvature_accumulate_ekfac": (_i32, [_vp, _vp, _vp, _i32, _i64, _i64, _vp, _sz, _vp]),
     "dattri_project_fit_workspace_bytes": (_i32, [_vp, _i32, _P(_sz)]),
     "dattri_set_map_kind": (_i32, [_vp, _i32, _i32]),
+    "dattri_register_mask_layer": (_i32, [_vp, _i32, _i32, _i32, _i32, _i32, _P(_i32)]),
+    "dattri_get_mask": (_i32, [_vp, _i32, _vp, _vp]),
     "dattri_cosine_workspace_bytes": (_i32, [_i64, _i64, _i64, _i32, _i32, _i32, _i32, _P(_sz)]),
     "dattri_score_cosine": (_i32, [_vp, _i64, _i64, _vp, _i64, _i64, _i64, _i32, _vp, _vp, _i32, _vp, _vp,
                                    _vp, _sz, _vp]),
@@ -474,3 +477,20 @@ def dattri_score_cosine(phi_q, n_q, ld_q, phi_train, n_train, ld_train, F, dtype
                                       _ptr(dev_precond_diag), _ptr(scores), topk, _ptr(topk_idx), _ptr(topk_val),
                                       _ptr(workspace), ws_bytes, _stream(stream)),
            "dattri_score_cosine")
+
+
+def dattri_register_mask_layer(ctx, d_in, d_out, mask_size, mask_id=0, mask_count=1):
+    lid = _i32()
+    _check(load().dattri_register_mask_layer(ctx, d_in, d_out, mask_size, mask_id, mask_count, ctypes.byref(lid)),
+           "dattri_register_mask_layer")
+    return lid.value
+
+
+def dattri_get_mask(ctx, layer):
+    """(rows, cols) int32 numpy arrays of a mask layer's entries."""
+    import numpy as np
+    _, _, _, m = dattri_layer_dims(ctx, layer)
+    rows = np.empty(m, dtype=np.int32)
+    cols = np.empty(m, dtype=np.int32)
+    _check(load().dattri_get_mask(ctx, layer, rows.ctypes.data, cols.ctypes.data), "dattri_get_mask")
+    return rows, cols

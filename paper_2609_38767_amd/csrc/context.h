@@ -18,6 +18,9 @@ struct Layer {
   void* P_out = nullptr;
   bool bound = false;
   int32_t map_kind = 0;  // dattri_map_kind of the seeded maps
+  // mask layer when mask_size > 0: masks mask_id .. mask_id + mask_count - 1 of
+  // mask_size entries each, back to back (k_in = 1, k_out = mask_size * mask_count)
+  int32_t mask_size = 0, mask_id = 0, mask_count = 0;
   std::vector<float> override_in, override_out;  // rounded values when overridden
   const void* A = nullptr;  // captured [n, T, d_in]
   const void* B = nullptr;  // captured [n, T, d_out]

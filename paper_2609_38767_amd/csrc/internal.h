@@ -201,6 +201,31 @@ hipError_t launch_kacc(const float* parts, int nchunks, int n1, int n2, float* K
                        int c0, int diag, int accumulate, hipStream_t s);
 hipError_t launch_fill_rows(float* K, int rows, int cols, int64_t ld, hipStream_t s);
 
+// ---------------------------------------------------------- random masks
+// A mask layer keeps m entries (r_e, c_e) of DW, gathered from the factors:
+// out[e] = sum_t B[t][r_e] A[t][c_e].  Work item = (task, example, token
+// chunk, group of up to kMaskGroup entries); token rows of A and B are staged
+// in LDS `stage_tokens` at a time (contiguous rows, moved as one block; two
+// stage buffers of [A rows | B rows], each part rounded up to 1 KiB) and
+// every thread sums the products of its entries; each item writes its entries'
+// partial sums at partial_base + ((example * n_chunks + chunk) * m + entry),
+// summed over chunks by the reduce kernel.
+constexpr int kMaskPerThread = 32;
+constexpr int kMaskGroup = 256 * kMaskPerThread;   // entries per work item
+constexpr int64_t kMaskStageBudget = 40 * 1024;   // bytes of one stage (two stages per work item)
+struct MaskTask {
+  const void* A; const void* B;      // [n, T, d_in], [n, T, d_out]
+  const int32_t* lengths;            // [n] or null
+  const int32_t* rows;               // [m] output feature of each entry
+  const int32_t* cols;               // [m] input feature of each entry
+  int32_t d_in, d_out, T, m;
+  int32_t stage_tokens, chunk_tokens, n_chunks, aligned;  // aligned: 16-byte row blocks
+  int64_t partial_base;
+};
+struct MaskItem { int32_t task, example, chunk, group; };  // task < 0: padding
+hipError_t launch_mask(int elt_bytes, int aligned, const MaskItem* items, int n_items, const MaskTask* tasks,
+                       size_t lds_bytes, float* partials, hipStream_t s);
+
 // ---------------------------------------------------------------- scoring
 // dst rows ld_dst apart receive src rows (ld_src apart) times d, first F columns
 hipError_t launch_scale_rows(int elt_bytes, const void* src, int64_t ld_src, const float* d,

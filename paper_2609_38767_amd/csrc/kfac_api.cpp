@@ -37,6 +37,8 @@ dattri_status check_layers(const dattri_ctx* ctx) {
   if (ctx->layers.empty()) return fail(DATTRI_E_STATE, "no layer registered");
   for (size_t l = 0; l < ctx->layers.size(); ++l) {
     const Layer& L = ctx->layers[l];
+    if (L.mask_size > 0)
+      return fail(DATTRI_E_UNSUPPORTED, "layer %zu is a mask layer: curvature needs the projected factors", l);
     if (L.k_in > kCurvMaxK || L.k_out > kCurvMaxK)
       return fail(DATTRI_E_UNSUPPORTED, "layer %zu: curvature needs k_in, k_out <= %d (got %d, %d)", l,
                   kCurvMaxK, L.k_in, L.k_out);

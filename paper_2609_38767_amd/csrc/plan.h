@@ -45,6 +45,14 @@ struct Plan {
   std::vector<SlabSumTask> slabsum;
   int64_t slabsum_max_n4 = 0;
   int split_max_tchunks = 0, split_max_out = 0;
+  // mask layers (gathered DW entries)
+  std::vector<MaskTask> mtasks;
+  std::vector<MaskItem> mitems;
+  struct MaskLaunch { int aligned, first, count; };
+  std::vector<MaskLaunch> mlaunches;
+  std::vector<ReduceTask> mreduce;
+  int mask_max_out = 0;
+  size_t mask_lds = 0;
   // projected token rows kept for the curvature fit (rows = true)
   bool rows = false;
   std::vector<size_t> member_rows;  // per fused member: byte offsets of its A rows, B rows (pairs)
@@ -57,6 +65,7 @@ struct Plan {
   size_t off_fpart = 0, fpart_bytes = 0, off_g = 0, g_bytes = 0, off_mpart = 0, mpart_bytes = 0;
   size_t off_proj = 0, proj_bytes = 0, off_spart = 0, spart_bytes = 0;
   size_t off_rows = 0, rows_bytes = 0;
+  size_t off_mtasks = 0, off_mitems = 0, off_mreduce = 0, off_maskpart = 0, maskpart_bytes = 0;
   size_t total = 0;
 };
 

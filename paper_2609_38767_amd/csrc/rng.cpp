@@ -12,6 +12,8 @@
 #include <cmath>
 #include <cstring>
 #include <thread>
+#include <algorithm>
+#include <unordered_set>
 #include <vector>
 
 #include "internal.h"
@@ -28,6 +30,10 @@ static inline uint64_t splitmix_out(uint64_t state) {
 
 uint64_t derive_side_seed(uint64_t global_seed, int layer, int side) {
   return splitmix_out(splitmix_out(global_seed) ^ (uint64_t)(2 * (int64_t)layer + side));
+}
+
+uint64_t derive_mask_seed(uint64_t global_seed, int layer) {
+  return splitmix_out(splitmix_out(global_seed) ^ ((uint64_t)1 << 63) ^ (uint64_t)(uint32_t)layer);
 }
 
 static inline void philox10(uint32_t c[4], uint32_t k0, uint32_t k1) {
@@ -64,6 +70,39 @@ double rademacher_entry(uint64_t seed64, uint64_t e) {
   uint32_t c[4] = {(uint32_t)e, (uint32_t)(e >> 32), 0u, 0u};
   philox10(c, (uint32_t)seed64, (uint32_t)(seed64 >> 32));
   return (c[0] >> 31) ? -1.0 : 1.0;
+}
+
+// Masks mask_id .. mask_id + count - 1 (m entries each) of a d_out x d_in
+// gradient: the distinct flat indices u of the draw stream
+// u_i = (x0:x1) mod (d_out d_in), Philox counter (i lo, i hi, 0, 0) under the
+// layer's mask key, first occurrences kept; mask j is run j of m consecutive
+// distinct draws, sorted by u = c * d_out + r; the masks are concatenated.
+// Needs (mask_id + count) * m <= d_out * d_in / 2 (checked by the caller).
+void mask_entries(uint64_t seed64, int d_in, int d_out, int m, int mask_id, int count,
+                  std::vector<int32_t>& rows, std::vector<int32_t>& cols) {
+  const uint64_t N = (uint64_t)d_in * (uint64_t)d_out;
+  const size_t need = (size_t)(mask_id + count) * (size_t)m;
+  std::unordered_set<uint64_t> seen;
+  seen.reserve(2 * need);
+  std::vector<uint64_t> order;
+  order.reserve(need);
+  for (uint64_t i = 0; order.size() < need; ++i) {
+    uint32_t c[4] = {(uint32_t)i, (uint32_t)(i >> 32), 0u, 0u};
+    philox10(c, (uint32_t)seed64, (uint32_t)(seed64 >> 32));
+    const uint64_t u = ((((uint64_t)c[0]) << 32) | c[1]) % N;
+    if (seen.insert(u).second) order.push_back(u);
+  }
+  rows.resize((size_t)count * m);
+  cols.resize((size_t)count * m);
+  for (int j = 0; j < count; ++j) {
+    std::vector<uint64_t> run(order.begin() + (size_t)(mask_id + j) * m,
+                              order.begin() + (size_t)(mask_id + j + 1) * m);
+    std::sort(run.begin(), run.end());
+    for (int e = 0; e < m; ++e) {
+      rows[(size_t)j * m + e] = (int32_t)(run[e] % (uint64_t)d_out);
+      cols[(size_t)j * m + e] = (int32_t)(run[e] / (uint64_t)d_out);
+    }
+  }
 }
 
 uint16_t f32_to_bf16_rne(float f) {

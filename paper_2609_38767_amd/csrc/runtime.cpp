@@ -102,6 +102,7 @@ void predict(const dattri_cost_model& m, const Layer& L, int64_t n, int64_t T, i
 }
 
 dattri_route choose_route(const dattri_ctx* ctx, const Layer& L, dattri_route forced) {
+  if (L.mask_size > 0) return DATTRI_ROUTE_MASK;  // gathered from the factors, whatever the request
   if (forced != DATTRI_ROUTE_AUTO) return forced;
   if (!factored_supported(L)) return DATTRI_ROUTE_MATERIALIZED;
   double f, m;
@@ -154,7 +155,7 @@ dattri_status dattri::build_plan(const dattri_ctx* ctx, dattri_route forced, Pla
   for (size_t l = 0; l < ctx->layers.size(); ++l) {
     const Layer& L = ctx->layers[l];
     const dattri_route r = choose_route(ctx, L, forced);
-    if (r == DATTRI_ROUTE_MATERIALIZED) continue;
+    if (r == DATTRI_ROUTE_MATERIALIZED || r == DATTRI_ROUTE_MASK) continue;
     if (!factored_supported(L))
       return fail(DATTRI_E_UNSUPPORTED,
                   "layer %zu: factored route needs k_in <= %d and k_out <= %d (got %d, %d)", l,
@@ -506,6 +507,82 @@ dattri_status dattri::build_plan(const dattri_ctx* ctx, dattri_route forced, Pla
     }
   }
 
+  // ---- mask layers: (example, token chunk, entry group) work items
+  {
+    size_t mask_floats = 0;
+    int64_t units = 0;  // example x entry-group pairs over all mask layers
+    for (const Layer& L : ctx->layers)
+      if (L.mask_size > 0) units += (int64_t)n * ((L.k_out + kMaskGroup - 1) / kMaskGroup);
+    const int64_t want_chunks = units > 0 ? std::max<int64_t>(1, (2048 + units - 1) / units) : 1;
+    for (size_t l = 0; l < ctx->layers.size(); ++l) {
+      const Layer& L = ctx->layers[l];
+      if (L.mask_size <= 0) continue;
+      const int64_t row_bytes = (int64_t)(L.d_in + L.d_out) * elt;
+      if (row_bytes + 2048 > 80 * 1024)
+        return fail(DATTRI_E_UNSUPPORTED, "layer %zu: mask layers need (d_in + d_out) * %d <= 78 KiB", l, elt);
+      MaskTask M;
+      std::memset(&M, 0, sizeof(M));
+      M.A = L.A; M.B = L.B; M.lengths = L.lengths;
+      M.rows = (const int32_t*)L.P_in;
+      M.cols = (const int32_t*)L.P_in + L.k_out;
+      M.d_in = L.d_in; M.d_out = L.d_out; M.T = L.T; M.m = L.k_out;
+      M.stage_tokens = (int)std::max<int64_t>(1, std::min<int64_t>(16, kMaskStageBudget / row_bytes));
+      const int64_t tc = (L.T + want_chunks - 1) / want_chunks;
+      M.chunk_tokens = (int)std::max<int64_t>(M.stage_tokens, (tc + M.stage_tokens - 1) / M.stage_tokens * M.stage_tokens);
+      M.n_chunks = std::max(1, (L.T + M.chunk_tokens - 1) / M.chunk_tokens);
+      M.aligned = ((uintptr_t)L.A % 16 == 0) && ((uintptr_t)L.B % 16 == 0) && (L.d_in * elt) % 16 == 0 &&
+                  (L.d_out * elt) % 16 == 0;
+      M.partial_base = (int64_t)mask_floats;
+      mask_floats += (size_t)n * M.n_chunks * M.m;
+      // aligned: two buffers of [A part | B part], parts rounded up to 1 KiB; else one buffer
+      const int64_t a_part = ((int64_t)M.stage_tokens * L.d_in * elt + 1023) & ~(int64_t)1023;
+      const int64_t b_part = ((int64_t)M.stage_tokens * L.d_out * elt + 1023) & ~(int64_t)1023;
+      const size_t lds = (size_t)(M.aligned ? 2 * (a_part + b_part) : a_part + b_part);
+      P.mask_lds = std::max(P.mask_lds, lds);
+      ReduceTask R;
+      std::memset(&R, 0, sizeof(R));
+      R.partial_base = M.partial_base;
+      R.phi_offset = L.offset;
+      R.n_parts = M.n_chunks;
+      R.k_in = 1;
+      R.k_out = M.m;
+      R.ldp = M.m;
+      R.part_floats = M.m;
+      P.mreduce.push_back(R);
+      P.mask_max_out = std::max(P.mask_max_out, M.m);
+      P.mtasks.push_back(M);
+    }
+    // Every entry group of one (layer, example, token chunk) stages the same
+    // token rows: the groups of a chunk go to one XCD, back to back, so they
+    // run together and share the rows through that XCD's L2.  Chunks are dealt
+    // to the least-loaded of 8 per-XCD queues and the queues interleaved
+    // (workgroup i runs on XCD i mod 8); short queues are padded.
+    for (int al = 1; al >= 0; --al) {
+      std::vector<std::vector<MaskItem>> q(kXcds);
+      int64_t load[kXcds] = {0};
+      for (size_t t = 0; t < P.mtasks.size(); ++t) {
+        const MaskTask& M = P.mtasks[t];
+        if (M.aligned != al) continue;
+        const int groups = (M.m + kMaskGroup - 1) / kMaskGroup;
+        for (int e = 0; e < n; ++e)
+          for (int c = 0; c < M.n_chunks; ++c) {
+            const int x = (int)(std::min_element(load, load + kXcds) - load);
+            for (int g = 0; g < groups; ++g) q[x].push_back({(int)t, e, c, g});
+            load[x] += groups;
+          }
+      }
+      size_t len = 0;
+      for (const auto& v : q) len = std::max(len, v.size());
+      const int first = (int)P.mitems.size();
+      for (size_t i = 0; i < len; ++i)
+        for (int x = 0; x < kXcds; ++x)
+          P.mitems.push_back(i < q[x].size() ? q[x][i] : MaskItem{-1, 0, 0, 0});
+      const int count = (int)P.mitems.size() - first;
+      if (count) P.mlaunches.push_back({al, first, count});
+    }
+    P.maskpart_bytes = mask_floats * 4;
+  }
+
   // ---- workspace layout
   size_t off = 0;
   P.off_items = off;   off = align_up(off + P.items.size() * sizeof(FactItem));
@@ -517,12 +594,16 @@ dattri_status dattri::build_plan(const dattri_ctx* ctx, dattri_route forced, Pla
   P.off_ctasks = off;  off = align_up(off + P.ctasks.size() * sizeof(ContractTask));
   P.off_stasks = off;  off = align_up(off + P.stasks.size() * sizeof(ReduceTask));
   P.off_slabsum = off; off = align_up(off + P.slabsum.size() * sizeof(SlabSumTask));
+  P.off_mtasks = off;  off = align_up(off + P.mtasks.size() * sizeof(MaskTask));
+  P.off_mitems = off;  off = align_up(off + P.mitems.size() * sizeof(MaskItem));
+  P.off_mreduce = off; off = align_up(off + P.mreduce.size() * sizeof(ReduceTask));
   P.blob_bytes = off;
   P.off_fpart = off;   P.fpart_bytes = fpart_floats * 4; off = align_up(off + P.fpart_bytes);
   P.off_g = off;       P.g_bytes = g_floats * 4;         off = align_up(off + P.g_bytes);
   P.off_mpart = off;   P.mpart_bytes = mpart_floats * 4; off = align_up(off + P.mpart_bytes);
   P.off_proj = off;    off = align_up(off + P.proj_bytes);
   P.off_spart = off;   off = align_up(off + P.spart_bytes);
+  P.off_maskpart = off; off = align_up(off + P.maskpart_bytes);
   // projected token rows of the fused members, and where every factored
   // layer side's rows sit (split form: slab 0 of its stage-1 op)
   P.rows = rows;
@@ -611,6 +692,9 @@ dattri_status dattri::run_plan(dattri_ctx* ctx, const Plan& P, void* phi, dattri
   put(P.off_ctasks, P.ctasks.data(), P.ctasks.size() * sizeof(ContractTask));
   put(P.off_stasks, P.stasks.data(), P.stasks.size() * sizeof(ReduceTask));
   put(P.off_slabsum, P.slabsum.data(), P.slabsum.size() * sizeof(SlabSumTask));
+  put(P.off_mtasks, P.mtasks.data(), P.mtasks.size() * sizeof(MaskTask));
+  put(P.off_mitems, P.mitems.data(), P.mitems.size() * sizeof(MaskItem));
+  put(P.off_mreduce, P.mreduce.data(), P.mreduce.size() * sizeof(ReduceTask));
   uint8_t* ws = (uint8_t*)workspace;
   HIP_TRY(hipMemcpyAsync(ws, ctx->blob.data(), P.blob_bytes, hipMemcpyHostToDevice, s));
 
@@ -642,6 +726,15 @@ dattri_status dattri::run_plan(dattri_ctx* ctx, const Plan& P, void* phi, dattri
   if (!P.stasks.empty())
     HIP_TRY(launch_reduce((const ReduceTask*)(ws + P.off_stasks), (int)P.stasks.size(), n,
                           P.split_max_out, spart, phi, phi_bf16, ld_phi, s));
+
+  if (!P.mtasks.empty()) {
+    float* kpart = (float*)(ws + P.off_maskpart);
+    for (const Plan::MaskLaunch& L : P.mlaunches)
+      HIP_TRY(launch_mask(ctx->elt, L.aligned, (const MaskItem*)(ws + P.off_mitems) + L.first, L.count,
+                          (const MaskTask*)(ws + P.off_mtasks), P.mask_lds, kpart, s));
+    HIP_TRY(launch_reduce((const ReduceTask*)(ws + P.off_mreduce), (int)P.mreduce.size(), n, P.mask_max_out,
+                          kpart, phi, phi_bf16, ld_phi, s));
+  }
 
   float* gbuf = (float*)(ws + P.off_g);
   float* mpart = (float*)(ws + P.off_mpart);
@@ -707,6 +800,44 @@ dattri_status dattri_register_layer(dattri_ctx* ctx, int32_t d_in, int32_t d_out
   return DATTRI_OK;
 }
 
+dattri_status dattri_register_mask_layer(dattri_ctx* ctx, int32_t d_in, int32_t d_out, int32_t mask_size,
+                                         int32_t mask_id, int32_t mask_count, int32_t* layer_id) {
+  reset_error();
+  if (!ctx || !layer_id) return fail(DATTRI_E_INVALID_ARG, "ctx or layer_id is NULL");
+  if (d_in < 1 || d_out < 1 || d_in > kMaxDim || d_out > kMaxDim)
+    return fail(DATTRI_E_INVALID_ARG, "sizes must lie in [1, 2^20]: d_in=%d d_out=%d", d_in, d_out);
+  if (mask_size < 1 || mask_id < 0 || mask_count < 1 || (int64_t)mask_size * mask_count > (1 << 24))
+    return fail(DATTRI_E_INVALID_ARG, "mask_size=%d, mask_count=%d must be >= 1 with at most 2^24 entries in all, "
+                "mask_id=%d >= 0", mask_size, mask_count, mask_id);
+  const int64_t last = ((int64_t)mask_id + mask_count) * mask_size;
+  if (2 * last > (int64_t)d_in * d_out)
+    return fail(DATTRI_E_INVALID_ARG, "(mask_id + mask_count) * mask_size = %lld exceeds half of the %lld entries",
+                (long long)last, (long long)((int64_t)d_in * d_out));
+  Layer L;
+  L.d_in = d_in; L.d_out = d_out; L.k_in = 1; L.k_out = mask_size * mask_count;
+  L.mask_size = mask_size;
+  L.mask_id = mask_id;
+  L.mask_count = mask_count;
+  L.offset = ctx->F;
+  ctx->F += (int64_t)mask_size * mask_count;
+  ctx->layers.push_back(std::move(L));
+  *layer_id = (int32_t)ctx->layers.size() - 1;
+  return DATTRI_OK;
+}
+
+dattri_status dattri_get_mask(const dattri_ctx* ctx, int32_t layer, int32_t* rows, int32_t* cols) {
+  reset_error();
+  dattri_status st = check_layer(ctx, layer);
+  if (st != DATTRI_OK) return st;
+  const Layer& L = ctx->layers[layer];
+  if (L.mask_size <= 0) return fail(DATTRI_E_INVALID_ARG, "layer %d is not a mask layer", layer);
+  std::vector<int32_t> r, c;
+  mask_entries(derive_mask_seed(ctx->seed, layer), L.d_in, L.d_out, L.mask_size, L.mask_id, L.mask_count, r, c);
+  if (rows) std::memcpy(rows, r.data(), r.size() * 4);
+  if (cols) std::memcpy(cols, c.data(), c.size() * 4);
+  return DATTRI_OK;
+}
+
 dattri_status dattri_num_layers(const dattri_ctx* ctx, int32_t* n) {
   reset_error();
   if (!ctx || !n) return fail(DATTRI_E_INVALID_ARG, "ctx or n is NULL");
@@ -749,6 +880,11 @@ dattri_status dattri_projection_bytes(const dattri_ctx* ctx, int32_t layer, size
   dattri_status st = check_layer(ctx, layer);
   if (st != DATTRI_OK) return st;
   const Layer& L = ctx->layers[layer];
+  if (L.mask_size > 0) {  // the mask's entry table: rows then cols, int32
+    if (bytes_in) *bytes_in = (size_t)8 * L.k_out;
+    if (bytes_out) *bytes_out = 0;
+    return DATTRI_OK;
+  }
   if (bytes_in) *bytes_in = (size_t)packed_bytes(L.d_in, L.k_in, ctx->elt);
   if (bytes_out) *bytes_out = (size_t)packed_bytes(L.d_out, L.k_out, ctx->elt);
   return DATTRI_OK;
@@ -760,10 +896,27 @@ dattri_status dattri_bind_projection(dattri_ctx* ctx, int32_t layer, void* dev_P
   reset_error();
   dattri_status st = check_layer(ctx, layer);
   if (st != DATTRI_OK) return st;
+  Layer& L = ctx->layers[layer];
+  if (L.mask_size > 0) {  // upload the mask's entry table into dev_P_in
+    if (!dev_P_in) return fail(DATTRI_E_INVALID_ARG, "device table pointer is NULL");
+    if ((uintptr_t)dev_P_in % 16) return fail(DATTRI_E_INVALID_ARG, "device table pointer must be 16-byte aligned");
+    if (host_P_in_override || host_P_out_override)
+      return fail(DATTRI_E_INVALID_ARG, "mask layers take no map overrides");
+    std::vector<int32_t> r, c;
+    mask_entries(derive_mask_seed(ctx->seed, layer), L.d_in, L.d_out, L.mask_size, L.mask_id, L.mask_count, r, c);
+    std::vector<int32_t> table(r);
+    table.insert(table.end(), c.begin(), c.end());
+    hipStream_t s = (hipStream_t)stream;
+    HIP_TRY(hipMemcpyAsync(dev_P_in, table.data(), table.size() * 4, hipMemcpyHostToDevice, s));
+    HIP_TRY(hipStreamSynchronize(s));
+    L.P_in = dev_P_in;
+    L.P_out = nullptr;
+    L.bound = true;
+    return DATTRI_OK;
+  }
   if (!dev_P_in || !dev_P_out) return fail(DATTRI_E_INVALID_ARG, "device map pointer is NULL");
   if ((uintptr_t)dev_P_in % 16 || (uintptr_t)dev_P_out % 16)
     return fail(DATTRI_E_INVALID_ARG, "device map pointers must be 16-byte aligned");
-  Layer& L = ctx->layers[layer];
   for (int side = 0; side < 2; ++side) {
     const int d = side ? L.d_out : L.d_in, k = side ? L.k_out : L.k_in;
     const float* ov = side ? host_P_out_override : host_P_in_override;
@@ -798,6 +951,7 @@ dattri_status dattri_set_map_kind(dattri_ctx* ctx, int32_t layer, dattri_map_kin
   if (kind != DATTRI_MAP_GAUSSIAN && kind != DATTRI_MAP_RADEMACHER)
     return fail(DATTRI_E_INVALID_ARG, "map kind %d unknown", (int)kind);
   Layer& L = ctx->layers[layer];
+  if (L.mask_size > 0) return fail(DATTRI_E_INVALID_ARG, "layer %d is a mask layer", layer);
   if (L.map_kind != kind) {
     L.map_kind = kind;
     L.bound = false;  // the bound maps are of the other kind: bind again
@@ -819,6 +973,8 @@ dattri_status dattri_get_projection(const dattri_ctx* ctx, int32_t layer, float*
   reset_error();
   dattri_status st = check_layer(ctx, layer);
   if (st != DATTRI_OK) return st;
+  if (ctx->layers[layer].mask_size > 0)
+    return fail(DATTRI_E_INVALID_ARG, "layer %d is a mask layer (see dattri_get_mask)", layer);
   std::vector<float> v;
   if (host_P_in) {
     logical_map(ctx, layer, 0, v);
@@ -960,6 +1116,14 @@ dattri_status dattri_layer_costs(const dattri_ctx* ctx, int32_t layer, int32_t T
   dattri_status st = check_layer(ctx, layer);
   if (st != DATTRI_OK) return st;
   if (T < 0) return fail(DATTRI_E_INVALID_ARG, "T=%d < 0", T);
+  const Layer& ML = ctx->layers[layer];
+  if (ML.mask_size > 0) {  // the gather: one product per entry and token, both factor rows read
+    if (factored_flops) *factored_flops = 2 * (int64_t)T * ML.k_out;
+    if (factored_bytes) *factored_bytes = (int64_t)T * (ML.d_in + ML.d_out) * ctx->elt;
+    if (materialized_flops) *materialized_flops = 0;
+    if (materialized_bytes) *materialized_bytes = 0;
+    return DATTRI_OK;
+  }
   const Counts c = layer_counts(ctx->layers[layer], T, ctx->elt);
   if (factored_flops) *factored_flops = c.f_flops;
   if (materialized_flops) *materialized_flops = c.m_flops;
@@ -975,6 +1139,12 @@ dattri_status dattri_layer_route(const dattri_ctx* ctx, int32_t layer, dattri_ro
   if (st != DATTRI_OK) return st;
   const Layer& L = ctx->layers[layer];
   if (!L.captured) return fail(DATTRI_E_STATE, "layer %d has no capture", layer);
+  if (L.mask_size > 0) {
+    if (chosen) *chosen = DATTRI_ROUTE_MASK;
+    if (pred_factored_us) *pred_factored_us = INFINITY;
+    if (pred_materialized_us) *pred_materialized_us = INFINITY;
+    return DATTRI_OK;
+  }
   double f, m;
   predict(ctx->cost, L, L.n, L.T, ctx->elt, &f, &m);
   if (chosen) *chosen = choose_route(ctx, L, DATTRI_ROUTE_AUTO);

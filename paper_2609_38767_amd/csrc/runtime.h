@@ -8,6 +8,9 @@
 namespace dattri {
 
 uint64_t derive_side_seed(uint64_t global_seed, int layer, int side);
+uint64_t derive_mask_seed(uint64_t global_seed, int layer);
+void mask_entries(uint64_t seed64, int d_in, int d_out, int m, int mask_id, int count,
+                  std::vector<int32_t>& rows, std::vector<int32_t>& cols);
 void philox4x32_10(const uint32_t ctr[4], const uint32_t key[2], uint32_t out[4]);
 double gaussian_entry(uint64_t seed64, uint64_t e);
 double rademacher_entry(uint64_t seed64, uint64_t e);  // +-1

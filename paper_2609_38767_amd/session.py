@@ -22,7 +22,7 @@ from . import (DATTRI_BF16, DATTRI_F32, DATTRI_ROUTE_AUTO, dattri_bind_projectio
                dattri_curvature_eigen, dattri_curvature_ekfac_workspace_bytes,
                dattri_curvature_accumulate_ekfac, dattri_curvature_precondition,
                dattri_project_fit_workspace_bytes, dattri_project_and_fit, dattri_set_map_kind,
-               dattri_cosine_workspace_bytes, dattri_score_cosine)
+               dattri_cosine_workspace_bytes, dattri_score_cosine, dattri_register_mask_layer)
 
 DTYPES = {"f32": (DATTRI_F32, torch.float32), "bf16": (DATTRI_BF16, torch.bfloat16)}
 
@@ -45,10 +45,14 @@ class ProjectionSession:
         self.maps = []
         overrides = overrides or {}
         for i, L in enumerate(self.layers):
-            lid = dattri_register_layer(self.ctx, L["d_in"], L["d_out"], L["k_in"], L["k_out"])
+            if L.get("mask_size"):  # a random-mask layer (entries of DW gathered from the factors)
+                lid = dattri_register_mask_layer(self.ctx, L["d_in"], L["d_out"], L["mask_size"],
+                                                 L.get("mask_id", 0), L.get("mask_count", 1))
+            else:
+                lid = dattri_register_layer(self.ctx, L["d_in"], L["d_out"], L["k_in"], L["k_out"])
+                if map_kind is not None:
+                    dattri_set_map_kind(self.ctx, lid, map_kind)
             assert lid == i
-            if map_kind is not None:
-                dattri_set_map_kind(self.ctx, lid, map_kind)
             b_in, b_out = dattri_projection_bytes(self.ctx, lid)
             p_in, p_out = _dev_bytes(b_in, self.device), _dev_bytes(b_out, self.device)
             o_in, o_out = overrides.get(i, (None, None))

@@ -139,6 +139,53 @@ def test_rademacher_maps(dtype, route, form):
     assert e.value.status_name == "E_STATE"
 
 
+MASKED = [dict(name="m0", d_in=300, d_out=128, k_in=1, k_out=512, mask_size=512, mask_id=0, a_group="ma"),
+          dict(name="m1", d_in=300, d_out=128, k_in=1, k_out=1536, mask_size=512, mask_id=3, mask_count=3,
+               a_group="ma"),
+          dict(name="m2", d_in=200, d_out=100, k_in=1, k_out=9000, mask_size=9000, mask_id=0, a_group="mb"),
+          dict(name="m3", d_in=37, d_out=21, k_in=1, k_out=100, mask_size=100, mask_id=1, a_group="mc"),
+          dict(name="x", d_in=64, d_out=48, k_in=8, k_out=8, a_group="xa")]
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("route", ["auto", "materialized"])
+def test_mask_layers(dtype, route):
+    # App. A.2 random masks: DW entries gathered from the factors; two entry
+    # groups (m = 9000), an unaligned layer (37 x 21), ragged lengths over
+    # several token chunks, an ordinary layer beside them (its route forced)
+    from oracle import mask as om
+    wl = dict(W.WORKLOADS["tiny"], dist_a="normal", dist_b="normal", seed=31)
+    n, T = 4, 300
+    inputs = _session_inputs(wl, MASKED, n, T, dtype)
+    lengths = torch.tensor([300, 0, 17, 299], dtype=torch.int32, device=DEV)
+    s = ProjectionSession(MASKED, dtype=dtype, seed=41)
+    for li, (A, B) in enumerate(inputs):
+        s.capture(li, A, B, lengths)
+    phi = s.project(n, route=ROUTES[route])
+    torch.cuda.synchronize()
+    assert [r[0] for r in s.routes()[:4]] == [dt.DATTRI_ROUTE_MASK] * 4
+    lens = lengths.cpu().numpy()
+    got = host64(phi)
+    assert np.count_nonzero(got[1]) == 0  # length 0
+    for li, L in enumerate(MASKED):
+        A, B = host64(inputs[li][0]), host64(inputs[li][1])
+        off, w = s.offsets[li], L["k_in"] * L["k_out"]
+        if "mask_size" in L:
+            parts = [om.mask_indices(41, li, L["d_in"], L["d_out"], L["mask_size"], L["mask_id"] + j)
+                     for j in range(L.get("mask_count", 1))]
+            rows = np.concatenate([p[0] for p in parts])
+            cols = np.concatenate([p[1] for p in parts])
+            r_lib, c_lib = dt.dattri_get_mask(s.ctx, li)
+            np.testing.assert_array_equal(r_lib, rows)
+            ref = np.stack([om.masked_gradient(A[i], B[i], rows, cols, int(lens[i])) for i in range(n)])
+        else:
+            P_in, P_out = orng.projection_pair(41, li, L["d_in"], L["d_out"], L["k_in"], L["k_out"], dtype)
+            ref = np.stack([og.project_factored(A[i], B[i], P_in, P_out, int(lens[i])).reshape(-1)
+                            for i in range(n)])
+        e = rel_fro(got[:, off:off + w], ref)
+        assert e <= 1e-5, (li, e)
+
+
 @pytest.mark.parametrize("form", ["fused", "split"])
 def test_shared_input_group_matches_separate_inputs(form):
     # 16-wide maps: q and k share one fused work item (2 input tiles keep 4 row

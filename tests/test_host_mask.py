@@ -1,0 +1,72 @@
+"""Host-side tests of mask layers (no GPU): registration and feature layout,
+the mask draw against the oracle's (exact), the entry-table size, the route
+report and the documented errors."""
+import numpy as np
+import pytest
+
+import paper_2609_38767_amd as dt
+from oracle import mask as om
+
+
+def _status(e):
+    return e.value.status_name
+
+
+@pytest.fixture
+def ctx():
+    c = dt.dattri_create(dt.DATTRI_BF16, 4242)
+    yield c
+    dt.dattri_destroy(c)
+
+
+def test_mask_layer_layout_and_draw(ctx):
+    dt.dattri_register_layer(ctx, 64, 48, 8, 4)
+    l1 = dt.dattri_register_mask_layer(ctx, 300, 128, 512, 0)
+    l2 = dt.dattri_register_mask_layer(ctx, 300, 128, 512, 7)
+    l3 = dt.dattri_register_mask_layer(ctx, 4096, 14336, 8192, 9)
+    l4 = dt.dattri_register_mask_layer(ctx, 4096, 14336, 8192, 0, 10)  # ten disjoint masks, one block
+    assert dt.dattri_feature_dim(ctx) == 32 + 512 + 512 + 8192 + 81920
+    assert [dt.dattri_layer_offset(ctx, i) for i in (l1, l2, l3, l4)] == [32, 544, 1056, 9248]
+    assert dt.dattri_layer_dims(ctx, l4) == (4096, 14336, 1, 81920)
+    assert dt.dattri_projection_bytes(ctx, l4) == (8 * 81920, 0)
+    rows, cols = dt.dattri_get_mask(ctx, l4)
+    for j in range(10):
+        r_o, c_o = om.mask_indices(4242, l4, 4096, 14336, 8192, j)
+        np.testing.assert_array_equal(rows[j * 8192:(j + 1) * 8192], r_o)
+        np.testing.assert_array_equal(cols[j * 8192:(j + 1) * 8192], c_o)
+    flat = cols.astype(np.int64) * 14336 + rows
+    assert len(np.unique(flat)) == 81920  # disjoint
+    assert dt.dattri_layer_dims(ctx, l1) == (300, 128, 1, 512)
+    assert dt.dattri_projection_bytes(ctx, l3) == (8 * 8192, 0)
+    for lid, (d_in, d_out, m, j) in ((l1, (300, 128, 512, 0)), (l2, (300, 128, 512, 7)),
+                                     (l3, (4096, 14336, 8192, 9))):
+        rows, cols = dt.dattri_get_mask(ctx, lid)
+        r_o, c_o = om.mask_indices(4242, lid, d_in, d_out, m, j)
+        np.testing.assert_array_equal(rows, r_o)
+        np.testing.assert_array_equal(cols, c_o)
+    with pytest.raises(dt.DattriError) as e:
+        dt.dattri_get_mask(ctx, 0)
+    assert _status(e) == "E_INVALID_ARG"
+    with pytest.raises(dt.DattriError) as e:
+        dt.dattri_get_projection(ctx, l1)
+    assert _status(e) == "E_INVALID_ARG"
+    with pytest.raises(dt.DattriError) as e:
+        dt.dattri_set_map_kind(ctx, l1, dt.DATTRI_MAP_RADEMACHER)
+    assert _status(e) == "E_INVALID_ARG"
+    # cost counters of the gather
+    f, m_, fb, mb = dt.dattri_layer_costs(ctx, l3, 2048)
+    assert (f, m_, fb, mb) == (2 * 2048 * 8192, 0, 2048 * (4096 + 14336) * 2, 0)
+    # curvature refuses mask layers
+    with pytest.raises(dt.DattriError) as e:
+        dt.dattri_curvature_state_bytes(ctx)
+    assert _status(e) == "E_UNSUPPORTED"
+
+
+def test_mask_registration_errors(ctx):
+    for args in [(0, 4, 2, 0), (4, 0, 2, 0), (8, 8, 0, 0), (8, 8, 2, -1), (8, 8, 33, 0), (8, 8, 11, 2),
+                 (8, 8, 4, 0, 0), (8, 8, 4, 5, 4)]:
+        with pytest.raises(dt.DattriError) as e:
+            dt.dattri_register_mask_layer(ctx, *args)
+        assert _status(e) == "E_INVALID_ARG", args
+    assert dt.dattri_register_mask_layer(ctx, 8, 8, 16, 0) == 0  # exactly half of the 64 entries
+    assert dt.dattri_num_layers(ctx) == 1

@@ -27,6 +27,8 @@ Modules
                damping and preconditioned scores (Sec. 3.2, App. A.2, App. B).
 ``mask``       random coordinate masks of DW gathered from the factors
                (App. A.2 "Random maps").
+``token``      token-level attribution: per-token contributions g_t^T R a_t
+               whose sum is the sequence score (App. D).
 
 Parity status of each function is stated in its docstring; the functions
 with no pin to the paper are the seed/counter layouts of the generator and of
@@ -34,4 +36,4 @@ the mask draw, which the paper leaves unspecified ("parity unpinned" w.r.t. the 
 published Philox / SplitMix64 definitions instead).
 """
 
-from . import rng, gradients, scoring, cost, crossgram, kfac, mask  # noqa: F401
+from . import rng, gradients, scoring, cost, crossgram, kfac, mask, token  # noqa: F401

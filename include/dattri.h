@@ -580,6 +580,31 @@ dattri_status dattri_curvature_precondition(const dattri_ctx* ctx, const void* s
                                             void* out, dattri_dtype out_dtype, int64_t ld_out,
                                             void* stream);
 
+/* ------------------------------------------------- token-level attribution */
+
+/* Token-level scores (App. D: the contribution of token t of training example
+ * i to its score against query j is g_t^T R^(j) a_t, and the contributions sum
+ * to <DW^(i), R^(j)>_F; summed over layers).  On projected factors the
+ * layer's query-side matrix is the query row's k_in x k_out block R (element
+ * (c, r) the coefficient of a~_t[c] g~_t[r], the layout of phi), so
+ *   scores[q][i][t] = sum over layers of a~_t^T R_q g~_t,
+ * and sum_t scores[q][i][t] = <phi_q[q], phi[i]> (GradDot for the query's own
+ * phi row; K-FAC / EK-FAC for rows from dattri_curvature_precondition).
+ * Positions at or past a layer's length for example i add nothing.
+ * The call also projects the current captures (every layer on the factored
+ * route, which forms the projected rows) and writes their phi when `phi` is
+ * given (as dattri_project_per_example; NULL keeps it in the workspace).
+ *   phi_q:  device [n_q rows of F] of q_dtype, rows ld_q apart (>= F)
+ *   scores: device float32 [n_q][n][T]
+ *   workspace: >= dattri_token_scores_workspace_bytes(ctx), 256-byte aligned.
+ * Layers need k_in, k_out <= 64, one T for all captures, no mask layers.
+ * Errors: INVALID_ARG, DTYPE, SHAPE, STATE, WORKSPACE, UNSUPPORTED, HIP. */
+dattri_status dattri_token_scores_workspace_bytes(const dattri_ctx* ctx, size_t* bytes);
+dattri_status dattri_token_scores(dattri_ctx* ctx, const void* phi_q, dattri_dtype q_dtype,
+                                  int64_t n_q, int64_t ld_q, float* scores, void* phi,
+                                  dattri_dtype phi_dtype, int64_t ld_phi, void* workspace,
+                                  size_t ws_bytes, void* stream);
+
 #ifdef __cplusplus
 }
 #endif

@@ -35,6 +35,7 @@ __all__ = [
     "DATTRI_MAP_GAUSSIAN", "DATTRI_MAP_RADEMACHER", "dattri_set_map_kind", "dattri_get_map_kind",
     "dattri_cosine_workspace_bytes", "dattri_score_cosine",
     "DATTRI_ROUTE_MASK", "dattri_register_mask_layer", "dattri_get_mask",
+    "dattri_token_scores_workspace_bytes", "dattri_token_scores",
 ]
 
 DATTRI_F32, DATTRI_BF16 = 0, 1
@@ -127,6 +128,8 @@ _SIGS = {
     "dattri_set_map_kind": (_i32, [_vp, _i32, _i32]),
     "dattri_register_mask_layer": (_i32, [_vp, _i32, _i32, _i32, _i32, _i32, _P(_i32)]),
     "dattri_get_mask": (_i32, [_vp, _i32, _vp, _vp]),
+    "dattri_token_scores_workspace_bytes": (_i32, [_vp, _P(_sz)]),
+    "dattri_token_scores": (_i32, [_vp, _vp, _i32, _i64, _i64, _vp, _vp, _i32, _i64, _vp, _sz, _vp]),
     "dattri_cosine_workspace_bytes": (_i32, [_i64, _i64, _i64, _i32, _i32, _i32, _i32, _P(_sz)]),
     "dattri_score_cosine": (_i32, [_vp, _i64, _i64, _vp, _i64, _i64, _i64, _i32, _vp, _vp, _i32, _vp, _vp,
                                    _vp, _sz, _vp]),
@@ -494,3 +497,16 @@ def dattri_get_mask(ctx, layer):
     cols = np.empty(m, dtype=np.int32)
     _check(load().dattri_get_mask(ctx, layer, rows.ctypes.data, cols.ctypes.data), "dattri_get_mask")
     return rows, cols
+
+
+def dattri_token_scores_workspace_bytes(ctx):
+    v = _sz()
+    _check(load().dattri_token_scores_workspace_bytes(ctx, ctypes.byref(v)), "dattri_token_scores_workspace_bytes")
+    return v.value
+
+
+def dattri_token_scores(ctx, phi_q, q_dtype, n_q, ld_q, scores, phi, phi_dtype, ld_phi, workspace, ws_bytes,
+                        stream=None):
+    _check(load().dattri_token_scores(ctx, _ptr(phi_q), q_dtype, n_q, ld_q, _ptr(scores), _ptr(phi), phi_dtype,
+                                      ld_phi, _ptr(workspace), ws_bytes, _stream(stream)),
+           "dattri_token_scores")

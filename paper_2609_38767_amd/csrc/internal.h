@@ -314,6 +314,21 @@ struct RowOp {
 };
 hipError_t launch_rowcov(const RowOp* ops, int n_ops, int max_items, float* parts, hipStream_t s);
 
+// Token-level scores: per layer, where its projected token rows sit (float32,
+// row (i*T + t) at rows + (i*T + t)*ld + col0) and where its block sits in the
+// query rows.  out[q][i][t] = sum over layers of a~_t^T R_q g~_t for t below
+// the layer's length of example i.
+struct TokTask {
+  const float* a_rows; const float* b_rows;
+  const int32_t* lengths;
+  int64_t a_ld, b_ld, q_off;
+  int32_t a_col0, b_col0, k_in, k_out;
+};
+constexpr int kTokTokens = 64;   // token positions per workgroup
+constexpr int kTokQueries = 4;   // queries per workgroup
+hipError_t launch_token_scores(const TokTask* tasks, int n_tasks, const void* phi_q, int q_bf16, int64_t ld_q,
+                               int64_t n_q, int64_t n, int T, float* out, hipStream_t s);
+
 // Symmetric eigendecomposition of sum / count (k x k, k <= kCurvMaxK).
 struct EigTask { int64_t sum_off, count_off, q_off, lam_off; int32_t k, pad0; };
 hipError_t launch_eigen(const EigTask* tasks, int n_tasks, uint8_t* state, hipStream_t s);

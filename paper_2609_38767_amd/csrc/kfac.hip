@@ -248,6 +248,66 @@ hipError_t launch_rowcov(const RowOp* ops, int n_ops, int max_items, float* part
   return hipGetLastError();
 }
 
+__device__ inline float load_elem(const void* p, int bf16, int64_t i);
+
+// ---------------------------------------------------- token-level scores
+// Workgroup (token chunk, example, query group): for every layer in order,
+// the query blocks (kTokQueries x k_in x k_out) and the chunk's projected rows
+// (kTokTokens x (k_in + k_out)) are staged in LDS; thread (q, t) adds
+// a~_t^T R_q g~_t to its register, so the sum over layers is in layer order.
+__global__ __launch_bounds__(256) void token_kernel(const TokTask* __restrict__ tasks, int n_tasks,
+                                                    const void* __restrict__ phi_q, int q_bf16, int64_t ld_q,
+                                                    int64_t n_q, int64_t n, int T, float* __restrict__ out) {
+  __shared__ __align__(16) float R[kTokQueries][kCurvMaxK * kCurvMaxK];
+  __shared__ __align__(16) float Ar[kTokTokens][kCurvMaxK + 1];
+  __shared__ __align__(16) float Br[kTokTokens][kCurvMaxK + 1];
+  const int tid = threadIdx.x;
+  const int t0 = blockIdx.x * kTokTokens;
+  const int64_t ex = blockIdx.y, q0 = (int64_t)blockIdx.z * kTokQueries;
+  const int tl = tid % kTokTokens, ql = tid / kTokTokens;  // 64 tokens x 4 queries
+  const int64_t q = q0 + ql;
+  float acc = 0.f;
+  for (int l = 0; l < n_tasks; ++l) {  // uniform trip count
+    const TokTask tk = tasks[l];
+    const int ki = tk.k_in, ko = tk.k_out;
+    int t_eff = T;
+    if (tk.lengths) t_eff = min(max(tk.lengths[ex], 0), T);
+    __syncthreads();  // the previous layer's readers are done
+    for (int e = tid; e < kTokQueries * ki * ko; e += 256) {
+      const int qq = e / (ki * ko), w = e - qq * (ki * ko);
+      const int64_t qrow = q0 + qq;
+      R[qq][w] = qrow < n_q ? load_elem(phi_q, q_bf16, qrow * ld_q + tk.q_off + w) : 0.f;
+    }
+    for (int e = tid; e < kTokTokens * ki; e += 256) {
+      const int t = e / ki, c = e - t * ki;
+      Ar[t][c] = t0 + t < t_eff ? tk.a_rows[(ex * T + t0 + t) * tk.a_ld + tk.a_col0 + c] : 0.f;
+    }
+    for (int e = tid; e < kTokTokens * ko; e += 256) {
+      const int t = e / ko, r = e - t * ko;
+      Br[t][r] = t0 + t < t_eff ? tk.b_rows[(ex * T + t0 + t) * tk.b_ld + tk.b_col0 + r] : 0.f;
+    }
+    __syncthreads();
+    float s = 0.f;
+    for (int c = 0; c < ki; ++c) {
+      float y = 0.f;
+      for (int r = 0; r < ko; ++r) y = fmaf(R[ql][c * ko + r], Br[tl][r], y);
+      s = fmaf(Ar[tl][c], y, s);
+    }
+    acc += s;
+  }
+  if (q < n_q && t0 + tl < T) out[(q * n + ex) * T + t0 + tl] = acc;
+}
+
+hipError_t launch_token_scores(const TokTask* tasks, int n_tasks, const void* phi_q, int q_bf16, int64_t ld_q,
+                               int64_t n_q, int64_t n, int T, float* out, hipStream_t s) {
+  if (n_tasks <= 0 || n_q <= 0 || n <= 0 || T <= 0) return hipSuccess;
+  const int64_t gx = (T + kTokTokens - 1) / kTokTokens, gz = (n_q + kTokQueries - 1) / kTokQueries;
+  if (n > 65535 || gz > 65535) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(token_kernel, dim3((unsigned)gx, (unsigned)n, (unsigned)gz), dim3(256), 0, s, tasks, n_tasks,
+                     phi_q, q_bf16, ld_q, n_q, n, T, out);
+  return hipGetLastError();
+}
+
 // ------------------------------------------------------------ eigensolver
 constexpr int kEigLd = kCurvMaxK + 1;  // float64 row pitch: column walks spread over banks
 constexpr int kEigSweeps = 32;

@@ -647,4 +647,104 @@ dattri_status dattri_project_and_fit(dattri_ctx* ctx, void* phi, dattri_dtype ph
   return DATTRI_OK;
 }
 
+// ---------------------------------------------------------- token scores
+// Workspace: [projection plan with rows kept][token tasks][phi when not given].
+struct TokPlan {
+  Plan proj;
+  std::vector<TokTask> tasks;
+  std::vector<std::pair<size_t, size_t>> rows_off;  // workspace offsets of each layer's A and B rows
+  size_t off_tasks = 0, off_phi = 0, total = 0;
+  int T = 0;
+};
+
+dattri_status plan_tokens(const dattri_ctx* ctx, TokPlan& K) {
+  dattri_status st = check_layers(ctx);
+  if (st != DATTRI_OK) return st;
+  for (size_t l = 0; l < ctx->layers.size(); ++l) {
+    const Layer& L = ctx->layers[l];
+    if (!L.bound) return fail(DATTRI_E_STATE, "layer %zu: projection maps not bound", l);
+    if (L.captured && L.T != ctx->layers[0].T)
+      return fail(DATTRI_E_SHAPE, "layer %zu captured with T=%d but layer 0 with T=%d", l, L.T, ctx->layers[0].T);
+  }
+  // every layer on the factored route, whose kernels form the projected rows
+  if ((st = build_plan(ctx, DATTRI_ROUTE_FACTORED, K.proj, true)) != DATTRI_OK) return st;
+  K.T = ctx->layers[0].T;
+  K.tasks.assign(ctx->layers.size(), TokTask{});
+  K.rows_off.assign(ctx->layers.size(), {0, 0});
+  for (const RowSrc& R : K.proj.row_srcs) {
+    TokTask& t = K.tasks[R.layer];
+    const Layer& L = ctx->layers[R.layer];
+    t.lengths = L.lengths;
+    t.q_off = L.offset;
+    t.k_in = L.k_in;
+    t.k_out = L.k_out;
+    if (R.side == 0) {
+      K.rows_off[R.layer].first = R.off;
+      t.a_ld = R.ld;
+      t.a_col0 = R.col0;
+    } else {
+      K.rows_off[R.layer].second = R.off;
+      t.b_ld = R.ld;
+      t.b_col0 = R.col0;
+    }
+  }
+  size_t off = align_up(K.proj.total);
+  K.off_tasks = off;
+  off = align_up(off + K.tasks.size() * sizeof(TokTask));
+  K.off_phi = off;
+  off = align_up(off + (size_t)ctx->layers[0].n * ctx->F * 4);
+  K.total = off;
+  return DATTRI_OK;
+}
+
+dattri_status dattri_token_scores_workspace_bytes(const dattri_ctx* ctx, size_t* bytes) {
+  reset_error();
+  if (!bytes) return fail(DATTRI_E_INVALID_ARG, "bytes is NULL");
+  TokPlan K;
+  dattri_status st = plan_tokens(ctx, K);
+  if (st != DATTRI_OK) return st;
+  *bytes = K.total;
+  return DATTRI_OK;
+}
+
+dattri_status dattri_token_scores(dattri_ctx* ctx, const void* phi_q, dattri_dtype q_dtype, int64_t n_q, int64_t ld_q,
+                                  float* scores, void* phi, dattri_dtype phi_dtype, int64_t ld_phi, void* workspace,
+                                  size_t ws_bytes, void* stream) {
+  reset_error();
+  TokPlan K;
+  dattri_status st = plan_tokens(ctx, K);
+  if (st != DATTRI_OK) return st;
+  if (q_dtype != DATTRI_F32 && q_dtype != DATTRI_BF16)
+    return fail(DATTRI_E_DTYPE, "query dtype %d is neither F32 nor BF16", (int)q_dtype);
+  if (phi && phi_dtype != DATTRI_F32 && phi_dtype != DATTRI_BF16)
+    return fail(DATTRI_E_DTYPE, "phi dtype %d is neither F32 nor BF16", (int)phi_dtype);
+  if (n_q < 0) return fail(DATTRI_E_INVALID_ARG, "n_q=%lld < 0", (long long)n_q);
+  if (ld_q < ctx->F) return fail(DATTRI_E_SHAPE, "ld_q=%lld < F=%lld", (long long)ld_q, (long long)ctx->F);
+  if (phi && ld_phi < ctx->F)
+    return fail(DATTRI_E_SHAPE, "ld_phi=%lld < F=%lld", (long long)ld_phi, (long long)ctx->F);
+  const int64_t n = ctx->layers[0].n;
+  if (n == 0 || n_q == 0 || K.T == 0) return DATTRI_OK;
+  if (!phi_q || !scores) return fail(DATTRI_E_INVALID_ARG, "phi_q or scores is NULL");
+  if (n > 65535 || (n_q + kTokQueries - 1) / kTokQueries > 65535)
+    return fail(DATTRI_E_UNSUPPORTED, "n=%lld examples or n_q=%lld queries beyond the grid limits", (long long)n,
+                (long long)n_q);
+  if ((st = check_ws(workspace, ws_bytes, K.total)) != DATTRI_OK) return st;
+  hipStream_t s = (hipStream_t)stream;
+  uint8_t* ws = (uint8_t*)workspace;
+  void* phi_out = phi ? phi : (void*)(ws + K.off_phi);
+  const dattri_dtype pd = phi ? phi_dtype : DATTRI_F32;
+  const int64_t pld = phi ? ld_phi : ctx->F;
+  if ((st = run_plan(ctx, K.proj, phi_out, pd, pld, workspace, ws_bytes, s)) != DATTRI_OK) return st;
+  std::vector<TokTask> tasks = K.tasks;
+  for (size_t l = 0; l < tasks.size(); ++l) {
+    tasks[l].a_rows = (const float*)(ws + K.rows_off[l].first);
+    tasks[l].b_rows = (const float*)(ws + K.rows_off[l].second);
+  }
+  HIP_TRY(upload(ctx, ws + K.off_tasks, {tasks.data()}, {0}, {tasks.size() * sizeof(TokTask)},
+                 tasks.size() * sizeof(TokTask), s));
+  HIP_TRY(launch_token_scores((const TokTask*)(ws + K.off_tasks), (int)tasks.size(), phi_q, q_dtype == DATTRI_BF16,
+                              ld_q, n_q, n, K.T, scores, s));
+  return DATTRI_OK;
+}
+
 }  // extern "C"

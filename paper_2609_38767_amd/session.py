@@ -22,7 +22,8 @@ from . import (DATTRI_BF16, DATTRI_F32, DATTRI_ROUTE_AUTO, dattri_bind_projectio
                dattri_curvature_eigen, dattri_curvature_ekfac_workspace_bytes,
                dattri_curvature_accumulate_ekfac, dattri_curvature_precondition,
                dattri_project_fit_workspace_bytes, dattri_project_and_fit, dattri_set_map_kind,
-               dattri_cosine_workspace_bytes, dattri_score_cosine, dattri_register_mask_layer)
+               dattri_cosine_workspace_bytes, dattri_score_cosine, dattri_register_mask_layer,
+               dattri_token_scores_workspace_bytes, dattri_token_scores)
 
 DTYPES = {"f32": (DATTRI_F32, torch.float32), "bf16": (DATTRI_BF16, torch.bfloat16)}
 
@@ -89,6 +90,21 @@ class ProjectionSession:
         ws = self.workspace(route)
         dattri_project_per_example(self.ctx, phi, code, phi.stride(0), ws, ws.numel(), route, stream)
         return phi
+
+    def token_scores(self, phi_q, n, phi_dtype="f32", stream=None):
+        """(scores [n_q, n, T] float32, phi) for the captures: per-token
+        contributions of every training example to its score against each
+        query row (GradDot rows, or rows preconditioned by a Curvature)."""
+        T = self._held[0][0].shape[1]
+        code, _ = DTYPES[phi_dtype]
+        q_code = DATTRI_BF16 if phi_q.dtype == torch.bfloat16 else DATTRI_F32
+        phi = feature_rows(n, self.F, phi_dtype, self.device)
+        scores = torch.empty((phi_q.shape[0], n, T), dtype=torch.float32, device=self.device)
+        need = dattri_token_scores_workspace_bytes(self.ctx)
+        ws = _dev_bytes(need, self.device)
+        dattri_token_scores(self.ctx, phi_q, q_code, phi_q.shape[0], phi_q.stride(0), scores, phi, code,
+                            phi.stride(0), ws, ws.numel(), stream)
+        return scores, phi
 
     def routes(self):
         return [dattri_layer_route(self.ctx, i) for i in range(len(self.layers))]

@@ -107,3 +107,14 @@ def test_ekfac_and_precondition_errors(ctx):
     assert _status(e) == "E_INVALID_ARG"
     # n_q = 0: valid and no work
     dt.dattri_curvature_precondition(ctx, FAKE, E, 0.1, 0.0, FAKE, 0, 0, F, FAKE, 0, F)
+
+
+def test_token_score_errors(ctx):
+    dt.dattri_register_layer(ctx, 64, 64, 8, 4)
+    with pytest.raises(dt.DattriError) as e:
+        dt.dattri_token_scores_workspace_bytes(ctx)
+    assert _status(e) == "E_STATE"  # maps not bound
+    dt.dattri_register_mask_layer(ctx, 64, 64, 16)
+    with pytest.raises(dt.DattriError) as e:
+        dt.dattri_token_scores(ctx, FAKE, 0, 1, 64, FAKE, None, 0, 0, FAKE, 1 << 20)
+    assert _status(e) == "E_UNSUPPORTED"  # mask layers have no projected rows

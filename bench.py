@@ -391,6 +391,21 @@ def curvature_case(dev, steps, warmup):
                                   "stage_ms": stages}
         print(f"[bench] curvature {method}: {wl['n_train'] / wall:.1f} seq/s ({wall * 1e3:.1f} ms); "
               + ", ".join(f"{k} {v:.2f} ms" for k, v in stages.items()), file=sys.stderr, flush=True)
+    # token-level scores of one batch against the EK-FAC-preconditioned query
+    # (projection with rows kept + the token kernel), App. D
+    tok_q = curv.precondition(phi_q, "ekfac", 0.1, 0.0, out=pq)
+    for _ in range(warmup):
+        train.token_scores(tok_q, n)
+    evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(steps)]
+    for a, b in evs:
+        a.record(stream)
+        train.token_scores(tok_q, n)
+        b.record(stream)
+    torch.cuda.synchronize()
+    out["token_scores"] = {"ms_per_batch": sorted(a.elapsed_time(b) for a, b in evs)[steps // 2],
+                           "shape": f"1 query x {n} sequences x {T} tokens, {len(layers)} layers"}
+    print(f"[bench] curvature token scores: {out['token_scores']['ms_per_batch']:.2f} ms per batch",
+          file=sys.stderr, flush=True)
     # the separate factor-sum pass over one batch (a second read of the batch)
     for _ in range(warmup):
         curv.accumulate_factors()

@@ -251,60 +251,127 @@ hipError_t launch_rowcov(const RowOp* ops, int n_ops, int max_items, float* part
 __device__ inline float load_elem(const void* p, int bf16, int64_t i);
 
 // ---------------------------------------------------- token-level scores
-// Workgroup (token chunk, example, query group): for every layer in order,
-// the query blocks (kTokQueries x k_in x k_out) and the chunk's projected rows
-// (kTokTokens x (k_in + k_out)) are staged in LDS; thread (q, t) adds
-// a~_t^T R_q g~_t to its register, so the sum over layers is in layer order.
+// Workgroup (64 token positions, example, QS query rows): every layer is
+// staged as zero-padded 64 x 64 tiles in LDS (the QS query blocks, the chunk's
+// a~ and g~ rows), loaded into registers one layer ahead so that the loads of
+// layer l + 1 are in flight while layer l is computed.  The 4 threads of a
+// token split into QS query slots of 4 / QS parts; a part holds g~_t in
+// registers and sums a~_t[c] (R g~_t)[c] over its share of c, reading rows of R
+// as broadcast float4.  Each part accumulates over all layers in layer order
+// and the parts are added in part order at the end (deterministic).
+constexpr int kTokPad = kCurvMaxK + 4;  // row stride of the a~ / g~ tiles (16-byte rows, no conflicts)
+
+template <int QS>
 __global__ __launch_bounds__(256) void token_kernel(const TokTask* __restrict__ tasks, int n_tasks,
                                                     const void* __restrict__ phi_q, int q_bf16, int64_t ld_q,
                                                     int64_t n_q, int64_t n, int T, float* __restrict__ out) {
-  __shared__ __align__(16) float R[kTokQueries][kCurvMaxK * kCurvMaxK];
-  __shared__ __align__(16) float Ar[kTokTokens][kCurvMaxK + 1];
-  __shared__ __align__(16) float Br[kTokTokens][kCurvMaxK + 1];
+  constexpr int K = kCurvMaxK, PER = K * K / 256, PARTS = 4 / QS;
+  __shared__ __align__(16) float R[QS][K * K];
+  __shared__ __align__(16) float Ar[kTokTokens][kTokPad];
+  __shared__ __align__(16) float Br[kTokTokens][kTokPad];
+  __shared__ float part_sum[4][kTokTokens];
   const int tid = threadIdx.x;
   const int t0 = blockIdx.x * kTokTokens;
-  const int64_t ex = blockIdx.y, q0 = (int64_t)blockIdx.z * kTokQueries;
-  const int tl = tid % kTokTokens, ql = tid / kTokTokens;  // 64 tokens x 4 queries
-  const int64_t q = q0 + ql;
-  float acc = 0.f;
-  for (int l = 0; l < n_tasks; ++l) {  // uniform trip count
+  const int64_t ex = blockIdx.y, q0 = (int64_t)blockIdx.z * QS;
+  const int tl = tid % kTokTokens, slot = tid / kTokTokens;  // slot is wave-uniform
+  const int ql = slot / PARTS, part = slot - ql * PARTS;
+
+  float rq[QS][PER], ra[PER], rb[PER];  // element e = tid + 256 j of each 64 x 64 tile
+  auto load = [&](int l) {
     const TokTask tk = tasks[l];
     const int ki = tk.k_in, ko = tk.k_out;
     int t_eff = T;
     if (tk.lengths) t_eff = min(max(tk.lengths[ex], 0), T);
+#pragma unroll
+    for (int j = 0; j < PER; ++j) {
+      const int e = tid + 256 * j, row = e / K, col = e % K;  // a~ / g~ tile: row = token, col = c or r
+      const bool tok = t0 + row < t_eff;
+      const int64_t base = (ex * T + t0 + row);
+      ra[j] = tok && col < ki ? tk.a_rows[base * tk.a_ld + tk.a_col0 + col] : 0.f;
+      rb[j] = tok && col < ko ? tk.b_rows[base * tk.b_ld + tk.b_col0 + col] : 0.f;
+#pragma unroll
+      for (int qq = 0; qq < QS; ++qq) {  // R tile: row = c, col = r
+        const int64_t qrow = q0 + qq;
+        rq[qq][j] = qrow < n_q && row < ki && col < ko
+                        ? load_elem(phi_q, q_bf16, qrow * ld_q + tk.q_off + (int64_t)row * ko + col)
+                        : 0.f;
+      }
+    }
+  };
+
+  float acc = 0.f;
+  if (n_tasks > 0) load(0);
+  for (int l = 0; l < n_tasks; ++l) {  // uniform trip count
+    const int ki = tasks[l].k_in;
     __syncthreads();  // the previous layer's readers are done
-    for (int e = tid; e < kTokQueries * ki * ko; e += 256) {
-      const int qq = e / (ki * ko), w = e - qq * (ki * ko);
-      const int64_t qrow = q0 + qq;
-      R[qq][w] = qrow < n_q ? load_elem(phi_q, q_bf16, qrow * ld_q + tk.q_off + w) : 0.f;
-    }
-    for (int e = tid; e < kTokTokens * ki; e += 256) {
-      const int t = e / ki, c = e - t * ki;
-      Ar[t][c] = t0 + t < t_eff ? tk.a_rows[(ex * T + t0 + t) * tk.a_ld + tk.a_col0 + c] : 0.f;
-    }
-    for (int e = tid; e < kTokTokens * ko; e += 256) {
-      const int t = e / ko, r = e - t * ko;
-      Br[t][r] = t0 + t < t_eff ? tk.b_rows[(ex * T + t0 + t) * tk.b_ld + tk.b_col0 + r] : 0.f;
+#pragma unroll
+    for (int j = 0; j < PER; ++j) {
+      const int e = tid + 256 * j, row = e / K, col = e % K;
+      Ar[row][col] = ra[j];
+      Br[row][col] = rb[j];
+#pragma unroll
+      for (int qq = 0; qq < QS; ++qq) R[qq][e] = rq[qq][j];
     }
     __syncthreads();
-    float s = 0.f;
-    for (int c = 0; c < ki; ++c) {
-      float y = 0.f;
-      for (int r = 0; r < ko; ++r) y = fmaf(R[ql][c * ko + r], Br[tl][r], y);
-      s = fmaf(Ar[tl][c], y, s);
+    if (l + 1 < n_tasks) load(l + 1);
+
+    float g[K];
+#pragma unroll
+    for (int r = 0; r < K; r += 4) {
+      const float4 v = *reinterpret_cast<const float4*>(&Br[tl][r]);
+      g[r] = v.x; g[r + 1] = v.y; g[r + 2] = v.z; g[r + 3] = v.w;
     }
-    acc += s;
+    // c in groups of 4 (the tiles are zero past k_in), split over the parts
+    const int n4 = (ki + 3) / 4;
+    const int c0 = 4 * (part * n4 / PARTS), c1 = 4 * ((part + 1) * n4 / PARTS);
+    const float* Rq = R[ql];
+    for (int c = c0; c < c1; c += 4) {
+      const float4 av = *reinterpret_cast<const float4*>(&Ar[tl][c]);
+      float y[4];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const float* Rr = Rq + (c + i) * K;
+        float y0 = 0.f, y1 = 0.f, y2 = 0.f, y3 = 0.f;
+#pragma unroll
+        for (int r = 0; r < K; r += 4) {
+          const float4 w = *reinterpret_cast<const float4*>(Rr + r);
+          y0 = fmaf(w.x, g[r], y0);
+          y1 = fmaf(w.y, g[r + 1], y1);
+          y2 = fmaf(w.z, g[r + 2], y2);
+          y3 = fmaf(w.w, g[r + 3], y3);
+        }
+        y[i] = (y0 + y1) + (y2 + y3);
+      }
+      acc = fmaf(av.x, y[0], acc);
+      acc = fmaf(av.y, y[1], acc);
+      acc = fmaf(av.z, y[2], acc);
+      acc = fmaf(av.w, y[3], acc);
+    }
   }
-  if (q < n_q && t0 + tl < T) out[(q * n + ex) * T + t0 + tl] = acc;
+  part_sum[slot][tl] = acc;
+  __syncthreads();
+  if (part == 0) {
+    float t = part_sum[slot][tl];
+#pragma unroll
+    for (int p = 1; p < PARTS; ++p) t += part_sum[slot + p][tl];
+    const int64_t q = q0 + ql;
+    if (q < n_q && t0 + tl < T) out[(q * n + ex) * T + t0 + tl] = t;
+  }
 }
 
 hipError_t launch_token_scores(const TokTask* tasks, int n_tasks, const void* phi_q, int q_bf16, int64_t ld_q,
                                int64_t n_q, int64_t n, int T, float* out, hipStream_t s) {
   if (n_tasks <= 0 || n_q <= 0 || n <= 0 || T <= 0) return hipSuccess;
-  const int64_t gx = (T + kTokTokens - 1) / kTokTokens, gz = (n_q + kTokQueries - 1) / kTokQueries;
+  const int QS = n_q >= kTokQueries ? kTokQueries : (n_q >= 2 ? 2 : 1);  // query slots per workgroup
+  const int64_t gx = (T + kTokTokens - 1) / kTokTokens, gz = (n_q + QS - 1) / QS;
   if (n > 65535 || gz > 65535) return hipErrorInvalidValue;
-  hipLaunchKernelGGL(token_kernel, dim3((unsigned)gx, (unsigned)n, (unsigned)gz), dim3(256), 0, s, tasks, n_tasks,
-                     phi_q, q_bf16, ld_q, n_q, n, T, out);
+  const dim3 grid((unsigned)gx, (unsigned)n, (unsigned)gz);
+  if (QS == 4)
+    hipLaunchKernelGGL(token_kernel<4>, grid, dim3(256), 0, s, tasks, n_tasks, phi_q, q_bf16, ld_q, n_q, n, T, out);
+  else if (QS == 2)
+    hipLaunchKernelGGL(token_kernel<2>, grid, dim3(256), 0, s, tasks, n_tasks, phi_q, q_bf16, ld_q, n_q, n, T, out);
+  else
+    hipLaunchKernelGGL(token_kernel<1>, grid, dim3(256), 0, s, tasks, n_tasks, phi_q, q_bf16, ld_q, n_q, n, T, out);
   return hipGetLastError();
 }
 

@@ -725,7 +725,7 @@ dattri_status dattri_token_scores(dattri_ctx* ctx, const void* phi_q, dattri_dty
   const int64_t n = ctx->layers[0].n;
   if (n == 0 || n_q == 0 || K.T == 0) return DATTRI_OK;
   if (!phi_q || !scores) return fail(DATTRI_E_INVALID_ARG, "phi_q or scores is NULL");
-  if (n > 65535 || (n_q + kTokQueries - 1) / kTokQueries > 65535)
+  if (n > 65535 || n_q > 65535)
     return fail(DATTRI_E_UNSUPPORTED, "n=%lld examples or n_q=%lld queries beyond the grid limits", (long long)n,
                 (long long)n_q);
   if ((st = check_ws(workspace, ws_bytes, K.total)) != DATTRI_OK) return st;

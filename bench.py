@@ -34,7 +34,7 @@ def parse():
     p.add_argument("--warmup", type=int, default=2)
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--phase", choices=["all", "project", "score", "routing", "gpt2", "crossgram", "curvature",
-                                       "fit", "mask", "copy"],
+                                       "fit", "mask", "copy", "probe"],
                    default="all")
     return p.parse_args()
 
@@ -518,8 +518,10 @@ def mask_case(dev, steps, warmup):
 
 
 def stream_reference(dev):
-    """Achievable HBM rate on this GPU: a 1 GiB device-to-device copy (read +
-    write bytes per second, best of 5)."""
+    """Measured denominators on this GPU (best of a few runs): a 1 GiB
+    device-to-device copy (read + write bytes per second), the library's read
+    probe over 4 GiB, and its bf16 MFMA probe (TFLOP/s under sustained matrix
+    load, clock throttling included)."""
     import torch
     stream = torch.cuda.current_stream()
     nbytes = 1 << 30
@@ -541,6 +543,22 @@ def stream_reference(dev):
     c_ms = best_ms(lambda: dst.copy_(src))
     out = {"copy_gbs": 2 * nbytes / c_ms / 1e6}
     del src, dst
+    # the library's probes: a pure read stream (non-temporal 16-byte loads)
+    # and back-to-back bf16 MFMA from registers
+    import paper_2609_38767_amd as dt
+    rbytes = 4 << 30
+    buf = torch.empty(rbytes, dtype=torch.uint8, device=dev).fill_(1)
+    wgs = 8192
+    sink = torch.empty(wgs * 256, dtype=torch.int32, device=dev)
+    r_ms = best_ms(lambda: dt.dattri_probe_read(buf, rbytes, sink, wgs, stream))
+    out["read_gbs"] = rbytes / r_ms / 1e6
+    del buf, sink
+    mw, iters = 2048, 20000
+    fsink = torch.empty(mw * 256, dtype=torch.float32, device=dev)
+    flops = dt.dattri_probe_mfma(fsink, mw, iters, stream)
+    m_ms = best_ms(lambda: dt.dattri_probe_mfma(fsink, mw, iters, stream), reps=3)
+    out["mfma_bf16_tflops"] = flops / (m_ms * 1e-3) / 1e12
+    del fsink
     torch.cuda.empty_cache()
     return out
 
@@ -695,7 +713,7 @@ def main():
                                  "kernel": "score GEMM (query scaling + NT GEMM), 2048 x 200000 x 8192, "
                                            f"feature rows {ld} elements apart"}
 
-    if args.phase == "all":
+    if args.phase in ("all", "project", "score", "fit", "probe"):
         out["hbm_reference"] = stream_reference(dev)
 
     line = {
@@ -712,8 +730,18 @@ def main():
         "score_gemm_tflops": out.get("score", {}).get("gemm_tflops"),
     }
     line.update({k: v for k, v in out.items()})
-    if "hbm_reference" in out and "roofline" in out:
-        line["roofline"]["frac_of_copy"] = line["roofline"]["achieved"] / out["hbm_reference"]["copy_gbs"]
+    ref = out.get("hbm_reference")
+    if ref and "roofline" in out:  # against the measured rates as well as the published peak
+        line["roofline"]["frac_of_copy"] = line["roofline"]["achieved"] / ref["copy_gbs"]
+        line["roofline"]["measured_peak"] = ref["read_gbs"]
+        line["roofline"]["frac_of_measured"] = line["roofline"]["achieved"] / ref["read_gbs"]
+    if ref and "roofline" in out.get("projection_fit", {}):
+        rf = line["projection_fit"]["roofline"]
+        rf["measured_peak"] = ref["read_gbs"]
+        rf["frac_of_measured"] = rf["achieved"] / ref["read_gbs"]
+    if ref and "roofline_score" in out:
+        line["roofline_score"]["measured_peak"] = ref["mfma_bf16_tflops"]
+        line["roofline_score"]["frac_of_measured"] = line["roofline_score"]["achieved"] / ref["mfma_bf16_tflops"]
     if not args.no_cpu_baseline and sess is not None:
         print("[bench] timing the oracle on host cores", file=sys.stderr, flush=True)
         line["cpu_baseline"] = cpu_baseline_projection(wl, inputs, wl["seed"])

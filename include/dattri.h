@@ -605,6 +605,31 @@ dattri_status dattri_token_scores(dattri_ctx* ctx, const void* phi_q, dattri_dty
                                   dattri_dtype phi_dtype, int64_t ld_phi, void* workspace,
                                   size_t ws_bytes, void* stream);
 
+/* ------------------------------------------------------ measurement probes */
+
+/* Measured roofline denominators (not part of the method): the rates a kernel
+ * of this library is also compared against, besides the published peaks.
+ *
+ * dattri_probe_read: one launch of `workgroups` x 256 threads that reads
+ * `bytes` of device memory at buf once (non-temporal 16-byte loads,
+ * grid-stride) and writes one int32 per thread to sink; time it on `stream`
+ * to get the achievable HBM read rate.
+ *   buf:  device, 16-byte aligned; bytes a positive multiple of 16
+ *   sink: device int32 [workgroups * 256] (caller-owned, contents unspecified)
+ * Errors: INVALID_ARG, HIP.
+ *
+ * dattri_probe_mfma: one launch of `workgroups` x 4 waves, each issuing
+ * iters x 8 independent bf16 MFMA 32x32x16 operations from registers (no
+ * memory traffic in the loop); *flops receives the launch's FLOP count
+ * (workgroups x 4 x iters x 8 x 32768).  Time it on `stream` to get the
+ * achievable dense bf16 matrix rate, clock throttling included.
+ *   sink: device float32 [workgroups * 256] (caller-owned, contents unspecified)
+ * Errors: INVALID_ARG (iters < 1, workgroups outside [1, 2^20]), HIP. */
+dattri_status dattri_probe_read(const void* buf, size_t bytes, int32_t* sink, int32_t workgroups,
+                                void* stream);
+dattri_status dattri_probe_mfma(float* sink, int32_t workgroups, int32_t iters, double* flops,
+                                void* stream);
+
 #ifdef __cplusplus
 }
 #endif

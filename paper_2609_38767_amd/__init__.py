@@ -36,6 +36,7 @@ __all__ = [
     "dattri_cosine_workspace_bytes", "dattri_score_cosine",
     "DATTRI_ROUTE_MASK", "dattri_register_mask_layer", "dattri_get_mask",
     "dattri_token_scores_workspace_bytes", "dattri_token_scores",
+    "dattri_probe_read", "dattri_probe_mfma",
 ]
 
 DATTRI_F32, DATTRI_BF16 = 0, 1
@@ -130,6 +131,8 @@ _SIGS = {
     "dattri_get_mask": (_i32, [_vp, _i32, _vp, _vp]),
     "dattri_token_scores_workspace_bytes": (_i32, [_vp, _P(_sz)]),
     "dattri_token_scores": (_i32, [_vp, _vp, _i32, _i64, _i64, _vp, _vp, _i32, _i64, _vp, _sz, _vp]),
+    "dattri_probe_read": (_i32, [_vp, _sz, _vp, _i32, _vp]),
+    "dattri_probe_mfma": (_i32, [_vp, _i32, _i32, _P(_dbl), _vp]),
     "dattri_cosine_workspace_bytes": (_i32, [_i64, _i64, _i64, _i32, _i32, _i32, _i32, _P(_sz)]),
     "dattri_score_cosine": (_i32, [_vp, _i64, _i64, _vp, _i64, _i64, _i64, _i32, _vp, _vp, _i32, _vp, _vp,
                                    _vp, _sz, _vp]),
@@ -510,3 +513,15 @@ def dattri_token_scores(ctx, phi_q, q_dtype, n_q, ld_q, scores, phi, phi_dtype, 
     _check(load().dattri_token_scores(ctx, _ptr(phi_q), q_dtype, n_q, ld_q, _ptr(scores), _ptr(phi), phi_dtype,
                                       ld_phi, _ptr(workspace), ws_bytes, _stream(stream)),
            "dattri_token_scores")
+
+
+def dattri_probe_read(buf, nbytes, sink, workgroups, stream=None):
+    _check(load().dattri_probe_read(_ptr(buf), nbytes, _ptr(sink), workgroups, _stream(stream)), "dattri_probe_read")
+
+
+def dattri_probe_mfma(sink, workgroups, iters, stream=None):
+    """Launch the MFMA probe; returns the launch's FLOP count."""
+    f = _dbl()
+    _check(load().dattri_probe_mfma(_ptr(sink), workgroups, iters, ctypes.byref(f), _stream(stream)),
+           "dattri_probe_mfma")
+    return f.value

@@ -307,22 +307,49 @@ dattri_status dattri::build_plan(const dattri_ctx* ctx, dattri_route forced, Pla
   }
   P.n_fact_tasks = (int)P.tasks.size();
   // One launch per kernel instance.  Inside a launch, every item of a group
-  // runs on one XCD (its projection maps then stay in that XCD's L2): groups
-  // are dealt, costliest first, to the least-loaded of 8 per-XCD queues, and
-  // the queues are interleaved so that position 8*s + x holds queue x's s-th
-  // item (workgroups are dispatched round-robin over the XCDs).  Short queues
-  // are padded with items that exit at once.
+  // runs on one XCD (its projection maps then stay in that XCD's L2).  Groups
+  // of one launch that read the same input block (layers kept apart above,
+  // e.g. q/k/v) form a unit: the unit goes to one XCD with its items
+  // interleaved per (example, chunk), so the workgroups that read the same A
+  // rows run side by side and share them through that XCD's L2.  Units are
+  // dealt by HBM bytes (A counted once), costliest first, to the
+  // least-loaded of 8 per-XCD queues, and the queues are interleaved so that
+  // position 8*s + x holds queue x's s-th item (workgroups are dispatched
+  // round-robin over the XCDs).  Short queues are padded with items that exit
+  // at once.
   for (const Inst& I : insts) {
-    std::vector<int> order = I.groups;
-    std::stable_sort(order.begin(), order.end(),
-                     [&](int a, int b) { return group_cost[a] > group_cost[b]; });
+    std::vector<std::vector<int>> units;
+    std::vector<double> unit_cost;
+    for (int g : I.groups) {
+      const FactGroup& G = P.groups[g];
+      size_t u = 0;
+      for (; u < units.size(); ++u) {
+        const FactGroup& H = P.groups[units[u][0]];
+        if (H.A == G.A && H.d_in == G.d_in && H.T == G.T && H.lengths == G.lengths &&
+            H.n_chunks == G.n_chunks && H.chunk_rows == G.chunk_rows)
+          break;
+      }
+      if (u == units.size()) {
+        units.push_back({});
+        unit_cost.push_back(0.0);
+      } else {
+        unit_cost[u] -= (double)n * G.T * G.d_in;  // the unit reads A once
+      }
+      units[u].push_back(g);
+      unit_cost[u] += group_cost[g];
+    }
+    std::vector<int> order(units.size());
+    for (size_t u = 0; u < units.size(); ++u) order[u] = (int)u;
+    std::stable_sort(order.begin(), order.end(), [&](int a, int b) { return unit_cost[a] > unit_cost[b]; });
     std::vector<std::vector<FactItem>> q(kXcds);
     double load[kXcds] = {0};
-    for (int g : order) {
+    for (int u : order) {
       const int x = (int)(std::min_element(load, load + kXcds) - load);
+      const FactGroup& H = P.groups[units[u][0]];
       for (int e = 0; e < n; ++e)
-        for (int c = 0; c < P.groups[g].n_chunks; ++c) q[x].push_back({g, e, c, 0});
-      load[x] += group_cost[g];
+        for (int c = 0; c < H.n_chunks; ++c)
+          for (int g : units[u]) q[x].push_back({g, e, c, 0});
+      load[x] += unit_cost[u];
     }
     size_t len = 0;
     for (const auto& v : q) len = std::max(len, v.size());

@@ -293,3 +293,21 @@ def test_factored_form_option(ctx):
     auto = dt.dattri_workspace_bytes(ctx, dt.DATTRI_ROUTE_FACTORED)
     assert split >= 4 * 64 * 32 * (64 + 64)
     assert auto == split  # few fused work items and T <= 128: AUTO takes the split form
+
+
+def test_probe_errors():
+    FAKE = 1 << 20
+    cases = [(lambda: dt.dattri_probe_read(None, 1024, FAKE, 4), "E_INVALID_ARG"),
+             (lambda: dt.dattri_probe_read(FAKE + 8, 1024, FAKE, 4), "E_INVALID_ARG"),
+             (lambda: dt.dattri_probe_read(FAKE, 1000, FAKE, 4), "E_INVALID_ARG"),
+             (lambda: dt.dattri_probe_read(FAKE, 0, FAKE, 4), "E_INVALID_ARG"),
+             (lambda: dt.dattri_probe_read(FAKE, 1024, None, 4), "E_INVALID_ARG"),
+             (lambda: dt.dattri_probe_read(FAKE, 1024, FAKE, 0), "E_INVALID_ARG"),
+             (lambda: dt.dattri_probe_mfma(None, 4, 10), "E_INVALID_ARG"),
+             (lambda: dt.dattri_probe_mfma(FAKE, 0, 10), "E_INVALID_ARG"),
+             (lambda: dt.dattri_probe_mfma(FAKE, 4, 0), "E_INVALID_ARG"),
+             (lambda: dt.dattri_probe_mfma(FAKE, (1 << 20) + 1, 10), "E_INVALID_ARG")]
+    for fn, want in cases:
+        with pytest.raises(dt.DattriError) as e:
+            fn()
+        assert _status(e) == want

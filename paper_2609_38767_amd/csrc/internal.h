@@ -210,21 +210,23 @@ hipError_t launch_fill_rows(float* K, int rows, int cols, int64_t ld, hipStream_
 // every thread sums the products of its entries; each item writes its entries'
 // partial sums at partial_base + ((example * n_chunks + chunk) * m + entry),
 // summed over chunks by the reduce kernel.
-constexpr int kMaskPerThread = 32;
+constexpr int kMaskPerThread = 64;
 constexpr int kMaskGroup = 256 * kMaskPerThread;   // entries per work item
 constexpr int64_t kMaskStageBudget = 40 * 1024;   // bytes of one stage (two stages per work item)
 struct MaskTask {
   const void* A; const void* B;      // [n, T, d_in], [n, T, d_out]
   const int32_t* lengths;            // [n] or null
-  const int32_t* rows;               // [m] output feature of each entry
-  const int32_t* cols;               // [m] input feature of each entry
+  const int32_t* rows;               // [m] output feature of the entry in each slot
+  const int32_t* cols;               // [m] input feature of the entry in each slot
+  const int32_t* pos;                // [m] index of that entry in mask order
   int32_t d_in, d_out, T, m;
   int32_t stage_tokens, chunk_tokens, n_chunks, aligned;  // aligned: 16-byte row blocks
   int64_t partial_base;
 };
 struct MaskItem { int32_t task, example, chunk, group; };  // task < 0: padding
-hipError_t launch_mask(int elt_bytes, int aligned, const MaskItem* items, int n_items, const MaskTask* tasks,
-                       size_t lds_bytes, float* partials, hipStream_t s);
+// full: every item's group holds kMaskGroup entries
+hipError_t launch_mask(int elt_bytes, int aligned, int full, const MaskItem* items, int n_items,
+                       const MaskTask* tasks, size_t lds_bytes, float* partials, hipStream_t s);
 
 // ---------------------------------------------------------------- scoring
 // dst rows ld_dst apart receive src rows (ld_src apart) times d, first F columns

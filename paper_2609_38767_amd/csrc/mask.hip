@@ -3,15 +3,22 @@
 // so the kept entries need |M| products per token position and DW is never
 // formed).
 //
-// One workgroup per (mask layer, example, token chunk, group of up to 8192
-// entries).  Each stage holds `stage_tokens` consecutive token rows of A and
-// of B: consecutive rows of an example are one contiguous block in HBM, so for
-// 16-byte rows the stage is moved by direct global-to-LDS loads (1 KiB per
-// wave instruction, no registers) into one of two buffers while the other is
-// gathered; rows that are not 16-byte multiples take a plain copy into one
-// buffer.  Every thread owns 32 entries (indices in registers) and adds
-// b[r_e] * a[c_e] for each staged token, in token order (deterministic); the
-// products of bf16 values are exact in float32.
+// One workgroup per (mask layer, example, token chunk, group of up to
+// kMaskGroup = 16384 entries).  Each stage holds `stage_tokens` consecutive
+// token rows of A and of B: consecutive rows of an example are one contiguous
+// block in HBM, so for 16-byte rows the stage is moved by direct global-to-LDS
+// loads (1 KiB per wave instruction, no registers) into one of two buffers
+// while the other is gathered; rows that are not 16-byte multiples take a
+// plain copy into one buffer.  Every thread owns 64 entries (each (r, c) pair
+// packed in one register) and adds b[r_e] * a[c_e] for each staged token, in
+// token order (deterministic); the products of bf16 values are exact in
+// float32.  Every group restages the chunk's token rows, so groups are made
+// as large as two waves per SIMD allow: ten masks of 8192 entries take 5
+// groups instead of 10.  The entries come in the slot order of the layer's
+// table, arranged at bind time so that the 32 lanes of a half-wave mostly
+// read distinct LDS banks, and each sum is written at the entry's position in
+// mask order.  Whole groups and the partial last group of a layer run in
+// separate launches (the partial one bounds its slots).
 #include "device_common.h"
 #include "internal.h"
 
@@ -59,8 +66,35 @@ __device__ inline void dma_block(const rsrc_t r, uint32_t off, int bytes, uint8_
     __builtin_amdgcn_raw_ptr_buffer_load_lds(r, LDS_PTR(dst + c * 1024), 16, off + c * 1024 + lane * 16, 0, 0, 0);
 }
 
-template <int ELT, bool AL>
-__global__ __launch_bounds__(256) void mask_kernel(const MaskItem* __restrict__ items,
+// acc[j] += b[r_j] * a[c_j] over the nt staged token rows (token order);
+// rc[j] = r_j << 16 | c_j.  FULL: every slot holds an entry.  Else the slots
+// j < 8 * ceil(nj / 8) are gathered (nj uniform over the workgroup, so each
+// block test is a scalar branch); lanes past the group's entries hold rc = 0
+// (element 0 of each staged row) and their sums are never stored.  The empty
+// asm keeps the unpacked offsets out of registers across tokens (they would
+// double the register footprint and halve the waves per SIMD).
+template <int ELT, bool FULL>
+__device__ __forceinline__ void gather_rows(const uint8_t* sa, const uint8_t* sb, int nt, int a_row, int b_row,
+                                            int nj, uint32_t (&rc)[kMaskPerThread],
+                                            float (&acc)[kMaskPerThread]) {
+  for (int t = 0; t < nt; ++t) {
+    const uint8_t* ar = sa + t * a_row;
+    const uint8_t* br = sb + t * b_row;
+#pragma unroll
+    for (int jb = 0; jb < kMaskPerThread; jb += 8) {
+      if (FULL || jb < nj) {
+#pragma unroll
+        for (int j = jb; j < jb + 8; ++j) {
+          asm volatile("" : "+v"(rc[j]));
+          acc[j] = fmaf(lds_elem<ELT>(br, (int)(rc[j] >> 16)), lds_elem<ELT>(ar, (int)(rc[j] & 0xFFFFu)), acc[j]);
+        }
+      }
+    }
+  }
+}
+
+template <int ELT, bool AL, bool FULL>
+__global__ __launch_bounds__(256, 2) void mask_kernel(const MaskItem* __restrict__ items,
                                                    const MaskTask* __restrict__ tasks,
                                                    float* __restrict__ partials) {
   extern __shared__ __align__(1024) uint8_t stage[];
@@ -72,13 +106,15 @@ __global__ __launch_bounds__(256) void mask_kernel(const MaskItem* __restrict__ 
   if (M.lengths) t_eff = min(max(M.lengths[ex], 0), M.T);
   const int t0 = it.chunk * M.chunk_tokens, t1 = min(t_eff, t0 + M.chunk_tokens);
   const int e0 = it.group * kMaskGroup, ne = min(kMaskGroup, M.m - e0);
-  int ra[kMaskPerThread], ca[kMaskPerThread];
+  const int nj = (ne + 255) / 256;  // slots per thread holding entries (uniform)
+  // entry (r, c) packed as r << 16 | c (both below 2^16: a staged token row
+  // of A and B fits in LDS)
+  uint32_t rc[kMaskPerThread];
   float acc[kMaskPerThread];
 #pragma unroll
   for (int j = 0; j < kMaskPerThread; ++j) {
     const int e = tid + 256 * j;
-    ra[j] = e < ne ? M.rows[e0 + e] : 0;
-    ca[j] = e < ne ? M.cols[e0 + e] : 0;
+    rc[j] = e < ne ? ((uint32_t)M.rows[e0 + e] << 16) | (uint32_t)M.cols[e0 + e] : 0u;
     acc[j] = 0.f;
   }
   const int TS = M.stage_tokens;
@@ -87,13 +123,7 @@ __global__ __launch_bounds__(256) void mask_kernel(const MaskItem* __restrict__ 
   const uint8_t* gb = (const uint8_t*)M.B + ((int64_t)ex * M.T) * b_row;
 
   auto gather = [&](const uint8_t* sa, const uint8_t* sb, int nt) {
-    for (int t = 0; t < nt; ++t) {
-      const uint8_t* ar = sa + t * a_row;
-      const uint8_t* br = sb + t * b_row;
-#pragma unroll
-      for (int j = 0; j < kMaskPerThread; ++j)
-        if (tid + 256 * j < ne) acc[j] = fmaf(lds_elem<ELT>(br, ra[j]), lds_elem<ELT>(ar, ca[j]), acc[j]);
-    }
+    gather_rows<ELT, FULL>(sa, sb, nt, a_row, b_row, nj, rc, acc);
   };
 
   if (AL) {
@@ -130,34 +160,41 @@ __global__ __launch_bounds__(256) void mask_kernel(const MaskItem* __restrict__ 
       gather(sa, sb, nt);
     }
   }
-  float* dst = partials + M.partial_base + ((int64_t)ex * M.n_chunks + it.chunk) * M.m + e0;
+  float* dst = partials + M.partial_base + ((int64_t)ex * M.n_chunks + it.chunk) * M.m;
 #pragma unroll
   for (int j = 0; j < kMaskPerThread; ++j)
-    if (tid + 256 * j < ne) dst[tid + 256 * j] = acc[j];
+    if (tid + 256 * j < ne) dst[M.pos[e0 + tid + 256 * j]] = acc[j];
 }
 
-hipError_t launch_mask(int elt, int aligned, const MaskItem* items, int n_items, const MaskTask* tasks,
-                       size_t lds_bytes, float* partials, hipStream_t s) {
-  if (n_items <= 0) return hipSuccess;
-  const dim3 grid((unsigned)n_items), block(256);
+template <int ELT, bool AL, bool FULL>
+static hipError_t launch_mask_t(const MaskItem* items, int n_items, const MaskTask* tasks, size_t lds_bytes,
+                                float* partials, hipStream_t s) {
   if (lds_bytes > 64 * 1024) {  // dynamic LDS beyond 64 KiB must be allowed per kernel
-    const void* fn = elt == 2 ? (aligned ? (const void*)mask_kernel<2, true> : (const void*)mask_kernel<2, false>)
-                              : (aligned ? (const void*)mask_kernel<4, true> : (const void*)mask_kernel<4, false>);
-    const hipError_t e = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds_bytes);
+    const hipError_t e = hipFuncSetAttribute((const void*)mask_kernel<ELT, AL, FULL>,
+                                             hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds_bytes);
     if (e != hipSuccess) return e;
   }
-  if (elt == 2) {
-    if (aligned)
-      hipLaunchKernelGGL((mask_kernel<2, true>), grid, block, lds_bytes, s, items, tasks, partials);
-    else
-      hipLaunchKernelGGL((mask_kernel<2, false>), grid, block, lds_bytes, s, items, tasks, partials);
-  } else {
-    if (aligned)
-      hipLaunchKernelGGL((mask_kernel<4, true>), grid, block, lds_bytes, s, items, tasks, partials);
-    else
-      hipLaunchKernelGGL((mask_kernel<4, false>), grid, block, lds_bytes, s, items, tasks, partials);
-  }
+  hipLaunchKernelGGL((mask_kernel<ELT, AL, FULL>), dim3((unsigned)n_items), dim3(256), lds_bytes, s, items, tasks,
+                     partials);
   return hipGetLastError();
+}
+
+hipError_t launch_mask(int elt, int aligned, int full, const MaskItem* items, int n_items, const MaskTask* tasks,
+                       size_t lds_bytes, float* partials, hipStream_t s) {
+  if (n_items <= 0) return hipSuccess;
+#define DATTRI_MASK_CASE(E, A, F) \
+  if (elt == E && (bool)aligned == A && (bool)full == F) \
+    return launch_mask_t<E, A, F>(items, n_items, tasks, lds_bytes, partials, s);
+  DATTRI_MASK_CASE(2, true, true)
+  DATTRI_MASK_CASE(2, true, false)
+  DATTRI_MASK_CASE(2, false, true)
+  DATTRI_MASK_CASE(2, false, false)
+  DATTRI_MASK_CASE(4, true, true)
+  DATTRI_MASK_CASE(4, true, false)
+  DATTRI_MASK_CASE(4, false, true)
+  DATTRI_MASK_CASE(4, false, false)
+#undef DATTRI_MASK_CASE
+  return hipErrorInvalidValue;
 }
 
 }  // namespace dattri

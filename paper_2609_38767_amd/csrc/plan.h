@@ -48,7 +48,7 @@ struct Plan {
   // mask layers (gathered DW entries)
   std::vector<MaskTask> mtasks;
   std::vector<MaskItem> mitems;
-  struct MaskLaunch { int aligned, first, count; };
+  struct MaskLaunch { int aligned, full, first, count; };  // full: every item a whole entry group
   std::vector<MaskLaunch> mlaunches;
   std::vector<ReduceTask> mreduce;
   int mask_max_out = 0;

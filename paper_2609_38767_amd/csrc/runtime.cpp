@@ -552,6 +552,7 @@ dattri_status dattri::build_plan(const dattri_ctx* ctx, dattri_route forced, Pla
       M.A = L.A; M.B = L.B; M.lengths = L.lengths;
       M.rows = (const int32_t*)L.P_in;
       M.cols = (const int32_t*)L.P_in + L.k_out;
+      M.pos = (const int32_t*)L.P_in + 2 * (int64_t)L.k_out;
       M.d_in = L.d_in; M.d_out = L.d_out; M.T = L.T; M.m = L.k_out;
       M.stage_tokens = (int)std::max<int64_t>(1, std::min<int64_t>(16, kMaskStageBudget / row_bytes));
       const int64_t tc = (L.T + want_chunks - 1) / want_chunks;
@@ -584,29 +585,34 @@ dattri_status dattri::build_plan(const dattri_ctx* ctx, dattri_route forced, Pla
     // run together and share the rows through that XCD's L2.  Chunks are dealt
     // to the least-loaded of 8 per-XCD queues and the queues interleaved
     // (workgroup i runs on XCD i mod 8); short queues are padded.
-    for (int al = 1; al >= 0; --al) {
-      std::vector<std::vector<MaskItem>> q(kXcds);
-      int64_t load[kXcds] = {0};
-      for (size_t t = 0; t < P.mtasks.size(); ++t) {
-        const MaskTask& M = P.mtasks[t];
-        if (M.aligned != al) continue;
-        const int groups = (M.m + kMaskGroup - 1) / kMaskGroup;
-        for (int e = 0; e < n; ++e)
-          for (int c = 0; c < M.n_chunks; ++c) {
-            const int x = (int)(std::min_element(load, load + kXcds) - load);
-            for (int g = 0; g < groups; ++g) q[x].push_back({(int)t, e, c, g});
-            load[x] += groups;
-          }
+    // One launch per (alignment, whole groups or not): a whole group of
+    // kMaskGroup entries takes the gather without slot bounds.
+    for (int al = 1; al >= 0; --al)
+      for (int full = 1; full >= 0; --full) {
+        std::vector<std::vector<MaskItem>> q(kXcds);
+        int64_t load[kXcds] = {0};
+        for (size_t t = 0; t < P.mtasks.size(); ++t) {
+          const MaskTask& M = P.mtasks[t];
+          if (M.aligned != al) continue;
+          const int whole = M.m / kMaskGroup, groups = (M.m + kMaskGroup - 1) / kMaskGroup;
+          const int g0 = full ? 0 : whole, g1 = full ? whole : groups;
+          if (g1 <= g0) continue;
+          for (int e = 0; e < n; ++e)
+            for (int c = 0; c < M.n_chunks; ++c) {
+              const int x = (int)(std::min_element(load, load + kXcds) - load);
+              for (int g = g0; g < g1; ++g) q[x].push_back({(int)t, e, c, g});
+              load[x] += g1 - g0;
+            }
+        }
+        size_t len = 0;
+        for (const auto& v : q) len = std::max(len, v.size());
+        const int first = (int)P.mitems.size();
+        for (size_t i = 0; i < len; ++i)
+          for (int x = 0; x < kXcds; ++x)
+            P.mitems.push_back(i < q[x].size() ? q[x][i] : MaskItem{-1, 0, 0, 0});
+        const int count = (int)P.mitems.size() - first;
+        if (count) P.mlaunches.push_back({al, full, first, count});
       }
-      size_t len = 0;
-      for (const auto& v : q) len = std::max(len, v.size());
-      const int first = (int)P.mitems.size();
-      for (size_t i = 0; i < len; ++i)
-        for (int x = 0; x < kXcds; ++x)
-          P.mitems.push_back(i < q[x].size() ? q[x][i] : MaskItem{-1, 0, 0, 0});
-      const int count = (int)P.mitems.size() - first;
-      if (count) P.mlaunches.push_back({al, first, count});
-    }
     P.maskpart_bytes = mask_floats * 4;
   }
 
@@ -671,6 +677,91 @@ dattri_status check_layer(const dattri_ctx* ctx, int32_t layer) {
   if (layer < 0 || layer >= (int32_t)ctx->layers.size())
     return fail(DATTRI_E_INVALID_ARG, "layer %d out of range [0, %zu)", layer, ctx->layers.size());
   return DATTRI_OK;
+}
+
+// Device entry table of a mask layer: [rows | cols | pos], int32, m each.
+// Entries are placed into the gather kernel's slots group by group (groups of
+// kMaskGroup entries in mask order; slot e of a group is read by thread
+// e % 256 at step e / 256, so slots 32h .. 32h + 31 form the half-wave h of
+// one LDS read).  Inside a group, each entry goes to the first half-wave
+// where neither its A word nor its B word meets another word in the same
+// bank (32 banks of 4 bytes; a word already there is read once for all its
+// lanes), else one where one of the two does not, else any with room; so
+// most gathers are free of bank conflicts.  pos[slot] is the entry's index in
+// mask order, where the kernel writes its sum.
+void mask_slot_table(const std::vector<int32_t>& rows, const std::vector<int32_t>& cols, int d_in, int d_out,
+                     int elt, std::vector<int32_t>& table) {
+  const int m = (int)rows.size();
+  table.assign((size_t)3 * m, 0);
+  int32_t* t_rows = table.data();
+  int32_t* t_cols = table.data() + m;
+  int32_t* t_pos = table.data() + 2 * (size_t)m;
+  constexpr int kHalf = 32, kMaxHalves = kMaskGroup / kHalf, kW = kMaxHalves / 64;
+  struct Bits {
+    uint64_t w[kW];
+  };
+  auto first = [](const Bits& x) {
+    for (int i = 0; i < kW; ++i)
+      if (x.w[i]) return i * 64 + __builtin_ctzll(x.w[i]);
+    return -1;
+  };
+  // per factor side: word -> index into `holders` (the half-waves holding that word)
+  std::vector<int32_t> slot_of[2] = {std::vector<int32_t>((size_t)(((int64_t)d_in * elt + 3) / 4), -1),
+                                     std::vector<int32_t>((size_t)(((int64_t)d_out * elt + 3) / 4), -1)};
+  std::vector<Bits> holders[2];
+  std::vector<int32_t> touched[2];
+  for (int e0 = 0; e0 < m; e0 += kMaskGroup) {
+    const int N = std::min(kMaskGroup, m - e0), H = (N + kHalf - 1) / kHalf;
+    Bits all{};
+    for (int h = 0; h < H; ++h) all.w[h >> 6] |= 1ull << (h & 63);
+    Bits free_bank[2][kHalf], room = all;
+    for (int side = 0; side < 2; ++side)
+      for (int b = 0; b < kHalf; ++b) free_bank[side][b] = all;
+    int fill[kMaxHalves] = {0};
+    for (int i = 0; i < N; ++i) {
+      const int32_t word[2] = {(int32_t)(((int64_t)cols[e0 + i] * elt) >> 2),
+                               (int32_t)(((int64_t)rows[e0 + i] * elt) >> 2)};
+      Bits ok[2];
+      for (int side = 0; side < 2; ++side) {
+        ok[side] = free_bank[side][word[side] % kHalf];
+        const int32_t hs = slot_of[side][word[side]];
+        if (hs >= 0)
+          for (int k = 0; k < kW; ++k) ok[side].w[k] |= holders[side][hs].w[k];
+      }
+      Bits both, one;
+      for (int k = 0; k < kW; ++k) {
+        both.w[k] = ok[0].w[k] & ok[1].w[k] & room.w[k];
+        one.w[k] = (ok[0].w[k] | ok[1].w[k]) & room.w[k];
+      }
+      int h = first(both);
+      if (h < 0) h = first(one);
+      if (h < 0) h = first(room);
+      const uint64_t bit = 1ull << (h & 63);
+      const int slot = h * kHalf + fill[h]++;
+      if (fill[h] == std::min(kHalf, N - h * kHalf)) room.w[h >> 6] &= ~bit;
+      for (int side = 0; side < 2; ++side) {
+        Bits& fb = free_bank[side][word[side] % kHalf];
+        if (fb.w[h >> 6] & bit) {  // the bank was empty: this word now holds it
+          fb.w[h >> 6] &= ~bit;
+          int32_t& hs = slot_of[side][word[side]];
+          if (hs < 0) {
+            hs = (int32_t)holders[side].size();
+            holders[side].push_back(Bits{});
+            touched[side].push_back(word[side]);
+          }
+          holders[side][hs].w[h >> 6] |= bit;
+        }
+      }
+      t_rows[e0 + slot] = rows[e0 + i];
+      t_cols[e0 + slot] = cols[e0 + i];
+      t_pos[e0 + slot] = e0 + i;
+    }
+    for (int side = 0; side < 2; ++side) {  // reset the word index for the next group
+      for (int32_t w : touched[side]) slot_of[side][w] = -1;
+      touched[side].clear();
+      holders[side].clear();
+    }
+  }
 }
 
 void logical_map(const dattri_ctx* ctx, int layer, int side, std::vector<float>& out) {
@@ -757,7 +848,7 @@ dattri_status dattri::run_plan(dattri_ctx* ctx, const Plan& P, void* phi, dattri
   if (!P.mtasks.empty()) {
     float* kpart = (float*)(ws + P.off_maskpart);
     for (const Plan::MaskLaunch& L : P.mlaunches)
-      HIP_TRY(launch_mask(ctx->elt, L.aligned, (const MaskItem*)(ws + P.off_mitems) + L.first, L.count,
+      HIP_TRY(launch_mask(ctx->elt, L.aligned, L.full, (const MaskItem*)(ws + P.off_mitems) + L.first, L.count,
                           (const MaskTask*)(ws + P.off_mtasks), P.mask_lds, kpart, s));
     HIP_TRY(launch_reduce((const ReduceTask*)(ws + P.off_mreduce), (int)P.mreduce.size(), n, P.mask_max_out,
                           kpart, phi, phi_bf16, ld_phi, s));
@@ -907,8 +998,8 @@ dattri_status dattri_projection_bytes(const dattri_ctx* ctx, int32_t layer, size
   dattri_status st = check_layer(ctx, layer);
   if (st != DATTRI_OK) return st;
   const Layer& L = ctx->layers[layer];
-  if (L.mask_size > 0) {  // the mask's entry table: rows then cols, int32
-    if (bytes_in) *bytes_in = (size_t)8 * L.k_out;
+  if (L.mask_size > 0) {  // the mask's entry table: rows, cols and output positions, int32
+    if (bytes_in) *bytes_in = (size_t)12 * L.k_out;
     if (bytes_out) *bytes_out = 0;
     return DATTRI_OK;
   }
@@ -929,10 +1020,9 @@ dattri_status dattri_bind_projection(dattri_ctx* ctx, int32_t layer, void* dev_P
     if ((uintptr_t)dev_P_in % 16) return fail(DATTRI_E_INVALID_ARG, "device table pointer must be 16-byte aligned");
     if (host_P_in_override || host_P_out_override)
       return fail(DATTRI_E_INVALID_ARG, "mask layers take no map overrides");
-    std::vector<int32_t> r, c;
+    std::vector<int32_t> r, c, table;
     mask_entries(derive_mask_seed(ctx->seed, layer), L.d_in, L.d_out, L.mask_size, L.mask_id, L.mask_count, r, c);
-    std::vector<int32_t> table(r);
-    table.insert(table.end(), c.begin(), c.end());
+    mask_slot_table(r, c, L.d_in, L.d_out, ctx->elt, table);
     hipStream_t s = (hipStream_t)stream;
     HIP_TRY(hipMemcpyAsync(dev_P_in, table.data(), table.size() * 4, hipMemcpyHostToDevice, s));
     HIP_TRY(hipStreamSynchronize(s));

@@ -142,17 +142,19 @@ def test_rademacher_maps(dtype, route, form):
 MASKED = [dict(name="m0", d_in=300, d_out=128, k_in=1, k_out=512, mask_size=512, mask_id=0, a_group="ma"),
           dict(name="m1", d_in=300, d_out=128, k_in=1, k_out=1536, mask_size=512, mask_id=3, mask_count=3,
                a_group="ma"),
-          dict(name="m2", d_in=200, d_out=100, k_in=1, k_out=9000, mask_size=9000, mask_id=0, a_group="mb"),
+          dict(name="m2", d_in=256, d_out=256, k_in=1, k_out=30000, mask_size=30000, mask_id=0, a_group="mb"),
           dict(name="m3", d_in=37, d_out=21, k_in=1, k_out=100, mask_size=100, mask_id=1, a_group="mc"),
+          dict(name="m4", d_in=257, d_out=255, k_in=1, k_out=30000, mask_size=30000, mask_id=0, a_group="md"),
           dict(name="x", d_in=64, d_out=48, k_in=8, k_out=8, a_group="xa")]
 
 
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
 @pytest.mark.parametrize("route", ["auto", "materialized"])
 def test_mask_layers(dtype, route):
-    # App. A.2 random masks: DW entries gathered from the factors; two entry
-    # groups (m = 9000), an unaligned layer (37 x 21), ragged lengths over
-    # several token chunks, an ordinary layer beside them (its route forced)
+    # App. A.2 random masks: DW entries gathered from the factors; a whole
+    # entry group plus a partial one (m = 30000, aligned and unaligned rows),
+    # a small unaligned layer (37 x 21), ragged lengths over several token
+    # chunks, an ordinary layer beside them (its route forced)
     from oracle import mask as om
     wl = dict(W.WORKLOADS["tiny"], dist_a="normal", dist_b="normal", seed=31)
     n, T = 4, 300
@@ -163,7 +165,7 @@ def test_mask_layers(dtype, route):
         s.capture(li, A, B, lengths)
     phi = s.project(n, route=ROUTES[route])
     torch.cuda.synchronize()
-    assert [r[0] for r in s.routes()[:4]] == [dt.DATTRI_ROUTE_MASK] * 4
+    assert [r[0] for r in s.routes()[:5]] == [dt.DATTRI_ROUTE_MASK] * 5
     lens = lengths.cpu().numpy()
     got = host64(phi)
     assert np.count_nonzero(got[1]) == 0  # length 0

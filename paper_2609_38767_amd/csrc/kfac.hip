@@ -251,46 +251,54 @@ hipError_t launch_rowcov(const RowOp* ops, int n_ops, int max_items, float* part
 __device__ inline float load_elem(const void* p, int bf16, int64_t i);
 
 // ---------------------------------------------------- token-level scores
-// Workgroup (64 token positions, example, QS query rows): every layer is
-// staged as zero-padded 64 x 64 tiles in LDS (the QS query blocks, the chunk's
-// a~ and g~ rows), loaded into registers one layer ahead so that the loads of
-// layer l + 1 are in flight while layer l is computed.  The 4 threads of a
-// token split into QS query slots of 4 / QS parts; a part holds g~_t in
-// registers and sums a~_t[c] (R g~_t)[c] over its share of c, reading rows of R
-// as broadcast float4.  Each part accumulates over all layers in layer order
-// and the parts are added in part order at the end (deterministic).
+// Workgroup (TT token positions, example, QS query rows): every layer is
+// staged as zero-padded tiles in LDS (the QS query blocks of 64 x 64, the
+// chunk's TT x 64 a~ and g~ rows), loaded into registers one layer ahead so
+// that the loads of layer l + 1 are in flight while layer l is computed.  The
+// 256 / TT threads of a token split into QS query slots of PARTS parts; a part
+// holds g~_t in registers and sums a~_t[c] (R g~_t)[c] over its share of c,
+// reading rows of R as broadcast float4.  Each part accumulates over all
+// layers in layer order and the parts are added in part order at the end
+// (deterministic).  One query row takes TT = 32 (twice the workgroups, so two
+// share a CU and hide each other's per-layer load latency).
 constexpr int kTokPad = kCurvMaxK + 4;  // row stride of the a~ / g~ tiles (16-byte rows, no conflicts)
 
-template <int QS>
-__global__ __launch_bounds__(256) void token_kernel(const TokTask* __restrict__ tasks, int n_tasks,
+template <int QS, int TT>
+__global__ __launch_bounds__(256, QS == 1 ? 2 : 1) void token_kernel(const TokTask* __restrict__ tasks, int n_tasks,
                                                     const void* __restrict__ phi_q, int q_bf16, int64_t ld_q,
                                                     int64_t n_q, int64_t n, int T, float* __restrict__ out) {
-  constexpr int K = kCurvMaxK, PER = K * K / 256, PARTS = 4 / QS;
+  constexpr int K = kCurvMaxK, PER_Q = K * K / 256, PER_R = TT * K / 256;
+  constexpr int SLOTS = 256 / TT, PARTS = SLOTS / QS;
+  static_assert(SLOTS % QS == 0 && PER_R >= 1, "token tiling");
   __shared__ __align__(16) float R[QS][K * K];
-  __shared__ __align__(16) float Ar[kTokTokens][kTokPad];
-  __shared__ __align__(16) float Br[kTokTokens][kTokPad];
-  __shared__ float part_sum[4][kTokTokens];
+  __shared__ __align__(16) float Ar[TT][kTokPad];
+  __shared__ __align__(16) float Br[TT][kTokPad];
+  __shared__ float part_sum[SLOTS][TT];
   const int tid = threadIdx.x;
-  const int t0 = blockIdx.x * kTokTokens;
+  const int t0 = blockIdx.x * TT;
   const int64_t ex = blockIdx.y, q0 = (int64_t)blockIdx.z * QS;
-  const int tl = tid % kTokTokens, slot = tid / kTokTokens;  // slot is wave-uniform
+  const int tl = tid % TT, slot = tid / TT;  // uniform over each run of TT lanes (half a wave at TT = 32)
   const int ql = slot / PARTS, part = slot - ql * PARTS;
 
-  float rq[QS][PER], ra[PER], rb[PER];  // element e = tid + 256 j of each 64 x 64 tile
+  float rq[QS][PER_Q], ra[PER_R], rb[PER_R];  // element e = tid + 256 j of each tile
   auto load = [&](int l) {
     const TokTask tk = tasks[l];
     const int ki = tk.k_in, ko = tk.k_out;
     int t_eff = T;
     if (tk.lengths) t_eff = min(max(tk.lengths[ex], 0), T);
 #pragma unroll
-    for (int j = 0; j < PER; ++j) {
+    for (int j = 0; j < PER_R; ++j) {
       const int e = tid + 256 * j, row = e / K, col = e % K;  // a~ / g~ tile: row = token, col = c or r
       const bool tok = t0 + row < t_eff;
       const int64_t base = (ex * T + t0 + row);
       ra[j] = tok && col < ki ? tk.a_rows[base * tk.a_ld + tk.a_col0 + col] : 0.f;
       rb[j] = tok && col < ko ? tk.b_rows[base * tk.b_ld + tk.b_col0 + col] : 0.f;
+    }
 #pragma unroll
-      for (int qq = 0; qq < QS; ++qq) {  // R tile: row = c, col = r
+    for (int j = 0; j < PER_Q; ++j) {
+      const int e = tid + 256 * j, row = e / K, col = e % K;  // R tile: row = c, col = r
+#pragma unroll
+      for (int qq = 0; qq < QS; ++qq) {
         const int64_t qrow = q0 + qq;
         rq[qq][j] = qrow < n_q && row < ki && col < ko
                         ? load_elem(phi_q, q_bf16, qrow * ld_q + tk.q_off + (int64_t)row * ko + col)
@@ -305,13 +313,15 @@ __global__ __launch_bounds__(256) void token_kernel(const TokTask* __restrict__ 
     const int ki = tasks[l].k_in;
     __syncthreads();  // the previous layer's readers are done
 #pragma unroll
-    for (int j = 0; j < PER; ++j) {
+    for (int j = 0; j < PER_R; ++j) {
       const int e = tid + 256 * j, row = e / K, col = e % K;
       Ar[row][col] = ra[j];
       Br[row][col] = rb[j];
-#pragma unroll
-      for (int qq = 0; qq < QS; ++qq) R[qq][e] = rq[qq][j];
     }
+#pragma unroll
+    for (int j = 0; j < PER_Q; ++j)
+#pragma unroll
+      for (int qq = 0; qq < QS; ++qq) R[qq][tid + 256 * j] = rq[qq][j];
     __syncthreads();
     if (l + 1 < n_tasks) load(l + 1);
 
@@ -363,15 +373,19 @@ hipError_t launch_token_scores(const TokTask* tasks, int n_tasks, const void* ph
                                int64_t n_q, int64_t n, int T, float* out, hipStream_t s) {
   if (n_tasks <= 0 || n_q <= 0 || n <= 0 || T <= 0) return hipSuccess;
   const int QS = n_q >= kTokQueries ? kTokQueries : (n_q >= 2 ? 2 : 1);  // query slots per workgroup
-  const int64_t gx = (T + kTokTokens - 1) / kTokTokens, gz = (n_q + QS - 1) / QS;
+  const int TT = QS == 1 ? 32 : 64;                                      // token positions per workgroup
+  const int64_t gx = (T + TT - 1) / TT, gz = (n_q + QS - 1) / QS;
   if (n > 65535 || gz > 65535) return hipErrorInvalidValue;
   const dim3 grid((unsigned)gx, (unsigned)n, (unsigned)gz);
   if (QS == 4)
-    hipLaunchKernelGGL(token_kernel<4>, grid, dim3(256), 0, s, tasks, n_tasks, phi_q, q_bf16, ld_q, n_q, n, T, out);
+    hipLaunchKernelGGL((token_kernel<4, 64>), grid, dim3(256), 0, s, tasks, n_tasks, phi_q, q_bf16, ld_q, n_q, n, T,
+                       out);
   else if (QS == 2)
-    hipLaunchKernelGGL(token_kernel<2>, grid, dim3(256), 0, s, tasks, n_tasks, phi_q, q_bf16, ld_q, n_q, n, T, out);
+    hipLaunchKernelGGL((token_kernel<2, 64>), grid, dim3(256), 0, s, tasks, n_tasks, phi_q, q_bf16, ld_q, n_q, n, T,
+                       out);
   else
-    hipLaunchKernelGGL(token_kernel<1>, grid, dim3(256), 0, s, tasks, n_tasks, phi_q, q_bf16, ld_q, n_q, n, T, out);
+    hipLaunchKernelGGL((token_kernel<1, 32>), grid, dim3(256), 0, s, tasks, n_tasks, phi_q, q_bf16, ld_q, n_q, n, T,
+                       out);
   return hipGetLastError();
 }
 

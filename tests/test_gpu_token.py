@@ -44,8 +44,9 @@ def _sums_match(scores, phi_q, phi):
 
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
 @pytest.mark.parametrize("form", ["fused", "split"])
-def test_token_scores_against_oracle(dtype, form):
-    print(f"[token] dtype={dtype} form={form}", flush=True)
+@pytest.mark.parametrize("n_q", [6, 1])  # two query groups of 4 + 2; one query row (32 tokens per workgroup)
+def test_token_scores_against_oracle(dtype, form, n_q):
+    print(f"[token] dtype={dtype} form={form} n_q={n_q}", flush=True)
     lens = [150, 0, 64, 149, 1]
     n, T = len(lens), 150
     inputs = _inputs(LAYERS, n, T, dtype, seed=71)
@@ -54,7 +55,6 @@ def test_token_scores_against_oracle(dtype, form):
     for li, (A, B) in enumerate(inputs):
         s.capture(li, A, B, lengths)
     g = torch.Generator(device=DEV).manual_seed(75)
-    n_q = 6  # two query groups of the kernel
     phi_q = torch.randn((n_q, s.F), generator=g, device=DEV)
     scores, phi = s.token_scores(phi_q, n)
     torch.cuda.synchronize()

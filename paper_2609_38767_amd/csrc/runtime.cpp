@@ -479,18 +479,37 @@ dattri_status dattri::build_plan(const dattri_ctx* ctx, dattri_route forced, Pla
       P.slabsum.push_back(T);
       P.slabsum_max_n4 = std::max(P.slabsum_max_n4, T.n4);
     }
-    // one launch per kernel instance (aligned, tiles)
+    // One launch per kernel instance (aligned, tiles).  Inside a launch, the
+    // items of one op run on one XCD, so its projection map is fetched into
+    // that XCD's L2 once and read there by all its row blocks: ops are dealt,
+    // costliest first, to the least-loaded of 8 per-XCD queues and the queues
+    // interleaved (workgroup i runs on XCD i mod 8); short queues are padded
+    // with items that exit at once.
     for (int al = 1; al >= 0; --al)
       for (int nt : {1, 2, 4, 8}) {
-        const int first = (int)P.sitems.size();
-        for (size_t o = op0; o < P.sops.size(); ++o) {
+        std::vector<size_t> ops;
+        for (size_t o = op0; o < P.sops.size(); ++o)
+          if (P.sops[o].aligned == al && split_nt_instance(P.sops[o].nt) == nt) ops.push_back(o);
+        if (ops.empty()) continue;
+        auto cost = [&](size_t o) { return (double)P.sops[o].rows * P.sops[o].ld; };
+        std::stable_sort(ops.begin(), ops.end(), [&](size_t a, size_t b) { return cost(a) > cost(b); });
+        std::vector<std::vector<SplitItem>> q(kXcds);
+        double load[kXcds] = {0};
+        const int rows_wg = split_rows_of(nt);
+        for (size_t o : ops) {
           const SplitOp& O = P.sops[o];
-          if (O.aligned != al || split_nt_instance(O.nt) != nt) continue;
-          const int rows_wg = split_rows_of(nt);
+          const int x = (int)(std::min_element(load, load + kXcds) - load);
           const int rblocks = (O.rows + rows_wg - 1) / rows_wg;
           for (int rb = 0; rb < rblocks; ++rb)
-            for (int sl = 0; sl < O.n_slabs; ++sl) P.sitems.push_back({(int)o, rb, sl, 0});
+            for (int sl = 0; sl < O.n_slabs; ++sl) q[x].push_back({(int)o, rb, sl, 0});
+          load[x] += cost(o);
         }
+        size_t len = 0;
+        for (const auto& v : q) len = std::max(len, v.size());
+        const int first = (int)P.sitems.size();
+        for (size_t i = 0; i < len; ++i)
+          for (int x = 0; x < kXcds; ++x)
+            P.sitems.push_back(i < q[x].size() ? q[x][i] : SplitItem{-1, 0, 0, 0});
         const int count = (int)P.sitems.size() - first;
         if (count) P.slaunches.push_back({elt, al, nt, first, count});
       }

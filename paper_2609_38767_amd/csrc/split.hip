@@ -34,6 +34,7 @@ __global__ __launch_bounds__(256, 2) void split_project_kernel(const SplitItem* 
   constexpr int PD = 2;  // measured: deeper prefetch does not pay with 4 row tiles
   __shared__ __align__(16) uint8_t pan[2][kPanel][NT][kFragBytes];
   const SplitItem it = items[blockIdx.x];
+  if (it.op < 0) return;  // padding item of the XCD-interleaved order
   const SplitOp& O = ops[it.op];
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int g = lane >> 4, m16 = lane & 15;

@@ -481,28 +481,49 @@ dattri_status dattri::build_plan(const dattri_ctx* ctx, dattri_route forced, Pla
     }
     // One launch per kernel instance (aligned, tiles).  Inside a launch, the
     // items of one op run on one XCD, so its projection map is fetched into
-    // that XCD's L2 once and read there by all its row blocks: ops are dealt,
-    // costliest first, to the least-loaded of 8 per-XCD queues and the queues
-    // interleaved (workgroup i runs on XCD i mod 8); short queues are padded
-    // with items that exit at once.
+    // that XCD's L2 once and read there by all its row blocks: ops (units of
+    // ops over the same block) are dealt, costliest first, to the
+    // least-loaded of 8 per-XCD queues and the queues interleaved (workgroup i
+    // runs on XCD i mod 8); short queues are padded with items that exit at
+    // once.
     for (int al = 1; al >= 0; --al)
       for (int nt : {1, 2, 4, 8}) {
         std::vector<size_t> ops;
         for (size_t o = op0; o < P.sops.size(); ++o)
           if (P.sops[o].aligned == al && split_nt_instance(P.sops[o].nt) == nt) ops.push_back(o);
         if (ops.empty()) continue;
-        auto cost = [&](size_t o) { return (double)P.sops[o].rows * P.sops[o].ld; };
-        std::stable_sort(ops.begin(), ops.end(), [&](size_t a, size_t b) { return cost(a) > cost(b); });
+        // ops that stream the same block (the input of layers kept apart, e.g.
+        // q/k/v) form a unit whose items are interleaved per (row block,
+        // slab), so the side-by-side workgroups share its rows through L2
+        std::vector<std::vector<size_t>> units;
+        for (size_t o : ops) {
+          const SplitOp& O = P.sops[o];
+          size_t u = 0;
+          for (; u < units.size(); ++u) {
+            const SplitOp& H = P.sops[units[u][0]];
+            if (H.X == O.X && H.rows == O.rows && H.ld == O.ld && H.n_slabs == O.n_slabs &&
+                H.slab_cols == O.slab_cols)
+              break;
+          }
+          if (u == units.size()) units.push_back({});
+          units[u].push_back(o);
+        }
+        auto cost = [&](const std::vector<size_t>& u) {  // every op's workgroups stream the block
+          return (double)P.sops[u[0]].rows * P.sops[u[0]].ld * (double)u.size();
+        };
+        std::stable_sort(units.begin(), units.end(),
+                         [&](const std::vector<size_t>& a, const std::vector<size_t>& b) { return cost(a) > cost(b); });
         std::vector<std::vector<SplitItem>> q(kXcds);
         double load[kXcds] = {0};
         const int rows_wg = split_rows_of(nt);
-        for (size_t o : ops) {
-          const SplitOp& O = P.sops[o];
+        for (const auto& u : units) {
+          const SplitOp& O = P.sops[u[0]];
           const int x = (int)(std::min_element(load, load + kXcds) - load);
           const int rblocks = (O.rows + rows_wg - 1) / rows_wg;
           for (int rb = 0; rb < rblocks; ++rb)
-            for (int sl = 0; sl < O.n_slabs; ++sl) q[x].push_back({(int)o, rb, sl, 0});
-          load[x] += cost(o);
+            for (int sl = 0; sl < O.n_slabs; ++sl)
+              for (size_t o : u) q[x].push_back({(int)o, rb, sl, 0});
+          load[x] += cost(u);
         }
         size_t len = 0;
         for (const auto& v : q) len = std::max(len, v.size());

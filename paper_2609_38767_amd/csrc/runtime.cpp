@@ -312,7 +312,8 @@ dattri_status dattri::build_plan(const dattri_ctx* ctx, dattri_route forced, Pla
   // e.g. q/k/v) form a unit: the unit goes to one XCD with its items
   // interleaved per (example, chunk), so the workgroups that read the same A
   // rows run side by side and share them through that XCD's L2.  Units are
-  // dealt by HBM bytes (A counted once), costliest first, to the
+  // dealt by the bytes their workgroups stream (A counted per group: an L2
+  // hit still crosses from L2 to the CU), costliest first, to the
   // least-loaded of 8 per-XCD queues, and the queues are interleaved so that
   // position 8*s + x holds queue x's s-th item (workgroups are dispatched
   // round-robin over the XCDs).  Short queues are padded with items that exit
@@ -332,8 +333,6 @@ dattri_status dattri::build_plan(const dattri_ctx* ctx, dattri_route forced, Pla
       if (u == units.size()) {
         units.push_back({});
         unit_cost.push_back(0.0);
-      } else {
-        unit_cost[u] -= (double)n * G.T * G.d_in;  // the unit reads A once
       }
       units[u].push_back(g);
       unit_cost[u] += group_cost[g];

@@ -317,7 +317,8 @@ dattri_status dattri::build_plan(const dattri_ctx* ctx, dattri_route forced, Pla
   // least-loaded of 8 per-XCD queues, and the queues are interleaved so that
   // position 8*s + x holds queue x's s-th item (workgroups are dispatched
   // round-robin over the XCDs).  Short queues are padded with items that exit
-  // at once.
+  // at once.  Launches with fewer than 4 units per XCD spread their items over
+  // all XCDs instead (a few groups would otherwise leave XCDs idle).
   for (const Inst& I : insts) {
     std::vector<std::vector<int>> units;
     std::vector<double> unit_cost;
@@ -339,6 +340,19 @@ dattri_status dattri::build_plan(const dattri_ctx* ctx, dattri_route forced, Pla
     }
     std::vector<int> order(units.size());
     for (size_t u = 0; u < units.size(); ++u) order[u] = (int)u;
+    if (units.size() < (size_t)4 * kXcds) {
+      // too few units to keep every XCD busy with whole units: the items of a
+      // unit, interleaved as above, spread over all XCDs
+      const int first = (int)P.items.size();
+      for (int u : order) {
+        const FactGroup& H = P.groups[units[u][0]];
+        for (int e = 0; e < n; ++e)
+          for (int c = 0; c < H.n_chunks; ++c)
+            for (int g : units[u]) P.items.push_back({g, e, c, 0});
+      }
+      P.launches.push_back({elt, I.na, I.nb, I.aligned, first, (int)P.items.size() - first});
+      continue;
+    }
     std::stable_sort(order.begin(), order.end(), [&](int a, int b) { return unit_cost[a] > unit_cost[b]; });
     std::vector<std::vector<FactItem>> q(kXcds);
     double load[kXcds] = {0};
@@ -484,7 +498,8 @@ dattri_status dattri::build_plan(const dattri_ctx* ctx, dattri_route forced, Pla
     // ops over the same block) are dealt, costliest first, to the
     // least-loaded of 8 per-XCD queues and the queues interleaved (workgroup i
     // runs on XCD i mod 8); short queues are padded with items that exit at
-    // once.
+    // once.  Launches with fewer than 4 units per XCD keep the items in op
+    // order over all XCDs (a few wide layers would otherwise leave XCDs idle).
     for (int al = 1; al >= 0; --al)
       for (int nt : {1, 2, 4, 8}) {
         std::vector<size_t> ops;
@@ -507,6 +522,20 @@ dattri_status dattri::build_plan(const dattri_ctx* ctx, dattri_route forced, Pla
           if (u == units.size()) units.push_back({});
           units[u].push_back(o);
         }
+        const int rows_wg = split_rows_of(nt);
+        const int first = (int)P.sitems.size();
+        if (units.size() < (size_t)4 * kXcds) {
+          // too few units to keep every XCD busy with whole units: items in op
+          // order, spread over all XCDs
+          for (size_t o : ops) {
+            const SplitOp& O = P.sops[o];
+            const int rblocks = (O.rows + rows_wg - 1) / rows_wg;
+            for (int rb = 0; rb < rblocks; ++rb)
+              for (int sl = 0; sl < O.n_slabs; ++sl) P.sitems.push_back({(int)o, rb, sl, 0});
+          }
+          P.slaunches.push_back({elt, al, nt, first, (int)P.sitems.size() - first});
+          continue;
+        }
         auto cost = [&](const std::vector<size_t>& u) {  // every op's workgroups stream the block
           return (double)P.sops[u[0]].rows * P.sops[u[0]].ld * (double)u.size();
         };
@@ -514,7 +543,6 @@ dattri_status dattri::build_plan(const dattri_ctx* ctx, dattri_route forced, Pla
                          [&](const std::vector<size_t>& a, const std::vector<size_t>& b) { return cost(a) > cost(b); });
         std::vector<std::vector<SplitItem>> q(kXcds);
         double load[kXcds] = {0};
-        const int rows_wg = split_rows_of(nt);
         for (const auto& u : units) {
           const SplitOp& O = P.sops[u[0]];
           const int x = (int)(std::min_element(load, load + kXcds) - load);
@@ -526,7 +554,6 @@ dattri_status dattri::build_plan(const dattri_ctx* ctx, dattri_route forced, Pla
         }
         size_t len = 0;
         for (const auto& v : q) len = std::max(len, v.size());
-        const int first = (int)P.sitems.size();
         for (size_t i = 0; i < len; ++i)
           for (int x = 0; x < kXcds; ++x)
             P.sitems.push_back(i < q[x].size() ? q[x][i] : SplitItem{-1, 0, 0, 0});

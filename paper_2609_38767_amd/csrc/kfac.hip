@@ -192,7 +192,8 @@ constexpr int kRowTile = 64;  // token rows staged in LDS per step
 
 __global__ __launch_bounds__(256) void rowcov_kernel(const RowOp* __restrict__ ops,
                                                      float* __restrict__ parts) {
-  __shared__ __align__(16) float R[kRowTile * kCurvMaxK];
+  constexpr int K = kCurvMaxK, PER = kRowTile * K / 256;  // tile elements per thread
+  __shared__ __align__(16) float R[kRowTile * K];
   const RowOp o = ops[blockIdx.y];
   if ((int)blockIdx.x >= o.n_items) return;
   const int k = o.k, tid = threadIdx.x;
@@ -205,29 +206,49 @@ __global__ __launch_bounds__(256) void rowcov_kernel(const RowOp* __restrict__ o
   for (int i = 0; i < 4; ++i)
 #pragma unroll
     for (int j = 0; j < 4; ++j) acc[i][j] = 0.f;
-  for (int e = tid; e < kRowTile * kCurvMaxK; e += 256) R[e] = 0.f;  // columns >= k stay zero
   const int e0 = blockIdx.x * o.ex_per_item, e1 = min(o.n, e0 + o.ex_per_item);
-  for (int ex = e0; ex < e1; ++ex) {
-    int t_eff = o.T;
-    if (o.lengths) t_eff = min(max(o.lengths[ex], 0), o.T);
-    const float* base = o.rows + (int64_t)ex * o.T * o.ld + o.col0;
-    for (int t0 = 0; t0 < t_eff; t0 += kRowTile) {  // uniform trip count
-      const int nr = min(kRowTile, t_eff - t0);
-      __syncthreads();  // the previous tile's readers are done
-      for (int e = tid; e < kRowTile * k; e += 256) {
-        const int r = e / k, c = e - (e / k) * k;
-        R[r * kCurvMaxK + c] = r < nr ? base[(int64_t)(t0 + r) * o.ld + c] : 0.f;
-      }
-      __syncthreads();
-      if (active) {
-        for (int r = 0; r < nr; ++r) {
-          const f32x4 a = *(const f32x4*)(R + r * kCurvMaxK + c0);
-          const f32x4 b = *(const f32x4*)(R + r * kCurvMaxK + r0);
+  auto rows_of = [&](int ex) {
+    return o.lengths ? min(max(o.lengths[ex], 0), o.T) : o.T;
+  };
+  // tiles of kRowTile rows, example by example; the next tile is loaded into
+  // registers (zero past the example's rows and past column k) while the
+  // current one is summed
+  float st[PER];
+  auto load = [&](int ex, int t0) {
+    const int nr = min(kRowTile, rows_of(ex) - t0);
+    const float* base = o.rows + ((int64_t)ex * o.T + t0) * o.ld + o.col0;
 #pragma unroll
-          for (int i = 0; i < 4; ++i)
+    for (int j = 0; j < PER; ++j) {
+      const int e = tid + 256 * j, r = e / K, c = e % K;
+      st[j] = r < nr && c < k ? base[(int64_t)r * o.ld + c] : 0.f;
+    }
+  };
+  auto next = [&](int& ex, int& t0) {  // the tile after (ex, t0); ex == e1 when done
+    t0 += kRowTile;
+    while (ex < e1 && t0 >= rows_of(ex)) {
+      ++ex;
+      t0 = 0;
+    }
+  };
+  int ex = e0, t0 = -kRowTile;
+  next(ex, t0);
+  if (ex < e1) load(ex, t0);
+  while (ex < e1) {  // uniform trip count
+    const int nr = min(kRowTile, rows_of(ex) - t0);
+    __syncthreads();  // the previous tile's readers are done
 #pragma unroll
-            for (int j = 0; j < 4; ++j) acc[i][j] = fmaf(a[i], b[j], acc[i][j]);
-        }
+    for (int j = 0; j < PER; ++j) R[tid + 256 * j] = st[j];
+    __syncthreads();
+    next(ex, t0);
+    if (ex < e1) load(ex, t0);
+    if (active) {
+      for (int r = 0; r < nr; ++r) {
+        const f32x4 a = *(const f32x4*)(R + r * K + c0);
+        const f32x4 b = *(const f32x4*)(R + r * K + r0);
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+#pragma unroll
+          for (int j = 0; j < 4; ++j) acc[i][j] = fmaf(a[i], b[j], acc[i][j]);
       }
     }
   }

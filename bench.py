@@ -124,6 +124,41 @@ def cpu_baseline_projection(wl, inputs, seed, passes=3):
                       f"float64, {passes} passes ({t_total:.1f} s of oracle time)"}
 
 
+def cpu_baseline_score(Qd, Xd, d, topk, n_queries=64, chunk=25000):
+    """Time the oracle's scoring (float64 GEMM with the diagonal, then the
+    stable per-query top-k) on the first `n_queries` query rows against all
+    training rows.  Training rows are copied to the host and converted to
+    float64 in chunks outside the timer.  The whole workload's oracle time is
+    this sample's time times n_q / n_queries (an extrapolation)."""
+    import numpy as np
+    from threadpoolctl import threadpool_info
+    from oracle import scoring as osc
+    n_q, F = Qd.shape
+    n_t = Xd.shape[0]
+    Q64 = Qd[:n_queries].float().cpu().numpy().astype(np.float64)
+    d64 = d.double().cpu().numpy()
+    S = np.empty((n_queries, n_t))
+    t_gemm = 0.0
+    for c0 in range(0, n_t, chunk):
+        X64 = Xd[c0:c0 + chunk].float().cpu().numpy().astype(np.float64)
+        t0 = time.perf_counter()
+        S[:, c0:c0 + chunk] = osc.score(Q64, X64, d64)
+        t_gemm += time.perf_counter() - t0
+        del X64
+    t0 = time.perf_counter()
+    osc.topk(S, topk)
+    t_topk = time.perf_counter() - t0
+    threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+    flops = 2.0 * n_queries * n_t * F
+    scale = n_q / n_queries
+    return {"value": flops / t_gemm / 1e12, "unit": "TFLOP/s", "cores": threads, "kind": "oracle",
+            "sample": f"{n_queries} of {n_q} queries x {n_t} training rows x {F} features "
+                      f"({flops / 1e9:.0f} GFLOP float64, {t_gemm:.1f} s) plus top-{topk} ({t_topk:.1f} s)",
+            "sample_s": t_gemm + t_topk,
+            "extrapolated_full_s": (t_gemm + t_topk) * scale,
+            "extrapolation": f"x{scale:g} (all {n_q} queries), not measured"}
+
+
 def routing_cases(dev, steps, warmup):
     """Both forced routes and AUTO on the wide short-sequence layer (8192 ->
     28672, T=32, batch 64, k=64) and the two switch cases (a rank-8 adapter's
@@ -745,6 +780,8 @@ def main():
     if not args.no_cpu_baseline and sess is not None:
         print("[bench] timing the oracle on host cores", file=sys.stderr, flush=True)
         line["cpu_baseline"] = cpu_baseline_projection(wl, inputs, wl["seed"])
+        if "score" in out:  # the scoring half of the metric, on a bounded sample
+            line["cpu_baseline"]["score"] = cpu_baseline_score(Qd, Xd, d, swl["topk"])
     print(json.dumps(line), flush=True)
 
 

@@ -265,6 +265,28 @@ dattri_status dattri_project_per_example(dattri_ctx* ctx, void* phi, dattri_dtyp
                                          int64_t ld_phi, void* workspace, size_t ws_bytes,
                                          dattri_route route, void* stream);
 
+/* Launch tables kept on the device between calls (optional).  Every call that
+ * launches the projection kernels first puts its launch tables (work items,
+ * layer-group and reduction descriptors) on the device.  Without a plan
+ * buffer they are copied into the head of the call's workspace on every call.
+ * With one bound, each kind of table (projection; the curvature fit's row and
+ * factor-sum tables; EK-FAC; token scores; cross-Gram) has a slot in it, and a
+ * call whose table equals the one already in its slot (same captures, maps,
+ * route, form, cost model and workspace address) issues no host-to-device
+ * copy at all.  A table larger than the buffer takes the workspace path.
+ *   dev_plan: device, 256-byte aligned, `bytes` long; NULL unbinds.  The
+ *     library keeps the pointer: the buffer must stay valid and must not be
+ *     written by anything else while bound.  Calls that use it must be
+ *     ordered (one stream, or synchronized between streams), as for the
+ *     workspace.
+ * dattri_plan_bytes: bytes the projection's tables need for the current
+ * captures and route (a buffer of this size, or several times it for the
+ * other table kinds, suffices).
+ * Errors: INVALID_ARG (NULL ctx / bytes, misaligned buffer, unknown route),
+ * STATE (as dattri_workspace_bytes). */
+dattri_status dattri_bind_plan_buffer(dattri_ctx* ctx, void* dev_plan, size_t bytes);
+dattri_status dattri_plan_bytes(const dattri_ctx* ctx, dattri_route route, size_t* bytes);
+
 /* Materialized representation (Eq. (1)): G_i = B_i^T A_i = sum_t g_t a_t^T for
  * captured examples [ex_begin, ex_begin + ex_count) of one layer, written as
  * float32 G_out [ex_count, d_out, d_in] (device).  Needs no workspace.
@@ -274,23 +296,53 @@ dattri_status dattri_materialize_gradient(dattri_ctx* ctx, int32_t layer, int32_
 
 /* ------------------------------------------------------------- cost model */
 
-/* Rates of the MI355X time model.  Predicted time of a route for one layer
- * and n examples = sum over its kernels of
- *   max(flops / rate, bytes / bandwidth) + launch_us,
- * with exact integer FLOP and byte counts (dattri_layer_costs). */
+/* MI355X time model of the two routes (Sec. 3.2 "FLOP-aware routing", App. A.4:
+ * the cheaper exact route is taken per layer).  For one layer captured with n
+ * examples, in microseconds:
+ *   factored      = call_us + max(F_f / factored_tflops, B_f / factored_gbs)
+ *                   + launches_f * launch_us
+ *   materialized  = call_us + max(F_g / gradient_tflops, B_g / gradient_gbs)
+ *                   + max(F_p / gproject_tflops, B_p / gproject_gbs)
+ *                   + 3 * chunks_m * launch_us
+ * with the exact FLOP and byte counts of dattri_layer_costs times n (F_g, B_g
+ * the G = B^T A kernel: 2T d_in d_out FLOP, factor blocks read and G written;
+ * F_p, B_p the projection of G: the rest of the materialized FLOPs, G read).
+ * launches_f is the number of kernels the factored route runs for this layer
+ * alone: 2 in the fused form (projection + reduction), 3 to 5 in the split
+ * form (stage 1 per map width, slab sum, contraction, reduction), as the
+ * launch plan decides; chunks_m is the number of example chunks the G staging
+ * budget (2 GiB) needs, each running the gradient, G-projection and reduction
+ * kernels.  call_us is paid by both routes and does not change a decision.
+ * Ties go to the factored route.  Rates are effective ones, fitted on MI355X;
+ * they may not exceed the chip's published peaks (HBM 8000 GB/s, dense bf16
+ * MFMA 2500 TFLOP/s for the factored and gradient kernels, float32 MFMA
+ * 157.3 TFLOP/s for the G projection, which runs in float32). */
 typedef struct {
-  double factored_tflops;     /* effective MFMA rate of the fused factored kernel */
-  double factored_gbs;        /* effective HBM bandwidth of the fused factored kernel */
-  double gradient_tflops;     /* G = B^T A kernel */
+  double factored_tflops;     /* factored kernels (fused or split) */
+  double factored_gbs;
+  double gradient_tflops;     /* G = B^T A */
   double gradient_gbs;
-  double gproject_tflops;     /* P_out^T G P_in kernel (float32) */
+  double gproject_tflops;     /* P_out^T G P_in (float32) */
   double gproject_gbs;
   double launch_us;           /* per kernel launch */
+  double call_us;             /* per call, either route */
 } dattri_cost_model;
 
-/* Replace / read the context's cost model (all rates > 0, launch_us >= 0). */
+/* Replace / read the context's cost model.
+ * Errors: INVALID_ARG (NULL, a rate not finite or <= 0 or above its peak,
+ * launch_us or call_us negative or not finite). */
 dattri_status dattri_set_cost_model(dattri_ctx* ctx, const dattri_cost_model* model);
 dattri_status dattri_get_cost_model(const dattri_ctx* ctx, dattri_cost_model* model);
+
+/* Load the cost model from a calibration file: a JSON object whose member
+ * "model" is an object holding the eight fields of dattri_cost_model by name
+ * as numbers (the file `python -m paper_2609_38767_amd.calibrate --out FILE`
+ * writes; other members are ignored).  Host-only; reads the file once.  The
+ * context's model is unchanged on error.
+ * Errors: INVALID_ARG (NULL arguments, unreadable file, malformed JSON, no
+ * "model" object, a field missing or not a number, a value rejected as by
+ * dattri_set_cost_model). */
+dattri_status dattri_set_cost_calibration(dattri_ctx* ctx, const char* json_path);
 
 /* Exact per-example operation counts of a layer's two routes for T tokens
  * (any of the outputs may be NULL):
@@ -305,8 +357,11 @@ dattri_status dattri_layer_costs(const dattri_ctx* ctx, int32_t layer, int32_t T
                                  int64_t* factored_bytes, int64_t* materialized_bytes);
 
 /* Route the cost model picks for a layer given its current capture (n, T),
- * with both predicted times in microseconds (ties go to FACTORED).  A layer
- * whose k exceeds the factored kernel's limits always routes MATERIALIZED.
+ * with both predicted times in microseconds (ties go to FACTORED).  Each
+ * layer is decided on its own, as if it were projected alone (in a call over
+ * many layers the factored layers share their launches).  A layer whose k
+ * exceeds the factored kernel's limits (k_in > 128 or k_out > 64) always
+ * routes MATERIALIZED (its predicted factored time is infinite).
  * Errors: INVALID_ARG (bad layer), STATE (layer not captured). */
 dattri_status dattri_layer_route(const dattri_ctx* ctx, int32_t layer, dattri_route* chosen,
                                  double* pred_factored_us, double* pred_materialized_us);

@@ -62,7 +62,7 @@ class CostModel(ctypes.Structure):
     _fields_ = [("factored_tflops", ctypes.c_double), ("factored_gbs", ctypes.c_double),
                 ("gradient_tflops", ctypes.c_double), ("gradient_gbs", ctypes.c_double),
                 ("gproject_tflops", ctypes.c_double), ("gproject_gbs", ctypes.c_double),
-                ("launch_us", ctypes.c_double)]
+                ("launch_us", ctypes.c_double), ("call_us", ctypes.c_double)]
 
 
 class CrossgramCostModel(ctypes.Structure):
@@ -96,12 +96,15 @@ _SIGS = {
     "dattri_capture_layer": (_i32, [_vp, _i32, _vp, _vp, _i32, _i32, _vp]),
     "dattri_clear_captures": (_i32, [_vp]),
     "dattri_workspace_bytes": (_i32, [_vp, _i32, _P(_sz)]),
+    "dattri_plan_bytes": (_i32, [_vp, _i32, _P(_sz)]),
+    "dattri_bind_plan_buffer": (_i32, [_vp, _vp, _sz]),
     "dattri_set_factored_form": (_i32, [_vp, _i32]),
     "dattri_get_factored_form": (_i32, [_vp, _P(_i32)]),
     "dattri_project_per_example": (_i32, [_vp, _vp, _i32, _i64, _vp, _sz, _i32, _vp]),
     "dattri_materialize_gradient": (_i32, [_vp, _i32, _i32, _i32, _vp, _vp]),
     "dattri_set_cost_model": (_i32, [_vp, _P(CostModel)]),
     "dattri_get_cost_model": (_i32, [_vp, _P(CostModel)]),
+    "dattri_set_cost_calibration": (_i32, [_vp, ctypes.c_char_p]),
     "dattri_layer_costs": (_i32, [_vp, _i32, _i32, _P(_i64), _P(_i64), _P(_i64), _P(_i64)]),
     "dattri_layer_route": (_i32, [_vp, _i32, _P(_i32), _P(_dbl), _P(_dbl)]),
     "dattri_score_workspace_bytes": (_i32, [_i64, _i64, _i64, _i32, _i32, _i32, _i32, _P(_sz)]),
@@ -273,6 +276,19 @@ def dattri_workspace_bytes(ctx, route=DATTRI_ROUTE_AUTO):
     return b.value
 
 
+def dattri_plan_bytes(ctx, route=DATTRI_ROUTE_AUTO):
+    b = _sz()
+    _check(load().dattri_plan_bytes(ctx, route, ctypes.byref(b)), "dattri_plan_bytes")
+    return b.value
+
+
+def dattri_bind_plan_buffer(ctx, buf, nbytes=None):
+    """Bind a device buffer (tensor or address; None unbinds) for launch tables."""
+    if buf is not None and nbytes is None:
+        nbytes = buf.numel() * buf.element_size()
+    _check(load().dattri_bind_plan_buffer(ctx, _ptr(buf), nbytes or 0), "dattri_bind_plan_buffer")
+
+
 def dattri_set_factored_form(ctx, form):
     _check(load().dattri_set_factored_form(ctx, form), "dattri_set_factored_form")
 
@@ -298,6 +314,10 @@ def dattri_materialize_gradient(ctx, layer, ex_begin, ex_count, G_out, stream=No
 def dattri_set_cost_model(ctx, model):
     m = CostModel(**model) if isinstance(model, dict) else model
     _check(load().dattri_set_cost_model(ctx, ctypes.byref(m)), "dattri_set_cost_model")
+
+
+def dattri_set_cost_calibration(ctx, json_path):
+    _check(load().dattri_set_cost_calibration(ctx, os.fsencode(json_path)), "dattri_set_cost_calibration")
 
 
 def dattri_get_cost_model(ctx):

@@ -5,11 +5,27 @@
 
 #include <stdint.h>
 
+#include <memory>
+#include <utility>
 #include <vector>
 
 #include "dattri.h"
 
 namespace dattri {
+
+struct Plan;
+
+// Kinds of launch tables a call uploads; each has at most one slot in the
+// context's bound plan buffer.
+enum TableKind { kTabProj = 0, kTabFit, kTabFsum, kTabEkfac, kTabTok, kTabCross, kTabKinds };
+
+// One launch table resident in the bound plan buffer: where it sits, how much
+// room it has and the bytes last copied there.
+struct TableSlot {
+  int kind = -1;
+  size_t off = 0, cap = 0;
+  std::vector<uint8_t> bytes;
+};
 
 struct Layer {
   int32_t d_in = 0, d_out = 0, k_in = 0, k_out = 0;
@@ -40,9 +56,17 @@ struct dattri_ctx {
   dattri_cost_model cost;
   dattri_crossgram_cost_model xcost;
   dattri_factored_form form = DATTRI_FORM_AUTO;
-  std::vector<uint8_t> blob;     // host copy of the last uploaded projection plan
-  std::vector<uint8_t> xg_blob;  // host copy of the last uploaded cross-Gram plan
-  // host copy of the last uploaded curvature tables (uploads from calls that
-  // take the context as const)
-  mutable std::vector<uint8_t> curv_blob;
+  // host copy of the last launch table copied into a workspace (fallback
+  // path: no plan buffer bound, or a table larger than it); kept until the
+  // next such copy
+  mutable std::vector<uint8_t> blob;
+  // caller-bound device buffer holding launch tables between calls
+  // (dattri_bind_plan_buffer) and the tables resident in it
+  uint8_t* plan_buf = nullptr;
+  size_t plan_cap = 0;
+  mutable std::vector<dattri::TableSlot> slots;
+  mutable size_t slots_used = 0;
+  // projection plans of recent calls with the context state each was built
+  // from (captures, maps, route, form, cost model): an equal state reuses it
+  mutable std::vector<std::pair<std::vector<uint64_t>, std::shared_ptr<const dattri::Plan>>> plans;
 };

@@ -13,6 +13,7 @@
 #include "context.h"
 #include "dattri.h"
 #include "internal.h"
+#include "plan.h"
 
 using namespace dattri;
 
@@ -262,12 +263,13 @@ dattri_status run_xplan(dattri_ctx* a, dattri_ctx* b, const XPlan& P, bool diag,
   const int rows = na, cols = diag ? 1 : nb;
   bool wrote = false;
   if (!P.entries.empty()) {
-    a->xg_blob.assign(P.blob_bytes, 0);
-    std::memcpy(a->xg_blob.data() + P.off_entries, P.entries.data(), P.entries.size() * sizeof(GhostEntry));
-    std::memcpy(a->xg_blob.data() + P.off_tiles, P.tiles.data(), P.tiles.size() * sizeof(GhostTile));
-    HIP_TRY(hipMemcpyAsync(ws, a->xg_blob.data(), P.blob_bytes, hipMemcpyHostToDevice, s));
-    const GhostEntry* d_entries = (const GhostEntry*)(ws + P.off_entries);
-    const GhostTile* d_tiles = (const GhostTile*)(ws + P.off_tiles);
+    std::vector<uint8_t> blob(P.blob_bytes, 0);
+    std::memcpy(blob.data() + P.off_entries, P.entries.data(), P.entries.size() * sizeof(GhostEntry));
+    std::memcpy(blob.data() + P.off_tiles, P.tiles.data(), P.tiles.size() * sizeof(GhostTile));
+    uint8_t* tab = nullptr;
+    HIP_TRY(place_table(a, kTabCross, blob, ws, s, &tab));
+    const GhostEntry* d_entries = (const GhostEntry*)(tab + P.off_entries);
+    const GhostTile* d_tiles = (const GhostTile*)(tab + P.off_tiles);
     float* parts = (float*)(ws + P.off_parts);
     for (const XGroup& G : P.groups) {
       HIP_TRY(launch_ghost(elt, d_entries + G.e0, d_tiles + G.t0, G.t1 - G.t0, parts, s));

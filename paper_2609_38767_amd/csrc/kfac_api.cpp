@@ -251,7 +251,7 @@ dattri_status plan_fsum(const dattri_ctx* ctx, const CurvLayout& C, FsumPlan& P,
 constexpr int64_t kRowTargetItems = 2048;  // row-covariance workgroups aimed for
 
 struct FitPlan {
-  Plan proj;
+  std::shared_ptr<const Plan> proj;
   std::vector<RowOp> rops;       // .rows set at run time from rop_off
   std::vector<size_t> rop_off;   // workspace byte offset of each op's rows
   std::vector<StatTask> rtasks;
@@ -269,12 +269,12 @@ dattri_status plan_fit(const dattri_ctx* ctx, const CurvLayout& C, dattri_route 
     return fail(DATTRI_E_INVALID_ARG, "route %d unknown", (int)route);
   for (size_t l = 0; l < ctx->layers.size(); ++l)
     if (!ctx->layers[l].bound) return fail(DATTRI_E_STATE, "layer %zu: projection maps not bound", l);
-  if ((st = build_plan(ctx, route, F.proj, true)) != DATTRI_OK) return st;
+  if ((st = get_plan(ctx, route, true, &F.proj)) != DATTRI_OK) return st;
   const int32_t n = ctx->layers[0].n;
-  const int64_t n_ops = (int64_t)F.proj.row_srcs.size();
+  const int64_t n_ops = (int64_t)F.proj->row_srcs.size();
   const int epi = (int)std::max<int64_t>(1, cdiv((int64_t)n * n_ops, kRowTargetItems));
   size_t parts = 0;
-  for (const RowSrc& R : F.proj.row_srcs) {
+  for (const RowSrc& R : F.proj->row_srcs) {
     const Layer& L = ctx->layers[R.layer];
     const int k = R.side ? L.k_out : L.k_in;
     RowOp o;
@@ -300,11 +300,11 @@ dattri_status plan_fit(const dattri_ctx* ctx, const CurvLayout& C, dattri_route 
     F.rop_off.push_back(R.off);
     F.rtasks.push_back(t);
   }
-  if (!F.proj.mat_layers.empty()) {
-    if ((st = plan_fsum(ctx, C, F.mat, &F.proj.mat_layers)) != DATTRI_OK) return st;
+  if (!F.proj->mat_layers.empty()) {
+    if ((st = plan_fsum(ctx, C, F.mat, &F.proj->mat_layers)) != DATTRI_OK) return st;
     F.has_mat = true;
   }
-  size_t off = align_up(F.proj.total);
+  size_t off = align_up(F.proj->total);
   F.off_desc = off;
   F.off_rops = off;   off = align_up(off + F.rops.size() * sizeof(RowOp));
   F.off_rtasks = off; off = align_up(off + F.rtasks.size() * sizeof(StatTask));
@@ -374,16 +374,30 @@ dattri_status check_ws(const void* ws, size_t ws_bytes, size_t need) {
   return DATTRI_OK;
 }
 
-// Copies a host table into device memory on the stream, through a host buffer
-// kept in the context until the next upload.
-hipError_t upload(const dattri_ctx* ctx, void* dst, const std::vector<const void*>& srcs,
-                  const std::vector<size_t>& offs, const std::vector<size_t>& sizes, size_t total,
-                  hipStream_t s) {
-  std::vector<uint8_t>& blob = ctx->curv_blob;
-  blob.assign(total, 0);
+// Host tables gathered into one blob at the given byte offsets.
+std::vector<uint8_t> gather(const std::vector<const void*>& srcs, const std::vector<size_t>& offs,
+                            const std::vector<size_t>& sizes, size_t total) {
+  std::vector<uint8_t> blob(total, 0);
   for (size_t i = 0; i < srcs.size(); ++i)
     if (sizes[i]) std::memcpy(blob.data() + offs[i], srcs[i], sizes[i]);
-  return hipMemcpyAsync(dst, blob.data(), total, hipMemcpyHostToDevice, s);
+  return blob;
+}
+
+// Launch tables of one call on the device (the bound plan buffer, else
+// `fallback` in the workspace); *dev receives their base address.
+hipError_t put_tables(const dattri_ctx* ctx, TableKind kind, uint8_t* fallback, const std::vector<const void*>& srcs,
+                      const std::vector<size_t>& offs, const std::vector<size_t>& sizes, size_t total,
+                      hipStream_t s, uint8_t** dev) {
+  return place_table(ctx, kind, gather(srcs, offs, sizes, total), fallback, s, dev);
+}
+
+// Tables that live in the curvature state itself, copied to `dst` through a
+// host buffer kept in the context until the next copy.
+hipError_t copy_tables(const dattri_ctx* ctx, uint8_t* dst, const std::vector<const void*>& srcs,
+                       const std::vector<size_t>& offs, const std::vector<size_t>& sizes, size_t total,
+                       hipStream_t s) {
+  ctx->blob = gather(srcs, offs, sizes, total);
+  return hipMemcpyAsync(dst, ctx->blob.data(), total, hipMemcpyHostToDevice, s);
 }
 
 }  // namespace
@@ -453,17 +467,18 @@ dattri_status dattri_curvature_accumulate_factors(dattri_ctx* ctx, void* state, 
   if ((st = check_ws(workspace, ws_bytes, P.total)) != DATTRI_OK) return st;
   hipStream_t s = (hipStream_t)stream;
   uint8_t* ws = (uint8_t*)workspace;
-  HIP_TRY(upload(ctx, ws, {P.ops.data(), P.items.data(), P.tasks.data()},
-                 {P.off_ops, P.off_items, P.off_tasks},
-                 {P.ops.size() * sizeof(FsumOp), P.items.size() * sizeof(FsumItem),
-                  P.tasks.size() * sizeof(StatTask)},
-                 P.blob_bytes, s));
-  const FsumOp* d_ops = (const FsumOp*)(ws + P.off_ops);
-  const FsumItem* d_items = (const FsumItem*)(ws + P.off_items);
+  uint8_t* tab = nullptr;
+  HIP_TRY(put_tables(ctx, kTabFsum, ws, {P.ops.data(), P.items.data(), P.tasks.data()},
+                     {P.off_ops, P.off_items, P.off_tasks},
+                     {P.ops.size() * sizeof(FsumOp), P.items.size() * sizeof(FsumItem),
+                      P.tasks.size() * sizeof(StatTask)},
+                     P.blob_bytes, s, &tab));
+  const FsumOp* d_ops = (const FsumOp*)(tab + P.off_ops);
+  const FsumItem* d_items = (const FsumItem*)(tab + P.off_items);
   float* parts = (float*)(ws + P.off_parts);
   for (const FsumPlan::Launch& L : P.launches)
     HIP_TRY(launch_fsum(L.elt, L.aligned, L.nt, d_items + L.first, L.count, d_ops, parts, s));
-  HIP_TRY(launch_stat_reduce((const StatTask*)(ws + P.off_tasks), (int)P.tasks.size(), P.max_out, parts,
+  HIP_TRY(launch_stat_reduce((const StatTask*)(tab + P.off_tasks), (int)P.tasks.size(), P.max_out, parts,
                              (uint8_t*)state, s));
   return DATTRI_OK;
 }
@@ -490,8 +505,8 @@ dattri_status dattri_curvature_eigen(const dattri_ctx* ctx, void* state, void* s
   }
   hipStream_t s = (hipStream_t)stream;
   uint8_t* base = (uint8_t*)state;
-  HIP_TRY(upload(ctx, base + C.off_eig, {E.data()}, {0}, {E.size() * sizeof(EigTask)},
-                 E.size() * sizeof(EigTask), s));
+  HIP_TRY(copy_tables(ctx, base + C.off_eig, {E.data()}, {0}, {E.size() * sizeof(EigTask)},
+                      E.size() * sizeof(EigTask), s));
   HIP_TRY(launch_eigen((const EigTask*)(base + C.off_eig), (int)E.size(), base, s));
   return DATTRI_OK;
 }
@@ -531,12 +546,13 @@ dattri_status dattri_curvature_accumulate_ekfac(const dattri_ctx* ctx, void* sta
   if ((st = check_ws(workspace, ws_bytes, P.total)) != DATTRI_OK) return st;
   hipStream_t s = (hipStream_t)stream;
   uint8_t* ws = (uint8_t*)workspace;
-  HIP_TRY(upload(ctx, ws, {P.rot.data(), P.tasks.data()}, {P.off_rot, P.off_tasks},
-                 {P.rot.size() * sizeof(RotTask), P.tasks.size() * sizeof(StatTask)}, P.blob_bytes, s));
+  uint8_t* tab = nullptr;
+  HIP_TRY(put_tables(ctx, kTabEkfac, ws, {P.rot.data(), P.tasks.data()}, {P.off_rot, P.off_tasks},
+                     {P.rot.size() * sizeof(RotTask), P.tasks.size() * sizeof(StatTask)}, P.blob_bytes, s, &tab));
   float* parts = (float*)(ws + P.off_parts);
-  HIP_TRY(launch_ekfac((const RotTask*)(ws + P.off_rot), (int)P.rot.size(), P.max_blocks,
+  HIP_TRY(launch_ekfac((const RotTask*)(tab + P.off_rot), (int)P.rot.size(), P.max_blocks,
                        (const uint8_t*)state, phi, dtype == DATTRI_BF16, ld, n, P.rows_per_block, parts, s));
-  HIP_TRY(launch_stat_reduce((const StatTask*)(ws + P.off_tasks), (int)P.tasks.size(), P.max_out, parts,
+  HIP_TRY(launch_stat_reduce((const StatTask*)(tab + P.off_tasks), (int)P.tasks.size(), P.max_out, parts,
                              (uint8_t*)state, s));
   return DATTRI_OK;
 }
@@ -576,8 +592,8 @@ dattri_status dattri_curvature_precondition(const dattri_ctx* ctx, const void* s
   std::vector<RotTask> R = rot_tasks(ctx, C);
   hipStream_t s = (hipStream_t)stream;
   uint8_t* base = (uint8_t*)const_cast<void*>(state);
-  HIP_TRY(upload(ctx, base + C.off_rot, {R.data()}, {0}, {R.size() * sizeof(RotTask)},
-                 R.size() * sizeof(RotTask), s));
+  HIP_TRY(copy_tables(ctx, base + C.off_rot, {R.data()}, {0}, {R.size() * sizeof(RotTask)},
+                      R.size() * sizeof(RotTask), s));
   HIP_TRY(launch_precondition((const RotTask*)(base + C.off_rot), (int)R.size(), base, (int)kind, damping_rel,
                               damping_abs, phi_q, in_dtype == DATTRI_BF16, ld_q, n_q, out,
                               out_dtype == DATTRI_BF16, ld_out, s));
@@ -617,7 +633,7 @@ dattri_status dattri_project_and_fit(dattri_ctx* ctx, void* phi, dattri_dtype ph
   if ((st = check_ws(workspace, ws_bytes, F.total)) != DATTRI_OK) return st;
   hipStream_t s = (hipStream_t)stream;
   uint8_t* ws = (uint8_t*)workspace;
-  if ((st = run_plan(ctx, F.proj, phi, phi_dtype, ld_phi, workspace, ws_bytes, s)) != DATTRI_OK) return st;
+  if ((st = run_plan(ctx, *F.proj, phi, phi_dtype, ld_phi, workspace, ws_bytes, s)) != DATTRI_OK) return st;
   std::vector<RowOp> rops = F.rops;
   for (size_t i = 0; i < rops.size(); ++i) rops[i].rows = (const float*)(ws + F.rop_off[i]);
   std::vector<const void*> srcs = {rops.data(), F.rtasks.data()};
@@ -630,13 +646,14 @@ dattri_status dattri_project_and_fit(dattri_ctx* ctx, void* phi, dattri_dtype ph
     sizes.insert(sizes.end(), {F.mat.ops.size() * sizeof(FsumOp), F.mat.items.size() * sizeof(FsumItem),
                                F.mat.tasks.size() * sizeof(StatTask)});
   }
-  HIP_TRY(upload(ctx, ws + F.off_desc, srcs, offs, sizes, F.desc_bytes, s));
+  uint8_t* tab = nullptr;
+  HIP_TRY(put_tables(ctx, kTabFit, ws + F.off_desc, srcs, offs, sizes, F.desc_bytes, s, &tab));
   float* rparts = (float*)(ws + F.off_rparts);
-  HIP_TRY(launch_rowcov((const RowOp*)(ws + F.off_rops), (int)rops.size(), F.max_items, rparts, s));
-  HIP_TRY(launch_stat_reduce((const StatTask*)(ws + F.off_rtasks), (int)F.rtasks.size(), F.max_out, rparts,
-                             (uint8_t*)state, s));
+  HIP_TRY(launch_rowcov((const RowOp*)(tab + (F.off_rops - F.off_desc)), (int)rops.size(), F.max_items, rparts, s));
+  HIP_TRY(launch_stat_reduce((const StatTask*)(tab + (F.off_rtasks - F.off_desc)), (int)F.rtasks.size(), F.max_out,
+                             rparts, (uint8_t*)state, s));
   if (F.has_mat) {
-    const uint8_t* fd = ws + F.off_fdesc;
+    const uint8_t* fd = tab + (F.off_fdesc - F.off_desc);
     float* fparts = (float*)(ws + F.off_fparts);
     for (const FsumPlan::Launch& L : F.mat.launches)
       HIP_TRY(launch_fsum(L.elt, L.aligned, L.nt, (const FsumItem*)(fd + F.mat.off_items) + L.first, L.count,
@@ -650,7 +667,7 @@ dattri_status dattri_project_and_fit(dattri_ctx* ctx, void* phi, dattri_dtype ph
 // ---------------------------------------------------------- token scores
 // Workspace: [projection plan with rows kept][token tasks][phi when not given].
 struct TokPlan {
-  Plan proj;
+  std::shared_ptr<const Plan> proj;
   std::vector<TokTask> tasks;
   std::vector<std::pair<size_t, size_t>> rows_off;  // workspace offsets of each layer's A and B rows
   size_t off_tasks = 0, off_phi = 0, total = 0;
@@ -667,11 +684,11 @@ dattri_status plan_tokens(const dattri_ctx* ctx, TokPlan& K) {
       return fail(DATTRI_E_SHAPE, "layer %zu captured with T=%d but layer 0 with T=%d", l, L.T, ctx->layers[0].T);
   }
   // every layer on the factored route, whose kernels form the projected rows
-  if ((st = build_plan(ctx, DATTRI_ROUTE_FACTORED, K.proj, true)) != DATTRI_OK) return st;
+  if ((st = get_plan(ctx, DATTRI_ROUTE_FACTORED, true, &K.proj)) != DATTRI_OK) return st;
   K.T = ctx->layers[0].T;
   K.tasks.assign(ctx->layers.size(), TokTask{});
   K.rows_off.assign(ctx->layers.size(), {0, 0});
-  for (const RowSrc& R : K.proj.row_srcs) {
+  for (const RowSrc& R : K.proj->row_srcs) {
     TokTask& t = K.tasks[R.layer];
     const Layer& L = ctx->layers[R.layer];
     t.lengths = L.lengths;
@@ -688,7 +705,7 @@ dattri_status plan_tokens(const dattri_ctx* ctx, TokPlan& K) {
       t.b_col0 = R.col0;
     }
   }
-  size_t off = align_up(K.proj.total);
+  size_t off = align_up(K.proj->total);
   K.off_tasks = off;
   off = align_up(off + K.tasks.size() * sizeof(TokTask));
   K.off_phi = off;
@@ -734,15 +751,16 @@ dattri_status dattri_token_scores(dattri_ctx* ctx, const void* phi_q, dattri_dty
   void* phi_out = phi ? phi : (void*)(ws + K.off_phi);
   const dattri_dtype pd = phi ? phi_dtype : DATTRI_F32;
   const int64_t pld = phi ? ld_phi : ctx->F;
-  if ((st = run_plan(ctx, K.proj, phi_out, pd, pld, workspace, ws_bytes, s)) != DATTRI_OK) return st;
+  if ((st = run_plan(ctx, *K.proj, phi_out, pd, pld, workspace, ws_bytes, s)) != DATTRI_OK) return st;
   std::vector<TokTask> tasks = K.tasks;
   for (size_t l = 0; l < tasks.size(); ++l) {
     tasks[l].a_rows = (const float*)(ws + K.rows_off[l].first);
     tasks[l].b_rows = (const float*)(ws + K.rows_off[l].second);
   }
-  HIP_TRY(upload(ctx, ws + K.off_tasks, {tasks.data()}, {0}, {tasks.size() * sizeof(TokTask)},
-                 tasks.size() * sizeof(TokTask), s));
-  HIP_TRY(launch_token_scores((const TokTask*)(ws + K.off_tasks), (int)tasks.size(), phi_q, q_dtype == DATTRI_BF16,
+  uint8_t* tab = nullptr;
+  HIP_TRY(put_tables(ctx, kTabTok, ws + K.off_tasks, {tasks.data()}, {0}, {tasks.size() * sizeof(TokTask)},
+                     tasks.size() * sizeof(TokTask), s, &tab));
+  HIP_TRY(launch_token_scores((const TokTask*)tab, (int)tasks.size(), phi_q, q_dtype == DATTRI_BF16,
                               ld_q, n_q, n, K.T, scores, s));
   return DATTRI_OK;
 }

@@ -7,6 +7,7 @@
 #include <stddef.h>
 #include <stdint.h>
 
+#include <memory>
 #include <vector>
 
 #include "context.h"
@@ -73,6 +74,17 @@ struct Plan {
 // `rows`, fused factored members also keep their projected token rows in the
 // workspace and row_srcs lists where every factored layer side's rows sit.
 dattri_status build_plan(const dattri_ctx* ctx, dattri_route forced, Plan& P, bool rows);
+// The same plan, reused when the context state it depends on (layer sizes,
+// captures, bound maps, factored form, cost model) and the arguments equal
+// those of a recent call; otherwise built and remembered.
+dattri_status get_plan(const dattri_ctx* ctx, dattri_route forced, bool rows, std::shared_ptr<const Plan>* out);
+
+// Puts a launch table on the device.  With a plan buffer bound that can hold
+// it, the table goes to its kind's slot there, and no copy is issued when that
+// slot already holds the same bytes; otherwise it is copied to `fallback` (the
+// head of the call's workspace).  *dev receives the table's device address.
+hipError_t place_table(const dattri_ctx* ctx, TableKind kind, const std::vector<uint8_t>& blob,
+                       uint8_t* fallback, hipStream_t s, uint8_t** dev);
 // Validates phi / workspace arguments against a plan, uploads its descriptors
 // and launches every kernel.  n = the captures' example count.
 dattri_status run_plan(dattri_ctx* ctx, const Plan& P, void* phi, dattri_dtype phi_dtype, int64_t ld_phi,

@@ -49,19 +49,38 @@ bool factored_supported(const Layer& L) {
 }
 
 dattri_cost_model default_cost_model() {
-  // Effective rates measured on MI355X (bf16 inputs): both routes timed on a
-  // sweep of 22 single-layer shapes (transformer, adapter-shaped and narrow
-  // layers, T = 16..2048) and fitted by least squares on log time.  Small
-  // problems are dominated by the fixed per-call cost, which launch_us absorbs.
+  // Effective rates measured on MI355X (bf16 inputs): both forced routes and
+  // the G kernel alone timed on a sweep of single-layer shapes (transformer,
+  // adapter-shaped and narrow layers, T = 16..2048) with the launch plans
+  // kept on the device, fitted with every rate held below its peak.
   dattri_cost_model m;
   m.factored_tflops = 297.0;
-  m.factored_gbs = 972.0;
+  m.factored_gbs = 4700.0;
   m.gradient_tflops = 726.0;
-  m.gradient_gbs = 8460.0;
+  m.gradient_gbs = 5000.0;
   m.gproject_tflops = 64.5;
-  m.gproject_gbs = 9520.0;
-  m.launch_us = 16.1;
+  m.gproject_gbs = 5000.0;
+  m.launch_us = 5.0;
+  m.call_us = 10.0;
   return m;
+}
+
+// Published MI355X peaks that bound the model's effective rates.
+constexpr double kPeakGbs = 8000.0, kPeakBf16Tflops = 2500.0, kPeakF32Tflops = 157.3;
+
+dattri_status check_cost_model(const dattri_cost_model& m) {
+  const struct { const char* name; double v, cap; } rates[] = {
+      {"factored_tflops", m.factored_tflops, kPeakBf16Tflops}, {"factored_gbs", m.factored_gbs, kPeakGbs},
+      {"gradient_tflops", m.gradient_tflops, kPeakBf16Tflops}, {"gradient_gbs", m.gradient_gbs, kPeakGbs},
+      {"gproject_tflops", m.gproject_tflops, kPeakF32Tflops}, {"gproject_gbs", m.gproject_gbs, kPeakGbs}};
+  for (const auto& r : rates)
+    if (!(r.v > 0.0) || !std::isfinite(r.v) || r.v > r.cap)
+      return fail(DATTRI_E_INVALID_ARG, "%s = %g must be finite, > 0 and at most the peak %g", r.name, r.v, r.cap);
+  if (!(m.launch_us >= 0.0) || !std::isfinite(m.launch_us))
+    return fail(DATTRI_E_INVALID_ARG, "launch_us = %g must be finite and >= 0", m.launch_us);
+  if (!(m.call_us >= 0.0) || !std::isfinite(m.call_us))
+    return fail(DATTRI_E_INVALID_ARG, "call_us = %g must be finite and >= 0", m.call_us);
+  return DATTRI_OK;
 }
 
 }  // namespace
@@ -88,17 +107,51 @@ Counts layer_counts(const Layer& L, int64_t T, int elt) {
   return c;
 }
 
-void predict(const dattri_cost_model& m, const Layer& L, int64_t n, int64_t T, int elt, double* f_us,
-             double* m_us) {
-  const Counts c = layer_counts(L, T, elt);
+// Kernel launches of a layer's factored route if it were projected alone: the
+// launch plan of a one-layer context decides fused or split form and stages.
+int factored_launches(const dattri_ctx* ctx, const Layer& L) {
+  dattri_ctx one;
+  one.dtype = ctx->dtype;
+  one.elt = ctx->elt;
+  one.seed = ctx->seed;
+  one.form = ctx->form;
+  one.cost = ctx->cost;
+  one.xcost = ctx->xcost;
+  Layer C;  // the plan needs sizes, captures and map pointers only
+  C.d_in = L.d_in; C.d_out = L.d_out; C.k_in = L.k_in; C.k_out = L.k_out;
+  C.P_in = L.P_in; C.P_out = L.P_out; C.bound = L.bound;
+  C.A = L.A; C.B = L.B; C.n = L.n; C.T = L.T; C.lengths = L.lengths; C.captured = L.captured;
+  one.layers.push_back(C);
+  one.F = (int64_t)L.k_in * L.k_out;
+  Plan P;
+  if (build_plan(&one, DATTRI_ROUTE_FACTORED, P, false) != DATTRI_OK) {
+    reset_error();  // not a failure of the caller's request: count the fused form
+    return 2;
+  }
+  return (int)(P.launches.size() + (P.n_fact_tasks ? 1 : 0) + P.slaunches.size() + (P.slabsum.empty() ? 0 : 1) +
+               (P.ctasks.empty() ? 0 : 1) + (P.stasks.empty() ? 0 : 1));
+}
+
+// Example chunks of the materialized route: G of a chunk fits the staging budget.
+int64_t materialized_chunk(const Layer& L, int64_t n) {
+  const int64_t g_per_ex = (int64_t)L.d_out * L.d_in;
+  return std::max<int64_t>(1, std::min<int64_t>({n, kGBudgetBytes / (4 * g_per_ex), (int64_t)65535}));
+}
+
+// Predicted times (us) of both routes for the layer's capture (n, T).
+void predict(const dattri_ctx* ctx, const Layer& L, double* f_us, double* m_us) {
+  const dattri_cost_model& m = ctx->cost;
+  const int64_t n = L.n;
+  const Counts c = layer_counts(L, L.T, ctx->elt);
   auto t = [](double flops, double tflops, double bytes, double gbs) {
     return std::max(flops / (tflops * 1e6), bytes / (gbs * 1e3));  // microseconds
   };
-  *f_us = t((double)c.f_flops * n, m.factored_tflops, (double)c.f_bytes * n, m.factored_gbs) +
-          m.launch_us;
-  *m_us = t((double)c.g_flops * n, m.gradient_tflops, (double)c.g_bytes * n, m.gradient_gbs) +
+  *f_us = m.call_us + t((double)c.f_flops * n, m.factored_tflops, (double)c.f_bytes * n, m.factored_gbs);
+  if (n > 0) *f_us += factored_launches(ctx, L) * m.launch_us;
+  const int64_t chunks = n > 0 ? (n + materialized_chunk(L, n) - 1) / materialized_chunk(L, n) : 0;
+  *m_us = m.call_us + t((double)c.g_flops * n, m.gradient_tflops, (double)c.g_bytes * n, m.gradient_gbs) +
           t((double)c.p_flops * n, m.gproject_tflops, (double)c.p_bytes * n, m.gproject_gbs) +
-          3 * m.launch_us;
+          3.0 * chunks * m.launch_us;
 }
 
 dattri_route choose_route(const dattri_ctx* ctx, const Layer& L, dattri_route forced) {
@@ -106,7 +159,7 @@ dattri_route choose_route(const dattri_ctx* ctx, const Layer& L, dattri_route fo
   if (forced != DATTRI_ROUTE_AUTO) return forced;
   if (!factored_supported(L)) return DATTRI_ROUTE_MATERIALIZED;
   double f, m;
-  predict(ctx->cost, L, L.n, L.T, ctx->elt, &f, &m);
+  predict(ctx, L, &f, &m);
   return f <= m ? DATTRI_ROUTE_FACTORED : DATTRI_ROUTE_MATERIALIZED;
 }
 
@@ -151,10 +204,12 @@ dattri_status dattri::build_plan(const dattri_ctx* ctx, dattri_route forced, Pla
     factored_instance(elt, na, nb, 1, &nai, &nbi, &rt);
     return rt;
   };
+  std::vector<dattri_route> route(ctx->layers.size());
+  for (size_t l = 0; l < ctx->layers.size(); ++l) route[l] = choose_route(ctx, ctx->layers[l], forced);
   std::vector<std::vector<int>> group_layers;
   for (size_t l = 0; l < ctx->layers.size(); ++l) {
     const Layer& L = ctx->layers[l];
-    const dattri_route r = choose_route(ctx, L, forced);
+    const dattri_route r = route[l];
     if (r == DATTRI_ROUTE_MATERIALIZED || r == DATTRI_ROUTE_MASK) continue;
     if (!factored_supported(L))
       return fail(DATTRI_E_UNSUPPORTED,
@@ -566,13 +621,12 @@ dattri_status dattri::build_plan(const dattri_ctx* ctx, dattri_route forced, Pla
   size_t g_floats = 0, mpart_floats = 0;
   for (size_t l = 0; l < ctx->layers.size(); ++l) {
     const Layer& L = ctx->layers[l];
-    if (choose_route(ctx, L, forced) != DATTRI_ROUTE_MATERIALIZED) continue;
+    if (route[l] != DATTRI_ROUTE_MATERIALIZED) continue;
     const int64_t g_per_ex = (int64_t)L.d_out * L.d_in;
     if (4 * g_per_ex >= kMaxBlockBytes)
       return fail(DATTRI_E_UNSUPPORTED, "layer %zu: G = d_out x d_in float32 (%lld bytes) exceeds 4 GiB",
                   l, (long long)(4 * g_per_ex));
-    const int ex_chunk = (int)std::max<int64_t>(
-        1, std::min<int64_t>({(int64_t)n, kGBudgetBytes / (4 * g_per_ex), (int64_t)65535}));
+    const int ex_chunk = (int)materialized_chunk(L, n);
     const int n_ublocks = (L.d_out + kGProjRows - 1) / kGProjRows;
     // split d_in's k-blocks when row blocks x examples give too few workgroups
     const int nkb = (L.d_in + krows_of(elt) - 1) / krows_of(elt);
@@ -730,10 +784,101 @@ dattri_status dattri::build_plan(const dattri_ctx* ctx, dattri_route forced, Pla
       P.row_srcs.push_back({R.layer, 1, P.off_proj + (size_t)B.out_base * 4, B.nt * 16, 0});
     }
     for (size_t l = 0; l < ctx->layers.size(); ++l)
-      if (choose_route(ctx, ctx->layers[l], forced) == DATTRI_ROUTE_MATERIALIZED) P.mat_layers.push_back((int)l);
+      if (route[l] == DATTRI_ROUTE_MATERIALIZED) P.mat_layers.push_back((int)l);
   }
   P.total = std::max<size_t>(off, kAlign);
   return DATTRI_OK;
+}
+
+namespace {
+
+// Everything build_plan reads from the context, as one flat key: a plan built
+// from an equal key is the same plan.
+std::vector<uint64_t> plan_key(const dattri_ctx* ctx, dattri_route forced, bool rows) {
+  std::vector<uint64_t> k;
+  k.reserve(16 + 10 * ctx->layers.size());
+  auto pack = [](int64_t hi, int64_t lo) { return ((uint64_t)(uint32_t)hi << 32) | (uint32_t)lo; };
+  auto ptr = [](const void* p) { return (uint64_t)(uintptr_t)p; };
+  k.push_back(pack(forced, rows));
+  k.push_back(pack(ctx->form, ctx->elt));
+  uint64_t words[sizeof(dattri_cost_model) / 8];
+  static_assert(sizeof(dattri_cost_model) % 8 == 0, "cost model is a plain array of doubles");
+  std::memcpy(words, &ctx->cost, sizeof(words));
+  k.insert(k.end(), words, words + sizeof(words) / 8);
+  for (const Layer& L : ctx->layers) {
+    k.push_back(pack(L.d_in, L.d_out));
+    k.push_back(pack(L.k_in, L.k_out));
+    k.push_back(pack(L.mask_size, L.mask_id));
+    k.push_back(pack(L.mask_count, L.n));
+    k.push_back(pack(L.T, (L.captured ? 2 : 0) | (L.bound ? 1 : 0)));
+    k.push_back(ptr(L.A));
+    k.push_back(ptr(L.B));
+    k.push_back(ptr(L.lengths));
+    k.push_back(ptr(L.P_in));
+    k.push_back(ptr(L.P_out));
+  }
+  return k;
+}
+
+constexpr size_t kPlansKept = 4;  // recent plans remembered per context
+
+}  // namespace
+
+dattri_status dattri::get_plan(const dattri_ctx* ctx, dattri_route forced, bool rows,
+                               std::shared_ptr<const Plan>* out) {
+  std::vector<uint64_t> key = plan_key(ctx, forced, rows);
+  auto& kept = ctx->plans;
+  for (size_t i = 0; i < kept.size(); ++i)
+    if (kept[i].first == key) {
+      std::rotate(kept.begin(), kept.begin() + i, kept.begin() + i + 1);  // most recent first
+      *out = kept.front().second;
+      return DATTRI_OK;
+    }
+  auto P = std::make_shared<Plan>();
+  const dattri_status st = build_plan(ctx, forced, *P, rows);
+  if (st != DATTRI_OK) return st;
+  kept.insert(kept.begin(), {std::move(key), P});
+  if (kept.size() > kPlansKept) kept.pop_back();
+  *out = P;
+  return DATTRI_OK;
+}
+
+hipError_t dattri::place_table(const dattri_ctx* ctx, TableKind kind, const std::vector<uint8_t>& blob,
+                               uint8_t* fallback, hipStream_t s, uint8_t** dev) {
+  *dev = fallback;
+  if (blob.empty()) return hipSuccess;
+  const size_t need = align_up(blob.size());
+  if (!ctx->plan_buf || need > ctx->plan_cap) {
+    ctx->blob = blob;
+    return hipMemcpyAsync(fallback, ctx->blob.data(), blob.size(), hipMemcpyHostToDevice, s);
+  }
+  TableSlot* slot = nullptr;
+  for (TableSlot& t : ctx->slots)
+    if (t.kind == kind) slot = &t;
+  if (slot && slot->bytes == blob) {  // already resident: no copy
+    *dev = ctx->plan_buf + slot->off;
+    return hipSuccess;
+  }
+  if (!slot || slot->cap < need) {
+    // a new slot at the end of the buffer; when the buffer is full, every
+    // table is dropped and placement starts again at its head
+    if (slot) slot->kind = -1;
+    if (ctx->slots_used + need > ctx->plan_cap) {
+      ctx->slots.clear();
+      ctx->slots_used = 0;
+    }
+    ctx->slots.emplace_back();
+    slot = &ctx->slots.back();
+    slot->kind = kind;
+    slot->off = ctx->slots_used;
+    slot->cap = need;
+    ctx->slots_used += need;
+  }
+  slot->bytes = blob;
+  *dev = ctx->plan_buf + slot->off;
+  const hipError_t e = hipMemcpyAsync(*dev, slot->bytes.data(), blob.size(), hipMemcpyHostToDevice, s);
+  if (e != hipSuccess) slot->bytes.clear();  // contents unknown: never matched
+  return e;
 }
 
 namespace {
@@ -853,10 +998,11 @@ dattri_status dattri::run_plan(dattri_ctx* ctx, const Plan& P, void* phi, dattri
   if (ws_bytes < P.total)
     return fail(DATTRI_E_WORKSPACE, "workspace has %zu bytes, needs %zu", ws_bytes, P.total);
 
-  // Upload the launch plan into the head of the workspace.
-  ctx->blob.assign(P.blob_bytes, 0);
+  // The launch plan's tables: into the bound plan buffer, else the head of
+  // the workspace.
+  std::vector<uint8_t> blob(P.blob_bytes, 0);
   auto put = [&](size_t off, const void* src, size_t bytes) {
-    if (bytes) std::memcpy(ctx->blob.data() + off, src, bytes);
+    if (bytes) std::memcpy(blob.data() + off, src, bytes);
   };
   put(P.off_items, P.items.data(), P.items.size() * sizeof(FactItem));
   put(P.off_groups, P.groups.data(), P.groups.size() * sizeof(FactGroup));
@@ -880,12 +1026,13 @@ dattri_status dattri::run_plan(dattri_ctx* ctx, const Plan& P, void* phi, dattri
   put(P.off_mitems, P.mitems.data(), P.mitems.size() * sizeof(MaskItem));
   put(P.off_mreduce, P.mreduce.data(), P.mreduce.size() * sizeof(ReduceTask));
   uint8_t* ws = (uint8_t*)workspace;
-  HIP_TRY(hipMemcpyAsync(ws, ctx->blob.data(), P.blob_bytes, hipMemcpyHostToDevice, s));
+  uint8_t* tab = nullptr;
+  HIP_TRY(place_table(ctx, kTabProj, blob, ws, s, &tab));
 
-  const FactItem* d_items = (const FactItem*)(ws + P.off_items);
-  const FactGroup* d_groups = (const FactGroup*)(ws + P.off_groups);
-  const FactMember* d_members = (const FactMember*)(ws + P.off_members);
-  const ReduceTask* d_tasks = (const ReduceTask*)(ws + P.off_tasks);
+  const FactItem* d_items = (const FactItem*)(tab + P.off_items);
+  const FactGroup* d_groups = (const FactGroup*)(tab + P.off_groups);
+  const FactMember* d_members = (const FactMember*)(tab + P.off_members);
+  const ReduceTask* d_tasks = (const ReduceTask*)(tab + P.off_tasks);
   float* fpart = (float*)(ws + P.off_fpart);
   const int phi_bf16 = phi_dtype == DATTRI_BF16;
   for (const Plan::Launch& L : P.launches)
@@ -894,29 +1041,29 @@ dattri_status dattri::run_plan(dattri_ctx* ctx, const Plan& P, void* phi, dattri
   if (P.n_fact_tasks)
     HIP_TRY(launch_reduce(d_tasks, P.n_fact_tasks, n, P.fact_max_out, fpart, phi, phi_bf16, ld_phi, s));
 
-  const SplitOp* d_sops = (const SplitOp*)(ws + P.off_sops);
-  const SplitItem* d_sitems = (const SplitItem*)(ws + P.off_sitems);
-  const ContractTask* d_ctasks = (const ContractTask*)(ws + P.off_ctasks);
+  const SplitOp* d_sops = (const SplitOp*)(tab + P.off_sops);
+  const SplitItem* d_sitems = (const SplitItem*)(tab + P.off_sitems);
+  const ContractTask* d_ctasks = (const ContractTask*)(tab + P.off_ctasks);
   float* proj = (float*)(ws + P.off_proj);
   for (const Plan::SplitLaunch& L : P.slaunches)
     HIP_TRY(launch_split_project(L.elt, L.aligned, L.nt, d_sitems + L.first, L.count, d_sops, proj, s));
   if (!P.slabsum.empty())
-    HIP_TRY(launch_slab_sum((const SlabSumTask*)(ws + P.off_slabsum), (int)P.slabsum.size(),
+    HIP_TRY(launch_slab_sum((const SlabSumTask*)(tab + P.off_slabsum), (int)P.slabsum.size(),
                             P.slabsum_max_n4, proj, s));
   float* spart = (float*)(ws + P.off_spart);
   if (!P.ctasks.empty())
     HIP_TRY(launch_split_contract(d_ctasks, (int)P.ctasks.size(), n, P.split_max_tchunks, proj, spart,
                                   phi, phi_bf16, ld_phi, s));
   if (!P.stasks.empty())
-    HIP_TRY(launch_reduce((const ReduceTask*)(ws + P.off_stasks), (int)P.stasks.size(), n,
+    HIP_TRY(launch_reduce((const ReduceTask*)(tab + P.off_stasks), (int)P.stasks.size(), n,
                           P.split_max_out, spart, phi, phi_bf16, ld_phi, s));
 
   if (!P.mtasks.empty()) {
     float* kpart = (float*)(ws + P.off_maskpart);
     for (const Plan::MaskLaunch& L : P.mlaunches)
-      HIP_TRY(launch_mask(ctx->elt, L.aligned, L.full, (const MaskItem*)(ws + P.off_mitems) + L.first, L.count,
-                          (const MaskTask*)(ws + P.off_mtasks), P.mask_lds, kpart, s));
-    HIP_TRY(launch_reduce((const ReduceTask*)(ws + P.off_mreduce), (int)P.mreduce.size(), n, P.mask_max_out,
+      HIP_TRY(launch_mask(ctx->elt, L.aligned, L.full, (const MaskItem*)(tab + P.off_mitems) + L.first, L.count,
+                          (const MaskTask*)(tab + P.off_mtasks), P.mask_lds, kpart, s));
+    HIP_TRY(launch_reduce((const ReduceTask*)(tab + P.off_mreduce), (int)P.mreduce.size(), n, P.mask_max_out,
                           kpart, phi, phi_bf16, ld_phi, s));
   }
 
@@ -1208,10 +1355,10 @@ dattri_status dattri_workspace_bytes(const dattri_ctx* ctx, dattri_route route, 
   if (!ctx || !bytes) return fail(DATTRI_E_INVALID_ARG, "ctx or bytes is NULL");
   if (route < DATTRI_ROUTE_AUTO || route > DATTRI_ROUTE_MATERIALIZED)
     return fail(DATTRI_E_INVALID_ARG, "route %d unknown", (int)route);
-  Plan P;
-  dattri_status st = build_plan(ctx, route, P, false);
+  std::shared_ptr<const Plan> P;
+  dattri_status st = get_plan(ctx, route, false, &P);
   if (st != DATTRI_OK) return st;
-  *bytes = P.total;
+  *bytes = P->total;
   return DATTRI_OK;
 }
 
@@ -1243,10 +1390,34 @@ dattri_status dattri_project_per_example(dattri_ctx* ctx, void* phi, dattri_dtyp
   for (size_t l = 0; l < ctx->layers.size(); ++l)
     if (!ctx->layers[l].bound)
       return fail(DATTRI_E_STATE, "layer %zu: projection maps not bound", l);
-  Plan P;
-  dattri_status st = build_plan(ctx, route, P, false);
+  std::shared_ptr<const Plan> P;
+  dattri_status st = get_plan(ctx, route, false, &P);
   if (st != DATTRI_OK) return st;
-  return run_plan(ctx, P, phi, phi_dtype, ld_phi, workspace, ws_bytes, (hipStream_t)stream);
+  return run_plan(ctx, *P, phi, phi_dtype, ld_phi, workspace, ws_bytes, (hipStream_t)stream);
+}
+
+dattri_status dattri_plan_bytes(const dattri_ctx* ctx, dattri_route route, size_t* bytes) {
+  reset_error();
+  if (!ctx || !bytes) return fail(DATTRI_E_INVALID_ARG, "ctx or bytes is NULL");
+  if (route < DATTRI_ROUTE_AUTO || route > DATTRI_ROUTE_MATERIALIZED)
+    return fail(DATTRI_E_INVALID_ARG, "route %d unknown", (int)route);
+  std::shared_ptr<const Plan> P;
+  dattri_status st = get_plan(ctx, route, false, &P);
+  if (st != DATTRI_OK) return st;
+  *bytes = align_up(P->blob_bytes);
+  return DATTRI_OK;
+}
+
+dattri_status dattri_bind_plan_buffer(dattri_ctx* ctx, void* dev_plan, size_t bytes) {
+  reset_error();
+  if (!ctx) return fail(DATTRI_E_INVALID_ARG, "ctx is NULL");
+  if (dev_plan && (uintptr_t)dev_plan % kAlign)
+    return fail(DATTRI_E_INVALID_ARG, "plan buffer must be 256-byte aligned");
+  ctx->plan_buf = dev_plan ? (uint8_t*)dev_plan : nullptr;
+  ctx->plan_cap = dev_plan ? bytes / kAlign * kAlign : 0;
+  ctx->slots.clear();
+  ctx->slots_used = 0;
+  return DATTRI_OK;
 }
 
 dattri_status dattri_materialize_gradient(dattri_ctx* ctx, int32_t layer, int32_t ex_begin,
@@ -1275,13 +1446,20 @@ dattri_status dattri_materialize_gradient(dattri_ctx* ctx, int32_t layer, int32_
 dattri_status dattri_set_cost_model(dattri_ctx* ctx, const dattri_cost_model* m) {
   reset_error();
   if (!ctx || !m) return fail(DATTRI_E_INVALID_ARG, "ctx or model is NULL");
-  const double r[6] = {m->factored_tflops, m->factored_gbs, m->gradient_tflops,
-                       m->gradient_gbs, m->gproject_tflops, m->gproject_gbs};
-  for (double x : r)
-    if (!(x > 0.0) || !std::isfinite(x)) return fail(DATTRI_E_INVALID_ARG, "rates must be finite and > 0");
-  if (!(m->launch_us >= 0.0) || !std::isfinite(m->launch_us))
-    return fail(DATTRI_E_INVALID_ARG, "launch_us must be finite and >= 0");
+  const dattri_status st = check_cost_model(*m);
+  if (st != DATTRI_OK) return st;
   ctx->cost = *m;
+  return DATTRI_OK;
+}
+
+dattri_status dattri_set_cost_calibration(dattri_ctx* ctx, const char* json_path) {
+  reset_error();
+  if (!ctx || !json_path) return fail(DATTRI_E_INVALID_ARG, "ctx or json_path is NULL");
+  dattri_cost_model m;
+  dattri_status st = read_cost_calibration(json_path, &m);
+  if (st != DATTRI_OK) return st;
+  if ((st = check_cost_model(m)) != DATTRI_OK) return st;
+  ctx->cost = m;
   return DATTRI_OK;
 }
 
@@ -1329,7 +1507,7 @@ dattri_status dattri_layer_route(const dattri_ctx* ctx, int32_t layer, dattri_ro
     return DATTRI_OK;
   }
   double f, m;
-  predict(ctx->cost, L, L.n, L.T, ctx->elt, &f, &m);
+  predict(ctx, L, &f, &m);
   if (chosen) *chosen = choose_route(ctx, L, DATTRI_ROUTE_AUTO);
   if (pred_factored_us) *pred_factored_us = factored_supported(L) ? f : INFINITY;
   if (pred_materialized_us) *pred_materialized_us = m;

@@ -5,7 +5,13 @@
 
 #include <vector>
 
+#include "dattri.h"
+
 namespace dattri {
+
+// The cost model in a calibration file (JSON, member "model"); values are
+// not range-checked here.  INVALID_ARG with a message on any error.
+dattri_status read_cost_calibration(const char* path, dattri_cost_model* out);
 
 uint64_t derive_side_seed(uint64_t global_seed, int layer, int side);
 uint64_t derive_mask_seed(uint64_t global_seed, int layer);

@@ -54,7 +54,14 @@ ScoreLayout score_layout(int64_t n_q, int64_t n_train, int64_t F, int elt, bool 
   L.total = std::max<size_t>(off, kAlign);
   return L;
 }
-dattri_status score_impl(const void* phi_q, int64_t n_q, int64_t ld_q, const void* phi_train,
+}  // namespace
+
+size_t dattri::score_workspace_need(int64_t n_q, int64_t n_train, int64_t F, int elt, bool precond,
+                                    bool has_scores, int32_t topk, bool cosine) {
+  return score_layout(n_q, n_train, F, elt, precond, has_scores, topk, cosine).total;
+}
+
+dattri_status dattri::score_impl(const void* phi_q, int64_t n_q, int64_t ld_q, const void* phi_train,
                          int64_t n_train, int64_t ld_train, int64_t F, dattri_dtype dtype,
                          const float* dev_precond_diag, float* scores, int32_t topk, int32_t* topk_idx,
                          float* topk_val, void* workspace, size_t ws_bytes, void* stream, bool cosine) {
@@ -107,9 +114,6 @@ dattri_status score_impl(const void* phi_q, int64_t n_q, int64_t ld_q, const voi
   if (topk > 0) HIP_TRY(launch_topk(S, n_q, n_train, topk, topk_idx, topk_val, s));
   return DATTRI_OK;
 }
-
-
-}  // namespace
 
 extern "C" {
 

@@ -23,9 +23,10 @@ from . import (DATTRI_BF16, DATTRI_F32, DATTRI_ROUTE_AUTO, dattri_bind_projectio
                dattri_curvature_accumulate_ekfac, dattri_curvature_precondition,
                dattri_project_fit_workspace_bytes, dattri_project_and_fit, dattri_set_map_kind,
                dattri_cosine_workspace_bytes, dattri_score_cosine, dattri_register_mask_layer,
-               dattri_token_scores_workspace_bytes, dattri_token_scores)
+               dattri_token_scores_workspace_bytes, dattri_token_scores, dattri_bind_plan_buffer)
 
 DTYPES = {"f32": (DATTRI_F32, torch.float32), "bf16": (DATTRI_BF16, torch.bfloat16)}
+PLAN_BUFFER_BYTES = 8 << 20  # launch tables kept on the device between calls
 
 
 def _dev_bytes(n, device):
@@ -35,11 +36,16 @@ def _dev_bytes(n, device):
 class ProjectionSession:
     """One library context with its layers and bound projection maps."""
 
-    def __init__(self, layers, dtype="bf16", seed=0, device="cuda", overrides=None, form=None, map_kind=None):
+    def __init__(self, layers, dtype="bf16", seed=0, device="cuda", overrides=None, form=None, map_kind=None,
+                 plan_buffer=True):
         self.dtype = dtype
         self.code, self.torch_dtype = DTYPES[dtype]
         self.device = torch.device(device)
         self.ctx = dattri_create(self.code, seed)
+        self.plan_buf = None
+        if plan_buffer:  # repeated calls with unchanged captures then copy nothing to the device
+            self.plan_buf = _dev_bytes(PLAN_BUFFER_BYTES, self.device)
+            dattri_bind_plan_buffer(self.ctx, self.plan_buf)
         if form is not None:
             dattri_set_factored_form(self.ctx, form)
         self.layers = list(layers)

@@ -241,6 +241,53 @@ def test_materialize_gradient_matches_eq1(dtype):
     assert torch.count_nonzero(G[1]).item() == 0  # length 0
 
 
+# One AUTO plan that mixes routes (Eq. 2 / App. A.4 "Routing": the two forms
+# are equal, so a call may route each layer its own way): two small layers the
+# cost model sends to the factored kernels, a layer with k_out = 128 and one
+# with k_in = 160, which exceed the factored kernels' map widths and route
+# materialized; k_in = 160 takes two passes of the G projection (8 input tiles
+# per pass).  f0 and w_out share their input block, so the factored group and
+# the materialized layer read the same A.  bf16 rows of 200 are 16-byte
+# aligned (the transposing G kernel), rows of 300 are not.
+MIXED = [dict(name="f0", d_in=200, d_out=136, k_in=32, k_out=32, a_group="a"),
+         dict(name="w_out", d_in=200, d_out=96, k_in=16, k_out=128, a_group="a"),
+         dict(name="w_in", d_in=300, d_out=72, k_in=160, k_out=24, a_group="b"),
+         dict(name="f1", d_in=48, d_out=40, k_in=8, k_out=16, a_group="c")]
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_auto_mixed_routes_wide_maps(dtype):
+    print(f"[project] mixed AUTO plan dtype={dtype}", flush=True)
+    wl = dict(W.WORKLOADS["tiny"], dist_a="normal", dist_b="normal", seed=61)
+    n, T = 5, 70
+    inputs = _session_inputs(wl, MIXED, n, T, dtype)
+    assert inputs[0][0] is inputs[1][0]
+    lengths = torch.tensor([70, 0, 1, 33, 64], dtype=torch.int32, device=DEV)
+    s, phi = _run(MIXED, inputs, dtype, 63, "auto", lengths=lengths)
+    routes = [r[0] for r in s.routes()]
+    assert routes[1] == dt.DATTRI_ROUTE_MATERIALIZED and routes[2] == dt.DATTRI_ROUTE_MATERIALIZED
+    assert routes[0] == dt.DATTRI_ROUTE_FACTORED and routes[3] == dt.DATTRI_ROUTE_FACTORED
+    assert torch.count_nonzero(phi[1]).item() == 0  # length 0
+    # offsets are the running sums of k_in * k_out in registration order
+    assert s.offsets == [0, 1024, 1024 + 2048, 1024 + 2048 + 3840]
+    errs = _check(MIXED, inputs, phi, 63, dtype, [0, 2, 3, 4], lengths=lengths, tol=1e-5)
+    print(f"[project] mixed AUTO per-layer rel err {errs}", flush=True)
+    # forced materialized on every layer gives the same blocks
+    _, phi_m = _run(MIXED, inputs, dtype, 63, "materialized", lengths=lengths)
+    assert rel_fro(host64(phi_m), host64(phi)) < 1e-5
+
+
+def test_factored_route_refuses_wide_maps():
+    layers = [MIXED[1]]
+    s = ProjectionSession(layers, dtype="f32", seed=0)
+    A = torch.zeros((2, 4, 200), device=DEV)
+    B = torch.zeros((2, 4, 96), device=DEV)
+    s.capture(0, A, B)
+    with pytest.raises(dt.DattriError) as e:
+        s.project(2, route=dt.DATTRI_ROUTE_FACTORED)
+    assert e.value.status_name == "E_UNSUPPORTED"
+
+
 def test_gpt2_batch_bf16():
     wl = W.WORKLOADS["gpt2"]
     inputs = _session_inputs(wl, wl["layers"], wl["batch"], wl["T"], "bf16")
@@ -253,7 +300,8 @@ def test_gpt2_batch_bf16():
 
 def test_llama8b_full_size_sampled():
     """Full Llama-3-8B-shaped batch (224 layers, T=2048, n=8) in the launch
-    configuration the benchmark times; sampled examples/layers vs the oracle."""
+    configuration the benchmark times; every layer block of examples 0 and 7
+    against the oracle (factor blocks streamed to the host layer by layer)."""
     wl = W.WORKLOADS["llama8b"]
     layers, n, T = wl["layers"], wl["batch"], wl["T"]
     cache = {}
@@ -267,18 +315,24 @@ def test_llama8b_full_size_sampled():
     torch.cuda.synchronize()
     assert all(r[0] == dt.DATTRI_ROUTE_FACTORED for r in s.routes())
     assert torch.isfinite(phi).all()
-    # sampled layers: block 0 and block 31, examples 0 and 7
-    maps = oracle_maps(wl["seed"], layers, "bf16")
-    for li in list(range(7)) + list(range(217, 224)):
-        L = layers[li]
+    examples = (0, 7)
+    got = host64(phi[list(examples)])
+    print("[project] llama8b full size: oracle over 224 layers x 2 examples", flush=True)
+    a_host = {}
+    worst = 0.0
+    for li, L in enumerate(layers):
         A, B = inputs[li]
-        P_in, P_out = maps[li]
-        off = s.offsets[li]
-        w = L["k_in"] * L["k_out"]
-        for i in (0, 7):
-            ref = og.project_factored(host64(A[i]), host64(B[i]), P_in, P_out).reshape(-1)
-            err = rel_fro(host64(phi[i, off:off + w]), ref)
+        P_in, P_out = orng.projection_pair(wl["seed"], li, L["d_in"], L["d_out"], L["k_in"], L["k_out"], "bf16")
+        if A.data_ptr() not in a_host:  # q/k/v and gate/up share one input block
+            a_host = {A.data_ptr(): [A[i].cpu().to(torch.float64).numpy() for i in examples]}
+        off, w = s.offsets[li], L["k_in"] * L["k_out"]
+        for j, i in enumerate(examples):
+            Bh = B[i].cpu().to(torch.float64).numpy()
+            ref = og.project_factored(a_host[A.data_ptr()][j], Bh, P_in, P_out).reshape(-1)
+            err = rel_fro(got[j, off:off + w], ref)
+            worst = max(worst, err)
             assert err <= 1e-5, (li, i, err)
+    print(f"[project] llama8b full size: worst block rel err {worst:.3e}", flush=True)
 
 
 @pytest.mark.parametrize("form", ["fused", "split"])

@@ -19,6 +19,20 @@ from paper_2609_38767_amd.session import score
 pytestmark = pytest.mark.gpu
 DEV = "cuda"
 TOL = {torch.float32: 1e-5, torch.bfloat16: 2e-2}
+# bf16 queries scaled by d are rounded once to bf16 (2^-9 relative per element)
+# and everything else is float32: the expected error is about 1e-3, so an error
+# above 5e-3 marks a defect even though it is within the 2e-2 tolerance.
+BF16_DEFECT = 5e-3
+
+
+def _assert_score_err(S, ref, dtype, precond):
+    e = rel_fro(S, ref)
+    assert e <= TOL[dtype]
+    if dtype == torch.float32 or not precond:
+        assert e <= 1e-5  # exact inputs, float32 accumulation
+    else:
+        assert e <= BF16_DEFECT
+    return e
 
 
 def _check_topk(S_gpu, S_ref, idx, val, k):
@@ -45,9 +59,7 @@ def test_score_ragged_tiles(dtype, precond):
     S, idx, val = score(Q, X, d, topk=17)
     torch.cuda.synchronize()
     ref = osc.score(host64(Q), host64(X), None if d is None else host64(d))
-    assert rel_fro(host64(S), ref) <= TOL[dtype]
-    if dtype == torch.float32 or not precond:
-        assert rel_fro(host64(S), ref) <= 1e-5  # exact inputs, float32 accumulation
+    _assert_score_err(host64(S), ref, dtype, precond)
     _check_topk(host64(S), ref, idx.cpu().numpy(), val.cpu().numpy(), 17)
 
 
@@ -68,7 +80,7 @@ def test_score_few_tiles_split_features(dtype, shape, precond):
     torch.cuda.synchronize()
     assert torch.equal(S, S2)  # deterministic
     ref = osc.score(host64(Q), host64(X), None if d is None else host64(d))
-    assert rel_fro(host64(S), ref) <= (1e-5 if dtype == torch.float32 or not precond else TOL[dtype])
+    _assert_score_err(host64(S), ref, dtype, precond)
     _check_topk(host64(S), ref, idx.cpu().numpy(), val.cpu().numpy(), 5)
 
 
@@ -90,8 +102,7 @@ def test_score_cosine(dtype, shape, precond):
     S, idx, val = score(Q, X, d, topk=5, cosine=True)
     torch.cuda.synchronize()
     ref = osc.cosine_scores(host64(Q), host64(X), None if d is None else host64(d))
-    tol = 1e-5 if (dtype == torch.float32 or not precond) else TOL[dtype]
-    assert rel_fro(host64(S), ref) <= tol
+    _assert_score_err(host64(S), ref, dtype, precond)
     assert np.all(host64(S)[:, min(3, n_t - 1)] == 0.0)
     assert np.max(np.abs(host64(S))) <= 1.0 + 1e-5
     _check_topk(host64(S), ref, idx.cpu().numpy(), val.cpu().numpy(), 5)
@@ -114,7 +125,7 @@ def test_score_large_tile_kernel_ragged(shape):
     S0, _, _ = score(Q, X)
     torch.cuda.synchronize()
     ref = osc.score(host64(Q), host64(X), host64(d))
-    assert rel_fro(host64(S), ref) <= 2e-2
+    _assert_score_err(host64(S), ref, torch.bfloat16, True)
     assert rel_fro(host64(S0), osc.score(host64(Q), host64(X))) <= 1e-5
     _check_topk(host64(S), ref, idx.cpu().numpy(), val.cpu().numpy(), 10)
 
@@ -129,8 +140,6 @@ def test_score_large_tile_kernel_ragged(shape):
 @pytest.mark.parametrize("precond", [False, True])
 def test_score_strided_rows(dtype, shape, ld_q, ld_t, precond):
     n_q, n_t, F = shape
-    if dtype == torch.float32 and F == 8192:
-        pytest.skip("float32 at this size is covered by the ragged cases")
     g = torch.Generator(device=DEV).manual_seed(11)
     Qd = torch.randn((n_q, F), generator=g, device=DEV).to(dtype)
     Xd = torch.randn((n_t, F), generator=g, device=DEV).to(dtype)
@@ -146,9 +155,7 @@ def test_score_strided_rows(dtype, shape, ld_q, ld_t, precond):
     S_dense, _, _ = score(Qd, Xd, d)
     torch.cuda.synchronize()
     ref = osc.score(host64(Qd), host64(Xd), None if d is None else host64(d))
-    assert rel_fro(host64(S), ref) <= TOL[dtype]
-    if dtype == torch.float32 or not precond:
-        assert rel_fro(host64(S), ref) <= 1e-5
+    _assert_score_err(host64(S), ref, dtype, precond)
     assert torch.equal(S, S_dense)  # the stride changes addressing only
     _check_topk(host64(S), ref, idx.cpu().numpy(), val.cpu().numpy(), 10)
 
@@ -244,14 +251,13 @@ def test_score_full_size_sampled(layout):
     torch.cuda.synchronize()
     assert torch.isfinite(S).all()
     rows = [0, 1023, 2047]
-    Qh = host64(Q[rows]) * host64(d)[None, :]
+    Qh, dh = host64(Q[rows]), host64(d)
     ref = np.zeros((len(rows), X.shape[0]))
-    for c0 in range(0, X.shape[0], 25000):
-        ref[:, c0:c0 + 25000] = Qh @ host64(X[c0:c0 + 25000]).T
+    for c0 in range(0, X.shape[0], 25000):  # training rows streamed to the host in chunks
+        ref[:, c0:c0 + 25000] = osc.score(Qh, host64(X[c0:c0 + 25000]), dh)
     got = host64(S[rows])
-    err = rel_fro(got, ref)
+    err = _assert_score_err(got, ref, torch.bfloat16, True)
     print(f"score full-size sampled rel err {err:.3e}")
-    assert err <= 2e-2
     _check_topk(got, ref, idx[rows].cpu().numpy(), val[rows].cpu().numpy(), wl["topk"])
 
 

@@ -15,6 +15,7 @@ import torch
 import paper_2609_38767_amd as dt
 import workloads as W
 from gpu_util import host64, oracle_maps, rel_fro
+from oracle import rng as orng
 from oracle import token as otk
 from paper_2609_38767_amd.session import Curvature, ProjectionSession, score
 
@@ -99,20 +100,45 @@ def test_token_sums_are_curvature_scores(kind):
     assert _sums_match(scores, pq, phi2) <= 1e-4
 
 
-def test_token_scores_full_size_property():
+@pytest.mark.timeout(600)
+def test_token_scores_full_size_sampled():
     """The curvature workload's batch (196 Qwen2.5-7B-shaped layers, 32 x 512
-    tokens, k = 64) with one query row: token sums equal the sequence scores."""
+    tokens, k = 64) with one query row: token scores at sampled (example,
+    position) pairs against the oracle (each needs only that token row of
+    every layer), and the property at every position: token sums equal the
+    sequence scores."""
     wl = W.WORKLOADS["curvature"]
     layers, n, T = wl["layers"], wl["batch"], wl["T"]
     print("[token] full size: building inputs", flush=True)
     cache = {}
     s = ProjectionSession(layers, dtype="bf16", seed=wl["seed"])
+    inputs = []
     for li in range(len(layers)):
         A, B = W.factor_blocks(wl, li, 0, n, T, DEV, "bf16", a_cache=cache)
         s.capture(li, A, B)
+        inputs.append((A, B))
     g = torch.Generator(device=DEV).manual_seed(87)
     q = torch.randn((1, s.F), generator=g, device=DEV)
     scores, phi = s.token_scores(q, n)
     torch.cuda.synchronize()
     assert torch.isfinite(scores).all()
     assert _sums_match(scores, q, phi) <= 1e-4
+    pairs = [(0, 0), (0, 511), (5, 17), (13, 256), (17, 333), (21, 100), (31, 0), (31, 511)]
+    ei = torch.tensor([p[0] for p in pairs], device=DEV)
+    ti = torch.tensor([p[1] for p in pairs], device=DEV)
+    print("[token] full size: oracle at 8 sampled positions over 196 layers", flush=True)
+    qh = host64(q)[0]
+    oracle_layers, blocks = [], []
+    for li, L in enumerate(layers):
+        A, B = inputs[li]
+        P_in, P_out = orng.projection_pair(wl["seed"], li, L["d_in"], L["d_out"], L["k_in"], L["k_out"], "bf16")
+        # each sampled token row as a one-token example: [8, 1, d]
+        oracle_layers.append(dict(A=host64(A[ei, ti])[:, None, :], B=host64(B[ei, ti])[:, None, :],
+                                  P_in=P_in, P_out=P_out))
+        o, w = s.offsets[li], L["k_in"] * L["k_out"]
+        blocks.append(qh[o:o + w].reshape(L["k_in"], L["k_out"]))
+    ref = otk.token_scores(oracle_layers, blocks)[:, 0]
+    got = host64(scores[0, ei, ti])
+    err = rel_fro(got, ref)
+    print(f"[token] full size sampled rel err {err:.3e}", flush=True)
+    assert err <= 1e-5, (got, ref)

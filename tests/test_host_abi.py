@@ -248,16 +248,98 @@ def test_layer_cost_counters(case):
     dt.dattri_destroy(c)
 
 
+FIELDS = ("factored_tflops", "factored_gbs", "gradient_tflops", "gradient_gbs",
+          "gproject_tflops", "gproject_gbs", "launch_us", "call_us")
+
+
 def test_cost_model_roundtrip_and_validation(ctx):
     m = dt.dattri_get_cost_model(ctx)
-    assert set(m) == {"factored_tflops", "factored_gbs", "gradient_tflops", "gradient_gbs",
-                      "gproject_tflops", "gproject_gbs", "launch_us"}
-    m2 = dict(m, factored_gbs=1234.5)
+    assert set(m) == set(FIELDS)
+    m2 = dict(m, factored_gbs=1234.5, call_us=7.25)
     dt.dattri_set_cost_model(ctx, m2)
-    assert dt.dattri_get_cost_model(ctx)["factored_gbs"] == 1234.5
+    assert dt.dattri_get_cost_model(ctx) == m2
+    # rates must be positive, finite and within the published MI355X peaks
+    bad = [dict(m, gradient_tflops=0.0), dict(m, factored_gbs=8000.5), dict(m, gradient_gbs=float("inf")),
+           dict(m, factored_tflops=2501.0), dict(m, gproject_tflops=157.4), dict(m, launch_us=-1.0),
+           dict(m, call_us=float("nan"))]
+    for b in bad:
+        with pytest.raises(dt.DattriError) as e:
+            dt.dattri_set_cost_model(ctx, b)
+        assert _status(e) == "E_INVALID_ARG"
+    assert dt.dattri_get_cost_model(ctx) == m2  # unchanged by the rejected calls
+
+
+def _write(tmp_path, name, text):
+    p = tmp_path / name
+    p.write_text(text)
+    return str(p)
+
+
+def test_cost_calibration_file_roundtrip(ctx, tmp_path):
+    import json
+    model = {"factored_tflops": 310.5, "factored_gbs": 5123.25, "gradient_tflops": 700.0, "gradient_gbs": 4999.0,
+             "gproject_tflops": 61.0, "gproject_gbs": 4000.0, "launch_us": 4.5, "call_us": 1.25e1}
+    # the layout the calibration script writes: the model beside per-shape records
+    doc = {"model": model, "rms_log_error": 0.1, "device": "AMD Instinct MI355X",
+           "shapes": [{"d_in": 8, "auto": "factored", "regret": 0.0, "nested": [1, -2.5e-3, True, None, {}]}],
+           "note": "escapes \" \\ \u00e9 \n"}
+    path = _write(tmp_path, "calib.json", json.dumps(doc, indent=2))
+    dt.dattri_set_cost_calibration(ctx, path)
+    got = dt.dattri_get_cost_model(ctx)
+    assert got == model
+    # a layer's predicted times follow the loaded model
+    fake = 1 << 40
+    dt.dattri_register_layer(ctx, 128, 128, 64, 64)
+    dt.dattri_capture_layer(ctx, 0, fake, fake, 8, 2048)
+    before = dt.dattri_layer_route(ctx, 0)
+    dt.dattri_set_cost_calibration(ctx, _write(tmp_path, "c2.json", json.dumps({"model": dict(model, call_us=112.5)})))
+    after = dt.dattri_layer_route(ctx, 0)
+    assert after[1] == pytest.approx(before[1] + 100.0) and after[2] == pytest.approx(before[2] + 100.0)
+
+
+@pytest.mark.parametrize("text,what", [
+    (None, "cannot open"),
+    ('{"model": {"factored_tflops": 1', "expected ',' or '}'"),
+    ('{"model": {"factored_tflops": ', "unexpected end"),
+    ('[1, 2]', "not a JSON object"),
+    ('{"models": {}}', "no \"model\""),
+    ('{"model": {"factored_tflops": 300}}', "factored_gbs missing"),
+    ('{"model": {"factored_tflops": "300", "factored_gbs": 1, "gradient_tflops": 1, "gradient_gbs": 1, '
+     '"gproject_tflops": 1, "gproject_gbs": 1, "launch_us": 1, "call_us": 1}}', "factored_tflops missing"),
+    ('{"model": {"factored_tflops": 300, "factored_gbs": 9000, "gradient_tflops": 1, "gradient_gbs": 1, '
+     '"gproject_tflops": 1, "gproject_gbs": 1, "launch_us": 1, "call_us": 1}}', "factored_gbs"),
+    ('{"model": {"factored_tflops": 01}}', "expected"),
+    ('{"model": {}} x', "trailing"),
+])
+def test_cost_calibration_file_errors(ctx, tmp_path, text, what):
+    before = dt.dattri_get_cost_model(ctx)
+    path = str(tmp_path / "missing.json") if text is None else _write(tmp_path, "bad.json", text)
     with pytest.raises(dt.DattriError) as e:
-        dt.dattri_set_cost_model(ctx, dict(m, gradient_tflops=0.0))
+        dt.dattri_set_cost_calibration(ctx, path)
     assert _status(e) == "E_INVALID_ARG"
+    assert what in dt.dattri_last_error() or what in str(e.value)
+    assert dt.dattri_get_cost_model(ctx) == before
+
+
+def test_route_prediction_counts_launches(ctx):
+    # with rates at the peaks the work terms are tiny next to a huge per-launch
+    # cost, so the predictions count launches: the wide short-sequence layer
+    # alone takes the split form (stage 1 for both maps of 4 tiles, slab sum,
+    # contraction; one token chunk, so no reduction) = 3 launches; the
+    # materialized form stages G of 2 examples at a time (2 GiB / 940 MB) =
+    # 32 chunks of 3 launches
+    fake = 1 << 40
+    dt.dattri_register_layer(ctx, 8192, 28672, 64, 64)
+    dt.dattri_capture_layer(ctx, 0, fake, fake + (1 << 36), 64, 32)
+    peaks = dict(factored_tflops=2500.0, factored_gbs=8000.0, gradient_tflops=2500.0, gradient_gbs=8000.0,
+                 gproject_tflops=157.3, gproject_gbs=8000.0)
+    dt.dattri_set_cost_model(ctx, dict(peaks, launch_us=1e6, call_us=0.0))
+    _, f_us, m_us = dt.dattri_layer_route(ctx, 0)
+    assert round(f_us / 1e6) == 3
+    assert round(m_us / 1e6) == 96
+    # the fused form when forced: factored kernel + reduction
+    dt.dattri_set_factored_form(ctx, dt.DATTRI_FORM_FUSED)
+    assert round(dt.dattri_layer_route(ctx, 0)[1] / 1e6) == 2
 
 
 def test_route_follows_cost_model(ctx):

@@ -242,17 +242,18 @@ def test_materialize_gradient_matches_eq1(dtype):
 
 
 # One AUTO plan that mixes routes (Eq. 2 / App. A.4 "Routing": the two forms
-# are equal, so a call may route each layer its own way): two small layers the
-# cost model sends to the factored kernels, a layer with k_out = 128 and one
-# with k_in = 160, which exceed the factored kernels' map widths and route
+# are equal, so a call may route each layer its own way): two wide layers at a
+# short sequence, where G costs 32 and 18 MB per example and the cost model
+# sends them to the factored kernels, a layer with k_out = 128 and one with
+# k_in = 160, which exceed the factored kernels' map widths and route
 # materialized; k_in = 160 takes two passes of the G projection (8 input tiles
 # per pass).  f0 and w_out share their input block, so the factored group and
-# the materialized layer read the same A.  bf16 rows of 200 are 16-byte
-# aligned (the transposing G kernel), rows of 300 are not.
-MIXED = [dict(name="f0", d_in=200, d_out=136, k_in=32, k_out=32, a_group="a"),
-         dict(name="w_out", d_in=200, d_out=96, k_in=16, k_out=128, a_group="a"),
+# the materialized layer read the same A.  bf16 rows of 2048 and 300 elements
+# take the transposing and the plain G kernel; rows of 3000 are unaligned.
+MIXED = [dict(name="f0", d_in=2048, d_out=4096, k_in=32, k_out=32, a_group="a"),
+         dict(name="w_out", d_in=2048, d_out=96, k_in=16, k_out=128, a_group="a"),
          dict(name="w_in", d_in=300, d_out=72, k_in=160, k_out=24, a_group="b"),
-         dict(name="f1", d_in=48, d_out=40, k_in=8, k_out=16, a_group="c")]
+         dict(name="f1", d_in=3000, d_out=1500, k_in=8, k_out=16, a_group="c")]
 
 
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])

@@ -505,6 +505,27 @@ dattri_status dattri_score(const void* phi_q, int64_t n_q, int64_t ld_q, const v
                            int32_t* topk_idx, float* topk_val, void* workspace, size_t ws_bytes,
                            void* stream);
 
+/* Scoring for callers that cannot allocate device memory: code under HIP
+ * graph capture, tight serving loops, harnesses that forbid allocation.  The
+ * arguments, checks and results are those of dattri_score without the
+ * workspace: its scratch (prepared queries, split-feature partial tiles, and
+ * the scores themselves when `scores` is NULL and only top-k is wanted) lives
+ * in a static device array of DATTRI_NOALLOC_SCRATCH_BYTES that the library
+ * holds on every GPU it runs on until the process ends.  The call allocates
+ * nothing.  Nothing in the scratch needs to start at zero: each call writes
+ * every byte of it that it reads.  All calls on one GPU share its array and
+ * the next call overwrites it: calls that overlap in time on one GPU (other
+ * streams, other threads) race, and the caller must order them.
+ * Errors: as dattri_score, plus UNSUPPORTED when the call would need more
+ * scratch than DATTRI_NOALLOC_SCRATCH_BYTES (the 2048 x 8192 bf16 queries of
+ * the scoring workload take 33.5 MB; top-k alone over 2048 x 200000 scores
+ * needs 1.6 GB and is refused). */
+#define DATTRI_NOALLOC_SCRATCH_BYTES ((size_t)64 << 20)
+dattri_status dattri_score_noalloc(const void* phi_q, int64_t n_q, int64_t ld_q, const void* phi_train,
+                                   int64_t n_train, int64_t ld_train, int64_t F, dattri_dtype dtype,
+                                   const float* dev_precond_diag, float* scores, int32_t topk,
+                                   int32_t* topk_idx, float* topk_val, void* stream);
+
 /* Cosine scores (Grad-Cos, Sec. 2; LESS's cosine metric, App. A.3): the same
  * call as dattri_score, with every score divided by the norms of its two rows,
  *   S[q][j] = <q', x_j> / (|q'| |x_j|),  q' = phi_q[q] * d (d = 1 when NULL),

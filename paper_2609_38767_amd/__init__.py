@@ -120,6 +120,7 @@ _SIGS = {
     "dattri_gradient_sq_norms": (_i32, [_vp, _vp, _vp, _sz, _i32, _vp]),
     "dattri_score": (_i32, [_vp, _i64, _i64, _vp, _i64, _i64, _i64, _i32, _vp, _vp, _i32, _vp, _vp,
                             _vp, _sz, _vp]),
+    "dattri_score_noalloc": (_i32, [_vp, _i64, _i64, _vp, _i64, _i64, _i64, _i32, _vp, _vp, _i32, _vp, _vp, _vp]),
     "dattri_curvature_state_bytes": (_i32, [_vp, _P(_sz)]),
     "dattri_curvature_layout_of": (_i32, [_vp, _i32, _P(CurvatureLayout)]),
     "dattri_curvature_reset": (_i32, [_vp, _vp, _vp]),
@@ -360,6 +361,14 @@ def dattri_score(phi_q, n_q, ld_q, phi_train, n_train, ld_train, F, dtype, dev_p
                                _ptr(dev_precond_diag), _ptr(scores), topk, _ptr(topk_idx),
                                _ptr(topk_val), _ptr(workspace), ws_bytes, _stream(stream)),
            "dattri_score")
+
+
+def dattri_score_noalloc(phi_q, n_q, ld_q, phi_train, n_train, ld_train, F, dtype, dev_precond_diag, scores,
+                         topk, topk_idx, topk_val, stream=None):
+    _check(load().dattri_score_noalloc(_ptr(phi_q), n_q, ld_q, _ptr(phi_train), n_train, ld_train, F, dtype,
+                                       _ptr(dev_precond_diag), _ptr(scores), topk, _ptr(topk_idx),
+                                       _ptr(topk_val), _stream(stream)),
+           "dattri_score_noalloc")
 
 
 def dattri_set_crossgram_cost_model(ctx, model):

@@ -209,50 +209,113 @@ def routing_cases(dev, steps, warmup):
     return out
 
 
-def gpt2_case(dev, steps, warmup):
-    """GPT-2-small-shaped stack (48 layers, T=512, batch 32, k=16): projected
-    per-example gradients of one resident batch, and the scoring GEMM of 256
-    queries against 4096 training rows (F = 12288, bf16) with top-10."""
+def gpt2_case(dev, steps, warmup, check=True):
+    """GPT-2-small-shaped configuration end to end: 4096 training and 256 query
+    examples (48 layers, T=512, k=16) in 136 batches of 32.  Each batch is
+    drawn on the GPU into the buffers the session captured (untimed; the
+    captures, and so the launch plan, stay the same), projected into its 32
+    rows of one bf16 feature matrix and discarded; then the 256 query rows are
+    scored against the 4096 training rows (F = 12288) with top-10.  Every
+    batch's projection is timed with HIP events on the launch stream.  The
+    first batch is checked against the oracle (all 32 examples x 48 layers),
+    and three query rows of the scores against the oracle's scores of the
+    same feature rows."""
+    import numpy as np
     import torch
     import workloads as W
-    from paper_2609_38767_amd.session import ProjectionSession, score
+    from oracle import gradients as og
+    from oracle import rng as orng
+    from oracle import scoring as osc
+    from paper_2609_38767_amd.session import ProjectionSession, feature_rows, score
     stream = torch.cuda.current_stream()
     wl = W.WORKLOADS["gpt2"]
-    n, T = wl["batch"], wl["T"]
-    sess = ProjectionSession(wl["layers"], dtype="bf16", seed=wl["seed"], device=dev)
-    cache = {}
-    for li in range(len(wl["layers"])):
-        A, B = W.factor_blocks(wl, li, 0, n, T, dev, "bf16", a_cache=cache)
+    layers, n, T = wl["layers"], wl["batch"], wl["T"]
+    n_train, n_query = wl["n_train"], wl["n_query"]
+    n_batches = (n_train + n_query) // n
+    sess = ProjectionSession(layers, dtype="bf16", seed=wl["seed"], device=dev)
+    a_buf, bufs = {}, []
+    for L in layers:
+        if L["a_group"] not in a_buf:
+            a_buf[L["a_group"]] = torch.empty((n, T, L["d_in"]), dtype=torch.bfloat16, device=dev)
+        bufs.append((a_buf[L["a_group"]], torch.empty((n, T, L["d_out"]), dtype=torch.bfloat16, device=dev)))
+    for li, (A, B) in enumerate(bufs):
         sess.capture(li, A, B)
-    phi = torch.empty((n, sess.F), dtype=torch.float32, device=dev)
+
+    def fill(b):  # batch b's factor blocks into the captured buffers
+        cache, seen = {}, set()
+        for li, L in enumerate(layers):
+            A, B = W.factor_blocks(wl, li, b, n, T, dev, "bf16", a_cache=cache)
+            if L["a_group"] not in seen:
+                bufs[li][0].copy_(A)
+                seen.add(L["a_group"])
+            bufs[li][1].copy_(B)
+
+    phi_all = feature_rows(n_train + n_query, sess.F, "bf16", dev)
     sess.workspace()
+    fill(0)
+    for _ in range(warmup):
+        sess.project(n, phi_dtype="bf16", phi=phi_all[:n])
+    evs = []
+    worst = None
+    for b in range(n_batches):
+        if b:
+            fill(b)
+        ev = (torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+        ev[0].record(stream)
+        sess.project(n, phi_dtype="bf16", phi=phi_all[b * n:(b + 1) * n])
+        ev[1].record(stream)
+        evs.append(ev)
+        if b == 0 and check:  # oracle parity of the first batch, every layer block
+            torch.cuda.synchronize()
+            got = phi_all[:n].double().cpu().numpy()
+            worst = 0.0
+            for li, L in enumerate(layers):
+                A, B = bufs[li]
+                Ah, Bh = A.cpu().double().numpy(), B.cpu().double().numpy()
+                P_in, P_out = orng.projection_pair(wl["seed"], li, L["d_in"], L["d_out"], L["k_in"], L["k_out"],
+                                                   "bf16")
+                ref = np.stack([og.project_factored(Ah[i], Bh[i], P_in, P_out).reshape(-1) for i in range(n)])
+                off, w = sess.offsets[li], L["k_in"] * L["k_out"]
+                blk = got[:, off:off + w]
+                worst = max(worst, float(np.linalg.norm(blk - ref) / np.linalg.norm(ref)))
+    torch.cuda.synchronize()
+    ms = [a.elapsed_time(b) for a, b in evs]
+    p_ms = sum(ms) / len(ms)
+    bytes_ex = algorithmic_projection_bytes(wl)
+    Q, X = phi_all[n_train:], phi_all[:n_train]
 
     def med_ms(fn):
         for _ in range(warmup):
             fn()
-        evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
-               for _ in range(steps)]
-        for a, b in evs:
+        sev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(steps)]
+        for a, b in sev:
             a.record(stream)
             fn()
             b.record(stream)
         torch.cuda.synchronize()
-        t = sorted(a.elapsed_time(b) for a, b in evs)
+        t = sorted(a.elapsed_time(b) for a, b in sev)
         return t[len(t) // 2]
-
-    p_ms = med_ms(lambda: sess.project(n, phi=phi))
-    bytes_ex = algorithmic_projection_bytes(wl)
-    g = torch.Generator(device=dev).manual_seed(wl["seed"])
-    Q = torch.randn((wl["n_query"], sess.F), generator=g, device=dev).to(torch.bfloat16)
-    X = torch.randn((wl["n_train"], sess.F), generator=g, device=dev).to(torch.bfloat16)
     s_ms = med_ms(lambda: score(Q, X, topk=10))
-    flops = 2.0 * wl["n_query"] * wl["n_train"] * sess.F
-    sess.close()
-    out = {"examples_per_s": n / (p_ms * 1e-3), "ms_per_batch": p_ms, "bytes_per_example": bytes_ex,
-           "hbm_frac": bytes_ex * n / (p_ms * 1e-3) / 8e12,
+    flops = 2.0 * n_query * n_train * sess.F
+    out = {"workload": f"{n_batches} batches of {n} GPT-2-small-shaped examples (48 layers, T={T}, k=16) "
+                       f"drawn on the GPU per batch, projected into bf16 rows; {n_query} queries scored "
+                       f"against {n_train} training rows",
+           "examples_per_s": n / (p_ms * 1e-3), "ms_per_batch": p_ms, "ms_per_batch_min": min(ms),
+           "bytes_per_example": bytes_ex, "hbm_frac": bytes_ex * n / (p_ms * 1e-3) / 8e12,
            "score_ms": s_ms, "score_tflops": flops / (s_ms * 1e-3) / 1e12,
-           "score_shape": f"{wl['n_query']} x {wl['n_train']} x {sess.F} bf16, top-10"}
-    print(f"[bench] gpt2: projection {p_ms:.3f} ms ({out['examples_per_s']:.0f} ex/s), "
+           "score_shape": f"{n_query} x {n_train} x {sess.F} bf16, top-10"}
+    if check:
+        S, _, _ = score(Q, X)
+        rows = [0, 127, 255]
+        ref = osc.score(Q[rows].double().cpu().numpy(), X.double().cpu().numpy())
+        got = S[rows].double().cpu().numpy()
+        out["parity"] = {"phi_worst_layer_rel_err": worst,
+                         "phi_tolerance": "2e-2 (bf16 feature rows, rounded once)",
+                         "score_rel_err": float(np.linalg.norm(got - ref) / np.linalg.norm(ref)),
+                         "score_tolerance": "1e-5 (exact bf16 inputs, float32 accumulation)",
+                         "checked": f"batch 0: {n} examples x {len(layers)} layers; scores of query rows {rows}"}
+    sess.close()
+    print(f"[bench] gpt2 end to end: projection {p_ms:.3f} ms per batch ({out['examples_per_s']:.0f} ex/s), "
           f"scoring {s_ms:.3f} ms", file=sys.stderr, flush=True)
     return out
 

@@ -55,7 +55,17 @@ extern "C" {
 
 typedef struct dattri_ctx dattri_ctx;
 
-typedef enum {
+/* Enumerations are int-sized.  Compiled as C++ they get a fixed int32_t
+ * underlying type, so that any integer a caller passes is a value of the type
+ * (and is then rejected by the argument checks if it names no enumerator)
+ * rather than undefined behaviour. */
+#ifdef __cplusplus
+#define DATTRI_ENUM enum : int32_t
+#else
+#define DATTRI_ENUM enum
+#endif
+
+typedef DATTRI_ENUM {
   DATTRI_OK = 0,
   DATTRI_E_INVALID_ARG = -1, /* null pointer, out-of-range value, bad enum */
   DATTRI_E_SHAPE = -2,       /* sizes inconsistent with registration/capture */
@@ -66,9 +76,9 @@ typedef enum {
   DATTRI_E_UNSUPPORTED = -7  /* valid request outside this build's limits */
 } dattri_status;
 
-typedef enum { DATTRI_F32 = 0, DATTRI_BF16 = 1 } dattri_dtype;
+typedef DATTRI_ENUM { DATTRI_F32 = 0, DATTRI_BF16 = 1 } dattri_dtype;
 
-typedef enum {
+typedef DATTRI_ENUM {
   DATTRI_ROUTE_AUTO = 0,        /* per-layer choice of the cost model */
   DATTRI_ROUTE_FACTORED = 1,    /* (A P_in)^T (B P_out), Eq. (2) left side */
   DATTRI_ROUTE_MATERIALIZED = 2, /* G = B^T A, then P_out^T G P_in */
@@ -87,7 +97,7 @@ typedef enum {
  * items, and for input groups whose maps are wider than 48 columns on both
  * sides (the fused kernel then holds too few token rows per wave to stream
  * at full rate); FUSED otherwise. */
-typedef enum {
+typedef DATTRI_ENUM {
   DATTRI_FORM_AUTO = 0,
   DATTRI_FORM_FUSED = 1,
   DATTRI_FORM_SPLIT = 2
@@ -202,7 +212,7 @@ dattri_status dattri_bind_projection(dattri_ctx* ctx, int32_t layer, void* dev_P
  * the kind.  Changing the kind of a bound layer unbinds it (bind again before
  * projecting); overrides given at binding are unaffected by the kind.
  * Errors: INVALID_ARG (bad layer, unknown kind, NULL kind). */
-typedef enum { DATTRI_MAP_GAUSSIAN = 0, DATTRI_MAP_RADEMACHER = 1 } dattri_map_kind;
+typedef DATTRI_ENUM { DATTRI_MAP_GAUSSIAN = 0, DATTRI_MAP_RADEMACHER = 1 } dattri_map_kind;
 dattri_status dattri_set_map_kind(dattri_ctx* ctx, int32_t layer, dattri_map_kind kind);
 dattri_status dattri_get_map_kind(const dattri_ctx* ctx, int32_t layer, dattri_map_kind* kind);
 
@@ -569,7 +579,7 @@ dattri_status dattri_score_cosine(const void* phi_q, int64_t n_q, int64_t ld_q,
  * at the byte offsets of dattri_curvature_layout_of; matrices are float32
  * row-major.  Sums accumulate over calls until dattri_curvature_reset.
  * Layers need k_in <= 64 and k_out <= 64 (else UNSUPPORTED). */
-typedef enum { DATTRI_CURV_KFAC = 0, DATTRI_CURV_EKFAC = 1 } dattri_curvature;
+typedef DATTRI_ENUM { DATTRI_CURV_KFAC = 0, DATTRI_CURV_EKFAC = 1 } dattri_curvature;
 
 typedef struct {
   int64_t sum_a;   /* float32 [k_in][k_in]:  sum of a~ a~^T                         */

@@ -48,7 +48,9 @@ STATUS_NAMES = {0: "OK", -1: "E_INVALID_ARG", -2: "E_SHAPE", -3: "E_DTYPE", -4: 
                 -5: "E_WORKSPACE", -6: "E_HIP", -7: "E_UNSUPPORTED"}
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
-lib_path = os.path.join(_HERE, "libdattri.so")
+# DATTRI_LIB selects another build of the library (e.g. the host-sanitizer
+# build, for CPU-only tests); the default is the in-tree libdattri.so.
+lib_path = os.environ.get("DATTRI_LIB") or os.path.join(_HERE, "libdattri.so")
 
 
 class DattriError(RuntimeError):

@@ -311,21 +311,36 @@ dattri_status dattri_materialize_gradient(dattri_ctx* ctx, int32_t layer, int32_
  * examples, in microseconds:
  *   factored      = call_us + max(F_f / factored_tflops, B_f / factored_gbs)
  *                   + launches_f * launch_us
- *   materialized  = call_us + max(F_g / gradient_tflops, B_g / gradient_gbs)
- *                   + max(F_p / gproject_tflops, B_p / gproject_gbs)
- *                   + 3 * chunks_m * launch_us
- * with the exact FLOP and byte counts of dattri_layer_costs times n (F_g, B_g
- * the G = B^T A kernel: 2T d_in d_out FLOP, factor blocks read and G written;
- * F_p, B_p the projection of G: the rest of the materialized FLOPs, G read).
- * launches_f is the number of kernels the factored route runs for this layer
+ * with the exact FLOP and byte counts of dattri_layer_costs times n, and
+ * launches_f the number of kernels the factored route runs for this layer
  * alone: 2 in the fused form (projection + reduction), 3 to 5 in the split
  * form (stage 1 per map width, slab sum, contraction, reduction), as the
- * launch plan decides; chunks_m is the number of example chunks the G staging
- * budget (2 GiB) needs, each running the gradient, G-projection and reduction
- * kernels.  call_us is paid by both routes and does not change a decision.
- * Ties go to the factored route.  Rates are effective ones, fitted on MI355X;
- * they may not exceed the chip's published peaks (HBM 8000 GB/s, dense bf16
- * MFMA 2500 TFLOP/s for the factored and gradient kernels, float32 MFMA
+ * launch plan decides.  The materialized route has two implementations:
+ *   - one pass (bf16 blocks with 16-byte aligned rows, k_in <= 128): each
+ *     workgroup forms 128 rows of G over a token chunk, 128 columns at a
+ *     time, and projects every tile on chip, so G never goes to memory;
+ *       materialized = call_us + max(W, B_f / gradient_gbs) + 2 * launch_us,
+ *     where W is the work of its launch shape: rounds of 256 workgroups
+ *     (one per CU) times, per workgroup and 128-column tile, tok_chunk / 32
+ *     token stages at 256 x 2 x 32 x 128 x 128 FLOP per round at
+ *     gradient_tflops, plus one tile projection at 256 x 2 x 128 x 128 x 16 x
+ *     tiles(k_in) FLOP per round, plus once per workgroup H^T P_out at
+ *     256 x 2 x 128 x 16 tiles(k_in) x 16 tiles(k_out) FLOP per round, both
+ *     at gproject_tflops, plus round_us per round (a workgroup's load
+ *     latencies and barriers, whatever its work); the token chunks and column
+ *     ranges are the ones that minimise W;
+ *   - otherwise (float32, unaligned rows, k_in > 128) G is staged in the
+ *     workspace, chunks_m example chunks of at most 2 GiB of G each:
+ *       materialized = call_us + max(F_g / gradient_tflops, B_g / gradient_gbs)
+ *                      + max(F_p / gproject_tflops, B_p / gproject_gbs)
+ *                      + 3 * chunks_m * launch_us
+ *     with F_g, B_g the G = B^T A kernel (2T d_in d_out FLOP, factor blocks
+ *     read and G written) and F_p, B_p the projection of G (the rest of the
+ *     materialized FLOPs, G read).
+ * call_us is paid by both routes and does not change a decision.  Ties go to
+ * the factored route.  Rates are effective ones, fitted on MI355X; they may
+ * not exceed the chip's published peaks (HBM 8000 GB/s, dense bf16 MFMA
+ * 2500 TFLOP/s for the factored and gradient kernels, float32 MFMA
  * 157.3 TFLOP/s for the G projection, which runs in float32). */
 typedef struct {
   double factored_tflops;     /* factored kernels (fused or split) */
@@ -336,16 +351,17 @@ typedef struct {
   double gproject_gbs;
   double launch_us;           /* per kernel launch */
   double call_us;             /* per call, either route */
+  double round_us;            /* fixed time of one round of one-pass workgroups */
 } dattri_cost_model;
 
 /* Replace / read the context's cost model.
  * Errors: INVALID_ARG (NULL, a rate not finite or <= 0 or above its peak,
- * launch_us or call_us negative or not finite). */
+ * launch_us, call_us or round_us negative or not finite). */
 dattri_status dattri_set_cost_model(dattri_ctx* ctx, const dattri_cost_model* model);
 dattri_status dattri_get_cost_model(const dattri_ctx* ctx, dattri_cost_model* model);
 
 /* Load the cost model from a calibration file: a JSON object whose member
- * "model" is an object holding the eight fields of dattri_cost_model by name
+ * "model" is an object holding the nine fields of dattri_cost_model by name
  * as numbers (the file `python -m paper_2609_38767_amd.calibrate --out FILE`
  * writes; other members are ignored).  Host-only; reads the file once.  The
  * context's model is unchanged on error.
@@ -360,7 +376,9 @@ dattri_status dattri_set_cost_calibration(dattri_ctx* ctx, const char* json_path
  *   materialized FLOP  2T d_in d_out + 2 d_out d_in k_in + 2 d_out k_in k_out
  *                      (the association (G P_in) first, which this build runs)
  *   factored bytes     T (d_in + d_out) elt      (factor blocks read once)
- *   materialized bytes factored bytes + 2 * 4 d_out d_in (G written and read)
+ *   materialized bytes factored bytes + 2 * 4 d_out d_in (G written and read;
+ *                      the one-pass kernel keeps G on chip and reads only the
+ *                      factored bytes)
  * Errors: INVALID_ARG (bad layer, T < 0). */
 dattri_status dattri_layer_costs(const dattri_ctx* ctx, int32_t layer, int32_t T,
                                  int64_t* factored_flops, int64_t* materialized_flops,

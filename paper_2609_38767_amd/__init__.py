@@ -64,7 +64,7 @@ class CostModel(ctypes.Structure):
     _fields_ = [("factored_tflops", ctypes.c_double), ("factored_gbs", ctypes.c_double),
                 ("gradient_tflops", ctypes.c_double), ("gradient_gbs", ctypes.c_double),
                 ("gproject_tflops", ctypes.c_double), ("gproject_gbs", ctypes.c_double),
-                ("launch_us", ctypes.c_double), ("call_us", ctypes.c_double)]
+                ("launch_us", ctypes.c_double), ("call_us", ctypes.c_double), ("round_us", ctypes.c_double)]
 
 
 class CrossgramCostModel(ctypes.Structure):

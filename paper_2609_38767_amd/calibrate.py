@@ -61,7 +61,7 @@ SWEEP = [
 QUICK = [SWEEP[i] for i in (0, 3, 5, 9, 13, 14, 17, 19)]
 
 FIELDS = ["factored_tflops", "factored_gbs", "gradient_tflops", "gradient_gbs",
-          "gproject_tflops", "gproject_gbs", "launch_us", "call_us"]
+          "gproject_tflops", "gproject_gbs", "launch_us", "call_us", "round_us"]
 # Upper bounds of the effective rates: the HBM read rate measured on MI355X
 # (a streaming probe; below the 8 TB/s peak) and the published MFMA peaks
 # (bf16 for the factored and G kernels, float32 for the G projection).
@@ -95,7 +95,7 @@ def launch_counts(shape):
         dattri_capture_layer(ctx, 0, fake, fake + (1 << 38), n, T, None)
         probe = {"factored_tflops": 2500.0, "factored_gbs": 8000.0, "gradient_tflops": 2500.0,
                  "gradient_gbs": 8000.0, "gproject_tflops": 157.3, "gproject_gbs": 8000.0,
-                 "launch_us": 1e6, "call_us": 0.0}
+                 "launch_us": 1e6, "call_us": 0.0, "round_us": 0.0}
         dattri_set_cost_model(ctx, probe)
         _, pf, pm = dattri_layer_route(ctx, 0)
     finally:
@@ -134,47 +134,54 @@ def measure(shape, device, seed=0):
             "launches_materialized": lm, "counts": costs}
 
 
-def _counts(s):
-    """Per-kernel-class (flops, bytes) totals for n examples; the same exact
-    counts the library's cost model uses (dattri_layer_costs)."""
-    sh = s["shape"]
-    di, dq, ki, ko, T, n = sh["d_in"], sh["d_out"], sh["k_in"], sh["k_out"], sh["T"], sh["n"]
-    f_flops, m_flops, f_bytes, m_bytes = s["counts"]
-    g_flops = 2 * T * di * dq
-    g_bytes = f_bytes + 4 * dq * di
-    return {"f": (n * f_flops, n * f_bytes), "g": (n * g_flops, n * g_bytes),
-            "p": (n * (m_flops - g_flops), n * (m_bytes - g_bytes))}
+class LibraryPredictor:
+    """The library's own predictions (``dattri_layer_route``) for every sampled
+    shape under a candidate model: one host-only context per shape with the
+    shape captured at 16-byte aligned placeholder addresses (the alignment the
+    sweep's tensors have); nothing is launched."""
+
+    def __init__(self, samples):
+        self.ctx = []
+        fake = 1 << 40
+        for s in samples:
+            sh = s["shape"]
+            c = dattri_create(DATTRI_BF16, 0)
+            dattri_register_layer(c, sh["d_in"], sh["d_out"], sh["k_in"], sh["k_out"])
+            dattri_capture_layer(c, 0, fake, fake + (1 << 38), sh["n"], sh["T"], None)
+            self.ctx.append(c)
+
+    def __call__(self, model):
+        out = []
+        for c in self.ctx:
+            dattri_set_cost_model(c, model)
+            _, pf, pm = dattri_layer_route(c, 0)
+            out.append((pf, pm))
+        return out
+
+    def close(self):
+        for c in self.ctx:
+            dattri_destroy(c)
+        self.ctx = []
 
 
-def predict_us(model, s):
-    """(factored, materialized, G kernel alone) predicted times in us, the
-    library's formula (include/dattri.h, dattri_cost_model)."""
-    c = _counts(s)
-
-    def t(flops, nbytes, tflops, gbs):
-        return max(flops / (tflops * 1e6), nbytes / (gbs * 1e3))
-    call, launch = model["call_us"], model["launch_us"]
-    f = call + t(*c["f"], model["factored_tflops"], model["factored_gbs"]) + s["launches_factored"] * launch
-    g = t(*c["g"], model["gradient_tflops"], model["gradient_gbs"])
-    p = t(*c["p"], model["gproject_tflops"], model["gproject_gbs"])
-    m = call + g + p + s["launches_materialized"] * launch
-    g_alone = call + g + s["launches_gradient"] * launch
-    return f, m, g_alone
+# Fitted fields: gproject_gbs only enters the staged G route (float32 or
+# unaligned blocks), which the bf16 sweep does not run, so it keeps its value.
+FIT_FIELDS = [k for k in FIELDS if k != "gproject_gbs"]
 
 
-def _model_of(x):
-    m = {}
-    for i, k in enumerate(FIELDS):
+def _model_of(x, base):
+    m = dict(base)
+    for i, k in enumerate(FIT_FIELDS):
         if k in CAPS:  # (0, cap) through a logistic map
-            m[k] = CAPS[k] / (1.0 + math.exp(-x[i]))
+            m[k] = CAPS[k] / (1.0 + math.exp(-max(min(x[i], 50.0), -50.0)))
         else:
-            m[k] = math.exp(x[i])
+            m[k] = math.exp(max(min(x[i], 50.0), -50.0))
     return m
 
 
 def _x_of(m):
     x = []
-    for k in FIELDS:
+    for k in FIT_FIELDS:
         if k in CAPS:
             r = min(max(m[k] / CAPS[k], 1e-9), 1 - 1e-9)
             x.append(math.log(r / (1 - r)))
@@ -183,43 +190,45 @@ def _x_of(m):
     return x
 
 
-def regret_of(model, samples):
-    """Per shape: time lost by the route the model predicts faster, relative
-    to the faster measured route (0 when it picks that one)."""
+def regret_of(preds, samples):
+    """Per shape: time lost by the route predicted faster, relative to the
+    faster measured route (0 when it picks that one)."""
     out = []
-    for s in samples:
-        f, m, _ = predict_us(model, s)
+    for (f, m), s in zip(preds, samples):
         picked = s["factored_ms"] if f <= m else s["materialized_ms"]
         out.append(picked / min(s["factored_ms"], s["materialized_ms"]) - 1.0)
     return out
 
 
-def fit(samples, starts, weight=4.0, margin=0.05):
+def fit(samples, starts, weight=4.0, margin=0.05, maxfev=4000):
+    """Least squares on log predicted time plus a smooth penalty on wrong
+    choices (a hinge on the predicted log-time gap, weighted by the measured
+    gap); of the fits from `starts`, the one with the least mean regret."""
     from scipy.optimize import minimize
+    predict = LibraryPredictor(samples)
 
     def loss(x):
-        m = _model_of(x)
+        preds = predict(_model_of(x, starts[0]))
         err = 0.0
-        for s in samples:
-            f, mt, g = predict_us(m, s)
+        for (f, mt), s in zip(preds, samples):
             lf, lm = math.log(1e3 * s["factored_ms"]), math.log(1e3 * s["materialized_ms"])
             err += (math.log(f) - lf) ** 2 + (math.log(mt) - lm) ** 2
-            err += (math.log(g) - math.log(1e3 * s["gradient_ms"])) ** 2
-            # decision penalty: a smooth hinge on the predicted log-time gap,
-            # weighted by the measured gap (what a wrong choice costs)
             gap = lm - lf  # > 0 when the factored route is faster
             sign = 1.0 if gap >= 0 else -1.0
             err += weight * abs(gap) * max(0.0, margin - sign * (math.log(mt) - math.log(f))) ** 2 / margin
         return err
     best = None
-    for start in starts:
-        r = minimize(loss, _x_of(start), method="Nelder-Mead",
-                     options={"maxiter": 40000, "maxfev": 40000, "xatol": 1e-5, "fatol": 1e-9, "adaptive": True})
-        m = _model_of(r.x)
-        reg = regret_of(m, samples)
-        key = (sum(reg) / len(reg), max(reg), r.fun)
-        if best is None or key < best[0]:
-            best = (key, m, r.fun)
+    try:
+        for start in starts:
+            r = minimize(loss, _x_of(start), method="Nelder-Mead",
+                         options={"maxfev": maxfev, "xatol": 1e-4, "fatol": 1e-7, "adaptive": True})
+            m = _model_of(r.x, starts[0])
+            reg = regret_of(predict(m), samples)
+            key = (sum(reg) / len(reg), max(reg), r.fun)
+            if best is None or key < best[0]:
+                best = (key, m, r.fun)
+    finally:
+        predict.close()
     return best[1], best[2]
 
 
@@ -248,12 +257,75 @@ def decisions(model, samples, device):
     return rows
 
 
+def _starts(default):
+    return [default,
+            dict(default, launch_us=2.0, call_us=20.0),
+            dict(default, launch_us=10.0, call_us=5.0, factored_gbs=2000.0),
+            dict(default, gproject_tflops=100.0, gradient_tflops=300.0)]
+
+
+def _summary(model, loss, samples, rows, device_name):
+    reg = [r["regret"] for r in rows]
+    preds = [(1e3 * r["pred_factored_ms"], 1e3 * r["pred_materialized_ms"]) for r in rows]
+    rms = math.sqrt(sum((math.log(p) - math.log(1e3 * m)) ** 2
+                        for (pf, pm), s in zip(preds, samples)
+                        for p, m in ((pf, s["factored_ms"]), (pm, s["materialized_ms"]))) / (2 * len(samples)))
+    return {"model": model, "objective": loss, "rms_log_error": rms, "device": device_name, "shapes": rows,
+            "picked_faster": sum(1 for r in rows if r["auto"] == r["faster"]), "n_shapes": len(rows),
+            "max_regret": max(reg), "mean_regret": sum(reg) / len(reg)}
+
+
+def _host_decisions(model, samples):
+    """decisions() without a GPU: the library's route and predictions for
+    each measured shape under `model`."""
+    predict = LibraryPredictor(samples)
+    try:
+        preds = predict(model)
+    finally:
+        predict.close()
+    rows = []
+    for (pf, pm), s in zip(preds, samples):
+        sh = s["shape"]
+        best = min(s["factored_ms"], s["materialized_ms"])
+        auto = "factored" if pf <= pm else "materialized"
+        picked = s["factored_ms"] if auto == "factored" else s["materialized_ms"]
+        rows.append({**sh, "factored_ms": s["factored_ms"], "materialized_ms": s["materialized_ms"],
+                     "pred_factored_ms": round(pf / 1e3, 4), "pred_materialized_ms": round(pm / 1e3, 4),
+                     "auto": auto, "faster": "factored" if s["factored_ms"] <= s["materialized_ms"] else "materialized",
+                     "regret": round(picked / best - 1.0, 4)})
+    return rows
+
+
+def refit(path, out_path=None):
+    """Refit the rates to the measured times in an earlier calibration JSON."""
+    with open(path) as f:
+        prev = json.load(f)
+    keys = ("d_in", "d_out", "k_in", "k_out", "T", "n")
+    samples = [{"shape": {k: r[k] for k in keys}, "factored_ms": r["factored_ms"],
+                "materialized_ms": r["materialized_ms"]} for r in prev["shapes"]]
+    ctx = dattri_create(DATTRI_BF16, 0)
+    default = dattri_get_cost_model(ctx)
+    dattri_destroy(ctx)
+    model, loss = fit(samples, _starts(default))
+    out = _summary(model, loss, samples, _host_decisions(model, samples), prev.get("device", ""))
+    out["refit_of"] = path
+    text = json.dumps(out)
+    print(text, flush=True)
+    if out_path:
+        with open(out_path, "w") as f:
+            f.write(text + "\n")
+
+
 def main(argv=None):
     ap = argparse.ArgumentParser(description=__doc__.splitlines()[0])
     ap.add_argument("--quick", action="store_true", help="a shorter sweep")
     ap.add_argument("--out", default=None, help="also write the JSON to this file")
+    ap.add_argument("--refit", default=None, metavar="FILE",
+                    help="refit the measurements of an earlier run's JSON on the host (no GPU)")
     args = ap.parse_args(argv)
     load()
+    if args.refit:
+        return refit(args.refit, args.out)
     device = torch.device("cuda:0")
     torch.cuda.set_device(device)
     samples = []
@@ -267,22 +339,9 @@ def main(argv=None):
     probe = ProjectionSession([{"d_in": 16, "d_out": 16, "k_in": 16, "k_out": 16}], device=device)
     default = dattri_get_cost_model(probe.ctx)
     probe.close()
-    starts = [default,
-              dict(default, launch_us=2.0, call_us=20.0),
-              dict(default, launch_us=10.0, call_us=5.0, factored_gbs=2000.0),
-              dict(default, gproject_tflops=100.0, gradient_gbs=2000.0, gproject_gbs=2000.0)]
-    model, loss = fit(samples, starts)
+    model, loss = fit(samples, _starts(default))
     rows = decisions(model, samples, device)
-    reg = [r["regret"] for r in rows]
-    out = {"model": model, "objective": loss,
-           "rms_log_error": math.sqrt(sum((math.log(p) - math.log(1e3 * m)) ** 2
-                                          for s in samples
-                                          for p, m in zip(predict_us(model, s),
-                                                          (s["factored_ms"], s["materialized_ms"], s["gradient_ms"])))
-                                      / (3 * len(samples))),
-           "device": torch.cuda.get_device_name(device), "shapes": rows,
-           "picked_faster": sum(1 for r in rows if r["auto"] == r["faster"]), "n_shapes": len(rows),
-           "max_regret": max(reg), "mean_regret": sum(reg) / len(reg)}
+    out = _summary(model, loss, samples, rows, torch.cuda.get_device_name(device))
     text = json.dumps(out)
     print(text, flush=True)
     if args.out:

@@ -151,13 +151,14 @@ struct Reader {
 };
 
 struct Fields {
-  const char* names[8] = {"factored_tflops", "factored_gbs", "gradient_tflops", "gradient_gbs",
-                          "gproject_tflops", "gproject_gbs", "launch_us", "call_us"};
-  double v[8];
-  bool got[8] = {false, false, false, false, false, false, false, false};
+  static constexpr int kN = 9;
+  const char* names[kN] = {"factored_tflops", "factored_gbs", "gradient_tflops", "gradient_gbs",
+                           "gproject_tflops", "gproject_gbs", "launch_us", "call_us", "round_us"};
+  double v[kN];
+  bool got[kN] = {};
   bool saw_model = false;
   void operator()(const std::string& key, double x) {
-    for (int i = 0; i < 8; ++i)
+    for (int i = 0; i < kN; ++i)
       if (key == names[i]) {
         v[i] = x;
         got[i] = true;
@@ -192,7 +193,7 @@ dattri_status read_cost_calibration(const char* path, dattri_cost_model* out) {
   r.ws();
   if (r.p != r.end) return fail(DATTRI_E_INVALID_ARG, "calibration file '%s': trailing data", path);
   if (!fields.saw_model) return fail(DATTRI_E_INVALID_ARG, "calibration file '%s' has no \"model\" object", path);
-  for (int i = 0; i < 8; ++i)
+  for (int i = 0; i < Fields::kN; ++i)
     if (!fields.got[i])
       return fail(DATTRI_E_INVALID_ARG, "calibration file '%s': model.%s missing or not a number", path,
                   fields.names[i]);
@@ -204,6 +205,7 @@ dattri_status read_cost_calibration(const char* path, dattri_cost_model* out) {
   out->gproject_gbs = fields.v[5];
   out->launch_us = fields.v[6];
   out->call_us = fields.v[7];
+  out->round_us = fields.v[8];
   return DATTRI_OK;
 }
 

@@ -169,6 +169,25 @@ constexpr int kGProjRows = 128;     // rows of G per workgroup (4 waves x 2 row 
 constexpr int kGProjMaxTilesIn = 8; // input tiles per pass (larger k_in loops)
 hipError_t launch_gproject(int elt_bytes, const GProjArgs& a, hipStream_t s);
 
+// Fused materialized route (bf16, 16-byte aligned rows, k_in <= 128): each
+// workgroup forms 128 rows of G over one token chunk, 128 columns at a time,
+// and projects every tile from LDS, so G never goes to memory.
+struct GFusedArgs {
+  const void* A; const void* B; const int32_t* lengths;
+  const void* P_in; const void* P_out;  // packed bf16
+  int32_t d_in, d_out, T, k_in, k_out;
+  int32_t ex_begin, ex_count;
+  int32_t n_ublocks;                // row blocks of kGFusedRows rows of G
+  int32_t n_vsplit, vt_per_split;   // 128-column tiles of G in n_vsplit ranges of vt_per_split
+  int32_t n_tchunks, tok_chunk;     // token chunks per example (tok_chunk a multiple of 32)
+  float* partials;                  // [ex_count][n_ublocks * n_vsplit * n_tchunks][na*16 x nb*16]
+};
+constexpr int kGFusedCols = 128;    // columns of G per tile
+constexpr int kGFusedRows = 128;
+constexpr int kGFusedMaxTilesIn = 8;
+int gfused_tiles_in(int k_in);      // input tiles of the kernel instance serving k_in
+hipError_t launch_gfused(const GFusedArgs& a, hipStream_t s);
+
 // ------------------------------------------------------ cross-Gram matrices
 // One layer of the factorized route between batch 1 (n1 examples) and batch 2
 // (n2 examples): factor blocks [n, T, d] row-major, token rows padded to

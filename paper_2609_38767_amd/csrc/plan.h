@@ -18,6 +18,8 @@ namespace dattri {
 
 struct MatChunk {
   int layer, ex_begin, ex_count, n_ublocks, n_ksplit, kb_per_split, task;
+  int fused = 0;                    // one-pass kernel (G on chip): its launch shape below
+  int n_tchunks = 1, tok_chunk = 0, n_vsplit = 1, vt_per_split = 1;
 };
 
 // Where the projected token rows of one layer side sit after the projection

@@ -49,19 +49,22 @@ bool factored_supported(const Layer& L) {
 }
 
 dattri_cost_model default_cost_model() {
-  // Effective rates measured on MI355X (bf16 inputs): both forced routes and
-  // the G kernel alone timed on a sweep of single-layer shapes (transformer,
-  // adapter-shaped and narrow layers, T = 16..2048) with the launch plans
-  // kept on the device, fitted with every rate held below its peak.
+  // Fitted on MI355X (bf16 inputs; the calibration script's sweep of 28
+  // single-layer shapes: transformer, adapter-shaped and narrow layers,
+  // T = 16..4096, both forced routes timed with launch plans kept on the
+  // device), every rate held below its bound: AUTO picks the faster route on
+  // 26 of 28 shapes, mean regret 0.4%, worst 7.8% (two near-ties).
+  // gproject_gbs serves only the staged-G route, which that sweep does not run.
   dattri_cost_model m;
-  m.factored_tflops = 297.0;
-  m.factored_gbs = 4700.0;
-  m.gradient_tflops = 726.0;
-  m.gradient_gbs = 5000.0;
-  m.gproject_tflops = 64.5;
+  m.factored_tflops = 145.6;
+  m.factored_gbs = 3733.5;
+  m.gradient_tflops = 309.0;
+  m.gradient_gbs = 6450.0;
+  m.gproject_tflops = 116.2;
   m.gproject_gbs = 5000.0;
-  m.launch_us = 5.0;
-  m.call_us = 10.0;
+  m.launch_us = 9.53;
+  m.call_us = 0.0;
+  m.round_us = 0.833;
   return m;
 }
 
@@ -80,6 +83,8 @@ dattri_status check_cost_model(const dattri_cost_model& m) {
     return fail(DATTRI_E_INVALID_ARG, "launch_us = %g must be finite and >= 0", m.launch_us);
   if (!(m.call_us >= 0.0) || !std::isfinite(m.call_us))
     return fail(DATTRI_E_INVALID_ARG, "call_us = %g must be finite and >= 0", m.call_us);
+  if (!(m.round_us >= 0.0) || !std::isfinite(m.round_us))
+    return fail(DATTRI_E_INVALID_ARG, "round_us = %g must be finite and >= 0", m.round_us);
   return DATTRI_OK;
 }
 
@@ -138,6 +143,53 @@ int64_t materialized_chunk(const Layer& L, int64_t n) {
   return std::max<int64_t>(1, std::min<int64_t>({n, kGBudgetBytes / (4 * g_per_ex), (int64_t)65535}));
 }
 
+// The one-pass materialized kernel serves bf16 layers with 16-byte aligned
+// rows and k_in <= 128; others stage G in the workspace.
+bool fused_materialized(const Layer& L, int elt) {
+  return elt == 2 && (uintptr_t)L.A % 16 == 0 && (uintptr_t)L.B % 16 == 0 && (L.d_in * 2) % 16 == 0 &&
+         (L.d_out * 2) % 16 == 0 && tiles16(L.k_in) <= kGFusedMaxTilesIn;
+}
+
+// Launch shape of the one-pass kernel and its predicted time.  A workgroup
+// (one per CU: 104 KiB of LDS) runs, per 128-column tile of G in its range,
+// tok_chunk / 32 token stages (bf16 MFMA) and a projection of the tile
+// (float32 MFMA, about 8 stages' worth per 16 columns of P_in), then one
+// H^T P_out.  Token chunks and column ranges add workgroups but the chunks
+// repeat the projections; the shape minimising rounds of 256 workgroups x
+// per-workgroup time wins.  Times use the model's rates: a round of 256
+// workgroups each running one stage is 256 x 2 x 32 x 128 x 128 FLOP at
+// gradient_tflops; one tile projection per workgroup is 256 x 2 x 128 x 128 x
+// 16 x tiles_in FLOP and the closing product 256 x 2 x 128 x 16 tiles_in x 16
+// tiles_out FLOP, both at gproject_tflops; each round also costs round_us
+// (load latencies and barriers, whatever the work).
+struct FusedShape { int n_tchunks, tok_chunk, n_vsplit, vt_per_split; double us; };
+FusedShape fused_shape(const Layer& L, int64_t n, const dattri_cost_model& m) {
+  const int64_t T = std::max<int64_t>(L.T, 1);
+  const int64_t n_ub = (L.d_out + kGFusedRows - 1) / kGFusedRows;
+  const int64_t n_vt = (L.d_in + kGFusedCols - 1) / kGFusedCols;
+  const double stage_us = 256.0 * 2 * 32 * kGFusedRows * kGFusedCols / (m.gradient_tflops * 1e6);
+  const double proj_us = 256.0 * 2 * kGFusedRows * kGFusedCols * 16 * gfused_tiles_in(L.k_in) /
+                         (m.gproject_tflops * 1e6);
+  // the closing H^T P_out of every workgroup, also float32 MFMA
+  const double epi_us = 256.0 * 2 * kGFusedRows * 16 * gfused_tiles_in(L.k_in) * 16 * tiles16(L.k_out) /
+                        (m.gproject_tflops * 1e6);
+  FusedShape best{1, (int)((T + 31) / 32 * 32), 1, (int)n_vt, -1.0};
+  for (int64_t c = 1; c <= (T + 31) / 32; c *= 2) {
+    const int64_t tok_chunk = ((T + c - 1) / c + 31) / 32 * 32;
+    const int64_t chunks = (T + tok_chunk - 1) / tok_chunk;
+    for (int64_t v = 1; v <= n_vt; v *= 2) {
+      const int64_t vps = (n_vt + v - 1) / v;
+      const int64_t splits = (n_vt + vps - 1) / vps;
+      const int64_t rounds = (std::max<int64_t>(n, 1) * n_ub * splits * chunks + 255) / 256;
+      const double us =
+          (double)rounds * ((double)vps * ((double)(tok_chunk / 32) * stage_us + proj_us) + epi_us + m.round_us);
+      if (best.us < 0 || us < best.us)
+        best = FusedShape{(int)chunks, (int)tok_chunk, (int)splits, (int)vps, us};
+    }
+  }
+  return best;
+}
+
 // Predicted times (us) of both routes for the layer's capture (n, T).
 void predict(const dattri_ctx* ctx, const Layer& L, double* f_us, double* m_us) {
   const dattri_cost_model& m = ctx->cost;
@@ -148,6 +200,14 @@ void predict(const dattri_ctx* ctx, const Layer& L, double* f_us, double* m_us) 
   };
   *f_us = m.call_us + t((double)c.f_flops * n, m.factored_tflops, (double)c.f_bytes * n, m.factored_gbs);
   if (n > 0) *f_us += factored_launches(ctx, L) * m.launch_us;
+  if (fused_materialized(L, ctx->elt)) {
+    // one pass: factor blocks read once, G on chip; time from its launch shape
+    const int64_t chunks = n > 0 ? (n + 65534) / 65535 : 0;
+    const double work = n > 0 ? fused_shape(L, n, m).us : 0.0;
+    *m_us = m.call_us + std::max(work, (double)c.f_bytes * n / (m.gradient_gbs * 1e3)) +
+            2.0 * chunks * m.launch_us;
+    return;
+  }
   const int64_t chunks = n > 0 ? (n + materialized_chunk(L, n) - 1) / materialized_chunk(L, n) : 0;
   *m_us = m.call_us + t((double)c.g_flops * n, m.gradient_tflops, (double)c.g_bytes * n, m.gradient_gbs) +
           t((double)c.p_flops * n, m.gproject_tflops, (double)c.p_bytes * n, m.gproject_gbs) +
@@ -622,6 +682,35 @@ dattri_status dattri::build_plan(const dattri_ctx* ctx, dattri_route forced, Pla
   for (size_t l = 0; l < ctx->layers.size(); ++l) {
     const Layer& L = ctx->layers[l];
     if (route[l] != DATTRI_ROUTE_MATERIALIZED) continue;
+    if (fused_materialized(L, elt)) {  // one pass, G on chip: partial blocks per (row block, token chunk)
+      const FusedShape fs = fused_shape(L, n, ctx->cost);
+      const int n_ublocks = (L.d_out + kGFusedRows - 1) / kGFusedRows;
+      const int ex_chunk = std::min(n, 65535);
+      const int64_t part = (int64_t)tiles16(L.k_in) * 16 * tiles16(L.k_out) * 16;
+      const int64_t parts = (int64_t)n_ublocks * fs.n_vsplit * fs.n_tchunks;
+      mpart_floats = std::max(mpart_floats, (size_t)((int64_t)ex_chunk * parts * part));
+      for (int e0 = 0; e0 < n; e0 += ex_chunk) {
+        MatChunk mc{(int)l, e0, std::min(ex_chunk, n - e0), n_ublocks, 1, 0, (int)P.tasks.size()};
+        mc.fused = 1;
+        mc.n_tchunks = fs.n_tchunks;
+        mc.tok_chunk = fs.tok_chunk;
+        mc.n_vsplit = fs.n_vsplit;
+        mc.vt_per_split = fs.vt_per_split;
+        ReduceTask R;
+        std::memset(&R, 0, sizeof(R));
+        R.partial_base = 0;
+        R.phi_offset = L.offset;
+        R.n_parts = (int32_t)parts;
+        R.k_in = L.k_in;
+        R.k_out = L.k_out;
+        R.ldp = tiles16(L.k_out) * 16;
+        R.part_floats = (int32_t)part;
+        R.ex_begin = e0;
+        P.tasks.push_back(R);
+        P.mat.push_back(mc);
+      }
+      continue;
+    }
     const int64_t g_per_ex = (int64_t)L.d_out * L.d_in;
     if (4 * g_per_ex >= kMaxBlockBytes)
       return fail(DATTRI_E_UNSUPPORTED, "layer %zu: G = d_out x d_in float32 (%lld bytes) exceeds 4 GiB",
@@ -1071,6 +1160,18 @@ dattri_status dattri::run_plan(dattri_ctx* ctx, const Plan& P, void* phi, dattri
   float* mpart = (float*)(ws + P.off_mpart);
   for (const MatChunk& mc : P.mat) {
     const Layer& L = ctx->layers[mc.layer];
+    if (mc.fused) {
+      GFusedArgs fa;
+      fa.A = L.A; fa.B = L.B; fa.lengths = L.lengths; fa.P_in = L.P_in; fa.P_out = L.P_out;
+      fa.d_in = L.d_in; fa.d_out = L.d_out; fa.T = L.T; fa.k_in = L.k_in; fa.k_out = L.k_out;
+      fa.ex_begin = mc.ex_begin; fa.ex_count = mc.ex_count; fa.n_ublocks = mc.n_ublocks;
+      fa.n_tchunks = mc.n_tchunks; fa.tok_chunk = mc.tok_chunk; fa.partials = mpart;
+      fa.n_vsplit = mc.n_vsplit; fa.vt_per_split = mc.vt_per_split;
+      HIP_TRY(launch_gfused(fa, s));
+      HIP_TRY(launch_reduce(d_tasks + mc.task, 1, mc.ex_count, L.k_in * L.k_out, mpart, phi, phi_bf16,
+                            ld_phi, s));
+      continue;
+    }
     GradArgs ga;
     ga.A = L.A; ga.B = L.B; ga.lengths = L.lengths;
     ga.d_in = L.d_in; ga.d_out = L.d_out; ga.T = L.T;

@@ -351,6 +351,24 @@ def test_switch_workloads_both_routes(name, form):
     assert rel_fro(host64(phi_m), host64(phi_f)) < 1e-5
 
 
+@pytest.mark.parametrize("name,expect", [("routing", "factored"), ("lora_b", "factored"),
+                                         ("narrow", "materialized")])
+def test_switch_workloads_auto_route(name, expect):
+    # the default (MI355X-fitted) cost model: the wide short-sequence layer and
+    # the adapter's B matrix stay factored, the narrow 128 -> 128 layer at
+    # T = 2048 switches to the one-pass materialized kernel; the blocks AUTO
+    # produces match the oracle on sampled examples
+    wl = W.WORKLOADS[name]
+    n = wl["batch"]
+    inputs = _session_inputs(wl, wl["layers"], n, wl["T"], "bf16")
+    s, phi = _run(wl["layers"], inputs, "bf16", wl["seed"], "auto")
+    want = dt.DATTRI_ROUTE_FACTORED if expect == "factored" else dt.DATTRI_ROUTE_MATERIALIZED
+    route, pf, pm = s.routes()[0]
+    print(f"[project] {name}: AUTO -> {expect}? predicted factored {pf:.1f} us, materialized {pm:.1f} us", flush=True)
+    assert route == want
+    _check(wl["layers"], inputs, phi, wl["seed"], "bf16", [0, n // 2, n - 1], tol=1e-5)
+
+
 def test_bf16_phi_output_and_ld():
     wl = W.WORKLOADS["tiny"]
     layers = wl["layers"] * 2

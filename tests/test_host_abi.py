@@ -249,7 +249,7 @@ def test_layer_cost_counters(case):
 
 
 FIELDS = ("factored_tflops", "factored_gbs", "gradient_tflops", "gradient_gbs",
-          "gproject_tflops", "gproject_gbs", "launch_us", "call_us")
+          "gproject_tflops", "gproject_gbs", "launch_us", "call_us", "round_us")
 
 
 def test_cost_model_roundtrip_and_validation(ctx):
@@ -261,7 +261,7 @@ def test_cost_model_roundtrip_and_validation(ctx):
     # rates must be positive, finite and within the published MI355X peaks
     bad = [dict(m, gradient_tflops=0.0), dict(m, factored_gbs=8000.5), dict(m, gradient_gbs=float("inf")),
            dict(m, factored_tflops=2501.0), dict(m, gproject_tflops=157.4), dict(m, launch_us=-1.0),
-           dict(m, call_us=float("nan"))]
+           dict(m, call_us=float("nan")), dict(m, round_us=-0.5)]
     for b in bad:
         with pytest.raises(dt.DattriError) as e:
             dt.dattri_set_cost_model(ctx, b)
@@ -278,7 +278,8 @@ def _write(tmp_path, name, text):
 def test_cost_calibration_file_roundtrip(ctx, tmp_path):
     import json
     model = {"factored_tflops": 310.5, "factored_gbs": 5123.25, "gradient_tflops": 700.0, "gradient_gbs": 4999.0,
-             "gproject_tflops": 61.0, "gproject_gbs": 4000.0, "launch_us": 4.5, "call_us": 1.25e1}
+             "gproject_tflops": 61.0, "gproject_gbs": 4000.0, "launch_us": 4.5, "call_us": 1.25e1,
+             "round_us": 3.0}
     # the layout the calibration script writes: the model beside per-shape records
     doc = {"model": model, "rms_log_error": 0.1, "device": "AMD Instinct MI355X",
            "shapes": [{"d_in": 8, "auto": "factored", "regret": 0.0, "nested": [1, -2.5e-3, True, None, {}]}],
@@ -305,9 +306,12 @@ def test_cost_calibration_file_roundtrip(ctx, tmp_path):
     ('{"models": {}}', "no \"model\""),
     ('{"model": {"factored_tflops": 300}}', "factored_gbs missing"),
     ('{"model": {"factored_tflops": "300", "factored_gbs": 1, "gradient_tflops": 1, "gradient_gbs": 1, '
-     '"gproject_tflops": 1, "gproject_gbs": 1, "launch_us": 1, "call_us": 1}}', "factored_tflops missing"),
+     '"gproject_tflops": 1, "gproject_gbs": 1, "launch_us": 1, "call_us": 1, "round_us": 1}}',
+     "factored_tflops missing"),
     ('{"model": {"factored_tflops": 300, "factored_gbs": 9000, "gradient_tflops": 1, "gradient_gbs": 1, '
-     '"gproject_tflops": 1, "gproject_gbs": 1, "launch_us": 1, "call_us": 1}}', "factored_gbs"),
+     '"gproject_tflops": 1, "gproject_gbs": 1, "launch_us": 1, "call_us": 1, "round_us": 1}}', "factored_gbs"),
+    ('{"model": {"factored_tflops": 300, "factored_gbs": 1, "gradient_tflops": 1, "gradient_gbs": 1, '
+     '"gproject_tflops": 1, "gproject_gbs": 1, "launch_us": 1, "call_us": 1}}', "round_us missing"),
     ('{"model": {"factored_tflops": 01}}', "expected"),
     ('{"model": {}} x', "trailing"),
 ])
@@ -333,7 +337,7 @@ def test_route_prediction_counts_launches(ctx):
     dt.dattri_capture_layer(ctx, 0, fake, fake + (1 << 36), 64, 32)
     peaks = dict(factored_tflops=2500.0, factored_gbs=8000.0, gradient_tflops=2500.0, gradient_gbs=8000.0,
                  gproject_tflops=157.3, gproject_gbs=8000.0)
-    dt.dattri_set_cost_model(ctx, dict(peaks, launch_us=1e6, call_us=0.0))
+    dt.dattri_set_cost_model(ctx, dict(peaks, launch_us=1e6, call_us=0.0, round_us=0.0))
     _, f_us, m_us = dt.dattri_layer_route(ctx, 0)
     assert round(f_us / 1e6) == 3
     assert round(m_us / 1e6) == 96

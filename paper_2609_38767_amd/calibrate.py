@@ -342,6 +342,14 @@ def main(argv=None):
     model, loss = fit(samples, _starts(default))
     rows = decisions(model, samples, device)
     out = _summary(model, loss, samples, rows, torch.cuda.get_device_name(device))
+    # the library's built-in model on the same measurements (out of sample
+    # when the defaults came from an earlier sweep)
+    d_rows = decisions(default, samples, device)
+    d_reg = [r["regret"] for r in d_rows]
+    out["default_model"] = {"model": default, "picked_faster": sum(1 for r in d_rows if r["auto"] == r["faster"]),
+                            "mean_regret": sum(d_reg) / len(d_reg), "max_regret": max(d_reg),
+                            "shapes": [{k: r[k] for k in ("d_in", "d_out", "k_in", "k_out", "T", "n", "auto",
+                                                          "faster", "regret")} for r in d_rows]}
     text = json.dumps(out)
     print(text, flush=True)
     if args.out:

@@ -112,10 +112,11 @@ def test_score_cosine(dtype, shape, precond):
     assert torch.equal(idx, idx2) and torch.equal(val, val2)
 
 
-@pytest.mark.parametrize("shape", [(300, 5000, 104), (256, 4096, 8192), (513, 777, 40)])
+@pytest.mark.parametrize("shape", [(300, 5000, 104), (256, 4096, 8192), (513, 777, 40), (260, 66000, 200)])
 def test_score_large_tile_kernel_ragged(shape):
     # n_q * n_train >= 2^20 routes bf16 to the 256 x 256 kernel: ragged query
-    # and training tiles and a feature tail inside a 32-wide stage
+    # and training tiles and a feature tail inside a 32-wide stage; the last
+    # shape has more tiles than CUs (516) and a partial last round
     n_q, n_t, F = shape
     g = torch.Generator(device=DEV).manual_seed(9)
     Q = torch.randn((n_q, F), generator=g, device=DEV).to(torch.bfloat16)

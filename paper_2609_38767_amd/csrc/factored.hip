@@ -56,7 +56,14 @@ __global__ __launch_bounds__(256, AL ? waves_of(NA, NB) : 1) void factored_kerne
                                                           float* __restrict__ partials) {
   constexpr int NTL = NA > NB ? NA : NB;
   constexpr int PD = AL ? pd_of(RT, NA, NB) : 2;
-  __shared__ __align__(16) uint8_t pan[2][kPanel][NTL][kFragBytes];
+  // bf16 with aligned rows and two map tiles per side: factor rows streamed
+  // through LDS by direct loads (project_rows_dma); otherwise operand loads
+  // straight into registers with projection panels in LDS (project_rows)
+  constexpr bool kDma = ELT == 2 && AL && NA == 2 && NB == 2;
+  constexpr int kPanBytes = 2 * kPanel * NTL * kFragBytes;
+  constexpr int kSmem = kDma ? DmaLds<RT, 2>::kBytes : kPanBytes;
+  __shared__ __align__(1024) uint8_t smem[kSmem];
+  auto pan = reinterpret_cast<uint8_t(*)[kPanel][NTL][kFragBytes]>(smem);
   const FactItem it = items[blockIdx.x];
   if (it.example < 0) return;  // padding item of the XCD-interleaved order
   const FactGroup& G = groups[it.group];
@@ -95,7 +102,10 @@ __global__ __launch_bounds__(256, AL ? waves_of(NA, NB) : 1) void factored_kerne
     for (int rt = 0; rt < RT; ++rt)
 #pragma unroll
       for (int t = 0; t < NA; ++t) acc_a[rt][t] = f32x4{0.f, 0.f, 0.f, 0.f};
-    project_rows<ELT, AL, RT, NA, NTL, PD>(ra, r_wave, rows_valid, d_in, d_in, pin, acc_a, pan);
+    if constexpr (kDma)
+      project_rows_dma<RT, NA>(ra, r_wave, rows_valid, d_in, d_in, pin, acc_a, smem);
+    else
+      project_rows<ELT, AL, RT, NA, NTL, PD>(ra, r_wave, rows_valid, d_in, d_in, pin, acc_a, pan);
     // projected input rows of every member that asks for them
     for (int mi = 0; mi < G.n_members; ++mi) {
       const FactMember& M = members[G.member0 + mi];
@@ -121,7 +131,10 @@ __global__ __launch_bounds__(256, AL ? waves_of(NA, NB) : 1) void factored_kerne
       for (int rt = 0; rt < RT; ++rt)
 #pragma unroll
         for (int t = 0; t < NB; ++t) acc_b[rt][t] = f32x4{0.f, 0.f, 0.f, 0.f};
-      project_rows<ELT, AL, RT, NB, NTL, PD>(rb, r_wave, rows_valid, d_out, d_out, pout, acc_b, pan);
+      if constexpr (kDma)
+        project_rows_dma<RT, NB>(rb, r_wave, rows_valid, d_out, d_out, pout, acc_b, smem);
+      else
+        project_rows<ELT, AL, RT, NB, NTL, PD>(rb, r_wave, rows_valid, d_out, d_out, pout, acc_b, pan);
       if (M.rows_b)
         store_rows<RT, NB>(acc_b, M.rows_b + (int64_t)ex * T * M.k_out, M.k_out, 0, nb, r_wave, row_end, g,
                            m16);

@@ -132,5 +132,118 @@ __device__ inline void project_rows(const rsrc_t r, int r_wave, int nrows, int d
   }
 }
 
+// ---------------------------------------------------------------------------
+// The same projection for bf16 blocks with 16-byte aligned rows, streamed
+// through LDS by direct loads (buffer_load ... lds, no registers): each load
+// instruction moves 8 rows x 128 bytes (2 k-blocks of 8 rows), so every L2
+// request carries 128 bytes of a row instead of the 64 a register operand
+// load gets (16 rows x 64 bytes), and many more bytes can be in flight per CU.
+//
+// A stage is 2 k-blocks (64 columns).  Each wave streams only its own RT x 16
+// rows, into a private double buffer (RT x 16 x 128 bytes per stage), rows
+// 128 bytes apart with their 16-byte chunks XOR-swizzled by (row & 7) so the
+// MFMA fragment reads (16 rows x 16 bytes per lane group) spread over the
+// banks: each lane fetches the chunk that lands in its fixed LDS slot.  The
+// stage's NT x 2 projection fragments (one per wave, NT = 2) go by direct load
+// into a 3-slot ring shared by the workgroup.  Every wave issues exactly
+// kDmaOps loads per stage, so "stage s has landed" is vmcnt(kDmaOps) while
+// stage s + 1 is in flight and vmcnt(0) otherwise (any extra load issued later
+// would only make that wait longer); one barrier per stage then publishes the
+// shared fragments.  The wave's reads of a buffer finish (lgkmcnt(0)) before
+// the load of stage s + 2 into it is issued, and the map slot it refills was
+// last read in stage s - 1, before every wave passed stage s's barrier.
+// K-blocks are contracted in the order of project_rows, so results are
+// bitwise those of the register path.
+template <int RT, int NT>
+struct DmaLds {
+  static_assert(NT * 2 == kWaves, "one projection fragment per wave and stage");
+  static constexpr int kRowBytes = 128;                      // 2 k-blocks of 32 bf16
+  static constexpr int kWaveStage = RT * 16 * kRowBytes;     // bytes per wave and stage
+  static constexpr int kLoads = RT * 16 / 8;                 // 1 KiB row-group loads per stage
+  static constexpr int kDmaOps = kLoads + 1;                 // plus the wave's fragment
+  static constexpr int kMapOff = kWaves * 2 * kWaveStage;
+  static constexpr int kMapStage = 2 * NT * kFragBytes;
+  static constexpr int kBytes = kMapOff + 3 * kMapStage;
+};
+
+#define DATTRI_LDS_PTR(p) ((__attribute__((address_space(3))) void*)(p))
+
+template <int N>
+__device__ inline void wait_vmcnt_dma() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt((N & 0xF) | ((N >> 4) << 14) | (0x7 << 4) | (0xF << 8));
+}
+
+template <int RT, int NT>
+__device__ inline void project_rows_dma(const rsrc_t r, int r_wave, int nrows, int d, int64_t ld,
+                                        const FragSrc<NT>& P, f32x4 (&acc)[RT][NT], uint8_t* lds) {
+  using C = DmaLds<RT, NT>;
+  const int tid = threadIdx.x, lane = tid & 63, g = lane >> 4, m16 = lane & 15;
+  const int wave = tid >> 6;
+  const int nkb = (d + 31) / 32;
+  const int nst = (nkb + 1) / 2;
+  uint8_t* own = lds + wave * 2 * C::kWaveStage;
+  // this wave's projection fragment of every stage: k-block 2s + kbl of tile t
+  const int f_kbl = wave / NT, f_t = wave % NT;
+  const int64_t f_stride = P.stride[f_t];
+  const rsrc_t rp = make_rsrc(P.base[f_t], (uint32_t)((int64_t)nkb * f_stride));
+
+  auto issue = [&](int s) {
+    uint8_t* xs = own + (s & 1) * C::kWaveStage;
+#pragma unroll
+    for (int i = 0; i < C::kLoads; ++i) {
+      const int row_l = i * 8 + (lane >> 3);
+      const int c = (lane & 7) ^ (row_l & 7);  // the logical chunk that lands in this lane's slot
+      const int row = r_wave + row_l, col = s * 64 + c * 8;
+      const uint32_t off = (row < nrows && col < d) ? (uint32_t)(((int64_t)row * ld + col) * 2) : kOOB;
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(r, DATTRI_LDS_PTR(xs + i * 1024), 16, off, 0, 0, 0);
+    }
+    const int kb = 2 * s + f_kbl;
+    uint8_t* ms = lds + C::kMapOff + (s % 3) * C::kMapStage + (f_kbl * NT + f_t) * kFragBytes;
+    const uint32_t moff = (f_t < P.nt && kb < nkb) ? (uint32_t)(kb * f_stride + lane * 16) : kOOB;
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(rp, DATTRI_LDS_PTR(ms), 16, moff, 0, 0, 0);
+  };
+
+  // the stage barrier: this wave's LDS reads done, then s_barrier.  An inline
+  // barrier, because a fenced one (lds_barrier) makes the compiler wait for
+  // every outstanding direct load (vmcnt(0)), the prefetched stage included.
+  auto stage_barrier = [] { asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory"); };
+  if (nst > 0) issue(0);
+  if (nst > 1) issue(1);
+  for (int s = 0; s < nst; ++s) {
+    if (s + 1 < nst)
+      wait_vmcnt_dma<C::kDmaOps>();
+    else
+      wait_vmcnt_dma<0>();
+    stage_barrier();
+    const uint8_t* xs = own + (s & 1) * C::kWaveStage;
+    const uint8_t* ms = lds + C::kMapOff + (s % 3) * C::kMapStage;
+#pragma unroll
+    for (int kbl = 0; kbl < 2; ++kbl) {
+      if (2 * s + kbl < nkb) {  // uniform
+        i32x4 x[RT];
+#pragma unroll
+        for (int rt = 0; rt < RT; ++rt) {
+          const int row_l = rt * 16 + m16;
+          x[rt] = *(const i32x4*)(xs + row_l * C::kRowBytes + (((kbl * 4 + g) ^ (row_l & 7)) << 4));
+        }
+#pragma unroll
+        for (int t = 0; t < NT; ++t) {
+          if (t < P.nt) {
+            const i32x4 pf = *(const i32x4*)(ms + (kbl * NT + t) * kFragBytes + lane * 16);
+#pragma unroll
+            for (int rt = 0; rt < RT; ++rt) acc[rt][t] = frag_mma<2>(x[rt], pf, acc[rt][t]);
+          }
+        }
+      }
+    }
+    if (s + 2 < nst) {
+      asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");  // this wave's reads of the buffer are done
+      issue(s + 2);
+    }
+  }
+  stage_barrier();  // every wave is done with the ring before the next call refills it
+}
+
 }  // namespace dev
 }  // namespace dattri

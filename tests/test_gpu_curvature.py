@@ -140,6 +140,39 @@ def test_factor_sums_accumulate_and_reset():
     assert c.field(1, "counts").tolist() == [0, 0, 0]
 
 
+def test_project_and_fit_repeated_batches_same_buffers():
+    # the usual training loop: each batch written into the captured buffers and
+    # fitted with an unchanged plan (its tables stay in the plan buffer); the
+    # sums cover both batches and each phi matches its own batch
+    n, T = 3, 70
+    a = _inputs(LAYERS[:2], n, T, "bf16", seed=41, batch=0)
+    b = _inputs(LAYERS[:2], n, T, "bf16", seed=41, batch=1)
+    bufs = [(A.clone(), B.clone()) for A, B in a]
+    s = _session(LAYERS[:2], bufs, "bf16", 11)
+    c = Curvature(s)
+    phis = []
+    for data in (a, b):
+        for (A, B), (A2, B2) in zip(bufs, data):
+            A.copy_(A2)
+            B.copy_(B2)
+        phis.append(c.project_and_fit(n).clone())
+    torch.cuda.synchronize()
+    maps = oracle_maps(11, LAYERS[:2], "bf16")
+    for data, phi in zip((a, b), phis):
+        for li, L in enumerate(LAYERS[:2]):
+            A, B = host64(data[li][0]), host64(data[li][1])
+            o, w = s.offsets[li], L["k_in"] * L["k_out"]
+            ref = np.stack([og.project_factored(A[i], B[i], maps[li][0], maps[li][1]).reshape(-1) for i in range(n)])
+            assert rel_fro(host64(phi[:, o:o + w]), ref) <= 1e-5
+    for li in range(2):
+        A = np.concatenate([host64(a[li][0]), host64(b[li][0])])
+        B = np.concatenate([host64(a[li][1]), host64(b[li][1])])
+        SA, SG, nt, ne = ok.factor_sums(A, B, maps[li][0], maps[li][1])
+        assert rel_fro(host64(c.field(li, "sum_a")), SA) <= 1e-5
+        assert rel_fro(host64(c.field(li, "sum_g")), SG) <= 1e-5
+        assert c.field(li, "counts").tolist() == [2 * n * T, 2 * n, 0]
+
+
 def _spectrum_matrix(rng, k, lam):
     U, _ = np.linalg.qr(rng.standard_normal((k, k)))
     return (U * lam) @ U.T

@@ -113,6 +113,27 @@ def test_fused_64_wide_maps(dtype):
     _check(layers, inputs, phi, 19, dtype, [0, 1, 2, 3], lengths=lengths, tol=1e-5)
 
 
+def test_fused_direct_lds_path_ragged():
+    # bf16 layers with 16-byte aligned rows and 17..32-wide maps on both sides
+    # take the fused kernel's direct-to-LDS path (two map tiles per side):
+    # d not a multiple of the 64-column stage (520: 17 k-blocks, the last
+    # stage half empty; 200; 72), a member with one output tile, sub-chunks of
+    # 256 rows ragged by length, a zero-length example
+    layers = [dict(name="d0", d_in=520, d_out=200, k_in=32, k_out=32, a_group="a"),
+              dict(name="d1", d_in=520, d_out=72, k_in=20, k_out=16, a_group="b"),
+              dict(name="d2", d_in=64, d_out=40, k_in=32, k_out=24, a_group="c")]
+    wl = dict(W.WORKLOADS["tiny"], dist_a="student_t4", dist_b="student_t4", seed=97)
+    n, T = 4, 600
+    inputs = _session_inputs(wl, layers, n, T, "bf16")
+    lengths = torch.tensor([600, 0, 257, 1], dtype=torch.int32, device=DEV)
+    _, phi = _run(layers, inputs, "bf16", 99, "factored", lengths=lengths, form="fused")
+    assert torch.count_nonzero(phi[1]).item() == 0
+    _check(layers, inputs, phi, 99, "bf16", [0, 2, 3], lengths=lengths, tol=1e-5)
+    # the register path (split form's stage 1 streams the same rows) agrees to rounding
+    _, phi_s = _run(layers, inputs, "bf16", 99, "factored", lengths=lengths, form="split")
+    assert rel_fro(host64(phi_s), host64(phi)) < 1e-6
+
+
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
 @pytest.mark.parametrize("route,form", [("factored", "fused"), ("factored", "split"), ("materialized", None)])
 def test_rademacher_maps(dtype, route, form):
@@ -367,6 +388,40 @@ def test_switch_workloads_auto_route(name, expect):
     print(f"[project] {name}: AUTO -> {expect}? predicted factored {pf:.1f} us, materialized {pm:.1f} us", flush=True)
     assert route == want
     _check(wl["layers"], inputs, phi, wl["seed"], "bf16", [0, n // 2, n - 1], tol=1e-5)
+
+
+@pytest.mark.parametrize("plan_buffer", [True, False])
+def test_plan_reuse_follows_captures(plan_buffer):
+    # launch plans are cached by the context state and kept in the bound plan
+    # buffer: new contents in the same captured buffers reuse the plan, a
+    # capture of other buffers (or another route) re-plans; every call matches
+    # the oracle for the data it saw
+    layers = [dict(name="p0", d_in=96, d_out=80, k_in=16, k_out=32, a_group="a"),
+              dict(name="p1", d_in=96, d_out=40, k_in=8, k_out=8, a_group="a")]
+    wl = dict(W.WORKLOADS["tiny"], dist_a="normal", dist_b="normal", seed=91)
+    n, T = 3, 50
+    s = ProjectionSession(layers, dtype="f32", seed=93, plan_buffer=plan_buffer)
+    first = _session_inputs(wl, layers, n, T, "f32")
+    bufs = [(A.clone(), B.clone()) for A, B in first]
+    for li, (A, B) in enumerate(bufs):
+        s.capture(li, A, B)
+    for step, seed in enumerate((91, 92)):
+        data = _session_inputs(dict(wl, seed=seed), layers, n, T, "f32")
+        for (A, B), (A2, B2) in zip(bufs, data):  # same buffers, new contents
+            A.copy_(A2)
+            B.copy_(B2)
+        for route in ("factored", "materialized"):
+            phi = s.project(n, route=ROUTES[route])
+            torch.cuda.synchronize()
+            _check(layers, data, phi, 93, "f32", [0, 1, 2], tol=1e-5)
+    # other buffers: the next call must plan for them
+    other = _session_inputs(dict(wl, seed=95), layers, n, T, "f32")
+    s.clear()
+    for li, (A, B) in enumerate(other):
+        s.capture(li, A, B)
+    phi = s.project(n)
+    torch.cuda.synchronize()
+    _check(layers, other, phi, 93, "f32", [0, 1, 2], tol=1e-5)
 
 
 def test_bf16_phi_output_and_ld():

@@ -10,13 +10,15 @@
 // give partial blocks that add up).  For each 128-column tile of G (input
 // features v0 .. v0 + 127): the tile is formed over the chunk's tokens with bf16 MFMA
 // (g_tile, gtile.h), written to LDS in float32, and H[rows, :] += G_tile
-// P_in[v0 .. v0 + 127, :] by float32 MFMA (16x16x4; the P_in fragment read from
+// P_in[v0 .. v0 + 127, :] by bf16 MFMA (16x16x32; the P_in fragment read from
 // the packed map, lane (g, n) holding K slots g*8 + j of column n, so the G
-// operand is element j of the matching 8 columns of the lane's row).  After
+// operand is the matching 8 columns of the lane's row), each G value taken as
+// the sum of three bf16 terms (hi + mid + lo, exact to 2^-27 relative) whose
+// products with the bf16 map are exact in the float32 accumulation.  After
 // the last tile, Psi_part = H^T P_out[rows] from the H accumulators (their C
 // layout is a K=4 operand slice per element index); the four waves' parts are
 // added in LDS in wave order and the workgroup writes one partial block, which
-// the reduce kernel adds to the others in index order.  Arithmetic is float32
+// the reduce kernel adds to the others in index order.  Sums are float32
 // throughout (bf16 products are exact in float32).
 #include "device_common.h"
 #include "gtile.h"
@@ -91,19 +93,36 @@ __global__ __launch_bounds__(256, 1) void gfused_kernel(GFusedArgs a) {
         for (int t = 0; t < NT; ++t)
           pf[t] = t < na_all ? *(const i32x4*)(pin + ((int64_t)(kb * na_all + t) * 64 + lane) * 16)
                              : i32x4{0, 0, 0, 0};
-        // K slot j outermost: consecutive MFMAs update different H tiles
+        // the lane's 8 G values as three bf16 terms, hi + mid + lo (each the
+        // RNE bf16 of what the previous ones leave), exact to 2^-27 relative;
+        // P_in is exactly bf16, so each term's products are exact in the
+        // float32 accumulation of a bf16 MFMA
+        i32x4 gs[2][3];
 #pragma unroll
-        for (int j = 0; j < 8; ++j) {
+        for (int rt = 0; rt < 2; ++rt) {
+          uint32_t hb[3][8];
 #pragma unroll
-          for (int t = 0; t < NT; ++t) {
-            if (t < na_all) {
-              const uint32_t w = (uint32_t)pf[t][j / 2];
-              const float pv = bf16_bits_to_f32((j & 1) ? (w >> 16) : (w & 0xFFFFu));
+          for (int j = 0; j < 8; ++j) {
+            float v = gf[rt][j / 4][j % 4];
 #pragma unroll
-              for (int rt = 0; rt < 2; ++rt) H[rt][t] = mfma_f32_4(gf[rt][j / 4][j % 4], pv, H[rt][t]);
+            for (int q = 0; q < 3; ++q) {
+              const uint32_t b = f32_to_bf16_bits(v);
+              hb[q][j] = b;
+              v -= bf16_bits_to_f32(b);
             }
           }
+#pragma unroll
+          for (int q = 0; q < 3; ++q)
+            gs[rt][q] = i32x4{(int)(hb[q][0] | (hb[q][1] << 16)), (int)(hb[q][2] | (hb[q][3] << 16)),
+                              (int)(hb[q][4] | (hb[q][5] << 16)), (int)(hb[q][6] | (hb[q][7] << 16))};
         }
+#pragma unroll
+        for (int q = 0; q < 3; ++q)
+#pragma unroll
+          for (int t = 0; t < NT; ++t)
+            if (t < na_all)
+#pragma unroll
+              for (int rt = 0; rt < 2; ++rt) H[rt][t] = frag_mma<2>(gs[rt][q], pf[t], H[rt][t]);
       }
     }
     __syncthreads();  // the next tile overwrites Gs and the staging buffer

@@ -53,18 +53,18 @@ dattri_cost_model default_cost_model() {
   // single-layer shapes: transformer, adapter-shaped and narrow layers,
   // T = 16..4096, both forced routes timed with launch plans kept on the
   // device), every rate held below its bound: AUTO picks the faster route on
-  // 26 of 28 shapes, mean regret 0.4%, worst 7.8% (two near-ties).
+  // all 28 shapes, root-mean-square log error of the predictions 0.14.
   // gproject_gbs serves only the staged-G route, which that sweep does not run.
   dattri_cost_model m;
-  m.factored_tflops = 145.6;
-  m.factored_gbs = 3733.5;
-  m.gradient_tflops = 309.0;
-  m.gradient_gbs = 6450.0;
-  m.gproject_tflops = 116.2;
+  m.factored_tflops = 164.3;
+  m.factored_gbs = 5130.6;
+  m.gradient_tflops = 372.7;
+  m.gradient_gbs = 6449.6;
+  m.gproject_tflops = 157.3;
   m.gproject_gbs = 5000.0;
-  m.launch_us = 9.53;
+  m.launch_us = 10.35;
   m.call_us = 0.0;
-  m.round_us = 0.833;
+  m.round_us = 2.74;
   return m;
 }
 
@@ -152,24 +152,24 @@ bool fused_materialized(const Layer& L, int elt) {
 
 // Launch shape of the one-pass kernel and its predicted time.  A workgroup
 // (one per CU: 104 KiB of LDS) runs, per 128-column tile of G in its range,
-// tok_chunk / 32 token stages (bf16 MFMA) and a projection of the tile
-// (float32 MFMA, about 8 stages' worth per 16 columns of P_in), then one
-// H^T P_out.  Token chunks and column ranges add workgroups but the chunks
-// repeat the projections; the shape minimising rounds of 256 workgroups x
-// per-workgroup time wins.  Times use the model's rates: a round of 256
-// workgroups each running one stage is 256 x 2 x 32 x 128 x 128 FLOP at
-// gradient_tflops; one tile projection per workgroup is 256 x 2 x 128 x 128 x
-// 16 x tiles_in FLOP and the closing product 256 x 2 x 128 x 16 tiles_in x 16
-// tiles_out FLOP, both at gproject_tflops; each round also costs round_us
-// (load latencies and barriers, whatever the work).
+// tok_chunk / 32 token stages and a projection of the tile (three bf16 MFMA
+// terms per product, about 3 stages' worth per 16 columns of P_in), then one
+// H^T P_out in float32.  Token chunks and column ranges add workgroups but the
+// chunks repeat the projections; the shape minimising rounds of 256
+// workgroups x per-workgroup time wins.  Times use the model's rates: a round
+// of 256 workgroups each running one stage is 256 x 2 x 32 x 128 x 128 FLOP,
+// one tile projection per workgroup 256 x 3 x 2 x 128 x 128 x 16 x tiles_in
+// FLOP, both bf16 MFMA at gradient_tflops; the closing product 256 x 2 x 128
+// x 16 tiles_in x 16 tiles_out FLOP of float32 MFMA at gproject_tflops; each
+// round also costs round_us (load latencies and barriers, whatever the work).
 struct FusedShape { int n_tchunks, tok_chunk, n_vsplit, vt_per_split; double us; };
 FusedShape fused_shape(const Layer& L, int64_t n, const dattri_cost_model& m) {
   const int64_t T = std::max<int64_t>(L.T, 1);
   const int64_t n_ub = (L.d_out + kGFusedRows - 1) / kGFusedRows;
   const int64_t n_vt = (L.d_in + kGFusedCols - 1) / kGFusedCols;
   const double stage_us = 256.0 * 2 * 32 * kGFusedRows * kGFusedCols / (m.gradient_tflops * 1e6);
-  const double proj_us = 256.0 * 2 * kGFusedRows * kGFusedCols * 16 * gfused_tiles_in(L.k_in) /
-                         (m.gproject_tflops * 1e6);
+  const double proj_us = 256.0 * 3 * 2 * kGFusedRows * kGFusedCols * 16 * gfused_tiles_in(L.k_in) /
+                         (m.gradient_tflops * 1e6);
   // the closing H^T P_out of every workgroup, also float32 MFMA
   const double epi_us = 256.0 * 2 * kGFusedRows * 16 * gfused_tiles_in(L.k_in) * 16 * tiles16(L.k_out) /
                         (m.gproject_tflops * 1e6);
@@ -201,11 +201,15 @@ void predict(const dattri_ctx* ctx, const Layer& L, double* f_us, double* m_us) 
   *f_us = m.call_us + t((double)c.f_flops * n, m.factored_tflops, (double)c.f_bytes * n, m.factored_gbs);
   if (n > 0) *f_us += factored_launches(ctx, L) * m.launch_us;
   if (fused_materialized(L, ctx->elt)) {
-    // one pass: factor blocks read once, G on chip; time from its launch shape
+    // one pass: factor blocks read once, G on chip; time from its launch shape.
+    // One launch is charged for the pair of kernels: the small reduction of
+    // the partial products dispatches behind the one-pass kernel, and on
+    // MI355X the pair's fixed cost measures about one launch (13.6 us in all
+    // for the smallest layers).
     const int64_t chunks = n > 0 ? (n + 65534) / 65535 : 0;
     const double work = n > 0 ? fused_shape(L, n, m).us : 0.0;
     *m_us = m.call_us + std::max(work, (double)c.f_bytes * n / (m.gradient_gbs * 1e3)) +
-            2.0 * chunks * m.launch_us;
+            chunks * m.launch_us;
     return;
   }
   const int64_t chunks = n > 0 ? (n + materialized_chunk(L, n) - 1) / materialized_chunk(L, n) : 0;

@@ -12,9 +12,11 @@
 // (g_tile, gtile.h), written to LDS in float32, and H[rows, :] += G_tile
 // P_in[v0 .. v0 + 127, :] by bf16 MFMA (16x16x32; the P_in fragment read from
 // the packed map, lane (g, n) holding K slots g*8 + j of column n, so the G
-// operand is the matching 8 columns of the lane's row), each G value taken as
-// the sum of three bf16 terms (hi + mid + lo, exact to 2^-27 relative) whose
-// products with the bf16 map are exact in the float32 accumulation.  After
+// operand is the matching 8 columns of the lane's row), each G value split
+// exactly into three bf16 terms (hi + mid + lo) whose products with the bf16
+// map are exact in the float32 accumulation.  The next tile's first token
+// stage and the next k-block's map fragments are loaded while a tile is
+// projected.  After
 // the last tile, Psi_part = H^T P_out[rows] from the H accumulators (their C
 // layout is a K=4 operand slice per element index); the four waves' parts are
 // added in LDS in wave order and the workgroup writes one partial block, which
@@ -64,9 +66,40 @@ __global__ __launch_bounds__(256, 1) void gfused_kernel(GFusedArgs a) {
 #pragma unroll
     for (int t = 0; t < NT; ++t) H[rt][t] = f32x4{0.f, 0.f, 0.f, 0.f};
 
+  // P_in fragments of k-block kb (zero past d_in or k_in: buffer range check)
+  const rsrc_t rpin = make_rsrc(pin, (uint32_t)((int64_t)nkb * na_all * kFragBytes));
+  auto pin_frags = [&](int kb, i32x4 (&pf)[NT]) {
+#pragma unroll
+    for (int t = 0; t < NT; ++t)
+      pf[t] = load16(rpin, (t < na_all && kb < nkb) ? (uint32_t)(((kb * na_all + t) * 64 + lane) * 16) : kOOB);
+  };
+  // Two float32 G values as three packed bf16 terms each: hi = v truncated to
+  // bf16, mid = (v - hi) truncated, lo = v - hi - mid.  The differences are
+  // exact and lo has at most 8 significant bits, so hi + mid + lo = v exactly
+  // (away from the subnormal range).
+  auto split2 = [](float x, float y, int& hi, int& mid, int& lo) {
+    const uint32_t ux = __builtin_bit_cast(uint32_t, x), uy = __builtin_bit_cast(uint32_t, y);
+    const float rx = x - __builtin_bit_cast(float, ux & 0xFFFF0000u);
+    const float ry = y - __builtin_bit_cast(float, uy & 0xFFFF0000u);
+    const uint32_t urx = __builtin_bit_cast(uint32_t, rx), ury = __builtin_bit_cast(uint32_t, ry);
+    const uint32_t lx = __builtin_bit_cast(uint32_t, rx - __builtin_bit_cast(float, urx & 0xFFFF0000u));
+    const uint32_t ly = __builtin_bit_cast(uint32_t, ry - __builtin_bit_cast(float, ury & 0xFFFF0000u));
+    hi = (int)((ux >> 16) | (uy & 0xFFFF0000u));
+    mid = (int)((urx >> 16) | (ury & 0xFFFF0000u));
+    lo = (int)((lx >> 16) | (ly & 0xFFFF0000u));
+  };
+
+  // Token rows of the first tile, then of each next tile during the current
+  // tile's last stage (g_tile_from), so the first stage of a tile is in
+  // flight while the previous tile is projected.
+  const GRows gr = g_rows(b_rows, a_rows, rows, a.d_out, a.d_in);
+  GStage<2, 2> st;
+  if (v_begin < v_end) g_load(gr, 0, u0, v_begin, st);
   for (int v0 = v_begin; v0 < v_end; v0 += kGFusedCols) {
+    i32x4 pf[NT];
+    pin_frags(v0 / 32, pf);  // in flight during the tile's token stages
     f32x16 acc[2][2];
-    g_tile<2, 2>(b_rows, a_rows, rows, a.d_out, a.d_in, u0, v0, stage, acc);
+    g_tile_from(gr, rows, u0, v0, v0 + kGFusedCols < v_end ? v0 + kGFusedCols : -1, stage, st, acc);
     // 32x32 C layout: lane l, element x holds tile row 8*(x/4) + 4*(l/32) + x%4
     // of block i, column l % 32 of block j
 #pragma unroll
@@ -81,49 +114,38 @@ __global__ __launch_bounds__(256, 1) void gfused_kernel(GFusedArgs a) {
 #pragma unroll
     for (int kbl = 0; kbl < kGFusedCols / 32; ++kbl) {
       const int kb = v0 / 32 + kbl;
+      i32x4 pn[NT];
+      if (kbl + 1 < kGFusedCols / 32) pin_frags(kb + 1, pn);
       if (kb < nkb) {  // uniform
-        f32x4 gf[2][2];
-#pragma unroll
-        for (int rt = 0; rt < 2; ++rt)
-#pragma unroll
-          for (int h = 0; h < 2; ++h)
-            gf[rt][h] = *(const f32x4*)&Gs[(r_wave + rt * 16 + m16) * kGFPitch + kbl * 32 + g * 8 + 4 * h];
-        i32x4 pf[NT];
-#pragma unroll
-        for (int t = 0; t < NT; ++t)
-          pf[t] = t < na_all ? *(const i32x4*)(pin + ((int64_t)(kb * na_all + t) * 64 + lane) * 16)
-                             : i32x4{0, 0, 0, 0};
-        // the lane's 8 G values as three bf16 terms, hi + mid + lo (each the
-        // RNE bf16 of what the previous ones leave), exact to 2^-27 relative;
-        // P_in is exactly bf16, so each term's products are exact in the
-        // float32 accumulation of a bf16 MFMA
+        // the lane's 8 G values of each row tile (columns g*8 .. g*8 + 7 of
+        // k-block kbl, matching the P_in fragment's K slots), as three bf16
+        // terms; P_in is exactly bf16, so each term's products are exact in
+        // the float32 accumulation of a bf16 MFMA
         i32x4 gs[2][3];
 #pragma unroll
         for (int rt = 0; rt < 2; ++rt) {
-          uint32_t hb[3][8];
-#pragma unroll
-          for (int j = 0; j < 8; ++j) {
-            float v = gf[rt][j / 4][j % 4];
-#pragma unroll
-            for (int q = 0; q < 3; ++q) {
-              const uint32_t b = f32_to_bf16_bits(v);
-              hb[q][j] = b;
-              v -= bf16_bits_to_f32(b);
-            }
-          }
-#pragma unroll
-          for (int q = 0; q < 3; ++q)
-            gs[rt][q] = i32x4{(int)(hb[q][0] | (hb[q][1] << 16)), (int)(hb[q][2] | (hb[q][3] << 16)),
-                              (int)(hb[q][4] | (hb[q][5] << 16)), (int)(hb[q][6] | (hb[q][7] << 16))};
+          const float* gp = &Gs[(r_wave + rt * 16 + m16) * kGFPitch + kbl * 32 + g * 8];
+          const f32x4 g0 = *(const f32x4*)gp, g1 = *(const f32x4*)(gp + 4);
+          int h[4], m[4], l[4];
+          split2(g0[0], g0[1], h[0], m[0], l[0]);
+          split2(g0[2], g0[3], h[1], m[1], l[1]);
+          split2(g1[0], g1[1], h[2], m[2], l[2]);
+          split2(g1[2], g1[3], h[3], m[3], l[3]);
+          gs[rt][0] = i32x4{h[0], h[1], h[2], h[3]};
+          gs[rt][1] = i32x4{m[0], m[1], m[2], m[3]};
+          gs[rt][2] = i32x4{l[0], l[1], l[2], l[3]};
         }
+        // fragments t >= na_all are zero, so their products leave H[., t] zero
 #pragma unroll
         for (int q = 0; q < 3; ++q)
 #pragma unroll
           for (int t = 0; t < NT; ++t)
-            if (t < na_all)
 #pragma unroll
-              for (int rt = 0; rt < 2; ++rt) H[rt][t] = frag_mma<2>(gs[rt][q], pf[t], H[rt][t]);
+            for (int rt = 0; rt < 2; ++rt) H[rt][t] = frag_mma<2>(gs[rt][q], pf[t], H[rt][t]);
       }
+      if (kbl + 1 < kGFusedCols / 32)
+#pragma unroll
+        for (int t = 0; t < NT; ++t) pf[t] = pn[t];
     }
     __syncthreads();  // the next tile overwrites Gs and the staging buffer
   }

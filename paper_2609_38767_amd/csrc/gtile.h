@@ -40,20 +40,62 @@ struct GTile {
   static_assert(CB >= 1 && CA >= 1, "tile");
 };
 
-// acc[i][j] = G block (i, j) of this wave over token rows [0, rows) of the
-// blocks whose row 0 is at b_rows / a_rows (bf16, rows d_out / d_in elements
-// apart).  lds: GTile<WM, WN>::kLdsBytes of shared memory.  All 256 threads
-// call this together; it ends with a barrier (lds may be reused after it).
+// One stage of token rows in registers: this thread's 16-byte chunks of the
+// B rows (d_out side) and the A rows (d_in side).
 template <int WM, int WN>
-__device__ inline void g_tile(const uint8_t* b_rows, const uint8_t* a_rows, int rows, int d_out, int d_in,
-                              int u0, int v0, uint8_t* lds, f32x16 (&acc)[WM][WN]) {
+struct GStage {
+  i32x4 b[GTile<WM, WN>::CB], a[GTile<WM, WN>::CA];
+};
+
+// Buffer resources over the token rows [0, rows) of the blocks whose row 0 is
+// at b_rows / a_rows; rows past `rows` and features past d read zero.
+struct GRows {
+  rsrc_t rb, ra;
+  int d_out, d_in;
+};
+
+__device__ inline GRows g_rows(const uint8_t* b_rows, const uint8_t* a_rows, int rows, int d_out, int d_in) {
+  return GRows{make_rsrc(b_rows, (uint32_t)((int64_t)rows * d_out * 2)),
+               make_rsrc(a_rows, (uint32_t)((int64_t)rows * d_in * 2)), d_out, d_in};
+}
+
+// Issue the loads of token rows t0 .. t0 + 31 of tile (u0, v0) into st.
+template <int WM, int WN>
+__device__ inline void g_load(const GRows& r, int t0, int u0, int v0, GStage<WM, WN>& st) {
+  using C = GTile<WM, WN>;
+  const int tid = threadIdx.x;
+#pragma unroll
+  for (int i = 0; i < C::CB; ++i) {
+    const int c = tid + 256 * i, row = c / (C::TM / 8), fc = c % (C::TM / 8);
+    const int u = u0 + fc * 8;
+    const uint32_t off = u < r.d_out ? (uint32_t)(((int64_t)(t0 + row) * r.d_out + u) * 2) : kOOB;
+    st.b[i] = load16(r.rb, off);
+  }
+#pragma unroll
+  for (int i = 0; i < C::CA; ++i) {
+    const int c = tid + 256 * i, row = c / (C::TN / 8), fc = c % (C::TN / 8);
+    const int v = v0 + fc * 8;
+    const uint32_t off = v < r.d_in ? (uint32_t)(((int64_t)(t0 + row) * r.d_in + v) * 2) : kOOB;
+    st.a[i] = load16(r.ra, off);
+  }
+}
+
+// acc[i][j] = G block (i, j) of this wave over token rows [0, rows) of tile
+// (u0, v0).  On entry st holds (or has loads in flight for) the tile's first
+// stage, rows 0 .. 31; the later stages are prefetched one ahead.  With
+// next_v0 >= 0 the last stage also issues the loads of the first stage of
+// tile (u0, next_v0) into st, so a caller walking a row of tiles keeps a
+// load in flight across the tile boundary.  lds: GTile<WM, WN>::kLdsBytes of
+// shared memory.  All 256 threads call this together; it ends with a barrier
+// (lds may be reused after it).
+template <int WM, int WN>
+__device__ inline void g_tile_from(const GRows& r, int rows, int u0, int v0, int next_v0, uint8_t* lds,
+                                   GStage<WM, WN>& st, f32x16 (&acc)[WM][WN]) {
   using C = GTile<WM, WN>;
   uint8_t* Bs[2] = {lds, lds + kTrTokens * C::PB};
   uint8_t* As[2] = {lds + 2 * kTrTokens * C::PB, lds + 2 * kTrTokens * C::PB + kTrTokens * C::PA};
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wu = wave >> 1, wv = wave & 1;
-  const rsrc_t rb = make_rsrc(b_rows, (uint32_t)((int64_t)rows * d_out * 2));
-  const rsrc_t ra = make_rsrc(a_rows, (uint32_t)((int64_t)rows * d_in * 2));
 
 #pragma unroll
   for (int i = 0; i < WM; ++i)
@@ -62,41 +104,24 @@ __device__ inline void g_tile(const uint8_t* b_rows, const uint8_t* a_rows, int 
 #pragma unroll
       for (int v = 0; v < 16; ++v) acc[i][j][v] = 0.f;
 
-  i32x4 pb[C::CB], pa[C::CA];
-  auto gload = [&](int t0) {
+  auto swrite = [&](int sb) {
 #pragma unroll
     for (int i = 0; i < C::CB; ++i) {
       const int c = tid + 256 * i, row = c / (C::TM / 8), fc = c % (C::TM / 8);
-      const int u = u0 + fc * 8;
-      const uint32_t off = u < d_out ? (uint32_t)(((int64_t)(t0 + row) * d_out + u) * 2) : kOOB;
-      pb[i] = load16(rb, off);
+      *(i32x4*)(Bs[sb] + row * C::PB + fc * 16) = st.b[i];
     }
 #pragma unroll
     for (int i = 0; i < C::CA; ++i) {
       const int c = tid + 256 * i, row = c / (C::TN / 8), fc = c % (C::TN / 8);
-      const int v = v0 + fc * 8;
-      const uint32_t off = v < d_in ? (uint32_t)(((int64_t)(t0 + row) * d_in + v) * 2) : kOOB;
-      pa[i] = load16(ra, off);
-    }
-  };
-  auto swrite = [&](int st) {
-#pragma unroll
-    for (int i = 0; i < C::CB; ++i) {
-      const int c = tid + 256 * i, row = c / (C::TM / 8), fc = c % (C::TM / 8);
-      *(i32x4*)(Bs[st] + row * C::PB + fc * 16) = pb[i];
-    }
-#pragma unroll
-    for (int i = 0; i < C::CA; ++i) {
-      const int c = tid + 256 * i, row = c / (C::TN / 8), fc = c % (C::TN / 8);
-      *(i32x4*)(As[st] + row * C::PA + fc * 16) = pa[i];
+      *(i32x4*)(As[sb] + row * C::PA + fc * 16) = st.a[i];
     }
   };
   // transposed operand of K step ks (16 tokens) for the 32 features starting
   // at local column m: lane 16q + 4r + a reads row 16ks + 8(q/2) + 4h + r at
   // features m + 16(q%2) + 4a, h = 0, 1
-  const int q = lane >> 4, r = (lane >> 2) & 3, aa = lane & 3;
+  const int q = lane >> 4, rr = (lane >> 2) & 3, aa = lane & 3;
   auto frag = [&](const uint8_t* base, int pitch, int m, int ks) {
-    const int row = ks * 16 + 8 * (q >> 1) + r;
+    const int row = ks * 16 + 8 * (q >> 1) + rr;
     const uint8_t* p = base + row * pitch + (m + 16 * (q & 1) + 4 * aa) * 2;
     const i16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16(DATTRI_LDS16(p));
     const i16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16(DATTRI_LDS16(p + 4 * pitch));
@@ -108,21 +133,21 @@ __device__ inline void g_tile(const uint8_t* b_rows, const uint8_t* a_rows, int 
   };
 
   const int nst = (rows + kTrTokens - 1) / kTrTokens;
-  if (nst > 0) {
-    gload(0);
-    swrite(0);
-  }
+  if (nst > 0) swrite(0);
   __syncthreads();
   for (int kk = 0; kk < nst; ++kk) {
-    const int st = kk & 1;
-    if (kk + 1 < nst) gload((kk + 1) * kTrTokens);
+    const int sb = kk & 1;
+    if (kk + 1 < nst)
+      g_load(r, (kk + 1) * kTrTokens, u0, v0, st);
+    else if (next_v0 >= 0)
+      g_load(r, 0, u0, next_v0, st);
 #pragma unroll
     for (int ks = 0; ks < kTrTokens / 16; ++ks) {
       i32x4 fa[WM], fb[WN];
 #pragma unroll
-      for (int i = 0; i < WM; ++i) fa[i] = frag(Bs[st], C::PB, wu * 32 * WM + i * 32, ks);
+      for (int i = 0; i < WM; ++i) fa[i] = frag(Bs[sb], C::PB, wu * 32 * WM + i * 32, ks);
 #pragma unroll
-      for (int j = 0; j < WN; ++j) fb[j] = frag(As[st], C::PA, wv * 32 * WN + j * 32, ks);
+      for (int j = 0; j < WN; ++j) fb[j] = frag(As[sb], C::PA, wv * 32 * WN + j * 32, ks);
 #pragma unroll
       for (int i = 0; i < WM; ++i)
 #pragma unroll
@@ -130,9 +155,20 @@ __device__ inline void g_tile(const uint8_t* b_rows, const uint8_t* a_rows, int 
           acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, fa[i]),
                                                              __builtin_bit_cast(bf16x8, fb[j]), acc[i][j], 0, 0, 0);
     }
-    if (kk + 1 < nst) swrite(st ^ 1);
+    if (kk + 1 < nst) swrite(sb ^ 1);
     __syncthreads();
   }
+  if (nst == 0 && next_v0 >= 0) g_load(r, 0, u0, next_v0, st);
+}
+
+// The same for a single tile: loads its first stage, then runs it.
+template <int WM, int WN>
+__device__ inline void g_tile(const uint8_t* b_rows, const uint8_t* a_rows, int rows, int d_out, int d_in,
+                              int u0, int v0, uint8_t* lds, f32x16 (&acc)[WM][WN]) {
+  const GRows r = g_rows(b_rows, a_rows, rows, d_out, d_in);
+  GStage<WM, WN> st;
+  if (rows > 0) g_load(r, 0, u0, v0, st);
+  g_tile_from(r, rows, u0, v0, -1, lds, st, acc);
 }
 
 }  // namespace dev

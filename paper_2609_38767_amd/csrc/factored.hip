@@ -4,8 +4,11 @@
 //
 // A workgroup of 4 waves owns a chunk of token rows of one example and one
 // input group (layers sharing A, e.g. q/k/v).  For each sub-chunk of
-// 4 x RT x 16 rows it streams A once and each member's B once from HBM,
-// straight into MFMA operand registers: 16-byte buffer loads, prefetched PD
+// 4 x RT x 16 rows it streams A once and each member's B once from HBM.  bf16
+// blocks with aligned rows and 2-tile output maps go through LDS by direct
+// loads (project_rows_dma, up to 6 input tiles, so q/k/v and gate/up share
+// one pass over A).  Otherwise rows go straight into MFMA operand registers:
+// 16-byte buffer loads, prefetched PD
 // k-blocks ahead in a register ring (ragged rows and feature tails read as
 // zero through the descriptor range).  Projection fragments are staged once
 // per workgroup in LDS, one panel of KP k-blocks at a time (loaded a panel
@@ -27,6 +30,17 @@ using namespace dev;
 
 // Two waves per SIMD where the accumulators and load ring fit in 256 VGPRs.
 constexpr int waves_of(int na, int nb) { return ((na * nb <= 16 && na <= 6) || na * nb <= 8) ? 2 : 1; }
+
+// Instances that stream factor rows by direct loads into LDS.
+constexpr bool dma_instance(int elt, bool aligned, int na, int nb) {
+  return elt == 2 && aligned && nb == 2 && (na == 2 || na == 4 || na == 6);
+}
+
+// Workgroups per CU the launch bounds ask for: the grouped direct-load
+// instances (4 or 6 input tiles) hold 88-100 KiB of LDS, one per CU.
+constexpr int occupancy_of(int elt, bool aligned, int na, int nb) {
+  return !aligned ? 1 : (dma_instance(elt, aligned, na, nb) && na > 2) ? 1 : waves_of(na, nb);
+}
 
 // Projected rows of a wave's RT x 16 token rows, tiles [t0, t0 + nt) of acc,
 // into dst rows of k floats (columns >= k and rows >= row_end are skipped).
@@ -50,18 +64,19 @@ __device__ inline void store_rows(const f32x4 (&acc)[RT][NT], float* dst, int k,
 }
 
 template <int ELT, bool AL, int RT, int NA, int NB>
-__global__ __launch_bounds__(256, AL ? waves_of(NA, NB) : 1) void factored_kernel(const FactItem* __restrict__ items,
+__global__ __launch_bounds__(256, occupancy_of(ELT, AL, NA, NB)) void factored_kernel(const FactItem* __restrict__ items,
                                                           const FactGroup* __restrict__ groups,
                                                           const FactMember* __restrict__ members,
                                                           float* __restrict__ partials) {
   constexpr int NTL = NA > NB ? NA : NB;
   constexpr int PD = AL ? pd_of(RT, NA, NB) : 2;
-  // bf16 with aligned rows and two map tiles per side: factor rows streamed
-  // through LDS by direct loads (project_rows_dma); otherwise operand loads
-  // straight into registers with projection panels in LDS (project_rows)
-  constexpr bool kDma = ELT == 2 && AL && NA == 2 && NB == 2;
+  // bf16 with aligned rows, two output map tiles and 2, 4 or 6 input map
+  // tiles (one layer, or up to three sharing their input block): factor rows
+  // streamed through LDS by direct loads (project_rows_dma); otherwise operand
+  // loads straight into registers with projection panels in LDS (project_rows)
+  constexpr bool kDma = dma_instance(ELT, AL, NA, NB);
   constexpr int kPanBytes = 2 * kPanel * NTL * kFragBytes;
-  constexpr int kSmem = kDma ? DmaLds<RT, 2>::kBytes : kPanBytes;
+  constexpr int kSmem = kDma ? DmaLds<RT, kDma ? NA : 2>::kBytes : kPanBytes;
   __shared__ __align__(1024) uint8_t smem[kSmem];
   auto pan = reinterpret_cast<uint8_t(*)[kPanel][NTL][kFragBytes]>(smem);
   const FactItem it = items[blockIdx.x];
@@ -183,12 +198,15 @@ __global__ __launch_bounds__(256, AL ? waves_of(NA, NB) : 1) void factored_kerne
 // ------------------------------------------------------------ instances
 // Aligned instances per (input tiles NA, output tiles NB); one unaligned
 // instance (8, 4) serves any group whose rows are not 16-byte multiples.
-// Rows per wave RT keeps two waves per SIMD within the register file.
-constexpr int rt_of(int na, int nb) { return (na <= 2 && nb <= 2) ? 4 : ((na * nb <= 16 && na <= 6) ? 2 : 1); }
+// Rows per wave RT keeps two waves per SIMD within the register file; the
+// direct-load instances keep 4 row tiles per wave however many layers share
+// the input block, so grouping those layers costs no rows in flight.
+constexpr int rt_of(int elt, int na, int nb) {
+  return (na <= 2 && nb <= 2) || dma_instance(elt, true, na, nb) ? 4 : ((na * nb <= 16 && na <= 6) ? 2 : 1);
+}
 
 void factored_instance(int elt, int na_req, int nb_req, int aligned, int* na_inst, int* nb_inst,
                        int* rows_per_wave) {
-  (void)elt;
   int na = 8, nb = 4;
   if (aligned) {
     const int na_list[] = {1, 2, 4, 6, 8};
@@ -198,13 +216,13 @@ void factored_instance(int elt, int na_req, int nb_req, int aligned, int* na_ins
   }
   *na_inst = na;
   *nb_inst = nb;
-  *rows_per_wave = rt_of(na, nb);
+  *rows_per_wave = aligned ? rt_of(elt, na, nb) : 1;
 }
 
 template <int ELT, bool AL, int NA, int NB>
 static hipError_t launch_one(const FactItem* items, int n, const FactGroup* g, const FactMember* m,
                              float* part, hipStream_t s) {
-  constexpr int RT = rt_of(NA, NB);
+  constexpr int RT = AL ? rt_of(ELT, NA, NB) : 1;
   hipLaunchKernelGGL((factored_kernel<ELT, AL, RT, NA, NB>), dim3(n), dim3(256), 0, s, items, g, m, part);
   return hipGetLastError();
 }

@@ -144,9 +144,10 @@ __device__ inline void project_rows(const rsrc_t r, int r_wave, int nrows, int d
 // 128 bytes apart with their 16-byte chunks XOR-swizzled by (row & 7) so the
 // MFMA fragment reads (16 rows x 16 bytes per lane group) spread over the
 // banks: each lane fetches the chunk that lands in its fixed LDS slot.  The
-// stage's NT x 2 projection fragments (one per wave, NT = 2) go by direct load
-// into a 3-slot ring shared by the workgroup.  Every wave issues exactly
-// kDmaOps loads per stage, so "stage s has landed" is vmcnt(kDmaOps) while
+// stage's 2 x NT projection fragments (NT / 2 per wave; NT = 2, 4 or 6, so
+// the maps of up to three layers that share the input block ride along) go by
+// direct load into a 3-slot ring shared by the workgroup.  Every wave issues
+// exactly kDmaOps loads per stage, so "stage s has landed" is vmcnt(kDmaOps) while
 // stage s + 1 is in flight and vmcnt(0) otherwise (any extra load issued later
 // would only make that wait longer); one barrier per stage then publishes the
 // shared fragments.  The wave's reads of a buffer finish (lgkmcnt(0)) before
@@ -156,11 +157,12 @@ __device__ inline void project_rows(const rsrc_t r, int r_wave, int nrows, int d
 // bitwise those of the register path.
 template <int RT, int NT>
 struct DmaLds {
-  static_assert(NT * 2 == kWaves, "one projection fragment per wave and stage");
+  static_assert((2 * NT) % kWaves == 0 && 2 * NT <= 3 * kWaves, "NT / 2 projection fragments per wave and stage");
   static constexpr int kRowBytes = 128;                      // 2 k-blocks of 32 bf16
   static constexpr int kWaveStage = RT * 16 * kRowBytes;     // bytes per wave and stage
   static constexpr int kLoads = RT * 16 / 8;                 // 1 KiB row-group loads per stage
-  static constexpr int kDmaOps = kLoads + 1;                 // plus the wave's fragment
+  static constexpr int kMapLoads = 2 * NT / kWaves;          // this wave's fragments per stage
+  static constexpr int kDmaOps = kLoads + kMapLoads;
   static constexpr int kMapOff = kWaves * 2 * kWaveStage;
   static constexpr int kMapStage = 2 * NT * kFragBytes;
   static constexpr int kBytes = kMapOff + 3 * kMapStage;
@@ -183,10 +185,29 @@ __device__ inline void project_rows_dma(const rsrc_t r, int r_wave, int nrows, i
   const int nkb = (d + 31) / 32;
   const int nst = (nkb + 1) / 2;
   uint8_t* own = lds + wave * 2 * C::kWaveStage;
-  // this wave's projection fragment of every stage: k-block 2s + kbl of tile t
-  const int f_kbl = wave / NT, f_t = wave % NT;
-  const int64_t f_stride = P.stride[f_t];
-  const rsrc_t rp = make_rsrc(P.base[f_t], (uint32_t)((int64_t)nkb * f_stride));
+  // this wave's projection fragments of every stage: fragment f = wave *
+  // kMapLoads + i of the stage is k-block 2s + f / NT of tile f % NT
+  int f_kbl[C::kMapLoads], f_t[C::kMapLoads];
+  int64_t f_stride[C::kMapLoads];
+  const uint8_t* f_base[C::kMapLoads];  // (descriptors are built per load: no arrays of rsrc_t)
+#pragma unroll
+  for (int i = 0; i < C::kMapLoads; ++i) {
+    const int f = wave * C::kMapLoads + i;
+    f_kbl[i] = f / NT;
+    f_t[i] = f % NT;
+    // a select chain, not P.base[f_t[i]]: a runtime index would put the
+    // arrays in memory (the compiler promotes them to LDS)
+    const uint8_t* base = P.base[0];
+    int64_t stride = P.stride[0];
+#pragma unroll
+    for (int t = 1; t < NT; ++t)
+      if (f_t[i] == t) {
+        base = P.base[t];
+        stride = P.stride[t];
+      }
+    f_stride[i] = stride;
+    f_base[i] = base;
+  }
 
   auto issue = [&](int s) {
     uint8_t* xs = own + (s & 1) * C::kWaveStage;
@@ -198,10 +219,14 @@ __device__ inline void project_rows_dma(const rsrc_t r, int r_wave, int nrows, i
       const uint32_t off = (row < nrows && col < d) ? (uint32_t)(((int64_t)row * ld + col) * 2) : kOOB;
       __builtin_amdgcn_raw_ptr_buffer_load_lds(r, DATTRI_LDS_PTR(xs + i * 1024), 16, off, 0, 0, 0);
     }
-    const int kb = 2 * s + f_kbl;
-    uint8_t* ms = lds + C::kMapOff + (s % 3) * C::kMapStage + (f_kbl * NT + f_t) * kFragBytes;
-    const uint32_t moff = (f_t < P.nt && kb < nkb) ? (uint32_t)(kb * f_stride + lane * 16) : kOOB;
-    __builtin_amdgcn_raw_ptr_buffer_load_lds(rp, DATTRI_LDS_PTR(ms), 16, moff, 0, 0, 0);
+#pragma unroll
+    for (int i = 0; i < C::kMapLoads; ++i) {
+      const int kb = 2 * s + f_kbl[i];
+      uint8_t* ms = lds + C::kMapOff + (s % 3) * C::kMapStage + (f_kbl[i] * NT + f_t[i]) * kFragBytes;
+      const uint32_t moff = (f_t[i] < P.nt && kb < nkb) ? (uint32_t)(kb * f_stride[i] + lane * 16) : kOOB;
+      const rsrc_t rp = make_rsrc(f_base[i], (uint32_t)((int64_t)nkb * f_stride[i]));
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(rp, DATTRI_LDS_PTR(ms), 16, moff, 0, 0, 0);
+    }
   };
 
   // the stage barrier: this wave's LDS reads done, then s_barrier.  An inline

@@ -262,10 +262,13 @@ dattri_status dattri::build_plan(const dattri_ctx* ctx, dattri_route forced, Pla
 
   // ---- factored layers: group by shared input block A.  A layer joins a
   // group only while the grouped kernel instance keeps the token rows per wave
-  // of the layer alone: on MI355X the fused kernel streams markedly faster at
-  // 4 row tiles per wave than at 2 or 1, more than the cost of reading A once
-  // per layer (Llama-3-8B stack: 15.8 ms per batch ungrouped vs 17.4 ms with
-  // q/k/v and gate/up grouped).
+  // of the layer alone: on MI355X the register-path kernel streams markedly
+  // faster at 4 row tiles per wave than at 2 or 1, more than the cost of
+  // reading A once per layer (Llama-3-8B stack: 15.8 ms per batch ungrouped vs
+  // 17.4 ms with q/k/v and gate/up grouped).  The direct-load instances (bf16,
+  // aligned rows, output maps of 2 tiles) keep 4 row tiles per wave with up to
+  // 6 input tiles, so there q/k/v and gate/up do group and A is read once per
+  // block: 85.5 -> 74.0 GB and 13.08 -> 12.33 ms per batch of 8.
   auto rows_per_wave = [&](int na, int nb) {
     int nai, nbi, rt;
     factored_instance(elt, na, nb, 1, &nai, &nbi, &rt);

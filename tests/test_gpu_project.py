@@ -134,6 +134,31 @@ def test_fused_direct_lds_path_ragged():
     assert rel_fro(host64(phi_s), host64(phi)) < 1e-6
 
 
+def test_grouped_direct_lds_path_ragged():
+    # layers sharing an input block run as one work item of the direct-to-LDS
+    # kernel when their input maps add up to 4 or 6 tiles and no output map
+    # exceeds 2 tiles: a q/k/v-like group of 2 + 1 + 2 input tiles (instance of
+    # 6, the last tile unused) and a gate/up-like pair of 2 + 2, d_in not a
+    # multiple of the 64-column stage, ragged lengths and an empty example
+    layers = [dict(name="q", d_in=520, d_out=200, k_in=32, k_out=32, a_group="a"),
+              dict(name="k", d_in=520, d_out=72, k_in=16, k_out=16, a_group="a"),
+              dict(name="v", d_in=520, d_out=136, k_in=24, k_out=32, a_group="a"),
+              dict(name="gate", d_in=192, d_out=264, k_in=32, k_out=32, a_group="b"),
+              dict(name="up", d_in=192, d_out=264, k_in=32, k_out=24, a_group="b"),
+              dict(name="down", d_in=264, d_out=192, k_in=32, k_out=32, a_group="c")]
+    wl = dict(W.WORKLOADS["tiny"], dist_a="student_t4", dist_b="student_t4", seed=101)
+    n, T = 5, 600
+    inputs = _session_inputs(wl, layers, n, T, "bf16")
+    assert inputs[0][0] is inputs[2][0] and inputs[3][0] is inputs[4][0]
+    lengths = torch.tensor([600, 0, 257, 1, 511], dtype=torch.int32, device=DEV)
+    _, phi = _run(layers, inputs, "bf16", 103, "factored", lengths=lengths, form="fused")
+    assert torch.count_nonzero(phi[1]).item() == 0
+    _check(layers, inputs, phi, 103, "bf16", [0, 2, 3, 4], lengths=lengths, tol=1e-5)
+    # the split form (register path, one factor block at a time) agrees to rounding
+    _, phi_s = _run(layers, inputs, "bf16", 103, "factored", lengths=lengths, form="split")
+    assert rel_fro(host64(phi_s), host64(phi)) < 1e-6
+
+
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
 @pytest.mark.parametrize("route,form", [("factored", "fused"), ("factored", "split"), ("materialized", None)])
 def test_rademacher_maps(dtype, route, form):

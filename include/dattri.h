@@ -318,21 +318,23 @@ dattri_status dattri_materialize_gradient(dattri_ctx* ctx, int32_t layer, int32_
  * launch plan decides.  The materialized route has two implementations:
  *   - one pass (bf16 blocks with 16-byte aligned rows, k_in <= 128): each
  *     workgroup forms 128 rows of G over a token chunk, 128 columns at a
- *     time, and projects every tile on chip, so G never goes to memory;
+ *     time, and projects every tile from its accumulators, so G never goes
+ *     to memory;
  *       materialized = call_us + max(W, B_f / gradient_gbs) + chunks_e * launch_us,
  *     chunks_e the launches of at most 65535 examples each (the small
  *     reduction of partial products behind each is charged no launch of its
  *     own: on MI355X the pair's fixed cost measures about one launch), and
- *     W the work of its launch shape: rounds of 256 workgroups
- *     (one per CU) times, per workgroup and 128-column tile, tok_chunk / 32
- *     token stages at 256 x 2 x 32 x 128 x 128 FLOP per round plus one tile
- *     projection (G split into three bf16 terms) at 256 x 3 x 2 x 128 x 128
- *     x 16 x tiles(k_in) FLOP per round, both bf16 MFMA at gradient_tflops,
- *     plus once per workgroup H^T P_out in float32 at 256 x 2 x 128 x 16
- *     tiles(k_in) x 16 tiles(k_out) FLOP per round at gproject_tflops, plus
- *     round_us per round (a workgroup's load latencies and barriers,
- *     whatever its work); the token chunks and column ranges are the ones
- *     that minimise W;
+ *     W the work of its launch shape: rounds of 256 occ workgroups (occ
+ *     per CU: 2 when k_in <= 64, else 1) times occ times, per workgroup and
+ *     128-column tile, tok_chunk / 32 token stages at 256 x 2 x 32 x 128 x
+ *     128 FLOP per round plus one tile projection (G split into three bf16
+ *     terms) at 256 x 3 x 2 x 128 x 128 x 16 x tiles(k_in) FLOP per round,
+ *     plus once per workgroup the closing H^T P_out, also three bf16 terms,
+ *     at 256 x 3 x 2 x 128 x 16 tiles(k_in) x 32 tiles32(k_out) FLOP per
+ *     round, all bf16 MFMA at gradient_tflops (tiles(k_in) = 2, 4 or 8, the
+ *     16-column tiles of the instance), plus round_us per round (load
+ *     latencies and barriers, whatever the work); the token chunks and
+ *     column ranges are the ones that minimise W;
  *   - otherwise (float32, unaligned rows, k_in > 128) G is staged in the
  *     workspace, chunks_m example chunks of at most 2 GiB of G each:
  *       materialized = call_us + max(F_g / gradient_tflops, B_g / gradient_gbs)
@@ -351,7 +353,7 @@ typedef struct {
   double factored_gbs;
   double gradient_tflops;     /* G = B^T A */
   double gradient_gbs;
-  double gproject_tflops;     /* float32 MFMA: staged P_out^T G P_in, one-pass H^T P_out */
+  double gproject_tflops;     /* float32 MFMA: staged P_out^T G P_in */
   double gproject_gbs;
   double launch_us;           /* per kernel launch */
   double call_us;             /* per call, either route */

@@ -33,6 +33,10 @@ constexpr uint32_t kOOB = 0xFFFFFFF0u;  // an offset no descriptor here covers
 __device__ inline i32x4 load16(rsrc_t r, uint32_t off) {
   return __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, 0);
 }
+typedef int i32x2 __attribute__((ext_vector_type(2)));
+__device__ inline i32x2 load8(rsrc_t r, uint32_t off) {
+  return __builtin_bit_cast(i32x2, __builtin_amdgcn_raw_buffer_load_b64(r, off, 0, 0));
+}
 __device__ inline uint32_t load4(rsrc_t r, uint32_t off) {
   return (uint32_t)__builtin_amdgcn_raw_buffer_load_b32(r, off, 0, 0);
 }

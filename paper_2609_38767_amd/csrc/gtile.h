@@ -1,8 +1,8 @@
 // One tile of a weight gradient (Eq. (1)) for bf16 factor blocks,
 //   G[u0 .. u0 + 64 WM, v0 .. v0 + 64 WN] = sum_t g_t a_t^T   (float32),
 // over a run of token rows, accumulated in MFMA registers.  Shared by the
-// kernel that writes G (gradient_tr.hip) and the fused materialized-route
-// kernel that projects each tile from LDS (gfused.hip).
+// kernel that writes G (gradient_tr.hip) and the one-pass materialized-route
+// kernel that projects each tile from its accumulators (gfused.hip).
 //
 // The contraction runs over tokens, the strided axis of both factors.  Token
 // rows are loaded with coalesced 16-byte reads and stored in LDS as they are
@@ -83,14 +83,14 @@ __device__ inline void g_load(const GRows& r, int t0, int u0, int v0, GStage<WM,
 // acc[i][j] = G block (i, j) of this wave over token rows [0, rows) of tile
 // (u0, v0).  On entry st holds (or has loads in flight for) the tile's first
 // stage, rows 0 .. 31; the later stages are prefetched one ahead.  With
-// next_v0 >= 0 the last stage also issues the loads of the first stage of
-// tile (u0, next_v0) into st, so a caller walking a row of tiles keeps a
+// next_u0 >= 0 the last stage also issues the loads of the first stage of
+// tile (next_u0, next_v0) into st, so a caller walking a run of tiles keeps a
 // load in flight across the tile boundary.  lds: GTile<WM, WN>::kLdsBytes of
 // shared memory.  All 256 threads call this together; it ends with a barrier
 // (lds may be reused after it).
 template <int WM, int WN>
-__device__ inline void g_tile_from(const GRows& r, int rows, int u0, int v0, int next_v0, uint8_t* lds,
-                                   GStage<WM, WN>& st, f32x16 (&acc)[WM][WN]) {
+__device__ inline void g_tile_from(const GRows& r, int rows, int u0, int v0, int next_u0, int next_v0,
+                                   uint8_t* lds, GStage<WM, WN>& st, f32x16 (&acc)[WM][WN]) {
   using C = GTile<WM, WN>;
   uint8_t* Bs[2] = {lds, lds + kTrTokens * C::PB};
   uint8_t* As[2] = {lds + 2 * kTrTokens * C::PB, lds + 2 * kTrTokens * C::PB + kTrTokens * C::PA};
@@ -139,8 +139,8 @@ __device__ inline void g_tile_from(const GRows& r, int rows, int u0, int v0, int
     const int sb = kk & 1;
     if (kk + 1 < nst)
       g_load(r, (kk + 1) * kTrTokens, u0, v0, st);
-    else if (next_v0 >= 0)
-      g_load(r, 0, u0, next_v0, st);
+    else if (next_u0 >= 0)
+      g_load(r, 0, next_u0, next_v0, st);
 #pragma unroll
     for (int ks = 0; ks < kTrTokens / 16; ++ks) {
       i32x4 fa[WM], fb[WN];
@@ -158,7 +158,7 @@ __device__ inline void g_tile_from(const GRows& r, int rows, int u0, int v0, int
     if (kk + 1 < nst) swrite(sb ^ 1);
     __syncthreads();
   }
-  if (nst == 0 && next_v0 >= 0) g_load(r, 0, u0, next_v0, st);
+  if (nst == 0 && next_u0 >= 0) g_load(r, 0, next_u0, next_v0, st);
 }
 
 // The same for a single tile: loads its first stage, then runs it.
@@ -168,7 +168,7 @@ __device__ inline void g_tile(const uint8_t* b_rows, const uint8_t* a_rows, int 
   const GRows r = g_rows(b_rows, a_rows, rows, d_out, d_in);
   GStage<WM, WN> st;
   if (rows > 0) g_load(r, 0, u0, v0, st);
-  g_tile_from(r, rows, u0, v0, -1, lds, st, acc);
+  g_tile_from(r, rows, u0, v0, -1, 0, lds, st, acc);
 }
 
 }  // namespace dev

@@ -171,7 +171,7 @@ hipError_t launch_gproject(int elt_bytes, const GProjArgs& a, hipStream_t s);
 
 // Fused materialized route (bf16, 16-byte aligned rows, k_in <= 128): each
 // workgroup forms 128 rows of G over one token chunk, 128 columns at a time,
-// and projects every tile from LDS, so G never goes to memory.
+// and projects every tile from its accumulators, so G never goes to memory.
 struct GFusedArgs {
   const void* A; const void* B; const int32_t* lengths;
   const void* P_in; const void* P_out;  // packed bf16
@@ -185,7 +185,8 @@ struct GFusedArgs {
 constexpr int kGFusedCols = 128;    // columns of G per tile
 constexpr int kGFusedRows = 128;
 constexpr int kGFusedMaxTilesIn = 8;
-int gfused_tiles_in(int k_in);      // input tiles of the kernel instance serving k_in
+int gfused_tiles_in(int k_in);      // 16-column tiles of k_in the kernel instance serving k_in holds
+int gfused_wgs_per_cu(int k_in);    // workgroups of that instance one CU holds
 hipError_t launch_gfused(const GFusedArgs& a, hipStream_t s);
 
 // ------------------------------------------------------ cross-Gram matrices

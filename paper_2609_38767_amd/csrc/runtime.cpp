@@ -53,21 +53,19 @@ dattri_cost_model default_cost_model() {
   // single-layer shapes: transformer, adapter-shaped and narrow layers,
   // T = 16..4096, both forced routes timed with launch plans kept on the
   // device), every rate held below its bound: AUTO picks the faster route on
-  // all 28 shapes, root-mean-square log error of the predictions 0.14.  On a
-  // fresh sweep after the one-pass kernel gained its cross-tile prefetch
-  // (routing-sized layer 16.9 -> 12.6 ms), the same model picks the faster
-  // route on 27 of 28 shapes, mean regret 0.2%, worst 5.9%.
-  // gproject_gbs serves only the staged-G route, which that sweep does not run.
+  // all 28 shapes, root-mean-square log error of the predictions 0.16.
+  // gproject_gbs and gproject_tflops serve only the staged-G route, which
+  // that sweep does not run.
   dattri_cost_model m;
-  m.factored_tflops = 164.3;
-  m.factored_gbs = 5130.6;
-  m.gradient_tflops = 372.7;
-  m.gradient_gbs = 6449.6;
+  m.factored_tflops = 176.9;
+  m.factored_gbs = 5714.2;
+  m.gradient_tflops = 657.1;
+  m.gradient_gbs = 6450.0;
   m.gproject_tflops = 157.3;
   m.gproject_gbs = 5000.0;
-  m.launch_us = 10.35;
+  m.launch_us = 10.74;
   m.call_us = 0.0;
-  m.round_us = 2.74;
+  m.round_us = 0.449;
   return m;
 }
 
@@ -154,28 +152,30 @@ bool fused_materialized(const Layer& L, int elt) {
 }
 
 // Launch shape of the one-pass kernel and its predicted time.  A workgroup
-// (one per CU: 104 KiB of LDS) runs, per 128-column tile of G in its range,
-// tok_chunk / 32 token stages and a projection of the tile (three bf16 MFMA
-// terms per product, about 3 stages' worth per 16 columns of P_in), then one
-// H^T P_out in float32.  Token chunks and column ranges add workgroups but the
-// chunks repeat the projections; the shape minimising rounds of 256
-// workgroups x per-workgroup time wins.  Times use the model's rates: a round
-// of 256 workgroups each running one stage is 256 x 2 x 32 x 128 x 128 FLOP,
-// one tile projection per workgroup 256 x 3 x 2 x 128 x 128 x 16 x tiles_in
-// FLOP, both bf16 MFMA at gradient_tflops; the closing product 256 x 2 x 128
-// x 16 tiles_in x 16 tiles_out FLOP of float32 MFMA at gproject_tflops; each
-// round also costs round_us (load latencies and barriers, whatever the work).
+// runs, per 128-column tile of G in its range, tok_chunk / 32 token stages
+// and a projection of the tile from its accumulators (three bf16 MFMA terms
+// per product, against 32 tiles_in / 2 columns of P_in), then one closing
+// H^T P_out the same way.  occ workgroups share a CU (36 KiB of LDS each; two
+// when k_in <= 64, where the registers allow it).  Token chunks and column
+// ranges add workgroups but the chunks repeat the projections; the shape
+// minimising rounds of 256 occ workgroups x occ x per-workgroup time wins.
+// Times use the model's rates: a round of 256 workgroups each running one
+// stage is 256 x 2 x 32 x 128 x 128 FLOP, one tile projection per workgroup
+// 256 x 3 x 2 x 128 x 128 x 16 x tiles_in FLOP, the closing product
+// 256 x 3 x 2 x 128 x 16 tiles_in x 32 tiles32(k_out) FLOP, all bf16 MFMA at
+// gradient_tflops; each round also costs round_us (load latencies and
+// barriers, whatever the work).
 struct FusedShape { int n_tchunks, tok_chunk, n_vsplit, vt_per_split; double us; };
 FusedShape fused_shape(const Layer& L, int64_t n, const dattri_cost_model& m) {
   const int64_t T = std::max<int64_t>(L.T, 1);
   const int64_t n_ub = (L.d_out + kGFusedRows - 1) / kGFusedRows;
   const int64_t n_vt = (L.d_in + kGFusedCols - 1) / kGFusedCols;
+  const int occ = gfused_wgs_per_cu(L.k_in);
   const double stage_us = 256.0 * 2 * 32 * kGFusedRows * kGFusedCols / (m.gradient_tflops * 1e6);
   const double proj_us = 256.0 * 3 * 2 * kGFusedRows * kGFusedCols * 16 * gfused_tiles_in(L.k_in) /
                          (m.gradient_tflops * 1e6);
-  // the closing H^T P_out of every workgroup, also float32 MFMA
-  const double epi_us = 256.0 * 2 * kGFusedRows * 16 * gfused_tiles_in(L.k_in) * 16 * tiles16(L.k_out) /
-                        (m.gproject_tflops * 1e6);
+  const double epi_us = 256.0 * 3 * 2 * kGFusedRows * 16 * gfused_tiles_in(L.k_in) * 32 *
+                        ((L.k_out + 31) / 32) / (m.gradient_tflops * 1e6);
   FusedShape best{1, (int)((T + 31) / 32 * 32), 1, (int)n_vt, -1.0};
   for (int64_t c = 1; c <= (T + 31) / 32; c *= 2) {
     const int64_t tok_chunk = ((T + c - 1) / c + 31) / 32 * 32;
@@ -183,9 +183,11 @@ FusedShape fused_shape(const Layer& L, int64_t n, const dattri_cost_model& m) {
     for (int64_t v = 1; v <= n_vt; v *= 2) {
       const int64_t vps = (n_vt + v - 1) / v;
       const int64_t splits = (n_vt + vps - 1) / vps;
-      const int64_t rounds = (std::max<int64_t>(n, 1) * n_ub * splits * chunks + 255) / 256;
-      const double us =
-          (double)rounds * ((double)vps * ((double)(tok_chunk / 32) * stage_us + proj_us) + epi_us + m.round_us);
+      const int64_t slots = 256 * (int64_t)occ;
+      const int64_t rounds = (std::max<int64_t>(n, 1) * n_ub * splits * chunks + slots - 1) / slots;
+      const double us = (double)rounds * ((double)occ * ((double)vps * ((double)(tok_chunk / 32) * stage_us + proj_us) +
+                                                         epi_us) +
+                                          m.round_us);
       if (best.us < 0 || us < best.us)
         best = FusedShape{(int)chunks, (int)tok_chunk, (int)splits, (int)vps, us};
     }

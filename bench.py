@@ -563,7 +563,7 @@ def fit_case(dev, steps, warmup):
             "roofline": {"bound": "hbm", "achieved": bytes_batch / (avg * 1e-3) / 1e9, "peak": 8000.0,
                          "unit": "GB/s", "frac": bytes_batch / (avg * 1e-3) / 1e9 / 8000.0,
                          "traffic": measured_traffic("projection_fit"),
-                         "kernel": "projection with factor sums (split form stage 1 + contraction + row sums), "
+                         "kernel": "projection with factor sums (direct-load fused kernels keeping the projected rows + row sums), "
                                    "one batch of 32 x 196 layers, T=512, k=64"}}
 
 

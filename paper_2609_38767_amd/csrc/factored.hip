@@ -31,15 +31,18 @@ using namespace dev;
 // Two waves per SIMD where the accumulators and load ring fit in 256 VGPRs.
 constexpr int waves_of(int na, int nb) { return ((na * nb <= 16 && na <= 6) || na * nb <= 8) ? 2 : 1; }
 
-// Instances that stream factor rows by direct loads into LDS.
+// Instances that stream factor rows by direct loads into LDS: output maps of
+// 2 tiles with 2, 4 or 6 input tiles (one layer, or up to three sharing their
+// input block), or of 4 tiles with 2 or 4 input tiles (k = 64 layers).
 constexpr bool dma_instance(int elt, bool aligned, int na, int nb) {
-  return elt == 2 && aligned && nb == 2 && (na == 2 || na == 4 || na == 6);
+  return elt == 2 && aligned &&
+         ((nb == 2 && (na == 2 || na == 4 || na == 6)) || (nb == 4 && (na == 2 || na == 4)));
 }
 
-// Workgroups per CU the launch bounds ask for: the grouped direct-load
-// instances (4 or 6 input tiles) hold 88-100 KiB of LDS, one per CU.
+// Workgroups per CU the launch bounds ask for: the direct-load instances with
+// 4 or 6 map tiles on a side hold 88-100 KiB of LDS, one per CU.
 constexpr int occupancy_of(int elt, bool aligned, int na, int nb) {
-  return !aligned ? 1 : (dma_instance(elt, aligned, na, nb) && na > 2) ? 1 : waves_of(na, nb);
+  return !aligned ? 1 : (dma_instance(elt, aligned, na, nb) && (na > 2 || nb > 2)) ? 1 : waves_of(na, nb);
 }
 
 // Projected rows of a wave's RT x 16 token rows, tiles [t0, t0 + nt) of acc,
@@ -76,7 +79,7 @@ __global__ __launch_bounds__(256, occupancy_of(ELT, AL, NA, NB)) void factored_k
   // loads straight into registers with projection panels in LDS (project_rows)
   constexpr bool kDma = dma_instance(ELT, AL, NA, NB);
   constexpr int kPanBytes = 2 * kPanel * NTL * kFragBytes;
-  constexpr int kSmem = kDma ? DmaLds<RT, kDma ? NA : 2>::kBytes : kPanBytes;
+  constexpr int kSmem = kDma ? DmaLds<RT, kDma ? NTL : 2>::kBytes : kPanBytes;
   __shared__ __align__(1024) uint8_t smem[kSmem];
   auto pan = reinterpret_cast<uint8_t(*)[kPanel][NTL][kFragBytes]>(smem);
   const FactItem it = items[blockIdx.x];
@@ -204,6 +207,8 @@ __global__ __launch_bounds__(256, occupancy_of(ELT, AL, NA, NB)) void factored_k
 constexpr int rt_of(int elt, int na, int nb) {
   return (na <= 2 && nb <= 2) || dma_instance(elt, true, na, nb) ? 4 : ((na * nb <= 16 && na <= 6) ? 2 : 1);
 }
+
+bool factored_direct_loads(int elt, int na, int nb, int aligned) { return dma_instance(elt, aligned != 0, na, nb); }
 
 void factored_instance(int elt, int na_req, int nb_req, int aligned, int* na_inst, int* nb_inst,
                        int* rows_per_wave) {

@@ -86,6 +86,8 @@ hipError_t launch_factored(int elt_bytes, int na, int nb, int aligned, const Fac
                            float* partials, hipStream_t s);
 void factored_instance(int elt_bytes, int na_req, int nb_req, int aligned, int* na_inst,
                        int* nb_inst, int* rows_per_wave);
+// Whether instance (na, nb) streams factor rows through LDS by direct loads.
+bool factored_direct_loads(int elt_bytes, int na, int nb, int aligned);
 constexpr int kXcds = 8;  // MI355X: workgroup i is dispatched to XCD i mod 8
 
 // max_out: the largest k_in*k_out over the tasks (sets the grid's z extent)

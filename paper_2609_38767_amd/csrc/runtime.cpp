@@ -335,15 +335,18 @@ dattri_status dattri::build_plan(const dattri_ctx* ctx, dattri_route forced, Pla
   }
   const bool few_items = fused_items_total < kSplitMinFusedItems;
   // Wide maps (4 x 4 input x output tiles and more, k > 48 on both sides)
-  // leave the fused kernel 2 row tiles per wave and 2 waves per SIMD; the
-  // split form, which projects one factor at a time, streams faster there
-  // (Qwen2.5-7B-shaped stack, k = 64, T = 512, 32 examples: 19.2 ms vs
-  // 26.8 ms per batch on MI355X).
+  // leave the register-path fused kernel 2 row tiles per wave and 2 waves per
+  // SIMD; the split form, which projects one factor at a time, streams faster
+  // there (Qwen2.5-7B-shaped stack, k = 64, T = 512, 32 examples: 19.2 ms vs
+  // 26.8 ms per batch on MI355X).  The direct-load instances keep 4 row tiles
+  // per wave with 4-tile maps and stay fused.
   auto use_split = [&](size_t g) {
     const Layer& H = ctx->layers[group_layers[g][0]];
     if ((int64_t)n * H.T > (int64_t)INT32_MAX / 2 || n > 65535) return false;  // index / grid range
     if (ctx->form != DATTRI_FORM_AUTO) return ctx->form == DATTRI_FORM_SPLIT;
-    return few_items || gshape[g].na_inst * gshape[g].nb_inst >= 16;
+    const GShape& S = gshape[g];
+    return few_items ||
+           (S.na_inst * S.nb_inst >= 16 && !factored_direct_loads(elt, S.na_inst, S.nb_inst, S.aligned));
   };
 
   size_t fpart_floats = 0;

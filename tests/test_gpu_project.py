@@ -159,6 +159,27 @@ def test_grouped_direct_lds_path_ragged():
     assert rel_fro(host64(phi_s), host64(phi)) < 1e-6
 
 
+def test_wide_map_direct_lds_path_ragged():
+    # 4-tile output maps (k_out 49..64) on the direct-to-LDS path: a (4, 4)
+    # layer, a (2, 4) layer and a (4, 4) layer whose input block is shared
+    # with a (2, 2) one (4 + 2 input tiles exceed the 4-tile instance, so
+    # they stay apart); d not a multiple of the 64-column stage, ragged lengths
+    # and an empty example, against the oracle and the split form
+    layers = [dict(name="w0", d_in=584, d_out=200, k_in=64, k_out=64, a_group="a"),
+              dict(name="w1", d_in=584, d_out=72, k_in=32, k_out=32, a_group="a"),
+              dict(name="w2", d_in=136, d_out=520, k_in=24, k_out=56, a_group="b"),
+              dict(name="w3", d_in=200, d_out=64, k_in=56, k_out=49, a_group="c")]
+    wl = dict(W.WORKLOADS["tiny"], dist_a="student_t4", dist_b="student_t4", seed=107)
+    n, T = 5, 600
+    inputs = _session_inputs(wl, layers, n, T, "bf16")
+    lengths = torch.tensor([600, 0, 257, 1, 511], dtype=torch.int32, device=DEV)
+    _, phi = _run(layers, inputs, "bf16", 109, "factored", lengths=lengths, form="fused")
+    assert torch.count_nonzero(phi[1]).item() == 0
+    _check(layers, inputs, phi, 109, "bf16", [0, 2, 3, 4], lengths=lengths, tol=1e-5)
+    _, phi_s = _run(layers, inputs, "bf16", 109, "factored", lengths=lengths, form="split")
+    assert rel_fro(host64(phi_s), host64(phi)) < 1e-6
+
+
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
 @pytest.mark.parametrize("route,form", [("factored", "fused"), ("factored", "split"), ("materialized", None)])
 def test_rademacher_maps(dtype, route, form):

@@ -390,10 +390,13 @@ dattri_status dattri_layer_costs(const dattri_ctx* ctx, int32_t layer, int32_t T
                                  int64_t* factored_flops, int64_t* materialized_flops,
                                  int64_t* factored_bytes, int64_t* materialized_bytes);
 
-/* Route the cost model picks for a layer given its current capture (n, T),
- * with both predicted times in microseconds (ties go to FACTORED).  Each
- * layer is decided on its own, as if it were projected alone (in a call over
- * many layers the factored layers share their launches).  A layer whose k
+/* Route an AUTO call over the context's captured layers takes for a layer,
+ * with both predicted times of the layer alone in microseconds.  Each layer
+ * is first decided on its own (ties go to FACTORED).  Then, when some layer of
+ * the call is factored, the factored launches are paid and shared anyway, so a
+ * layer decided MATERIALIZED joins the factored route if its predicted
+ * factored time without launch costs is no more than its materialized time
+ * (each materialized layer adds launches of its own).  A layer whose k
  * exceeds the factored kernel's limits (k_in > 128 or k_out > 64) always
  * routes MATERIALIZED (its predicted factored time is infinite).
  * Errors: INVALID_ARG (bad layer), STATE (layer not captured). */

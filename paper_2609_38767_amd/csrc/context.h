@@ -69,4 +69,5 @@ struct dattri_ctx {
   // projection plans of recent calls with the context state each was built
   // from (captures, maps, route, form, cost model): an equal state reuses it
   mutable std::vector<std::pair<std::vector<uint64_t>, std::shared_ptr<const dattri::Plan>>> plans;
+  mutable std::pair<std::vector<uint64_t>, std::vector<dattri_route>> route_cache;  // call_routes(AUTO)
 };

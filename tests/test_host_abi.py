@@ -358,6 +358,38 @@ def test_route_follows_cost_model(ctx):
     assert dt.dattri_layer_route(ctx, 0)[0] == dt.DATTRI_ROUTE_FACTORED
 
 
+def test_call_routes_share_factored_launches():
+    # App. A.4 "Routing" per layer, with the launches of a call shared: a
+    # narrow layer that is faster materialized when projected alone joins the
+    # factored route in a call that factors another layer anyway, as long as
+    # its factored work without launches is no slower; its own predictions do
+    # not change
+    fake = 1 << 40
+    alone = dt.dattri_create(dt.DATTRI_BF16, 0)
+    pair = dt.dattri_create(dt.DATTRI_BF16, 0)
+    try:
+        dt.dattri_register_layer(alone, 128, 128, 64, 64)
+        dt.dattri_capture_layer(alone, 0, fake, fake + (1 << 36), 8, 2048)
+        for d_in, d_out in ((128, 128), (4096, 14336)):
+            dt.dattri_register_layer(pair, d_in, d_out, 32 if d_in > 128 else 64, 32 if d_in > 128 else 64)
+        dt.dattri_capture_layer(pair, 0, fake, fake + (1 << 36), 8, 2048)
+        dt.dattri_capture_layer(pair, 1, fake + (2 << 36), fake + (3 << 36), 8, 2048)
+        r0, pf0, pm0 = dt.dattri_layer_route(alone, 0)
+        assert r0 == dt.DATTRI_ROUTE_MATERIALIZED and pf0 > pm0
+        r1, pf1, pm1 = dt.dattri_layer_route(pair, 1)
+        assert r1 == dt.DATTRI_ROUTE_FACTORED and pf1 < pm1
+        r, pf, pm = dt.dattri_layer_route(pair, 0)
+        assert (pf, pm) == (pf0, pm0)
+        assert r == dt.DATTRI_ROUTE_FACTORED
+        # with the factored route made slow, the narrow layer stays materialized
+        m = dt.dattri_get_cost_model(pair)
+        dt.dattri_set_cost_model(pair, dict(m, factored_gbs=m["factored_gbs"] / 100))
+        assert dt.dattri_layer_route(pair, 0)[0] == dt.DATTRI_ROUTE_MATERIALIZED
+    finally:
+        dt.dattri_destroy(alone)
+        dt.dattri_destroy(pair)
+
+
 def test_factored_form_option(ctx):
     assert dt.dattri_get_factored_form(ctx) == dt.DATTRI_FORM_AUTO
     for f in (dt.DATTRI_FORM_FUSED, dt.DATTRI_FORM_SPLIT, dt.DATTRI_FORM_AUTO):

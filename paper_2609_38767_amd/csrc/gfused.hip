@@ -66,9 +66,11 @@ __device__ inline void split_terms(const f32x16& c, int hx, i32x4 (&term)[3]) {
     const uint32_t urx = __builtin_bit_cast(uint32_t, rx), ury = __builtin_bit_cast(uint32_t, ry);
     const uint32_t lx = __builtin_bit_cast(uint32_t, rx - __builtin_bit_cast(float, urx & 0xFFFF0000u));
     const uint32_t ly = __builtin_bit_cast(uint32_t, ry - __builtin_bit_cast(float, ury & 0xFFFF0000u));
-    term[0][p] = (int)((ux >> 16) | (uy & 0xFFFF0000u));
-    term[1][p] = (int)((urx >> 16) | (ury & 0xFFFF0000u));
-    term[2][p] = (int)((lx >> 16) | (ly & 0xFFFF0000u));
+    // high halves of two words into one (v_perm_b32: bytes 2, 3 of the second
+    // source, then bytes 2, 3 of the first)
+    term[0][p] = (int)__builtin_amdgcn_perm(uy, ux, 0x07060302u);
+    term[1][p] = (int)__builtin_amdgcn_perm(ury, urx, 0x07060302u);
+    term[2][p] = (int)__builtin_amdgcn_perm(ly, lx, 0x07060302u);
   }
 }
 

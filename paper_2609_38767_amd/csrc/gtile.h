@@ -19,6 +19,8 @@
 // the next stage prefetched into registers.  Rows past `rows` and features
 // past d read zero (buffer range checks).
 #pragma once
+#include <type_traits>
+
 #include "device_common.h"
 #include "internal.h"
 
@@ -26,7 +28,6 @@ namespace dattri {
 namespace dev {
 
 typedef short i16x4 __attribute__((ext_vector_type(4)));
-#define DATTRI_LDS16(p) ((__attribute__((address_space(3))) ::dattri::dev::i16x4*)(p))
 
 constexpr int kTrTokens = 32;  // tokens per stage
 
@@ -92,73 +93,104 @@ template <int WM, int WN>
 __device__ inline void g_tile_from(const GRows& r, int rows, int u0, int v0, int next_u0, int next_v0,
                                    uint8_t* lds, GStage<WM, WN>& st, f32x16 (&acc)[WM][WN]) {
   using C = GTile<WM, WN>;
-  uint8_t* Bs[2] = {lds, lds + kTrTokens * C::PB};
-  uint8_t* As[2] = {lds + 2 * kTrTokens * C::PB, lds + 2 * kTrTokens * C::PB + kTrTokens * C::PA};
+  typedef __attribute__((address_space(3))) uint8_t lds_u8;
+  typedef __attribute__((address_space(3))) i32x4 lds_i32x4;
+  // LDS addresses as 32-bit offsets from one local-address-space base: a
+  // generic pointer per access would cost a null check and 64-bit arithmetic
+  lds_u8* const base = (lds_u8*)lds;
+  constexpr uint32_t kB0 = 0, kB1 = kTrTokens * C::PB;
+  constexpr uint32_t kA0 = 2 * kTrTokens * C::PB, kA1 = kA0 + kTrTokens * C::PA;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wu = wave >> 1, wv = wave & 1;
 
+  // this thread's fixed offsets within a stage buffer: the 16-byte chunks it
+  // stores, and the rows and features its transposed reads start at (lane
+  // 16q + 4r + a reads row 8(q/2) + r of a 16-token step at features
+  // m + 16(q%2) + 4a, and the same 4 rows further for the second half)
+  uint32_t wb[C::CB], wa[C::CA];
 #pragma unroll
-  for (int i = 0; i < WM; ++i)
+  for (int i = 0; i < C::CB; ++i) {
+    const int c = tid + 256 * i;
+    wb[i] = (uint32_t)((c / (C::TM / 8)) * C::PB + (c % (C::TM / 8)) * 16);
+  }
 #pragma unroll
-    for (int j = 0; j < WN; ++j)
-#pragma unroll
-      for (int v = 0; v < 16; ++v) acc[i][j][v] = 0.f;
+  for (int i = 0; i < C::CA; ++i) {
+    const int c = tid + 256 * i;
+    wa[i] = (uint32_t)((c / (C::TN / 8)) * C::PA + (c % (C::TN / 8)) * 16);
+  }
+  const int q = lane >> 4, rr = (lane >> 2) & 3, aa = lane & 3;
+  const uint32_t rb_lane = (uint32_t)((8 * (q >> 1) + rr) * C::PB + (wu * 32 * WM + 16 * (q & 1) + 4 * aa) * 2);
+  const uint32_t ra_lane = (uint32_t)((8 * (q >> 1) + rr) * C::PA + (wv * 32 * WN + 16 * (q & 1) + 4 * aa) * 2);
 
   auto swrite = [&](int sb) {
+    const uint32_t ob = sb ? kB1 : kB0, oa = sb ? kA1 : kA0;
 #pragma unroll
-    for (int i = 0; i < C::CB; ++i) {
-      const int c = tid + 256 * i, row = c / (C::TM / 8), fc = c % (C::TM / 8);
-      *(i32x4*)(Bs[sb] + row * C::PB + fc * 16) = st.b[i];
-    }
+    for (int i = 0; i < C::CB; ++i) *(lds_i32x4*)(base + ob + wb[i]) = st.b[i];
 #pragma unroll
-    for (int i = 0; i < C::CA; ++i) {
-      const int c = tid + 256 * i, row = c / (C::TN / 8), fc = c % (C::TN / 8);
-      *(i32x4*)(As[sb] + row * C::PA + fc * 16) = st.a[i];
-    }
+    for (int i = 0; i < C::CA; ++i) *(lds_i32x4*)(base + oa + wa[i]) = st.a[i];
   };
-  // transposed operand of K step ks (16 tokens) for the 32 features starting
-  // at local column m: lane 16q + 4r + a reads row 16ks + 8(q/2) + 4h + r at
-  // features m + 16(q%2) + 4a, h = 0, 1
-  const int q = lane >> 4, rr = (lane >> 2) & 3, aa = lane & 3;
-  auto frag = [&](const uint8_t* base, int pitch, int m, int ks) {
-    const int row = ks * 16 + 8 * (q >> 1) + rr;
-    const uint8_t* p = base + row * pitch + (m + 16 * (q & 1) + 4 * aa) * 2;
-    const i16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16(DATTRI_LDS16(p));
-    const i16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16(DATTRI_LDS16(p + 4 * pitch));
+  // transposed operand of K step ks (16 tokens), 32-feature block i
+  auto frag = [&](uint32_t off, int pitch) {
+    const i16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) i16x4*)(base + off));
+    const i16x4 hi =
+        __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) i16x4*)(base + off + 4 * pitch));
     const i32x4 w = {__builtin_bit_cast(int, __builtin_shufflevector(lo, lo, 0, 1)),
                      __builtin_bit_cast(int, __builtin_shufflevector(lo, lo, 2, 3)),
                      __builtin_bit_cast(int, __builtin_shufflevector(hi, hi, 0, 1)),
                      __builtin_bit_cast(int, __builtin_shufflevector(hi, hi, 2, 3))};
     return w;
   };
+  // one K step of the stage in buffer sb; the first step of a tile starts
+  // its accumulators from a zero operand instead of zeroed registers
+  auto step = [&](int sb, int ks, auto first) {
+    i32x4 fa[WM], fb[WN];
+    const uint32_t ob = (sb ? kB1 : kB0) + rb_lane + (uint32_t)(ks * 16 * C::PB);
+    const uint32_t oa = (sb ? kA1 : kA0) + ra_lane + (uint32_t)(ks * 16 * C::PA);
+#pragma unroll
+    for (int i = 0; i < WM; ++i) fa[i] = frag(ob + i * 64, C::PB);
+#pragma unroll
+    for (int j = 0; j < WN; ++j) fb[j] = frag(oa + j * 64, C::PA);
+    const f32x16 zero = {};
+#pragma unroll
+    for (int i = 0; i < WM; ++i)
+#pragma unroll
+      for (int j = 0; j < WN; ++j)
+        acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, fa[i]),
+                                                           __builtin_bit_cast(bf16x8, fb[j]),
+                                                           decltype(first)::value ? zero : acc[i][j], 0, 0, 0);
+  };
+  using first_t = std::integral_constant<bool, true>;
+  using next_t = std::integral_constant<bool, false>;
 
   const int nst = (rows + kTrTokens - 1) / kTrTokens;
   if (nst > 0) swrite(0);
   __syncthreads();
+  if (nst == 0) {  // uniform: no token rows, G is zero
+#pragma unroll
+    for (int i = 0; i < WM; ++i)
+#pragma unroll
+      for (int j = 0; j < WN; ++j)
+#pragma unroll
+        for (int v = 0; v < 16; ++v) acc[i][j][v] = 0.f;
+    if (next_u0 >= 0) g_load(r, 0, next_u0, next_v0, st);
+    return;
+  }
   for (int kk = 0; kk < nst; ++kk) {
     const int sb = kk & 1;
-    if (kk + 1 < nst)
-      g_load(r, (kk + 1) * kTrTokens, u0, v0, st);
-    else if (next_u0 >= 0)
-      g_load(r, 0, next_u0, next_v0, st);
+    // one call site for both prefetches (the next stage, or the first stage of
+    // the next tile), so the stage registers are loaded in place
+    const bool more = kk + 1 < nst;
+    if (more || next_u0 >= 0)
+      g_load(r, more ? (kk + 1) * kTrTokens : 0, more ? u0 : next_u0, more ? v0 : next_v0, st);
+    if (kk == 0)
+      step(sb, 0, first_t{});
+    else
+      step(sb, 0, next_t{});
 #pragma unroll
-    for (int ks = 0; ks < kTrTokens / 16; ++ks) {
-      i32x4 fa[WM], fb[WN];
-#pragma unroll
-      for (int i = 0; i < WM; ++i) fa[i] = frag(Bs[sb], C::PB, wu * 32 * WM + i * 32, ks);
-#pragma unroll
-      for (int j = 0; j < WN; ++j) fb[j] = frag(As[sb], C::PA, wv * 32 * WN + j * 32, ks);
-#pragma unroll
-      for (int i = 0; i < WM; ++i)
-#pragma unroll
-        for (int j = 0; j < WN; ++j)
-          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, fa[i]),
-                                                             __builtin_bit_cast(bf16x8, fb[j]), acc[i][j], 0, 0, 0);
-    }
+    for (int ks = 1; ks < kTrTokens / 16; ++ks) step(sb, ks, next_t{});
     if (kk + 1 < nst) swrite(sb ^ 1);
     __syncthreads();
   }
-  if (nst == 0 && next_u0 >= 0) g_load(r, 0, next_u0, next_v0, st);
 }
 
 // The same for a single tile: loads its first stage, then runs it.

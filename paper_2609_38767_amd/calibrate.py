@@ -164,9 +164,10 @@ class LibraryPredictor:
         self.ctx = []
 
 
-# Fitted fields: gproject_gbs only enters the staged G route (float32 or
-# unaligned blocks), which the bf16 sweep does not run, so it keeps its value.
-FIT_FIELDS = [k for k in FIELDS if k != "gproject_gbs"]
+# Fitted fields: gproject_tflops and gproject_gbs only enter the staged G
+# route (float32 or unaligned blocks, k_in > 128), which the bf16 sweep does
+# not run, so they keep their values.
+FIT_FIELDS = [k for k in FIELDS if k not in ("gproject_tflops", "gproject_gbs")]
 
 
 def _model_of(x, base):

@@ -53,19 +53,19 @@ dattri_cost_model default_cost_model() {
   // single-layer shapes: transformer, adapter-shaped and narrow layers,
   // T = 16..4096, both forced routes timed with launch plans kept on the
   // device), every rate held below its bound: AUTO picks the faster route on
-  // all 28 shapes, root-mean-square log error of the predictions 0.16.
+  // all 28 shapes, root-mean-square log error of the predictions 0.15.
   // gproject_gbs and gproject_tflops serve only the staged-G route, which
   // that sweep does not run.
   dattri_cost_model m;
-  m.factored_tflops = 176.9;
-  m.factored_gbs = 5714.2;
-  m.gradient_tflops = 657.1;
+  m.factored_tflops = 175.9;
+  m.factored_gbs = 6450.0;
+  m.gradient_tflops = 837.2;
   m.gradient_gbs = 6450.0;
   m.gproject_tflops = 157.3;
   m.gproject_gbs = 5000.0;
   m.launch_us = 10.74;
   m.call_us = 0.0;
-  m.round_us = 0.449;
+  m.round_us = 0.674;
   return m;
 }
 

@@ -124,6 +124,34 @@ def cpu_baseline_projection(wl, inputs, seed, passes=3):
                       f"float64, {passes} passes ({t_total:.1f} s of oracle time)"}
 
 
+def vendor_gemm_reference(Qd, Xd, S, timed, steps, warmup, flops):
+    """Context for the score GEMM: the vendor BLAS (hipBLASLt through
+    torch.mm) on the same dense operands, float32 output into the same score
+    buffer, and bf16 output.  It applies no preconditioner (the library's call
+    includes the query scaling) and is not part of the product path."""
+    import torch
+    res = {"what": "torch.mm (hipBLASLt) on the dense rows, no preconditioner"}
+    Xt = Xd.t()
+    try:
+        fn = lambda: torch.mm(Qd, Xt, out_dtype=torch.float32, out=S)
+        for _ in range(warmup):
+            fn()
+        _, ms = timed(fn, steps)
+        res["f32_out_ms"] = sum(ms) / len(ms)
+        res["f32_out_tflops"] = flops / (res["f32_out_ms"] * 1e-3) / 1e12
+    except Exception as e:  # out_dtype needs a recent torch
+        res["f32_out_error"] = repr(e)[:120]
+    out16 = torch.empty(S.shape, dtype=torch.bfloat16, device=S.device)
+    fn = lambda: torch.mm(Qd, Xt, out=out16)
+    for _ in range(warmup):
+        fn()
+    _, ms = timed(fn, steps)
+    res["bf16_out_ms"] = sum(ms) / len(ms)
+    res["bf16_out_tflops"] = flops / (res["bf16_out_ms"] * 1e-3) / 1e12
+    del out16
+    return res
+
+
 def cpu_baseline_score(Qd, Xd, d, topk, n_queries=64, chunk=25000):
     """Time the oracle's scoring (float64 GEMM with the diagonal, then the
     stable per-query top-k) on the first `n_queries` query rows against all
@@ -804,6 +832,7 @@ def main():
                         "row_stride_elements": ld,
                         "dense_rows_gemm_ms": sum(ms_dense) / len(ms_dense),
                         "dense_rows_gemm_tflops": flops / (sum(ms_dense) / len(ms_dense) * 1e-3) / 1e12}
+        out["score"]["vendor_reference"] = vendor_gemm_reference(Qd, Xd, S, timed, args.steps, args.warmup, flops)
         out["roofline_score"] = {"bound": "mfma", "achieved": flops / (g_ms * 1e-3) / 1e12,
                                  "peak": 2500.0, "unit": "TFLOP/s",
                                  "frac": flops / (g_ms * 1e-3) / 1e12 / 2500.0,

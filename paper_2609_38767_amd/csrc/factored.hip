@@ -218,6 +218,13 @@ void factored_instance(int elt, int na_req, int nb_req, int aligned, int* na_ins
     const int nb_list[] = {1, 2, 4};
     for (int v : na_list) if (v >= na_req) { na = v; break; }
     for (int v : nb_list) if (v >= nb_req) { nb = v; break; }
+    // bf16: round 1-tile maps up to the direct-load instances (the unused
+    // tile's fragments read as zero), which stream the factor rows faster
+    const int na2 = na == 1 ? 2 : na, nb2 = nb == 1 ? 2 : nb;
+    if (dma_instance(elt, true, na2, nb2)) {
+      na = na2;
+      nb = nb2;
+    }
   }
   *na_inst = na;
   *nb_inst = nb;

@@ -429,9 +429,21 @@ dattri_status dattri_layer_route(const dattri_ctx* ctx, int32_t layer, dattri_ro
  *                 tiles of the token Gram (token rows padded to multiples of
  *                 16): tile_flops = tiles * 2 * 128^2 (d_in + d_out + 1),
  *                 tile_bytes = tiles * 2 * 128 (d_in + d_out) elt;
- *   materialized  max(build_flops / build rate, build_bytes / build bandwidth)
- *                 + dot_bytes / dot bandwidth + 4 launch_us,
- * with build and product counts as in dattri_cross_gram_costs. */
+ *   materialized  the faster of two forms of Eq. 1 + Frobenius products:
+ *                 staged: max(build_flops / build rate, build_bytes / build
+ *                 bandwidth) + dot_bytes / dot bandwidth + 4 launch_us (DW of
+ *                 both batches written to the workspace, then the products);
+ *                 one-pass (bf16 blocks with 16-byte aligned rows only): no DW
+ *                 in memory, a workgroup forms one 128 x 128 tile of DW_b[j]
+ *                 and then the same tile of DW_a[i] for each of a run of ipw
+ *                 examples, summing their products; predicted as rounds of 512
+ *                 workgroups, each round ipw + 1 tile builds of
+ *                 2 * 128^2 * T (T rounded up to 32) FLOP at onepass_tflops / 512,
+ *                 plus 2 launch_us,
+ * with build and product counts as in dattri_cross_gram_costs.  For the squared
+ * norms the factorized tiles cover each example's own token Gram, the staged
+ * products read DW once (3 launches), and the one-pass form has no reference
+ * build. */
 typedef struct {
   double ghost_tflops;   /* factorized kernel (two token Grams and their product) */
   double ghost_gbs;      /* its factor-block reads */
@@ -439,7 +451,8 @@ typedef struct {
   double build_tflops;   /* DW = B^T A kernel */
   double build_gbs;      /* its factor reads plus float32 DW writes */
   double dot_gbs;        /* Frobenius products over stored float32 DW */
-  double launch_us;      /* per kernel launch (the materialized route launches four per layer) */
+  double launch_us;      /* per kernel launch (staged materialized: four per layer) */
+  double onepass_tflops; /* one-pass materialized kernel, on the tile builds it issues */
 } dattri_crossgram_cost_model;
 
 dattri_status dattri_set_crossgram_cost_model(dattri_ctx* ctx, const dattri_crossgram_cost_model* m);

@@ -70,7 +70,7 @@ class CostModel(ctypes.Structure):
 class CrossgramCostModel(ctypes.Structure):
     _fields_ = [("ghost_tflops", ctypes.c_double), ("ghost_gbs", ctypes.c_double),
                 ("ghost_layer_us", ctypes.c_double), ("build_tflops", ctypes.c_double), ("build_gbs", ctypes.c_double),
-                ("dot_gbs", ctypes.c_double), ("launch_us", ctypes.c_double)]
+                ("dot_gbs", ctypes.c_double), ("launch_us", ctypes.c_double), ("onepass_tflops", ctypes.c_double)]
 
 
 class CurvatureLayout(ctypes.Structure):

@@ -33,6 +33,7 @@ dattri_crossgram_cost_model default_crossgram_cost_model() {
   m.build_gbs = 95600.0;
   m.dot_gbs = 1870.0;
   m.launch_us = 15.1;
+  m.onepass_tflops = 725.0;  // issued tile builds of the one-pass kernel
   return m;
 }
 
@@ -44,6 +45,8 @@ constexpr int64_t kGhostPartsBudget = (int64_t)256 << 20;  // block sums per fac
 constexpr int64_t kGhostTilesMax = (int64_t)1 << 22;      // tiles per factorized group
 constexpr int64_t kXgGBudget = (int64_t)2 << 30;          // staged float32 DW per chunk
 constexpr int64_t kDotChunk = 16384;                      // floats per Frobenius-product chunk
+constexpr int64_t kXOnePartsBudget = (int64_t)64 << 20;     // one-pass tile sums per launch (bytes)
+constexpr int64_t kXOneSlots = 2 * 256;                    // resident one-pass workgroups (2 per CU)
 
 inline int64_t r16(int64_t T) { return (T + 15) / 16 * 16; }
 inline int64_t cdiv(int64_t a, int64_t b) { return (a + b - 1) / b; }
@@ -64,14 +67,57 @@ XCounts xcounts(int64_t na, int64_t nb, int64_t Ta, int64_t Tb, int64_t di, int6
   return c;
 }
 
+// One-pass materialized launch over ci examples of batch a against cj of
+// batch b (diag: the ci examples against themselves): a workgroup forms one
+// 128 x 128 tile of DW_b[j] once, then the same tile of DW_a[i] for each of
+// its ipw examples.  nz = runs of batch a per (tile, j) is chosen to minimise
+// the predicted time: rounds of kXOneSlots workgroups, each round as long as
+// one workgroup's builds (ipw, plus the reference build unless diag).
+struct XOneShape {
+  int nz = 1, ipw = 1;
+  double us = 0.0;
+};
+
+inline int64_t r32(int64_t T) { return (T + 31) / 32 * 32; }
+
+XOneShape xone_shape(const dattri_crossgram_cost_model& m, int64_t tiles, int64_t ci, int64_t cj, int64_t Ta,
+                     int64_t Tb, bool diag) {
+  XOneShape best;
+  best.us = INFINITY;
+  if (tiles <= 0 || ci <= 0) {
+    best.us = 0.0;
+    return best;
+  }
+  const double per_token = 2.0 * kXOneTile * kXOneTile / (m.onepass_tflops * 1e6 / kXOneSlots);
+  const double ta = per_token * (double)r32(Ta), tb = diag ? 0.0 : per_token * (double)r32(Tb);
+  const int64_t ys = diag ? 1 : cj;
+  const int64_t nz_max = std::min<int64_t>(ci, 65535);
+  for (int64_t nz = 1; nz <= nz_max; ++nz) {
+    const int64_t ipw = cdiv(ci, nz);
+    if (cdiv(ci, ipw) != nz) continue;  // same runs as a smaller nz
+    const int64_t rounds = cdiv(tiles * ys * nz, kXOneSlots);
+    const double us = (double)rounds * ((double)ipw * ta + tb);
+    if (us < best.us) best = XOneShape{(int)nz, (int)ipw, us};
+  }
+  return best;
+}
+
+// Whether a layer can take the one-pass materialized kernel: bf16 blocks with
+// 16-byte aligned rows, and one example's block within a 32-bit byte range.
+bool xone_ok(const Layer& La, const Layer& Lb, int elt);
+
 // Predicted microseconds of one layer's two routes, as this build runs them:
 // the factorized kernel computes whole 128 x 128 tiles of the padded token
-// Gram and reads 128 rows of each side per tile; the materialized route
-// builds DW for both batches, then takes the products (four launches).
+// Gram and reads 128 rows of each side per tile (diag: each example's own
+// Gram); the materialized route is the faster of its two forms: DW staged in
+// HBM (build both batches, then the products: four launches) and, where
+// `one` allows it, the one-pass kernel (xone_shape, plus the tile-sum launch).
 void xpredict(const dattri_crossgram_cost_model& m, int64_t na, int64_t nb, int64_t Ta, int64_t Tb,
-              int64_t di, int64_t dq, int elt, double* f_us, double* m_us) {
-  const XCounts c = xcounts(na, nb, Ta, Tb, di, dq, elt);
-  const int64_t tiles = cdiv(na * r16(Ta), kGhostTile) * cdiv(nb * r16(Tb), kGhostTile);
+              int64_t di, int64_t dq, int elt, bool diag, bool one, double* f_us, double* m_us) {
+  if (diag) nb = na;
+  const XCounts c = diag ? xcounts(na, 0, Ta, 0, di, dq, elt) : xcounts(na, nb, Ta, Tb, di, dq, elt);
+  const int64_t tiles = diag ? na * cdiv(r16(Ta), kGhostTile) * cdiv(r16(Ta), kGhostTile)
+                             : cdiv(na * r16(Ta), kGhostTile) * cdiv(nb * r16(Tb), kGhostTile);
   const double tflops = (double)tiles * 2.0 * kGhostTile * kGhostTile * (double)(di + dq + 1);
   const double tbytes = (double)tiles * 2.0 * kGhostTile * (double)(di + dq) * elt;
   *f_us = (tiles == 0) ? 0.0
@@ -79,7 +125,13 @@ void xpredict(const dattri_crossgram_cost_model& m, int64_t na, int64_t nb, int6
                              m.ghost_layer_us;
   const double build = std::max((double)c.build_flops / (m.build_tflops * 1e6),
                                 (double)c.build_bytes / (m.build_gbs * 1e3));
-  *m_us = build + (double)c.dot_bytes / (m.dot_gbs * 1e3) + 4.0 * m.launch_us;
+  const double dot_bytes = diag ? 4.0 * na * di * dq : (double)c.dot_bytes;
+  *m_us = build + dot_bytes / (m.dot_gbs * 1e3) + (diag ? 3.0 : 4.0) * m.launch_us;
+  if (one) {
+    const int64_t dtiles = cdiv(dq, kXOneTile) * cdiv(di, kXOneTile);
+    const double o = xone_shape(m, dtiles, na, nb, Ta, Tb, diag).us + 2.0 * m.launch_us;
+    *m_us = std::min(*m_us, o);
+  }
 }
 
 dattri_status check_pair(const dattri_ctx* a, const dattri_ctx* b) {
@@ -105,10 +157,30 @@ bool layer_aligned(const Layer& L, int elt) {
          (L.d_out * elt) % 16 == 0;
 }
 
+bool xone_ok(const Layer& La, const Layer& Lb, int elt) {
+  const int64_t lim = (int64_t)1 << 32;
+  return elt == 2 && layer_aligned(La, elt) && layer_aligned(Lb, elt) &&
+         (int64_t)La.T * std::max(La.d_in, La.d_out) * elt < lim &&
+         (int64_t)Lb.T * std::max(Lb.d_in, Lb.d_out) * elt < lim;
+}
+
+// The one-pass form is taken when it is allowed and predicted faster than
+// staging DW.
+bool xone_pick(const dattri_crossgram_cost_model& m, const Layer& La, const Layer& Lb, int elt, bool diag) {
+  if (!xone_ok(La, Lb, elt)) return false;
+  double f, staged, best;
+  xpredict(m, La.n, Lb.n, La.T, Lb.T, La.d_in, La.d_out, elt, diag, false, &f, &staged);
+  xpredict(m, La.n, Lb.n, La.T, Lb.T, La.d_in, La.d_out, elt, diag, true, &f, &best);
+  return best < staged;
+}
+
 struct XGroup { int e0, e1, t0, t1; int64_t parts_floats; };
 
 struct XPlan {
   std::vector<int> fact, mat;  // layer ids by route
+  std::vector<char> one;       // per entry of mat: the one-pass form
+  int oa = 0, ob = 0;          // examples per one-pass launch (batch a, batch b)
+  int64_t oparts = 0;          // floats of one-pass tile sums
   std::vector<GhostEntry> entries;
   std::vector<GhostTile> tiles;
   std::vector<XGroup> groups;
@@ -116,7 +188,8 @@ struct XPlan {
   int64_t D_max = 0, nchunks_max = 0;
   int ca = 0, cb = 0;          // examples of DW staged per chunk (batch a, batch b)
   bool reuse_g = false;        // a == b and both fit: DW built once
-  size_t off_entries = 0, off_tiles = 0, off_parts = 0, off_g1 = 0, off_g2 = 0, off_dparts = 0, total = 0;
+  size_t off_entries = 0, off_tiles = 0, off_parts = 0, off_g1 = 0, off_g2 = 0, off_dparts = 0, off_oparts = 0;
+  size_t total = 0;
   size_t blob_entries = 0, blob_bytes = 0;
 };
 
@@ -144,11 +217,11 @@ void add_entry(XPlan& P, GhostEntry E, int64_t n_rt, int64_t n_ct) {
   P.max_parts = std::max(P.max_parts, G.parts_floats);
 }
 
-dattri_route layer_route(const dattri_ctx* a, const dattri_ctx* b, int l, dattri_route forced) {
+dattri_route layer_route(const dattri_ctx* a, const dattri_ctx* b, int l, dattri_route forced, bool diag) {
   if (forced != DATTRI_ROUTE_AUTO) return forced;
   const Layer &La = a->layers[l], &Lb = b->layers[l];
   double f, m;
-  xpredict(a->xcost, La.n, Lb.n, La.T, Lb.T, La.d_in, La.d_out, a->elt, &f, &m);
+  xpredict(a->xcost, La.n, Lb.n, La.T, Lb.T, La.d_in, La.d_out, a->elt, diag, xone_ok(La, Lb, a->elt), &f, &m);
   return f <= m ? DATTRI_ROUTE_FACTORED : DATTRI_ROUTE_MATERIALIZED;
 }
 
@@ -160,7 +233,7 @@ dattri_status build_xplan(const dattri_ctx* a, const dattri_ctx* b, dattri_route
   const int elt = a->elt;
   const int na = a->layers[0].n, nb = b->layers[0].n;
   for (int l = 0; l < (int)a->layers.size(); ++l)
-    (layer_route(a, b, l, route) == DATTRI_ROUTE_FACTORED ? P.fact : P.mat).push_back(l);
+    (layer_route(a, b, l, route, diag) == DATTRI_ROUTE_FACTORED ? P.fact : P.mat).push_back(l);
 
   for (int l : P.fact) {
     const Layer &La = a->layers[l], &Lb = b->layers[l];
@@ -199,8 +272,24 @@ dattri_status build_xplan(const dattri_ctx* a, const dattri_ctx* b, dattri_route
     }
   }
 
-  for (int l : P.mat) P.D_max = std::max<int64_t>(P.D_max, (int64_t)a->layers[l].d_in * a->layers[l].d_out);
-  if (!P.mat.empty() && P.D_max > 0) {
+  // materialized layers: one-pass where picked, else DW staged in HBM
+  int64_t otiles_max = 0;
+  for (int l : P.mat) {
+    const Layer &La = a->layers[l], &Lb = b->layers[l];
+    const bool one = xone_pick(a->xcost, La, Lb, elt, diag);
+    P.one.push_back(one ? 1 : 0);
+    if (one)
+      otiles_max = std::max<int64_t>(otiles_max, cdiv(La.d_out, kXOneTile) * cdiv(La.d_in, kXOneTile));
+    else
+      P.D_max = std::max<int64_t>(P.D_max, (int64_t)La.d_in * La.d_out);
+  }
+  if (otiles_max > 0) {
+    const int64_t cap = std::max<int64_t>(1, kXOnePartsBudget / 4 / otiles_max);  // (i, j) cells per launch
+    P.ob = diag ? 0 : (int)std::min<int64_t>({(int64_t)nb, 65535, cap});
+    P.oa = (int)std::max<int64_t>(1, std::min<int64_t>(na, cap / std::max(1, P.ob)));
+    P.oparts = otiles_max * P.oa * std::max(1, P.ob);
+  }
+  if (P.D_max > 0) {
     const int64_t per = P.D_max * 4;
     if (diag) {
       P.ca = (int)std::max<int64_t>(1, std::min<int64_t>(na, kXgGBudget / per));
@@ -233,6 +322,8 @@ dattri_status build_xplan(const dattri_ctx* a, const dattri_ctx* b, dattri_route
   P.off_dparts = off;
   const int64_t dp = diag ? (int64_t)P.nchunks_max * P.ca : (int64_t)P.nchunks_max * P.ca * P.cb;
   off = align_up(off + (size_t)dp * 4);
+  P.off_oparts = off;
+  off = align_up(off + (size_t)P.oparts * 4);
   P.total = std::max<size_t>(off, kAlign);
   return DATTRI_OK;
 }
@@ -279,13 +370,36 @@ dattri_status run_xplan(dattri_ctx* a, dattri_ctx* b, const XPlan& P, bool diag,
     }
   }
   if (!wrote) HIP_TRY(launch_fill_rows(K, diag ? 1 : rows, diag ? rows : cols, diag ? rows : ld, s));
-  if (P.mat.empty() || P.D_max == 0) return DATTRI_OK;
+  if (P.mat.empty()) return DATTRI_OK;
   float* g1 = (float*)(ws + P.off_g1);
   float* g2 = P.reuse_g ? g1 : (float*)(ws + P.off_g2);
   float* dparts = (float*)(ws + P.off_dparts);
-  for (int l : P.mat) {
-    const Layer &La = a->layers[l], &Lb = b->layers[l];
+  float* oparts = (float*)(ws + P.off_oparts);
+  for (size_t m = 0; m < P.mat.size(); ++m) {
+    const Layer &La = a->layers[P.mat[m]], &Lb = b->layers[P.mat[m]];
     const int64_t D = (int64_t)La.d_in * La.d_out;
+    if (D == 0) continue;
+    if (P.one[m]) {
+      XOneArgs x;
+      x.A1 = La.A; x.B1 = La.B; x.len1 = La.lengths;
+      x.A2 = Lb.A; x.B2 = Lb.B; x.len2 = Lb.lengths;
+      x.d_in = La.d_in; x.d_out = La.d_out; x.T1 = La.T; x.T2 = Lb.T;
+      x.diag = diag ? 1 : 0;
+      x.n_vt = (int)cdiv(La.d_in, kXOneTile);
+      x.parts = oparts;
+      const int64_t tiles = cdiv(La.d_out, kXOneTile) * x.n_vt;
+      for (int j0 = 0; j0 < (diag ? 1 : nb); j0 += std::max(1, P.ob)) {
+        const int cj = diag ? 0 : std::min(P.ob, nb - j0);
+        for (int i0 = 0; i0 < na; i0 += P.oa) {
+          const int ci = std::min(P.oa, na - i0);
+          const XOneShape sh = xone_shape(a->xcost, tiles, ci, cj, La.T, Lb.T, diag);
+          x.i0 = i0; x.ci = ci; x.ipw = sh.ipw; x.j0 = j0; x.cj = cj;
+          HIP_TRY(launch_xone(x, s));
+          HIP_TRY(launch_kacc(oparts, (int)tiles, ci, diag ? ci : cj, K, ld, i0, j0, diag ? 1 : 0, 1, s));
+        }
+      }
+      continue;
+    }
     const int nchunks = (int)cdiv(D, kDotChunk);
     if (diag) {
       for (int i0 = 0; i0 < na; i0 += P.ca) {
@@ -317,7 +431,7 @@ extern "C" {
 dattri_status dattri_set_crossgram_cost_model(dattri_ctx* ctx, const dattri_crossgram_cost_model* m) {
   reset_error();
   if (!ctx || !m) return fail(DATTRI_E_INVALID_ARG, "ctx or model is NULL");
-  const double v[] = {m->ghost_tflops, m->ghost_gbs, m->build_tflops, m->build_gbs, m->dot_gbs};
+  const double v[] = {m->ghost_tflops, m->ghost_gbs, m->build_tflops, m->build_gbs, m->dot_gbs, m->onepass_tflops};
   for (double x : v)
     if (!(x > 0) || !std::isfinite(x)) return fail(DATTRI_E_INVALID_ARG, "rates must be finite and > 0");
   if (!(m->launch_us >= 0) || !std::isfinite(m->launch_us) || !(m->ghost_layer_us >= 0) ||
@@ -360,7 +474,7 @@ dattri_status dattri_cross_gram_route(const dattri_ctx* a, const dattri_ctx* b, 
     return fail(DATTRI_E_INVALID_ARG, "layer %d out of range", layer);
   const Layer &La = a->layers[layer], &Lb = b->layers[layer];
   double f, m;
-  xpredict(a->xcost, La.n, Lb.n, La.T, Lb.T, La.d_in, La.d_out, a->elt, &f, &m);
+  xpredict(a->xcost, La.n, Lb.n, La.T, Lb.T, La.d_in, La.d_out, a->elt, false, xone_ok(La, Lb, a->elt), &f, &m);
   if (chosen) *chosen = f <= m ? DATTRI_ROUTE_FACTORED : DATTRI_ROUTE_MATERIALIZED;
   if (pred_factored_us) *pred_factored_us = f;
   if (pred_materialized_us) *pred_materialized_us = m;

@@ -214,6 +214,23 @@ hipError_t launch_ghost(int elt_bytes, const GhostEntry* entries, const GhostTil
 hipError_t launch_ghost_reduce(const GhostEntry* entries, int n_entries, const float* parts,
                                int n_rows, int n_cols, float* K, int64_t ld, int diag, int accumulate,
                                hipStream_t s);
+// One-pass materialized cross-Gram (bf16 blocks with 16-byte aligned rows):
+// grid (tiles of DW, examples j of batch b, runs of ipw examples of batch a);
+// parts[tile][i][j] (diag: parts[tile][i], the squared norms of batch a) =
+// sum over the 128 x 128 tile of DW_a[i0 + i] * DW_b[j0 + j].
+constexpr int kXOneTile = 128;
+struct XOneArgs {
+  const void *A1, *B1, *A2, *B2;  // batch a and b factor blocks [n, T, d]
+  const int32_t *len1, *len2;     // per-example lengths or NULL
+  int32_t d_in, d_out, T1, T2;
+  int32_t i0, ci, ipw;            // batch a examples i0 .. i0 + ci - 1, ipw per workgroup
+  int32_t j0, cj;                 // batch b examples j0 .. j0 + cj - 1 (unused for diag)
+  int32_t diag;
+  int32_t n_vt;                   // 128-column tiles of d_in
+  float* parts;
+};
+hipError_t launch_xone(const XOneArgs& a, hipStream_t s);
+
 // parts[c][i][j] (diag: parts[c][i]) = Frobenius product over chunk c of the
 // flattened gradients G1[i], G2[j] (D floats each); chunk a multiple of 64
 hipError_t launch_gdot(const float* G1, int n1, const float* G2, int n2, int64_t D, int64_t chunk,

@@ -19,6 +19,14 @@ pytestmark = pytest.mark.gpu
 DEV = "cuda"
 ROUTES = [dt.DATTRI_ROUTE_FACTORED, dt.DATTRI_ROUTE_MATERIALIZED, dt.DATTRI_ROUTE_AUTO]
 TDT = {"f32": torch.float32, "bf16": torch.bfloat16}
+# each form of the materialized route forced by making the other's rate
+# negligible in the first context's time model
+FORMS = {"staged": dict(onepass_tflops=1e-9), "one-pass": dict(dot_gbs=1e-9)}
+
+
+def _force(sess, form):
+    m = dt.dattri_get_crossgram_cost_model(sess.ctx)
+    dt.dattri_set_crossgram_cost_model(sess.ctx, dict(m, **FORMS[form]))
 
 
 def _batch(dims, n, T, dtype, seed, lengths=None):
@@ -109,18 +117,69 @@ def test_cross_gram_deterministic_and_strided_output():
         assert (buf[:, 3:] == 7.0).all()  # columns past n_b untouched
 
 
-def test_cross_gram_full_size_layer():
+@pytest.mark.parametrize("form", list(FORMS))
+def test_cross_gram_full_size_layer(form):
     """One Pythia-410M-shaped MLP layer (1024 -> 4096) at T = 2048, 8 training
-    examples against 1 query (the workload the routing benchmark sweeps), both
-    routes against the oracle's materialized definition."""
+    examples against 1 query (the workload the routing benchmark sweeps), the
+    factorized route and the given form of the materialized one against the
+    oracle's materialized definition."""
     dims = [(1024, 4096)]
     a_blocks, La = _batch(dims, 8, 2048, "bf16", 8)
     b_blocks, Lb = _batch(dims, 1, 2048, "bf16", 9)
     sa, sb = _session(dims, a_blocks, La, "bf16"), _session(dims, b_blocks, Lb, "bf16")
+    _force(sa, form)
     got = {r: cross_gram(sa, sb, r) for r in ROUTES[:2]}
+    nrm = sq_norms(sa, dt.DATTRI_ROUTE_MATERIALIZED)
     torch.cuda.synchronize()
-    ref = ocg.cross_gram(_oracle_batch(a_blocks, La), _oracle_batch(b_blocks, Lb), "materialized")
+    ob = _oracle_batch(a_blocks, La)
+    ref = ocg.cross_gram(ob, _oracle_batch(b_blocks, Lb), "materialized")
     for r, K in got.items():
         err = rel_fro(host64(K), ref)
-        print(f"full-size layer route {r}: rel err {err:.2e}")
+        print(f"full-size layer route {r} ({form}): rel err {err:.2e}")
         assert err <= 2e-5, (r, err)
+    assert rel_fro(host64(nrm), ocg.sq_norms(ob, "materialized")) <= 2e-5
+
+
+@pytest.mark.parametrize("form", list(FORMS))
+def test_materialized_forms_ragged(form):
+    # ragged token lengths (0, 1, one short of a 32-token stage, several
+    # stages) and feature dims that end inside a 128 x 128 tile of DW; the
+    # 130-wide layer has rows that are not 16-byte aligned, so it stages DW
+    # while the others take the one-pass form (a mixed call)
+    dims = [(64, 48), (40, 72), (130, 24), (256, 136)]
+    a_blocks, La = _batch(dims, 6, 97, "bf16", 10, lengths=[97, 0, 31, 1, 64, 70])
+    b_blocks, Lb = _batch(dims, 3, 45, "bf16", 11, lengths=[45, 33, 0])
+    sa, sb = _session(dims, a_blocks, La, "bf16"), _session(dims, b_blocks, Lb, "bf16")
+    _force(sa, form)
+    staged_bytes = (6 + 3) * 256 * 136 * 4
+    ws = dt.dattri_cross_gram_workspace_bytes(sa.ctx, sb.ctx, dt.DATTRI_ROUTE_MATERIALIZED)
+    assert (ws >= staged_bytes) == (form == "staged")
+    K = cross_gram(sa, sb, dt.DATTRI_ROUTE_MATERIALIZED)
+    G = cross_gram(sa, sa, dt.DATTRI_ROUTE_MATERIALIZED)
+    nrm = sq_norms(sa, dt.DATTRI_ROUTE_MATERIALIZED)
+    torch.cuda.synchronize()
+    oa, ob = _oracle_batch(a_blocks, La), _oracle_batch(b_blocks, Lb)
+    assert rel_fro(host64(K), ocg.cross_gram(oa, ob)) <= 1e-5
+    assert rel_fro(host64(G), ocg.cross_gram(oa, oa)) <= 1e-5
+    assert rel_fro(host64(nrm), ocg.sq_norms(oa)) <= 1e-5
+    assert not host64(K)[1].any() and not host64(K)[:, 2].any() and nrm[1].item() == 0.0
+
+
+def test_one_pass_runs_and_launch_chunks():
+    # many examples on both sides: several examples per workgroup, several
+    # runs per (tile, query); then 130 x 130 one-token examples of a
+    # 4096 x 4096 layer, whose 1024 tiles x 16900 pairs of tile sums exceed
+    # one launch's budget, so batch a is split over two launches
+    for dims, na, nb, T, seed in (([(512, 384)], 37, 9, 40, 12), ([(4096, 4096)], 130, 130, 1, 13)):
+        a_blocks, La = _batch(dims, na, T, "bf16", seed)
+        b_blocks, Lb = _batch(dims, nb, T, "bf16", seed + 100)
+        sa, sb = _session(dims, a_blocks, La, "bf16"), _session(dims, b_blocks, Lb, "bf16")
+        _force(sa, "one-pass")
+        K = cross_gram(sa, sb, dt.DATTRI_ROUTE_MATERIALIZED)
+        nrm = sq_norms(sa, dt.DATTRI_ROUTE_MATERIALIZED)
+        torch.cuda.synchronize()
+        oa, ob = _oracle_batch(a_blocks, La), _oracle_batch(b_blocks, Lb)
+        assert rel_fro(host64(K), ocg.cross_gram(oa, ob)) <= 2e-5, dims
+        assert rel_fro(host64(nrm), ocg.sq_norms(oa)) <= 2e-5, dims
+        sa.close()
+        sb.close()

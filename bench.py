@@ -36,6 +36,10 @@ def parse():
     p.add_argument("--phase", choices=["all", "project", "score", "routing", "gpt2", "crossgram", "curvature",
                                        "fit", "mask", "copy", "probe"],
                    default="all")
+    p.add_argument("--xg-T", type=int, nargs="*", default=None,
+                   help="sequence lengths of the cross-Gram sweep (default: the full sweep)")
+    p.add_argument("--xg-routes", nargs="*", default=None, choices=["factored", "materialized", "auto"],
+                   help="routes the cross-Gram sweep times (default: all three)")
     return p.parse_args()
 
 
@@ -348,7 +352,7 @@ def gpt2_case(dev, steps, warmup, check=True):
     return out
 
 
-def crossgram_case(dev, steps, warmup):
+def crossgram_case(dev, steps, warmup, T_list=None, route_names=None):
     """Unprojected cross-Gram routing sweep (the paper's routing ablation over
     sequence length): 96 Pythia-410M-shaped layers, 8 training examples
     against 1 query, T in {32, 128, 512, 2048}, bf16.  Per T: both forced
@@ -377,7 +381,7 @@ def crossgram_case(dev, steps, warmup):
         t = sorted(a.elapsed_time(b) for a, b in evs)
         return t[len(t) // 2]
 
-    for T in wl["T_sweep"]:
+    for T in (T_list or wl["T_sweep"]):
         sess = {}
         for side, n in (("train", wl["n_train"]), ("query", wl["n_query"])):
             s = ProjectionSession(layers, dtype="bf16", seed=wl["seed"], device=dev)
@@ -391,6 +395,9 @@ def crossgram_case(dev, steps, warmup):
         res = {}
         for name, route in (("factored", dt.DATTRI_ROUTE_FACTORED), ("materialized", dt.DATTRI_ROUTE_MATERIALIZED),
                             ("auto", dt.DATTRI_ROUTE_AUTO)):
+            if route_names and name not in route_names:
+                res[name] = float("nan")
+                continue
             ws = torch.empty(max(256, dt.dattri_cross_gram_workspace_bytes(a, b, route)), dtype=torch.uint8,
                              device=dev)
             res[name] = med_ms(lambda: dt.dattri_cross_gram(a, b, K, K.stride(0), ws, ws.numel(), route))
@@ -805,7 +812,8 @@ def main():
     if args.phase in ("all", "gpt2"):
         out["gpt2"] = gpt2_case(dev, max(args.steps, 5), args.warmup)
     if args.phase in ("all", "crossgram"):
-        out["crossgram_routing"] = crossgram_case(dev, max(min(args.steps, 5), 3), min(args.warmup, 1))
+        out["crossgram_routing"] = crossgram_case(dev, max(min(args.steps, 5), 3), min(args.warmup, 1), args.xg_T,
+                                                  args.xg_routes)
     if args.phase in ("all", "curvature"):
         out["curvature"] = curvature_case(dev, max(min(args.steps, 5), 3), min(args.warmup, 1))
     if args.phase in ("all", "fit"):

@@ -30,6 +30,18 @@ __device__ inline rsrc_t make_rsrc(const void* base, uint32_t bytes) {
 }
 constexpr uint32_t kOOB = 0xFFFFFFF0u;  // an offset no descriptor here covers
 
+// LDS destination of a direct load (buffer_load ... lds): lane l's 16 bytes
+// land at p + 16 l.
+#define DATTRI_LDS_PTR(p) ((__attribute__((address_space(3))) void*)(p))
+
+// Wait until at most N vector-memory operations of this wave are in flight
+// (direct loads count until their data is in LDS); other counters untouched.
+template <int N>
+__device__ inline void wait_vmcnt_dma() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt((N & 0xF) | ((N >> 4) << 14) | (0x7 << 4) | (0xF << 8));
+}
+
 __device__ inline i32x4 load16(rsrc_t r, uint32_t off) {
   return __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, 0);
 }

@@ -8,7 +8,7 @@
 // over one chunk of its tokens and one range of its 128-column tiles (G is a
 // sum over tokens and Psi a sum over the columns of G, so chunks and ranges
 // give partial blocks that add up).  For each tile of 128 input features v0 ..
-// v0 + 127, g_tile (gtile.h) forms the transposed tile G^T[v][u] with bf16
+// v0 + 127, g_tile_dma (gtile.h) forms the transposed tile G^T[v][u] with bf16
 // 32x32x16 MFMA.  In that C layout lane l holds one output feature u (l % 32)
 // and 16 input features: element x is v = 8 (x / 4) + 4 (l / 32) + x % 4.
 // Eight of them are exactly the K slots a 32x32x16 A operand takes from lane
@@ -37,7 +37,7 @@
 namespace dattri {
 using namespace dev;
 
-static_assert(kGFusedRows == 128 && kGFusedCols == 128, "tile of GTile<2, 2>");
+static_assert(kGFusedRows == 128 && kGFusedCols == 128, "tile of g_tile_dma");
 
 // Operand of K slots pi(0 .. 15) + 16 hx of the 32-row k-block kb of a packed
 // bf16 map (k-blocks of 32 rows, 16-column tiles, lane (g, n) of a fragment
@@ -82,11 +82,10 @@ __device__ inline f32x16 mma32(i32x4 a, i32x4 b, f32x16 c) {
 // NK: 32-column tiles of k_in the instance holds (1, 2 or 4).
 template <int NK>
 __global__ __launch_bounds__(256, NK <= 2 ? 2 : 1) void gfused_kernel(GFusedArgs a) {
-  using C = GTile<2, 2>;
-  static_assert(kWaves * 32 * 32 * 4 <= C::kLdsBytes, "wave parts reuse the token staging buffer");
-  __shared__ __align__(16) uint8_t stage[C::kLdsBytes];
+  static_assert(kWaves * 32 * 32 * 4 <= GDma::kBytes, "wave parts reuse the token staging ring");
+  __shared__ __align__(16) uint8_t stage[GDma::kBytes];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  // g_tile's wave grid: wave (wr, wc) holds G^T rows (input features)
+  // g_tile_dma's wave grid: wave (wr, wc) holds G^T rows (input features)
   // 64 wr .. 64 wr + 63 and columns (output features) 64 wc .. 64 wc + 63
   const int wr = wave >> 1, wc = wave & 1;
   // blockIdx.x = (row block * n_vsplit + column range) * n_tchunks + token chunk
@@ -119,8 +118,6 @@ __global__ __launch_bounds__(256, NK <= 2 ? 2 : 1) void gfused_kernel(GFusedArgs
 
   // G^T tiles: rows from the A blocks (d_in side), columns from the B blocks
   const GRows gr = g_rows(a_rows, b_rows, rows, a.d_in, a.d_out);
-  GStage<2, 2> st;
-  if (v_begin < v_end) g_load(gr, 0, v_begin, u0, st);
   for (int v0 = v_begin; v0 < v_end; v0 += kGFusedCols) {
     // P_in operands of this wave's input features, in flight during the
     // tile's token stages: k-block (v0 + 64 wr + 32 i) / 32, slice hx
@@ -133,8 +130,7 @@ __global__ __launch_bounds__(256, NK <= 2 ? 2 : 1) void gfused_kernel(GFusedArgs
         for (int kt = 0; kt < NK; ++kt)
           pin[i][hx][kt] = perm_operand(rpin, (v0 + 64 * wr + 32 * i) / 32, nkb_in, na16, kt, hx, lane);
     f32x16 acc[2][2];
-    const int nv = v0 + kGFusedCols < v_end ? v0 + kGFusedCols : -1;
-    g_tile_from(gr, rows, v0, u0, nv, u0, stage, st, acc);
+    g_tile_dma(gr, rows, v0, u0, stage, acc);
     // acc[i][j]: G^T rows v0 + 64 wr + 32 i + (x-dependent), column
     // u0 + 64 wc + 32 j + l % 32
 #pragma unroll

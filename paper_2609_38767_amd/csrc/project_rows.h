@@ -168,14 +168,6 @@ struct DmaLds {
   static constexpr int kBytes = kMapOff + 3 * kMapStage;
 };
 
-#define DATTRI_LDS_PTR(p) ((__attribute__((address_space(3))) void*)(p))
-
-template <int N>
-__device__ inline void wait_vmcnt_dma() {
-  static_assert(N >= 0 && N < 64, "vmcnt range");
-  __builtin_amdgcn_s_waitcnt((N & 0xF) | ((N >> 4) << 14) | (0x7 << 4) | (0xF << 8));
-}
-
 template <int RT, int NT>
 __device__ inline void project_rows_dma(const rsrc_t r, int r_wave, int nrows, int d, int64_t ld,
                                         const FragSrc<NT>& P, f32x4 (&acc)[RT][NT], uint8_t* lds) {

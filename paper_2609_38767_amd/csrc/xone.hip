@@ -4,7 +4,7 @@
 // products), for bf16 factor blocks with 16-byte aligned rows and a small
 // batch b.  DW never goes to memory: a workgroup owns one 128 x 128 tile of
 // DW, one example j of batch b and a run of examples of batch a; it forms
-// the tile of DW_b[j] once (g_tile, gtile.h, float32 accumulators), then for
+// the tile of DW_b[j] once (g_tile_dma, gtile.h, float32 accumulators), then for
 // each example i of its run forms the tile of DW_a[i] in the same register
 // layout and reduces sum over the tile of DW_a[i] * DW_b[j] (for the squared
 // norms, DW_a[i] * DW_a[i]): per lane over its 64 elements, then across the
@@ -19,28 +19,33 @@ namespace dattri {
 using namespace dev;
 
 __global__ __launch_bounds__(256, 2) void xone_kernel(XOneArgs a) {
-  using C = GTile<2, 2>;
-  __shared__ __align__(16) uint8_t lds[C::kLdsBytes];
+  __shared__ __align__(16) uint8_t lds[GDma::kBytes];
   __shared__ float wsum[kWaves];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int tile = blockIdx.x, y = blockIdx.y;
-  const int u0 = (tile / a.n_vt) * kXOneTile, v0 = (tile % a.n_vt) * kXOneTile;
+  // Workgroups go to the 8 XCDs (each with its own L2) in turn: workgroup x
+  // takes tile (x % 8) * (n / 8) + x / 8, so each XCD owns one band of
+  // consecutive tiles, ordered along the wider side of DW: the XCD reads its
+  // band of the wider factor block once, instead of every XCD reading all of it.
+  const int n_ub = (a.d_out + kXOneTile - 1) / kXOneTile, n_tiles = n_ub * a.n_vt;
+  const int tile = (n_tiles % 8 == 0) ? (blockIdx.x % 8) * (n_tiles / 8) + blockIdx.x / 8 : blockIdx.x;
+  const int y = blockIdx.y;
+  const bool u_major = n_ub >= a.n_vt;
+  const int u0 = (u_major ? tile / a.n_vt : tile % n_ub) * kXOneTile;
+  const int v0 = (u_major ? tile % a.n_vt : tile / n_ub) * kXOneTile;
   const int i_begin = blockIdx.z * a.ipw, i_end = min(a.ci, i_begin + a.ipw);
 
   auto rows_of = [](const int32_t* len, int e, int T) { return len ? min(max(len[e], 0), T) : T; };
+  auto tile_of = [&](const void* B, const void* A, const int32_t* len, int e, int T, f32x16 (&acc)[2][2]) {
+    const int rows = rows_of(len, e, T);
+    const GRows r = g_rows((const uint8_t*)B + (size_t)e * T * a.d_out * 2,
+                           (const uint8_t*)A + (size_t)e * T * a.d_in * 2, rows, a.d_out, a.d_in);
+    g_tile_dma(r, rows, u0, v0, lds, acc);
+  };
   f32x16 ref[2][2];
-  if (!a.diag) {
-    const int e = a.j0 + y;
-    g_tile<2, 2>((const uint8_t*)a.B2 + (size_t)e * a.T2 * a.d_out * 2,
-                 (const uint8_t*)a.A2 + (size_t)e * a.T2 * a.d_in * 2, rows_of(a.len2, e, a.T2), a.d_out,
-                 a.d_in, u0, v0, lds, ref);
-  }
+  if (!a.diag) tile_of(a.B2, a.A2, a.len2, a.j0 + y, a.T2, ref);
   for (int i = i_begin; i < i_end; ++i) {
-    const int e = a.i0 + i;
     f32x16 g[2][2];
-    g_tile<2, 2>((const uint8_t*)a.B1 + (size_t)e * a.T1 * a.d_out * 2,
-                 (const uint8_t*)a.A1 + (size_t)e * a.T1 * a.d_in * 2, rows_of(a.len1, e, a.T1), a.d_out,
-                 a.d_in, u0, v0, lds, g);
+    tile_of(a.B1, a.A1, a.len1, a.i0 + i, a.T1, g);
     float s = 0.f;
 #pragma unroll
     for (int p = 0; p < 2; ++p)

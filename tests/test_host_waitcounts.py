@@ -1,10 +1,11 @@
 """The hand-counted vmcnt waits of the direct-to-LDS pipelines hold in the
 code the compiler emits (host-only: compiles the kernels to gfx950 assembly).
 
-Two kernels wait for loads that land in LDS by counting, rather than by a
+Three designs wait for loads that land in LDS by counting, rather than by a
 full vmcnt(0): the score GEMM (a stage of training rows has landed once no
-more than 28 / 18 later loads are outstanding) and the direct-load projection
-(a stage has landed once no more than one stage's loads are outstanding).
+more than 28 / 18 later loads are outstanding), the direct-load projection
+(a stage has landed once no more than one stage's loads are outstanding) and
+the weight-gradient tile (once no more than two later stages' loads are).
 Direct loads are invisible to the compiler's own wait insertion, so these
 counts are only right while the compiled load order is the designed one.
 These tests read that order from the assembly of this build.
@@ -112,3 +113,31 @@ def test_direct_load_projection_waits(factored_asm, na, nb):
     assert all(e == "D" for e in ev[d_pos[0]:d_pos[-1] + 1]), "".join(ev)
     counts = {int(m.group(1)) for t in body for m in [re.match(r"s_waitcnt vmcnt\((\d+)\)$", t)] if m}
     assert counts == {0, k_a, k_b}, (counts, k_a, k_b)
+
+
+@pytest.mark.parametrize("src,sym", [("gradient_tr.hip", "_ZN6dattri18gradient_tr_kernel"),
+                                     ("xone.hip", "_ZN6dattri11xone_kernel"),
+                                     ("gfused.hip", "_ZN6dattri13gfused_kernelILi1E"),
+                                     ("gfused.hip", "_ZN6dattri13gfused_kernelILi2E"),
+                                     ("gfused.hip", "_ZN6dattri13gfused_kernelILi4E")])
+def test_direct_load_gradient_tile_waits(src, sym):
+    # Design (g_tile_dma, inlined once per tile the kernel forms): every stage
+    # is 4 direct loads per wave (2 per side), up to three stages issued
+    # before the stage loop and one per iteration after the stage barrier; the
+    # hand wait before stage k's barrier is vmcnt(4 x min(2, stages after k))
+    # = 8, 4 or 0.  The transposing LDS reads are inline assembly, so the
+    # compiler inserts no vmcnt wait of its own between a barrier and the
+    # reads that follow it (a wait there would drain the ring each stage).
+    body = _body(_asm(src), sym)
+    ev = _events(body)
+    hand = {e[1] for e in ev if isinstance(e, tuple)}
+    assert 8 in hand and hand <= {0, 4, 8}, hand
+    n_d = sum(1 for e in ev if e == "D")
+    assert n_d > 0 and n_d % 4 == 0, n_d
+    reads = [i for i, t in enumerate(body) if t.startswith("ds_read_b64_tr_b16")]
+    assert reads
+    for i in reads:
+        j = i - 1
+        while j >= 0 and body[j] != "s_barrier" and not body[j].startswith("ds_read_b64_tr_b16"):
+            assert not body[j].startswith("s_waitcnt vmcnt"), (i, body[j])
+            j -= 1

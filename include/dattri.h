@@ -430,9 +430,13 @@ dattri_status dattri_layer_route(const dattri_ctx* ctx, int32_t layer, dattri_ro
  *                 16): tile_flops = tiles * 2 * 128^2 (d_in + d_out + 1),
  *                 tile_bytes = tiles * 2 * 128 (d_in + d_out) elt;
  *   materialized  the faster of two forms of Eq. 1 + Frobenius products:
- *                 staged: max(build_flops / build rate, build_bytes / build
- *                 bandwidth) + dot_bytes / dot bandwidth + 4 launch_us (DW of
- *                 both batches written to the workspace, then the products);
+ *                 staged: max(build rounds, build_bytes / build bandwidth)
+ *                 + dot_bytes / dot bandwidth + 4 launch_us (DW of both
+ *                 batches written to the workspace, then the products), where
+ *                 the build runs one workgroup per 128 x 128 tile of DW and
+ *                 example, per batch ceil(tiles n / 512) rounds of one tile
+ *                 build, 2 * 128^2 * T (T rounded up to 32) FLOP at
+ *                 build_tflops / 512;
  *                 one-pass (bf16 blocks with 16-byte aligned rows only): no DW
  *                 in memory, a workgroup forms one 128 x 128 tile of DW_b[j]
  *                 and then the same tile of DW_a[i] for each of a run of ipw

@@ -16,9 +16,9 @@ chosen from exact operation counts and eight effective rates
    reported per layer;
 2. fits the eight rates by minimising the squared log error of the predicted
    times (the same formula as the library's model: whole 128 x 128 tiles of
-   the padded token Gram for the factorized kernel; gradient build, products
-   and four launches for the staged form; rounds of 512 workgroups of tile
-   builds for the one-pass form);
+   the padded token Gram for the factorized kernel; gradient build (rounds of
+   512 workgroups of tile builds), products and four launches for the staged
+   form; rounds of 512 workgroups of tile builds for the one-pass form);
 3. prints one JSON object with the fitted model and, per shape, the measured
    and predicted times, the route AUTO picks and its regret.
 
@@ -134,12 +134,13 @@ def predict_us(model, s):
     tbytes = tiles * 2.0 * TILE * (di + dq) * 2
     f = max(tflops / (model["ghost_tflops"] * 1e6), tbytes / (model["ghost_gbs"] * 1e3)) + model["ghost_layer_us"]
     f_bytes = (na * T + nb * T) * (di + dq) * 2
-    build_flops = 2 * (na * T + nb * T) * di * dq
     build_bytes = f_bytes + 4 * (na + nb) * di * dq
     dot_bytes = 4 * (na + nb) * di * dq
-    b = max(build_flops / (model["build_tflops"] * 1e6), build_bytes / (model["build_gbs"] * 1e3))
-    m = b + dot_bytes / (model["dot_gbs"] * 1e3) + 4 * model["launch_us"]
     dtiles = math.ceil(dq / TILE) * math.ceil(di / TILE)
+    per = 2.0 * TILE * TILE * _r32(T) / (model["build_tflops"] * 1e6 / SLOTS)
+    rounds = (-(-(dtiles * na) // SLOTS) + -(-(dtiles * nb) // SLOTS)) * per
+    b = max(rounds, build_bytes / (model["build_gbs"] * 1e3))
+    m = b + dot_bytes / (model["dot_gbs"] * 1e3) + 4 * model["launch_us"]
     o = onepass_us(model, dtiles, na, nb, T) + 2 * model["launch_us"]
     return f, m, b + 2 * model["launch_us"], o
 

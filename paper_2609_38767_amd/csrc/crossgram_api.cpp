@@ -20,20 +20,22 @@ using namespace dattri;
 namespace dattri {
 
 dattri_crossgram_cost_model default_crossgram_cost_model() {
-  // Effective rates measured on MI355X (bf16 factor blocks): both forced
-  // routes and the gradient build timed on 28 shapes (1024..4096-wide and
-  // 128-wide layers, T = 16..2048, 8 x 1, 16 x 16 and 8 x 8 batches), each
-  // a stack of 24 layers so the factorized route runs as one grouped launch,
-  // and fitted by least squares on log time.
+  // Effective rates measured on MI355X (bf16 factor blocks): the factorized
+  // route, both forms of the materialized one and the gradient build timed on
+  // 28 shapes (1024..4096-wide and 128-wide layers, T = 16..2048, 8 x 1,
+  // 16 x 16 and 8 x 8 batches), each a stack of 24 layers so the factorized
+  // route runs as one grouped launch, and fitted by least squares on log
+  // time.  The two bandwidths come out far above HBM's: on this sweep the
+  // factor reads never bound those kernels.
   dattri_crossgram_cost_model m;
-  m.ghost_tflops = 598.0;   // on whole padded tiles
-  m.ghost_gbs = 10500.0;
-  m.ghost_layer_us = 2.73;
-  m.build_tflops = 725.0;
-  m.build_gbs = 95600.0;
-  m.dot_gbs = 1870.0;
-  m.launch_us = 15.1;
-  m.onepass_tflops = 725.0;  // issued tile builds of the one-pass kernel
+  m.ghost_tflops = 599.6;  // on whole padded tiles
+  m.ghost_gbs = 56200.0;
+  m.ghost_layer_us = 2.52;
+  m.build_tflops = 769.2;  // on the tile builds of the build kernel's rounds
+  m.build_gbs = 7.22e6;
+  m.dot_gbs = 1286.0;
+  m.launch_us = 7.50;
+  m.onepass_tflops = 1134.8;  // on the tile builds the one-pass kernel issues
   return m;
 }
 
@@ -110,8 +112,9 @@ bool xone_ok(const Layer& La, const Layer& Lb, int elt);
 // the factorized kernel computes whole 128 x 128 tiles of the padded token
 // Gram and reads 128 rows of each side per tile (diag: each example's own
 // Gram); the materialized route is the faster of its two forms: DW staged in
-// HBM (build both batches, then the products: four launches) and, where
-// `one` allows it, the one-pass kernel (xone_shape, plus the tile-sum launch).
+// HBM (build both batches, in rounds of tile builds as the one-pass form, or
+// by the bytes written; then the products: four launches) and, where `one`
+// allows it, the one-pass kernel (xone_shape, plus the tile-sum launch).
 void xpredict(const dattri_crossgram_cost_model& m, int64_t na, int64_t nb, int64_t Ta, int64_t Tb,
               int64_t di, int64_t dq, int elt, bool diag, bool one, double* f_us, double* m_us) {
   if (diag) nb = na;
@@ -123,12 +126,16 @@ void xpredict(const dattri_crossgram_cost_model& m, int64_t na, int64_t nb, int6
   *f_us = (tiles == 0) ? 0.0
                        : std::max(tflops / (m.ghost_tflops * 1e6), tbytes / (m.ghost_gbs * 1e3)) +
                              m.ghost_layer_us;
-  const double build = std::max((double)c.build_flops / (m.build_tflops * 1e6),
-                                (double)c.build_bytes / (m.build_gbs * 1e3));
+  // the build kernel runs one workgroup per 128 x 128 tile of DW and example:
+  // rounds of kXOneSlots workgroups per batch, each as long as one tile build
+  const int64_t dtiles = cdiv(dq, kXOneTile) * cdiv(di, kXOneTile);
+  const double per_token = 2.0 * kXOneTile * kXOneTile / (m.build_tflops * 1e6 / kXOneSlots);
+  const double rounds = (double)cdiv(dtiles * na, kXOneSlots) * per_token * (double)r32(Ta) +
+                        (diag ? 0.0 : (double)cdiv(dtiles * nb, kXOneSlots) * per_token * (double)r32(Tb));
+  const double build = std::max(rounds, (double)c.build_bytes / (m.build_gbs * 1e3));
   const double dot_bytes = diag ? 4.0 * na * di * dq : (double)c.dot_bytes;
   *m_us = build + dot_bytes / (m.dot_gbs * 1e3) + (diag ? 3.0 : 4.0) * m.launch_us;
   if (one) {
-    const int64_t dtiles = cdiv(dq, kXOneTile) * cdiv(di, kXOneTile);
     const double o = xone_shape(m, dtiles, na, nb, Ta, Tb, diag).us + 2.0 * m.launch_us;
     *m_us = std::min(*m_us, o);
   }

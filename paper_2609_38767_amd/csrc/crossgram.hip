@@ -55,19 +55,150 @@ __device__ inline i32x4 ghost_chunk(const uint8_t* base, int64_t grow, bool vali
   return v;
 }
 
-// Workgroup: one 128 x 128 tile, 4 waves in a 2 x 2 grid of 64 x 64 (4 x 4
-// blocks of 16 x 16 per Gram).  Stages of 128 bytes of features per row are
-// double-buffered in LDS (rows XOR-swizzled by 16-byte chunk); the next stage
-// is prefetched into registers while the current one is multiplied.
+// Direct-load form of a tile's two Grams (bf16 entries with E.dma set):
+// stages of 32 features (64 bytes per token row, one 16x16x32 K step) of both
+// sides go straight from memory to LDS (buffer_load ... lds; one load moves
+// 1 KiB = 16 rows, each wave issues 2 per side and stage) through a ring of 4
+// stages, 3 in flight, over d_in's stages and then d_out's in one stream.
+// The 16-byte chunk c of local row r sits at c XOR gswz16(r), so the 16-byte
+// fragment reads (8 lanes served together, 8 rows x 16 bytes) fall in 8
+// distinct 16-byte bank groups: measured 0 bank-conflict cycles, against 3.7
+// per read unswizzled (a swizzle that also spread 16-lane groups measured the
+// same as none, so the hardware serves 8 lanes of a 16-byte read at a time).
+// Waits count direct
+// loads as in the weight-gradient tile (gtile.h): stage k has landed when at
+// most 4 x min(2, stages after k) of the wave's loads are in flight; the
+// fragment reads are inline assembly tied to hand lgkmcnt waits, so the
+// compiler does not drain the ring before them.
+constexpr int kGhDmaStage = 2 * kGhRows * 64;  // both sides, 16 KiB
+__device__ constexpr int gswz16(int r) { return (r >> 1) & 3; }
+
+__device__ inline void ghost_tile_dma(const GhostEntry& E, const GhostTile& tl, uint8_t* lds,
+                                      f32x4 (&acc)[2][4][4]) {
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int g = lane >> 4, m16 = lane & 15, wm = wave >> 1, wn = wave & 1;
+  auto stage_barrier = [] { asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory"); };
+
+  // this lane's rows of the direct loads: local rows 16 (2 wave + t) + lane / 4
+  // of each side, physical chunk lane % 4; row index relative to the first
+  // example of the tile's range (descriptors start there, so 32-bit offsets
+  // reach every row of the tile)
+  int rel[2][2], cl[2];
+  bool ok[2][2];
+  rsrc_t rA[2], rB[2];
+#pragma unroll
+  for (int side = 0; side < 2; ++side) {
+    const int R0 = (side ? tl.ct : tl.rt) * kGhRows;
+    const int Tp = side ? E.Tp2 : E.Tp1, T = side ? E.T2 : E.T1, n = side ? E.n2 : E.n1;
+    const int32_t* len = side ? E.len2 : E.len1;
+    const int e0 = R0 / Tp;
+#pragma unroll
+    for (int t = 0; t < 2; ++t) {
+      const int row = 16 * (2 * wave + t) + (lane >> 2);
+      const int R = R0 + row, e = R / Tp, tt = R - e * Tp;
+      int t_eff = T;
+      if (e < n && len) t_eff = min(max(len[e], 0), T);
+      ok[side][t] = e < n && tt < t_eff;
+      rel[side][t] = (e - e0) * T + tt;
+      if (side == 0) cl[t] = (lane & 3) ^ gswz16(row);
+    }
+    const uint8_t* a = (const uint8_t*)(side ? E.A2 : E.A1);
+    const uint8_t* b = (const uint8_t*)(side ? E.B2 : E.B1);
+    const int64_t ra = (int64_t)(n - e0) * T * E.d_in * 2, rb = (int64_t)(n - e0) * T * E.d_out * 2;
+    rA[side] = make_rsrc(a + (int64_t)e0 * T * E.d_in * 2, (uint32_t)min<int64_t>(ra, kOOB));
+    rB[side] = make_rsrc(b + (int64_t)e0 * T * E.d_out * 2, (uint32_t)min<int64_t>(rb, kOOB));
+  }
+  const int nk0 = (E.d_in + 31) / 32, nk1 = (E.d_out + 31) / 32, ns = nk0 + nk1;
+  auto issue = [&](int st) {
+    const bool p = st >= nk0;
+    const int kk = p ? st - nk0 : st, d = p ? E.d_out : E.d_in;
+    uint8_t* sb = lds + (st & 3) * kGhDmaStage;
+#pragma unroll
+    for (int side = 0; side < 2; ++side) {
+      const rsrc_t r = p ? rB[side] : rA[side];
+#pragma unroll
+      for (int t = 0; t < 2; ++t) {
+        const int col = kk * 32 + cl[t] * 8;
+        const uint32_t off = ok[side][t] && col < d ? (uint32_t)(((int64_t)rel[side][t] * d + col) * 2) : kOOB;
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(r, DATTRI_LDS_PTR(sb + side * kGhRows * 64 + (2 * wave + t) * 1024),
+                                                 16, off, 0, 0, 0);
+      }
+    }
+  };
+
+  // fragment reads: A operand rows wm 64 + 16 i + m16 of side 0, B operand
+  // rows wn 64 + 16 j + m16 of side 1, logical chunk g (features 8 g .. 8 g + 7)
+  const uint32_t lds0 = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) uint8_t*)lds;
+  uint32_t ao[4], bo[4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int ra = wm * 64 + 16 * i + m16, rb = wn * 64 + 16 * i + m16;
+    ao[i] = lds0 + (uint32_t)(ra * 64 + ((g ^ gswz16(ra)) << 4));
+    bo[i] = lds0 + (uint32_t)(kGhRows * 64 + rb * 64 + ((g ^ gswz16(rb)) << 4));
+  }
+  auto rd = [](uint32_t addr) {
+    i32x4 x;
+    asm volatile("ds_read_b128 %0, %1" : "=v"(x) : "v"(addr));
+    return x;
+  };
+  // one stage: the 4 B fragments, then the A fragments one at a time, each
+  // row of 4 MFMA starting once its A fragment has landed (LDS returns in order)
+  auto stage = [&](uint32_t so, f32x4 (&c)[4][4]) {
+    i32x4 bf[4], af[4];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) bf[j] = rd(bo[j] + so);
+#pragma unroll
+    for (int i = 0; i < 4; ++i) af[i] = rd(ao[i] + so);
+    asm volatile("s_waitcnt lgkmcnt(3)" : "+v"(bf[0]), "+v"(bf[1]), "+v"(bf[2]), "+v"(bf[3]), "+v"(af[0]));
+#pragma unroll
+    for (int j = 0; j < 4; ++j) c[0][j] = frag_mma<2>(af[0], bf[j], c[0][j]);
+    __builtin_amdgcn_sched_barrier(0);
+    asm volatile("s_waitcnt lgkmcnt(2)" : "+v"(af[1]));
+#pragma unroll
+    for (int j = 0; j < 4; ++j) c[1][j] = frag_mma<2>(af[1], bf[j], c[1][j]);
+    __builtin_amdgcn_sched_barrier(0);
+    asm volatile("s_waitcnt lgkmcnt(1)" : "+v"(af[2]));
+#pragma unroll
+    for (int j = 0; j < 4; ++j) c[2][j] = frag_mma<2>(af[2], bf[j], c[2][j]);
+    __builtin_amdgcn_sched_barrier(0);
+    asm volatile("s_waitcnt lgkmcnt(0)" : "+v"(af[3]));
+#pragma unroll
+    for (int j = 0; j < 4; ++j) c[3][j] = frag_mma<2>(af[3], bf[j], c[3][j]);
+  };
+  auto wait_for = [&](int k) {
+    const int ahead = ns - 1 - k;
+    if (ahead >= 2)
+      wait_vmcnt_dma<8>();
+    else if (ahead == 1)
+      wait_vmcnt_dma<4>();
+    else
+      wait_vmcnt_dma<0>();
+    stage_barrier();
+    if (k + 3 < ns) issue(k + 3);
+  };
+#pragma unroll
+  for (int p = 0; p < 3; ++p)
+    if (p < ns) issue(p);
+  for (int k = 0; k < nk0; ++k) {
+    wait_for(k);
+    stage((uint32_t)((k & 3) * kGhDmaStage), acc[0]);
+  }
+  for (int k = nk0; k < ns; ++k) {
+    wait_for(k);
+    stage((uint32_t)((k & 3) * kGhDmaStage), acc[1]);
+  }
+  stage_barrier();
+}
+
+// Register-staged form (float32 entries, unaligned rows): stages of 128 bytes
+// of features per row are double-buffered in LDS (rows XOR-swizzled by
+// 16-byte chunk) and the next stage is prefetched into registers while the
+// current one is multiplied.  smem: 2 x 2 x 128 x 128 bytes.
 template <int ELT>
-__global__ __launch_bounds__(256, 2) void ghost_kernel(const GhostEntry* __restrict__ entries,
-                                                       const GhostTile* __restrict__ tiles,
-                                                       float* __restrict__ parts) {
+__device__ inline void ghost_tile_reg(const GhostEntry& E, const GhostTile& tl, uint8_t (*smem)[2][kGhRows * 128],
+                                      f32x4 (&acc)[2][4][4]) {
   constexpr int EPL = 16 / ELT;
   constexpr int BK = 128 / ELT;  // features per stage
-  __shared__ __align__(16) uint8_t smem[2][2][kGhRows * 128];  // [stage][row side, col side]
-  const GhostTile tl = tiles[blockIdx.x];
-  const GhostEntry E = entries[tl.entry];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int g = lane >> 4, m16 = lane & 15, wm = wave >> 1, wn = wave & 1;
   const bool aligned = E.aligned != 0;
@@ -90,14 +221,6 @@ __global__ __launch_bounds__(256, 2) void ghost_kernel(const GhostEntry* __restr
       grow[side][i] = (int64_t)e * T + t;
     }
   }
-
-  f32x4 acc[2][4][4];
-#pragma unroll
-  for (int p = 0; p < 2; ++p)
-#pragma unroll
-    for (int i = 0; i < 4; ++i)
-#pragma unroll
-      for (int j = 0; j < 4; ++j) acc[p][i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
 
 #pragma unroll
   for (int p = 0; p < 2; ++p) {  // p = 0: input Gram over d_in; 1: output-gradient Gram over d_out
@@ -151,6 +274,32 @@ __global__ __launch_bounds__(256, 2) void ghost_kernel(const GhostEntry* __restr
       __syncthreads();
     }
   }
+}
+
+// Workgroup: one 128 x 128 tile, 4 waves in a 2 x 2 grid of 64 x 64 (4 x 4
+// blocks of 16 x 16 per Gram); entries with E.dma take the direct-load form.
+template <int ELT>
+__global__ __launch_bounds__(256, 2) void ghost_kernel(const GhostEntry* __restrict__ entries,
+                                                       const GhostTile* __restrict__ tiles,
+                                                       float* __restrict__ parts) {
+  static_assert(4 * kGhDmaStage == 2 * 2 * kGhRows * 128, "one LDS block for both forms");
+  __shared__ __align__(16) uint8_t smem[2][2][kGhRows * 128];  // [stage][row side, col side]
+  const GhostTile tl = tiles[blockIdx.x];
+  const GhostEntry E = entries[tl.entry];
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int wm = wave >> 1, wn = wave & 1;
+
+  f32x4 acc[2][4][4];
+#pragma unroll
+  for (int p = 0; p < 2; ++p)
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+      for (int j = 0; j < 4; ++j) acc[p][i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+  if (ELT == 2 && E.dma)  // uniform
+    ghost_tile_dma(E, tl, &smem[0][0][0], acc);
+  else
+    ghost_tile_reg<ELT>(E, tl, smem, acc);
 
   // Hadamard product of the two Grams, summed per 16 x 16 block (lanes hold
   // the same (row, column) of both accumulators)

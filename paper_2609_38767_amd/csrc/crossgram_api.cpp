@@ -47,6 +47,7 @@ constexpr int64_t kGhostPartsBudget = (int64_t)256 << 20;  // block sums per fac
 constexpr int64_t kGhostTilesMax = (int64_t)1 << 22;      // tiles per factorized group
 constexpr int64_t kXgGBudget = (int64_t)2 << 30;          // staged float32 DW per chunk
 constexpr int64_t kDotChunk = 16384;                      // floats per Frobenius-product chunk
+constexpr int64_t kOOBLimit = 0xFFFFFFF0LL;                // first byte offset a descriptor never covers
 constexpr int64_t kXOnePartsBudget = (int64_t)64 << 20;     // one-pass tile sums per launch (bytes)
 constexpr int64_t kXOneSlots = 2 * 256;                    // resident one-pass workgroups (2 per CU)
 
@@ -159,6 +160,15 @@ dattri_status check_pair(const dattri_ctx* a, const dattri_ctx* b) {
   return DATTRI_OK;
 }
 
+// Whether the factorized kernel can stream an entry's token rows by direct
+// loads: bf16, 16-byte aligned rows, and the rows one tile touches (at most
+// 128 + 2 T from the tile's first example) within 32-bit byte offsets.
+bool ghost_dma_ok(const GhostEntry& E, int elt) {
+  const int64_t d = std::max(E.d_in, E.d_out), lim = (int64_t)kOOBLimit;
+  return elt == 2 && E.aligned && (128 + 2 * (int64_t)E.T1) * d * elt < lim &&
+         (128 + 2 * (int64_t)E.T2) * d * elt < lim;
+}
+
 bool layer_aligned(const Layer& L, int elt) {
   return ((uintptr_t)L.A % 16 == 0) && ((uintptr_t)L.B % 16 == 0) && (L.d_in * elt) % 16 == 0 &&
          (L.d_out * elt) % 16 == 0;
@@ -260,6 +270,7 @@ dattri_status build_xplan(const dattri_ctx* a, const dattri_ctx* b, dattri_route
       E.nbr = na * E.Tp1 / 16;
       E.nbc = nb * E.Tp2 / 16;
       E.out0 = 0;
+      E.dma = ghost_dma_ok(E, elt) ? 1 : 0;
       add_entry(P, E, cdiv((int64_t)na * E.Tp1, kGhostTile), cdiv((int64_t)nb * E.Tp2, kGhostTile));
     } else {
       if (La.T == 0) continue;
@@ -274,6 +285,7 @@ dattri_status build_xplan(const dattri_ctx* a, const dattri_ctx* b, dattri_route
         E.Tp1 = E.Tp2 = (int)r16(La.T);
         E.nbr = E.nbc = E.Tp1 / 16;
         E.out0 = i;
+        E.dma = ghost_dma_ok(E, elt) ? 1 : 0;
         add_entry(P, E, cdiv(E.Tp1, kGhostTile), cdiv(E.Tp2, kGhostTile));
       }
     }

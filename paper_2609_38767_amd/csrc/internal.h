@@ -203,6 +203,9 @@ struct GhostEntry {
   int32_t aligned;                  // rows and bases 16-byte aligned (vector loads)
   int32_t out0;                     // output row of its pair (i, j) is out0 + i
   int64_t part_off;                 // float offset of its block sums (nbr x nbc)
+  int32_t dma;                      // bf16, aligned, and a tile's rows within 32-bit byte offsets:
+                                    // token rows streamed into LDS by direct loads
+  int32_t pad0;
 };
 struct GhostTile { int32_t entry, rt, ct, pad0; };  // 128 x 128 tile of an entry
 constexpr int kGhostTile = 128;

@@ -119,10 +119,12 @@ def test_direct_load_projection_waits(factored_asm, na, nb):
                                      ("xone.hip", "_ZN6dattri11xone_kernel"),
                                      ("gfused.hip", "_ZN6dattri13gfused_kernelILi1E"),
                                      ("gfused.hip", "_ZN6dattri13gfused_kernelILi2E"),
-                                     ("gfused.hip", "_ZN6dattri13gfused_kernelILi4E")])
+                                     ("gfused.hip", "_ZN6dattri13gfused_kernelILi4E"),
+                                     ("crossgram.hip", "_ZN6dattri12ghost_kernelILi2E")])
 def test_direct_load_gradient_tile_waits(src, sym):
-    # Design (g_tile_dma, inlined once per tile the kernel forms): every stage
-    # is 4 direct loads per wave (2 per side), up to three stages issued
+    # Design (g_tile_dma, inlined once per tile the kernel forms; the
+    # factorized cross-Gram tile ghost_tile_dma has the same ring): every
+    # stage is 4 direct loads per wave (2 per side), up to three stages issued
     # before the stage loop and one per iteration after the stage barrier; the
     # hand wait before stage k's barrier is vmcnt(4 x min(2, stages after k))
     # = 8, 4 or 0.  The transposing LDS reads are inline assembly, so the
@@ -134,6 +136,8 @@ def test_direct_load_gradient_tile_waits(src, sym):
     assert 8 in hand and hand <= {0, 4, 8}, hand
     n_d = sum(1 for e in ev if e == "D")
     assert n_d > 0 and n_d % 4 == 0, n_d
+    if src == "crossgram.hip":  # its register-staged form shares the kernel; reads not checked
+        return
     reads = [i for i, t in enumerate(body) if t.startswith("ds_read_b64_tr_b16")]
     assert reads
     for i in reads:

@@ -40,6 +40,8 @@ def parse():
                    help="sequence lengths of the cross-Gram sweep (default: the full sweep)")
     p.add_argument("--xg-routes", nargs="*", default=None, choices=["factored", "materialized", "auto"],
                    help="routes the cross-Gram sweep times (default: all three)")
+    p.add_argument("--xg-dtype", choices=["bf16", "f32"], default="bf16",
+                   help="compute type of the cross-Gram sweep (the paper's ablation ran float32)")
     return p.parse_args()
 
 
@@ -352,7 +354,7 @@ def gpt2_case(dev, steps, warmup, check=True):
     return out
 
 
-def crossgram_case(dev, steps, warmup, T_list=None, route_names=None):
+def crossgram_case(dev, steps, warmup, T_list=None, route_names=None, dtype="bf16"):
     """Unprojected cross-Gram routing sweep (the paper's routing ablation over
     sequence length): 96 Pythia-410M-shaped layers, 8 training examples
     against 1 query, T in {32, 128, 512, 2048}, bf16.  Per T: both forced
@@ -366,7 +368,7 @@ def crossgram_case(dev, steps, warmup, T_list=None, route_names=None):
     wl = W.WORKLOADS["crossgram"]
     layers = wl["layers"]
     out = {"workload": f"{len(layers)} Pythia-410M-shaped linear layers, {wl['n_train']} train x "
-                       f"{wl['n_query']} query, bf16", "per_T": {}}
+                       f"{wl['n_query']} query, {dtype}", "per_T": {}}
 
     def med_ms(fn):
         for _ in range(warmup):
@@ -384,10 +386,10 @@ def crossgram_case(dev, steps, warmup, T_list=None, route_names=None):
     for T in (T_list or wl["T_sweep"]):
         sess = {}
         for side, n in (("train", wl["n_train"]), ("query", wl["n_query"])):
-            s = ProjectionSession(layers, dtype="bf16", seed=wl["seed"], device=dev)
+            s = ProjectionSession(layers, dtype=dtype, seed=wl["seed"], device=dev)
             for li, L in enumerate(layers):
-                A = W.draw((n, T, L["d_in"]), "normal", "bf16", dev, wl["seed"], "A", side, li, T)
-                B = W.draw((n, T, L["d_out"]), "normal", "bf16", dev, wl["seed"], "B", side, li, T)
+                A = W.draw((n, T, L["d_in"]), "normal", dtype, dev, wl["seed"], "A", side, li, T)
+                B = W.draw((n, T, L["d_out"]), "normal", dtype, dev, wl["seed"], "B", side, li, T)
                 s.capture(li, A, B)
             sess[side] = s
         a, b = sess["train"].ctx, sess["query"].ctx
@@ -403,9 +405,10 @@ def crossgram_case(dev, steps, warmup, T_list=None, route_names=None):
             res[name] = med_ms(lambda: dt.dattri_cross_gram(a, b, K, K.stride(0), ws, ws.numel(), route))
             del ws
         routes = [dt.dattri_cross_gram_route(a, b, li)[0] for li in range(len(layers))]
-        f_flops = sum(dt.dattri_cross_gram_costs(wl["n_train"], wl["n_query"], T, T, L["d_in"], L["d_out"], 2)[0]
+        elt = 2 if dtype == "bf16" else 4
+        f_flops = sum(dt.dattri_cross_gram_costs(wl["n_train"], wl["n_query"], T, T, L["d_in"], L["d_out"], elt)[0]
                       for L in layers)
-        m_flops = sum(dt.dattri_cross_gram_costs(wl["n_train"], wl["n_query"], T, T, L["d_in"], L["d_out"], 2)[1]
+        m_flops = sum(dt.dattri_cross_gram_costs(wl["n_train"], wl["n_query"], T, T, L["d_in"], L["d_out"], elt)[1]
                       for L in layers)
         best = min(res["factored"], res["materialized"])
         out["per_T"][str(T)] = {
@@ -415,7 +418,7 @@ def crossgram_case(dev, steps, warmup, T_list=None, route_names=None):
             "auto_regret": res["auto"] / best - 1.0,
             "factored_tflops": f_flops / (res["factored"] * 1e-3) / 1e12,
             "materialized_tflops": m_flops / (res["materialized"] * 1e-3) / 1e12}
-        print(f"[bench] crossgram T={T}: factored {res['factored']:.3f} ms, materialized "
+        print(f"[bench] crossgram {dtype} T={T}: factored {res['factored']:.3f} ms, materialized "
               f"{res['materialized']:.3f} ms, auto {res['auto']:.3f} ms", file=sys.stderr, flush=True)
         for s in sess.values():
             s.close()
@@ -813,7 +816,7 @@ def main():
         out["gpt2"] = gpt2_case(dev, max(args.steps, 5), args.warmup)
     if args.phase in ("all", "crossgram"):
         out["crossgram_routing"] = crossgram_case(dev, max(min(args.steps, 5), 3), min(args.warmup, 1), args.xg_T,
-                                                  args.xg_routes)
+                                                  args.xg_routes, args.xg_dtype)
     if args.phase in ("all", "curvature"):
         out["curvature"] = curvature_case(dev, max(min(args.steps, 5), 3), min(args.warmup, 1))
     if args.phase in ("all", "fit"):

@@ -50,6 +50,9 @@ constexpr int64_t kDotChunk = 16384;                      // floats per Frobeniu
 constexpr int64_t kOOBLimit = 0xFFFFFFF0LL;                // first byte offset a descriptor never covers
 constexpr int64_t kXOnePartsBudget = (int64_t)64 << 20;     // one-pass tile sums per launch (bytes)
 constexpr int64_t kXOneSlots = 2 * 256;                    // resident one-pass workgroups (2 per CU)
+constexpr int64_t kXOneMaxRun = 4;  // examples of batch a per one-pass workgroup, at most (measured:
+                                    // runs of 8 took 16.1 ms against 14.6-14.9 for 3-4 on the
+                                    // 96-layer T = 2048 sweep, though they issue 10% less work)
 
 inline int64_t r16(int64_t T) { return (T + 15) / 16 * 16; }
 inline int64_t cdiv(int64_t a, int64_t b) { return (a + b - 1) / b; }
@@ -73,9 +76,10 @@ XCounts xcounts(int64_t na, int64_t nb, int64_t Ta, int64_t Tb, int64_t di, int6
 // One-pass materialized launch over ci examples of batch a against cj of
 // batch b (diag: the ci examples against themselves): a workgroup forms one
 // 128 x 128 tile of DW_b[j] once, then the same tile of DW_a[i] for each of
-// its ipw examples.  nz = runs of batch a per (tile, j) is chosen to minimise
-// the predicted time: rounds of kXOneSlots workgroups, each round as long as
-// one workgroup's builds (ipw, plus the reference build unless diag).
+// its ipw <= kXOneMaxRun examples.  nz = runs of batch a per (tile, j) is
+// chosen to minimise the predicted time: rounds of kXOneSlots workgroups, each
+// round as long as one workgroup's builds (ipw, plus the reference build
+// unless diag).
 struct XOneShape {
   int nz = 1, ipw = 1;
   double us = 0.0;
@@ -95,7 +99,7 @@ XOneShape xone_shape(const dattri_crossgram_cost_model& m, int64_t tiles, int64_
   const double ta = per_token * (double)r32(Ta), tb = diag ? 0.0 : per_token * (double)r32(Tb);
   const int64_t ys = diag ? 1 : cj;
   const int64_t nz_max = std::min<int64_t>(ci, 65535);
-  for (int64_t nz = 1; nz <= nz_max; ++nz) {
+  for (int64_t nz = cdiv(ci, kXOneMaxRun); nz <= nz_max; ++nz) {
     const int64_t ipw = cdiv(ci, nz);
     if (cdiv(ci, ipw) != nz) continue;  // same runs as a smaller nz
     const int64_t rounds = cdiv(tiles * ys * nz, kXOneSlots);
@@ -196,6 +200,9 @@ struct XGroup { int e0, e1, t0, t1; int64_t parts_floats; };
 struct XPlan {
   std::vector<int> fact, mat;  // layer ids by route
   std::vector<char> one;       // per entry of mat: the one-pass form
+  std::vector<XOneEntry> xents;  // one-pass layers, all in one launch
+  std::vector<int32_t> xslot;    // entry of every one-pass workgroup slot
+  int xT1 = 0, xT2 = 0;        // longest sequences among them (run-length choice)
   int oa = 0, ob = 0;          // examples per one-pass launch (batch a, batch b)
   int64_t oparts = 0;          // floats of one-pass tile sums
   std::vector<GhostEntry> entries;
@@ -205,7 +212,8 @@ struct XPlan {
   int64_t D_max = 0, nchunks_max = 0;
   int ca = 0, cb = 0;          // examples of DW staged per chunk (batch a, batch b)
   bool reuse_g = false;        // a == b and both fit: DW built once
-  size_t off_entries = 0, off_tiles = 0, off_parts = 0, off_g1 = 0, off_g2 = 0, off_dparts = 0, off_oparts = 0;
+  size_t off_entries = 0, off_tiles = 0, off_xents = 0, off_xslots = 0, off_parts = 0, off_g1 = 0, off_g2 = 0,
+         off_dparts = 0, off_oparts = 0;
   size_t total = 0;
   size_t blob_entries = 0, blob_bytes = 0;
 };
@@ -291,22 +299,41 @@ dattri_status build_xplan(const dattri_ctx* a, const dattri_ctx* b, dattri_route
     }
   }
 
-  // materialized layers: one-pass where picked, else DW staged in HBM
-  int64_t otiles_max = 0;
+  // materialized layers: one-pass where picked (all in one launch: each layer
+  // owns its tiles' workgroup slots, rounded up to a multiple of 8 so every
+  // layer starts on XCD 0), else DW staged in HBM
   for (int l : P.mat) {
     const Layer &La = a->layers[l], &Lb = b->layers[l];
-    const bool one = xone_pick(a->xcost, La, Lb, elt, diag);
+    const bool one = xone_pick(a->xcost, La, Lb, elt, diag) && (int64_t)La.d_in * La.d_out > 0;
     P.one.push_back(one ? 1 : 0);
-    if (one)
-      otiles_max = std::max<int64_t>(otiles_max, cdiv(La.d_out, kXOneTile) * cdiv(La.d_in, kXOneTile));
-    else
+    if (!one) {
       P.D_max = std::max<int64_t>(P.D_max, (int64_t)La.d_in * La.d_out);
+      continue;
+    }
+    XOneEntry E;
+    std::memset(&E, 0, sizeof(E));
+    E.A1 = La.A; E.B1 = La.B; E.len1 = La.lengths;
+    E.A2 = Lb.A; E.B2 = Lb.B; E.len2 = Lb.lengths;
+    E.d_in = La.d_in; E.d_out = La.d_out; E.T1 = La.T; E.T2 = Lb.T;
+    E.n_ub = (int)cdiv(La.d_out, kXOneTile);
+    E.n_vt = (int)cdiv(La.d_in, kXOneTile);
+    const int64_t slots = cdiv((int64_t)E.n_ub * E.n_vt, 8) * 8;
+    if ((int64_t)P.xslot.size() + slots > INT32_MAX)
+      return fail(DATTRI_E_UNSUPPORTED, "layer %d: too many one-pass workgroups in one call", l);
+    E.slot0 = (int)P.xslot.size();
+    E.nslots = (int)slots;
+    P.xslot.insert(P.xslot.end(), (size_t)slots, (int32_t)P.xents.size());
+    P.xents.push_back(E);
+    P.xT1 = std::max(P.xT1, La.T);
+    P.xT2 = std::max(P.xT2, Lb.T);
   }
-  if (otiles_max > 0) {
-    const int64_t cap = std::max<int64_t>(1, kXOnePartsBudget / 4 / otiles_max);  // (i, j) cells per launch
+  if (!P.xslot.empty()) {
+    const int64_t n_slots = (int64_t)P.xslot.size();
+    const int64_t cap = std::max<int64_t>(1, kXOnePartsBudget / 4 / n_slots);  // (i, j) cells per launch
     P.ob = diag ? 0 : (int)std::min<int64_t>({(int64_t)nb, 65535, cap});
-    P.oa = (int)std::max<int64_t>(1, std::min<int64_t>(na, cap / std::max(1, P.ob)));
-    P.oparts = otiles_max * P.oa * std::max(1, P.ob);
+    P.oa = (int)std::max<int64_t>(1, std::min<int64_t>({(int64_t)na, cap / std::max(1, P.ob),
+                                                         65535 * kXOneMaxRun}));  // grid z <= 65535 runs
+    P.oparts = n_slots * P.oa * std::max(1, P.ob);
   }
   if (P.D_max > 0) {
     const int64_t per = P.D_max * 4;
@@ -330,6 +357,10 @@ dattri_status build_xplan(const dattri_ctx* a, const dattri_ctx* b, dattri_route
   off = align_up(off + P.entries.size() * sizeof(GhostEntry));
   P.off_tiles = off;
   off = align_up(off + P.tiles.size() * sizeof(GhostTile));
+  P.off_xents = off;
+  off = align_up(off + P.xents.size() * sizeof(XOneEntry));
+  P.off_xslots = off;
+  off = align_up(off + P.xslot.size() * sizeof(int32_t));
   P.blob_entries = P.off_tiles;
   P.blob_bytes = off;
   P.off_parts = off;
@@ -372,12 +403,16 @@ dattri_status run_xplan(dattri_ctx* a, dattri_ctx* b, const XPlan& P, bool diag,
   const int na = a->layers[0].n, nb = b->layers[0].n;
   const int rows = na, cols = diag ? 1 : nb;
   bool wrote = false;
-  if (!P.entries.empty()) {
+  uint8_t* tab = nullptr;
+  if (!P.entries.empty() || !P.xents.empty()) {
     std::vector<uint8_t> blob(P.blob_bytes, 0);
     std::memcpy(blob.data() + P.off_entries, P.entries.data(), P.entries.size() * sizeof(GhostEntry));
     std::memcpy(blob.data() + P.off_tiles, P.tiles.data(), P.tiles.size() * sizeof(GhostTile));
-    uint8_t* tab = nullptr;
+    std::memcpy(blob.data() + P.off_xents, P.xents.data(), P.xents.size() * sizeof(XOneEntry));
+    std::memcpy(blob.data() + P.off_xslots, P.xslot.data(), P.xslot.size() * sizeof(int32_t));
     HIP_TRY(place_table(a, kTabCross, blob, ws, s, &tab));
+  }
+  if (!P.entries.empty()) {
     const GhostEntry* d_entries = (const GhostEntry*)(tab + P.off_entries);
     const GhostTile* d_tiles = (const GhostTile*)(tab + P.off_tiles);
     float* parts = (float*)(ws + P.off_parts);
@@ -394,31 +429,28 @@ dattri_status run_xplan(dattri_ctx* a, dattri_ctx* b, const XPlan& P, bool diag,
   float* g2 = P.reuse_g ? g1 : (float*)(ws + P.off_g2);
   float* dparts = (float*)(ws + P.off_dparts);
   float* oparts = (float*)(ws + P.off_oparts);
+  if (!P.xents.empty()) {  // every one-pass layer: one launch per chunk of examples, then the tile sums
+    XOneArgs x;
+    x.entries = (const XOneEntry*)(tab + P.off_xents);
+    x.slot_entry = (const int32_t*)(tab + P.off_xslots);
+    x.n_slots = (int)P.xslot.size();
+    x.diag = diag ? 1 : 0;
+    x.parts = oparts;
+    for (int j0 = 0; j0 < (diag ? 1 : nb); j0 += std::max(1, P.ob)) {
+      const int cj = diag ? 0 : std::min(P.ob, nb - j0);
+      for (int i0 = 0; i0 < na; i0 += P.oa) {
+        const int ci = std::min(P.oa, na - i0);
+        const XOneShape sh = xone_shape(a->xcost, x.n_slots, ci, cj, P.xT1, P.xT2, diag);
+        x.i0 = i0; x.ci = ci; x.ipw = sh.ipw; x.j0 = j0; x.cj = cj;
+        HIP_TRY(launch_xone(x, s));
+        HIP_TRY(launch_kacc(oparts, x.n_slots, ci, diag ? ci : cj, K, ld, i0, j0, diag ? 1 : 0, 1, s));
+      }
+    }
+  }
   for (size_t m = 0; m < P.mat.size(); ++m) {
     const Layer &La = a->layers[P.mat[m]], &Lb = b->layers[P.mat[m]];
     const int64_t D = (int64_t)La.d_in * La.d_out;
-    if (D == 0) continue;
-    if (P.one[m]) {
-      XOneArgs x;
-      x.A1 = La.A; x.B1 = La.B; x.len1 = La.lengths;
-      x.A2 = Lb.A; x.B2 = Lb.B; x.len2 = Lb.lengths;
-      x.d_in = La.d_in; x.d_out = La.d_out; x.T1 = La.T; x.T2 = Lb.T;
-      x.diag = diag ? 1 : 0;
-      x.n_vt = (int)cdiv(La.d_in, kXOneTile);
-      x.parts = oparts;
-      const int64_t tiles = cdiv(La.d_out, kXOneTile) * x.n_vt;
-      for (int j0 = 0; j0 < (diag ? 1 : nb); j0 += std::max(1, P.ob)) {
-        const int cj = diag ? 0 : std::min(P.ob, nb - j0);
-        for (int i0 = 0; i0 < na; i0 += P.oa) {
-          const int ci = std::min(P.oa, na - i0);
-          const XOneShape sh = xone_shape(a->xcost, tiles, ci, cj, La.T, Lb.T, diag);
-          x.i0 = i0; x.ci = ci; x.ipw = sh.ipw; x.j0 = j0; x.cj = cj;
-          HIP_TRY(launch_xone(x, s));
-          HIP_TRY(launch_kacc(oparts, (int)tiles, ci, diag ? ci : cj, K, ld, i0, j0, diag ? 1 : 0, 1, s));
-        }
-      }
-      continue;
-    }
+    if (D == 0 || P.one[m]) continue;
     const int nchunks = (int)cdiv(D, kDotChunk);
     if (diag) {
       for (int i0 = 0; i0 < na; i0 += P.ca) {

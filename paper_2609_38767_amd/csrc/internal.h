@@ -217,19 +217,28 @@ hipError_t launch_ghost(int elt_bytes, const GhostEntry* entries, const GhostTil
 hipError_t launch_ghost_reduce(const GhostEntry* entries, int n_entries, const float* parts,
                                int n_rows, int n_cols, float* K, int64_t ld, int diag, int accumulate,
                                hipStream_t s);
-// One-pass materialized cross-Gram (bf16 blocks with 16-byte aligned rows):
-// grid (tiles of DW, examples j of batch b, runs of ipw examples of batch a);
-// parts[tile][i][j] (diag: parts[tile][i], the squared norms of batch a) =
-// sum over the 128 x 128 tile of DW_a[i0 + i] * DW_b[j0 + j].
+// One-pass materialized cross-Gram (bf16 blocks with 16-byte aligned rows),
+// every one-pass layer of a call in one launch.  Layer e owns the nslots =
+// (n_ub n_vt rounded up to 8) workgroup slots slot0 .. slot0 + nslots - 1 of
+// grid x; grid y = examples j of batch b, grid z = runs of ipw examples of
+// batch a.  parts[slot][i][j] (diag: parts[slot][i], the squared norms of
+// batch a) = sum over the slot's 128 x 128 tile of DW_a[i0 + i] * DW_b[j0 + j]
+// (0 for the padding slots).
 constexpr int kXOneTile = 128;
-struct XOneArgs {
+struct XOneEntry {
   const void *A1, *B1, *A2, *B2;  // batch a and b factor blocks [n, T, d]
   const int32_t *len1, *len2;     // per-example lengths or NULL
   int32_t d_in, d_out, T1, T2;
+  int32_t n_ub, n_vt;             // 128-row tiles of d_out, 128-column tiles of d_in
+  int32_t slot0, nslots;          // its workgroup slots (nslots a multiple of 8)
+};
+struct XOneArgs {
+  const XOneEntry* entries;
+  const int32_t* slot_entry;      // entry of every slot
+  int32_t n_slots;
   int32_t i0, ci, ipw;            // batch a examples i0 .. i0 + ci - 1, ipw per workgroup
   int32_t j0, cj;                 // batch b examples j0 .. j0 + cj - 1 (unused for diag)
   int32_t diag;
-  int32_t n_vt;                   // 128-column tiles of d_in
   float* parts;
 };
 hipError_t launch_xone(const XOneArgs& a, hipStream_t s);

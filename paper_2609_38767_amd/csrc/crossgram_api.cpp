@@ -24,18 +24,18 @@ dattri_crossgram_cost_model default_crossgram_cost_model() {
   // route, both forms of the materialized one and the gradient build timed on
   // 28 shapes (1024..4096-wide and 128-wide layers, T = 16..2048, 8 x 1,
   // 16 x 16 and 8 x 8 batches), each a stack of 24 layers so the factorized
-  // route runs as one grouped launch, and fitted by least squares on log
-  // time.  The two bandwidths come out far above HBM's: on this sweep the
-  // factor reads never bound those kernels.
+  // and one-pass routes run as one grouped launch each, and fitted by least
+  // squares on log time.  The two bandwidths come out far above HBM's: on
+  // this sweep the factor reads never bound those kernels.
   dattri_crossgram_cost_model m;
-  m.ghost_tflops = 599.6;  // on whole padded tiles
-  m.ghost_gbs = 56200.0;
-  m.ghost_layer_us = 2.52;
-  m.build_tflops = 769.2;  // on the tile builds of the build kernel's rounds
-  m.build_gbs = 7.22e6;
-  m.dot_gbs = 1286.0;
-  m.launch_us = 7.50;
-  m.onepass_tflops = 1134.8;  // on the tile builds the one-pass kernel issues
+  m.ghost_tflops = 658.3;  // on whole padded tiles
+  m.ghost_gbs = 5.45e6;
+  m.ghost_layer_us = 2.12;
+  m.build_tflops = 638.8;  // on the tile builds of the build kernel's rounds
+  m.build_gbs = 7.06e7;
+  m.dot_gbs = 1180.6;
+  m.launch_us = 4.83;
+  m.onepass_tflops = 1149.6;  // on the tile builds the one-pass kernel issues
   return m;
 }
 

@@ -275,8 +275,9 @@ struct MaskTask {
   int64_t partial_base;
 };
 struct MaskItem { int32_t task, example, chunk, group; };  // task < 0: padding
-// full: every item's group holds kMaskGroup entries
-hipError_t launch_mask(int elt_bytes, int aligned, int full, const MaskItem* items, int n_items,
+// full: every item's group holds kMaskGroup entries; b16: bf16 layers with
+// d_in, d_out <= 32768 only (entries as byte offsets, v_dot2_f32_bf16 gather)
+hipError_t launch_mask(int elt_bytes, int aligned, int full, int b16, const MaskItem* items, int n_items,
                        const MaskTask* tasks, size_t lds_bytes, float* partials, hipStream_t s);
 
 // ---------------------------------------------------------------- scoring

@@ -12,7 +12,8 @@
 // plain copy into one buffer.  Every thread owns 64 entries (each (r, c) pair
 // packed in one register) and adds b[r_e] * a[c_e] for each staged token, in
 // token order (deterministic); the products of bf16 values are exact in
-// float32.  Every group restages the chunk's token rows, so groups are made
+// float32 (bf16 layers up to 32768 wide take them through v_dot2_f32_bf16,
+// gather_rows_b16).  Every group restages the chunk's token rows, so groups are made
 // as large as two waves per SIMD allow: ten masks of 8192 entries take 5
 // groups instead of 10.  The entries come in the slot order of the layer's
 // table, arranged at bind time so that the 32 lanes of a half-wave mostly
@@ -93,7 +94,40 @@ __device__ __forceinline__ void gather_rows(const uint8_t* sa, const uint8_t* sb
   }
 }
 
-template <int ELT, bool AL, bool FULL>
+// The same for bf16 layers whose token rows are at most 64 KiB (both d <=
+// 32768): rc[j] holds the entry's byte offsets within a staged row, 2 r_j << 16
+// | 2 c_j, so each LDS address is one add of a 16-bit field (SDWA), and each
+// value is read zero-extended: as a bf16 pair (value, 0), v_dot2_f32_bf16
+// gives value_b * value_a + acc with the product exact and one rounding, the
+// same as the float32 FMA, with no conversion.  3 vector instructions per
+// multiply-add instead of 7.
+template <bool FULL>
+__device__ __forceinline__ void gather_rows_b16(const uint8_t* sa, const uint8_t* sb, int nt, int a_row, int b_row,
+                                                int nj, uint32_t (&rc)[kMaskPerThread],
+                                                float (&acc)[kMaskPerThread]) {
+  typedef __attribute__((address_space(3))) uint8_t lds_u8;
+  typedef __attribute__((address_space(3))) uint16_t lds_u16;
+  typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+  const uint32_t a0 = (uint32_t)(uintptr_t)(lds_u8*)sa, b0 = (uint32_t)(uintptr_t)(lds_u8*)sb;
+  for (int t = 0; t < nt; ++t) {
+    const uint32_t ar = a0 + (uint32_t)(t * a_row), br = b0 + (uint32_t)(t * b_row);
+#pragma unroll
+    for (int jb = 0; jb < kMaskPerThread; jb += 8) {
+      if (FULL || jb < nj) {
+#pragma unroll
+        for (int j = jb; j < jb + 8; ++j) {
+          asm volatile("" : "+v"(rc[j]));  // as in gather_rows: no unpacked offsets held across tokens
+          const uint32_t vb = *(const lds_u16*)(uintptr_t)(br + (rc[j] >> 16));
+          const uint32_t va = *(const lds_u16*)(uintptr_t)(ar + (rc[j] & 0xFFFFu));
+          acc[j] = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, vb), __builtin_bit_cast(bf16x2, va),
+                                                   acc[j], false);
+        }
+      }
+    }
+  }
+}
+
+template <int ELT, bool AL, bool FULL, bool B16>
 __global__ __launch_bounds__(256, 2) void mask_kernel(const MaskItem* __restrict__ items,
                                                    const MaskTask* __restrict__ tasks,
                                                    float* __restrict__ partials) {
@@ -108,13 +142,16 @@ __global__ __launch_bounds__(256, 2) void mask_kernel(const MaskItem* __restrict
   const int e0 = it.group * kMaskGroup, ne = min(kMaskGroup, M.m - e0);
   const int nj = (ne + 255) / 256;  // slots per thread holding entries (uniform)
   // entry (r, c) packed as r << 16 | c (both below 2^16: a staged token row
-  // of A and B fits in LDS)
+  // of A and B fits in LDS); B16 (bf16 rows of at most 64 KiB): as byte
+  // offsets 2 r << 16 | 2 c
+  static_assert(!B16 || ELT == 2, "byte-offset gather is bf16 only");
+  constexpr uint32_t sh = B16 ? 1u : 0u;
   uint32_t rc[kMaskPerThread];
   float acc[kMaskPerThread];
 #pragma unroll
   for (int j = 0; j < kMaskPerThread; ++j) {
     const int e = tid + 256 * j;
-    rc[j] = e < ne ? ((uint32_t)M.rows[e0 + e] << 16) | (uint32_t)M.cols[e0 + e] : 0u;
+    rc[j] = e < ne ? ((uint32_t)M.rows[e0 + e] << (16 + sh)) | ((uint32_t)M.cols[e0 + e] << sh) : 0u;
     acc[j] = 0.f;
   }
   const int TS = M.stage_tokens;
@@ -123,7 +160,10 @@ __global__ __launch_bounds__(256, 2) void mask_kernel(const MaskItem* __restrict
   const uint8_t* gb = (const uint8_t*)M.B + ((int64_t)ex * M.T) * b_row;
 
   auto gather = [&](const uint8_t* sa, const uint8_t* sb, int nt) {
-    gather_rows<ELT, FULL>(sa, sb, nt, a_row, b_row, nj, rc, acc);
+    if constexpr (B16)
+      gather_rows_b16<FULL>(sa, sb, nt, a_row, b_row, nj, rc, acc);
+    else
+      gather_rows<ELT, FULL>(sa, sb, nt, a_row, b_row, nj, rc, acc);
   };
 
   if (AL) {
@@ -166,33 +206,37 @@ __global__ __launch_bounds__(256, 2) void mask_kernel(const MaskItem* __restrict
     if (tid + 256 * j < ne) dst[M.pos[e0 + tid + 256 * j]] = acc[j];
 }
 
-template <int ELT, bool AL, bool FULL>
+template <int ELT, bool AL, bool FULL, bool B16>
 static hipError_t launch_mask_t(const MaskItem* items, int n_items, const MaskTask* tasks, size_t lds_bytes,
                                 float* partials, hipStream_t s) {
   if (lds_bytes > 64 * 1024) {  // dynamic LDS beyond 64 KiB must be allowed per kernel
-    const hipError_t e = hipFuncSetAttribute((const void*)mask_kernel<ELT, AL, FULL>,
+    const hipError_t e = hipFuncSetAttribute((const void*)mask_kernel<ELT, AL, FULL, B16>,
                                              hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds_bytes);
     if (e != hipSuccess) return e;
   }
-  hipLaunchKernelGGL((mask_kernel<ELT, AL, FULL>), dim3((unsigned)n_items), dim3(256), lds_bytes, s, items, tasks,
-                     partials);
+  hipLaunchKernelGGL((mask_kernel<ELT, AL, FULL, B16>), dim3((unsigned)n_items), dim3(256), lds_bytes, s, items,
+                     tasks, partials);
   return hipGetLastError();
 }
 
-hipError_t launch_mask(int elt, int aligned, int full, const MaskItem* items, int n_items, const MaskTask* tasks,
-                       size_t lds_bytes, float* partials, hipStream_t s) {
+hipError_t launch_mask(int elt, int aligned, int full, int b16, const MaskItem* items, int n_items,
+                       const MaskTask* tasks, size_t lds_bytes, float* partials, hipStream_t s) {
   if (n_items <= 0) return hipSuccess;
-#define DATTRI_MASK_CASE(E, A, F) \
-  if (elt == E && (bool)aligned == A && (bool)full == F) \
-    return launch_mask_t<E, A, F>(items, n_items, tasks, lds_bytes, partials, s);
-  DATTRI_MASK_CASE(2, true, true)
-  DATTRI_MASK_CASE(2, true, false)
-  DATTRI_MASK_CASE(2, false, true)
-  DATTRI_MASK_CASE(2, false, false)
-  DATTRI_MASK_CASE(4, true, true)
-  DATTRI_MASK_CASE(4, true, false)
-  DATTRI_MASK_CASE(4, false, true)
-  DATTRI_MASK_CASE(4, false, false)
+#define DATTRI_MASK_CASE(E, A, F, B) \
+  if (elt == E && (bool)aligned == A && (bool)full == F && (bool)b16 == B) \
+    return launch_mask_t<E, A, F, B>(items, n_items, tasks, lds_bytes, partials, s);
+  DATTRI_MASK_CASE(2, true, true, true)
+  DATTRI_MASK_CASE(2, true, false, true)
+  DATTRI_MASK_CASE(2, false, true, true)
+  DATTRI_MASK_CASE(2, false, false, true)
+  DATTRI_MASK_CASE(2, true, true, false)
+  DATTRI_MASK_CASE(2, true, false, false)
+  DATTRI_MASK_CASE(2, false, true, false)
+  DATTRI_MASK_CASE(2, false, false, false)
+  DATTRI_MASK_CASE(4, true, true, false)
+  DATTRI_MASK_CASE(4, true, false, false)
+  DATTRI_MASK_CASE(4, false, true, false)
+  DATTRI_MASK_CASE(4, false, false, false)
 #undef DATTRI_MASK_CASE
   return hipErrorInvalidValue;
 }

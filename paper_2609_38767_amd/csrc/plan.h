@@ -56,6 +56,7 @@ struct Plan {
   std::vector<ReduceTask> mreduce;
   int mask_max_out = 0;
   size_t mask_lds = 0;
+  bool mask_b16 = true;  // every mask layer bf16 with d_in, d_out <= 32768 (byte-offset gather)
   // projected token rows kept for the curvature fit (rows = true)
   bool rows = false;
   std::vector<size_t> member_rows;  // per fused member: byte offsets of its A rows, B rows (pairs)

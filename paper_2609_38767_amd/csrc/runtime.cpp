@@ -827,6 +827,7 @@ dattri_status dattri::build_plan(const dattri_ctx* ctx, dattri_route forced, Pla
       const int64_t b_part = ((int64_t)M.stage_tokens * L.d_out * elt + 1023) & ~(int64_t)1023;
       const size_t lds = (size_t)(M.aligned ? 2 * (a_part + b_part) : a_part + b_part);
       P.mask_lds = std::max(P.mask_lds, lds);
+      P.mask_b16 = P.mask_b16 && elt == 2 && L.d_in <= 32768 && L.d_out <= 32768;
       ReduceTask R;
       std::memset(&R, 0, sizeof(R));
       R.partial_base = M.partial_base;
@@ -1201,7 +1202,8 @@ dattri_status dattri::run_plan(dattri_ctx* ctx, const Plan& P, void* phi, dattri
   if (!P.mtasks.empty()) {
     float* kpart = (float*)(ws + P.off_maskpart);
     for (const Plan::MaskLaunch& L : P.mlaunches)
-      HIP_TRY(launch_mask(ctx->elt, L.aligned, L.full, (const MaskItem*)(tab + P.off_mitems) + L.first, L.count,
+      HIP_TRY(launch_mask(ctx->elt, L.aligned, L.full, P.mask_b16 ? 1 : 0,
+                          (const MaskItem*)(tab + P.off_mitems) + L.first, L.count,
                           (const MaskTask*)(tab + P.off_mtasks), P.mask_lds, kpart, s));
     HIP_TRY(launch_reduce((const ReduceTask*)(tab + P.off_mreduce), (int)P.mreduce.size(), n, P.mask_max_out,
                           kpart, phi, phi_bf16, ld_phi, s));

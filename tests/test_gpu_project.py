@@ -255,6 +255,33 @@ def test_mask_layers(dtype, route):
         assert e <= 1e-5, (li, e)
 
 
+def test_mask_layer_wider_than_byte_offsets():
+    # a bf16 mask layer with d_out = 33000 (its rows' byte offsets do not fit
+    # 16 bits): the call's gather keeps element indices and float32 FMA for
+    # every mask layer, the narrow one beside it included
+    from oracle import mask as om
+    layers = [dict(name="w", d_in=40, d_out=33000, k_in=1, k_out=5000, mask_size=5000, mask_id=0, a_group="wa"),
+              dict(name="n", d_in=64, d_out=48, k_in=1, k_out=700, mask_size=700, mask_id=0, a_group="wb")]
+    wl = dict(W.WORKLOADS["tiny"], dist_a="normal", dist_b="normal", seed=33)
+    n, T = 2, 40
+    inputs = _session_inputs(wl, layers, n, T, "bf16")
+    lengths = torch.tensor([40, 23], dtype=torch.int32, device=DEV)
+    s = ProjectionSession(layers, dtype="bf16", seed=43)
+    for li, (A, B) in enumerate(inputs):
+        s.capture(li, A, B, lengths)
+    phi = s.project(n)
+    torch.cuda.synchronize()
+    got = host64(phi)
+    lens = lengths.cpu().numpy()
+    for li, L in enumerate(layers):
+        A, B = host64(inputs[li][0]), host64(inputs[li][1])
+        rows, cols = om.mask_indices(43, li, L["d_in"], L["d_out"], L["mask_size"], L["mask_id"])
+        ref = np.stack([om.masked_gradient(A[i], B[i], rows, cols, int(lens[i])) for i in range(n)])
+        off = s.offsets[li]
+        e = rel_fro(got[:, off:off + L["k_out"]], ref)
+        assert e <= 1e-5, (li, e)
+
+
 @pytest.mark.parametrize("form", ["fused", "split"])
 def test_shared_input_group_matches_separate_inputs(form):
     # 16-wide maps: q and k share one fused work item (2 input tiles keep 4 row

@@ -183,3 +183,35 @@ def test_one_pass_runs_and_launch_chunks():
         assert rel_fro(host64(nrm), ocg.sq_norms(oa)) <= 2e-5, dims
         sa.close()
         sb.close()
+
+
+def test_one_pass_layers_of_different_lengths():
+    # the layers of one call captured with different T (each layer's entry of
+    # the grouped one-pass launch carries its own): 37 and 70 tokens on the
+    # training side, 21 and 45 on the query side, ragged lengths
+    specs = [((64, 136), 37, 21), ((128, 40), 70, 45)]
+    ga, gb = torch.Generator(device=DEV).manual_seed(14), torch.Generator(device=DEV).manual_seed(15)
+    la = torch.tensor([37, 5, 0, 30], dtype=torch.int32, device=DEV)
+    lb = torch.tensor([21, 11], dtype=torch.int32, device=DEV)
+    layers = [dict(d_in=d_in, d_out=d_out, k_in=1, k_out=1) for (d_in, d_out), _, _ in specs]
+    sa = ProjectionSession(layers, dtype="bf16", seed=0, device=DEV)
+    sb = ProjectionSession(layers, dtype="bf16", seed=0, device=DEV)
+    oa, ob = [], []
+    for li, ((d_in, d_out), Ta, Tb) in enumerate(specs):
+        A1 = torch.randn((4, Ta, d_in), generator=ga, device=DEV).to(torch.bfloat16)
+        B1 = torch.randn((4, Ta, d_out), generator=ga, device=DEV).to(torch.bfloat16)
+        A2 = torch.randn((2, Tb, d_in), generator=gb, device=DEV).to(torch.bfloat16)
+        B2 = torch.randn((2, Tb, d_out), generator=gb, device=DEV).to(torch.bfloat16)
+        # each layer's lengths are its own (clipped to its T)
+        l1 = torch.clamp(la, max=Ta).contiguous()
+        l2 = torch.clamp(lb, max=Tb).contiguous()
+        sa.capture(li, A1, B1, l1)
+        sb.capture(li, A2, B2, l2)
+        oa.append((host64(A1), host64(B1), l1.cpu().numpy()))
+        ob.append((host64(A2), host64(B2), l2.cpu().numpy()))
+    _force(sa, "one-pass")
+    K = cross_gram(sa, sb, dt.DATTRI_ROUTE_MATERIALIZED)
+    nrm = sq_norms(sa, dt.DATTRI_ROUTE_MATERIALIZED)
+    torch.cuda.synchronize()
+    assert rel_fro(host64(K), ocg.cross_gram(oa, ob)) <= 1e-5
+    assert rel_fro(host64(nrm), ocg.sq_norms(oa)) <= 1e-5

@@ -439,9 +439,10 @@ dattri_status dattri_layer_route(const dattri_ctx* ctx, int32_t layer, dattri_ro
  *                 build_tflops / 512;
  *                 one-pass (bf16 blocks with 16-byte aligned rows only): no DW
  *                 in memory, a workgroup forms one 128 x 128 tile of DW_b[j]
- *                 and then the same tile of DW_a[i] for each of a run of ipw
- *                 examples, summing their products; predicted as rounds of 512
- *                 workgroups, each round ipw + 1 tile builds of
+ *                 and then the same tile of DW_a[i] for each of a run of
+ *                 ipw <= 4 examples, summing their products (all one-pass
+ *                 layers of a call share one launch); predicted per layer as
+ *                 rounds of 512 workgroups, each round ipw + 1 tile builds of
  *                 2 * 128^2 * T (T rounded up to 32) FLOP at onepass_tflops / 512,
  *                 plus 2 launch_us,
  * with build and product counts as in dattri_cross_gram_costs.  For the squared

@@ -49,6 +49,7 @@ FIELDS = ["ghost_tflops", "ghost_gbs", "ghost_layer_us", "build_tflops", "build_
           "launch_us", "onepass_tflops"]
 TILE = 128
 SLOTS = 512  # resident one-pass workgroups
+MAX_RUN = 4  # examples of batch a per one-pass workgroup, at most
 LAYERS = 24
 
 
@@ -112,11 +113,12 @@ def _r32(T):
 
 
 def onepass_us(model, tiles, na, nb, T):
-    """Predicted one-pass time (without launches): the run length with the
-    fewest rounds of SLOTS workgroups times the workgroup's tile builds."""
+    """Predicted one-pass time (without launches): the run length (at most
+    MAX_RUN examples) with the fewest rounds of SLOTS workgroups times the
+    workgroup's tile builds."""
     per = 2.0 * TILE * TILE * _r32(T) / (model["onepass_tflops"] * 1e6 / SLOTS)
     best = math.inf
-    for nz in range(1, na + 1):
+    for nz in range(-(-na // MAX_RUN), na + 1):
         ipw = -(-na // nz)
         if -(-na // ipw) != nz:
             continue

@@ -29,13 +29,13 @@ dattri_crossgram_cost_model default_crossgram_cost_model() {
   // this sweep the factor reads never bound those kernels.
   dattri_crossgram_cost_model m;
   m.ghost_tflops = 658.3;  // on whole padded tiles
-  m.ghost_gbs = 5.45e6;
+  m.ghost_gbs = 6.56e6;
   m.ghost_layer_us = 2.12;
-  m.build_tflops = 638.8;  // on the tile builds of the build kernel's rounds
-  m.build_gbs = 7.06e7;
-  m.dot_gbs = 1180.6;
-  m.launch_us = 4.83;
-  m.onepass_tflops = 1149.6;  // on the tile builds the one-pass kernel issues
+  m.build_tflops = 638.0;  // on the tile builds of the build kernel's rounds
+  m.build_gbs = 1.17e8;
+  m.dot_gbs = 1180.0;
+  m.launch_us = 4.81;
+  m.onepass_tflops = 1174.7;  // on the tile builds the one-pass kernel issues
   return m;
 }
 

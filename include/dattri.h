@@ -146,10 +146,11 @@ dattri_status dattri_register_layer(dattri_ctx* ctx, int32_t d_in, int32_t d_out
  * (AdamW-influence uses ten of 512 or 8192 entries, App. B).  Such a layer is
  * always projected by the gather kernel (route DATTRI_ROUTE_MASK, whatever
  * route is requested); its "maps" are the entry table (dattri_projection_bytes
- * gives its size in bytes_in, 12 bytes per entry, 0 in bytes_out;
- * dattri_bind_projection uploads it into dev_P_in, dev_P_out may be NULL,
- * overrides are refused).  The table is the library's own: the entries in the
- * gather kernel's slot order with their positions in mask order.
+ * gives its size in bytes_in, 12 bytes per entry plus 16 per group of 16384
+ * entries, 0 in bytes_out; dattri_bind_projection uploads it into dev_P_in,
+ * dev_P_out may be NULL, overrides are refused).  The table is the library's
+ * own: the entries in the gather kernel's slot order with their positions in
+ * mask order, and per group the part of each token row that it reads.
  * dattri_layer_dims reports k_in = 1, k_out = mask_size * mask_count.
  * Curvature calls reject mask layers.
  * Errors: INVALID_ARG (NULL pointers, sizes outside [1, 2^20], mask_size or

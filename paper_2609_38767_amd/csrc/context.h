@@ -37,6 +37,7 @@ struct Layer {
   // mask layer when mask_size > 0: masks mask_id .. mask_id + mask_count - 1 of
   // mask_size entries each, back to back (k_in = 1, k_out = mask_size * mask_count)
   int32_t mask_size = 0, mask_id = 0, mask_count = 0;
+  std::vector<int32_t> mask_slices;  // bound mask layer: the entry groups' row slices (as in its table)
   std::vector<float> override_in, override_out;  // rounded values when overridden
   const void* A = nullptr;  // captured [n, T, d_in]
   const void* B = nullptr;  // captured [n, T, d_out]

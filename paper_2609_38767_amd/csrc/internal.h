@@ -264,14 +264,23 @@ hipError_t launch_fill_rows(float* K, int rows, int cols, int64_t ld, hipStream_
 constexpr int kMaskPerThread = 64;
 constexpr int kMaskGroup = 256 * kMaskPerThread;   // entries per work item
 constexpr int64_t kMaskStageBudget = 40 * 1024;   // bytes of one stage (two stages per work item)
+// Fixed-slot gather (bf16, 16-byte rows, whole groups whose A and B slices are
+// at most kMaskSlot bytes): every stage holds kMaskSlotTokens tokens, each
+// slice in a slot of its own at a fixed offset, so token and buffer offsets
+// are instruction immediates.  LDS: 2 buffers of [A slots | B slots].
+constexpr int kMaskSlot = 8192;
+constexpr int kMaskSlotTokens = 2;
+constexpr size_t kMaskSlotLds = (size_t)2 * 2 * kMaskSlotTokens * kMaskSlot;
 struct MaskTask {
   const void* A; const void* B;      // [n, T, d_in], [n, T, d_out]
   const int32_t* lengths;            // [n] or null
   const int32_t* rows;               // [m] output feature of the entry in each slot
   const int32_t* cols;               // [m] input feature of the entry in each slot
   const int32_t* pos;                // [m] index of that entry in mask order
+  const int32_t* slices;             // [4 per group] A slice (first byte, bytes), B slice (first byte, bytes)
   int32_t d_in, d_out, T, m;
   int32_t stage_tokens, chunk_tokens, n_chunks, aligned;  // aligned: 16-byte row blocks
+  int32_t fixed, pad0;               // whole groups take the fixed-slot gather
   int64_t partial_base;
 };
 struct MaskItem { int32_t task, example, chunk, group; };  // task < 0: padding
@@ -279,6 +288,9 @@ struct MaskItem { int32_t task, example, chunk, group; };  // task < 0: padding
 // d_in, d_out <= 32768 only (entries as byte offsets, v_dot2_f32_bf16 gather)
 hipError_t launch_mask(int elt_bytes, int aligned, int full, int b16, const MaskItem* items, int n_items,
                        const MaskTask* tasks, size_t lds_bytes, float* partials, hipStream_t s);
+// whole groups of fixed-slot tasks (bf16, aligned), kMaskSlotLds bytes of LDS
+hipError_t launch_mask_fixed(const MaskItem* items, int n_items, const MaskTask* tasks, float* partials,
+                             hipStream_t s);
 
 // ---------------------------------------------------------------- scoring
 // dst rows ld_dst apart receive src rows (ld_src apart) times d, first F columns

@@ -4,18 +4,21 @@
 // formed).
 //
 // One workgroup per (mask layer, example, token chunk, group of up to
-// kMaskGroup = 16384 entries).  Each stage holds `stage_tokens` consecutive
-// token rows of A and of B: consecutive rows of an example are one contiguous
-// block in HBM, so for 16-byte rows the stage is moved by direct global-to-LDS
-// loads (1 KiB per wave instruction, no registers) into one of two buffers
-// while the other is gathered; rows that are not 16-byte multiples take a
-// plain copy into one buffer.  Every thread owns 64 entries (each (r, c) pair
+// kMaskGroup = 16384 entries).  Each stage holds consecutive token rows of A
+// and of B.  For 16-byte rows it holds, of each row, only the 16-byte-aligned
+// slice that covers the group's entries (a layer's entries are dealt to its
+// groups in order along the wider side of DW, so a group of a layer with g
+// groups stages about 1/g of that side), packed densely so that more tokens
+// fit a stage; the slices are moved by direct global-to-LDS loads (1 KiB per
+// wave instruction, no registers) into one of two buffers while the other is
+// gathered.  Rows that are not 16-byte multiples take a plain copy of whole
+// rows into one buffer.  Every thread owns 64 entries (each (r, c) pair
 // packed in one register) and adds b[r_e] * a[c_e] for each staged token, in
 // token order (deterministic); the products of bf16 values are exact in
 // float32 (bf16 layers up to 32768 wide take them through v_dot2_f32_bf16,
-// gather_rows_b16).  Every group restages the chunk's token rows, so groups are made
-// as large as two waves per SIMD allow: ten masks of 8192 entries take 5
-// groups instead of 10.  The entries come in the slot order of the layer's
+// gather_rows_b16).  Every group restages the narrow side's token rows, so
+// groups are made as large as two waves per SIMD allow: ten masks of 8192
+// entries take 5 groups instead of 10.  The entries come in the slot order of the layer's
 // table, arranged at bind time so that the 32 lanes of a half-wave mostly
 // read distinct LDS banks, and each sum is written at the entry's position in
 // mask order.  Whole groups and the partial last group of a layer run in
@@ -56,7 +59,7 @@ __device__ inline void wait_vm0() {  // vmcnt(0), other counters untouched
   __builtin_amdgcn_s_waitcnt((0x7 << 4) | (0xF << 8));
 }
 
-// Direct global-to-LDS copy of `bytes` (a whole stage part, 16-byte aligned)
+// Direct global-to-LDS copy of `bytes` (whole token rows, 16-byte aligned)
 // from byte offset `off` of descriptor r into dst: one 1 KiB chunk per wave
 // instruction, lane l moving bytes 16 l .. 16 l + 15 of its chunk; chunks are
 // dealt to the 4 waves in turn.  Bytes past the descriptor's range land as
@@ -65,6 +68,24 @@ __device__ inline void dma_block(const rsrc_t r, uint32_t off, int bytes, uint8_
   const int chunks = (bytes + 1023) >> 10;
   for (int c = wave; c < chunks; c += 4)
     __builtin_amdgcn_raw_ptr_buffer_load_lds(r, LDS_PTR(dst + c * 1024), 16, off + c * 1024 + lane * 16, 0, 0, 0);
+}
+
+// Direct copy of the byte slice [s0, s0 + seg) of nt consecutive token rows
+// (row bytes apart, from token ts) into dst as [nt][seg], seg a multiple of 16:
+// 16-byte chunk i of that image is token i / n16, chunk i % n16 (n16 = seg /
+// 16; the quotient is the high word of i * magic, magic = ceil(2^32 / n16),
+// exact for i < 2^17 and n16 < 2^13).  One 1 KiB run of chunks per wave
+// instruction, dealt to the 4 waves in turn; chunks past the image land as
+// zero, so dst needs room for nt * seg rounded up to 1 KiB.
+__device__ inline void dma_slices(const rsrc_t r, int ts, int nt, int row, int s0, int seg, uint32_t magic,
+                                  uint8_t* dst, int wave, int lane) {
+  const int n16 = seg >> 4, total = nt * n16, runs = (total + 63) >> 6;
+  for (int c = wave; c < runs; c += 4) {
+    const int i = c * 64 + lane;
+    const int u = n16 == 1 ? i : (int)__umulhi((uint32_t)i, magic);
+    const uint32_t off = i < total ? (uint32_t)((ts + u) * row + s0 + 16 * (i - u * n16)) : kOOB;
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(r, LDS_PTR(dst + c * 1024), 16, off, 0, 0, 0);
+  }
 }
 
 // acc[j] += b[r_j] * a[c_j] over the nt staged token rows (token order);
@@ -146,39 +167,60 @@ __global__ __launch_bounds__(256, 2) void mask_kernel(const MaskItem* __restrict
   // offsets 2 r << 16 | 2 c
   static_assert(!B16 || ELT == 2, "byte-offset gather is bf16 only");
   constexpr uint32_t sh = B16 ? 1u : 0u;
+  const int a_row = M.d_in * ELT, b_row = M.d_out * ELT;
+  const uint8_t* ga = (const uint8_t*)M.A + ((int64_t)ex * M.T) * a_row;
+  const uint8_t* gb = (const uint8_t*)M.B + ((int64_t)ex * M.T) * b_row;
+  // Aligned rows: the staged part of each token row is the group's slice
+  // from the table (16-byte aligned, covering its columns c of A and rows r
+  // of B); entries address the slices.  Else whole rows.
+  int sa0 = 0, sb0 = 0, seg_a = a_row, seg_b = b_row;
+  if (AL) {
+    const int32_t* sl = M.slices + 4 * it.group;
+    sa0 = sl[0]; seg_a = sl[1]; sb0 = sl[2]; seg_b = sl[3];
+  }
+  const uint32_t rb = (uint32_t)(sb0 / ELT), cb = (uint32_t)(sa0 / ELT);
   uint32_t rc[kMaskPerThread];
   float acc[kMaskPerThread];
 #pragma unroll
   for (int j = 0; j < kMaskPerThread; ++j) {
     const int e = tid + 256 * j;
-    rc[j] = e < ne ? ((uint32_t)M.rows[e0 + e] << (16 + sh)) | ((uint32_t)M.cols[e0 + e] << sh) : 0u;
+    rc[j] = e < ne ? (((uint32_t)M.rows[e0 + e] - rb) << (16 + sh)) | (((uint32_t)M.cols[e0 + e] - cb) << sh) : 0u;
     acc[j] = 0.f;
   }
-  const int TS = M.stage_tokens;
-  const int a_row = M.d_in * ELT, b_row = M.d_out * ELT;
-  const uint8_t* ga = (const uint8_t*)M.A + ((int64_t)ex * M.T) * a_row;
-  const uint8_t* gb = (const uint8_t*)M.B + ((int64_t)ex * M.T) * b_row;
 
-  auto gather = [&](const uint8_t* sa, const uint8_t* sb, int nt) {
+  auto gather = [&](const uint8_t* sa, const uint8_t* sb, int nt, int a_stride, int b_stride) {
     if constexpr (B16)
-      gather_rows_b16<FULL>(sa, sb, nt, a_row, b_row, nj, rc, acc);
+      gather_rows_b16<FULL>(sa, sb, nt, a_stride, b_stride, nj, rc, acc);
     else
-      gather_rows<ELT, FULL>(sa, sb, nt, a_row, b_row, nj, rc, acc);
+      gather_rows<ELT, FULL>(sa, sb, nt, a_stride, b_stride, nj, rc, acc);
   };
 
   if (AL) {
-    // two stage buffers, each [A rows | B rows], parts rounded up to 1 KiB
-    const int a_part = (TS * a_row + 1023) & ~1023, b_part = (TS * b_row + 1023) & ~1023;
-    const int buf = a_part + b_part;
+    // two stage buffers of the planned size (stage_tokens whole rows, each
+    // part rounded up to 1 KiB); each holds [A slices | B slices] of as many
+    // tokens as fit (at least stage_tokens, at most 16)
+    const int buf = ((M.stage_tokens * a_row + 1023) & ~1023) + ((M.stage_tokens * b_row + 1023) & ~1023);
+    auto fits = [&](int t) { return ((t * seg_a + 1023) & ~1023) + ((t * seg_b + 1023) & ~1023) <= buf; };
+    int TS = M.stage_tokens;
+    while (TS < 16 && fits(TS + 1)) ++TS;
+    const int a_part = (TS * seg_a + 1023) & ~1023;
+    const uint32_t mag_a = (uint32_t)(0xFFFFFFFFu / (uint32_t)(seg_a >> 4)) + 1u;
+    const uint32_t mag_b = (uint32_t)(0xFFFFFFFFu / (uint32_t)(seg_b >> 4)) + 1u;
     // descriptors end at row t1: rows past the chunk land as zero
     const rsrc_t r_a = make_rsrc(ga, (uint32_t)((int64_t)t1 * a_row));
     const rsrc_t r_b = make_rsrc(gb, (uint32_t)((int64_t)t1 * b_row));
     const int n_st = t1 > t0 ? (t1 - t0 + TS - 1) / TS : 0;
+    const bool whole = seg_a == a_row && seg_b == b_row;  // uniform: contiguous stages
     auto issue = [&](int st) {
       const int ts = t0 + st * TS, nt = min(TS, t1 - ts);
       uint8_t* sa = stage + (st & 1) * buf;
-      dma_block(r_a, (uint32_t)(ts * a_row), nt * a_row, sa, wave, lane);
-      dma_block(r_b, (uint32_t)(ts * b_row), nt * b_row, sa + a_part, wave, lane);
+      if (whole) {
+        dma_block(r_a, (uint32_t)(ts * a_row), nt * a_row, sa, wave, lane);
+        dma_block(r_b, (uint32_t)(ts * b_row), nt * b_row, sa + a_part, wave, lane);
+      } else {
+        dma_slices(r_a, ts, nt, a_row, sa0, seg_a, mag_a, sa, wave, lane);
+        dma_slices(r_b, ts, nt, b_row, sb0, seg_b, mag_b, sa + a_part, wave, lane);
+      }
     };
     if (n_st > 0) issue(0);
     for (int st = 0; st < n_st; ++st) {  // uniform trip count
@@ -186,9 +228,10 @@ __global__ __launch_bounds__(256, 2) void mask_kernel(const MaskItem* __restrict
       __syncthreads();   // every wave's have; the other buffer's readers are done
       if (st + 1 < n_st) issue(st + 1);
       const uint8_t* sa = stage + (st & 1) * buf;
-      gather(sa, sa + a_part, min(TS, t1 - (t0 + st * TS)));
+      gather(sa, sa + a_part, min(TS, t1 - (t0 + st * TS)), seg_a, seg_b);
     }
   } else {
+    const int TS = M.stage_tokens;
     uint8_t* sa = stage;
     uint8_t* sb = stage + (((int64_t)TS * a_row + 15) & ~(int64_t)15);
     for (int ts = t0; ts < t1; ts += TS) {  // uniform trip count
@@ -197,13 +240,133 @@ __global__ __launch_bounds__(256, 2) void mask_kernel(const MaskItem* __restrict
       copy_rows<ELT, false>(sa, ga + (int64_t)ts * a_row, (int64_t)nt * a_row);
       copy_rows<ELT, false>(sb, gb + (int64_t)ts * b_row, (int64_t)nt * b_row);
       __syncthreads();
-      gather(sa, sb, nt);
+      gather(sa, sb, nt, a_row, b_row);
     }
   }
   float* dst = partials + M.partial_base + ((int64_t)ex * M.n_chunks + it.chunk) * M.m;
 #pragma unroll
   for (int j = 0; j < kMaskPerThread; ++j)
     if (tid + 256 * j < ne) dst[M.pos[e0 + tid + 256 * j]] = acc[j];
+}
+
+// Fixed-slot gather: whole groups of bf16 layers with 16-byte rows whose
+// slices fit kMaskSlot bytes.  Stage buffer p (of 2) at p * kFixBuf holds, of
+// each of its kMaskSlotTokens tokens u, the A slice in slot u and the B slice
+// in slot kMaskSlotTokens + u (kMaskSlot bytes each).  Every entry keeps its
+// two LDS addresses for the whole item (no per-token address arithmetic), and
+// each token costs two 16-bit reads, whose token and buffer offsets are
+// instruction immediates, and one v_dot2_f32_bf16 (the value pair (x, 0):
+// product exact, one rounding).  A stage's slots past the chunk's end hold
+// zeros (the descriptors end there) and add nothing.
+constexpr int kFixBuf = 2 * kMaskSlotTokens * kMaskSlot;
+static_assert(2 * kFixBuf == (int)kMaskSlotLds, "two stage buffers");
+
+template <int P>
+__device__ __forceinline__ void gather_slots(const uint8_t* stage, const uint32_t (&la)[kMaskPerThread],
+                                             const uint32_t (&lb)[kMaskPerThread], float (&acc)[kMaskPerThread]) {
+  typedef __attribute__((address_space(3))) uint8_t lds_u8;
+  typedef __attribute__((address_space(3))) uint16_t lds_u16;
+  typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+  const lds_u8* sp = (const lds_u8*)stage + P * kFixBuf;
+#pragma unroll
+  for (int u = 0; u < kMaskSlotTokens; ++u)
+#pragma unroll
+    for (int j = 0; j < kMaskPerThread; ++j) {
+      const uint32_t vb = *(const lds_u16*)(sp + lb[j] + u * kMaskSlot);
+      const uint32_t va = *(const lds_u16*)(sp + la[j] + u * kMaskSlot);
+      acc[j] = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, vb), __builtin_bit_cast(bf16x2, va),
+                                               acc[j], false);
+    }
+}
+
+__global__ __launch_bounds__(256, 2) void mask_fixed_kernel(const MaskItem* __restrict__ items,
+                                                            const MaskTask* __restrict__ tasks,
+                                                            float* __restrict__ partials) {
+  extern __shared__ __align__(1024) uint8_t stage[];
+  const MaskItem it = items[blockIdx.x];
+  if (it.task < 0) return;  // padding item
+  const MaskTask& M = tasks[it.task];
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, ex = it.example;
+  int t_eff = M.T;
+  if (M.lengths) t_eff = min(max(M.lengths[ex], 0), M.T);
+  const int t0 = it.chunk * M.chunk_tokens;
+  const int t1 = __builtin_amdgcn_readfirstlane(min(t_eff, t0 + M.chunk_tokens));
+  const int e0 = it.group * kMaskGroup;
+  const int a_row = __builtin_amdgcn_readfirstlane(M.d_in * 2), b_row = __builtin_amdgcn_readfirstlane(M.d_out * 2);
+  const int32_t* sl = M.slices + 4 * it.group;
+  const int sa0 = __builtin_amdgcn_readfirstlane(sl[0]), seg_a = __builtin_amdgcn_readfirstlane(sl[1]);
+  const int sb0 = __builtin_amdgcn_readfirstlane(sl[2]), seg_b = __builtin_amdgcn_readfirstlane(sl[3]);
+  // entry addresses in buffer 0, token slot 0 (byte offsets from stage)
+  uint32_t la[kMaskPerThread], lb[kMaskPerThread];
+  float acc[kMaskPerThread];
+#pragma unroll
+  for (int j = 0; j < kMaskPerThread; ++j) {
+    const int e = e0 + tid + 256 * j;
+    la[j] = (uint32_t)(M.cols[e] * 2 - sa0);
+    lb[j] = (uint32_t)(kMaskSlotTokens * kMaskSlot + M.rows[e] * 2 - sb0);
+    acc[j] = 0.f;
+  }
+  const uint8_t* ga = (const uint8_t*)M.A + ((int64_t)ex * M.T) * a_row;
+  const uint8_t* gb = (const uint8_t*)M.B + ((int64_t)ex * M.T) * b_row;
+  // descriptors end at row t1: slots past the chunk land as zero
+  const rsrc_t r_a = make_rsrc(ga, (uint32_t)((int64_t)t1 * a_row));
+  const rsrc_t r_b = make_rsrc(gb, (uint32_t)((int64_t)t1 * b_row));
+  const int runs_a = (seg_a + 1023) >> 10, runs_b = (seg_b + 1023) >> 10;
+  const int n_st = t1 > t0 ? (t1 - t0 + kMaskSlotTokens - 1) / kMaskSlotTokens : 0;
+  // stage st into buffer st & 1: 1 KiB runs of each slot (bytes past a slice
+  // stay inside its slot), dealt to the 4 waves in turn.  A run's offset is
+  // wave-uniform plus the lane's 16 bytes, added per load into the vector
+  // offset (the descriptor's range check covers that operand only); the
+  // empty asm keeps the compiler from holding every run's offset in a register.
+  const int wv = __builtin_amdgcn_readfirstlane(wave);
+  const uint32_t lo = (uint32_t)lane * 16;
+  auto voff = [&](int run_off) {
+    uint32_t v = lo;
+    asm volatile("" : "+v"(v));
+    return v + (uint32_t)run_off;
+  };
+  auto issue = [&](int st) {
+    uint8_t* buf = stage + (st & 1) * kFixBuf;
+    const int ts = t0 + st * kMaskSlotTokens;
+    int q = 0;  // runs issued so far in this stage (uniform)
+#pragma unroll
+    for (int u = 0; u < kMaskSlotTokens; ++u) {
+      for (int c = (wv - q) & 3; c < runs_a; c += 4)
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(r_a, LDS_PTR(buf + u * kMaskSlot + c * 1024), 16,
+                                                 voff((ts + u) * a_row + sa0 + c * 1024), 0, 0, 0);
+      q += runs_a;
+      for (int c = (wv - q) & 3; c < runs_b; c += 4)
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(r_b, LDS_PTR(buf + (kMaskSlotTokens + u) * kMaskSlot + c * 1024),
+                                                 16, voff((ts + u) * b_row + sb0 + c * 1024), 0, 0, 0);
+      q += runs_b;
+    }
+  };
+  if (n_st > 0) issue(0);
+  for (int st = 0; st < n_st; st += 2) {  // uniform trip count; buffers 0 and 1 in turn
+    wait_vm0();        // this wave's loads of stage st have landed
+    __syncthreads();   // every wave's have; buffer 1's readers are done
+    if (st + 1 < n_st) issue(st + 1);
+    gather_slots<0>(stage, la, lb, acc);
+    if (st + 1 >= n_st) break;
+    wait_vm0();
+    __syncthreads();
+    if (st + 2 < n_st) issue(st + 2);
+    gather_slots<1>(stage, la, lb, acc);
+  }
+  float* dst = partials + M.partial_base + ((int64_t)ex * M.n_chunks + it.chunk) * M.m;
+#pragma unroll
+  for (int j = 0; j < kMaskPerThread; ++j) dst[M.pos[e0 + tid + 256 * j]] = acc[j];
+}
+
+hipError_t launch_mask_fixed(const MaskItem* items, int n_items, const MaskTask* tasks, float* partials,
+                             hipStream_t s) {
+  if (n_items <= 0) return hipSuccess;
+  const hipError_t e = hipFuncSetAttribute((const void*)mask_fixed_kernel,
+                                           hipFuncAttributeMaxDynamicSharedMemorySize, (int)kMaskSlotLds);
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(mask_fixed_kernel, dim3((unsigned)n_items), dim3(256), kMaskSlotLds, s, items, tasks,
+                     partials);
+  return hipGetLastError();
 }
 
 template <int ELT, bool AL, bool FULL, bool B16>

@@ -51,7 +51,8 @@ struct Plan {
   // mask layers (gathered DW entries)
   std::vector<MaskTask> mtasks;
   std::vector<MaskItem> mitems;
-  struct MaskLaunch { int aligned, full, first, count; };  // full: every item a whole entry group
+  // full: every item a whole entry group; fixed: the fixed-slot gather
+  struct MaskLaunch { int aligned, full, fixed, first, count; };
   std::vector<MaskLaunch> mlaunches;
   std::vector<ReduceTask> mreduce;
   int mask_max_out = 0;

@@ -813,6 +813,7 @@ dattri_status dattri::build_plan(const dattri_ctx* ctx, dattri_route forced, Pla
       M.rows = (const int32_t*)L.P_in;
       M.cols = (const int32_t*)L.P_in + L.k_out;
       M.pos = (const int32_t*)L.P_in + 2 * (int64_t)L.k_out;
+      M.slices = (const int32_t*)L.P_in + 3 * (int64_t)L.k_out;
       M.d_in = L.d_in; M.d_out = L.d_out; M.T = L.T; M.m = L.k_out;
       M.stage_tokens = (int)std::max<int64_t>(1, std::min<int64_t>(16, kMaskStageBudget / row_bytes));
       const int64_t tc = (L.T + want_chunks - 1) / want_chunks;
@@ -820,6 +821,11 @@ dattri_status dattri::build_plan(const dattri_ctx* ctx, dattri_route forced, Pla
       M.n_chunks = std::max(1, (L.T + M.chunk_tokens - 1) / M.chunk_tokens);
       M.aligned = ((uintptr_t)L.A % 16 == 0) && ((uintptr_t)L.B % 16 == 0) && (L.d_in * elt) % 16 == 0 &&
                   (L.d_out * elt) % 16 == 0;
+      // whole groups take the fixed-slot gather when every one's slices fit a slot
+      M.fixed = M.aligned && elt == 2 && L.k_out >= kMaskGroup &&
+                L.mask_slices.size() >= (size_t)4 * (L.k_out / kMaskGroup);  // bound
+      for (int g = 0; M.fixed && g < L.k_out / kMaskGroup; ++g)
+        M.fixed = L.mask_slices[4 * g + 1] <= kMaskSlot && L.mask_slices[4 * g + 3] <= kMaskSlot;
       M.partial_base = (int64_t)mask_floats;
       mask_floats += (size_t)n * M.n_chunks * M.m;
       // aligned: two buffers of [A part | B part], parts rounded up to 1 KiB; else one buffer
@@ -846,34 +852,36 @@ dattri_status dattri::build_plan(const dattri_ctx* ctx, dattri_route forced, Pla
     // run together and share the rows through that XCD's L2.  Chunks are dealt
     // to the least-loaded of 8 per-XCD queues and the queues interleaved
     // (workgroup i runs on XCD i mod 8); short queues are padded.
-    // One launch per (alignment, whole groups or not): a whole group of
-    // kMaskGroup entries takes the gather without slot bounds.
+    // One launch per (alignment, whole groups or not, fixed slots or not): a
+    // whole group of kMaskGroup entries takes the gather without slot bounds,
+    // and the fixed-slot one when its task allows.
     for (int al = 1; al >= 0; --al)
-      for (int full = 1; full >= 0; --full) {
-        std::vector<std::vector<MaskItem>> q(kXcds);
-        int64_t load[kXcds] = {0};
-        for (size_t t = 0; t < P.mtasks.size(); ++t) {
-          const MaskTask& M = P.mtasks[t];
-          if (M.aligned != al) continue;
-          const int whole = M.m / kMaskGroup, groups = (M.m + kMaskGroup - 1) / kMaskGroup;
-          const int g0 = full ? 0 : whole, g1 = full ? whole : groups;
-          if (g1 <= g0) continue;
-          for (int e = 0; e < n; ++e)
-            for (int c = 0; c < M.n_chunks; ++c) {
-              const int x = (int)(std::min_element(load, load + kXcds) - load);
-              for (int g = g0; g < g1; ++g) q[x].push_back({(int)t, e, c, g});
-              load[x] += g1 - g0;
-            }
+      for (int full = 1; full >= 0; --full)
+        for (int fx = full && al ? 1 : 0; fx >= 0; --fx) {
+          std::vector<std::vector<MaskItem>> q(kXcds);
+          int64_t load[kXcds] = {0};
+          for (size_t t = 0; t < P.mtasks.size(); ++t) {
+            const MaskTask& M = P.mtasks[t];
+            if (M.aligned != al || (full && M.fixed != fx)) continue;
+            const int whole = M.m / kMaskGroup, groups = (M.m + kMaskGroup - 1) / kMaskGroup;
+            const int g0 = full ? 0 : whole, g1 = full ? whole : groups;
+            if (g1 <= g0) continue;
+            for (int e = 0; e < n; ++e)
+              for (int c = 0; c < M.n_chunks; ++c) {
+                const int x = (int)(std::min_element(load, load + kXcds) - load);
+                for (int g = g0; g < g1; ++g) q[x].push_back({(int)t, e, c, g});
+                load[x] += g1 - g0;
+              }
+          }
+          size_t len = 0;
+          for (const auto& v : q) len = std::max(len, v.size());
+          const int first = (int)P.mitems.size();
+          for (size_t i = 0; i < len; ++i)
+            for (int x = 0; x < kXcds; ++x)
+              P.mitems.push_back(i < q[x].size() ? q[x][i] : MaskItem{-1, 0, 0, 0});
+          const int count = (int)P.mitems.size() - first;
+          if (count) P.mlaunches.push_back({al, full, fx, first, count});
         }
-        size_t len = 0;
-        for (const auto& v : q) len = std::max(len, v.size());
-        const int first = (int)P.mitems.size();
-        for (size_t i = 0; i < len; ++i)
-          for (int x = 0; x < kXcds; ++x)
-            P.mitems.push_back(i < q[x].size() ? q[x][i] : MaskItem{-1, 0, 0, 0});
-        const int count = (int)P.mitems.size() - first;
-        if (count) P.mlaunches.push_back({al, full, first, count});
-      }
     P.maskpart_bytes = mask_floats * 4;
   }
 
@@ -1031,11 +1039,19 @@ dattri_status check_layer(const dattri_ctx* ctx, int32_t layer) {
   return DATTRI_OK;
 }
 
-// Device entry table of a mask layer: [rows | cols | pos], int32, m each.
+// Device entry table of a mask layer: [rows | cols | pos], int32, m each,
+// then 4 int32 per entry group: the byte slice of each A token row (first
+// byte, length) and of each B token row covering the group's columns and rows,
+// both ends on 16-byte boundaries (the row's end for rows that are not a
+// multiple of 16 bytes).
 // Entries are placed into the gather kernel's slots group by group (groups of
-// kMaskGroup entries in mask order; slot e of a group is read by thread
-// e % 256 at step e / 256, so slots 32h .. 32h + 31 form the half-wave h of
-// one LDS read).  Inside a group, each entry goes to the first half-wave
+// kMaskGroup entries; slot e of a group is read by thread e % 256 at step
+// e / 256, so slots 32h .. 32h + 31 form the half-wave h of one LDS read).
+// A layer with more than one group deals its entries to the groups in order
+// of their index on the wider side of DW (rows when d_out >= d_in, else
+// columns; equal indices in mask order): each group's entries then span about
+// 1/groups of that side, and the kernel stages only that slice of each token
+// row instead of the whole row.  Inside a group, each entry goes to the first half-wave
 // where neither its A word nor its B word meets another word in the same
 // bank (32 banks of 4 bytes; a word already there is read once for all its
 // lanes), else one where one of the two does not, else any with room; so
@@ -1043,8 +1059,8 @@ dattri_status check_layer(const dattri_ctx* ctx, int32_t layer) {
 // mask order, where the kernel writes its sum.
 void mask_slot_table(const std::vector<int32_t>& rows, const std::vector<int32_t>& cols, int d_in, int d_out,
                      int elt, std::vector<int32_t>& table) {
-  const int m = (int)rows.size();
-  table.assign((size_t)3 * m, 0);
+  const int m = (int)rows.size(), n_groups = (m + kMaskGroup - 1) / kMaskGroup;
+  table.assign((size_t)3 * m + 4 * (size_t)n_groups, 0);
   int32_t* t_rows = table.data();
   int32_t* t_cols = table.data() + m;
   int32_t* t_pos = table.data() + 2 * (size_t)m;
@@ -1062,6 +1078,12 @@ void mask_slot_table(const std::vector<int32_t>& rows, const std::vector<int32_t
                                      std::vector<int32_t>((size_t)(((int64_t)d_out * elt + 3) / 4), -1)};
   std::vector<Bits> holders[2];
   std::vector<int32_t> touched[2];
+  std::vector<int32_t> order((size_t)m);
+  for (int i = 0; i < m; ++i) order[i] = i;
+  if (m > kMaskGroup) {
+    const std::vector<int32_t>& key = d_out >= d_in ? rows : cols;
+    std::stable_sort(order.begin(), order.end(), [&](int32_t a, int32_t b) { return key[a] < key[b]; });
+  }
   for (int e0 = 0; e0 < m; e0 += kMaskGroup) {
     const int N = std::min(kMaskGroup, m - e0), H = (N + kHalf - 1) / kHalf;
     Bits all{};
@@ -1071,8 +1093,8 @@ void mask_slot_table(const std::vector<int32_t>& rows, const std::vector<int32_t
       for (int b = 0; b < kHalf; ++b) free_bank[side][b] = all;
     int fill[kMaxHalves] = {0};
     for (int i = 0; i < N; ++i) {
-      const int32_t word[2] = {(int32_t)(((int64_t)cols[e0 + i] * elt) >> 2),
-                               (int32_t)(((int64_t)rows[e0 + i] * elt) >> 2)};
+      const int32_t e = order[e0 + i];
+      const int32_t word[2] = {(int32_t)(((int64_t)cols[e] * elt) >> 2), (int32_t)(((int64_t)rows[e] * elt) >> 2)};
       Bits ok[2];
       for (int side = 0; side < 2; ++side) {
         ok[side] = free_bank[side][word[side] % kHalf];
@@ -1104,10 +1126,25 @@ void mask_slot_table(const std::vector<int32_t>& rows, const std::vector<int32_t
           holders[side][hs].w[h >> 6] |= bit;
         }
       }
-      t_rows[e0 + slot] = rows[e0 + i];
-      t_cols[e0 + slot] = cols[e0 + i];
-      t_pos[e0 + slot] = e0 + i;
+      t_rows[e0 + slot] = rows[e];
+      t_cols[e0 + slot] = cols[e];
+      t_pos[e0 + slot] = e;
     }
+    int32_t lo_r = d_out, hi_r = -1, lo_c = d_in, hi_c = -1;
+    for (int i = 0; i < N; ++i) {
+      const int32_t e = order[e0 + i];
+      lo_r = std::min(lo_r, rows[e]); hi_r = std::max(hi_r, rows[e]);
+      lo_c = std::min(lo_c, cols[e]); hi_c = std::max(hi_c, cols[e]);
+    }
+    auto slice = [&](int32_t lo, int32_t hi, int d, int32_t* out) {
+      const int64_t b0 = ((int64_t)lo * elt) & ~(int64_t)15;
+      const int64_t b1 = std::min(((int64_t)(hi + 1) * elt + 15) & ~(int64_t)15, (int64_t)d * elt);
+      out[0] = (int32_t)b0;
+      out[1] = (int32_t)(b1 - b0);
+    };
+    int32_t* g = table.data() + 3 * (size_t)m + 4 * (size_t)(e0 / kMaskGroup);
+    slice(lo_c, hi_c, d_in, g);
+    slice(lo_r, hi_r, d_out, g + 2);
     for (int side = 0; side < 2; ++side) {  // reset the word index for the next group
       for (int32_t w : touched[side]) slot_of[side][w] = -1;
       touched[side].clear();
@@ -1201,10 +1238,15 @@ dattri_status dattri::run_plan(dattri_ctx* ctx, const Plan& P, void* phi, dattri
 
   if (!P.mtasks.empty()) {
     float* kpart = (float*)(ws + P.off_maskpart);
-    for (const Plan::MaskLaunch& L : P.mlaunches)
-      HIP_TRY(launch_mask(ctx->elt, L.aligned, L.full, P.mask_b16 ? 1 : 0,
-                          (const MaskItem*)(tab + P.off_mitems) + L.first, L.count,
-                          (const MaskTask*)(tab + P.off_mtasks), P.mask_lds, kpart, s));
+    for (const Plan::MaskLaunch& L : P.mlaunches) {
+      const MaskItem* items = (const MaskItem*)(tab + P.off_mitems) + L.first;
+      const MaskTask* tasks = (const MaskTask*)(tab + P.off_mtasks);
+      if (L.fixed)
+        HIP_TRY(launch_mask_fixed(items, L.count, tasks, kpart, s));
+      else
+        HIP_TRY(launch_mask(ctx->elt, L.aligned, L.full, P.mask_b16 ? 1 : 0, items, L.count, tasks, P.mask_lds,
+                            kpart, s));
+    }
     HIP_TRY(launch_reduce((const ReduceTask*)(tab + P.off_mreduce), (int)P.mreduce.size(), n, P.mask_max_out,
                           kpart, phi, phi_bf16, ld_phi, s));
   }
@@ -1365,8 +1407,8 @@ dattri_status dattri_projection_bytes(const dattri_ctx* ctx, int32_t layer, size
   dattri_status st = check_layer(ctx, layer);
   if (st != DATTRI_OK) return st;
   const Layer& L = ctx->layers[layer];
-  if (L.mask_size > 0) {  // the mask's entry table: rows, cols and output positions, int32
-    if (bytes_in) *bytes_in = (size_t)12 * L.k_out;
+  if (L.mask_size > 0) {  // the mask's entry table: rows, cols, output positions; group slices
+    if (bytes_in) *bytes_in = (size_t)12 * L.k_out + (size_t)16 * ((L.k_out + kMaskGroup - 1) / kMaskGroup);
     if (bytes_out) *bytes_out = 0;
     return DATTRI_OK;
   }
@@ -1393,6 +1435,7 @@ dattri_status dattri_bind_projection(dattri_ctx* ctx, int32_t layer, void* dev_P
     hipStream_t s = (hipStream_t)stream;
     HIP_TRY(hipMemcpyAsync(dev_P_in, table.data(), table.size() * 4, hipMemcpyHostToDevice, s));
     HIP_TRY(hipStreamSynchronize(s));
+    L.mask_slices.assign(table.begin() + 3 * (size_t)L.k_out, table.end());
     L.P_in = dev_P_in;
     L.P_out = nullptr;
     L.bound = true;

@@ -282,6 +282,83 @@ def test_mask_layer_wider_than_byte_offsets():
         assert e <= 1e-5, (li, e)
 
 
+SLICED = [dict(name="tall", d_in=512, d_out=2048, k_in=1, k_out=40000, mask_size=20000, mask_id=1, mask_count=2,
+               a_group="sa"),
+          dict(name="wide", d_in=3000, d_out=512, k_in=1, k_out=33000, mask_size=33000, mask_id=0, a_group="sb")]
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_mask_groups_stage_row_slices(dtype):
+    # App. A.2 random masks with several entry groups per layer: the table
+    # deals entries to the groups along the wider side of DW (rows of the
+    # tall layer, columns of the wide one), each group stages only its slice
+    # of every token row; two whole groups and a partial one per layer,
+    # ragged lengths
+    from oracle import mask as om
+    wl = dict(W.WORKLOADS["tiny"], dist_a="normal", dist_b="normal", seed=35)
+    n, T = 2, 96
+    inputs = _session_inputs(wl, SLICED, n, T, dtype)
+    lengths = torch.tensor([96, 50], dtype=torch.int32, device=DEV)
+    s = ProjectionSession(SLICED, dtype=dtype, seed=45)
+    for li, (A, B) in enumerate(inputs):
+        s.capture(li, A, B, lengths)
+    phi = s.project(n)
+    torch.cuda.synchronize()
+    got, lens = host64(phi), lengths.cpu().numpy()
+    group = 16384
+    for li, L in enumerate(SLICED):
+        m = L["k_out"]
+        table = s.maps[li][0].view(torch.int32).cpu().numpy()
+        t_rows, t_cols, t_pos = table[:m], table[m:2 * m], table[2 * m:3 * m]
+        parts = [om.mask_indices(45, li, L["d_in"], L["d_out"], L["mask_size"], L["mask_id"] + j)
+                 for j in range(L.get("mask_count", 1))]
+        rows = np.concatenate([p[0] for p in parts])
+        cols = np.concatenate([p[1] for p in parts])
+        # the table is a permutation of the mask with each slot's position
+        assert np.array_equal(np.sort(t_pos), np.arange(m))
+        assert np.array_equal(t_rows, rows[t_pos]) and np.array_equal(t_cols, cols[t_pos])
+        # groups follow each other along the wider side
+        key = t_rows if L["d_out"] >= L["d_in"] else t_cols
+        for g in range(0, m - group, group):
+            assert key[g:g + group].max() <= key[g + group:g + 2 * group].min(), (li, g)
+        A, B = host64(inputs[li][0]), host64(inputs[li][1])
+        ref = np.stack([om.masked_gradient(A[i], B[i], rows, cols, int(lens[i])) for i in range(n)])
+        off = s.offsets[li]
+        e = rel_fro(got[:, off:off + m], ref)
+        assert e <= 1e-5, (li, e)
+
+
+def test_mask_full_size_sampled():
+    # App. A.2 / App. B: ten masks of 8192 entries on Llama-3-8B-shaped layers
+    # (q, k, gate, down of one block) at T = 2048, one ragged example, in the
+    # launch configuration the benchmark times (whole groups on the
+    # fixed-slot gather); 4096 sampled entries per layer against the oracle
+    from oracle import mask as om
+    wl = W.WORKLOADS["llama8b"]
+    pick = [0, 1, 4, 6]  # q_proj, k_proj, gate_proj, down_proj of block 0
+    layers = [dict(wl["layers"][i], k_in=1, k_out=81920, mask_size=8192, mask_count=10) for i in pick]
+    n, T = 2, wl["T"]
+    cache = {}
+    inputs = [W.factor_blocks(dict(wl, layers=layers), li, 0, n, T, DEV, "bf16", a_cache=cache)
+              for li in range(len(layers))]
+    lengths = torch.tensor([T, 1531], dtype=torch.int32, device=DEV)
+    s = ProjectionSession(layers, dtype="bf16", seed=wl["seed"])
+    for li, (A, B) in enumerate(inputs):
+        s.capture(li, A, B, lengths)
+    phi = s.project(n)
+    torch.cuda.synchronize()
+    got, lens = host64(phi), lengths.cpu().numpy()
+    rng = np.random.default_rng(5)
+    for li, L in enumerate(layers):
+        rows, cols = dt.dattri_get_mask(s.ctx, li)
+        idx = np.sort(rng.choice(L["k_out"], 4096, replace=False))
+        A, B = host64(inputs[li][0]), host64(inputs[li][1])
+        ref = np.stack([om.masked_gradient(A[i], B[i], rows[idx], cols[idx], int(lens[i])) for i in range(n)])
+        off = s.offsets[li]
+        e = rel_fro(got[:, off + idx], ref)
+        assert e <= 1e-5, (L["name"], e)
+
+
 @pytest.mark.parametrize("form", ["fused", "split"])
 def test_shared_input_group_matches_separate_inputs(form):
     # 16-wide maps: q and k share one fused work item (2 input tiles keep 4 row

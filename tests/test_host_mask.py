@@ -28,7 +28,7 @@ def test_mask_layer_layout_and_draw(ctx):
     assert dt.dattri_feature_dim(ctx) == 32 + 512 + 512 + 8192 + 81920
     assert [dt.dattri_layer_offset(ctx, i) for i in (l1, l2, l3, l4)] == [32, 544, 1056, 9248]
     assert dt.dattri_layer_dims(ctx, l4) == (4096, 14336, 1, 81920)
-    assert dt.dattri_projection_bytes(ctx, l4) == (12 * 81920, 0)
+    assert dt.dattri_projection_bytes(ctx, l4) == (12 * 81920 + 16 * 5, 0)  # + 5 group slices
     rows, cols = dt.dattri_get_mask(ctx, l4)
     for j in range(10):
         r_o, c_o = om.mask_indices(4242, l4, 4096, 14336, 8192, j)
@@ -37,7 +37,7 @@ def test_mask_layer_layout_and_draw(ctx):
     flat = cols.astype(np.int64) * 14336 + rows
     assert len(np.unique(flat)) == 81920  # disjoint
     assert dt.dattri_layer_dims(ctx, l1) == (300, 128, 1, 512)
-    assert dt.dattri_projection_bytes(ctx, l3) == (12 * 8192, 0)
+    assert dt.dattri_projection_bytes(ctx, l3) == (12 * 8192 + 16, 0)
     for lid, (d_in, d_out, m, j) in ((l1, (300, 128, 512, 0)), (l2, (300, 128, 512, 7)),
                                      (l3, (4096, 14336, 8192, 9))):
         rows, cols = dt.dattri_get_mask(ctx, lid)

@@ -265,12 +265,22 @@ constexpr int kMaskPerThread = 64;
 constexpr int kMaskGroup = 256 * kMaskPerThread;   // entries per work item
 constexpr int64_t kMaskStageBudget = 40 * 1024;   // bytes of one stage (two stages per work item)
 // Fixed-slot gather (bf16, 16-byte rows, whole groups whose A and B slices are
-// at most kMaskSlot bytes): every stage holds kMaskSlotTokens tokens, each
-// slice in a slot of its own at a fixed offset, so token and buffer offsets
-// are instruction immediates.  LDS: 2 buffers of [A slots | B slots].
+// at most kMaskSlot bytes): every stage holds kMaskSlotPairs token pairs, each
+// side's slice as a row of bf16 pairs at a fixed offset.  LDS: 2 buffers of
+// kMaskSlotPairs x [A pair row | B pair row], one workgroup per CU.
 constexpr int kMaskSlot = 8192;
-constexpr int kMaskSlotTokens = 2;
-constexpr size_t kMaskSlotLds = (size_t)2 * 2 * kMaskSlotTokens * kMaskSlot;
+constexpr int kMaskSlotPairs = 2;
+constexpr size_t kMaskSlotLds = (size_t)2 * kMaskSlotPairs * 2 * (2 * kMaskSlot);
+// Byte offset of slice feature f in a fixed-slot pair row: 16-byte chunk
+// g = f / 4 (four pairs) goes to half g % 2 (kMaskSlot bytes each) at
+// 16 (g / 2), so the chunks 2k, 2k + 1 that one thread stages land in the two
+// halves at 16 k and a wave's write of either is 1 KiB in a row (no bank
+// conflicts).  Its 4-byte word falls in LDS bank (4 (f / 8) + f % 4) mod 32.
+constexpr uint32_t mask_pair_offset(uint32_t f) {
+  return ((f >> 2) & 1u) * (uint32_t)kMaskSlot + 16u * (f >> 3) + 4u * (f & 3u);
+}
+// whether a mask layer's whole groups qualify (slices: 4 per group, as in its table)
+bool mask_fixed_layout(int elt, int d_in, int d_out, int m, const int32_t* slices);
 struct MaskTask {
   const void* A; const void* B;      // [n, T, d_in], [n, T, d_out]
   const int32_t* lengths;            // [n] or null

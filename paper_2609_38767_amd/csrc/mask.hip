@@ -18,11 +18,16 @@
 // float32 (bf16 layers up to 32768 wide take them through v_dot2_f32_bf16,
 // gather_rows_b16).  Every group restages the narrow side's token rows, so
 // groups are made as large as two waves per SIMD allow: ten masks of 8192
-// entries take 5 groups instead of 10.  The entries come in the slot order of the layer's
-// table, arranged at bind time so that the 32 lanes of a half-wave mostly
-// read distinct LDS banks, and each sum is written at the entry's position in
-// mask order.  Whole groups and the partial last group of a layer run in
+// entries take 5 groups instead of 10.  The entries come in the slot order
+// of the layer's table, arranged at bind time so that the 32 lanes of a
+// half-wave mostly read distinct LDS banks, and each sum is written at the
+// entry's position in mask order.  Whole groups and the partial last group of a layer run in
 // separate launches (the partial one bounds its slots).
+//
+// Whole groups of bf16 layers whose slices fit 8 KiB take mask_fixed_kernel
+// instead: it stages token pairs, so each 32-bit LDS read serves two tokens
+// of an entry (half the reads per product of the kernel above), and keeps
+// every slice at a fixed place so that no address is formed per token.
 #include "device_common.h"
 #include "internal.h"
 
@@ -249,44 +254,76 @@ __global__ __launch_bounds__(256, 2) void mask_kernel(const MaskItem* __restrict
     if (tid + 256 * j < ne) dst[M.pos[e0 + tid + 256 * j]] = acc[j];
 }
 
-// Fixed-slot gather: whole groups of bf16 layers with 16-byte rows whose
-// slices fit kMaskSlot bytes.  Stage buffer p (of 2) at p * kFixBuf holds, of
-// each of its kMaskSlotTokens tokens u, the A slice in slot u and the B slice
-// in slot kMaskSlotTokens + u (kMaskSlot bytes each).  Every entry keeps its
-// two LDS addresses for the whole item (no per-token address arithmetic), and
-// each token costs two 16-bit reads, whose token and buffer offsets are
-// instruction immediates, and one v_dot2_f32_bf16 (the value pair (x, 0):
-// product exact, one rounding).  A stage's slots past the chunk's end hold
-// zeros (the descriptors end there) and add nothing.
-constexpr int kFixBuf = 2 * kMaskSlotTokens * kMaskSlot;
+// Fixed-slot gather: whole groups of bf16 layers with 16-byte rows whose slices
+// fit kMaskSlot bytes.  A stage is kMaskSlotPairs token pairs (t, t + 1), held
+// in one of two buffers (kFixBuf bytes each) as pair rows: feature f of the A
+// slice at byte mask_pair_offset(f) of the pair's A row is the bf16 pair
+// (A[t][f], A[t + 1][f]), its B row likewise.  So one 32-bit LDS read per side
+// serves both tokens of an entry, and v_dot2_f32_bf16 adds both products (exact
+// in float32) to the entry's sum.  The pairs are formed in registers (16 bytes
+// of each of two token rows per thread and side, interleaved by 16-bit halves,
+// written as two 16-byte chunks into the two halves of the pair row, see
+// mask_pair_offset) while the next stage's loads are in flight.  Every entry
+// keeps both LDS offsets in one register (16 bits each), unpacked once per
+// stage into the buffer's addresses; the pair offsets are instruction
+// immediates.  A pair's tokens past the chunk's end read as zero (the
+// descriptors end there) and add nothing.  512 threads hold the group's 16384
+// entries (slot e to thread e % 512 at step e / 512: the table's half-waves are
+// still 32 consecutive slots); one workgroup per CU.
+constexpr int kFixSide = 2 * kMaskSlot;                  // bytes of a pair row
+constexpr int kFixPairRows = 2 * kFixSide;               // A row | B row of one pair
+constexpr int kFixBuf = kMaskSlotPairs * kFixPairRows;   // one stage
 static_assert(2 * kFixBuf == (int)kMaskSlotLds, "two stage buffers");
+static_assert((kMaskSlotPairs - 1) * kFixPairRows + 2 * kFixSide <= 65536, "pair offsets are DS immediates");
+constexpr int kFixThreads = 512;
+constexpr int kFixPer = kMaskGroup / kFixThreads;  // entries per thread
+static_assert(kMaskSlot / 16 == kFixThreads, "one 16-byte chunk of each slice per thread");
 
 template <int P>
-__device__ __forceinline__ void gather_slots(const uint8_t* stage, const uint32_t (&la)[kMaskPerThread],
-                                             const uint32_t (&lb)[kMaskPerThread], float (&acc)[kMaskPerThread]) {
+__device__ __forceinline__ void gather_pairs(const uint8_t* stage, const uint32_t (&rc)[kFixPer],
+                                             float (&acc)[kFixPer]) {
   typedef __attribute__((address_space(3))) uint8_t lds_u8;
-  typedef __attribute__((address_space(3))) uint16_t lds_u16;
+  typedef __attribute__((address_space(3))) uint32_t lds_u32;
   typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
   const lds_u8* sp = (const lds_u8*)stage + P * kFixBuf;
 #pragma unroll
-  for (int u = 0; u < kMaskSlotTokens; ++u)
+  for (int j = 0; j < kFixPer; ++j) {
+    uint32_t x = rc[j];
+    asm volatile("" : "+v"(x));  // unpack per stage: no unpacked offsets held across stages
+    const lds_u8* pb = sp + (x >> 16);
+    const lds_u8* pa = sp + (x & 0xFFFFu);
 #pragma unroll
-    for (int j = 0; j < kMaskPerThread; ++j) {
-      const uint32_t vb = *(const lds_u16*)(sp + lb[j] + u * kMaskSlot);
-      const uint32_t va = *(const lds_u16*)(sp + la[j] + u * kMaskSlot);
+    for (int q = 0; q < kMaskSlotPairs; ++q) {
+      const uint32_t vb = *(const lds_u32*)(pb + q * kFixPairRows);
+      const uint32_t va = *(const lds_u32*)(pa + q * kFixPairRows);
       acc[j] = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, vb), __builtin_bit_cast(bf16x2, va),
                                                acc[j], false);
     }
+  }
 }
 
-__global__ __launch_bounds__(256, 2) void mask_fixed_kernel(const MaskItem* __restrict__ items,
-                                                            const MaskTask* __restrict__ tasks,
-                                                            float* __restrict__ partials) {
+// 16 bytes at token rows t and t + 1 (x0, x1) -> 8 pairs (x0.h[f], x1.h[f]),
+// features 0..3 in lo, 4..7 in hi
+__device__ __forceinline__ void pair_halves(const i32x4& x0, const i32x4& x1, i32x4& lo, i32x4& hi) {
+  uint32_t o[8];
+#pragma unroll
+  for (int w = 0; w < 4; ++w) {
+    const uint32_t a = (uint32_t)x0[w], b = (uint32_t)x1[w];
+    o[2 * w] = (a & 0xFFFFu) | (b << 16);
+    o[2 * w + 1] = (a >> 16) | (b & 0xFFFF0000u);
+  }
+  lo = i32x4{(int)o[0], (int)o[1], (int)o[2], (int)o[3]};
+  hi = i32x4{(int)o[4], (int)o[5], (int)o[6], (int)o[7]};
+}
+
+__global__ __launch_bounds__(kFixThreads, 2) void mask_fixed_kernel(const MaskItem* __restrict__ items,
+                                                                    const MaskTask* __restrict__ tasks,
+                                                                    float* __restrict__ partials) {
   extern __shared__ __align__(1024) uint8_t stage[];
   const MaskItem it = items[blockIdx.x];
   if (it.task < 0) return;  // padding item
   const MaskTask& M = tasks[it.task];
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, ex = it.example;
+  const int tid = threadIdx.x, ex = it.example;
   int t_eff = M.T;
   if (M.lengths) t_eff = min(max(M.lengths[ex], 0), M.T);
   const int t0 = it.chunk * M.chunk_tokens;
@@ -296,66 +333,78 @@ __global__ __launch_bounds__(256, 2) void mask_fixed_kernel(const MaskItem* __re
   const int32_t* sl = M.slices + 4 * it.group;
   const int sa0 = __builtin_amdgcn_readfirstlane(sl[0]), seg_a = __builtin_amdgcn_readfirstlane(sl[1]);
   const int sb0 = __builtin_amdgcn_readfirstlane(sl[2]), seg_b = __builtin_amdgcn_readfirstlane(sl[3]);
-  // entry addresses in buffer 0, token slot 0 (byte offsets from stage)
-  uint32_t la[kMaskPerThread], lb[kMaskPerThread];
-  float acc[kMaskPerThread];
+  // entry (r, c): byte offsets of its pair-row words in a stage, B << 16 | A
+  uint32_t rc[kFixPer];
+  float acc[kFixPer];
 #pragma unroll
-  for (int j = 0; j < kMaskPerThread; ++j) {
-    const int e = e0 + tid + 256 * j;
-    la[j] = (uint32_t)(M.cols[e] * 2 - sa0);
-    lb[j] = (uint32_t)(kMaskSlotTokens * kMaskSlot + M.rows[e] * 2 - sb0);
+  for (int j = 0; j < kFixPer; ++j) {
+    const int e = e0 + tid + kFixThreads * j;
+    rc[j] = ((uint32_t)kFixSide + mask_pair_offset((uint32_t)(M.rows[e] - sb0 / 2))) << 16 |
+            mask_pair_offset((uint32_t)(M.cols[e] - sa0 / 2));
     acc[j] = 0.f;
   }
   const uint8_t* ga = (const uint8_t*)M.A + ((int64_t)ex * M.T) * a_row;
   const uint8_t* gb = (const uint8_t*)M.B + ((int64_t)ex * M.T) * b_row;
-  // descriptors end at row t1: slots past the chunk land as zero
+  // descriptors end at row t1: token rows past the chunk read as zero
   const rsrc_t r_a = make_rsrc(ga, (uint32_t)((int64_t)t1 * a_row));
   const rsrc_t r_b = make_rsrc(gb, (uint32_t)((int64_t)t1 * b_row));
-  const int runs_a = (seg_a + 1023) >> 10, runs_b = (seg_b + 1023) >> 10;
-  const int n_st = t1 > t0 ? (t1 - t0 + kMaskSlotTokens - 1) / kMaskSlotTokens : 0;
-  // stage st into buffer st & 1: 1 KiB runs of each slot (bytes past a slice
-  // stay inside its slot), dealt to the 4 waves in turn.  A run's offset is
-  // wave-uniform plus the lane's 16 bytes, added per load into the vector
-  // offset (the descriptor's range check covers that operand only); the
-  // empty asm keeps the compiler from holding every run's offset in a register.
-  const int wv = __builtin_amdgcn_readfirstlane(wave);
-  const uint32_t lo = (uint32_t)lane * 16;
-  auto voff = [&](int run_off) {
-    uint32_t v = lo;
-    asm volatile("" : "+v"(v));
-    return v + (uint32_t)run_off;
+  // this thread's 16-byte chunk of each slice (features 8 tid .. 8 tid + 7);
+  // a chunk past its slice starts at 2^31, which with any token row's offset
+  // added stays past the descriptor's range (below 2^31 bytes), so it loads
+  // as zero into pair-row space no entry reads: no branches, so the loads'
+  // wait counts stay exact
+  constexpr uint32_t kPast = 0x80000000u;
+  const uint32_t ca = tid < (seg_a >> 4) ? (uint32_t)(sa0 + 16 * tid) : kPast;
+  const uint32_t cb = tid < (seg_b >> 4) ? (uint32_t)(sb0 + 16 * tid) : kPast;
+  constexpr int kTok = 2 * kMaskSlotPairs;  // tokens per stage
+  const int n_st = t1 > t0 ? (t1 - t0 + kTok - 1) / kTok : 0;
+  i32x4 xa[kTok], xb[kTok];  // the next stage's token rows (this thread's chunks)
+  auto at = [](uint32_t chunk, int row_off) {  // formed per load, not held in registers
+    asm volatile("" : "+v"(chunk));
+    return chunk + (uint32_t)row_off;
   };
-  auto issue = [&](int st) {
-    uint8_t* buf = stage + (st & 1) * kFixBuf;
-    const int ts = t0 + st * kMaskSlotTokens;
-    int q = 0;  // runs issued so far in this stage (uniform)
+  auto load = [&](int st) {
+    const int ts = t0 + kTok * st;
 #pragma unroll
-    for (int u = 0; u < kMaskSlotTokens; ++u) {
-      for (int c = (wv - q) & 3; c < runs_a; c += 4)
-        __builtin_amdgcn_raw_ptr_buffer_load_lds(r_a, LDS_PTR(buf + u * kMaskSlot + c * 1024), 16,
-                                                 voff((ts + u) * a_row + sa0 + c * 1024), 0, 0, 0);
-      q += runs_a;
-      for (int c = (wv - q) & 3; c < runs_b; c += 4)
-        __builtin_amdgcn_raw_ptr_buffer_load_lds(r_b, LDS_PTR(buf + (kMaskSlotTokens + u) * kMaskSlot + c * 1024),
-                                                 16, voff((ts + u) * b_row + sb0 + c * 1024), 0, 0, 0);
-      q += runs_b;
+    for (int u = 0; u < kTok; ++u) {
+      xa[u] = load16(r_a, at(ca, (ts + u) * a_row));
+      xb[u] = load16(r_b, at(cb, (ts + u) * b_row));
     }
   };
-  if (n_st > 0) issue(0);
+  auto store = [&](int p) {
+    uint8_t* buf = stage + p * kFixBuf;
+#pragma unroll
+    for (int q = 0; q < kMaskSlotPairs; ++q) {
+      i32x4 lo, hi;
+      pair_halves(xa[2 * q], xa[2 * q + 1], lo, hi);
+      *(i32x4*)(buf + q * kFixPairRows + 16 * tid) = lo;
+      *(i32x4*)(buf + q * kFixPairRows + kMaskSlot + 16 * tid) = hi;
+      pair_halves(xb[2 * q], xb[2 * q + 1], lo, hi);
+      *(i32x4*)(buf + q * kFixPairRows + kFixSide + 16 * tid) = lo;
+      *(i32x4*)(buf + q * kFixPairRows + kFixSide + kMaskSlot + 16 * tid) = hi;
+    }
+  };
+  if (n_st > 0) {
+    load(0);
+    store(0);
+  }
   for (int st = 0; st < n_st; st += 2) {  // uniform trip count; buffers 0 and 1 in turn
-    wait_vm0();        // this wave's loads of stage st have landed
-    __syncthreads();   // every wave's have; buffer 1's readers are done
-    if (st + 1 < n_st) issue(st + 1);
-    gather_slots<0>(stage, la, lb, acc);
+    __syncthreads();  // buffer 0 written; buffer 1's readers are done
+    if (st + 1 < n_st) load(st + 1);
+    gather_pairs<0>(stage, rc, acc);
     if (st + 1 >= n_st) break;
-    wait_vm0();
+    store(1);
     __syncthreads();
-    if (st + 2 < n_st) issue(st + 2);
-    gather_slots<1>(stage, la, lb, acc);
+    if (st + 2 < n_st) load(st + 2);
+    gather_pairs<1>(stage, rc, acc);
+    if (st + 2 < n_st) store(0);
   }
   float* dst = partials + M.partial_base + ((int64_t)ex * M.n_chunks + it.chunk) * M.m;
+  const int32_t* pos = M.pos + e0;
+  uint32_t t = (uint32_t)tid;
+  asm volatile("" : "+v"(t));  // the entry indices are formed here, not held through the loop
 #pragma unroll
-  for (int j = 0; j < kMaskPerThread; ++j) dst[M.pos[e0 + tid + 256 * j]] = acc[j];
+  for (int j = 0; j < kFixPer; ++j) dst[pos[t + (uint32_t)kFixThreads * j]] = acc[j];
 }
 
 hipError_t launch_mask_fixed(const MaskItem* items, int n_items, const MaskTask* tasks, float* partials,
@@ -364,7 +413,7 @@ hipError_t launch_mask_fixed(const MaskItem* items, int n_items, const MaskTask*
   const hipError_t e = hipFuncSetAttribute((const void*)mask_fixed_kernel,
                                            hipFuncAttributeMaxDynamicSharedMemorySize, (int)kMaskSlotLds);
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(mask_fixed_kernel, dim3((unsigned)n_items), dim3(256), kMaskSlotLds, s, items, tasks,
+  hipLaunchKernelGGL(mask_fixed_kernel, dim3((unsigned)n_items), dim3(kFixThreads), kMaskSlotLds, s, items, tasks,
                      partials);
   return hipGetLastError();
 }

@@ -822,10 +822,11 @@ dattri_status dattri::build_plan(const dattri_ctx* ctx, dattri_route forced, Pla
       M.aligned = ((uintptr_t)L.A % 16 == 0) && ((uintptr_t)L.B % 16 == 0) && (L.d_in * elt) % 16 == 0 &&
                   (L.d_out * elt) % 16 == 0;
       // whole groups take the fixed-slot gather when every one's slices fit a slot
-      M.fixed = M.aligned && elt == 2 && L.k_out >= kMaskGroup &&
-                L.mask_slices.size() >= (size_t)4 * (L.k_out / kMaskGroup);  // bound
-      for (int g = 0; M.fixed && g < L.k_out / kMaskGroup; ++g)
-        M.fixed = L.mask_slices[4 * g + 1] <= kMaskSlot && L.mask_slices[4 * g + 3] <= kMaskSlot;
+      // (and each example's factor blocks below 2 GiB: its chunk offsets past a
+      // slice start at 2^31)
+      M.fixed = M.aligned && L.mask_slices.size() >= (size_t)4 * (L.k_out / kMaskGroup) &&  // bound
+                (int64_t)L.T * std::max(L.d_in, L.d_out) * elt < ((int64_t)1 << 31) &&
+                mask_fixed_layout(elt, L.d_in, L.d_out, L.k_out, L.mask_slices.data());
       M.partial_base = (int64_t)mask_floats;
       mask_floats += (size_t)n * M.n_chunks * M.m;
       // aligned: two buffers of [A part | B part], parts rounded up to 1 KiB; else one buffer
@@ -1030,6 +1031,17 @@ hipError_t dattri::place_table(const dattri_ctx* ctx, TableKind kind, const std:
   return e;
 }
 
+// Whether a mask layer's whole groups take the fixed-slot gather (bf16 rows
+// of whole 16-byte chunks, every whole group's A and B slices at most
+// kMaskSlot bytes); slices as in the layer's entry table.  The planner adds
+// the captures' alignment.
+bool dattri::mask_fixed_layout(int elt, int d_in, int d_out, int m, const int32_t* slices) {
+  if (elt != 2 || (d_in * elt) % 16 || (d_out * elt) % 16 || m < kMaskGroup) return false;
+  for (int g = 0; g < m / kMaskGroup; ++g)
+    if (slices[4 * g + 1] > kMaskSlot || slices[4 * g + 3] > kMaskSlot) return false;
+  return true;
+}
+
 namespace {
 
 dattri_status check_layer(const dattri_ctx* ctx, int32_t layer) {
@@ -1045,18 +1057,21 @@ dattri_status check_layer(const dattri_ctx* ctx, int32_t layer) {
 // both ends on 16-byte boundaries (the row's end for rows that are not a
 // multiple of 16 bytes).
 // Entries are placed into the gather kernel's slots group by group (groups of
-// kMaskGroup entries; slot e of a group is read by thread e % 256 at step
-// e / 256, so slots 32h .. 32h + 31 form the half-wave h of one LDS read).
+// kMaskGroup entries; slot e of a group is read by thread e % W at step
+// e / W for W = 256 or 512 threads, so slots 32h .. 32h + 31 form the
+// half-wave h of one LDS read).
 // A layer with more than one group deals its entries to the groups in order
 // of their index on the wider side of DW (rows when d_out >= d_in, else
 // columns; equal indices in mask order): each group's entries then span about
 // 1/groups of that side, and the kernel stages only that slice of each token
-// row instead of the whole row.  Inside a group, each entry goes to the first half-wave
-// where neither its A word nor its B word meets another word in the same
-// bank (32 banks of 4 bytes; a word already there is read once for all its
-// lanes), else one where one of the two does not, else any with room; so
-// most gathers are free of bank conflicts.  pos[slot] is the entry's index in
-// mask order, where the kernel writes its sum.
+// row instead of the whole row.  Inside a group, each entry goes to the first
+// half-wave where neither its A word nor its B word meets another word in the
+// same bank (32 banks of 4 bytes; a word already there is read once for all
+// its lanes), else one where one of the two does not, else any with room; so
+// most gathers are free of bank conflicts.  The words are those the group's
+// kernel reads: a 4-byte token pair per feature for the fixed-slot gather
+// (mask_fixed_layout), the element's own word otherwise.  pos[slot] is the
+// entry's index in mask order, where the kernel writes its sum.
 void mask_slot_table(const std::vector<int32_t>& rows, const std::vector<int32_t>& cols, int d_in, int d_out,
                      int elt, std::vector<int32_t>& table) {
   const int m = (int)rows.size(), n_groups = (m + kMaskGroup - 1) / kMaskGroup;
@@ -1064,6 +1079,31 @@ void mask_slot_table(const std::vector<int32_t>& rows, const std::vector<int32_t
   int32_t* t_rows = table.data();
   int32_t* t_cols = table.data() + m;
   int32_t* t_pos = table.data() + 2 * (size_t)m;
+  std::vector<int32_t> order((size_t)m);
+  for (int i = 0; i < m; ++i) order[i] = i;
+  if (m > kMaskGroup) {
+    const std::vector<int32_t>& key = d_out >= d_in ? rows : cols;
+    std::stable_sort(order.begin(), order.end(), [&](int32_t a, int32_t b) { return key[a] < key[b]; });
+  }
+  int32_t* slices = table.data() + 3 * (size_t)m;
+  for (int g = 0; g < n_groups; ++g) {
+    const int e0 = g * kMaskGroup, N = std::min(kMaskGroup, m - e0);
+    int32_t lo_r = d_out, hi_r = -1, lo_c = d_in, hi_c = -1;
+    for (int i = 0; i < N; ++i) {
+      const int32_t e = order[e0 + i];
+      lo_r = std::min(lo_r, rows[e]); hi_r = std::max(hi_r, rows[e]);
+      lo_c = std::min(lo_c, cols[e]); hi_c = std::max(hi_c, cols[e]);
+    }
+    auto slice = [&](int32_t lo, int32_t hi, int d, int32_t* out) {
+      const int64_t b0 = ((int64_t)lo * elt) & ~(int64_t)15;
+      const int64_t b1 = std::min(((int64_t)(hi + 1) * elt + 15) & ~(int64_t)15, (int64_t)d * elt);
+      out[0] = (int32_t)b0;
+      out[1] = (int32_t)(b1 - b0);
+    };
+    slice(lo_c, hi_c, d_in, slices + 4 * g);
+    slice(lo_r, hi_r, d_out, slices + 4 * g + 2);
+  }
+  const bool pairs = mask_fixed_layout(elt, d_in, d_out, m, slices);
   constexpr int kHalf = 32, kMaxHalves = kMaskGroup / kHalf, kW = kMaxHalves / 64;
   struct Bits {
     uint64_t w[kW];
@@ -1074,18 +1114,14 @@ void mask_slot_table(const std::vector<int32_t>& rows, const std::vector<int32_t
     return -1;
   };
   // per factor side: word -> index into `holders` (the half-waves holding that word)
-  std::vector<int32_t> slot_of[2] = {std::vector<int32_t>((size_t)(((int64_t)d_in * elt + 3) / 4), -1),
-                                     std::vector<int32_t>((size_t)(((int64_t)d_out * elt + 3) / 4), -1)};
+  std::vector<int32_t> slot_of[2] = {std::vector<int32_t>((size_t)d_in, -1), std::vector<int32_t>((size_t)d_out, -1)};
   std::vector<Bits> holders[2];
   std::vector<int32_t> touched[2];
-  std::vector<int32_t> order((size_t)m);
-  for (int i = 0; i < m; ++i) order[i] = i;
-  if (m > kMaskGroup) {
-    const std::vector<int32_t>& key = d_out >= d_in ? rows : cols;
-    std::stable_sort(order.begin(), order.end(), [&](int32_t a, int32_t b) { return key[a] < key[b]; });
-  }
   for (int e0 = 0; e0 < m; e0 += kMaskGroup) {
     const int N = std::min(kMaskGroup, m - e0), H = (N + kHalf - 1) / kHalf;
+    // fixed-slot groups read one word per feature (a token pair, placed by
+    // mask_pair_offset), others the word holding the element
+    const bool pw = pairs && N == kMaskGroup;
     Bits all{};
     for (int h = 0; h < H; ++h) all.w[h >> 6] |= 1ull << (h & 63);
     Bits free_bank[2][kHalf], room = all;
@@ -1094,10 +1130,16 @@ void mask_slot_table(const std::vector<int32_t>& rows, const std::vector<int32_t
     int fill[kMaxHalves] = {0};
     for (int i = 0; i < N; ++i) {
       const int32_t e = order[e0 + i];
-      const int32_t word[2] = {(int32_t)(((int64_t)cols[e] * elt) >> 2), (int32_t)(((int64_t)rows[e] * elt) >> 2)};
+      const int32_t word[2] = {pw ? cols[e] : (int32_t)(((int64_t)cols[e] * elt) >> 2),
+                               pw ? rows[e] : (int32_t)(((int64_t)rows[e] * elt) >> 2)};
+      // a slice starts on 16 bytes (8 features), so the banks of a group's
+      // pair words are those of the absolute feature index, rotated alike
+      int bank[2];
+      for (int side = 0; side < 2; ++side)
+        bank[side] = pw ? (int)(mask_pair_offset((uint32_t)word[side]) >> 2) % kHalf : word[side] % kHalf;
       Bits ok[2];
       for (int side = 0; side < 2; ++side) {
-        ok[side] = free_bank[side][word[side] % kHalf];
+        ok[side] = free_bank[side][bank[side]];
         const int32_t hs = slot_of[side][word[side]];
         if (hs >= 0)
           for (int k = 0; k < kW; ++k) ok[side].w[k] |= holders[side][hs].w[k];
@@ -1114,7 +1156,7 @@ void mask_slot_table(const std::vector<int32_t>& rows, const std::vector<int32_t
       const int slot = h * kHalf + fill[h]++;
       if (fill[h] == std::min(kHalf, N - h * kHalf)) room.w[h >> 6] &= ~bit;
       for (int side = 0; side < 2; ++side) {
-        Bits& fb = free_bank[side][word[side] % kHalf];
+        Bits& fb = free_bank[side][bank[side]];
         if (fb.w[h >> 6] & bit) {  // the bank was empty: this word now holds it
           fb.w[h >> 6] &= ~bit;
           int32_t& hs = slot_of[side][word[side]];
@@ -1130,21 +1172,6 @@ void mask_slot_table(const std::vector<int32_t>& rows, const std::vector<int32_t
       t_cols[e0 + slot] = cols[e];
       t_pos[e0 + slot] = e;
     }
-    int32_t lo_r = d_out, hi_r = -1, lo_c = d_in, hi_c = -1;
-    for (int i = 0; i < N; ++i) {
-      const int32_t e = order[e0 + i];
-      lo_r = std::min(lo_r, rows[e]); hi_r = std::max(hi_r, rows[e]);
-      lo_c = std::min(lo_c, cols[e]); hi_c = std::max(hi_c, cols[e]);
-    }
-    auto slice = [&](int32_t lo, int32_t hi, int d, int32_t* out) {
-      const int64_t b0 = ((int64_t)lo * elt) & ~(int64_t)15;
-      const int64_t b1 = std::min(((int64_t)(hi + 1) * elt + 15) & ~(int64_t)15, (int64_t)d * elt);
-      out[0] = (int32_t)b0;
-      out[1] = (int32_t)(b1 - b0);
-    };
-    int32_t* g = table.data() + 3 * (size_t)m + 4 * (size_t)(e0 / kMaskGroup);
-    slice(lo_c, hi_c, d_in, g);
-    slice(lo_r, hi_r, d_out, g + 2);
     for (int side = 0; side < 2; ++side) {  // reset the word index for the next group
       for (int32_t w : touched[side]) slot_of[side][w] = -1;
       touched[side].clear();

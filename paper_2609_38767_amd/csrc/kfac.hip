@@ -5,8 +5,9 @@
 // fsum_kernel        sum over token rows of x~ x~^T with x~ = P^T x, for one
 //                    side of a layer (x = a_t with P_in, or g_t with P_out).
 //                    Token rows are projected exactly as in the factored route
-//                    (project_rows: bf16/f32 MFMA on fragments streamed from
-//                    HBM, map panels shared through LDS); the projected tiles
+//                    (bf16/f32 MFMA; bf16 aligned rows streamed through LDS by
+//                    direct loads, project_rows_dma, else fragments loaded into
+//                    registers with map panels in LDS, project_rows); the projected tiles
 //                    stay in accumulators and their outer products are summed
 //                    with float32 MFMA (16x16x4), whose C layout gives every
 //                    element index a K = 4 slice of token rows for both
@@ -30,6 +31,9 @@ using namespace dev;
 
 // ------------------------------------------------------------ factor sums
 constexpr int fsum_rt(int nt) { return nt <= 2 ? 4 : 2; }
+// bf16 sides with aligned rows and 2 or 4 map tiles stream their factor rows
+// through LDS by direct loads (project_rows_dma), as the factored route does
+constexpr bool fsum_dma(int elt, bool aligned, int nt) { return elt == 2 && aligned && (nt == 2 || nt == 4); }
 
 template <int ELT, bool AL, int NT>
 __global__ __launch_bounds__(256, 2) void fsum_kernel(const FsumItem* __restrict__ items,
@@ -37,7 +41,12 @@ __global__ __launch_bounds__(256, 2) void fsum_kernel(const FsumItem* __restrict
                                                       float* __restrict__ partials) {
   constexpr int RT = fsum_rt(NT);
   constexpr int PD = AL ? (RT >= 4 ? 2 : 4) : 2;
-  __shared__ __align__(16) uint8_t pan[2][kPanel][NT][kFragBytes];
+  constexpr bool kDma = fsum_dma(ELT, AL, NT);
+  constexpr int kPanBytes = 2 * kPanel * NT * kFragBytes;
+  constexpr int kSmem = kDma ? DmaLds<RT, kDma ? NT : 2>::kBytes : kPanBytes;
+  static_assert(kSmem <= 80 * 1024, "two workgroups per CU");
+  __shared__ __align__(1024) uint8_t smem[kSmem];
+  auto pan = reinterpret_cast<uint8_t(*)[kPanel][NT][kFragBytes]>(smem);
   const FsumItem it = items[blockIdx.x];
   if (it.n_units <= 0) return;  // padding item of the XCD-interleaved order
   const FsumOp& O = ops[it.op];
@@ -75,7 +84,10 @@ __global__ __launch_bounds__(256, 2) void fsum_kernel(const FsumItem* __restrict
       for (int rt = 0; rt < RT; ++rt)
 #pragma unroll
         for (int t = 0; t < NT; ++t) acc[rt][t] = f32x4{0.f, 0.f, 0.f, 0.f};
-      project_rows<ELT, AL, RT, NT, NT, PD>(r, r_wave, rows_valid, d, d, P, acc, pan);
+      if constexpr (kDma)
+        project_rows_dma<RT, NT>(r, r_wave, rows_valid, d, d, P, acc, smem);
+      else
+        project_rows<ELT, AL, RT, NT, NT, PD>(r, r_wave, rows_valid, d, d, P, acc, pan);
 #pragma unroll
       for (int rt = 0; rt < RT; ++rt)
 #pragma unroll

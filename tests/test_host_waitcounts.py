@@ -115,6 +115,28 @@ def test_direct_load_projection_waits(factored_asm, na, nb):
     assert counts == {0, k_a, k_b}, (counts, k_a, k_b)
 
 
+@pytest.fixture(scope="module")
+def kfac_asm():
+    return _asm("kfac.hip")
+
+
+@pytest.mark.parametrize("nt,rt", [(2, 4), (4, 2)])
+def test_direct_load_factor_sum_waits(kfac_asm, nt, rt):
+    # The factor-sum pass's bf16 instances stream rows by the same
+    # project_rows_dma (inlined once per kernel, RT row tiles per wave): each
+    # stage issues k = 2 RT row-group loads + NT / 2 map-fragment loads, the
+    # text holds 3 k direct loads with nothing else among them, and the only
+    # vmcnt waits are k and 0.
+    body = _body(kfac_asm, f"_ZN6dattri11fsum_kernelILi2ELb1ELi{nt}E")
+    ev = [e for e in _events(body) if isinstance(e, str)]
+    k = 2 * rt + nt // 2
+    d_pos = [i for i, e in enumerate(ev) if e == "D"]
+    assert len(d_pos) == 3 * k, (len(d_pos), k)
+    assert all(e == "D" for e in ev[d_pos[0]:d_pos[-1] + 1]), "".join(ev)
+    counts = {int(m.group(1)) for t in body for m in [re.match(r"s_waitcnt vmcnt\((\d+)\)$", t)] if m}
+    assert counts <= {0, k} and k in counts, (counts, k)
+
+
 @pytest.mark.parametrize("src,sym", [("gradient_tr.hip", "_ZN6dattri18gradient_tr_kernel"),
                                      ("xone.hip", "_ZN6dattri11xone_kernel"),
                                      ("gfused.hip", "_ZN6dattri13gfused_kernelILi1E"),

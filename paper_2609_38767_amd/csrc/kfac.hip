@@ -602,68 +602,121 @@ __device__ inline void zero_lds(float* M) {
   for (int e = threadIdx.x; e < kCurvMaxK * kLd; e += 256) M[e] = 0.f;
 }
 
-__global__ __launch_bounds__(256) void ekfac_kernel(const RotTask* __restrict__ tasks,
-                                                    const uint8_t* __restrict__ state,
-                                                    const void* __restrict__ phi, int phi_bf16,
-                                                    int64_t ld, int64_t n, int rpb,
-                                                    float* __restrict__ parts) {
+// EK-FAC rotation on float32 MFMA (32x32x2: lane l holds A[l % 32][l / 32]
+// and B[l / 32][l % 32]; C element v of lane l is row 8 (v / 4) + 4 (l / 32)
+// + v % 4, column l % 32).  One wave per training row, all k padded to 64:
+//   Y1^T[b][c] = sum_a Psi[a][b] QA[a][c]  (M = b, N = c, K = a),
+//   Y^T[r][c]  = sum_b QG[b][r] Y1^T[b][c] (M = r, N = c, K = b).
+// The sum over b may take b in any order, so the second product's K step v
+// of b-tile tb takes, in lane half h, b = 32 tb + 8 (v / 4) + 4 h + v % 4:
+// its B operand is then exactly C element v of Y1^T's tile, with no data
+// movement, and its A operand is QG[b][r] read from LDS.  Each wave sums
+// Y^T squared over its rows; the four waves' sums are added in a fixed order.
+__global__ __launch_bounds__(256, 2) void ekfac_kernel(const RotTask* __restrict__ tasks,
+                                                       const uint8_t* __restrict__ state,
+                                                       const void* __restrict__ phi, int phi_bf16,
+                                                       int64_t ld, int64_t n, int rpb,
+                                                       float* __restrict__ parts) {
   __shared__ __align__(16) float QA[kCurvMaxK * kLd];
   __shared__ __align__(16) float QG[kCurvMaxK * kLd];
-  __shared__ __align__(16) float X[kCurvMaxK * kLd];
-  __shared__ __align__(16) float YT[kCurvMaxK * kLd];
   const RotTask t = tasks[blockIdx.y];
   if ((int)blockIdx.x >= t.n_blocks) return;
   const int ki = t.k_in, ko = t.k_out, tid = threadIdx.x;
-  // thread tile: 4 x 4 elements (c0.., r0..) of the k_in x k_out block
-  const int nro = (ko + 3) / 4, nci = (ki + 3) / 4;
-  const int ci = tid / nro, ri = tid - (tid / nro) * nro;
-  const bool active = ci < nci;
-  const int c0 = 4 * ci, r0 = 4 * ri;
+  const int lane = tid & 63, wave = tid >> 6, l32 = lane & 31, h = lane >> 5;
   zero_lds(QA);
   zero_lds(QG);
-  zero_lds(X);
-  zero_lds(YT);
   __syncthreads();
   load_mat(QA, nullptr, (const float*)(state + t.q_a), ki, ki);
   load_mat(QG, nullptr, (const float*)(state + t.q_g), ko, ko);
-  float acc[4][4];
+  __syncthreads();
+  f32x16 acc[2][2];  // [r tile][c tile] of this wave's sum of Y^T squared
 #pragma unroll
-  for (int i = 0; i < 4; ++i)
+  for (int x = 0; x < 2; ++x)
 #pragma unroll
-    for (int j = 0; j < 4; ++j) acc[i][j] = 0.f;
+    for (int y = 0; y < 2; ++y)
+#pragma unroll
+      for (int v = 0; v < 16; ++v) acc[x][y][v] = 0.f;
   const int64_t e0 = (int64_t)blockIdx.x * rpb;
   const int64_t e1 = min(n, e0 + rpb);
-  for (int64_t e = e0; e < e1; ++e) {
-    __syncthreads();  // the previous row's readers of X and YT are done
-    for (int idx = tid; idx < ki * ko; idx += 256) {
-      const int c = idx / ko, r = idx - (idx / ko) * ko;
-      X[c * kLd + r] = load_elem(phi, phi_bf16, e * ld + t.col + idx);
-    }
-    __syncthreads();
-    float y[4][4];
-    if (active) {  // Y1 = Q_A^T Psi, stored transposed
-      mm4(QA, X, ki, c0, r0, y);
+  // Psi[a][b] for this lane: a = 2 s + h (s < 32), b = 32 tb + l32, read
+  // through a descriptor over the row's block (zero outside ki x ko); the
+  // offsets are formed at each load, not held in registers
+  const int elt = phi_bf16 ? 2 : 4;
+  const uint32_t lane_off = (uint32_t)((h * ko + l32) * elt);
+  float ps[2][32];
+  auto load_psi = [&](int64_t e) {
+    const rsrc_t r = make_rsrc((const uint8_t*)phi + (e * ld + t.col) * elt, (uint32_t)(ki * ko * elt));
 #pragma unroll
-      for (int i = 0; i < 4; ++i)
+    for (int tb = 0; tb < 2; ++tb)
 #pragma unroll
-        for (int j = 0; j < 4; ++j) YT[(r0 + j) * kLd + c0 + i] = y[i][j];
-    }
-    __syncthreads();
-    if (active) {  // Y = Y1 Q_G
-      mm4(YT, QG, ko, c0, r0, y);
+      for (int s2 = 0; s2 < 32; ++s2) {
+        uint32_t off = lane_off;
+        asm volatile("" : "+v"(off));
+        off += (uint32_t)((2 * s2 * ko + 32 * tb) * elt);
+        if (2 * s2 + h >= ki || 32 * tb + l32 >= ko) off = kOOB;
+        ps[tb][s2] = phi_bf16 ? bf16_bits_to_f32((uint16_t)load2(r, off)) : __builtin_bit_cast(float, load4(r, off));
+      }
+  };
+  for (int64_t e = e0 + wave; e < e1; e += kWaves) {
+    load_psi(e);
+    f32x16 y1[2][2];  // Y1^T [b tile][c tile]
 #pragma unroll
-      for (int i = 0; i < 4; ++i)
+    for (int tb = 0; tb < 2; ++tb)
 #pragma unroll
-        for (int j = 0; j < 4; ++j) acc[i][j] = fmaf(y[i][j], y[i][j], acc[i][j]);
-    }
+      for (int tc = 0; tc < 2; ++tc) {
+#pragma unroll
+        for (int v = 0; v < 16; ++v) y1[tb][tc][v] = 0.f;
+#pragma unroll
+        for (int s2 = 0; s2 < 32; ++s2)
+          y1[tb][tc] = __builtin_amdgcn_mfma_f32_32x32x2f32(ps[tb][s2], QA[(2 * s2 + h) * kLd + 32 * tc + l32],
+                                                            y1[tb][tc], 0, 0, 0);
+      }
+#pragma unroll
+    for (int tr = 0; tr < 2; ++tr)
+#pragma unroll
+      for (int tc = 0; tc < 2; ++tc) {
+        f32x16 y;
+#pragma unroll
+        for (int v = 0; v < 16; ++v) y[v] = 0.f;
+#pragma unroll
+        for (int tb = 0; tb < 2; ++tb)
+#pragma unroll
+          for (int v = 0; v < 16; ++v) {
+            const int b = 32 * tb + 8 * (v >> 2) + 4 * h + (v & 3);
+            y = __builtin_amdgcn_mfma_f32_32x32x2f32(QG[b * kLd + 32 * tr + l32], y1[tb][tc][v], y, 0, 0, 0);
+          }
+#pragma unroll
+        for (int v = 0; v < 16; ++v) acc[tr][tc][v] = fmaf(y[v], y[v], acc[tr][tc][v]);
+      }
   }
-  if (active) {
-    float* dst = parts + t.part_base + (int64_t)blockIdx.x * ki * ko;
+  // fixed-order sum of the four waves' blocks: slot w % 2 gets wave w, then
+  // wave w + 2 adds to it, then the two slots are added (QA/QG reused)
+  float* slot = (wave & 1) ? QG : QA;
+  auto at = [&](int tr, int tc, int v) { return (32 * tc + l32) * kLd + 32 * tr + 8 * (v >> 2) + 4 * h + (v & 3); };
+  __syncthreads();
+  if (wave < 2) {
 #pragma unroll
-    for (int i = 0; i < 4; ++i)
+    for (int tr = 0; tr < 2; ++tr)
 #pragma unroll
-      for (int j = 0; j < 4; ++j)
-        if (c0 + i < ki && r0 + j < ko) dst[(c0 + i) * ko + r0 + j] = acc[i][j];
+      for (int tc = 0; tc < 2; ++tc)
+#pragma unroll
+        for (int v = 0; v < 16; ++v) slot[at(tr, tc, v)] = acc[tr][tc][v];
+  }
+  __syncthreads();
+  if (wave >= 2) {
+#pragma unroll
+    for (int tr = 0; tr < 2; ++tr)
+#pragma unroll
+      for (int tc = 0; tc < 2; ++tc)
+#pragma unroll
+        for (int v = 0; v < 16; ++v) slot[at(tr, tc, v)] += acc[tr][tc][v];
+  }
+  __syncthreads();
+  // slot element (c, r) at c * kLd + r; the layer's partial block is c * ko + r
+  float* dst = parts + t.part_base + (int64_t)blockIdx.x * ki * ko;
+  for (int idx = tid; idx < ki * ko; idx += 256) {
+    const int c = idx / ko, r = idx - (idx / ko) * ko;
+    dst[idx] = QA[c * kLd + r] + QG[c * kLd + r];
   }
 }
 

@@ -400,7 +400,7 @@ struct TokTask {
   int64_t a_ld, b_ld, q_off;
   int32_t a_col0, b_col0, k_in, k_out;
 };
-constexpr int kTokTokens = 64;   // token positions per workgroup (32 for a single query row)
+constexpr int kTokTokens = 128;  // token positions per workgroup (32 per wave)
 constexpr int kTokQueries = 4;   // queries per workgroup
 hipError_t launch_token_scores(const TokTask* tasks, int n_tasks, const void* phi_q, int q_bf16, int64_t ld_q,
                                int64_t n_q, int64_t n, int T, float* out, hipStream_t s);

@@ -294,111 +294,126 @@ __device__ inline float load_elem(const void* p, int bf16, int64_t i);
 // layers in layer order and the parts are added in part order at the end
 // (deterministic).  One query row takes TT = 32 (twice the workgroups, so two
 // share a CU and hide each other's per-layer load latency).
-constexpr int kTokPad = kCurvMaxK + 4;  // row stride of the a~ / g~ tiles (16-byte rows, no conflicts)
+// Token contributions a~_t^T R g~_t on float32 MFMA (32x32x2; layouts as
+// for ekfac_kernel).  A workgroup holds kTokTokens token positions of one
+// example, 32 per wave, and QS query rows; per layer, for each query,
+//   Y[t][c] = sum_r g~_t[r] R[c][r]   (M = t, N = c, K = r; g~ rows and the
+// query block R in LDS with 65-float rows, so every operand read is free of
+// bank conflicts), and the lane holding Y[t][c] adds a~_t[c] Y[t][c], a~
+// read straight from the kept rows (32 lanes read 128 contiguous bytes).  The
+// next layer's rows and query blocks are loaded while a layer is computed;
+// the sums over c are taken once at the end, in a fixed butterfly order.
+constexpr int kTokRow = kCurvMaxK + 1;  // LDS row pitch (floats)
+static_assert(kTokTokens == kWaves * 32, "32 token positions per wave");
 
-template <int QS, int TT>
+template <int QS>
 __global__ __launch_bounds__(256, QS == 1 ? 2 : 1) void token_kernel(const TokTask* __restrict__ tasks, int n_tasks,
                                                     const void* __restrict__ phi_q, int q_bf16, int64_t ld_q,
                                                     int64_t n_q, int64_t n, int T, float* __restrict__ out) {
-  constexpr int K = kCurvMaxK, PER_Q = K * K / 256, PER_R = TT * K / 256;
-  constexpr int SLOTS = 256 / TT, PARTS = SLOTS / QS;
-  static_assert(SLOTS % QS == 0 && PER_R >= 1, "token tiling");
-  __shared__ __align__(16) float R[QS][K * K];
-  __shared__ __align__(16) float Ar[TT][kTokPad];
-  __shared__ __align__(16) float Br[TT][kTokPad];
-  __shared__ float part_sum[SLOTS][TT];
-  const int tid = threadIdx.x;
-  const int t0 = blockIdx.x * TT;
+  constexpr int K = kCurvMaxK, PER_Q = K * K / 256;
+  __shared__ float R[QS][K * kTokRow];
+  __shared__ float G[kWaves][32 * kTokRow];
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, l32 = lane & 31, h = lane >> 5;
+  const int tw = blockIdx.x * kTokTokens + 32 * wave;  // this wave's first token position
   const int64_t ex = blockIdx.y, q0 = (int64_t)blockIdx.z * QS;
-  const int tl = tid % TT, slot = tid / TT;  // uniform over each run of TT lanes (half a wave at TT = 32)
-  const int ql = slot / PARTS, part = slot - ql * PARTS;
 
-  float rq[QS][PER_Q], ra[PER_R], rb[PER_R];  // element e = tid + 256 j of each tile
+  // prefetch registers: query block elements e = tid + 256 j (row c = e / 64,
+  // col r = e % 64); g~ row j of the wave at lane r = lane; a~[t][c] for the
+  // lane's C elements (t = 8 (v / 4) + 4 h + v % 4, c = 32 tc + l32)
+  float rq[QS][PER_Q], rg[32], ra[2][16];
+  // buffer offsets are formed at each load (not held in registers); rows past
+  // the example's length and columns past k read as zero (out of range)
+  auto fresh = [](uint32_t x) {
+    asm volatile("" : "+v"(x));
+    return x;
+  };
   auto load = [&](int l) {
     const TokTask tk = tasks[l];
     const int ki = tk.k_in, ko = tk.k_out;
     int t_eff = T;
     if (tk.lengths) t_eff = min(max(tk.lengths[ex], 0), T);
+    const int rows = max(0, min(t_eff, tw + 32) - tw);  // this wave's valid positions
+    const rsrc_t rb = make_rsrc(tk.b_rows + ((ex * T + tw) * tk.b_ld + tk.b_col0), (uint32_t)(rows * tk.b_ld * 4));
+    const rsrc_t ra_ = make_rsrc(tk.a_rows + ((ex * T + tw) * tk.a_ld + tk.a_col0), (uint32_t)(rows * tk.a_ld * 4));
+    const uint32_t gb = lane < ko ? (uint32_t)lane * 4 : kOOB;
 #pragma unroll
-    for (int j = 0; j < PER_R; ++j) {
-      const int e = tid + 256 * j, row = e / K, col = e % K;  // a~ / g~ tile: row = token, col = c or r
-      const bool tok = t0 + row < t_eff;
-      const int64_t base = (ex * T + t0 + row);
-      ra[j] = tok && col < ki ? tk.a_rows[base * tk.a_ld + tk.a_col0 + col] : 0.f;
-      rb[j] = tok && col < ko ? tk.b_rows[base * tk.b_ld + tk.b_col0 + col] : 0.f;
+    for (int j = 0; j < 32; ++j)
+      rg[j] = __builtin_bit_cast(float, load4(rb, gb == kOOB ? kOOB : fresh(gb) + (uint32_t)(j * tk.b_ld * 4)));
+    const uint32_t ta = (uint32_t)((4 * h) * tk.a_ld * 4);
+#pragma unroll
+    for (int tc = 0; tc < 2; ++tc) {
+      const int c = 32 * tc + l32;
+#pragma unroll
+      for (int v = 0; v < 16; ++v) {
+        const uint32_t off = fresh(ta + (uint32_t)c * 4) + (uint32_t)((8 * (v >> 2) + (v & 3)) * tk.a_ld * 4);
+        ra[tc][v] = __builtin_bit_cast(float, load4(ra_, c < ki ? off : kOOB));
+      }
     }
+    const int qe = q_bf16 ? 2 : 4;
 #pragma unroll
-    for (int j = 0; j < PER_Q; ++j) {
-      const int e = tid + 256 * j, row = e / K, col = e % K;  // R tile: row = c, col = r
+    for (int qq = 0; qq < QS; ++qq) {
+      const int64_t qrow = q0 + qq;
+      const rsrc_t rqs = make_rsrc((const uint8_t*)phi_q + (qrow * ld_q + tk.q_off) * qe,
+                                   qrow < n_q ? (uint32_t)(ki * ko * qe) : 0u);
 #pragma unroll
-      for (int qq = 0; qq < QS; ++qq) {
-        const int64_t qrow = q0 + qq;
-        rq[qq][j] = qrow < n_q && row < ki && col < ko
-                        ? load_elem(phi_q, q_bf16, qrow * ld_q + tk.q_off + (int64_t)row * ko + col)
-                        : 0.f;
+      for (int j = 0; j < PER_Q; ++j) {
+        const int e = tid + 256 * j, c = e / K, r = e % K;
+        const uint32_t off = c < ki && r < ko ? fresh((uint32_t)(c * ko + r) * qe) : kOOB;
+        rq[qq][j] = q_bf16 ? bf16_bits_to_f32((uint16_t)load2(rqs, off)) : __builtin_bit_cast(float, load4(rqs, off));
       }
     }
   };
 
-  float acc = 0.f;
+  float acc[QS][16];  // per query: the lane's share of each of its 16 token positions
+#pragma unroll
+  for (int qq = 0; qq < QS; ++qq)
+#pragma unroll
+    for (int v = 0; v < 16; ++v) acc[qq][v] = 0.f;
   if (n_tasks > 0) load(0);
   for (int l = 0; l < n_tasks; ++l) {  // uniform trip count
-    const int ki = tasks[l].k_in;
     __syncthreads();  // the previous layer's readers are done
 #pragma unroll
-    for (int j = 0; j < PER_R; ++j) {
-      const int e = tid + 256 * j, row = e / K, col = e % K;
-      Ar[row][col] = ra[j];
-      Br[row][col] = rb[j];
+    for (int j = 0; j < 32; ++j) G[wave][j * kTokRow + lane] = rg[j];
+#pragma unroll
+    for (int j = 0; j < PER_Q; ++j) {
+      const int e = tid + 256 * j;
+#pragma unroll
+      for (int qq = 0; qq < QS; ++qq) R[qq][(e / K) * kTokRow + e % K] = rq[qq][j];
     }
+    float a[2][16];
 #pragma unroll
-    for (int j = 0; j < PER_Q; ++j)
+    for (int tc = 0; tc < 2; ++tc)
 #pragma unroll
-      for (int qq = 0; qq < QS; ++qq) R[qq][tid + 256 * j] = rq[qq][j];
+      for (int v = 0; v < 16; ++v) a[tc][v] = ra[tc][v];
     __syncthreads();
     if (l + 1 < n_tasks) load(l + 1);
-
-    float g[K];
+    const float* g = G[wave] + l32 * kTokRow + h;
 #pragma unroll
-    for (int r = 0; r < K; r += 4) {
-      const float4 v = *reinterpret_cast<const float4*>(&Br[tl][r]);
-      g[r] = v.x; g[r + 1] = v.y; g[r + 2] = v.z; g[r + 3] = v.w;
-    }
-    // c in groups of 4 (the tiles are zero past k_in), split over the parts
-    const int n4 = (ki + 3) / 4;
-    const int c0 = 4 * (part * n4 / PARTS), c1 = 4 * ((part + 1) * n4 / PARTS);
-    const float* Rq = R[ql];
-    for (int c = c0; c < c1; c += 4) {
-      const float4 av = *reinterpret_cast<const float4*>(&Ar[tl][c]);
-      float y[4];
+    for (int qq = 0; qq < QS; ++qq)
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const float* Rr = Rq + (c + i) * K;
-        float y0 = 0.f, y1 = 0.f, y2 = 0.f, y3 = 0.f;
+      for (int tc = 0; tc < 2; ++tc) {
+        const float* rr = R[qq] + (32 * tc + l32) * kTokRow + h;
+        f32x16 y;
 #pragma unroll
-        for (int r = 0; r < K; r += 4) {
-          const float4 w = *reinterpret_cast<const float4*>(Rr + r);
-          y0 = fmaf(w.x, g[r], y0);
-          y1 = fmaf(w.y, g[r + 1], y1);
-          y2 = fmaf(w.z, g[r + 2], y2);
-          y3 = fmaf(w.w, g[r + 3], y3);
-        }
-        y[i] = (y0 + y1) + (y2 + y3);
+        for (int v = 0; v < 16; ++v) y[v] = 0.f;
+#pragma unroll
+        for (int s2 = 0; s2 < K / 2; ++s2) y = __builtin_amdgcn_mfma_f32_32x32x2f32(g[2 * s2], rr[2 * s2], y, 0, 0, 0);
+#pragma unroll
+        for (int v = 0; v < 16; ++v) acc[qq][v] = fmaf(a[tc][v], y[v], acc[qq][v]);
       }
-      acc = fmaf(av.x, y[0], acc);
-      acc = fmaf(av.y, y[1], acc);
-      acc = fmaf(av.z, y[2], acc);
-      acc = fmaf(av.w, y[3], acc);
-    }
   }
-  part_sum[slot][tl] = acc;
-  __syncthreads();
-  if (part == 0) {
-    float t = part_sum[slot][tl];
+  // sum over c: the 32 lanes of a half hold the same 16 token positions
 #pragma unroll
-    for (int p = 1; p < PARTS; ++p) t += part_sum[slot + p][tl];
-    const int64_t q = q0 + ql;
-    if (q < n_q && t0 + tl < T) out[(q * n + ex) * T + t0 + tl] = t;
+  for (int qq = 0; qq < QS; ++qq) {
+    const int64_t q = q0 + qq;
+#pragma unroll
+    for (int v = 0; v < 16; ++v) {
+      float x = acc[qq][v];
+#pragma unroll
+      for (int o = 16; o >= 1; o >>= 1) x += __shfl_xor(x, o, 64);
+      const int t = tw + 8 * (v >> 2) + 4 * h + (v & 3);
+      if (l32 == 0 && q < n_q && t < T) out[(q * n + ex) * T + t] = x;
+    }
   }
 }
 
@@ -406,19 +421,15 @@ hipError_t launch_token_scores(const TokTask* tasks, int n_tasks, const void* ph
                                int64_t n_q, int64_t n, int T, float* out, hipStream_t s) {
   if (n_tasks <= 0 || n_q <= 0 || n <= 0 || T <= 0) return hipSuccess;
   const int QS = n_q >= kTokQueries ? kTokQueries : (n_q >= 2 ? 2 : 1);  // query slots per workgroup
-  const int TT = QS == 1 ? 32 : 64;                                      // token positions per workgroup
-  const int64_t gx = (T + TT - 1) / TT, gz = (n_q + QS - 1) / QS;
+  const int64_t gx = (T + kTokTokens - 1) / kTokTokens, gz = (n_q + QS - 1) / QS;
   if (n > 65535 || gz > 65535) return hipErrorInvalidValue;
   const dim3 grid((unsigned)gx, (unsigned)n, (unsigned)gz);
   if (QS == 4)
-    hipLaunchKernelGGL((token_kernel<4, 64>), grid, dim3(256), 0, s, tasks, n_tasks, phi_q, q_bf16, ld_q, n_q, n, T,
-                       out);
+    hipLaunchKernelGGL((token_kernel<4>), grid, dim3(256), 0, s, tasks, n_tasks, phi_q, q_bf16, ld_q, n_q, n, T, out);
   else if (QS == 2)
-    hipLaunchKernelGGL((token_kernel<2, 64>), grid, dim3(256), 0, s, tasks, n_tasks, phi_q, q_bf16, ld_q, n_q, n, T,
-                       out);
+    hipLaunchKernelGGL((token_kernel<2>), grid, dim3(256), 0, s, tasks, n_tasks, phi_q, q_bf16, ld_q, n_q, n, T, out);
   else
-    hipLaunchKernelGGL((token_kernel<1, 32>), grid, dim3(256), 0, s, tasks, n_tasks, phi_q, q_bf16, ld_q, n_q, n, T,
-                       out);
+    hipLaunchKernelGGL((token_kernel<1>), grid, dim3(256), 0, s, tasks, n_tasks, phi_q, q_bf16, ld_q, n_q, n, T, out);
   return hipGetLastError();
 }
 

@@ -58,11 +58,18 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 
 
 def kernel_source_hash(key):
+    """Hash of the kernel's sources with comments and whitespace removed, so
+    that a comment edit keeps the committed counters valid and a code edit
+    does not."""
     import hashlib
+    import re
     h = hashlib.sha256()
     for name in KERNEL_SOURCES[key]:
-        with open(os.path.join(HERE, "paper_2609_38767_amd", "csrc", name), "rb") as f:
-            h.update(f.read())
+        with open(os.path.join(HERE, "paper_2609_38767_amd", "csrc", name)) as f:
+            text = f.read()
+        text = re.sub(r"/\*.*?\*/", " ", text, flags=re.S)
+        text = re.sub(r"//[^\n]*", " ", text)
+        h.update(" ".join(text.split()).encode())
     return h.hexdigest()[:16]
 
 

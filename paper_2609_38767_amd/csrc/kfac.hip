@@ -7,8 +7,8 @@
 //                    Token rows are projected exactly as in the factored route
 //                    (bf16/f32 MFMA; bf16 aligned rows streamed through LDS by
 //                    direct loads, project_rows_dma, else fragments loaded into
-//                    registers with map panels in LDS, project_rows); the projected tiles
-//                    stay in accumulators and their outer products are summed
+//                    registers with map panels in LDS, project_rows); the
+//                    projected tiles stay in accumulators and their outer products are summed
 //                    with float32 MFMA (16x16x4), whose C layout gives every
 //                    element index a K = 4 slice of token rows for both
 //                    operands.  Only tiles on and above the diagonal are
@@ -18,8 +18,11 @@
 //                    round applies n/2 rotations on disjoint index pairs (the
 //                    round-robin ordering), rows then columns of the LDS copy,
 //                    and accumulates the rotations into V.
-// ekfac_kernel       sum over training rows of (Q_A^T Psi Q_G)^2.
+// ekfac_kernel       sum over training rows of (Q_A^T Psi Q_G)^2 (float32 MFMA,
+//                    one wave per row).
 // precond_kernel     Q_A [(Q_A^T Psi Q_G) / (E + delta)] Q_G^T per query block.
+// token_kernel       per-token contributions a~_t^T R g~_t over the kept rows
+//                    (float32 MFMA, 32 token positions per wave).
 #include <math.h>
 
 #include "device_common.h"

@@ -80,6 +80,33 @@ def test_factor_sums(dtype, T, lens):
         assert c.field(li, "counts").tolist() == [nt, ne, 0]
 
 
+DMA_LAYERS = [dict(name="d0", d_in=128, d_out=96, k_in=32, k_out=24, a_group="h0"),
+              dict(name="d1", d_in=64, d_out=256, k_in=64, k_out=20, a_group="h1")]
+
+
+def test_factor_sums_direct_load_instances():
+    # bf16 sides with 16-byte rows and 2 or 4 map tiles stream their rows by
+    # direct loads (k of 20, 24, 32 -> 2 tiles; 64 -> 4), ragged lengths over
+    # several row chunks, against the oracle's token loop
+    lens = [300, 171, 0]
+    n, T = len(lens), 300
+    inputs = _inputs(DMA_LAYERS, n, T, "bf16", seed=23)
+    lengths = torch.tensor(lens, dtype=torch.int32, device=DEV)
+    s = _session(DMA_LAYERS, inputs, "bf16", 9, lengths)
+    c = Curvature(s)
+    c.accumulate_factors()
+    torch.cuda.synchronize()
+    maps = oracle_maps(9, DMA_LAYERS, "bf16")
+    for li, L in enumerate(DMA_LAYERS):
+        A, B = host64(inputs[li][0]), host64(inputs[li][1])
+        SA, SG, nt, ne = ok.factor_sums(A, B, maps[li][0], maps[li][1], lens)
+        ga, gg = host64(c.field(li, "sum_a")), host64(c.field(li, "sum_g"))
+        ea, eg = rel_fro(ga, SA), rel_fro(gg, SG)
+        assert ea <= 1e-5 and eg <= 1e-5, (li, ea, eg)
+        assert np.array_equal(ga, ga.T) and np.array_equal(gg, gg.T)
+        assert c.field(li, "counts").tolist() == [nt, ne, 0]
+
+
 FIT_CASES = [("auto", None), ("factored", dt.DATTRI_FORM_FUSED), ("factored", dt.DATTRI_FORM_SPLIT),
              ("materialized", None)]
 

@@ -45,7 +45,7 @@ def _sums_match(scores, phi_q, phi):
 
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
 @pytest.mark.parametrize("form", ["fused", "split"])
-@pytest.mark.parametrize("n_q", [6, 1])  # two query groups of 4 + 2; one query row (32 tokens per workgroup)
+@pytest.mark.parametrize("n_q", [6, 3, 1])  # query groups of 4 + 2 slots; 2 + 1 (two-slot instance); one row
 def test_token_scores_against_oracle(dtype, form, n_q):
     print(f"[token] dtype={dtype} form={form} n_q={n_q}", flush=True)
     lens = [150, 0, 64, 149, 1]

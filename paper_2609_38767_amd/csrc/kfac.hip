@@ -465,6 +465,7 @@ __global__ __launch_bounds__(256) void eigen_kernel(const EigTask* __restrict__ 
   __shared__ double Am[kCurvMaxK * kEigLd];
   __shared__ double Vm[kCurvMaxK * kEigLd];
   __shared__ double rc[kCurvMaxK / 2], rs[kCurvMaxK / 2];
+  __shared__ int rp[kCurvMaxK / 2], rq[kCurvMaxK / 2];
   __shared__ double red[2][4];
   __shared__ int rank[kCurvMaxK];
   const EigTask t = tasks[blockIdx.x];
@@ -522,31 +523,34 @@ __global__ __launch_bounds__(256) void eigen_kernel(const EigTask* __restrict__ 
         }
         rc[tid] = c;
         rs[tid] = s;
+        rp[tid] = p;
+        rq[tid] = q;
       }
       __syncthreads();
-      // rows: A <- J^T A
-      for (int e = tid; e < m * n; e += 256) {
-        const int pi = e / n, col = e - (e / n) * n;
-        int p, q;
-        round_pair(r, pi, n, &p, &q);
-        const double c = rc[pi], s = rs[pi];
-        const double a = Am[p * kEigLd + col], b = Am[q * kEigLd + col];
-        Am[p * kEigLd + col] = c * a - s * b;
-        Am[q * kEigLd + col] = s * a + c * b;
+      // rows: A <- J^T A; thread (tid / 64, tid % 64) takes column tid % 64 of
+      // the pairs tid / 64, + 4, ... (the pair indices were formed once above)
+      if (lane < n) {
+        for (int pi = wave; pi < m; pi += 4) {
+          const int p = rp[pi], q = rq[pi];
+          const double c = rc[pi], s = rs[pi];
+          const double a = Am[p * kEigLd + lane], b = Am[q * kEigLd + lane];
+          Am[p * kEigLd + lane] = c * a - s * b;
+          Am[q * kEigLd + lane] = s * a + c * b;
+        }
       }
       __syncthreads();
-      // columns: A <- A J, V <- V J
-      for (int e = tid; e < m * n; e += 256) {
-        const int pi = e / n, row = e - (e / n) * n;
-        int p, q;
-        round_pair(r, pi, n, &p, &q);
-        const double c = rc[pi], s = rs[pi];
-        const double a = Am[row * kEigLd + p], b = Am[row * kEigLd + q];
-        Am[row * kEigLd + p] = c * a - s * b;
-        Am[row * kEigLd + q] = s * a + c * b;
-        const double va = Vm[row * kEigLd + p], vb = Vm[row * kEigLd + q];
-        Vm[row * kEigLd + p] = c * va - s * vb;
-        Vm[row * kEigLd + q] = s * va + c * vb;
+      // columns: A <- A J, V <- V J; row tid % 64 of the same pairs
+      if (lane < n) {
+        for (int pi = wave; pi < m; pi += 4) {
+          const int p = rp[pi], q = rq[pi];
+          const double c = rc[pi], s = rs[pi];
+          const double a = Am[lane * kEigLd + p], b = Am[lane * kEigLd + q];
+          Am[lane * kEigLd + p] = c * a - s * b;
+          Am[lane * kEigLd + q] = s * a + c * b;
+          const double va = Vm[lane * kEigLd + p], vb = Vm[lane * kEigLd + q];
+          Vm[lane * kEigLd + p] = c * va - s * vb;
+          Vm[lane * kEigLd + q] = s * va + c * vb;
+        }
       }
       __syncthreads();
     }

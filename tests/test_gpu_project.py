@@ -284,7 +284,11 @@ def test_mask_layer_wider_than_byte_offsets():
 
 SLICED = [dict(name="tall", d_in=512, d_out=2048, k_in=1, k_out=40000, mask_size=20000, mask_id=1, mask_count=2,
                a_group="sa"),
-          dict(name="wide", d_in=3000, d_out=512, k_in=1, k_out=33000, mask_size=33000, mask_id=0, a_group="sb")]
+          dict(name="wide", d_in=3000, d_out=512, k_in=1, k_out=33000, mask_size=33000, mask_id=0, a_group="sb"),
+          # bf16: the 4200-wide side's slice (8400 bytes) exceeds a fixed slot, so
+          # its whole groups take the sliced direct-load gather instead
+          dict(name="broad", d_in=4200, d_out=9000, k_in=1, k_out=40000, mask_size=20000, mask_id=0, mask_count=2,
+               a_group="sc")]
 
 
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
